@@ -1,0 +1,43 @@
+"""Plain CPU oracle for tuple-oriented compression (TOC).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or call anything in this package.
+The product path (``libtoc.so`` and its Python binding) never imports it, and this
+package imports nothing from the product.
+
+Everything here follows Li et al., "Tuple-oriented Compression for Large-scale
+Mini-batch Stochastic Gradient Descent" (arXiv 1702.06943); each function cites the
+section, algorithm, table or equation it restates.  Floating point is fp64.
+
+Parity status of each function (what pins it, see ``tests/test_oracle.py``):
+  canonicalize   pinned: sparse-encoding example of §3 (row R2), error cases
+  encode         pinned: Table 2 traces + its caption (worked example), brute-force
+                 greedy re-encoder on random tiny tables, round trip
+  build_cprime   pinned: Table 4 (all 11 nodes), node-count closed form, invariants
+  decode         pinned: lossless round trip on random inputs + worked example
+  dense_right    pinned: hand-computed worked-example sums, numpy dense matmul on the
+                 densified batch, integer exactness
+  dense_left     pinned: as dense_right, plus duality <G, A W> = <A^T G, W>
+  toc_right      pinned: Theorem 1 (equals dense_right) + integer exactness
+  toc_left       pinned: Theorem 2 (equals dense_left) + integer exactness
+  layout_stats   pinned: hand count on the worked example (live set, depths)
+  physical_bytes parity unpinned (the paper prints sizes only in missing figures;
+                 the formula of §3.3 is checked on the worked example by hand)
+"""
+
+from .toc_oracle import (  # noqa: F401
+    TocInputError,
+    canonicalize,
+    encode,
+    build_cprime,
+    decode,
+    decoded_to_csr,
+    dense_right,
+    dense_left,
+    toc_right,
+    toc_left,
+    layout_stats,
+    physical_bytes,
+    f32_bits,
+    bits_f32,
+)

@@ -1,0 +1,355 @@
+"""Plain, slow, obviously correct TOC oracle (TEST INFRASTRUCTURE ONLY).
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may use this
+module.  It shares no code with the HIP path and imports nothing from it.
+
+Paper: Li et al., "Tuple-oriented Compression for Large-scale Mini-batch Stochastic
+Gradient Descent", arXiv 1702.06943.
+
+Representation used throughout: a mini-batch is a list of rows; a row is a list of
+column_index:value pairs ``(col, bits)`` in increasing column order, where ``bits``
+is the IEEE-754 binary32 bit pattern of the value (keys compare on bits).
+Columns are 0-based (the paper's worked example is 1-based).
+"""
+
+from __future__ import annotations
+
+import math
+import struct
+
+import numpy as np
+
+
+class TocInputError(ValueError):
+    """Raised for inputs the sparse encoding cannot represent."""
+
+
+def f32_bits(x: float) -> int:
+    """Bit pattern of x rounded to binary32."""
+    return struct.unpack("<I", struct.pack("<f", x))[0]
+
+
+def bits_f32(b: int) -> float:
+    """Value (as a Python float, exact) of a binary32 bit pattern."""
+    return struct.unpack("<f", struct.pack("<I", b))[0]
+
+
+# ---------------------------------------------------------------------------
+# Sparse encoding (§3, first paragraphs): drop zeros, prefix each nonzero with its
+# column index.  Our readings: values are binary32, a value compares equal to zero
+# (+0.0 or -0.0) is dropped, NaN/Inf are rejected, columns must be strictly
+# increasing inside a row (the pairs come from scanning a dense row left to right).
+# ---------------------------------------------------------------------------
+def canonicalize(n_rows, n_cols, rowptr, col, val):
+    """CSR (rowptr, col, val as float32) -> list of rows of (col, bits) pairs."""
+    rowptr = np.asarray(rowptr, dtype=np.int64)
+    col = np.asarray(col, dtype=np.int64)
+    val = np.asarray(val, dtype=np.float32)
+    if n_rows < 0 or n_cols < 0:
+        raise TocInputError("negative shape")
+    if rowptr.shape != (n_rows + 1,):
+        raise TocInputError("rowptr must have n_rows + 1 entries")
+    if rowptr[0] != 0 or np.any(np.diff(rowptr) < 0):
+        raise TocInputError("rowptr must start at 0 and be non-decreasing")
+    nnz = int(rowptr[-1])
+    if col.shape != (nnz,) or val.shape != (nnz,):
+        raise TocInputError("col/val length must equal rowptr[n_rows]")
+    rows = []
+    for i in range(n_rows):
+        row = []
+        prev = -1
+        for p in range(int(rowptr[i]), int(rowptr[i + 1])):
+            c = int(col[p])
+            v = float(val[p])
+            if c < 0 or c >= n_cols:
+                raise TocInputError("column index out of range")
+            if c <= prev:
+                raise TocInputError("columns must be strictly increasing in a row")
+            prev = c
+            if math.isnan(v) or math.isinf(v):
+                raise TocInputError("non-finite value")
+            if v == 0.0:
+                continue
+            row.append((c, f32_bits(v)))
+        rows.append(row)
+    return rows
+
+
+# ---------------------------------------------------------------------------
+# Logical encoding: Algorithm 1 (PrefixTreeEncode with LongestMatchFromTree), §3.1.
+# The prefix tree C is kept as one dict mapping (node, key) -> child index: this is
+# the per-node child hash map of §3.1.1 with the node folded into the dict key.
+# AddNode hands out indices from a sequence number; the root is node 0.
+# ---------------------------------------------------------------------------
+def _longest_match(t, i, children):
+    """LongestMatchFromTree (Alg. 1): greedy longest tree sequence starting at t[i].
+
+    Returns (n, j): the node of the longest match and the next start position.
+    The match has length >= 1 because phase I put every pair under the root.
+    """
+    j = i
+    n_next = children[(0, t[j])]
+    while True:
+        n = n_next
+        j = j + 1
+        if j < len(t):
+            n_next = children.get((n, t[j]), -1)
+        else:
+            n_next = -1
+        if n_next == -1:
+            return n, j
+
+
+def encode(rows):
+    """Algorithm 1.  rows -> (I, D, N).
+
+    I: list of (col, bits), the first layer of C in node-index order (nodes 1..|I|).
+    D: list (one per row) of lists of node indices.
+    N: number of nodes of C including the root (= next sequence number).
+    """
+    children = {}
+    next_index = 1
+    I = []
+    # phase I: every distinct pair becomes a child of the root, first appearance first
+    for t in rows:
+        for pair in t:
+            if (0, pair) not in children:
+                children[(0, pair)] = next_index
+                next_index += 1
+                I.append(pair)
+    # phase II: encode each tuple by greedy longest matches, growing the tree
+    D = []
+    for t in rows:
+        i = 0
+        codes = []
+        while i < len(t):
+            n, j = _longest_match(t, i, children)
+            codes.append(n)
+            if j < len(t):
+                children[(n, t[j])] = next_index
+                next_index += 1
+            i = j
+        D.append(codes)
+    return I, D, next_index
+
+
+# ---------------------------------------------------------------------------
+# Decoding tree C': Algorithm 2 (BuildPrefixTree), §4.1.2, Table 4.
+# Each node keeps its key and its parent; F holds the first pair of each node's
+# sequence.  depth (the length of a node's sequence) is derived alongside:
+# a new node extends its parent's sequence by one pair.
+# ---------------------------------------------------------------------------
+def build_cprime(I, D):
+    """Algorithm 2.  Returns dict with lists parent, key (pairs), depth; index 0 = root."""
+    n_nodes = 1 + len(I) + sum(max(len(d) - 1, 0) for d in D)
+    parent = [None] * n_nodes
+    key = [None] * n_nodes
+    first = [None] * n_nodes
+    depth = [0] * n_nodes
+    # phase I: initialise with I
+    for i in range(1, len(I) + 1):
+        key[i] = I[i - 1]
+        parent[i] = 0
+        first[i] = I[i - 1]
+        depth[i] = 1
+    # phase II: replay the node creations of Algorithm 1 from D
+    idx = len(I) + 1
+    for d in D:
+        for j in range(0, len(d) - 1):
+            parent[idx] = d[j]
+            first[idx] = first[d[j]]
+            key[idx] = first[d[j + 1]]
+            depth[idx] = depth[d[j]] + 1
+            idx += 1
+    assert idx == n_nodes
+    return {"parent": parent, "key": key, "depth": depth, "n_nodes": n_nodes}
+
+
+# ---------------------------------------------------------------------------
+# Full decode: the backtracking loop of Algorithm 6 (§4.5), without the final
+# densify-and-add-c step.
+# ---------------------------------------------------------------------------
+def decode(I, D):
+    """(I, D) -> rows of (col, bits) pairs."""
+    cp = build_cprime(I, D)
+    parent, key = cp["parent"], cp["key"]
+    rows = []
+    for d in D:
+        row = []
+        for code in d:
+            reverse_seq = []
+            node = code
+            while node != 0:
+                reverse_seq.append(key[node])
+                node = parent[node]
+            for q in range(len(reverse_seq) - 1, -1, -1):
+                row.append(reverse_seq[q])
+        rows.append(row)
+    return rows
+
+
+def decoded_to_csr(rows):
+    """rows of (col, bits) -> (rowptr int64, col int32, val float32) arrays."""
+    rowptr = np.zeros(len(rows) + 1, dtype=np.int64)
+    cols, bits = [], []
+    for i, r in enumerate(rows):
+        rowptr[i + 1] = rowptr[i] + len(r)
+        for c, b in r:
+            cols.append(c)
+            bits.append(b)
+    col = np.asarray(cols, dtype=np.int32)
+    val = np.asarray(bits, dtype=np.uint32).view(np.float32)
+    return rowptr, col, val
+
+
+def _coo(rows):
+    """rows -> (row index, col, value fp64) arrays of the nonzeros."""
+    ri, ci, vi = [], [], []
+    for i, r in enumerate(rows):
+        for c, b in r:
+            ri.append(i)
+            ci.append(c)
+            vi.append(bits_f32(b))
+    return (np.asarray(ri, dtype=np.int64), np.asarray(ci, dtype=np.int64),
+            np.asarray(vi, dtype=np.float64))
+
+
+# ---------------------------------------------------------------------------
+# Reference products.  Theorems 1 and 2 (and their matrix forms in the appendix)
+# state that the TOC algorithms compute exactly A.W and M.A; so the reference is the
+# plain definition over the nonzeros of the decoded batch, in fp64:
+#   R[i, q]   = sum_j a_ij w_jq         (right multiplication, A.W)
+#   out[j, q] = sum_i a_ij g_iq         (left multiplication G^T.A, stored transposed)
+# The tolerance scales are the same sums of absolute values of the terms.
+# ---------------------------------------------------------------------------
+def dense_right(rows, n_cols, W):
+    """R = A.W and S_R = |A|.|W| in fp64.  W: (n_cols, k)."""
+    W = np.asarray(W, dtype=np.float64)
+    if W.ndim != 2 or W.shape[0] != n_cols:
+        raise TocInputError("W must be n_cols x k")
+    k = W.shape[1]
+    ri, ci, vi = _coo(rows)
+    R = np.zeros((len(rows), k))
+    S = np.zeros((len(rows), k))
+    terms = vi[:, None] * W[ci, :]
+    np.add.at(R, ri, terms)
+    np.add.at(S, ri, np.abs(terms))
+    return R, S
+
+
+def dense_left(rows, n_cols, G):
+    """out = (G^T.A)^T (n_cols x k) and S_out = |A|^T.|G| in fp64.  G: (n_rows, k)."""
+    G = np.asarray(G, dtype=np.float64)
+    if G.ndim != 2 or G.shape[0] != len(rows):
+        raise TocInputError("G must be n_rows x k")
+    k = G.shape[1]
+    ri, ci, vi = _coo(rows)
+    out = np.zeros((n_cols, k))
+    S = np.zeros((n_cols, k))
+    terms = vi[:, None] * G[ri, :]
+    np.add.at(out, ci, terms)
+    np.add.at(S, ci, np.abs(terms))
+    return out, S
+
+
+# ---------------------------------------------------------------------------
+# The TOC algorithms themselves, in fp64 and in the paper's order, used to check
+# Theorems 1 and 2 against the plain products above.
+# ---------------------------------------------------------------------------
+def toc_right(I, D, W):
+    """Algorithm 4 / Algorithm 7: scan C' forward computing H, then scan D summing H."""
+    W = np.asarray(W, dtype=np.float64)
+    k = W.shape[1]
+    cp = build_cprime(I, D)
+    parent, key = cp["parent"], cp["key"]
+    H = np.zeros((cp["n_nodes"], k))
+    for i in range(1, cp["n_nodes"]):
+        c, b = key[i]
+        H[i, :] = bits_f32(b) * W[c, :] + H[parent[i], :]
+    R = np.zeros((len(D), k))
+    for i, d in enumerate(D):
+        for code in d:
+            R[i, :] = R[i, :] + H[code, :]
+    return R
+
+
+def toc_left(I, D, G, n_cols):
+    """Algorithm 5 / Algorithm 8: scan D scattering G rows into H, then scan C'
+    backwards adding key * H[i] into the result and H[i] into H[parent]."""
+    G = np.asarray(G, dtype=np.float64)
+    k = G.shape[1]
+    cp = build_cprime(I, D)
+    parent, key = cp["parent"], cp["key"]
+    H = np.zeros((cp["n_nodes"], k))
+    for i, d in enumerate(D):
+        for code in d:
+            H[code, :] = G[i, :] + H[code, :]
+    out = np.zeros((n_cols, k))
+    for i in range(cp["n_nodes"] - 1, 0, -1):
+        c, b = key[i]
+        out[c, :] = out[c, :] + bits_f32(b) * H[i, :]
+        H[parent[i], :] = H[parent[i], :] + H[i, :]
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Sizes.
+# ---------------------------------------------------------------------------
+def layout_stats(I, D):
+    """Counts that define the canonical compressed size of a batch.
+
+    live: codes referenced by D plus all their ancestors (the only codes any of the
+    operations of §4 touch); max_depth over live codes; canonical bytes
+      B_toc = 4|D| + 4(n+1) + 10 live + 4 (max_depth + 1)
+    i.e. a u32 per code occurrence, a u32 per row boundary, (u32 parent, u16 column,
+    f32 value) per live code and a u32 per level boundary.
+    """
+    cp = build_cprime(I, D)
+    parent, depth = cp["parent"], cp["depth"]
+    live = [False] * cp["n_nodes"]
+    stack = [c for d in D for c in d]
+    while stack:
+        c = stack.pop()
+        if c != 0 and not live[c]:
+            live[c] = True
+            stack.append(parent[c])
+    n_live = sum(live)
+    max_depth = max((depth[c] for c in range(cp["n_nodes"]) if live[c]), default=0)
+    n_codes = sum(len(d) for d in D)
+    n_deep = sum(1 for c in range(cp["n_nodes"]) if live[c] and depth[c] >= 2)
+    canon = 4 * n_codes + 4 * (len(D) + 1) + 10 * n_live + 4 * (max_depth + 1)
+    return {
+        "n_rows": len(D),
+        "n_first": len(I),
+        "n_codes": n_codes,
+        "n_nodes": cp["n_nodes"],
+        "n_live": n_live,
+        "n_deep": n_deep,
+        "max_depth": max_depth,
+        "canon_bytes": canon,
+    }
+
+
+def _packed_array_bytes(values):
+    """Bit packing of §3.3: ceil(log2(max+1)/8) bytes per integer (at least one),
+    plus a header holding the count (u32) and the bytes per integer (u8)."""
+    mx = max(values, default=0)
+    width = max(1, math.ceil(math.log2(mx + 1) / 8)) if mx > 0 else 1
+    return 5 + width * len(values)
+
+
+def physical_bytes(I, D):
+    """Physical encoding of §3.3: I's columns bit-packed, I's values replaced by
+    indices into an array of unique values (4 bytes each) which are bit-packed,
+    D's codes concatenated and bit-packed, tuple start offsets bit-packed."""
+    uniq = sorted(set(b for _, b in I))
+    where = {b: q for q, b in enumerate(uniq)}
+    size = _packed_array_bytes([c for c, _ in I])
+    size += 5 + 4 * len(uniq)
+    size += _packed_array_bytes([where[b] for _, b in I])
+    size += _packed_array_bytes([c for d in D for c in d])
+    starts = [0]
+    for d in D:
+        starts.append(starts[-1] + len(d))
+    size += _packed_array_bytes(starts)
+    return size
