@@ -1,0 +1,314 @@
+#!/usr/bin/env python3
+"""Benchmark of the TOC hot path on one MI355X.
+
+One step = A.W (right multiplication), G^T.A (left multiplication) and decode to
+CSR over every mini-batch of a workload, with the compressed image, W and G
+already resident in HBM.  Encoding and upload happen once before timing, as the
+paper excludes compression time from training time.
+
+Prints one JSON line (see --help for the options).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK = 8.0e12                     # bytes/s, MI355X HBM3E
+# 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz x 2 flops per fused multiply-add, with the
+# packed-FP32 instructions excluded from the build (they would double it to 157.3)
+FP32_FMA_PEAK = 256 * 4 * 16 * 2.4e9 * 2
+METRIC = "uncompressed nnz/s for TOC A·W and Gᵀ·A; % HBM peak on compressed bytes"
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def log(msg):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle, timed on a sample of the workload's batches
+# ---------------------------------------------------------------------------
+def _oracle_batch(args):
+    cfg, b, k = args
+    import oracle as O
+    from workloads import config_batches, config_G, config_W
+    B = config_batches(cfg, b, 1)
+    n, rp, c, v = B.batch(0)
+    W = config_W(cfg, k)
+    G = config_G(cfg, b, 1, k)
+    rows = O.canonicalize(n, B.n_cols, rp, c, v)
+    I, D, _ = O.encode(rows)             # encoding is not part of a step
+    t0 = time.perf_counter()
+    dec = O.decode(I, D)
+    O.decoded_to_csr(dec)
+    O.dense_right(dec, B.n_cols, W)
+    O.dense_left(dec, B.n_cols, G)
+    return time.perf_counter() - t0, int(B.nnz)
+
+
+def cpu_baseline(pool, workers, cfg, nb, k, budget_s):
+    t1, _ = _oracle_batch((cfg, 0, k))
+    n_sample = int(min(max(workers, round(budget_s * workers / max(t1, 1e-3))), nb, 4000))
+    ids = sorted(set(np.linspace(0, nb - 1, n_sample).astype(int).tolist()))
+    t0 = time.perf_counter()
+    res = pool.map(_oracle_batch, [(cfg, b, k) for b in ids])
+    wall = time.perf_counter() - t0
+    nnz = sum(r[1] for r in res)
+    cpu = sum(r[0] for r in res)
+    return {
+        "value": nnz / wall,
+        "unit": "nnz/s",
+        "cores": workers,
+        "kind": "oracle",
+        "sample": f"{len(ids)} of {nb} mini-batches evenly spaced over the workload; per "
+                  f"batch the oracle's decode (Algorithm 6) + fp64 A.W + fp64 G^T.A on the "
+                  f"decoded batch (its encode untimed); {workers} worker processes, "
+                  f"{wall:.1f} s wall, {cpu:.1f} s CPU",
+    }
+
+
+def host_cpu():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# ---------------------------------------------------------------------------
+# Workload preparation: generate (process pool) -> encode (C++ threads) -> upload
+# ---------------------------------------------------------------------------
+class Workload:
+    pass
+
+
+def encode_workload(cfg, nb, pool, chunk=400):
+    import paper_1702_06943_amd as T
+    from workloads.parallel import iter_chunks
+    w = Workload()
+    w.cfg, w.nb = cfg, nb
+    w.encs, w.nnz, w.rows = [], 0, 0
+    t0 = time.perf_counter()
+    last = t0
+    for part in iter_chunks(cfg, nb, 0, chunk, pool):
+        w.encs.extend(T.toc_encode_batches(part.n_rows, part.n_cols, part.rowptr, part.col,
+                                           part.val))
+        w.nnz += part.nnz
+        w.rows += int(part.n_rows.sum())
+        w.n_cols = part.n_cols
+        if time.perf_counter() - last > 10 or len(w.encs) == nb:
+            log(f"generated+encoded {len(w.encs)}/{nb} batches "
+                f"({time.perf_counter() - t0:.1f} s)")
+            last = time.perf_counter()
+    w.encode_s = time.perf_counter() - t0
+    return w
+
+
+def upload_workload(w, k, device="cuda:0", seed_G=None):
+    import torch
+    import paper_1702_06943_amd as T
+    from workloads import CONFIGS, config_W, dense_normal_device, SEED
+    spec = CONFIGS[w.cfg]
+    t0 = time.perf_counter()
+    size = T.toc_upload_size(w.encs)
+    w.buf = torch.empty(size, dtype=torch.uint8, device=device)
+    w.dev = T.toc_upload(w.encs, w.buf)
+    w.upload_s = time.perf_counter() - t0
+    w.info = T.toc_dev_info_get(w.dev)
+    log(f"uploaded image: {size / 1e9:.2f} GB in {w.upload_s:.1f} s")
+    w.k = k
+    w.W = torch.from_numpy(config_W(w.cfg, k)).to(device)
+    seed = SEED * 16 + spec["cid"] if seed_G is None else seed_G
+    w.G = dense_normal_device((w.info["n_rows"], k), 1.0, seed, device)
+    w.R = torch.empty((w.info["n_rows"], k), device=device)
+    w.out = torch.empty((w.info["n_batches"] * w.info["n_cols"], k), device=device)
+    w.rowptr = torch.empty(w.info["n_rows"] + 1, dtype=torch.int64, device=device)
+    w.ccol = torch.empty(max(w.info["nnz"], 1), dtype=torch.int32, device=device)[:w.info["nnz"]]
+    w.cval = torch.empty(max(w.info["nnz"], 1), dtype=torch.float32, device=device)[:w.info["nnz"]]
+    ws_r, _ = T.toc_workspace_size(w.dev, T.TOC_OP_RIGHT, k)
+    ws_l, _ = T.toc_workspace_size(w.dev, T.TOC_OP_LEFT, k)
+    w.ws_r = torch.empty(max(ws_r // 4, 1), device=device) if ws_r else None
+    w.ws_l = torch.empty(max(ws_l // 4, 1), device=device) if ws_l else None
+    torch.cuda.synchronize()
+    return w
+
+
+def run_ops(w, which=("right", "left", "decode")):
+    import paper_1702_06943_amd as T
+    if "right" in which:
+        T.toc_right_mul(w.dev, w.W, w.R, w.ws_r)
+    if "left" in which:
+        T.toc_left_mul(w.dev, w.G, w.out, False, w.ws_l)
+    if "decode" in which:
+        T.toc_decode_csr(w.dev, w.rowptr, w.ccol, w.cval)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
+        h.update(open(os.path.join(HERE, "paper_1702_06943_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(op, cfg):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(HERE, "profiles", f"traffic_{cfg}.txt")
+    if not os.path.exists(path):
+        return None
+    src = kernel_source_hash()
+    for line in open(path):
+        parts = line.split()
+        if len(parts) >= 4 and parts[0] == "traffic" and parts[1] == op and parts[2] == src:
+            return float(parts[3])
+    return None
+
+
+# ---------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="c3", help="workload c1..c5 (default c3)")
+    ap.add_argument("--batches", type=int, default=0,
+                    help="mini-batches (default: the workload's full count)")
+    ap.add_argument("--k", type=int, default=0, help="width of W and G (default: workload's)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--workers", type=int, default=0)
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(see DESIGN.md for how the batches would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    from workloads import CONFIGS
+    from workloads.parallel import default_workers, make_pool
+    cfg = args.config
+    spec = CONFIGS[cfg]
+    nb = args.batches or spec["n_batches"]
+    k = args.k or spec["k"]
+    workers = args.workers or default_workers()
+
+    # everything that forks happens before the GPU is touched
+    pool = make_pool(workers)
+    cpu = None
+    if args.cpu_seconds > 0:
+        log(f"oracle CPU baseline on {workers} processes ...")
+        cpu = cpu_baseline(pool, workers, cfg, nb, k, args.cpu_seconds)
+        log(f"oracle: {cpu['value']:.3e} nnz/s ({cpu['sample']})")
+    w = encode_workload(cfg, nb, pool)
+    pool.close()
+    pool.join()
+
+    import torch
+    upload_workload(w, k)
+    w.encs = None
+
+    stream = torch.cuda.current_stream()
+    log(f"warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        run_ops(w)
+    torch.cuda.synchronize()
+
+    names = ("right", "left", "decode")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for s in range(args.steps):
+        ev[s][0].record(stream)
+        for i, op in enumerate(names):
+            run_ops(w, (op,))
+            ev[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    op_ms = {op: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1])
+                                for s in range(args.steps)])) for i, op in enumerate(names)}
+    step_ms = float(np.mean([ev[s][0].elapsed_time(ev[s][3]) for s in range(args.steps)]))
+    log(f"step {step_ms:.3f} ms ({', '.join(f'{o} {op_ms[o]:.3f}' for o in names)}); "
+        f"wall {t_wall / args.steps * 1e3:.3f} ms/step")
+
+    info = w.info
+    nnz = info["nnz"]
+    canon = info["canon_bytes"]
+    n_rows, m = info["n_rows"], info["n_cols"]
+    # algorithmic bytes and flops per op (whole workload = one launch of each op)
+    dense = {
+        "right": 4 * m * k + 4 * n_rows * k,                         # W once, R
+        "left": 4 * n_rows * k + 4 * info["n_batches"] * m * k,      # G, out
+        "decode": 8 * (n_rows + 1) + 8 * nnz,                        # rowptr, col+val
+    }
+    flops = {
+        "right": 2.0 * k * (info["n_deep"] + info["n_codes"]),
+        "left": 2.0 * k * (info["n_codes"] + info["n_stored"] + info["n_deep"]),
+        "decode": 0.0,
+    }
+    ops = {}
+    for op in names:
+        t = op_ms[op] / 1e3
+        ops[op] = {
+            "ms": round(op_ms[op], 4),
+            "nnz_per_s": nnz / t,
+            "hbm_frac_compressed": canon / t / HBM_PEAK,
+            "hbm_frac_whole_op": (canon + dense[op]) / t / HBM_PEAK,
+            "tflops": flops[op] / t / 1e12,
+        }
+    dom = max(("right", "left", "decode"), key=lambda o: op_ms[o])
+    t_dom = op_ms[dom] / 1e3
+    bytes_dom = canon + dense[dom]
+    intensity = flops[dom] / bytes_dom
+    if intensity > FP32_FMA_PEAK / HBM_PEAK:
+        roof = {"bound": "alu", "achieved": flops[dom] / t_dom / 1e12,
+                "peak": FP32_FMA_PEAK / 1e12, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": bytes_dom / t_dom / 1e9,
+                "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = measured_traffic(dom, cfg)
+    roof["kernel"] = dom
+
+    line = {
+        "metric": METRIC,
+        "value": nnz / (step_ms / 1e3),
+        "unit": "nnz/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg}: {spec['name']}, {nb} mini-batches x {spec['rows']} rows x "
+                        f"{m} columns, W {m}x{k}, G {spec['rows']}x{k} per batch",
+            "batches": nb, "rows_per_batch": spec["rows"], "cols": m, "k": k,
+            "nnz": nnz, "codes": info["n_codes"], "live_codes": info["n_stored"],
+            "canon_bytes": canon, "image_bytes": info["image_bytes"],
+            "step": "right_mul + left_mul + decode_csr over all batches",
+        },
+        "hbm_frac_compressed": {op: ops[op]["hbm_frac_compressed"] for op in names},
+        "ops": ops,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
+                 "cpu": host_cpu()},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

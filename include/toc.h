@@ -1,0 +1,222 @@
+/*
+ * toc.h -- C ABI of libtoc: tuple-oriented compression (TOC) of mini-batches and
+ * matrix products run directly on the compressed form, on one MI355X (gfx950).
+ *
+ * Method: Li et al., "Tuple-oriented Compression for Large-scale Mini-batch
+ * Stochastic Gradient Descent" (arXiv 1702.06943).
+ *
+ * Conventions shared by every call
+ *  - Columns are 0-based.  Values, W, G, R and out are IEEE binary32.
+ *  - Every call returns a toc_status; on anything but TOC_OK, toc_last_error()
+ *    gives a message (thread-local).  No call aborts, exits or throws.
+ *  - Handles (toc_enc, toc_dev) are allocated and freed by the library and are
+ *    immutable once created: concurrent calls on one handle from several host
+ *    threads are allowed, as are device calls on distinct streams.
+ *  - Device memory (the upload buffer, W, G, R, out, workspaces, decoded CSR) is
+ *    always allocated and owned by the caller.  `stream` is a hipStream_t passed
+ *    as void* (NULL = the null stream).  Device calls only enqueue work: they are
+ *    asynchronous with respect to the host, and every argument is checked on the
+ *    host before anything is enqueued.
+ */
+#ifndef TOC_H
+#define TOC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TOC_OK = 0,
+  TOC_EINVAL = 1,       /* invalid argument: shape, pointer, CSR form, value      */
+  TOC_ENOMEM = 2,       /* host allocation failed                                 */
+  TOC_ESIZE = 3,        /* caller's buffer (upload buffer, workspace) too small   */
+  TOC_EDEVICE = 4,      /* HIP runtime reported an error (copy, launch)           */
+  TOC_EUNSUPPORTED = 5  /* valid, but beyond a documented limit of this build     */
+} toc_status;
+
+/* Host-side encoded mini-batch: the pair (I, D) of Algorithm 1. */
+typedef struct toc_enc toc_enc;
+/* Host descriptor of batches uploaded into a caller-owned device buffer. */
+typedef struct toc_dev toc_dev;
+
+typedef struct {
+  int32_t n_rows;       /* rows of the mini-batch                                 */
+  int32_t n_cols;       /* columns (m)                                            */
+  int64_t nnz;          /* column_index:value pairs kept (zeros dropped)          */
+  int64_t n_first;      /* |I|: distinct pairs = first layer of the prefix tree   */
+  int64_t n_codes;      /* |D|: codes over all rows                               */
+  int64_t n_nodes;      /* |C'| including the root = 1 + |I| + sum(len(D_i)-1)    */
+  int64_t n_live;       /* codes referenced by D plus their ancestors             */
+  int64_t n_deep;       /* live codes whose sequence has two or more pairs        */
+  int32_t max_depth;    /* longest live sequence                                  */
+  int32_t reserved;
+  int64_t phys_bytes;   /* size of the paper's physical encoding (section 3.3)   */
+  int64_t canon_bytes;  /* canonical compressed bytes:
+                           4|D| + 4(n_rows+1) + 10 n_live + 4(max_depth+1)       */
+} toc_enc_info;
+
+/* ---------------------------------------------------------------------------
+ * Encoding (host).  Section 3: sparse encoding, then the logical encoding of
+ * Algorithm 1 (PrefixTreeEncode): phase I makes every distinct pair a child of
+ * the root in order of first appearance, phase II encodes each tuple by greedy
+ * longest matches in the prefix tree and grows the tree by one node after every
+ * match that does not end the tuple.
+ *
+ * Input is one mini-batch as CSR: rowptr[n_rows+1] (rowptr[0] == 0, non-
+ * decreasing), col[rowptr[n_rows]] strictly increasing inside each row and in
+ * [0, n_cols), val[rowptr[n_rows]] finite.  Entries equal to zero (+0.0 or -0.0)
+ * are dropped, as the sparse encoding ignores zeros.  Pairs compare equal when
+ * column and the binary32 bit pattern of the value are equal.
+ * Errors: TOC_EINVAL for any violation above or NULL pointers (col/val may be
+ * NULL when rowptr[n_rows] == 0); TOC_EUNSUPPORTED when a batch would need more
+ * than 2^31-1 tree nodes; TOC_ENOMEM.  *out is NULL unless TOC_OK.
+ * The input arrays are read only during the call.
+ * ------------------------------------------------------------------------- */
+toc_status toc_encode(int32_t n_rows, int32_t n_cols, const int64_t *rowptr,
+                      const int32_t *col, const float *val, toc_enc **out);
+
+/* Encode n_batches mini-batches held in one concatenated CSR, in parallel on
+ * n_threads host threads (<= 0: all hardware threads).  Batch b owns the
+ * n_rows[b] rows that follow those of batches 0..b-1; rowptr has
+ * sum(n_rows)+1 entries and rowptr[0] == 0.  Each batch is encoded on its own
+ * exactly as toc_encode would (its own prefix tree; section 3.1).  out[] receives
+ * n_batches handles; on any error none is kept and all out[b] are NULL. */
+toc_status toc_encode_batches(int64_t n_batches, const int32_t *n_rows, int32_t n_cols,
+                              const int64_t *rowptr, const int32_t *col,
+                              const float *val, int32_t n_threads, toc_enc **out);
+
+/* Sizes and counts of an encoded batch (see toc_enc_info). */
+toc_status toc_enc_info_get(const toc_enc *enc, toc_enc_info *info);
+
+/* Copy out (I, D) in the numbering of Algorithm 1 (node 0 is the root, I holds
+ * nodes 1..|I|).  I_col/I_val: n_first entries; D_rowptr: n_rows+1 entries
+ * (offsets into D_codes); D_codes: n_codes entries.  Any pointer may be NULL to
+ * skip that array.  Host memory, caller-owned. */
+toc_status toc_enc_export(const toc_enc *enc, int32_t *I_col, float *I_val,
+                          int64_t *D_rowptr, uint32_t *D_codes);
+
+void toc_enc_free(toc_enc *enc);
+
+/* ---------------------------------------------------------------------------
+ * Upload.  Rebuilds the decoding tree C' of each batch from (I, D) with
+ * Algorithm 2 (section 4.1.2), derives each node's depth, keeps the live codes
+ * (those referenced by D and their ancestors; the others take part in no
+ * operation of section 4), orders them by depth so that every parent precedes its
+ * children, renumbers parents and D, and writes the result into `buf` as one
+ * structure-of-arrays image laid out as described by toc_layout below.
+ *
+ * All batches must have the same n_cols.  toc_upload_size gives the bytes `buf`
+ * needs; toc_upload copies the image with hipMemcpyAsync on `stream` and waits
+ * for it, so the handles in `encs` may be freed afterwards.  `buf` must stay
+ * allocated for as long as the returned toc_dev is used.
+ * flags: TOC_UPLOAD_KEEP_DEAD keeps every node of C' (results are identical);
+ *        TOC_UPLOAD_HOST writes the image into host memory `buf` without any HIP
+ *        call (for inspection; device operations reject such a toc_dev).
+ * Errors: TOC_EINVAL (NULL, n_batches < 0, mismatched n_cols, unknown flag),
+ * TOC_ESIZE (bytes < toc_upload_size), TOC_EUNSUPPORTED (a batch above 2^31-1
+ * codes or rows), TOC_EDEVICE, TOC_ENOMEM.
+ * ------------------------------------------------------------------------- */
+#define TOC_UPLOAD_KEEP_DEAD 1u
+#define TOC_UPLOAD_HOST 2u
+
+toc_status toc_upload_size(const toc_enc *const *encs, int64_t n_batches,
+                           uint32_t flags, size_t *bytes);
+toc_status toc_upload(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
+                      void *buf, size_t bytes, void *stream, toc_dev **out);
+void toc_dev_free(toc_dev *dev); /* frees the descriptor only, never `buf` */
+
+typedef struct {
+  int64_t n_batches;
+  int64_t n_rows;        /* sum of rows over batches (rows of R, G, CSR)           */
+  int32_t n_cols;        /* m                                                      */
+  int32_t max_depth;     /* over all batches                                       */
+  int64_t nnz;           /* pairs over all batches (decoded CSR size)              */
+  int64_t n_codes;       /* |D| over all batches                                   */
+  int64_t n_stored;      /* codes stored in the image (live, or all with KEEP_DEAD)*/
+  int64_t n_deep;        /* stored codes of depth >= 2                             */
+  int64_t canon_bytes;   /* sum of toc_enc_info.canon_bytes                        */
+  int64_t image_bytes;   /* bytes of the uploaded image                            */
+} toc_dev_info;
+
+toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
+
+/* Byte offsets (from `buf`) of the arrays of the uploaded image.  Codes of batch b
+ * are local indices 0..n_codes-1, stored from code_base; local code c is at
+ * depth d when level[lvl_base+d-1] <= c < level[lvl_base+d] (level[lvl_base] = 0).
+ * Depth-1 codes come first; among them the n_int1 codes that have children
+ * precede the others.  Within a level the order of Algorithm 2 is kept.
+ *   batches : toc_batch[n_batches]
+ *   level   : uint32 per batch n_levels+1 entries (lvl_base)
+ *   parent  : uint32 local parent of each code (0xFFFFFFFF at depth 1)
+ *   col     : uint32 key column of each code
+ *   val     : float  key value of each code
+ *   depth   : uint32 depth of each code
+ *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
+ *   dcodes  : uint32 local code of each entry of D (d_base)                      */
+typedef struct {
+  int64_t code_base, d_base, row_base, span_base, nnz_base, deep_base, tree_base,
+      lvl_base;
+  int32_t n_rows, n_codes, n_lvl1, n_int1, n_levels, n_d;
+  int32_t pad[2];
+} toc_batch;
+
+typedef struct {
+  int64_t batches, level, parent, col, val, depth, span, dcodes, end;
+} toc_layout;
+
+toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);
+
+/* ---------------------------------------------------------------------------
+ * Device operations.  Workspace: toc_workspace_size gives the bytes an op needs
+ * to run in one pass over all batches; an op given less (but at least its
+ * per-batch minimum, returned in *min_bytes when not NULL) runs in several
+ * passes; less than the minimum is TOC_ESIZE.  A size of 0 means ws may be NULL.
+ * The workspace is scratch: its contents on entry do not matter.
+ * op: TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE.
+ * ------------------------------------------------------------------------- */
+#define TOC_OP_RIGHT 0
+#define TOC_OP_LEFT 1
+#define TOC_OP_DECODE 2
+
+toc_status toc_workspace_size(const toc_dev *dev, int32_t op, int32_t k,
+                              size_t *bytes, size_t *min_bytes);
+
+/* Right multiplication R = A.W on every batch (Theorem 1; Algorithm 4 for k = 1,
+ * Algorithm 7 for a matrix): the dictionary table H[c] = H[parent(c)] +
+ * val(c) W[col(c), :] built level by level over C', then R[i, :] = sum of H over
+ * the codes of tuple i.  W: n_cols x k, row-major with row stride ldw >= k.
+ * R: (sum of rows) x k, row stride ldr >= k, rows stacked in batch order.
+ * Errors: TOC_EINVAL (k < 1, strides, NULL, host-image toc_dev), TOC_ESIZE,
+ * TOC_EDEVICE. */
+toc_status toc_right_mul(const toc_dev *dev, const float *W, int32_t k, int64_t ldw,
+                         float *R, int64_t ldr, void *ws, size_t ws_bytes,
+                         void *stream);
+
+/* Left multiplication G^T.A on every batch (Theorem 2; Algorithm 5 for k = 1,
+ * Algorithm 8 for a matrix): scatter G rows onto the codes of each tuple,
+ * propagate child to parent in reverse depth order, and accumulate
+ * val(c) H[c, :] into out[col(c), :].  The result is stored transposed, one
+ * n_cols x k block per batch: out[(b n_cols + j) ldo + q] = (G_b^T A_b)[q, j].
+ * G: (sum of rows) x k, row stride ldg >= k.  accumulate != 0 adds into out
+ * instead of overwriting it.  Errors as toc_right_mul. */
+toc_status toc_left_mul(const toc_dev *dev, const float *G, int32_t k, int64_t ldg,
+                        float *out, int64_t ldo, int32_t accumulate, void *ws,
+                        size_t ws_bytes, void *stream);
+
+/* Full decode of every batch to one CSR (the backtracking of Algorithm 6, without
+ * its densify step): rowptr[(sum of rows)+1] (int64), col[nnz] (int32),
+ * val[nnz] (float, bit-identical to the encoded values).  Rows in batch order.
+ * Errors: TOC_EINVAL, TOC_EDEVICE. */
+toc_status toc_decode_csr(const toc_dev *dev, int64_t *rowptr, int32_t *col,
+                          float *val, void *stream);
+
+/* Message for the last non-OK status returned on this thread. */
+const char *toc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TOC_H */

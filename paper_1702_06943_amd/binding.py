@@ -1,0 +1,280 @@
+"""ctypes binding of libtoc.so: argument marshalling only.
+
+Every function has the name of the C entry point it calls (include/toc.h) and
+raises TocError on any status other than TOC_OK.  Host arrays are numpy arrays;
+device arrays are torch tensors on the GPU, used only for their pointers; the
+stream defaults to torch's current stream.  Nothing here computes any part of the
+compression or of the products.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtoc.so")
+
+TOC_OK, TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED = range(6)
+TOC_UPLOAD_KEEP_DEAD = 1
+TOC_UPLOAD_HOST = 2
+TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE = 0, 1, 2
+STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
+                4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
+
+
+class TocError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class EncInfo(C.Structure):
+    _fields_ = [("n_rows", C.c_int32), ("n_cols", C.c_int32), ("nnz", C.c_int64),
+                ("n_first", C.c_int64), ("n_codes", C.c_int64), ("n_nodes", C.c_int64),
+                ("n_live", C.c_int64), ("n_deep", C.c_int64), ("max_depth", C.c_int32),
+                ("reserved", C.c_int32), ("phys_bytes", C.c_int64),
+                ("canon_bytes", C.c_int64)]
+
+
+class DevInfo(C.Structure):
+    _fields_ = [("n_batches", C.c_int64), ("n_rows", C.c_int64), ("n_cols", C.c_int32),
+                ("max_depth", C.c_int32), ("nnz", C.c_int64), ("n_codes", C.c_int64),
+                ("n_stored", C.c_int64), ("n_deep", C.c_int64), ("canon_bytes", C.c_int64),
+                ("image_bytes", C.c_int64)]
+
+
+class Layout(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in
+                ("batches", "level", "parent", "col", "val", "depth", "span", "dcodes", "end")]
+
+
+BATCH_DTYPE = np.dtype([
+    ("code_base", "<i8"), ("d_base", "<i8"), ("row_base", "<i8"), ("span_base", "<i8"),
+    ("nnz_base", "<i8"), ("deep_base", "<i8"), ("tree_base", "<i8"), ("lvl_base", "<i8"),
+    ("n_rows", "<i4"), ("n_codes", "<i4"), ("n_lvl1", "<i4"), ("n_int1", "<i4"),
+    ("n_levels", "<i4"), ("n_d", "<i4"), ("pad", "<i4", (2,))])
+
+_lib = None
+
+
+def lib():
+    """The loaded libtoc.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_1702_06943_amd.build`")
+    # torch ships its own HIP runtime under the same soname; loading torch first
+    # makes libtoc bind to that one, so that streams and device pointers agree.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    L = C.CDLL(LIB_PATH)
+    P, I32, I64, U32, SZ = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_size_t
+    sig = {
+        "toc_encode": [I32, I32, P, P, P, P],
+        "toc_encode_batches": [I64, P, I32, P, P, P, I32, P],
+        "toc_enc_info_get": [P, P],
+        "toc_enc_export": [P, P, P, P, P],
+        "toc_upload_size": [P, I64, U32, P],
+        "toc_upload": [P, I64, U32, P, SZ, P, P],
+        "toc_dev_info_get": [P, P],
+        "toc_dev_layout_get": [P, P],
+        "toc_workspace_size": [P, I32, I32, P, P],
+        "toc_right_mul": [P, P, I32, I64, P, I64, P, SZ, P],
+        "toc_left_mul": [P, P, I32, I64, P, I64, I32, P, SZ, P],
+        "toc_decode_csr": [P, P, P, P, P],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    L.toc_enc_free.argtypes = [P]
+    L.toc_enc_free.restype = None
+    L.toc_dev_free.argtypes = [P]
+    L.toc_dev_free.restype = None
+    L.toc_last_error.argtypes = []
+    L.toc_last_error.restype = C.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status):
+    if status != TOC_OK:
+        raise TocError(status, lib().toc_last_error().decode(errors="replace"))
+
+
+def _ptr(a):
+    """Pointer of a numpy array or torch tensor (None -> NULL)."""
+    if a is None:
+        return None
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data if a.size else None
+    return a.data_ptr() if a.numel() else None
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Enc:
+    """Owner of a toc_enc handle."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.toc_enc_free(self.handle)
+            self.handle = None
+
+
+class Dev:
+    """Owner of a toc_dev descriptor; keeps the image buffer alive."""
+
+    def __init__(self, handle, buf):
+        self.handle = handle
+        self.buf = buf
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.toc_dev_free(self.handle)
+            self.handle = None
+
+
+def _arr(x, dtype):
+    return np.ascontiguousarray(np.asarray(x), dtype=dtype)
+
+
+def toc_encode(n_rows, n_cols, rowptr, col, val):
+    rowptr, col, val = _arr(rowptr, np.int64), _arr(col, np.int32), _arr(val, np.float32)
+    h = C.c_void_p()
+    _check(lib().toc_encode(int(n_rows), int(n_cols), _ptr(rowptr), _ptr(col), _ptr(val),
+                            C.byref(h)))
+    return Enc(h.value)
+
+
+def toc_encode_batches(n_rows, n_cols, rowptr, col, val, n_threads=0):
+    """n_rows: rows per batch; rowptr/col/val: one concatenated CSR."""
+    n_rows = _arr(n_rows, np.int32)
+    rowptr, col, val = _arr(rowptr, np.int64), _arr(col, np.int32), _arr(val, np.float32)
+    nb = len(n_rows)
+    handles = (C.c_void_p * max(nb, 1))()
+    _check(lib().toc_encode_batches(nb, _ptr(n_rows), int(n_cols), _ptr(rowptr), _ptr(col),
+                                    _ptr(val), int(n_threads), handles))
+    return [Enc(handles[b]) for b in range(nb)]
+
+
+def toc_enc_info_get(enc):
+    info = EncInfo()
+    _check(lib().toc_enc_info_get(enc.handle, C.byref(info)))
+    return {f: getattr(info, f) for f, _ in EncInfo._fields_ if f != "reserved"}
+
+
+def toc_enc_export(enc):
+    """-> (I_col int32, I_val float32, D_rowptr int64, D_codes uint32), paper numbering."""
+    info = toc_enc_info_get(enc)
+    I_col = np.empty(info["n_first"], np.int32)
+    I_val = np.empty(info["n_first"], np.float32)
+    D_rowptr = np.empty(info["n_rows"] + 1, np.int64)
+    D_codes = np.empty(info["n_codes"], np.uint32)
+    _check(lib().toc_enc_export(enc.handle, _ptr(I_col), _ptr(I_val), D_rowptr.ctypes.data,
+                                _ptr(D_codes)))
+    return I_col, I_val, D_rowptr, D_codes
+
+
+def _handles(encs):
+    arr = (C.c_void_p * max(len(encs), 1))()
+    for i, e in enumerate(encs):
+        arr[i] = e.handle
+    return arr
+
+
+def toc_upload_size(encs, flags=0):
+    n = C.c_size_t()
+    _check(lib().toc_upload_size(_handles(encs), len(encs), flags, C.byref(n)))
+    return n.value
+
+
+def toc_upload(encs, buf, flags=0, stream=None):
+    """buf: torch uint8 tensor on the GPU (or a numpy uint8 array with TOC_UPLOAD_HOST)."""
+    if isinstance(buf, np.ndarray):
+        nbytes, s = buf.nbytes, None
+    else:
+        nbytes, s = buf.numel() * buf.element_size(), _stream(stream)
+    h = C.c_void_p()
+    _check(lib().toc_upload(_handles(encs), len(encs), flags, _ptr(buf), nbytes, s,
+                            C.byref(h)))
+    return Dev(h.value, buf)
+
+
+def toc_dev_info_get(dev):
+    info = DevInfo()
+    _check(lib().toc_dev_info_get(dev.handle, C.byref(info)))
+    return {f: getattr(info, f) for f, _ in DevInfo._fields_}
+
+
+def toc_dev_layout_get(dev):
+    L = Layout()
+    _check(lib().toc_dev_layout_get(dev.handle, C.byref(L)))
+    return {f: getattr(L, f) for f, _ in Layout._fields_}
+
+
+def toc_workspace_size(dev, op, k):
+    n, mn = C.c_size_t(), C.c_size_t()
+    _check(lib().toc_workspace_size(dev.handle, op, int(k), C.byref(n), C.byref(mn)))
+    return n.value, mn.value
+
+
+def _mat(t, name):
+    """(pointer, leading dimension, k) of a row-major 2-D float32 device tensor."""
+    import torch
+    if t.dtype != torch.float32 or t.dim() != 2 or t.stride(1) != 1 or not t.is_cuda:
+        raise TocError(TOC_EINVAL, f"{name} must be a 2-D float32 CUDA tensor with unit "
+                                   "column stride")
+    return t.data_ptr(), max(t.stride(0), t.shape[1]), t.shape[1]
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def toc_right_mul(dev, W, R, ws=None, stream=None):
+    info = toc_dev_info_get(dev)
+    wp, ldw, k = _mat(W, "W")
+    rp, ldr, kr = _mat(R, "R")
+    if W.shape[0] != info["n_cols"] or R.shape[0] != info["n_rows"] or kr != k:
+        raise TocError(TOC_EINVAL, "W must be n_cols x k and R n_rows x k")
+    _check(lib().toc_right_mul(dev.handle, wp, k, ldw, rp, ldr, _ptr(ws), _nbytes(ws),
+                               _stream(stream)))
+
+
+def toc_left_mul(dev, G, out, accumulate=False, ws=None, stream=None):
+    """out: (n_batches * n_cols) x k, block b holding (G_b^T A_b)^T."""
+    info = toc_dev_info_get(dev)
+    gp, ldg, k = _mat(G, "G")
+    op_, ldo, ko = _mat(out, "out")
+    if (G.shape[0] != info["n_rows"] or out.shape[0] != info["n_batches"] * info["n_cols"]
+            or ko != k):
+        raise TocError(TOC_EINVAL, "G must be n_rows x k, out (n_batches*n_cols) x k")
+    _check(lib().toc_left_mul(dev.handle, gp, k, ldg, op_, ldo, int(bool(accumulate)),
+                              _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def toc_decode_csr(dev, rowptr, col, val, stream=None):
+    info = toc_dev_info_get(dev)
+    if (rowptr.numel() != info["n_rows"] + 1 or col.numel() != info["nnz"]
+            or val.numel() != info["nnz"]):
+        raise TocError(TOC_EINVAL, "rowptr/col/val sizes do not match the image")
+    _check(lib().toc_decode_csr(dev.handle, rowptr.data_ptr(), _ptr(col), _ptr(val),
+                                _stream(stream)))

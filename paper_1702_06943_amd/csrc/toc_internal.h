@@ -1,0 +1,53 @@
+// Internal declarations shared by the host encoder/upload code and the device code.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "toc.h"
+
+// One encoded mini-batch: (I, D) of Algorithm 1 plus counts of its prefix tree,
+// gathered while encoding (the tree itself is not kept: C' is rebuilt from (I, D)
+// by Algorithm 2 at upload time).
+struct toc_enc {
+  int32_t n_rows = 0, n_cols = 0;
+  int64_t nnz = 0;
+  std::vector<int32_t> I_col;
+  std::vector<uint32_t> I_bits;
+  std::vector<int64_t> D_rowptr;  // n_rows + 1
+  std::vector<uint32_t> D_codes;  // paper numbering, 1..n_nodes-1
+  int64_t n_nodes = 1;            // including the root
+  int64_t n_live = 0, n_deep_live = 0;
+  int32_t max_depth_live = 0, max_depth_all = 0;
+  int64_t n_deep_all = 0;
+};
+
+struct toc_dev {
+  void *buf = nullptr;
+  size_t bytes = 0;
+  bool host = false;
+  int device = -1;
+  uint32_t flags = 0;
+  toc_layout layout{};
+  toc_dev_info info{};
+  std::vector<toc_batch> batches;  // host copy of the batch table
+  int32_t max_rows = 0, max_codes = 0, max_levels = 0;
+  int64_t max_deep = 0, max_tree = 0, max_d = 0;
+  int64_t total_deep = 0, total_tree = 0;
+};
+
+namespace toc {
+
+// Records a message for toc_last_error() and returns s.
+toc_status fail(toc_status s, const char *fmt, ...);
+void clear_error();
+
+// Builds the upload image into `dst` (host memory of layout.end bytes).
+toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
+                       toc_dev *dev, uint8_t *dst);
+// Computes layout and totals only.
+toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
+                      toc_dev *dev);
+
+}  // namespace toc

@@ -1,0 +1,205 @@
+"""CPU checks of the upload image (TOC_UPLOAD_HOST writes it into host memory).
+
+The image is read back with numpy and checked against the invariants of the
+decoding tree (Algorithm 2) and against the oracle: walking it must decode every
+batch exactly and give the same fp64 products.
+"""
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_1702_06943_amd as T
+from workloads import config_batches, tiny_batch
+
+
+def read_image(dev, buf):
+    L = T.toc_dev_layout_get(dev)
+    info = T.toc_dev_info_get(dev)
+    nb = info["n_batches"]
+    bt = np.frombuffer(buf, T.BATCH_DTYPE, count=nb, offset=L["batches"])
+
+    def arr(name, dtype, count):
+        return np.frombuffer(buf, dtype, count=count, offset=L[name])
+
+    n_codes = info["n_stored"]
+    n_levels = int((bt["n_levels"] + 1).sum()) if nb else 0
+    img = dict(
+        bt=bt, info=info,
+        level=arr("level", np.uint32, n_levels),
+        parent=arr("parent", np.uint32, n_codes),
+        col=arr("col", np.uint32, n_codes),
+        val=arr("val", np.float32, n_codes),
+        depth=arr("depth", np.uint32, n_codes),
+        span=arr("span", np.uint32, int((bt["n_rows"] + 1).sum()) if nb else 0),
+        dcodes=arr("dcodes", np.uint32, info["n_codes"]),
+    )
+    return img
+
+
+def batch_view(img, b):
+    t = img["bt"][b]
+    cb, nc = int(t["code_base"]), int(t["n_codes"])
+    return dict(
+        t=t,
+        level=img["level"][int(t["lvl_base"]):int(t["lvl_base"]) + int(t["n_levels"]) + 1],
+        parent=img["parent"][cb:cb + nc], col=img["col"][cb:cb + nc],
+        val=img["val"][cb:cb + nc], depth=img["depth"][cb:cb + nc],
+        span=img["span"][int(t["span_base"]):int(t["span_base"]) + int(t["n_rows"]) + 1],
+        dc=img["dcodes"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
+    )
+
+
+def check_invariants(v):
+    t = v["t"]
+    nc, n1, ni, nl = int(t["n_codes"]), int(t["n_lvl1"]), int(t["n_int1"]), int(t["n_levels"])
+    lv = v["level"]
+    assert lv[0] == 0 and lv[-1] == nc and np.all(np.diff(lv.astype(np.int64)) >= 0)
+    assert (lv[1] if nl else 0) == n1
+    for d in range(1, nl + 1):
+        codes = np.arange(lv[d - 1], lv[d])
+        assert np.all(v["depth"][codes] == d)
+        if d == 1:
+            assert np.all(v["parent"][codes] == 0xFFFFFFFF)
+        else:
+            p = v["parent"][codes]
+            assert np.all((p >= lv[d - 2]) & (p < lv[d - 1])), "parent one level up"
+    # depth-1 codes with children come first
+    has_child = np.zeros(nc, bool)
+    deep = v["parent"] != 0xFFFFFFFF
+    has_child[v["parent"][deep]] = True
+    assert np.all(has_child[:ni]) and not np.any(has_child[ni:n1])
+    # siblings have distinct keys
+    keys = set()
+    for c in range(nc):
+        k = (int(v["parent"][c]), int(v["col"][c]), int(v["val"][c:c + 1].view(np.uint32)[0]))
+        assert k not in keys
+        keys.add(k)
+    assert np.all(v["dc"] < nc)
+    assert v["span"][0] == 0 and v["span"][-1] == len(v["dc"])
+
+
+def walk_decode(v):
+    rows = []
+    span, dc = v["span"], v["dc"]
+    bits = v["val"].view(np.uint32)
+    for r in range(len(span) - 1):
+        row = []
+        for c in dc[span[r]:span[r + 1]]:
+            seq = []
+            x = int(c)
+            while x != 0xFFFFFFFF:
+                seq.append((int(v["col"][x]), int(bits[x])))
+                x = int(v["parent"][x])
+            row.extend(seq[::-1])
+        rows.append(row)
+    return rows
+
+
+BATCHES = [
+    ("tiny", dict(n_rows=12, n_cols=9, density=0.9, n_values=2, prefix_copy=0.8)),
+    ("tiny", dict(n_rows=30, n_cols=20, density=0.5, n_values=3, prefix_copy=0.5)),
+    ("tiny", dict(n_rows=3, n_cols=4, density=0.0, n_values=1)),
+    ("tiny", dict(n_rows=1, n_cols=50, density=1.0, n_values=1)),
+]
+
+
+def _tiny_csrs():
+    out = []
+    for i, (_, spec) in enumerate(BATCHES):
+        rp, c, v = tiny_batch(77 + i, zeros=True, **{**spec, "n_cols": 50})
+        out.append((spec["n_rows"], rp, c, v))
+    return out
+
+
+@pytest.mark.parametrize("flags", [0, T.TOC_UPLOAD_KEEP_DEAD])
+def test_image_invariants_and_walk(flags):
+    csrs = _tiny_csrs()
+    B = config_batches("c1", 0, 1)
+    csrs.append(B.batch(0)[:1] + B.batch(0)[1:])
+    n_cols = 68
+    csrs = [(n, rp, c, v) for (n, rp, c, v) in csrs]
+    # pad tiny batches to the same n_cols as c1
+    encs, oracle_rows = [], []
+    for n, rp, c, v in csrs:
+        encs.append(T.toc_encode(n, n_cols, rp, c, v))
+        oracle_rows.append(O.canonicalize(n, n_cols, rp, c, v))
+    size = T.toc_upload_size(encs, flags)
+    buf = np.zeros(size, np.uint8)
+    dev = T.toc_upload(encs, buf, flags | T.TOC_UPLOAD_HOST)
+    img = read_image(dev, buf)
+    assert img["info"]["n_batches"] == len(encs)
+    nnz_base = 0
+    for b, rows in enumerate(oracle_rows):
+        v = batch_view(img, b)
+        check_invariants(v)
+        assert walk_decode(v) == rows
+        assert int(v["t"]["nnz_base"]) == nnz_base
+        nnz_base += sum(len(r) for r in rows)
+        I, D, N = O.encode(rows)
+        st = O.layout_stats(I, D)
+        if flags & T.TOC_UPLOAD_KEEP_DEAD:
+            assert int(v["t"]["n_codes"]) == N - 1
+        else:
+            assert int(v["t"]["n_codes"]) == st["n_live"]
+            assert int(v["t"]["n_levels"]) == st["max_depth"]
+    assert img["info"]["nnz"] == nnz_base
+
+
+def test_image_products_match_oracle():
+    """fp64 products computed by walking the image equal the oracle's."""
+    B = config_batches("c1", 0, 1)
+    n, rp, cc, vv = B.batch(0)
+    enc = T.toc_encode(n, B.n_cols, rp, cc, vv)
+    buf = np.zeros(T.toc_upload_size([enc]), np.uint8)
+    dev = T.toc_upload([enc], buf, T.TOC_UPLOAD_HOST)
+    im = batch_view(read_image(dev, buf), 0)
+    rng = np.random.default_rng(0)
+    W = rng.standard_normal((B.n_cols, 2))
+    G = rng.standard_normal((n, 2))
+    nc = len(im["col"])
+    H = np.zeros((nc, 2))
+    for c in range(nc):
+        p = int(im["parent"][c])
+        H[c] = im["val"][c] * W[im["col"][c]] + (H[p] if p != 0xFFFFFFFF else 0)
+    R = np.array([H[im["dc"][im["span"][r]:im["span"][r + 1]]].sum(0) for r in range(n)])
+    rows = O.canonicalize(n, B.n_cols, rp, cc, vv)
+    R_o, S = O.dense_right(rows, B.n_cols, W)
+    assert np.all(np.abs(R - R_o) <= 1e-12 * S)
+    H = np.zeros((nc, 2))
+    for r in range(n):
+        for x in im["dc"][im["span"][r]:im["span"][r + 1]]:
+            H[x] += G[r]
+    out = np.zeros((B.n_cols, 2))
+    for c in range(nc - 1, -1, -1):
+        out[im["col"][c]] += im["val"][c] * H[c]
+        p = int(im["parent"][c])
+        if p != 0xFFFFFFFF:
+            H[p] += H[c]
+    out_o, S = O.dense_left(rows, B.n_cols, G)
+    assert np.all(np.abs(out - out_o) <= 1e-12 * S)
+
+
+def test_upload_errors():
+    e1 = T.toc_encode(1, 3, [0, 1], [0], np.ones(1, np.float32))
+    e2 = T.toc_encode(1, 4, [0, 1], [0], np.ones(1, np.float32))
+    with pytest.raises(T.TocError) as ei:
+        T.toc_upload_size([e1, e2])
+    assert ei.value.status == T.TOC_EINVAL
+    size = T.toc_upload_size([e1])
+    with pytest.raises(T.TocError) as ei:
+        T.toc_upload([e1], np.zeros(size - 1, np.uint8), T.TOC_UPLOAD_HOST)
+    assert ei.value.status == T.TOC_ESIZE
+    with pytest.raises(T.TocError) as ei:
+        T.toc_upload_size([e1], 1 << 7)
+    assert ei.value.status == T.TOC_EINVAL
+
+
+def test_host_image_rejected_by_device_ops():
+    e1 = T.toc_encode(1, 3, [0, 1], [0], np.ones(1, np.float32))
+    buf = np.zeros(T.toc_upload_size([e1]), np.uint8)
+    dev = T.toc_upload([e1], buf, T.TOC_UPLOAD_HOST)
+    lib = T.lib()
+    assert lib.toc_right_mul(dev.handle, 8, 1, 1, 8, 1, None, 0, None) == T.TOC_EINVAL
+    assert "host" in lib.toc_last_error().decode()
+    assert lib.toc_decode_csr(dev.handle, 8, 8, 8, None) == T.TOC_EINVAL

@@ -14,4 +14,5 @@ from .gen import (  # noqa: F401
     config_G,
     tiny_batch,
     dense_normal,
+    dense_normal_device,
 )
