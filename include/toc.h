@@ -147,7 +147,7 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  * are local indices 0..n_codes-1, stored from code_base; local code c is at
  * depth d when level[lvl_base+d-1] <= c < level[lvl_base+d] (level[lvl_base] = 0).
  * Depth-1 codes come first; among them the n_int1 codes that have children
- * precede the others.  Within a level the order of Algorithm 2 is kept.
+ * precede the others.
  *   batches : toc_batch[n_batches]
  *   level   : uint32 per batch n_levels+1 entries (lvl_base)
  *   parent  : uint32 local parent of each code (0xFFFFFFFF at depth 1)
@@ -155,7 +155,14 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   val     : float  key value of each code
  *   depth   : uint32 depth of each code
  *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
- *   dcodes  : uint32 local code of each entry of D (d_base)                      */
+ *   dcodes  : uint32 local code of each entry of D (d_base)
+ *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b)
+ *   occ_row : uint32 row of each entry of D, grouped by code (d_base): D inverted,
+ *             the index set of the sum that defines G(x) in Theorem 2
+ *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
+ *             by key column (tree_base)
+ * Depth-1 codes without children are sorted by key column; the codes of each
+ * level d >= 2 are sorted by parent.                                             */
 typedef struct {
   int64_t code_base, d_base, row_base, span_base, nnz_base, deep_base, tree_base,
       lvl_base;
@@ -164,7 +171,8 @@ typedef struct {
 } toc_batch;
 
 typedef struct {
-  int64_t batches, level, parent, col, val, depth, span, dcodes, end;
+  int64_t batches, level, parent, col, val, depth, span, dcodes, occ_off, occ_row, tlist,
+      end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

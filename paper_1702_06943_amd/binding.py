@@ -48,7 +48,8 @@ class DevInfo(C.Structure):
 
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
-                ("batches", "level", "parent", "col", "val", "depth", "span", "dcodes", "end")]
+                ("batches", "level", "parent", "col", "val", "depth", "span", "dcodes",
+                 "occ_off", "occ_row", "tlist", "end")]
 
 
 BATCH_DTYPE = np.dtype([

@@ -22,7 +22,6 @@ constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / kWave;
 constexpr int kMaxKpl = 8;                    // wide kernels: up to 8 columns per lane
 constexpr int kKTile = kWave * kMaxKpl;       // 512 columns per pass
-constexpr int kRowsTile = 1024;               // decode: rows scanned per LDS pass
 constexpr size_t kLdsMax = 160 * 1024;        // gfx950 LDS per workgroup
 constexpr int kOutLdsMax = 8192;              // k = 1 left: out block kept in LDS up to m
 
@@ -313,45 +312,297 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
 }
 
 // ===========================================================================
-// Decode to CSR (Algorithm 6's backtracking): per tuple, row length = sum of the
-// depths of its codes; an exclusive scan gives row starts; each code writes its
-// sequence backwards while walking to the root.
+// Tiled kernels for wide k.  One workgroup per (batch, column tile); the tiles of
+// a batch are consecutive blocks of one XCD (the dispatcher deals blocks to the
+// 8 XCDs round-robin), so they share the batch's image through that XCD's L2.
 // ===========================================================================
-__device__ void block_exclusive_scan(uint32_t *a, int n, uint32_t *wave_tot, uint32_t &total) {
-  // n <= 4 * kBlock; each thread owns 4 consecutive entries
-  const int t = threadIdx.x, lane = t % kWave, w = t / kWave;
-  uint32_t v[4], s = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int x = 4 * t + i;
-    v[i] = x < n ? a[x] : 0u;
-    s += v[i];
-  }
-  const uint32_t incl = wave_incl_scan(s, lane);
-  if (lane == kWave - 1) wave_tot[w] = incl;
-  __syncthreads();
-  uint32_t off = 0, tot = 0;
-  for (int i = 0; i < kWaves; ++i) {
-    if (i < w) off += wave_tot[i];
-    tot += wave_tot[i];
-  }
-  uint32_t run = off + incl - s;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int x = 4 * t + i;
-    if (x < n) a[x] = run;
-    run += v[i];
-  }
-  total = tot;
-  __syncthreads();
+constexpr int kXcd = 8;
+constexpr int kTileBlock = 512;
+constexpr int kTileWaves = kTileBlock / kWave;
+
+__device__ inline void xcd_tile_map(int64_t blk, int n_tiles, int64_t &b, int &tile) {
+  const int64_t x = blk % kXcd, j = blk / kXcd;
+  tile = (int)(j % n_tiles);
+  b = (j / n_tiles) * kXcd + x;
 }
 
-__global__ __launch_bounds__(kBlock) void decode_kernel(Img im, int64_t b0,
-                                                        int64_t *__restrict__ rowptr,
-                                                        int32_t *__restrict__ ocol,
-                                                        uint32_t *__restrict__ oval) {
-  __shared__ uint32_t rlen[kRowsTile];
-  __shared__ uint32_t wave_tot[kWaves];
+__device__ inline float4 f4fma(float s, float4 x, float4 a) {
+  return make_float4(fmaf(s, x.x, a.x), fmaf(s, x.y, a.y), fmaf(s, x.z, a.z), fmaf(s, x.w, a.w));
+}
+
+// Right multiplication with a KT-column tile of W resident in LDS.  Lanes form 8
+// groups of 8; a lane holds 4 consecutive columns, so a group covers the tile
+// for one code and a wave takes 8 codes of a tuple per step.  H rows of depth >= 2
+// codes are built level by level first (in LDS when they fit, else in `ws`).
+constexpr int kRtKT = 32;
+constexpr uint32_t kRtGlobal = 0x80000000u;   // staged address refers to ws
+
+template <bool DEEP_LDS>
+__global__ __launch_bounds__(kTileBlock) void right_tiled_kernel(
+    Img im, int64_t b0, int64_t nb, int n_tiles, int m, const float *__restrict__ W,
+    int64_t ldw, int k, float *__restrict__ R, int64_t ldr, float *__restrict__ ws,
+    int64_t ws_base) {
+  extern __shared__ float4 smem4[];
+  float *lds = (float *)smem4;
+  int64_t bl;
+  int tile;
+  xcd_tile_map(blockIdx.x, n_tiles, bl, tile);
+  if (bl >= nb) return;
+  const int64_t b = b0 + bl;
+  const toc_batch bt = im.batches[b];
+  const int k0 = tile * kRtKT;
+  const int kt = min(kRtKT, k - k0);
+  const uint32_t *lvl = im.level + bt.lvl_base;
+  const uint32_t *par = im.parent + bt.code_base;
+  const uint32_t *col = im.col + bt.code_base;
+  const float *val = im.val + bt.code_base;
+  const uint32_t n1 = (uint32_t)bt.n_lvl1;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int grp = lane / 8, q = 4 * (lane % 8);
+  float *Wt = lds;                                   // m rows of kRtKT floats
+  float *Hl = lds + (size_t)m * kRtKT;               // deep rows (DEEP_LDS)
+  const int64_t kpad = (int64_t)n_tiles * kRtKT;
+  float *Hg = ws + (bt.deep_base - ws_base) * kpad + k0;
+  // stage W[:, k0:k0+kt]
+  for (int e = threadIdx.x; e < m * (kRtKT / 4); e += kTileBlock) {
+    const int c = e / (kRtKT / 4), q4 = 4 * (e % (kRtKT / 4));
+    const float *src = W + (int64_t)c * ldw + k0 + q4;
+    float4 v;
+    v.x = q4 + 0 < kt ? src[0] : 0.0f;
+    v.y = q4 + 1 < kt ? src[1] : 0.0f;
+    v.z = q4 + 2 < kt ? src[2] : 0.0f;
+    v.w = q4 + 3 < kt ? src[3] : 0.0f;
+    *(float4 *)&Wt[c * kRtKT + q4] = v;
+  }
+  __syncthreads();
+  // H of depth >= 2 codes, level by level
+  for (int d = 2; d <= bt.n_levels; ++d) {
+    const uint32_t a = lvl[d - 1], e = lvl[d];
+    for (uint32_t c = a + wave * 8 + grp; c < e; c += kTileWaves * 8) {
+      const uint32_t p = par[c];
+      float4 base;
+      if (p < n1) {
+        base = *(const float4 *)&Wt[col[p] * kRtKT + q];
+        const float vp = val[p];
+        base = make_float4(vp * base.x, vp * base.y, vp * base.z, vp * base.w);
+      } else if (DEEP_LDS) {
+        base = *(const float4 *)&Hl[(p - n1) * kRtKT + q];
+      } else {
+        base = *(const float4 *)&Hg[(int64_t)(p - n1) * kpad + q];
+      }
+      const float4 h = f4fma(val[c], *(const float4 *)&Wt[col[c] * kRtKT + q], base);
+      if (DEEP_LDS) *(float4 *)&Hl[(c - n1) * kRtKT + q] = h;
+      else *(float4 *)&Hg[(int64_t)(c - n1) * kpad + q] = h;
+    }
+    __syncthreads();
+  }
+  // per-tuple sums
+  const uint32_t *span = im.span + bt.span_base;
+  const uint32_t *dc = im.dcodes + bt.d_base;
+  for (int r = wave; r < bt.n_rows; r += kTileWaves) {
+    const uint32_t s = span[r], e = span[r + 1];
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (uint32_t j0 = s; j0 < e; j0 += kWave) {
+      const uint32_t n = min((uint32_t)kWave, e - j0);
+      // lane i fetches code j0+i: LDS row offset and multiplier
+      uint32_t my_addr = 0;
+      float my_mult = 0.0f;
+      if ((uint32_t)lane < n) {
+        const uint32_t c = dc[j0 + lane];
+        if (c < n1) {
+          my_addr = col[c] * kRtKT;
+          my_mult = val[c];
+        } else {
+          my_addr = DEEP_LDS ? (uint32_t)m * kRtKT + (c - n1) * kRtKT : (kRtGlobal | (c - n1));
+          my_mult = 1.0f;
+        }
+      }
+      // every lane takes part in the shuffles; lanes past n carry multiplier 0
+      for (uint32_t t0 = 0; t0 < n; t0 += 8) {
+        const int t = (int)t0 + grp;
+        const uint32_t addr = (uint32_t)__shfl((int)my_addr, t, kWave);
+        const float mult = __shfl(my_mult, t, kWave);
+        float4 x;
+        if (!DEEP_LDS && (addr & kRtGlobal))
+          x = *(const float4 *)&Hg[(int64_t)(addr & ~kRtGlobal) * kpad + q];
+        else
+          x = *(const float4 *)&lds[addr + q];
+        acc = f4fma(mult, x, acc);
+      }
+    }
+#pragma unroll
+    for (int o = 8; o < kWave; o <<= 1) {
+      acc.x += __shfl_xor(acc.x, o, kWave);
+      acc.y += __shfl_xor(acc.y, o, kWave);
+      acc.z += __shfl_xor(acc.z, o, kWave);
+      acc.w += __shfl_xor(acc.w, o, kWave);
+    }
+    if (grp == 0) {
+      float *rr = R + (bt.row_base + r) * ldr + k0 + q;
+      if (q + 0 < kt) rr[0] = acc.x;
+      if (q + 1 < kt) rr[1] = acc.y;
+      if (q + 2 < kt) rr[2] = acc.z;
+      if (q + 3 < kt) rr[3] = acc.w;
+    }
+  }
+}
+
+// Left multiplication by pulling (Theorem 2 read as a definition): for each code,
+// G(x) = sum of G rows over the entries of D equal to x (the inverted index
+// occ_off/occ_row), plus the G values of its children; out[col] = sum over the
+// codes with that key column of val * G(x).  No atomics: each output row and each
+// H row has one writer.  A KT-column tile of G lives in LDS; lane = column.
+constexpr int kLpKT = 64;
+constexpr int kLpColsPerGrab = 4;
+
+__device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
+}
+
+template <int DUMMY>
+__global__ __launch_bounds__(kTileBlock) void left_pull_kernel(
+    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
+    const uint32_t *__restrict__ tlist_all, int64_t b0, int64_t nb, int n_tiles, int m,
+    const float *__restrict__ G, int64_t ldg, int k, float *__restrict__ out, int64_t ldo,
+    int accumulate, float *__restrict__ ws, int64_t ws_base) {
+  extern __shared__ float4 smem4[];
+  __shared__ uint32_t ctr;
+  int64_t bl;
+  int tile;
+  xcd_tile_map(blockIdx.x, n_tiles, bl, tile);
+  if (bl >= nb) return;
+  const int64_t b = b0 + bl;
+  const toc_batch bt = im.batches[b];
+  const int k0 = tile * kLpKT;
+  const int kt = min(kLpKT, k - k0);
+  const uint32_t *lvl = im.level + bt.lvl_base;
+  const uint32_t *par = im.parent + bt.code_base;
+  const uint32_t *col = im.col + bt.code_base;
+  const float *val = im.val + bt.code_base;
+  const uint32_t *oo = occ_off_all + bt.code_base + b;
+  const uint32_t *orow = occ_row_all + bt.d_base;
+  const uint32_t *tl = tlist_all + bt.tree_base;
+  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+  const uint32_t n_tree = ni + (nc - n1);
+  const int nrows = bt.n_rows;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  float *Gt = (float *)smem4;                          // nrows x kLpKT
+  uint32_t *Loff = (uint32_t *)(Gt + (size_t)nrows * kLpKT);  // m + 1
+  uint32_t *Toff = Loff + m + 1;                       // m + 1
+  uint32_t *Coff = Toff + m + 1;                       // n_tree + 1
+  const int64_t kpad = (int64_t)n_tiles * kLpKT;
+  float *Ht = ws + (bt.tree_base - ws_base) * kpad + k0;
+  auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
+  for (int e = threadIdx.x; e < nrows * kLpKT; e += kTileBlock) {
+    const int r = e / kLpKT, qq = e % kLpKT;
+    Gt[e] = qq < kt ? G[(bt.row_base + r) * ldg + k0 + qq] : 0.0f;
+  }
+  // column boundaries of the depth-1 leaves [ni, n1) (sorted by column)
+  for (uint32_t i = ni + threadIdx.x; i < n1; i += kTileBlock) {
+    const int64_t cc = col[i], cp = i > ni ? (int64_t)col[i - 1] : -1;
+    for (int64_t j = cp + 1; j <= cc; ++j) Loff[j] = i;
+  }
+  {
+    const int64_t last = n1 > ni ? (int64_t)col[n1 - 1] : -1;
+    for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kTileBlock) Loff[j] = n1;
+  }
+  // column boundaries of the tree-code list
+  for (uint32_t t = threadIdx.x; t < n_tree; t += kTileBlock) {
+    const int64_t cc = col[tl[t]], cp = t > 0 ? (int64_t)col[tl[t - 1]] : -1;
+    for (int64_t j = cp + 1; j <= cc; ++j) Toff[j] = t;
+  }
+  {
+    const int64_t last = n_tree > 0 ? (int64_t)col[tl[n_tree - 1]] : -1;
+    for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kTileBlock) Toff[j] = n_tree;
+  }
+  // children ranges: codes of depth >= 2 are sorted by (level, parent), so the
+  // children of the tree code with H row h are [Coff[h], Coff[h+1])
+  for (uint32_t c = n1 + threadIdx.x; c < nc; c += kTileBlock) {
+    const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
+    for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
+  }
+  {
+    const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
+    for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kTileBlock) Coff[h] = nc;
+  }
+  if (threadIdx.x == 0) ctr = 0;
+  __syncthreads();
+  // tree codes, deepest level first; one wave per code
+  for (int d = bt.n_levels; d >= 1; --d) {
+    const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+    for (uint32_t c = a + wave; c < e; c += kTileWaves) {
+      const uint32_t h = hrow(c);
+      float s = 0.0f;
+      for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) s += Gt[orow[o] * kLpKT + lane];
+      for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) s += Ht[(int64_t)hrow(ch) * kpad + lane];
+      Ht[(int64_t)h * kpad + lane] = s;
+    }
+    __syncthreads();
+  }
+  // columns, a few at a time per wave; code and occurrence info is fetched 64
+  // entries at a time into registers and broadcast with readlane
+  for (;;) {
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(&ctr, (uint32_t)kLpColsPerGrab);
+    base = rdlane(base, 0);
+    if (base >= (uint32_t)m) break;
+    const uint32_t jend = min(base + kLpColsPerGrab, (uint32_t)m);
+    bool have_c = false, have_o = false;
+    uint32_t cwin = 0, owin = 0, v_oo = 0, v_val = 0, v_row = 0;
+    for (uint32_t j = base; j < jend; ++j) {
+      float acc = 0.0f;
+      const uint32_t c_lo = Loff[j], c_hi = Loff[j + 1];
+      for (uint32_t c = c_lo; c < c_hi; ++c) {
+        if (!have_c || c - cwin >= 63u) {  // codes cwin..cwin+62 with both bounds
+          have_c = true;
+          cwin = c;
+          v_oo = c + lane <= nc ? oo[c + lane] : 0u;
+          v_val = c + lane < nc ? __float_as_uint(val[c + lane]) : 0u;
+        }
+        const uint32_t o_lo = rdlane(v_oo, c - cwin), o_hi = rdlane(v_oo, c - cwin + 1);
+        const float vc = __uint_as_float(rdlane(v_val, c - cwin));
+        float s = 0.0f;
+        for (uint32_t o = o_lo; o < o_hi; ++o) {
+          if (!have_o || o - owin >= 64u) {
+            have_o = true;
+            owin = o;
+            v_row = o + lane < (uint32_t)bt.n_d ? orow[o + lane] : 0u;
+          }
+          s += Gt[rdlane(v_row, o - owin) * kLpKT + lane];
+        }
+        acc = fmaf(vc, s, acc);
+      }
+      for (uint32_t t = Toff[j]; t < Toff[j + 1]; ++t) {
+        const uint32_t c = tl[t];
+        acc = fmaf(val[c], Ht[(int64_t)hrow(c) * kpad + lane], acc);
+      }
+      if (lane < kt) {
+        float *p = out + (b * m + j) * ldo + k0 + lane;
+        *p = accumulate ? *p + acc : acc;
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// Decode to CSR (the backtracking of Algorithm 6).  Rows are concatenated in D
+// and in the CSR alike, so the output position of entry j of D is the sum of the
+// depths of entries 0..j-1: one flat exclusive scan over D gives every position
+// and, at the row boundaries, rowptr.  Each entry then writes its sequence
+// backwards while walking to the root.
+// ===========================================================================
+constexpr int kDecBlock = 1024;
+constexpr int kDecWaves = kDecBlock / kWave;
+constexpr int kDecPer = 4;                       // entries of D per thread per tile
+constexpr int kDecTile = kDecBlock * kDecPer;
+
+__global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, int64_t b0,
+                                                           int64_t *__restrict__ rowptr,
+                                                           int32_t *__restrict__ ocol,
+                                                           uint32_t *__restrict__ oval) {
+  __shared__ uint32_t pre[kDecTile];
+  __shared__ uint32_t wave_tot[kDecWaves];
+  __shared__ uint32_t row_range[2];
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *par = im.parent + bt.code_base;
   const uint32_t *col = im.col + bt.code_base;
@@ -360,49 +611,63 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(Img im, int64_t b0,
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const uint32_t nd = (uint32_t)bt.n_d;
+  const int nrows = bt.n_rows;
+  // first row whose span starts at or after x (spans are non-decreasing)
+  auto lower_row = [&](uint32_t x) -> uint32_t {
+    uint32_t lo = 0, hi = (uint32_t)nrows + 1;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (span[mid] < x) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo;
+  };
   int64_t base = bt.nnz_base;
-  for (int t0 = 0; t0 < bt.n_rows; t0 += kRowsTile) {
-    const int nr = min(kRowsTile, bt.n_rows - t0);
-    for (int r = wave; r < nr; r += kWaves) {
-      const uint32_t s = span[t0 + r], e = span[t0 + r + 1];
-      uint32_t len = 0;
-      for (uint32_t j = s + lane; j < e; j += kWave) len += dep[dc[j]];
+  for (uint32_t t0 = 0; t0 < nd; t0 += kDecTile) {
+    uint32_t c[kDecPer], d[kDecPer], s = 0;
 #pragma unroll
-      for (int o = kWave / 2; o > 0; o >>= 1) len += __shfl_xor(len, o, kWave);
-      if (lane == 0) rlen[r] = len;
+    for (int i = 0; i < kDecPer; ++i) {
+      const uint32_t j = t0 + threadIdx.x * kDecPer + i;
+      c[i] = j < nd ? dc[j] : 0u;
+      d[i] = j < nd ? dep[c[i]] : 0u;
+      s += d[i];
+    }
+    const uint32_t incl = wave_incl_scan(s, lane);
+    if (lane == kWave - 1) wave_tot[wave] = incl;
+    if (threadIdx.x == 0) row_range[0] = lower_row(t0);
+    if (threadIdx.x == 1) row_range[1] = lower_row(t0 + kDecTile);
+    __syncthreads();
+    uint32_t off = 0, total = 0;
+    for (int w = 0; w < kDecWaves; ++w) {
+      off += w < wave ? wave_tot[w] : 0u;
+      total += wave_tot[w];
+    }
+    uint32_t run = off + incl - s;
+#pragma unroll
+    for (int i = 0; i < kDecPer; ++i) {
+      pre[threadIdx.x * kDecPer + i] = run;
+      const uint32_t j = t0 + threadIdx.x * kDecPer + i;
+      if (j < nd) {
+        int64_t p = base + run + d[i] - 1;
+        uint32_t x = c[i];
+        for (uint32_t t = 0; t < d[i]; ++t, --p) {
+          ocol[p] = (int32_t)col[x];
+          oval[p] = val[x];
+          x = par[x];
+        }
+      }
+      run += d[i];
     }
     __syncthreads();
-    uint32_t total;
-    block_exclusive_scan(rlen, nr, wave_tot, total);
-    for (int r = threadIdx.x; r < nr; r += kBlock) rowptr[bt.row_base + t0 + r] = base + rlen[r];
-    for (int r = wave; r < nr; r += kWaves) {
-      int64_t pos = base + rlen[r];
-      const uint32_t s = span[t0 + r], e = span[t0 + r + 1];
-      for (uint32_t j0 = s; j0 < e; j0 += kWave) {
-        const uint32_t j = j0 + lane;
-        uint32_t c = 0, d = 0;
-        if (j < e) {
-          c = dc[j];
-          d = dep[c];
-        }
-        const uint32_t incl = wave_incl_scan(d, lane);
-        const uint32_t tot = __shfl(incl, kWave - 1, kWave);
-        if (j < e) {
-          int64_t p = pos + (incl - d) + d - 1;
-          uint32_t x = c;
-          for (uint32_t t = 0; t < d; ++t, --p) {
-            ocol[p] = (int32_t)col[x];
-            oval[p] = val[x];
-            x = par[x];
-          }
-        }
-        pos += tot;
-      }
-    }
+    for (uint32_t r = row_range[0] + threadIdx.x; r < row_range[1]; r += kDecBlock)
+      if ((int)r <= nrows && span[r] < nd) rowptr[bt.row_base + r] = base + pre[span[r] - t0];
     base += total;
     __syncthreads();
   }
-  if (threadIdx.x == 0) rowptr[bt.row_base + bt.n_rows] = base;
+  // rows whose span starts at the end of D (trailing empty rows and the end mark)
+  for (uint32_t r = lower_row(nd) + threadIdx.x; r <= (uint32_t)nrows; r += kDecBlock)
+    rowptr[bt.row_base + r] = base;
 }
 
 // ===========================================================================
@@ -448,12 +713,53 @@ bool k1_fits(const toc_dev *d, int op) {
   return h + 16 <= kLdsMax;
 }
 
-int64_t rows_per_batch_need(const toc_dev *d, int op) {
-  return op == TOC_OP_RIGHT ? d->max_deep : d->max_tree;
-}
+// Execution plan of an op: which kernel family, its LDS bytes, and the workspace
+// it needs (rows of row_floats floats per code that needs an H row in memory).
+enum { kPathK1 = 0, kPathTiled = 1, kPathWide = 2 };
 
-int64_t rows_total_need(const toc_dev *d, int op) {
-  return op == TOC_OP_RIGHT ? d->total_deep : d->total_tree;
+struct OpPlan {
+  int path = kPathWide;
+  int n_tiles = 1;
+  bool deep_lds = false;
+  size_t lds = 0;
+  int64_t row_floats = 0;     // workspace floats per H row (0: no workspace)
+  int64_t rows_max = 0, rows_total = 0;
+};
+
+OpPlan plan_op(const toc_dev *d, int op, int k) {
+  OpPlan p;
+  const int64_t m = d->info.n_cols;
+  const bool right = op == TOC_OP_RIGHT;
+  p.rows_max = right ? d->max_deep : d->max_tree;
+  p.rows_total = right ? d->total_deep : d->total_tree;
+  if (k == 1 && k1_fits(d, op)) {
+    p.path = kPathK1;
+    return p;
+  }
+  if (right) {
+    const size_t wt = (size_t)m * kRtKT * 4;
+    if (k >= 4 && wt <= kLdsMax) {
+      p.path = kPathTiled;
+      p.n_tiles = (k + kRtKT - 1) / kRtKT;
+      p.deep_lds = wt + (size_t)d->max_deep * kRtKT * 4 <= kLdsMax;
+      p.lds = std::max<size_t>(16, p.deep_lds ? wt + (size_t)d->max_deep * kRtKT * 4 : wt);
+      p.row_floats = p.deep_lds ? 0 : (int64_t)p.n_tiles * kRtKT;
+      return p;
+    }
+  } else {
+    const size_t lds = ((size_t)d->max_rows * kLpKT + 2 * ((size_t)m + 1) +
+                        (size_t)d->max_tree + 1) * 4;
+    if (k >= 2 && lds <= kLdsMax) {
+      p.path = kPathTiled;
+      p.n_tiles = (k + kLpKT - 1) / kLpKT;
+      p.lds = lds;
+      p.row_floats = (int64_t)p.n_tiles * kLpKT;
+      return p;
+    }
+  }
+  p.path = kPathWide;
+  p.row_floats = std::min<int64_t>(k, kKTile);
+  return p;
 }
 
 // Splits batches into passes whose workspace rows fit `cap_rows`; calls fn(b0, nb, base).
@@ -461,7 +767,7 @@ template <typename F>
 toc_status for_each_pass(const toc_dev *d, int op, int64_t cap_rows, F fn) {
   const int64_t nb = (int64_t)d->batches.size();
   int64_t b0 = 0;
-  const int64_t max_grid = 1 << 30;
+  const int64_t max_grid = 1 << 26;
   while (b0 < nb) {
     const toc_batch &first = d->batches[b0];
     const int64_t base = op == TOC_OP_RIGHT ? first.deep_base : first.tree_base;
@@ -478,6 +784,17 @@ toc_status for_each_pass(const toc_dev *d, int op, int64_t cap_rows, F fn) {
     if (st != TOC_OK) return st;
     b0 = b1;
   }
+  return TOC_OK;
+}
+
+// Rows of the workspace available to a plan, or an error when below the minimum.
+toc_status ws_capacity(const OpPlan &p, void *ws, size_t ws_bytes, int64_t &cap_rows) {
+  cap_rows = INT64_MAX / 2;
+  if (p.row_floats == 0 || p.rows_max == 0) return TOC_OK;
+  cap_rows = (int64_t)(ws_bytes / 4) / p.row_floats;
+  if (!ws || cap_rows < p.rows_max)
+    return fail(TOC_ESIZE, "workspace of %zu bytes below the per-batch minimum of %lld", ws_bytes,
+                (long long)(p.rows_max * p.row_floats * 4));
   return TOC_OK;
 }
 
@@ -586,10 +903,12 @@ toc_status toc_workspace_size(const toc_dev *d, int32_t op, int32_t k, size_t *b
   if (op != TOC_OP_RIGHT && op != TOC_OP_LEFT && op != TOC_OP_DECODE)
     return fail(TOC_EINVAL, "unknown op %d", op);
   size_t need = 0, minimum = 0;
-  if (op != TOC_OP_DECODE && !(k == 1 && k1_fits(d, op))) {
-    const int64_t kt = std::min<int64_t>(k, kKTile);
-    minimum = (size_t)(rows_per_batch_need(d, op) * kt * 4);
-    need = std::max(minimum, (size_t)(rows_total_need(d, op) * kt * 4));
+  if (op != TOC_OP_DECODE) {
+    const OpPlan p = plan_op(d, op, k);
+    if (p.row_floats > 0 && p.rows_max > 0) {
+      minimum = (size_t)(p.rows_max * p.row_floats * 4);
+      need = std::max(minimum, (size_t)(p.rows_total * p.row_floats * 4));
+    }
   }
   *bytes = need;
   if (min_bytes) *min_bytes = minimum;
@@ -627,13 +946,30 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
     }
     return TOC_OK;
   }
+  const OpPlan plan = plan_op(d, TOC_OP_RIGHT, k);
+  int64_t cap_rows = 0;
+  if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
+  if (plan.path == kPathTiled) {
+    const int m = d->info.n_cols;
+    if ((st = plan.deep_lds ? allow_lds(right_tiled_kernel<true>, plan.lds)
+                            : allow_lds(right_tiled_kernel<false>, plan.lds)))
+      return st;
+    return for_each_pass(d, TOC_OP_RIGHT, cap_rows,
+                         [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
+      const unsigned grid = (unsigned)(((n + kXcd - 1) / kXcd) * kXcd * plan.n_tiles);
+      if (plan.deep_lds)
+        hipLaunchKernelGGL(right_tiled_kernel<true>, dim3(grid), dim3(kTileBlock), plan.lds, s,
+                           im, b0, n, plan.n_tiles, m, W, ldw, k, R, ldr, (float *)ws, base);
+      else
+        hipLaunchKernelGGL(right_tiled_kernel<false>, dim3(grid), dim3(kTileBlock), plan.lds, s,
+                           im, b0, n, plan.n_tiles, m, W, ldw, k, R, ldr, (float *)ws, base);
+      return launch_status("right_tiled_kernel");
+    });
+  }
   for (int64_t k0 = 0; k0 < k; k0 += kKTile) {
     const int kt = (int)std::min<int64_t>(kKTile, k - k0);
     const int kpl = (kt + kWave - 1) / kWave;
-    const int64_t cap_rows = (int64_t)(ws_bytes / 4) / kt;
-    if (d->max_deep > 0 && (!ws || cap_rows < d->max_deep))
-      return fail(TOC_ESIZE, "workspace too small (%zu bytes)", ws_bytes);
-    st = for_each_pass(d, TOC_OP_RIGHT, d->max_deep > 0 ? cap_rows : INT64_MAX / 2,
+    st = for_each_pass(d, TOC_OP_RIGHT, cap_rows,
                        [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
       TOC_DISPATCH_KPL(kpl, right_wide_kernel, dim3((unsigned)n), dim3(kBlock), 0, s, im, b0,
                        base, W + k0, ldw, kt, R + k0, ldr, (float *)ws);
@@ -689,13 +1025,28 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     }
     return TOC_OK;
   }
+  const OpPlan plan = plan_op(d, TOC_OP_LEFT, k);
+  int64_t cap_rows = 0;
+  if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
+  if (plan.path == kPathTiled) {
+    if ((st = allow_lds(left_pull_kernel<0>, plan.lds))) return st;
+    const uint8_t *bb = (const uint8_t *)d->buf;
+    const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
+    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
+    const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
+    return for_each_pass(d, TOC_OP_LEFT, cap_rows,
+                         [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
+      const unsigned grid = (unsigned)(((n + kXcd - 1) / kXcd) * kXcd * plan.n_tiles);
+      hipLaunchKernelGGL(left_pull_kernel<0>, dim3(grid), dim3(kTileBlock), plan.lds, s, im,
+                         occ_off, occ_row, tlist, b0, n, plan.n_tiles, m, G, ldg, k, out, ldo,
+                         accumulate, (float *)ws, base);
+      return launch_status("left_pull_kernel");
+    });
+  }
   for (int64_t k0 = 0; k0 < k; k0 += kKTile) {
     const int kt = (int)std::min<int64_t>(kKTile, k - k0);
     const int kpl = (kt + kWave - 1) / kWave;
-    const int64_t cap_rows = (int64_t)(ws_bytes / 4) / kt;
-    if (d->max_tree > 0 && (!ws || cap_rows < d->max_tree))
-      return fail(TOC_ESIZE, "workspace too small (%zu bytes)", ws_bytes);
-    st = for_each_pass(d, TOC_OP_LEFT, d->max_tree > 0 ? cap_rows : INT64_MAX / 2,
+    st = for_each_pass(d, TOC_OP_LEFT, cap_rows,
                        [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
       TOC_DISPATCH_KPL(kpl, left_wide_kernel, dim3((unsigned)n), dim3(kBlock), 0, s, im, b0,
                        base, m, G + k0, ldg, kt, out + k0, ldo, accumulate, (float *)ws);
@@ -724,7 +1075,7 @@ toc_status toc_decode_csr(const toc_dev *d, int64_t *rowptr, int32_t *col, float
   const Img im = image_of(d);
   for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
     const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-    hipLaunchKernelGGL(decode_kernel, dim3(g), dim3(kBlock), 0, s, im, b0, rowptr, col,
+    hipLaunchKernelGGL(decode_kernel, dim3(g), dim3(kDecBlock), 0, s, im, b0, rowptr, col,
                        (uint32_t *)val);
     if ((st = launch_status("decode_kernel"))) return st;
   }

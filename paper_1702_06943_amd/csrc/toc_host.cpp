@@ -170,6 +170,7 @@ toc_status encode_one(int32_t n_rows, int32_t n_cols, const int64_t *rowptr,
   e->n_nodes = next;
   // --- counts of the tree: live codes are those referenced by D and their
   // ancestors; parents always have smaller indices than their children.
+  // flags: 1 live, 2 has a live child, 4 has a child
   S.live.assign(next, 0);
   for (uint32_t c : e->D_codes) S.live[c] = 1;
   int64_t n_live = 0, n_deep_live = 0, n_deep_all = 0;
@@ -177,12 +178,20 @@ toc_status encode_one(int32_t n_rows, int32_t n_cols, const int64_t *rowptr,
   for (int64_t c = (int64_t)next - 1; c >= 1; --c) {
     md_all = std::max(md_all, S.depth[c]);
     if (S.depth[c] >= 2) ++n_deep_all;
-    if (!S.live[c]) continue;
+    S.live[S.parent[c]] |= 4;
+    if (!(S.live[c] & 1)) continue;
     ++n_live;
     if (S.depth[c] >= 2) ++n_deep_live;
     md_live = std::max(md_live, S.depth[c]);
-    S.live[S.parent[c]] = 1;
+    S.live[S.parent[c]] |= 1 | 2;
   }
+  int64_t ni_live = 0, ni_all = 0;
+  for (int64_t c = 1; c < (int64_t)next && S.depth[c] == 1; ++c) {
+    ni_live += (S.live[c] & 2) != 0;
+    ni_all += (S.live[c] & 4) != 0;
+  }
+  e->n_int1_live = ni_live;
+  e->n_int1_all = ni_all;
   e->n_live = n_live;
   e->n_deep_live = n_deep_live;
   e->n_deep_all = n_deep_all;
@@ -373,14 +382,15 @@ Counts counts_of(const toc_enc *e, uint32_t flags) {
 }
 
 struct ImgScratch {
-  std::vector<uint32_t> parent, first, depth, newidx;
+  std::vector<uint32_t> parent, first, depth, newidx, bucket, fill;
   std::vector<uint8_t> live, has_child;
-  std::vector<int64_t> cnt;
+  std::vector<int64_t> cnt, bucket_off;
+  std::vector<uint64_t> keys;
 };
 
 // Algorithm 2 on (I, D), then live marking and the depth-ordered renumbering;
 // writes the batch's arrays at its offsets.  Returns the per-batch counts through bt.
-toc_status write_batch(const toc_enc *e, uint32_t flags, const toc_layout &L,
+toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_layout &L,
                        uint8_t *dst, toc_batch &bt, ImgScratch &S) {
   const bool keep = flags & TOC_UPLOAD_KEEP_DEAD;
   const int64_t nI = (int64_t)e->I_col.size();
@@ -431,7 +441,10 @@ toc_status write_batch(const toc_enc *e, uint32_t flags, const toc_layout &L,
   const Counts want = counts_of(e, flags);
   if (n_codes != want.codes || levels != want.levels)
     return fail(TOC_EINVAL, "corrupt encoding (tree counts disagree)");
-  // level order: depth 1 codes with children, depth 1 leaves, then depth 2, 3, ...
+  // Order of the stored codes (every order with parents before children is valid
+  // for the scans of section 4; this one serves the kernels):
+  //   depth 1: codes with children (node order), then leaves sorted by column,
+  //   depth d >= 2: sorted by parent, so the children of a node are contiguous.
   S.cnt.assign((size_t)levels + 2, 0);
   int64_t n_int1 = 0;
   for (int64_t c = 1; c < N; ++c) {
@@ -439,21 +452,38 @@ toc_status write_batch(const toc_enc *e, uint32_t flags, const toc_layout &L,
     S.cnt[S.depth[c]]++;
     if (S.depth[c] == 1 && S.has_child[c]) ++n_int1;
   }
+  if (n_int1 != bt.n_int1) return fail(TOC_EINVAL, "corrupt encoding (tree counts disagree)");
   uint32_t *level = (uint32_t *)(dst + L.level) + bt.lvl_base;
   level[0] = 0;
   for (int32_t d = 1; d <= levels; ++d) level[d] = level[d - 1] + (uint32_t)S.cnt[d];
   S.newidx.assign((size_t)N, 0xFFFFFFFFu);
   {
-    int64_t pos_int = 0, pos_leaf = n_int1;
-    std::vector<int64_t> pos((size_t)levels + 2, 0);
-    for (int32_t d = 2; d <= levels; ++d) pos[d] = level[d - 1];
-    for (int64_t c = 1; c < N; ++c) {
-      if (!S.live[c]) continue;
-      const uint32_t d = S.depth[c];
-      int64_t at;
-      if (d == 1) at = S.has_child[c] ? pos_int++ : pos_leaf++;
-      else at = pos[d]++;
-      S.newidx[c] = (uint32_t)at;
+    // bucket live codes by depth, node order inside each bucket
+    S.bucket_off.assign((size_t)levels + 3, 0);
+    for (int32_t d = 1; d <= levels; ++d) S.bucket_off[d + 1] = S.bucket_off[d] + S.cnt[d];
+    S.bucket.assign((size_t)n_codes, 0);
+    std::vector<int64_t> fill(S.bucket_off.begin(), S.bucket_off.end());
+    for (int64_t c = 1; c < N; ++c)
+      if (S.live[c]) S.bucket[fill[S.depth[c]]++] = (uint32_t)c;
+    int64_t pos_int = 0;
+    S.keys.clear();
+    for (int64_t i = S.bucket_off[1]; i < S.bucket_off[2]; ++i) {
+      const uint32_t c = S.bucket[i];
+      if (S.has_child[c]) S.newidx[c] = (uint32_t)pos_int++;
+      else S.keys.push_back(((uint64_t)(uint32_t)e->I_col[c - 1] << 32) | c);
+    }
+    std::sort(S.keys.begin(), S.keys.end());
+    int64_t at = n_int1;
+    for (uint64_t kc : S.keys) S.newidx[(uint32_t)kc] = (uint32_t)at++;
+    for (int32_t d = 2; d <= levels; ++d) {
+      S.keys.clear();
+      for (int64_t i = S.bucket_off[d]; i < S.bucket_off[d + 1]; ++i) {
+        const uint32_t c = S.bucket[i];
+        S.keys.push_back(((uint64_t)S.newidx[S.parent[c]] << 32) | c);
+      }
+      std::sort(S.keys.begin(), S.keys.end());
+      at = level[d - 1];
+      for (uint64_t kc : S.keys) S.newidx[(uint32_t)kc] = (uint32_t)at++;
     }
   }
   uint32_t *parent = (uint32_t *)(dst + L.parent) + bt.code_base;
@@ -488,9 +518,29 @@ toc_status write_batch(const toc_enc *e, uint32_t flags, const toc_layout &L,
   uint32_t *dcodes = (uint32_t *)(dst + L.dcodes) + bt.d_base;
   for (int32_t r = 0; r <= e->n_rows; ++r) span[r] = (uint32_t)e->D_rowptr[r];
   for (size_t j = 0; j < e->D_codes.size(); ++j) dcodes[j] = S.newidx[e->D_codes[j]];
+  // occurrences of each code (D inverted): rows of the entries of D equal to the
+  // code, ascending, grouped by code.  This is the index set of the sum that
+  // defines G(x) in Theorem 2.
+  uint32_t *occ_off = (uint32_t *)(dst + L.occ_off) + bt.code_base + b;
+  uint32_t *occ_row = (uint32_t *)(dst + L.occ_row) + bt.d_base;
+  std::fill(occ_off, occ_off + n_codes + 1, 0u);
+  for (size_t j = 0; j < e->D_codes.size(); ++j) occ_off[dcodes[j] + 1]++;
+  for (int64_t c = 0; c < n_codes; ++c) occ_off[c + 1] += occ_off[c];
+  S.fill.assign(occ_off, occ_off + n_codes);
+  for (int32_t r = 0; r < e->n_rows; ++r)
+    for (int64_t j = e->D_rowptr[r]; j < e->D_rowptr[r + 1]; ++j)
+      occ_row[S.fill[dcodes[j]]++] = (uint32_t)r;
+  // codes with an H row in the left multiplication (children or depth >= 2),
+  // listed by column
+  const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;
+  uint32_t *tlist = (uint32_t *)(dst + L.tlist) + bt.tree_base;
+  S.keys.clear();
+  for (int64_t c = 0; c < n_codes; ++c)
+    if (c < n_int1 || c >= n1) S.keys.push_back(((uint64_t)colv[c] << 32) | (uint64_t)c);
+  std::sort(S.keys.begin(), S.keys.end());
+  for (size_t t = 0; t < S.keys.size(); ++t) tlist[t] = (uint32_t)S.keys[t];
   bt.n_codes = (int32_t)n_codes;
-  bt.n_lvl1 = levels >= 1 ? (int32_t)S.cnt[1] : 0;
-  bt.n_int1 = (int32_t)n_int1;
+  bt.n_lvl1 = (int32_t)n1;
   bt.n_levels = levels;
   return TOC_OK;
 }
@@ -502,11 +552,12 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   if (n_batches < 0) return fail(TOC_EINVAL, "n_batches < 0");
   if (n_batches > 0 && !encs) return fail(TOC_EINVAL, "encs is NULL");
   if (flags & ~(TOC_UPLOAD_KEEP_DEAD | TOC_UPLOAD_HOST)) return fail(TOC_EINVAL, "unknown flag");
-  int64_t codes = 0, levels = 0, rows = 0, d = 0, spans = 0, nnz = 0, canon = 0, deep = 0;
+  int64_t codes = 0, levels = 0, rows = 0, d = 0, spans = 0, nnz = 0, canon = 0, deep = 0,
+          tree = 0;
   int32_t n_cols = -1, max_depth = 0;
   dev->batches.assign((size_t)n_batches, toc_batch{});
   dev->max_rows = dev->max_codes = dev->max_levels = 0;
-  dev->max_d = 0;
+  dev->max_d = dev->max_deep = dev->max_tree = 0;
   for (int64_t b = 0; b < n_batches; ++b) {
     const toc_enc *e = encs[b];
     if (!e) return fail(TOC_EINVAL, "encs[%lld] is NULL", (long long)b);
@@ -525,13 +576,22 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
     bt.n_codes = (int32_t)c.codes;
     bt.n_levels = (int32_t)c.levels;
     bt.n_d = (int32_t)c.d;
+    const bool keep = flags & TOC_UPLOAD_KEEP_DEAD;
+    const int64_t nd = keep ? e->n_deep_all : e->n_deep_live;
+    const int64_t ni = keep ? e->n_int1_all : e->n_int1_live;
+    bt.n_int1 = (int32_t)ni;
+    bt.deep_base = deep;
+    bt.tree_base = tree;
+    dev->max_deep = std::max(dev->max_deep, nd);
+    dev->max_tree = std::max(dev->max_tree, nd + ni);
+    tree += nd + ni;
     codes += c.codes;
     levels += c.levels + 1;
     rows += c.rows;
     spans += c.rows + 1;
     d += c.d;
     nnz += e->nnz;
-    deep += (flags & TOC_UPLOAD_KEEP_DEAD) ? e->n_deep_all : e->n_deep_live;
+    deep += nd;
     canon += 4 * c.d + 4 * (c.rows + 1) + 10 * e->n_live + 4 * ((int64_t)e->max_depth_live + 1);
     max_depth = std::max<int32_t>(max_depth, (int32_t)c.levels);
     dev->max_rows = std::max<int32_t>(dev->max_rows, e->n_rows);
@@ -549,7 +609,12 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.depth = off;   off = align256(off + 4 * codes);
   L.span = off;    off = align256(off + 4 * spans);
   L.dcodes = off;  off = align256(off + 4 * d);
+  L.occ_off = off; off = align256(off + 4 * (codes + n_batches));
+  L.occ_row = off; off = align256(off + 4 * d);
+  L.tlist = off;   off = align256(off + 4 * tree);
   L.end = std::max<int64_t>(off, 256);
+  dev->total_deep = deep;
+  dev->total_tree = tree;
   toc_dev_info &I = dev->info;
   I = toc_dev_info{};
   I.n_batches = n_batches;
@@ -583,7 +648,7 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
       if (b >= n_batches || first_err.load() != 0) return;
       toc_status st;
       try {
-        st = write_batch(encs[b], flags, L, dst, dev->batches[b], S);
+        st = write_batch(encs[b], b, flags, L, dst, dev->batches[b], S);
       } catch (const std::bad_alloc &) {
         st = fail(TOC_ENOMEM, "out of host memory");
       }
@@ -602,21 +667,6 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
   work();
   for (auto &t : th) t.join();
   if (first_err.load() != 0) return fail((toc_status)first_err.load(), "%s", err_msg.c_str());
-  // workspace row bases: deep codes (right) and codes with an H row (left)
-  int64_t deep = 0, tree = 0;
-  dev->max_deep = dev->max_tree = 0;
-  for (auto &bt : dev->batches) {
-    const int64_t nd = bt.n_codes - bt.n_lvl1;
-    const int64_t nt2 = nd + bt.n_int1;
-    bt.deep_base = deep;
-    bt.tree_base = tree;
-    deep += nd;
-    tree += nt2;
-    dev->max_deep = std::max(dev->max_deep, nd);
-    dev->max_tree = std::max(dev->max_tree, nt2);
-  }
-  dev->total_deep = deep;
-  dev->total_tree = tree;
   std::memcpy(dst + L.batches, dev->batches.data(), sizeof(toc_batch) * dev->batches.size());
   return TOC_OK;
 }

@@ -21,6 +21,7 @@ struct toc_enc {
   int64_t n_live = 0, n_deep_live = 0;
   int32_t max_depth_live = 0, max_depth_all = 0;
   int64_t n_deep_all = 0;
+  int64_t n_int1_live = 0, n_int1_all = 0;  // depth-1 codes with (live / any) children
 };
 
 struct toc_dev {

@@ -33,6 +33,10 @@ def read_image(dev, buf):
         depth=arr("depth", np.uint32, n_codes),
         span=arr("span", np.uint32, int((bt["n_rows"] + 1).sum()) if nb else 0),
         dcodes=arr("dcodes", np.uint32, info["n_codes"]),
+        occ_off=arr("occ_off", np.uint32, n_codes + nb),
+        occ_row=arr("occ_row", np.uint32, info["n_codes"]),
+        tlist=arr("tlist", np.uint32,
+                  int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0),
     )
     return img
 
@@ -47,6 +51,10 @@ def batch_view(img, b):
         val=img["val"][cb:cb + nc], depth=img["depth"][cb:cb + nc],
         span=img["span"][int(t["span_base"]):int(t["span_base"]) + int(t["n_rows"]) + 1],
         dc=img["dcodes"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
+        occ_off=img["occ_off"][cb + b:cb + b + nc + 1],
+        occ_row=img["occ_row"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
+        tlist=img["tlist"][int(t["tree_base"]):int(t["tree_base"]) + int(t["n_int1"]) + nc
+                           - int(t["n_lvl1"])],
     )
 
 
@@ -77,6 +85,23 @@ def check_invariants(v):
         keys.add(k)
     assert np.all(v["dc"] < nc)
     assert v["span"][0] == 0 and v["span"][-1] == len(v["dc"])
+    # depth-1 leaves sorted by column; deeper levels sorted by parent
+    assert np.all(np.diff(v["col"][ni:n1].astype(np.int64)) >= 0)
+    for d in range(2, nl + 1):
+        assert np.all(np.diff(v["parent"][lv[d - 1]:lv[d]].astype(np.int64)) >= 0)
+    # inverted D: the rows listed for each code are exactly the rows using it
+    oo, orow = v["occ_off"], v["occ_row"]
+    assert oo[0] == 0 and oo[-1] == len(v["dc"]) and np.all(np.diff(oo.astype(np.int64)) >= 0)
+    row_of = np.repeat(np.arange(len(v["span"]) - 1), np.diff(v["span"].astype(np.int64)))
+    for c in range(nc):
+        got = orow[oo[c]:oo[c + 1]]
+        assert np.all(np.diff(got.astype(np.int64)) >= 0)
+        assert np.array_equal(got, row_of[v["dc"] == c])
+    # tree list: codes with children or depth >= 2, sorted by column
+    tree = [c for c in range(nc) if c < ni or c >= n1]
+    tl = v["tlist"]
+    assert sorted(tl.tolist()) == tree
+    assert np.all(np.diff(v["col"][tl].astype(np.int64)) >= 0)
 
 
 def walk_decode(v):
