@@ -186,6 +186,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--workers", type=int, default=0)
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device three times "
+                         "(reference dispatches for HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -239,6 +242,15 @@ def main():
     step_ms = float(np.mean([ev[s][0].elapsed_time(ev[s][3]) for s in range(args.steps)]))
     log(f"step {step_ms:.3f} ms ({', '.join(f'{o} {op_ms[o]:.3f}' for o in names)}); "
         f"wall {t_wall / args.steps * 1e3:.3f} ms/step")
+    if args.copy_calib_mib > 0:
+        n = args.copy_calib_mib * (1 << 20) // 4
+        src = torch.ones(n, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 3 copies of {n * 4} bytes")
+        del src, dst
 
     info = w.info
     nnz = info["nnz"]

@@ -158,7 +158,8 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   dcodes  : uint32 local code of each entry of D (d_base)
  *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b)
  *   occ_row : uint32 row of each entry of D, grouped by code (d_base): D inverted,
- *             the index set of the sum that defines G(x) in Theorem 2
+ *             the index set of the sum that defines G(x) in Theorem 2; bit 31 is
+ *             set on the first entry of each code
  *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
  *             by key column (tree_base)
  * Depth-1 codes without children are sorted by key column; the codes of each

@@ -45,6 +45,11 @@ Img image_of(const toc_dev *d) {
              (const uint32_t *)(b + L.span),     (const uint32_t *)(b + L.dcodes)};
 }
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
+__device__ inline int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
+
 template <int W>
 __device__ inline float group_sum(float x) {
 #pragma unroll
@@ -173,7 +178,7 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
   const uint32_t *par = im.parent + bt.code_base;
   const uint32_t *col = im.col + bt.code_base;
   const float *val = im.val + bt.code_base;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
   float *Hd = ws + (bt.deep_base - ws_base) * kt;
   for (int d = 2; d <= bt.n_levels; ++d) {
@@ -246,7 +251,7 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
   const float *val = im.val + bt.code_base;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
   const int64_t n_tree = (int64_t)ni + (bt.n_codes - bt.n_lvl1);
   float *Ht = ws + (bt.tree_base - ws_base) * kt;
@@ -312,59 +317,78 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
 }
 
 // ===========================================================================
-// Tiled kernels for wide k.  One workgroup per (batch, column tile); the tiles of
-// a batch are consecutive blocks of one XCD (the dispatcher deals blocks to the
-// 8 XCDs round-robin), so they share the batch's image through that XCD's L2.
+// ===========================================================================
+// Tiled kernels for wide k.  Persistent workgroups, one per CU: worker (x, s) on
+// XCD x (blocks are dealt to the 8 XCDs round-robin) keeps column tile
+// s % n_tiles resident in LDS and walks the batches of stream s / n_tiles, so the
+// n_tiles workers of a batch run together on one XCD and share its image in L2.
 // ===========================================================================
 constexpr int kXcd = 8;
-constexpr int kTileBlock = 512;
-constexpr int kTileWaves = kTileBlock / kWave;
+constexpr int kCuPerXcd = 32;
 
-__device__ inline void xcd_tile_map(int64_t blk, int n_tiles, int64_t &b, int &tile) {
-  const int64_t x = blk % kXcd, j = blk / kXcd;
-  tile = (int)(j % n_tiles);
-  b = (j / n_tiles) * kXcd + x;
+struct TileWorker {
+  int tile;
+  bool active;
+  int64_t first, stride;
+};
+
+__device__ inline TileWorker tile_worker(int n_tiles, int spx) {
+  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
+  TileWorker w;
+  w.tile = s % n_tiles;
+  const int stream = s / n_tiles;
+  w.active = stream < spx;
+  w.first = (int64_t)stream * kXcd + x;
+  w.stride = (int64_t)spx * kXcd;
+  return w;
 }
 
 __device__ inline float4 f4fma(float s, float4 x, float4 a) {
   return make_float4(fmaf(s, x.x, a.x), fmaf(s, x.y, a.y), fmaf(s, x.z, a.z), fmaf(s, x.w, a.w));
 }
 
-// Right multiplication with a KT-column tile of W resident in LDS.  Lanes form 8
-// groups of 8; a lane holds 4 consecutive columns, so a group covers the tile
-// for one code and a wave takes 8 codes of a tuple per step.  H rows of depth >= 2
-// codes are built level by level first (in LDS when they fit, else in `ws`).
+__device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
+}
+
+// ---------------------------------------------------------------------------
+// Right multiplication (Theorem 1, Algorithm 7).  A 32-column tile of W sits in
+// LDS.  Lanes form 8 groups of 8; a lane holds 4 consecutive columns, so a group
+// covers the tile for one entry of D and a wave takes 8 entries of a tuple per
+// step.  For each piece of up to 128 entries of a tuple the wave fetches the
+// codes' (LDS row, multiplier) one piece ahead and stages them in LDS, where each
+// group reads its entry by broadcast.  H rows of depth >= 2 codes are built level
+// by level first, in LDS when they fit.
+// ---------------------------------------------------------------------------
 constexpr int kRtKT = 32;
-constexpr uint32_t kRtGlobal = 0x80000000u;   // staged address refers to ws
+constexpr int kRtBlock = 1024;
+constexpr int kRtWaves = kRtBlock / kWave;
+constexpr int kRtPiece = 128;
+constexpr uint32_t kRtGlobal = 0x80000000u;   // staged row lives in the workspace
+
+struct RtPiece {
+  int r;            // tuple (row of the batch); >= n_rows: none
+  uint32_t j, e;    // entries [j, min(j + kRtPiece, e)) of D; e = end of the tuple
+};
 
 template <bool DEEP_LDS>
-__global__ __launch_bounds__(kTileBlock) void right_tiled_kernel(
-    Img im, int64_t b0, int64_t nb, int n_tiles, int m, const float *__restrict__ W,
+__global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
+    Img im, int64_t nb, int n_tiles, int spx, int m, const float *__restrict__ W,
     int64_t ldw, int k, float *__restrict__ R, int64_t ldr, float *__restrict__ ws,
-    int64_t ws_base) {
+    int64_t slot_floats) {
   extern __shared__ float4 smem4[];
   float *lds = (float *)smem4;
-  int64_t bl;
-  int tile;
-  xcd_tile_map(blockIdx.x, n_tiles, bl, tile);
-  if (bl >= nb) return;
-  const int64_t b = b0 + bl;
-  const toc_batch bt = im.batches[b];
-  const int k0 = tile * kRtKT;
+  const TileWorker tw = tile_worker(n_tiles, spx);
+  if (!tw.active) return;
+  const int k0 = tw.tile * kRtKT;
   const int kt = min(kRtKT, k - k0);
-  const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
-  const uint32_t n1 = (uint32_t)bt.n_lvl1;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave, wave = wave_id();
   const int grp = lane / 8, q = 4 * (lane % 8);
-  float *Wt = lds;                                   // m rows of kRtKT floats
-  float *Hl = lds + (size_t)m * kRtKT;               // deep rows (DEEP_LDS)
-  const int64_t kpad = (int64_t)n_tiles * kRtKT;
-  float *Hg = ws + (bt.deep_base - ws_base) * kpad + k0;
-  // stage W[:, k0:k0+kt]
-  for (int e = threadIdx.x; e < m * (kRtKT / 4); e += kTileBlock) {
+  float *Wt = lds;                                               // m x kRtKT
+  uint2 *stage = (uint2 *)(lds + (size_t)m * kRtKT) + wave * kRtPiece;
+  const uint32_t hl_base = (uint32_t)m * kRtKT + kRtWaves * kRtPiece * 2;   // floats
+  float *Hg = ws + blockIdx.x * slot_floats;
+  for (int e = threadIdx.x; e < m * (kRtKT / 4); e += kRtBlock) {
     const int c = e / (kRtKT / 4), q4 = 4 * (e % (kRtKT / 4));
     const float *src = W + (int64_t)c * ldw + k0 + q4;
     float4 v;
@@ -374,212 +398,360 @@ __global__ __launch_bounds__(kTileBlock) void right_tiled_kernel(
     v.w = q4 + 3 < kt ? src[3] : 0.0f;
     *(float4 *)&Wt[c * kRtKT + q4] = v;
   }
-  __syncthreads();
-  // H of depth >= 2 codes, level by level
-  for (int d = 2; d <= bt.n_levels; ++d) {
-    const uint32_t a = lvl[d - 1], e = lvl[d];
-    for (uint32_t c = a + wave * 8 + grp; c < e; c += kTileWaves * 8) {
-      const uint32_t p = par[c];
-      float4 base;
-      if (p < n1) {
-        base = *(const float4 *)&Wt[col[p] * kRtKT + q];
-        const float vp = val[p];
-        base = make_float4(vp * base.x, vp * base.y, vp * base.z, vp * base.w);
-      } else if (DEEP_LDS) {
-        base = *(const float4 *)&Hl[(p - n1) * kRtKT + q];
-      } else {
-        base = *(const float4 *)&Hg[(int64_t)(p - n1) * kpad + q];
-      }
-      const float4 h = f4fma(val[c], *(const float4 *)&Wt[col[c] * kRtKT + q], base);
-      if (DEEP_LDS) *(float4 *)&Hl[(c - n1) * kRtKT + q] = h;
-      else *(float4 *)&Hg[(int64_t)(c - n1) * kpad + q] = h;
-    }
-    __syncthreads();
-  }
-  // per-tuple sums
-  const uint32_t *span = im.span + bt.span_base;
-  const uint32_t *dc = im.dcodes + bt.d_base;
-  for (int r = wave; r < bt.n_rows; r += kTileWaves) {
-    const uint32_t s = span[r], e = span[r + 1];
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (uint32_t j0 = s; j0 < e; j0 += kWave) {
-      const uint32_t n = min((uint32_t)kWave, e - j0);
-      // lane i fetches code j0+i: LDS row offset and multiplier
-      uint32_t my_addr = 0;
-      float my_mult = 0.0f;
-      if ((uint32_t)lane < n) {
-        const uint32_t c = dc[j0 + lane];
-        if (c < n1) {
-          my_addr = col[c] * kRtKT;
-          my_mult = val[c];
+  for (int64_t b = tw.first; b < nb; b += tw.stride) {
+    const toc_batch bt = im.batches[b];
+    const uint32_t *lvl = im.level + bt.lvl_base;
+    const uint32_t *par = im.parent + bt.code_base;
+    const uint32_t *col = im.col + bt.code_base;
+    const float *val = im.val + bt.code_base;
+    const uint32_t *span = im.span + bt.span_base;
+    const uint32_t *dc = im.dcodes + bt.d_base;
+    const uint32_t n1 = (uint32_t)bt.n_lvl1;
+    const int nrows = bt.n_rows;
+    __syncthreads();   // W tile ready / previous batch's deep rows no longer read
+    // H of depth >= 2 codes, level by level
+    for (int d = 2; d <= bt.n_levels; ++d) {
+      const uint32_t a = lvl[d - 1], e = lvl[d];
+      for (uint32_t c = a + wave * 8 + grp; c < e; c += kRtWaves * 8) {
+        const uint32_t p = par[c];
+        float4 base;
+        if (p < n1) {
+          base = *(const float4 *)&Wt[col[p] * kRtKT + q];
+          const float vp = val[p];
+          base = make_float4(vp * base.x, vp * base.y, vp * base.z, vp * base.w);
+        } else if (DEEP_LDS) {
+          base = *(const float4 *)&lds[hl_base + (p - n1) * kRtKT + q];
         } else {
-          my_addr = DEEP_LDS ? (uint32_t)m * kRtKT + (c - n1) * kRtKT : (kRtGlobal | (c - n1));
-          my_mult = 1.0f;
+          base = *(const float4 *)&Hg[(int64_t)(p - n1) * kRtKT + q];
         }
+        const float4 h = f4fma(val[c], *(const float4 *)&Wt[col[c] * kRtKT + q], base);
+        if (DEEP_LDS) *(float4 *)&lds[hl_base + (c - n1) * kRtKT + q] = h;
+        else *(float4 *)&Hg[(int64_t)(c - n1) * kRtKT + q] = h;
       }
-      // every lane takes part in the shuffles; lanes past n carry multiplier 0
-      for (uint32_t t0 = 0; t0 < n; t0 += 8) {
-        const int t = (int)t0 + grp;
-        const uint32_t addr = (uint32_t)__shfl((int)my_addr, t, kWave);
-        const float mult = __shfl(my_mult, t, kWave);
-        float4 x;
-        if (!DEEP_LDS && (addr & kRtGlobal))
-          x = *(const float4 *)&Hg[(int64_t)(addr & ~kRtGlobal) * kpad + q];
-        else
-          x = *(const float4 *)&lds[addr + q];
-        acc = f4fma(mult, x, acc);
-      }
+      __syncthreads();
     }
+    // per-tuple sums, software-pipelined over pieces of tuples
+    auto piece_after = [&](RtPiece p) -> RtPiece {
+      if (p.j + kRtPiece < p.e) return RtPiece{p.r, p.j + kRtPiece, p.e};
+      const int r = p.r + kRtWaves;
+      if (r >= nrows) return RtPiece{nrows, 0, 0};
+      return RtPiece{r, span[r], span[r + 1]};
+    };
+    auto fetch = [&](RtPiece p, uint32_t half, uint32_t code) -> uint2 {
+      const uint32_t j = p.j + half * kWave + lane;
+      if (p.r >= nrows || j >= p.e || j >= p.j + kRtPiece) return make_uint2(0u, 0u);
+      if (code < n1) return make_uint2(col[code] * kRtKT, __float_as_uint(val[code]));
+      return make_uint2(DEEP_LDS ? hl_base + (code - n1) * kRtKT : (kRtGlobal | (code - n1)),
+                        __float_as_uint(1.0f));
+    };
+    auto load_codes = [&](RtPiece p, uint32_t &d0, uint32_t &d1) {
+      const uint32_t j0 = p.j + lane, j1 = p.j + kWave + lane;
+      const uint32_t lim = min(p.e, p.j + kRtPiece);
+      d0 = p.r < nrows && j0 < lim ? dc[j0] : 0u;
+      d1 = p.r < nrows && j1 < lim ? dc[j1] : 0u;
+    };
+    // pipeline: codes of pieces p3, p4 loading; their (row, multiplier) for p1, p2
+    // gathering; p0 staged and computed
+    auto next_piece = [&](RtPiece p) -> RtPiece { return p.r < nrows ? piece_after(p) : p; };
+    RtPiece p0{wave, 0, 0};
+    if (wave < nrows) p0 = RtPiece{wave, span[wave], span[wave + 1]};
+    else p0.r = nrows;
+    RtPiece p1 = next_piece(p0), p2 = next_piece(p1), p3 = next_piece(p2), p4 = next_piece(p3);
+    uint32_t x0, x1, dA0, dA1, dB0, dB1;
+    load_codes(p0, x0, x1);
+    uint2 c0 = fetch(p0, 0, x0), c1 = fetch(p0, 1, x1);
+    load_codes(p1, x0, x1);
+    uint2 cA0 = fetch(p1, 0, x0), cA1 = fetch(p1, 1, x1);
+    load_codes(p2, x0, x1);
+    uint2 cB0 = fetch(p2, 0, x0), cB1 = fetch(p2, 1, x1);
+    load_codes(p3, dA0, dA1);
+    load_codes(p4, dB0, dB1);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    while (p0.r < nrows) {
+      stage[lane] = c0;
+      stage[kWave + lane] = c1;
+      c0 = cA0;
+      c1 = cA1;
+      cA0 = cB0;
+      cA1 = cB1;
+      cB0 = fetch(p3, 0, dA0);
+      cB1 = fetch(p3, 1, dA1);
+      dA0 = dB0;
+      dA1 = dB1;
+      const RtPiece p5 = next_piece(p4);
+      load_codes(p5, dB0, dB1);
+      const uint32_t n = min(p0.e - p0.j, (uint32_t)kRtPiece);
+      const uint32_t steps = ((n + 31) / 32) * 4;
+      for (uint32_t t = 0; t < steps; t += 4) {
+        const uint2 e0 = stage[(t + 0) * 8 + grp], e1 = stage[(t + 1) * 8 + grp];
+        const uint2 e2 = stage[(t + 2) * 8 + grp], e3 = stage[(t + 3) * 8 + grp];
+        float4 x0, x1, x2, x3;
+        if (!DEEP_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
+          x0 = e0.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e0.x & ~kRtGlobal) * kRtKT + q]
+                                : *(const float4 *)&lds[e0.x + q];
+          x1 = e1.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e1.x & ~kRtGlobal) * kRtKT + q]
+                                : *(const float4 *)&lds[e1.x + q];
+          x2 = e2.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e2.x & ~kRtGlobal) * kRtKT + q]
+                                : *(const float4 *)&lds[e2.x + q];
+          x3 = e3.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e3.x & ~kRtGlobal) * kRtKT + q]
+                                : *(const float4 *)&lds[e3.x + q];
+        } else {
+          x0 = *(const float4 *)&lds[e0.x + q];
+          x1 = *(const float4 *)&lds[e1.x + q];
+          x2 = *(const float4 *)&lds[e2.x + q];
+          x3 = *(const float4 *)&lds[e3.x + q];
+        }
+        acc = f4fma(__uint_as_float(e0.y), x0, acc);
+        acc = f4fma(__uint_as_float(e1.y), x1, acc);
+        acc = f4fma(__uint_as_float(e2.y), x2, acc);
+        acc = f4fma(__uint_as_float(e3.y), x3, acc);
+      }
+      if (p0.j + kRtPiece >= p0.e) {   // last piece of the tuple
 #pragma unroll
-    for (int o = 8; o < kWave; o <<= 1) {
-      acc.x += __shfl_xor(acc.x, o, kWave);
-      acc.y += __shfl_xor(acc.y, o, kWave);
-      acc.z += __shfl_xor(acc.z, o, kWave);
-      acc.w += __shfl_xor(acc.w, o, kWave);
-    }
-    if (grp == 0) {
-      float *rr = R + (bt.row_base + r) * ldr + k0 + q;
-      if (q + 0 < kt) rr[0] = acc.x;
-      if (q + 1 < kt) rr[1] = acc.y;
-      if (q + 2 < kt) rr[2] = acc.z;
-      if (q + 3 < kt) rr[3] = acc.w;
+        for (int o = 8; o < kWave; o <<= 1) {
+          acc.x += __shfl_xor(acc.x, o, kWave);
+          acc.y += __shfl_xor(acc.y, o, kWave);
+          acc.z += __shfl_xor(acc.z, o, kWave);
+          acc.w += __shfl_xor(acc.w, o, kWave);
+        }
+        if (grp == 0) {
+          float *rr = R + (bt.row_base + p0.r) * ldr + k0 + q;
+          if (q + 0 < kt) rr[0] = acc.x;
+          if (q + 1 < kt) rr[1] = acc.y;
+          if (q + 2 < kt) rr[2] = acc.z;
+          if (q + 3 < kt) rr[3] = acc.w;
+        }
+        acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      p0 = p1;
+      p1 = p2;
+      p2 = p3;
+      p3 = p4;
+      p4 = p5;
     }
   }
 }
 
-// Left multiplication by pulling (Theorem 2 read as a definition): for each code,
-// G(x) = sum of G rows over the entries of D equal to x (the inverted index
-// occ_off/occ_row), plus the G values of its children; out[col] = sum over the
-// codes with that key column of val * G(x).  No atomics: each output row and each
-// H row has one writer.  A KT-column tile of G lives in LDS; lane = column.
-constexpr int kLpKT = 64;
-constexpr int kLpColsPerGrab = 4;
-
-__device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
-  return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
-}
+// ---------------------------------------------------------------------------
+// Left multiplication by pulling (Theorem 2 read as a definition): G(x) is the sum
+// of the G rows over the entries of D equal to x, which the inverted index
+// occ_off/occ_row lists per code.  A tile of up to 128 columns of the batch's G
+// sits in LDS (2 columns per lane).
+//  * Codes with children or of depth >= 2 ("tree codes", few): deepest level
+//    first, one wave per code, H = own occurrences + children's H (children of a
+//    code are contiguous because levels are sorted by parent); H rows go to this
+//    worker's workspace slot.
+//  * Depth-1 leaves (sorted by column): their occurrences form one flat stream in
+//    column order; each wave owns a contiguous range of columns (balanced by
+//    occurrence count), walks its part of the stream 64 entries at a time and
+//    writes each output row once: val(code) * G[row] summed per column, plus the
+//    tree codes of that column.  The code of an entry comes from the
+//    first-occurrence bit of occ_row through a ballot and a popcount.
+// ---------------------------------------------------------------------------
+constexpr int kLpBlock = 1024;
+constexpr int kLpWaves = kLpBlock / kWave;
+constexpr int kLpMaxTW = 128;
+constexpr uint32_t kFirstOcc = 0x80000000u;
 
 template <int DUMMY>
-__global__ __launch_bounds__(kTileBlock) void left_pull_kernel(
+__global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, int64_t b0, int64_t nb, int n_tiles, int m,
-    const float *__restrict__ G, int64_t ldg, int k, float *__restrict__ out, int64_t ldo,
-    int accumulate, float *__restrict__ ws, int64_t ws_base) {
+    const uint32_t *__restrict__ tlist_all, int64_t nb, int n_tiles, int spx, int tw,
+    int max_rows, int m, const float *__restrict__ G, int64_t ldg, int k,
+    float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
+    int64_t slot_floats) {
   extern __shared__ float4 smem4[];
-  __shared__ uint32_t ctr;
-  int64_t bl;
-  int tile;
-  xcd_tile_map(blockIdx.x, n_tiles, bl, tile);
-  if (bl >= nb) return;
-  const int64_t b = b0 + bl;
-  const toc_batch bt = im.batches[b];
-  const int k0 = tile * kLpKT;
-  const int kt = min(kLpKT, k - k0);
-  const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
-  const uint32_t *oo = occ_off_all + bt.code_base + b;
-  const uint32_t *orow = occ_row_all + bt.d_base;
-  const uint32_t *tl = tlist_all + bt.tree_base;
-  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
-  const uint32_t n_tree = ni + (nc - n1);
-  const int nrows = bt.n_rows;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  float *Gt = (float *)smem4;                          // nrows x kLpKT
-  uint32_t *Loff = (uint32_t *)(Gt + (size_t)nrows * kLpKT);  // m + 1
-  uint32_t *Toff = Loff + m + 1;                       // m + 1
-  uint32_t *Coff = Toff + m + 1;                       // n_tree + 1
-  const int64_t kpad = (int64_t)n_tiles * kLpKT;
-  float *Ht = ws + (bt.tree_base - ws_base) * kpad + k0;
-  auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
-  for (int e = threadIdx.x; e < nrows * kLpKT; e += kTileBlock) {
-    const int r = e / kLpKT, qq = e % kLpKT;
-    Gt[e] = qq < kt ? G[(bt.row_base + r) * ldg + k0 + qq] : 0.0f;
-  }
-  // column boundaries of the depth-1 leaves [ni, n1) (sorted by column)
-  for (uint32_t i = ni + threadIdx.x; i < n1; i += kTileBlock) {
-    const int64_t cc = col[i], cp = i > ni ? (int64_t)col[i - 1] : -1;
-    for (int64_t j = cp + 1; j <= cc; ++j) Loff[j] = i;
-  }
-  {
-    const int64_t last = n1 > ni ? (int64_t)col[n1 - 1] : -1;
-    for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kTileBlock) Loff[j] = n1;
-  }
-  // column boundaries of the tree-code list
-  for (uint32_t t = threadIdx.x; t < n_tree; t += kTileBlock) {
-    const int64_t cc = col[tl[t]], cp = t > 0 ? (int64_t)col[tl[t - 1]] : -1;
-    for (int64_t j = cp + 1; j <= cc; ++j) Toff[j] = t;
-  }
-  {
-    const int64_t last = n_tree > 0 ? (int64_t)col[tl[n_tree - 1]] : -1;
-    for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kTileBlock) Toff[j] = n_tree;
-  }
-  // children ranges: codes of depth >= 2 are sorted by (level, parent), so the
-  // children of the tree code with H row h are [Coff[h], Coff[h+1])
-  for (uint32_t c = n1 + threadIdx.x; c < nc; c += kTileBlock) {
-    const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
-    for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
-  }
-  {
-    const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
-    for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kTileBlock) Coff[h] = nc;
-  }
-  if (threadIdx.x == 0) ctr = 0;
-  __syncthreads();
-  // tree codes, deepest level first; one wave per code
-  for (int d = bt.n_levels; d >= 1; --d) {
-    const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
-    for (uint32_t c = a + wave; c < e; c += kTileWaves) {
-      const uint32_t h = hrow(c);
-      float s = 0.0f;
-      for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) s += Gt[orow[o] * kLpKT + lane];
-      for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) s += Ht[(int64_t)hrow(ch) * kpad + lane];
-      Ht[(int64_t)h * kpad + lane] = s;
+  __shared__ uint32_t jsplit[kLpWaves + 1];
+  const TileWorker twk = tile_worker(n_tiles, spx);
+  if (!twk.active) return;
+  const int k0 = twk.tile * tw;
+  const int kt = min(tw, k - k0);
+  const int lane = threadIdx.x % kWave, wave = wave_id();
+  const int qq = 2 * lane;
+  const bool lane_on = qq < tw;
+  float *Gt = (float *)smem4;                                   // max_rows x tw
+  uint32_t *Loff = (uint32_t *)(Gt + (size_t)max_rows * tw);    // m + 1: first leaf code
+  uint32_t *Ost = Loff + m + 1;                                 // m + 1: first occurrence
+  uint32_t *Toff = Ost + m + 1;                                 // m + 1: tree-list start
+  uint32_t *Coff = Toff + m + 1;                                // children ranges
+  float *Ht = ws + blockIdx.x * slot_floats;
+  const float2 zero2 = make_float2(0.f, 0.f);
+  for (int64_t b = twk.first; b < nb; b += twk.stride) {
+    const toc_batch bt = im.batches[b];
+    const uint32_t *lvl = im.level + bt.lvl_base;
+    const uint32_t *par = im.parent + bt.code_base;
+    const uint32_t *col = im.col + bt.code_base;
+    const float *val = im.val + bt.code_base;
+    const uint32_t *oo = occ_off_all + bt.code_base + b;
+    const uint32_t *orow = occ_row_all + bt.d_base;
+    const uint32_t *tl = tlist_all + bt.tree_base;
+    const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+    const uint32_t n_tree = ni + (nc - n1);
+    const int nrows = bt.n_rows;
+    auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
+    __syncthreads();   // previous batch done with the LDS tables
+    for (int e = threadIdx.x; e < nrows * (tw / 2); e += kLpBlock) {
+      const int r = e / (tw / 2), c2 = 2 * (e % (tw / 2));
+      const float *src = G + (bt.row_base + r) * ldg + k0 + c2;
+      *(float2 *)&Gt[r * tw + c2] =
+          make_float2(c2 < kt ? src[0] : 0.0f, c2 + 1 < kt ? src[1] : 0.0f);
+    }
+    const uint32_t obase = n1 > ni ? oo[ni] : 0u;
+    for (uint32_t i = ni + threadIdx.x; i < n1; i += kLpBlock) {
+      const int64_t cc = col[i], cp = i > ni ? (int64_t)col[i - 1] : -1;
+      if (cp < cc) {
+        const uint32_t os = oo[i] - obase;
+        for (int64_t j = cp + 1; j <= cc; ++j) {
+          Loff[j] = i;
+          Ost[j] = os;
+        }
+      }
+    }
+    {
+      const int64_t last = n1 > ni ? (int64_t)col[n1 - 1] : -1;
+      const uint32_t oend = n1 > ni ? oo[n1] - obase : 0u;
+      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLpBlock) {
+        Loff[j] = n1;
+        Ost[j] = oend;
+      }
+    }
+    for (uint32_t t = threadIdx.x; t < n_tree; t += kLpBlock) {
+      const int64_t cc = col[tl[t]], cp = t > 0 ? (int64_t)col[tl[t - 1]] : -1;
+      for (int64_t j = cp + 1; j <= cc; ++j) Toff[j] = t;
+    }
+    {
+      const int64_t last = n_tree > 0 ? (int64_t)col[tl[n_tree - 1]] : -1;
+      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLpBlock) Toff[j] = n_tree;
+    }
+    for (uint32_t c = n1 + threadIdx.x; c < nc; c += kLpBlock) {
+      const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
+      for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
+    }
+    {
+      const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
+      for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kLpBlock) Coff[h] = nc;
     }
     __syncthreads();
-  }
-  // columns, a few at a time per wave; code and occurrence info is fetched 64
-  // entries at a time into registers and broadcast with readlane
-  for (;;) {
-    uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(&ctr, (uint32_t)kLpColsPerGrab);
-    base = rdlane(base, 0);
-    if (base >= (uint32_t)m) break;
-    const uint32_t jend = min(base + kLpColsPerGrab, (uint32_t)m);
-    bool have_c = false, have_o = false;
-    uint32_t cwin = 0, owin = 0, v_oo = 0, v_val = 0, v_row = 0;
-    for (uint32_t j = base; j < jend; ++j) {
-      float acc = 0.0f;
-      const uint32_t c_lo = Loff[j], c_hi = Loff[j + 1];
-      for (uint32_t c = c_lo; c < c_hi; ++c) {
-        if (!have_c || c - cwin >= 63u) {  // codes cwin..cwin+62 with both bounds
-          have_c = true;
-          cwin = c;
-          v_oo = c + lane <= nc ? oo[c + lane] : 0u;
-          v_val = c + lane < nc ? __float_as_uint(val[c + lane]) : 0u;
+    // column ranges of the waves, balanced by leaf occurrences
+    if (threadIdx.x <= kLpWaves) {
+      const uint32_t w = threadIdx.x, total = Ost[m];
+      uint32_t j;
+      if (w == 0) j = 0;
+      else if (w == kLpWaves) j = m;
+      else {
+        const uint32_t target = (uint32_t)(((uint64_t)total * w) / kLpWaves);
+        uint32_t lo = 0, hi = (uint32_t)m;
+        while (lo < hi) {
+          const uint32_t mid = (lo + hi) / 2;
+          if (Ost[mid] < target) lo = mid + 1;
+          else hi = mid;
         }
-        const uint32_t o_lo = rdlane(v_oo, c - cwin), o_hi = rdlane(v_oo, c - cwin + 1);
-        const float vc = __uint_as_float(rdlane(v_val, c - cwin));
-        float s = 0.0f;
-        for (uint32_t o = o_lo; o < o_hi; ++o) {
-          if (!have_o || o - owin >= 64u) {
-            have_o = true;
-            owin = o;
-            v_row = o + lane < (uint32_t)bt.n_d ? orow[o + lane] : 0u;
-          }
-          s += Gt[rdlane(v_row, o - owin) * kLpKT + lane];
-        }
-        acc = fmaf(vc, s, acc);
+        j = lo;
       }
+      jsplit[w] = j;
+    }
+    __syncthreads();
+    // tree codes, deepest level first
+    for (int d = bt.n_levels; d >= 1; --d) {
+      const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+      for (uint32_t c = a + wave; c < e; c += kLpWaves) {
+        const uint32_t h = hrow(c);
+        float2 s = zero2;
+        for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) {
+          if (lane_on) {
+            const float2 g = *(const float2 *)&Gt[(orow[o] & ~kFirstOcc) * tw + qq];
+            s.x += g.x;
+            s.y += g.y;
+          }
+        }
+        for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) {
+          if (lane_on) {
+            const float2 g = *(const float2 *)&Ht[(int64_t)hrow(ch) * tw + qq];
+            s.x += g.x;
+            s.y += g.y;
+          }
+        }
+        if (lane_on) *(float2 *)&Ht[(int64_t)h * tw + qq] = s;
+      }
+      __syncthreads();
+    }
+    // leaf stream, one column range per wave
+    const uint32_t J0 = jsplit[wave], J1 = jsplit[wave + 1];
+    float *ob = out + (b * m) * ldo + k0 + qq;
+    auto flush = [&](uint32_t j, float2 acc) {
       for (uint32_t t = Toff[j]; t < Toff[j + 1]; ++t) {
         const uint32_t c = tl[t];
-        acc = fmaf(val[c], Ht[(int64_t)hrow(c) * kpad + lane], acc);
+        const float v = val[c];
+        if (lane_on) {
+          const float2 h = *(const float2 *)&Ht[(int64_t)hrow(c) * tw + qq];
+          acc.x = fmaf(v, h.x, acc.x);
+          acc.y = fmaf(v, h.y, acc.y);
+        }
       }
-      if (lane < kt) {
-        float *p = out + (b * m + j) * ldo + k0 + lane;
-        *p = accumulate ? *p + acc : acc;
+      float *p = ob + (int64_t)j * ldo;
+      if (qq < kt) p[0] = accumulate ? p[0] + acc.x : acc.x;
+      if (qq + 1 < kt) p[1] = accumulate ? p[1] + acc.y : acc.y;
+    };
+    uint32_t cur = J0;
+    float2 acc = zero2;
+    if (J0 < J1) {
+      const uint32_t fend = Ost[J1];
+      uint32_t prev_code = Loff[J0] - 1;    // code of the entry before the stream
+      // chunk i is computed while chunk i+1's codes are gathered and chunk i+2's
+      // rows load
+      auto load_rows = [&](uint32_t f) -> uint32_t {
+        return f + lane < fend ? orow[obase + f + lane] : 0u;
+      };
+      uint32_t n_roff = 0, n_v = 0, n_cc = 0xFFFFFFFFu, n_n = 0;
+      auto decode_chunk = [&](uint32_t f, uint32_t w) {
+        const bool ok = f + lane < fend;
+        const uint64_t firsts = __ballot(ok && (w & kFirstOcc));
+        const uint32_t code = prev_code + (uint32_t)__popcll(firsts & (~0ull >> (63 - lane)));
+        prev_code += (uint32_t)__popcll(firsts);
+        n_roff = (w & ~kFirstOcc) * (uint32_t)tw * 4u;
+        n_v = ok ? __float_as_uint(val[code]) : 0u;
+        n_cc = ok ? col[code] : 0xFFFFFFFFu;
+        n_n = f < fend ? min((uint32_t)kWave, fend - f) : 0u;
+      };
+      uint32_t f0 = Ost[J0];
+      decode_chunk(f0, load_rows(f0));
+      uint32_t w_next = load_rows(f0 + kWave);
+      for (; f0 < fend; f0 += kWave) {
+        const uint32_t roff = n_roff, v = n_v, cc = n_cc, n = n_n;
+        if (f0 + kWave < fend) decode_chunk(f0 + kWave, w_next);
+        w_next = load_rows(f0 + 2 * kWave);
+        const uint32_t cprev = (uint32_t)__shfl_up((int)cc, 1, kWave);
+        const uint64_t bnd = __ballot((uint32_t)lane < n && (lane == 0 || cc != cprev));
+        for (uint32_t i0 = 0; i0 < n; i0 += 8) {
+          float2 x[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t ro = rdlane(roff, i0 + i);
+            x[i] = lane_on ? *(const float2 *)((const char *)Gt + ro + qq * 4) : zero2;
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            if (i0 + i < n) {
+              if ((bnd >> (i0 + i)) & 1) {
+                const uint32_t cj = rdlane(cc, i0 + i);
+                while (cur < cj) {
+                  flush(cur, acc);
+                  acc = zero2;
+                  ++cur;
+                }
+              }
+              const float vv = __uint_as_float(rdlane(v, i0 + i));
+              acc.x = fmaf(vv, x[i].x, acc.x);
+              acc.y = fmaf(vv, x[i].y, acc.y);
+            }
+          }
+        }
       }
+    }
+    while (cur < J1) {
+      flush(cur, acc);
+      acc = zero2;
+      ++cur;
     }
   }
 }
@@ -589,20 +761,21 @@ __global__ __launch_bounds__(kTileBlock) void left_pull_kernel(
 // and in the CSR alike, so the output position of entry j of D is the sum of the
 // depths of entries 0..j-1: one flat exclusive scan over D gives every position
 // and, at the row boundaries, rowptr.  Each entry then writes its sequence
-// backwards while walking to the root.
+// backwards while walking to the root.  Entries are dealt to threads with stride
+// kDecBlock so that loads and (depth-1) stores are coalesced; the scan runs on
+// the transposed copy in LDS.
 // ===========================================================================
 constexpr int kDecBlock = 1024;
 constexpr int kDecWaves = kDecBlock / kWave;
-constexpr int kDecPer = 4;                       // entries of D per thread per tile
+constexpr int kDecPer = 4;
 constexpr int kDecTile = kDecBlock * kDecPer;
 
 __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, int64_t b0,
                                                            int64_t *__restrict__ rowptr,
                                                            int32_t *__restrict__ ocol,
                                                            uint32_t *__restrict__ oval) {
-  __shared__ uint32_t pre[kDecTile];
+  __shared__ uint32_t sh[kDecTile];
   __shared__ uint32_t wave_tot[kDecWaves];
-  __shared__ uint32_t row_range[2];
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *par = im.parent + bt.code_base;
   const uint32_t *col = im.col + bt.code_base;
@@ -610,64 +783,68 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, int64_t b0,
   const uint32_t *dep = im.depth + bt.code_base;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t nd = (uint32_t)bt.n_d;
   const int nrows = bt.n_rows;
-  // first row whose span starts at or after x (spans are non-decreasing)
-  auto lower_row = [&](uint32_t x) -> uint32_t {
-    uint32_t lo = 0, hi = (uint32_t)nrows + 1;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) / 2;
-      if (span[mid] < x) lo = mid + 1;
-      else hi = mid;
-    }
-    return lo;
-  };
   int64_t base = bt.nnz_base;
   for (uint32_t t0 = 0; t0 < nd; t0 += kDecTile) {
-    uint32_t c[kDecPer], d[kDecPer], s = 0;
-#pragma unroll
-    for (int i = 0; i < kDecPer; ++i) {
-      const uint32_t j = t0 + threadIdx.x * kDecPer + i;
-      c[i] = j < nd ? dc[j] : 0u;
-      d[i] = j < nd ? dep[c[i]] : 0u;
-      s += d[i];
+    uint32_t c0, c1, c2, c3;
+    {
+      const uint32_t j = t0 + threadIdx.x;
+      c0 = j < nd ? dc[j] : 0u;
+      c1 = j + kDecBlock < nd ? dc[j + kDecBlock] : 0u;
+      c2 = j + 2 * kDecBlock < nd ? dc[j + 2 * kDecBlock] : 0u;
+      c3 = j + 3 * kDecBlock < nd ? dc[j + 3 * kDecBlock] : 0u;
+      sh[threadIdx.x] = j < nd ? dep[c0] : 0u;
+      sh[threadIdx.x + kDecBlock] = j + kDecBlock < nd ? dep[c1] : 0u;
+      sh[threadIdx.x + 2 * kDecBlock] = j + 2 * kDecBlock < nd ? dep[c2] : 0u;
+      sh[threadIdx.x + 3 * kDecBlock] = j + 3 * kDecBlock < nd ? dep[c3] : 0u;
     }
+    __syncthreads();
+    // exclusive scan of sh in entry order: thread t owns entries 4t..4t+3
+    const uint32_t v0 = sh[4 * threadIdx.x], v1 = sh[4 * threadIdx.x + 1];
+    const uint32_t v2 = sh[4 * threadIdx.x + 2], v3 = sh[4 * threadIdx.x + 3];
+    const uint32_t s = v0 + v1 + v2 + v3;
     const uint32_t incl = wave_incl_scan(s, lane);
     if (lane == kWave - 1) wave_tot[wave] = incl;
-    if (threadIdx.x == 0) row_range[0] = lower_row(t0);
-    if (threadIdx.x == 1) row_range[1] = lower_row(t0 + kDecTile);
     __syncthreads();
     uint32_t off = 0, total = 0;
     for (int w = 0; w < kDecWaves; ++w) {
       off += w < wave ? wave_tot[w] : 0u;
       total += wave_tot[w];
     }
-    uint32_t run = off + incl - s;
-#pragma unroll
-    for (int i = 0; i < kDecPer; ++i) {
-      pre[threadIdx.x * kDecPer + i] = run;
-      const uint32_t j = t0 + threadIdx.x * kDecPer + i;
-      if (j < nd) {
-        int64_t p = base + run + d[i] - 1;
-        uint32_t x = c[i];
-        for (uint32_t t = 0; t < d[i]; ++t, --p) {
-          ocol[p] = (int32_t)col[x];
-          oval[p] = val[x];
-          x = par[x];
-        }
-      }
-      run += d[i];
-    }
+    const uint32_t x0 = off + incl - s;
+    sh[4 * threadIdx.x] = x0;
+    sh[4 * threadIdx.x + 1] = x0 + v0;
+    sh[4 * threadIdx.x + 2] = x0 + v0 + v1;
+    sh[4 * threadIdx.x + 3] = x0 + v0 + v1 + v2;
     __syncthreads();
-    for (uint32_t r = row_range[0] + threadIdx.x; r < row_range[1]; r += kDecBlock)
-      if ((int)r <= nrows && span[r] < nd) rowptr[bt.row_base + r] = base + pre[span[r] - t0];
+    auto emit = [&](uint32_t i, uint32_t c) {
+      const uint32_t j = t0 + i * kDecBlock + threadIdx.x;
+      if (j >= nd) return;
+      const uint32_t d = dep[c];
+      int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
+      uint32_t x = c;
+      for (uint32_t t = 0; t < d; ++t, --p) {
+        ocol[p] = (int32_t)col[x];
+        oval[p] = val[x];
+        x = par[x];
+      }
+    };
+    emit(0, c0);
+    emit(1, c1);
+    emit(2, c2);
+    emit(3, c3);
+    for (int r = threadIdx.x; r <= nrows; r += kDecBlock) {
+      const uint32_t sr = span[r];
+      if (sr >= t0 && sr < t0 + kDecTile && sr < nd) rowptr[bt.row_base + r] = base + sh[sr - t0];
+    }
     base += total;
     __syncthreads();
   }
   // rows whose span starts at the end of D (trailing empty rows and the end mark)
-  for (uint32_t r = lower_row(nd) + threadIdx.x; r <= (uint32_t)nrows; r += kDecBlock)
-    rowptr[bt.row_base + r] = base;
+  for (int r = threadIdx.x; r <= nrows; r += kDecBlock)
+    if (span[r] >= nd) rowptr[bt.row_base + r] = base;
 }
 
 // ===========================================================================
@@ -719,11 +896,13 @@ enum { kPathK1 = 0, kPathTiled = 1, kPathWide = 2 };
 
 struct OpPlan {
   int path = kPathWide;
-  int n_tiles = 1;
+  int n_tiles = 1, tw = 0, spx = 1;
   bool deep_lds = false;
   size_t lds = 0;
+  unsigned grid = 0;
   int64_t row_floats = 0;     // workspace floats per H row (0: no workspace)
   int64_t rows_max = 0, rows_total = 0;
+  int64_t ws_floats = 0;      // tiled: whole workspace (one slot per worker)
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -737,23 +916,33 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
     return p;
   }
   if (right) {
-    const size_t wt = (size_t)m * kRtKT * 4;
-    if (k >= 4 && wt <= kLdsMax) {
+    const size_t fixed = ((size_t)m * kRtKT + (size_t)kRtWaves * kRtPiece * 2) * 4;
+    if (k >= 4 && fixed <= kLdsMax) {
       p.path = kPathTiled;
       p.n_tiles = (k + kRtKT - 1) / kRtKT;
-      p.deep_lds = wt + (size_t)d->max_deep * kRtKT * 4 <= kLdsMax;
-      p.lds = std::max<size_t>(16, p.deep_lds ? wt + (size_t)d->max_deep * kRtKT * 4 : wt);
-      p.row_floats = p.deep_lds ? 0 : (int64_t)p.n_tiles * kRtKT;
+      p.tw = kRtKT;
+      p.deep_lds = fixed + (size_t)d->max_deep * kRtKT * 4 <= kLdsMax;
+      p.lds = p.deep_lds ? fixed + (size_t)d->max_deep * kRtKT * 4 : fixed;
+      p.spx = std::max(1, kCuPerXcd / p.n_tiles);
+      p.grid = (unsigned)(kXcd * p.spx * p.n_tiles);
+      p.row_floats = p.deep_lds ? 0 : kRtKT;
+      p.ws_floats = p.deep_lds ? 0 : (int64_t)p.grid * d->max_deep * kRtKT;
       return p;
     }
   } else {
-    const size_t lds = ((size_t)d->max_rows * kLpKT + 2 * ((size_t)m + 1) +
-                        (size_t)d->max_tree + 1) * 4;
-    if (k >= 2 && lds <= kLdsMax) {
+    const int n_tiles = (k + kLpMaxTW - 1) / kLpMaxTW;
+    int tw = (k + n_tiles - 1) / n_tiles;
+    tw += tw & 1;
+    const size_t lds = ((size_t)d->max_rows * tw + 3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) * 4;
+    if (k >= 2 && lds <= kLdsMax - 256) {
       p.path = kPathTiled;
-      p.n_tiles = (k + kLpKT - 1) / kLpKT;
+      p.n_tiles = n_tiles;
+      p.tw = tw;
       p.lds = lds;
-      p.row_floats = (int64_t)p.n_tiles * kLpKT;
+      p.spx = std::max(1, kCuPerXcd / p.n_tiles);
+      p.grid = (unsigned)(kXcd * p.spx * p.n_tiles);
+      p.row_floats = tw;
+      p.ws_floats = (int64_t)p.grid * d->max_tree * tw;
       return p;
     }
   }
@@ -905,7 +1094,9 @@ toc_status toc_workspace_size(const toc_dev *d, int32_t op, int32_t k, size_t *b
   size_t need = 0, minimum = 0;
   if (op != TOC_OP_DECODE) {
     const OpPlan p = plan_op(d, op, k);
-    if (p.row_floats > 0 && p.rows_max > 0) {
+    if (p.path == kPathTiled) {
+      minimum = need = (size_t)p.ws_floats * 4;
+    } else if (p.row_floats > 0 && p.rows_max > 0) {
       minimum = (size_t)(p.rows_max * p.row_floats * 4);
       need = std::max(minimum, (size_t)(p.rows_total * p.row_floats * 4));
     }
@@ -947,25 +1138,26 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
     return TOC_OK;
   }
   const OpPlan plan = plan_op(d, TOC_OP_RIGHT, k);
+  if (plan.path == kPathTiled) {
+    if (plan.ws_floats > 0 && (!ws || ws_bytes < (size_t)plan.ws_floats * 4))
+      return fail(TOC_ESIZE, "workspace of %zu bytes below the %lld needed", ws_bytes,
+                  (long long)plan.ws_floats * 4);
+    const int m = d->info.n_cols;
+    if (plan.deep_lds) {
+      if ((st = allow_lds(right_tiled_kernel<true>, plan.lds))) return st;
+      hipLaunchKernelGGL(right_tiled_kernel<true>, dim3(plan.grid), dim3(kRtBlock), plan.lds, s,
+                         im, nb, plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr, (float *)ws,
+                         (int64_t)0);
+    } else {
+      if ((st = allow_lds(right_tiled_kernel<false>, plan.lds))) return st;
+      hipLaunchKernelGGL(right_tiled_kernel<false>, dim3(plan.grid), dim3(kRtBlock), plan.lds,
+                         s, im, nb, plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr, (float *)ws,
+                         (int64_t)d->max_deep * kRtKT);
+    }
+    return launch_status("right_tiled_kernel");
+  }
   int64_t cap_rows = 0;
   if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
-  if (plan.path == kPathTiled) {
-    const int m = d->info.n_cols;
-    if ((st = plan.deep_lds ? allow_lds(right_tiled_kernel<true>, plan.lds)
-                            : allow_lds(right_tiled_kernel<false>, plan.lds)))
-      return st;
-    return for_each_pass(d, TOC_OP_RIGHT, cap_rows,
-                         [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
-      const unsigned grid = (unsigned)(((n + kXcd - 1) / kXcd) * kXcd * plan.n_tiles);
-      if (plan.deep_lds)
-        hipLaunchKernelGGL(right_tiled_kernel<true>, dim3(grid), dim3(kTileBlock), plan.lds, s,
-                           im, b0, n, plan.n_tiles, m, W, ldw, k, R, ldr, (float *)ws, base);
-      else
-        hipLaunchKernelGGL(right_tiled_kernel<false>, dim3(grid), dim3(kTileBlock), plan.lds, s,
-                           im, b0, n, plan.n_tiles, m, W, ldw, k, R, ldr, (float *)ws, base);
-      return launch_status("right_tiled_kernel");
-    });
-  }
   for (int64_t k0 = 0; k0 < k; k0 += kKTile) {
     const int kt = (int)std::min<int64_t>(kKTile, k - k0);
     const int kpl = (kt + kWave - 1) / kWave;
@@ -1026,23 +1218,23 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     return TOC_OK;
   }
   const OpPlan plan = plan_op(d, TOC_OP_LEFT, k);
-  int64_t cap_rows = 0;
-  if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
   if (plan.path == kPathTiled) {
+    if (plan.ws_floats > 0 && (!ws || ws_bytes < (size_t)plan.ws_floats * 4))
+      return fail(TOC_ESIZE, "workspace of %zu bytes below the %lld needed", ws_bytes,
+                  (long long)plan.ws_floats * 4);
     if ((st = allow_lds(left_pull_kernel<0>, plan.lds))) return st;
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
     const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
-    return for_each_pass(d, TOC_OP_LEFT, cap_rows,
-                         [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
-      const unsigned grid = (unsigned)(((n + kXcd - 1) / kXcd) * kXcd * plan.n_tiles);
-      hipLaunchKernelGGL(left_pull_kernel<0>, dim3(grid), dim3(kTileBlock), plan.lds, s, im,
-                         occ_off, occ_row, tlist, b0, n, plan.n_tiles, m, G, ldg, k, out, ldo,
-                         accumulate, (float *)ws, base);
-      return launch_status("left_pull_kernel");
-    });
+    hipLaunchKernelGGL(left_pull_kernel<0>, dim3(plan.grid), dim3(kLpBlock), plan.lds, s, im,
+                       occ_off, occ_row, tlist, nb, plan.n_tiles, plan.spx, plan.tw,
+                       d->max_rows, m, G, ldg, k, out, ldo, accumulate, (float *)ws,
+                       (int64_t)d->max_tree * plan.tw);
+    return launch_status("left_pull_kernel");
   }
+  int64_t cap_rows = 0;
+  if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
   for (int64_t k0 = 0; k0 < k; k0 += kKTile) {
     const int kt = (int)std::min<int64_t>(kKTile, k - k0);
     const int kpl = (kt + kWave - 1) / kWave;

@@ -530,6 +530,10 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   for (int32_t r = 0; r < e->n_rows; ++r)
     for (int64_t j = e->D_rowptr[r]; j < e->D_rowptr[r + 1]; ++j)
       occ_row[S.fill[dcodes[j]]++] = (uint32_t)r;
+  // bit 31 marks the first occurrence of each code, so a scan over occ_row alone
+  // can tell which code an entry belongs to
+  for (int64_t c = 0; c < n_codes; ++c)
+    if (occ_off[c] < occ_off[c + 1]) occ_row[occ_off[c]] |= 0x80000000u;
   // codes with an H row in the left multiplication (children or depth >= 2),
   // listed by column
   const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;

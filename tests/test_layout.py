@@ -93,6 +93,9 @@ def check_invariants(v):
     oo, orow = v["occ_off"], v["occ_row"]
     assert oo[0] == 0 and oo[-1] == len(v["dc"]) and np.all(np.diff(oo.astype(np.int64)) >= 0)
     row_of = np.repeat(np.arange(len(v["span"]) - 1), np.diff(v["span"].astype(np.int64)))
+    first = (orow >> 31).astype(bool)
+    assert np.array_equal(np.flatnonzero(first), oo[:-1][np.diff(oo.astype(np.int64)) > 0])
+    orow = orow & 0x7FFFFFFF
     for c in range(nc):
         got = orow[oo[c]:oo[c + 1]]
         assert np.all(np.diff(got.astype(np.int64)) >= 0)
