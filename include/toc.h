@@ -162,6 +162,9 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *             set on the first entry of each code
  *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
  *             by key column (tree_base)
+ *   dtiles  : uint32 x 4 per run of 1024 entries of D (at least one per batch):
+ *             batch, first entry, pairs of the batch before that entry, first
+ *             row whose span starts at or after that entry
  * Depth-1 codes without children are sorted by key column; the codes of each
  * level d >= 2 are sorted by parent.                                             */
 typedef struct {
@@ -173,7 +176,7 @@ typedef struct {
 
 typedef struct {
   int64_t batches, level, parent, col, val, depth, span, dcodes, occ_off, occ_row, tlist,
-      end;
+      dtiles, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

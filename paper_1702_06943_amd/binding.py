@@ -49,7 +49,7 @@ class DevInfo(C.Structure):
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
                 ("batches", "level", "parent", "col", "val", "depth", "span", "dcodes",
-                 "occ_off", "occ_row", "tlist", "end")]
+                 "occ_off", "occ_row", "tlist", "dtiles", "end")]
 
 
 BATCH_DTYPE = np.dtype([

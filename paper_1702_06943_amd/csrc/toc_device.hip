@@ -23,7 +23,6 @@ constexpr int kWaves = kBlock / kWave;
 constexpr int kMaxKpl = 8;                    // wide kernels: up to 8 columns per lane
 constexpr int kKTile = kWave * kMaxKpl;       // 512 columns per pass
 constexpr size_t kLdsMax = 160 * 1024;        // gfx950 LDS per workgroup
-constexpr int kOutLdsMax = 8192;              // k = 1 left: out block kept in LDS up to m
 
 struct Img {
   const toc_batch *batches;
@@ -108,57 +107,104 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   }
 }
 
-// Left multiplication (Theorem 2, Algorithm 5): scatter G onto codes, propagate
-// child to parent deepest level first, accumulate val * H into out[col].
-template <int LPR, bool OUT_LDS>
-__global__ __launch_bounds__(kBlock) void left_k1_kernel(Img im, int64_t b0, int32_t m,
-                                                         int32_t h_words,
-                                                         const float *__restrict__ G,
-                                                         int64_t ldg, float *__restrict__ out,
-                                                         int64_t ldo, int accumulate) {
+// Left multiplication (Theorem 2, Algorithm 5) without atomics: H[c] = G(c) is
+// pulled from the inverted index (the sum over the entries of D equal to c), each
+// code then adds its children's H (children are contiguous: levels are sorted by
+// parent), deepest level first; finally every key column has one writer, the
+// thread at the head of its run of depth-1 leaves (sorted by column) or, for a
+// column with no leaf, the head of its run in the column-sorted tree list.
+constexpr uint32_t kFirstOccK1 = 0x80000000u;
+
+__global__ __launch_bounds__(kBlock) void left_k1_kernel(
+    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
+    const uint32_t *__restrict__ tlist_all, int64_t b0, int32_t m, int32_t max_rows,
+    int32_t max_codes, int32_t max_tree, const float *__restrict__ G, int64_t ldg,
+    float *__restrict__ out, int64_t ldo, int accumulate) {
   extern __shared__ float sm[];
-  float *H = sm;
-  float *O = sm + h_words;
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = im.batches[b];
   const uint32_t *lvl = im.level + bt.lvl_base;
   const uint32_t *par = im.parent + bt.code_base;
   const uint32_t *col = im.col + bt.code_base;
   const float *val = im.val + bt.code_base;
-  const uint32_t *span = im.span + bt.span_base;
-  const uint32_t *dc = im.dcodes + bt.d_base;
+  const uint32_t *oo = occ_off_all + bt.code_base + b;
+  const uint32_t *orow = occ_row_all + bt.d_base;
+  const uint32_t *tl = tlist_all + bt.tree_base;
+  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+  const uint32_t n_tree = ni + (nc - n1);
+  float *Gs = sm;                                     // max_rows
+  float *H = sm + max_rows;                           // max_codes
+  uint32_t *Coff = (uint32_t *)(H + max_codes);       // n_tree + 1 children ranges
+  uint32_t *tcol = Coff + max_tree + 1;               // n_tree (column of each list entry)
+  auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
   float *ob = out + b * (int64_t)m * ldo;
-  for (int c = threadIdx.x; c < bt.n_codes; c += kBlock) H[c] = 0.0f;
-  if (OUT_LDS) {
-    for (int j = threadIdx.x; j < m; j += kBlock) O[j] = 0.0f;
-  } else if (!accumulate) {
+  for (int r = threadIdx.x; r < bt.n_rows; r += kBlock) Gs[r] = G[(bt.row_base + r) * ldg];
+  if (!accumulate)
     for (int j = threadIdx.x; j < m; j += kBlock) ob[(int64_t)j * ldo] = 0.0f;
-    __threadfence();
+  for (uint32_t c = n1 + threadIdx.x; c < nc; c += kBlock) {
+    const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
+    for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
+  }
+  {
+    const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
+    for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kBlock) Coff[h] = nc;
+  }
+  for (uint32_t t = threadIdx.x; t < n_tree; t += kBlock) tcol[t] = col[tl[t]];
+  __threadfence_block();
+  __syncthreads();
+  // G(c) for every code
+  for (uint32_t c = threadIdx.x; c < nc; c += kBlock) {
+    float s = 0.0f;
+    for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) s += Gs[orow[o] & ~kFirstOccK1];
+    H[c] = s;
   }
   __syncthreads();
-  const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
-  for (int r = grp; r < bt.n_rows; r += kBlock / LPR) {
-    const float g = G[(bt.row_base + r) * ldg];
-    const uint32_t s = span[r], e = span[r + 1];
-    for (uint32_t j = s + lane; j < e; j += LPR) atomicAdd(&H[dc[j]], g);
-  }
-  __syncthreads();
-  for (int d = bt.n_levels; d >= 2; --d) {
-    const uint32_t a = lvl[d - 1], e = lvl[d];
-    for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) atomicAdd(&H[par[c]], H[c]);
-    __syncthreads();
-  }
-  for (int c = threadIdx.x; c < bt.n_codes; c += kBlock) {
-    const float x = val[c] * H[c];
-    if (OUT_LDS) atomicAdd(&O[col[c]], x);
-    else unsafeAtomicAdd(&ob[(int64_t)col[c] * ldo], x);
-  }
-  if (OUT_LDS) {
-    __syncthreads();
-    for (int j = threadIdx.x; j < m; j += kBlock) {
-      float *p = &ob[(int64_t)j * ldo];
-      *p = accumulate ? *p + O[j] : O[j];
+  // children into parents, deepest parent level first
+  for (int d = bt.n_levels - 1; d >= 1; --d) {
+    const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+    for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
+      const uint32_t h = hrow(c);
+      float s = H[c];
+      for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) s += H[ch];
+      H[c] = s;
     }
+    __syncthreads();
+  }
+  // first tree-list entry with column >= j
+  auto tree_lb = [&](uint32_t j) -> uint32_t {
+    uint32_t lo = 0, hi = n_tree;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (tcol[mid] < j) lo = mid + 1;
+      else hi = mid;
+    }
+    return lo;
+  };
+  // columns owned by the head of a run of depth-1 leaves
+  for (uint32_t i = ni + threadIdx.x; i < n1; i += kBlock) {
+    const uint32_t j = col[i];
+    if (i > ni && col[i - 1] == j) continue;
+    float s = 0.0f;
+    for (uint32_t x = i; x < n1 && col[x] == j; ++x) s = fmaf(val[x], H[x], s);
+    for (uint32_t t = tree_lb(j); t < n_tree && tcol[t] == j; ++t) s = fmaf(val[tl[t]], H[tl[t]], s);
+    float *p = ob + (int64_t)j * ldo;
+    *p = accumulate ? *p + s : s;
+  }
+  // columns that only tree codes have
+  for (uint32_t t = threadIdx.x; t < n_tree; t += kBlock) {
+    const uint32_t j = tcol[t];
+    if (t > 0 && tcol[t - 1] == j) continue;
+    uint32_t lo = ni, hi = n1;           // is there a leaf with column j?
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) / 2;
+      if (col[mid] < j) lo = mid + 1;
+      else hi = mid;
+    }
+    if (lo < n1 && col[lo] == j) continue;
+    float s = 0.0f;
+    for (uint32_t u = t; u < n_tree && tcol[u] == j; ++u) s = fmaf(val[tl[u]], H[tl[u]], s);
+    float *p = ob + (int64_t)j * ldo;
+    *p = accumulate ? *p + s : s;
   }
 }
 
@@ -758,25 +804,34 @@ __global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
 
 // ===========================================================================
 // Decode to CSR (the backtracking of Algorithm 6).  Rows are concatenated in D
-// and in the CSR alike, so the output position of entry j of D is the sum of the
-// depths of entries 0..j-1: one flat exclusive scan over D gives every position
-// and, at the row boundaries, rowptr.  Each entry then writes its sequence
-// backwards while walking to the root.  Entries are dealt to threads with stride
-// kDecBlock so that loads and (depth-1) stores are coalesced; the scan runs on
-// the transposed copy in LDS.
+// and in the CSR alike, so the output position of entry j of D is the number of
+// pairs of the entries before it.  The upload recorded, for every run of
+// kDecodeTile entries, that count at the run's start and the first row starting
+// in it, so each run is an independent workgroup: an exclusive scan of the
+// entries' depths inside the run gives every position (and rowptr at row
+// starts), then each entry writes its sequence backwards while walking to the
+// root.  Entries are dealt to threads with stride kDecBlock, so loads and
+// depth-1 stores are coalesced; the scan runs on a transposed copy in LDS.
 // ===========================================================================
-constexpr int kDecBlock = 1024;
+constexpr int kDecBlock = 256;
 constexpr int kDecWaves = kDecBlock / kWave;
-constexpr int kDecPer = 4;
-constexpr int kDecTile = kDecBlock * kDecPer;
+constexpr int kDecPer = (int)toc::kDecodeTile / kDecBlock;   // 4
 
-__global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, int64_t b0,
+__global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *__restrict__ dtiles,
+                                                           int64_t t0, int64_t n_runs,
                                                            int64_t *__restrict__ rowptr,
                                                            int32_t *__restrict__ ocol,
                                                            uint32_t *__restrict__ oval) {
-  __shared__ uint32_t sh[kDecTile];
+  __shared__ uint32_t sh[toc::kDecodeTile];
   __shared__ uint32_t wave_tot[kDecWaves];
-  const toc_batch bt = im.batches[b0 + blockIdx.x];
+  // blocks are dealt to the 8 XCDs round-robin; the grid is a multiple of 8 and
+  // each XCD gets a contiguous range of runs, so the runs of a batch share its L2
+  const int64_t per_xcd = (int64_t)gridDim.x / kXcd;
+  const int64_t slot = (int64_t)(blockIdx.x % kXcd) * per_xcd + blockIdx.x / kXcd;
+  if (slot >= n_runs) return;
+  const int64_t t = t0 + slot;
+  const uint4 dt = dtiles[t];                       // batch, first entry, pairs before, first row
+  const toc_batch bt = im.batches[dt.x];
   const uint32_t *par = im.parent + bt.code_base;
   const uint32_t *col = im.col + bt.code_base;
   const uint32_t *val = (const uint32_t *)im.val + bt.code_base;
@@ -784,67 +839,65 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, int64_t b0,
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = wave_id();
-  const uint32_t nd = (uint32_t)bt.n_d;
-  const int nrows = bt.n_rows;
-  int64_t base = bt.nnz_base;
-  for (uint32_t t0 = 0; t0 < nd; t0 += kDecTile) {
-    uint32_t c0, c1, c2, c3;
-    {
-      const uint32_t j = t0 + threadIdx.x;
-      c0 = j < nd ? dc[j] : 0u;
-      c1 = j + kDecBlock < nd ? dc[j + kDecBlock] : 0u;
-      c2 = j + 2 * kDecBlock < nd ? dc[j + 2 * kDecBlock] : 0u;
-      c3 = j + 3 * kDecBlock < nd ? dc[j + 3 * kDecBlock] : 0u;
-      sh[threadIdx.x] = j < nd ? dep[c0] : 0u;
-      sh[threadIdx.x + kDecBlock] = j + kDecBlock < nd ? dep[c1] : 0u;
-      sh[threadIdx.x + 2 * kDecBlock] = j + 2 * kDecBlock < nd ? dep[c2] : 0u;
-      sh[threadIdx.x + 3 * kDecBlock] = j + 3 * kDecBlock < nd ? dep[c3] : 0u;
-    }
-    __syncthreads();
-    // exclusive scan of sh in entry order: thread t owns entries 4t..4t+3
-    const uint32_t v0 = sh[4 * threadIdx.x], v1 = sh[4 * threadIdx.x + 1];
-    const uint32_t v2 = sh[4 * threadIdx.x + 2], v3 = sh[4 * threadIdx.x + 3];
-    const uint32_t s = v0 + v1 + v2 + v3;
-    const uint32_t incl = wave_incl_scan(s, lane);
-    if (lane == kWave - 1) wave_tot[wave] = incl;
-    __syncthreads();
-    uint32_t off = 0, total = 0;
-    for (int w = 0; w < kDecWaves; ++w) {
-      off += w < wave ? wave_tot[w] : 0u;
-      total += wave_tot[w];
-    }
-    const uint32_t x0 = off + incl - s;
-    sh[4 * threadIdx.x] = x0;
-    sh[4 * threadIdx.x + 1] = x0 + v0;
-    sh[4 * threadIdx.x + 2] = x0 + v0 + v1;
-    sh[4 * threadIdx.x + 3] = x0 + v0 + v1 + v2;
-    __syncthreads();
-    auto emit = [&](uint32_t i, uint32_t c) {
-      const uint32_t j = t0 + i * kDecBlock + threadIdx.x;
-      if (j >= nd) return;
-      const uint32_t d = dep[c];
+  const uint32_t nd = (uint32_t)bt.n_d, es = dt.y;
+  const int64_t base = bt.nnz_base + dt.z;
+  uint32_t c[kDecPer];
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    const uint32_t j = es + i * kDecBlock + threadIdx.x;
+    c[i] = j < nd ? dc[j] : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    const uint32_t j = es + i * kDecBlock + threadIdx.x;
+    sh[i * kDecBlock + threadIdx.x] = j < nd ? dep[c[i]] : 0u;
+  }
+  __syncthreads();
+  // exclusive scan in entry order: thread t owns entries kDecPer*t .. +kDecPer-1
+  uint32_t v[kDecPer], s = 0;
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    v[i] = sh[kDecPer * threadIdx.x + i];
+    s += v[i];
+  }
+  const uint32_t incl = wave_incl_scan(s, lane);
+  if (lane == kWave - 1) wave_tot[wave] = incl;
+  __syncthreads();
+  uint32_t off = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kDecWaves; ++w) {
+    off += w < wave ? wave_tot[w] : 0u;
+    total += wave_tot[w];
+  }
+  uint32_t run = off + incl - s;
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    sh[kDecPer * threadIdx.x + i] = run;
+    run += v[i];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    const uint32_t j = es + i * kDecBlock + threadIdx.x;
+    if (j < nd) {
+      uint32_t x = c[i];
+      const uint32_t d = dep[x];
       int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
-      uint32_t x = c;
-      for (uint32_t t = 0; t < d; ++t, --p) {
+      for (uint32_t q = 0; q < d; ++q, --p) {
         ocol[p] = (int32_t)col[x];
         oval[p] = val[x];
         x = par[x];
       }
-    };
-    emit(0, c0);
-    emit(1, c1);
-    emit(2, c2);
-    emit(3, c3);
-    for (int r = threadIdx.x; r <= nrows; r += kDecBlock) {
-      const uint32_t sr = span[r];
-      if (sr >= t0 && sr < t0 + kDecTile && sr < nd) rowptr[bt.row_base + r] = base + sh[sr - t0];
     }
-    base += total;
-    __syncthreads();
   }
-  // rows whose span starts at the end of D (trailing empty rows and the end mark)
-  for (int r = threadIdx.x; r <= nrows; r += kDecBlock)
-    if (span[r] >= nd) rowptr[bt.row_base + r] = base;
+  // rows starting in this run; the batch's last run also writes the rows that
+  // start at the end of D and the end mark
+  const bool last = (uint64_t)es + toc::kDecodeTile >= nd;
+  const uint32_t r_end = last ? (uint32_t)bt.n_rows + 1 : dtiles[t + 1].w;
+  for (uint32_t r = dt.w + threadIdx.x; r < r_end; r += kDecBlock) {
+    const uint32_t sr = span[r];
+    rowptr[bt.row_base + r] = sr < nd ? base + sh[sr - es] : base + total;
+  }
 }
 
 // ===========================================================================
@@ -884,11 +937,12 @@ int lanes_per_row(const toc_dev *d) {
 }
 
 // Whether the k = 1 kernels can keep a batch's H in LDS.
-bool k1_fits(const toc_dev *d, int op) {
-  size_t h = (size_t)d->max_codes * 4;
-  if (op == TOC_OP_LEFT && d->info.n_cols <= kOutLdsMax) h += (size_t)d->info.n_cols * 4;
-  return h + 16 <= kLdsMax;
+size_t k1_lds(const toc_dev *d, int op) {
+  if (op == TOC_OP_RIGHT) return std::max<size_t>(16, (size_t)d->max_codes * 4);
+  return ((size_t)d->max_rows + d->max_codes + 2 * (size_t)d->max_tree + 1) * 4;
 }
+
+bool k1_fits(const toc_dev *d, int op) { return k1_lds(d, op) <= kLdsMax; }
 
 // Execution plan of an op: which kernel family, its LDS bytes, and the workspace
 // it needs (rows of row_floats floats per code that needs an H row in memory).
@@ -1119,7 +1173,7 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
   hipStream_t s = (hipStream_t)stream;
   const Img im = image_of(d);
   if (k == 1 && k1_fits(d, TOC_OP_RIGHT)) {
-    const size_t lds = std::max<size_t>(16, (size_t)d->max_codes * 4);
+    const size_t lds = k1_lds(d, TOC_OP_RIGHT);
     const int lpr = lanes_per_row(d);
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
@@ -1187,32 +1241,17 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
   hipStream_t s = (hipStream_t)stream;
   const Img im = image_of(d);
   if (k == 1 && k1_fits(d, TOC_OP_LEFT)) {
-    const bool out_lds = m <= kOutLdsMax;
-    const int32_t hw = d->max_codes;
-    const size_t lds = std::max<size_t>(16, ((size_t)hw + (out_lds ? m : 0)) * 4);
-    const int lpr = lanes_per_row(d);
+    const size_t lds = k1_lds(d, TOC_OP_LEFT);
+    if ((st = allow_lds(left_k1_kernel, lds))) return st;
+    const uint8_t *bb = (const uint8_t *)d->buf;
+    const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
+    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
+    const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-#define TOC_LEFT_K1(L, O)                                                                  \
-  if ((st = allow_lds(left_k1_kernel<L, O>, lds))) return st;                               \
-  hipLaunchKernelGGL((left_k1_kernel<L, O>), dim3(g), dim3(kBlock), lds, s, im, b0, m, hw, G, \
-                     ldg, out, ldo, accumulate);
-      if (out_lds) {
-        switch (lpr) {
-          case 8: TOC_LEFT_K1(8, true) break;
-          case 16: TOC_LEFT_K1(16, true) break;
-          case 32: TOC_LEFT_K1(32, true) break;
-          default: TOC_LEFT_K1(64, true) break;
-        }
-      } else {
-        switch (lpr) {
-          case 8: TOC_LEFT_K1(8, false) break;
-          case 16: TOC_LEFT_K1(16, false) break;
-          case 32: TOC_LEFT_K1(32, false) break;
-          default: TOC_LEFT_K1(64, false) break;
-        }
-      }
-#undef TOC_LEFT_K1
+      hipLaunchKernelGGL(left_k1_kernel, dim3(g), dim3(kBlock), lds, s, im, occ_off, occ_row,
+                         tlist, b0, m, d->max_rows, d->max_codes, (int32_t)d->max_tree, G, ldg,
+                         out, ldo, accumulate);
       if ((st = launch_status("left_k1_kernel"))) return st;
     }
     return TOC_OK;
@@ -1265,10 +1304,12 @@ toc_status toc_decode_csr(const toc_dev *d, int64_t *rowptr, int32_t *col, float
     return TOC_OK;
   }
   const Img im = image_of(d);
-  for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
-    const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-    hipLaunchKernelGGL(decode_kernel, dim3(g), dim3(kDecBlock), 0, s, im, b0, rowptr, col,
-                       (uint32_t *)val);
+  const uint4 *dtiles = (const uint4 *)((const uint8_t *)d->buf + d->layout.dtiles);
+  for (int64_t t0 = 0; t0 < d->n_dtiles; t0 += (1 << 30)) {
+    const int64_t n = std::min<int64_t>(d->n_dtiles - t0, 1 << 30);
+    const unsigned g = (unsigned)(((n + kXcd - 1) / kXcd) * kXcd);
+    hipLaunchKernelGGL(decode_kernel, dim3(g), dim3(kDecBlock), 0, s, im, dtiles, t0, n, rowptr,
+                       col, (uint32_t *)val);
     if ((st = launch_status("decode_kernel"))) return st;
   }
   return TOC_OK;

@@ -391,7 +391,7 @@ struct ImgScratch {
 // Algorithm 2 on (I, D), then live marking and the depth-ordered renumbering;
 // writes the batch's arrays at its offsets.  Returns the per-batch counts through bt.
 toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_layout &L,
-                       uint8_t *dst, toc_batch &bt, ImgScratch &S) {
+                       uint8_t *dst, toc_batch &bt, int64_t dtile_base, ImgScratch &S) {
   const bool keep = flags & TOC_UPLOAD_KEEP_DEAD;
   const int64_t nI = (int64_t)e->I_col.size();
   const int64_t N = e->n_nodes;
@@ -543,6 +543,24 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     if (c < n_int1 || c >= n1) S.keys.push_back(((uint64_t)colv[c] << 32) | (uint64_t)c);
   std::sort(S.keys.begin(), S.keys.end());
   for (size_t t = 0; t < S.keys.size(); ++t) tlist[t] = (uint32_t)S.keys[t];
+  // decode tiles: for every kDecodeTile entries of D, the batch, the first entry,
+  // the number of pairs before it in the batch and the first row starting in it
+  {
+    uint32_t *dt = (uint32_t *)(dst + L.dtiles) + 4 * dtile_base;
+    const int64_t nd = (int64_t)e->D_codes.size();
+    const int64_t ntiles = std::max<int64_t>(1, (nd + kDecodeTile - 1) / kDecodeTile);
+    uint64_t pairs = 0;
+    int64_t row = 0;
+    for (int64_t t = 0; t < ntiles; ++t) {
+      const int64_t es = t * kDecodeTile;
+      while (row < e->n_rows && e->D_rowptr[row] < es) ++row;
+      dt[4 * t + 0] = (uint32_t)b;
+      dt[4 * t + 1] = (uint32_t)es;
+      dt[4 * t + 2] = (uint32_t)pairs;
+      dt[4 * t + 3] = (uint32_t)row;
+      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += depv[dcodes[j]];
+    }
+  }
   bt.n_codes = (int32_t)n_codes;
   bt.n_lvl1 = (int32_t)n1;
   bt.n_levels = levels;
@@ -562,6 +580,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   dev->batches.assign((size_t)n_batches, toc_batch{});
   dev->max_rows = dev->max_codes = dev->max_levels = 0;
   dev->max_d = dev->max_deep = dev->max_tree = 0;
+  dev->dtile_base.assign((size_t)n_batches, 0);
+  int64_t dtiles = 0;
   for (int64_t b = 0; b < n_batches; ++b) {
     const toc_enc *e = encs[b];
     if (!e) return fail(TOC_EINVAL, "encs[%lld] is NULL", (long long)b);
@@ -589,6 +609,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
     dev->max_deep = std::max(dev->max_deep, nd);
     dev->max_tree = std::max(dev->max_tree, nd + ni);
     tree += nd + ni;
+    dev->dtile_base[b] = dtiles;
+    dtiles += std::max<int64_t>(1, (c.d + kDecodeTile - 1) / kDecodeTile);
     codes += c.codes;
     levels += c.levels + 1;
     rows += c.rows;
@@ -616,6 +638,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.occ_off = off; off = align256(off + 4 * (codes + n_batches));
   L.occ_row = off; off = align256(off + 4 * d);
   L.tlist = off;   off = align256(off + 4 * tree);
+  L.dtiles = off;  off = align256(off + 16 * dtiles);
+  dev->n_dtiles = dtiles;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;
   dev->total_tree = tree;
@@ -652,7 +676,7 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
       if (b >= n_batches || first_err.load() != 0) return;
       toc_status st;
       try {
-        st = write_batch(encs[b], b, flags, L, dst, dev->batches[b], S);
+        st = write_batch(encs[b], b, flags, L, dst, dev->batches[b], dev->dtile_base[b], S);
       } catch (const std::bad_alloc &) {
         st = fail(TOC_ENOMEM, "out of host memory");
       }

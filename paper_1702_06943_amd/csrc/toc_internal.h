@@ -36,9 +36,14 @@ struct toc_dev {
   int32_t max_rows = 0, max_codes = 0, max_levels = 0;
   int64_t max_deep = 0, max_tree = 0, max_d = 0;
   int64_t total_deep = 0, total_tree = 0;
+  std::vector<int64_t> dtile_base;  // first decode tile of each batch
+  int64_t n_dtiles = 0;
 };
 
 namespace toc {
+
+// Entries of D per decode tile (one independent workgroup each).
+constexpr int64_t kDecodeTile = 1024;
 
 // Records a message for toc_last_error() and returns s.
 toc_status fail(toc_status s, const char *fmt, ...);
