@@ -162,7 +162,7 @@ def kernel_source_hash():
 def measured_traffic(op, cfg):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
     taken on the current kernel sources; else None."""
-    path = os.path.join(HERE, "profiles", f"traffic_{cfg}.txt")
+    path = os.path.join(HERE, "profiles", f"toc_kernels_{cfg}_hbm_traffic.txt")
     if not os.path.exists(path):
         return None
     src = kernel_source_hash()
@@ -288,7 +288,8 @@ def main():
         roof = {"bound": "hbm", "achieved": bytes_dom / t_dom / 1e9,
                 "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dom, cfg)
+    full_size = nb == spec["n_batches"] and k == spec["k"]
+    roof["traffic"] = measured_traffic(dom, cfg) if full_size else None
     roof["kernel"] = dom
 
     line = {

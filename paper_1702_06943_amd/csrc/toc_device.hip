@@ -984,11 +984,19 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
       return p;
     }
   } else {
-    const int n_tiles = (k + kLpMaxTW - 1) / kLpMaxTW;
-    int tw = (k + n_tiles - 1) / n_tiles;
-    tw += tw & 1;
-    const size_t lds = ((size_t)d->max_rows * tw + 3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) * 4;
-    if (k >= 2 && lds <= kLdsMax - 256) {
+    // tile widths are multiples of 32 columns, so tiles of G rows and out rows
+    // start on 128-byte boundaries; the widest that fits LDS is taken
+    int tw = 0;
+    size_t lds = 0;
+    for (int cand = std::min(kLpMaxTW, (k + 31) / 32 * 32); cand >= 32; cand -= 32) {
+      lds = ((size_t)d->max_rows * cand + 3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) * 4;
+      if (lds <= kLdsMax - 256) {
+        tw = cand;
+        break;
+      }
+    }
+    const int n_tiles = tw ? (k + tw - 1) / tw : 1;
+    if (k >= 2 && tw > 0) {
       p.path = kPathTiled;
       p.n_tiles = n_tiles;
       p.tw = tw;
