@@ -48,8 +48,12 @@ class DevInfo(C.Structure):
 
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
-                ("batches", "level", "parent", "col", "val", "depth", "span", "dcodes",
-                 "occ_off", "occ_row", "tlist", "dtiles", "end")]
+                ("batches", "level", "node", "span", "dcodes", "occ_off", "occ_row",
+                 "tlist", "dtiles", "end")]
+
+
+# one record of the image's node array (toc_node)
+NODE_DTYPE = np.dtype([("col", "<u4"), ("val", "<f4"), ("parent", "<u4"), ("depth", "<u4")])
 
 
 BATCH_DTYPE = np.dtype([

@@ -27,10 +27,7 @@ constexpr size_t kLdsMax = 160 * 1024;        // gfx950 LDS per workgroup
 struct Img {
   const toc_batch *batches;
   const uint32_t *level;
-  const uint32_t *parent;
-  const uint32_t *col;
-  const float *val;
-  const uint32_t *depth;
+  const toc_node *node;
   const uint32_t *span;
   const uint32_t *dcodes;
 };
@@ -39,10 +36,23 @@ Img image_of(const toc_dev *d) {
   const uint8_t *b = (const uint8_t *)d->buf;
   const toc_layout &L = d->layout;
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
-             (const uint32_t *)(b + L.parent),   (const uint32_t *)(b + L.col),
-             (const float *)(b + L.val),         (const uint32_t *)(b + L.depth),
-             (const uint32_t *)(b + L.span),     (const uint32_t *)(b + L.dcodes)};
+             (const toc_node *)(b + L.node), (const uint32_t *)(b + L.span),
+             (const uint32_t *)(b + L.dcodes)};
 }
+
+// Views of one field of a batch's node records, indexed by local code.
+struct NodeCol {
+  const toc_node *n;
+  __device__ uint32_t operator[](int64_t c) const { return n[c].col; }
+};
+struct NodeVal {
+  const toc_node *n;
+  __device__ float operator[](int64_t c) const { return n[c].val; }
+};
+struct NodePar {
+  const toc_node *n;
+  __device__ uint32_t operator[](int64_t c) const { return n[c].parent; }
+};
 
 // Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
 __device__ inline int wave_id() {
@@ -84,9 +94,9 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   extern __shared__ float H[];
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
+  const NodePar par{im.node + bt.code_base};
+  const NodeCol col{im.node + bt.code_base};
+  const NodeVal val{im.node + bt.code_base};
   for (int d = 1; d <= bt.n_levels; ++d) {
     const uint32_t a = lvl[d - 1], e = lvl[d];
     for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
@@ -124,9 +134,9 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = im.batches[b];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
+  const NodePar par{im.node + bt.code_base};
+  const NodeCol col{im.node + bt.code_base};
+  const NodeVal val{im.node + bt.code_base};
   const uint32_t *oo = occ_off_all + bt.code_base + b;
   const uint32_t *orow = occ_row_all + bt.d_base;
   const uint32_t *tl = tlist_all + bt.tree_base;
@@ -221,9 +231,9 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
     float *__restrict__ R, int64_t ldr, float *__restrict__ ws) {
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
+  const NodePar par{im.node + bt.code_base};
+  const NodeCol col{im.node + bt.code_base};
+  const NodeVal val{im.node + bt.code_base};
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
   float *Hd = ws + (bt.deep_base - ws_base) * kt;
@@ -292,9 +302,9 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = im.batches[b];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const float *val = im.val + bt.code_base;
+  const NodePar par{im.node + bt.code_base};
+  const NodeCol col{im.node + bt.code_base};
+  const NodeVal val{im.node + bt.code_base};
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = wave_id();
@@ -397,183 +407,367 @@ __device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
 }
 
+// A batch record read into wave-uniform (scalar) registers, so that pointers and
+// buffer descriptors derived from it stay scalar.
+__device__ inline int64_t uniform64(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ inline toc_batch uniform_batch(const toc_batch *p) {
+  toc_batch t = *p;
+  t.code_base = uniform64(t.code_base);
+  t.d_base = uniform64(t.d_base);
+  t.row_base = uniform64(t.row_base);
+  t.span_base = uniform64(t.span_base);
+  t.nnz_base = uniform64(t.nnz_base);
+  t.deep_base = uniform64(t.deep_base);
+  t.tree_base = uniform64(t.tree_base);
+  t.lvl_base = uniform64(t.lvl_base);
+  t.n_rows = __builtin_amdgcn_readfirstlane(t.n_rows);
+  t.n_codes = __builtin_amdgcn_readfirstlane(t.n_codes);
+  t.n_lvl1 = __builtin_amdgcn_readfirstlane(t.n_lvl1);
+  t.n_int1 = __builtin_amdgcn_readfirstlane(t.n_int1);
+  t.n_levels = __builtin_amdgcn_readfirstlane(t.n_levels);
+  t.n_d = __builtin_amdgcn_readfirstlane(t.n_d);
+  return t;
+}
+
+// Raw buffer resource over n 32-bit elements: loads at an index >= n return 0
+// instead of touching memory (the range check of buffer instructions).
+using BufRes = __amdgpu_buffer_rsrc_t;
+constexpr int kBufFlags = 0x00020000;   // dword 3 of a raw 32-bit buffer descriptor on gfx9
+
+__device__ inline BufRes buf_res(const void *p, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)(n * 4u),
+                                           kBufFlags);
+}
+
+__device__ inline uint32_t buf_load(BufRes r, uint32_t i) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, i * 4u, 0, 0);
+}
+
+// Buffer over n node records; key_load reads the key pair (col, val bits) of one.
+__device__ inline BufRes node_res(const toc_node *p, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<toc_node *>(p), (short)0,
+                                           (int)(n * (uint32_t)sizeof(toc_node)), kBufFlags);
+}
+
+__device__ inline uint2 key_load(BufRes r, uint32_t c) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, c * (uint32_t)sizeof(toc_node), 0, 0);
+  return make_uint2(v[0], v[1]);
+}
+
+__device__ inline uint4 node_load(const toc_node *n, int64_t c) { return *(const uint4 *)(n + c); }
+
 // ---------------------------------------------------------------------------
-// Right multiplication (Theorem 1, Algorithm 7).  A 32-column tile of W sits in
-// LDS.  Lanes form 8 groups of 8; a lane holds 4 consecutive columns, so a group
-// covers the tile for one entry of D and a wave takes 8 entries of a tuple per
-// step.  For each piece of up to 128 entries of a tuple the wave fetches the
-// codes' (LDS row, multiplier) one piece ahead and stages them in LDS, where each
-// group reads its entry by broadcast.  H rows of depth >= 2 codes are built level
-// by level first, in LDS when they fit.
+// Right multiplication (Theorem 1, Algorithm 7), tiled over the columns of W.
+// Work items are (batch, 32-column tile) pairs.  The items of one batch are
+// consecutive in the item order of one XCD, so the workers that take them run
+// together there and share the batch's image in that XCD's L2.  A worker keeps
+// the tile of W it last used in LDS (rows 0..m-1; row m is all zeros) and the H
+// rows of the batch's depth >= 2 codes after it, built level by level.
+// An 8-lane group owns one tuple (a lane holds 4 columns), so a wave sums 8
+// tuples at once and needs no cross-lane reduction.  The codes of the wave's
+// entries are loaded two chunks ahead and translated to (LDS row, multiplier)
+// one chunk ahead; a chunk (16 entries of each of the 8 tuples) is staged in the
+// wave's part of LDS, where every lane of a group reads its tuple's entry by
+// broadcast.  Entries past the end of a tuple point at the zero row.
 // ---------------------------------------------------------------------------
 constexpr int kRtKT = 32;
 constexpr int kRtBlock = 1024;
 constexpr int kRtWaves = kRtBlock / kWave;
-constexpr int kRtPiece = 128;
-constexpr uint32_t kRtGlobal = 0x80000000u;   // staged row lives in the workspace
+constexpr int kRtGroups = kWave / 8;              // tuples per wave
+constexpr int kRtChunk = 16;                      // entries per tuple per pipeline step
+constexpr uint32_t kRtStageBytes = kRtWaves * kRtChunk * kRtGroups * 8;
+constexpr uint32_t kRtStaticBytes = 16;           // static LDS: two tuple-group counters
+constexpr uint32_t kRtGlobal = 0x80000000u;       // H row lives in the workspace
+constexpr uint32_t kRtNone = 0xFFFFFFFFu;         // no entry
 
-struct RtPiece {
-  int r;            // tuple (row of the batch); >= n_rows: none
-  uint32_t j, e;    // entries [j, min(j + kRtPiece, e)) of D; e = end of the tuple
+struct RtChunk {
+  int tg;           // tuple group (tuples 8*tg .. 8*tg+7 of the batch); >= n_tg: none
+  uint32_t steps;   // entries per tuple to process, rounded up to a multiple of 4
+  bool last;        // last chunk of the tuple group
 };
 
 template <bool DEEP_LDS>
 __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
-    Img im, int64_t nb, int n_tiles, int spx, int m, const float *__restrict__ W,
+    Img im, int64_t nb, int n_tiles, int spw, int m, const float *__restrict__ W,
     int64_t ldw, int k, float *__restrict__ R, int64_t ldr, float *__restrict__ ws,
     int64_t slot_floats) {
   extern __shared__ float4 smem4[];
-  float *lds = (float *)smem4;
-  const TileWorker tw = tile_worker(n_tiles, spx);
-  if (!tw.active) return;
-  const int k0 = tw.tile * kRtKT;
-  const int kt = min(kRtKT, k - k0);
+  char *lds = (char *)smem4;
+  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
   const int lane = threadIdx.x % kWave, wave = wave_id();
-  const int grp = lane / 8, q = 4 * (lane % 8);
-  float *Wt = lds;                                               // m x kRtKT
-  uint2 *stage = (uint2 *)(lds + (size_t)m * kRtKT) + wave * kRtPiece;
-  const uint32_t hl_base = (uint32_t)m * kRtKT + kRtWaves * kRtPiece * 2;   // floats
+  const int grp = lane / 8, sub = lane % 8, q = 4 * sub;
+  __shared__ uint32_t tg_next[2];                             // next free tuple group, by item parity
+  uint2 *stage = (uint2 *)lds + wave * (kRtChunk * kRtGroups);
+  float *Wt = (float *)(lds + kRtStageBytes);                 // (m + 1) x kRtKT, then deep rows
+  const uint32_t qb = kRtStageBytes + 4u * (uint32_t)q;       // byte offset of this lane's columns
+  const uint32_t zrow = (uint32_t)m;
   float *Hg = ws + blockIdx.x * slot_floats;
-  for (int e = threadIdx.x; e < m * (kRtKT / 4); e += kRtBlock) {
-    const int c = e / (kRtKT / 4), q4 = 4 * (e % (kRtKT / 4));
-    const float *src = W + (int64_t)c * ldw + k0 + q4;
-    float4 v;
-    v.x = q4 + 0 < kt ? src[0] : 0.0f;
-    v.y = q4 + 1 < kt ? src[1] : 0.0f;
-    v.z = q4 + 2 < kt ? src[2] : 0.0f;
-    v.w = q4 + 3 < kt ? src[3] : 0.0f;
-    *(float4 *)&Wt[c * kRtKT + q4] = v;
-  }
-  for (int64_t b = tw.first; b < nb; b += tw.stride) {
-    const toc_batch bt = im.batches[b];
+  for (int e = threadIdx.x; e < kRtKT; e += kRtBlock) Wt[m * kRtKT + e] = 0.0f;
+  if (threadIdx.x < 2) tg_next[threadIdx.x] = kRtWaves;
+  const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
+  const int64_t n_items = nbx * n_tiles;
+  int cur_tile = -1;
+  uint32_t parity = 0;
+  for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
+    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
+    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
+    const int k0 = tile * kRtKT;
+    const int kt = min(kRtKT, k - k0);
+    const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const uint32_t *par = im.parent + bt.code_base;
-    const uint32_t *col = im.col + bt.code_base;
-    const float *val = im.val + bt.code_base;
+    const NodePar par{im.node + bt.code_base};
+    const NodeCol col{im.node + bt.code_base};
+    const NodeVal val{im.node + bt.code_base};
     const uint32_t *span = im.span + bt.span_base;
     const uint32_t *dc = im.dcodes + bt.d_base;
     const uint32_t n1 = (uint32_t)bt.n_lvl1;
     const int nrows = bt.n_rows;
-    __syncthreads();   // W tile ready / previous batch's deep rows no longer read
-    // H of depth >= 2 codes, level by level
+    __syncthreads();   // the previous item no longer reads the W tile or the deep rows
+    // the counter of the previous item is free again: ready for the next one
+    if (threadIdx.x == 0) tg_next[parity ^ 1u] = kRtWaves;
+    if (tile != cur_tile) {
+      // all loads of a pass first, then the stores
+      const int n4 = m * (kRtKT / 4);
+      const bool vec = kt == kRtKT && (ldw % 4) == 0 && (((uintptr_t)(W + k0)) & 15u) == 0;
+      for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * kRtBlock) {
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kRtBlock;
+          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e < n4) {
+            const int c = e / (kRtKT / 4), q4 = 4 * (e % (kRtKT / 4));
+            const float *src = W + (int64_t)c * ldw + k0 + q4;
+            if (vec) {
+              v[i] = *(const float4 *)src;
+            } else {
+              if (q4 + 0 < kt) v[i].x = src[0];
+              if (q4 + 1 < kt) v[i].y = src[1];
+              if (q4 + 2 < kt) v[i].z = src[2];
+              if (q4 + 3 < kt) v[i].w = src[3];
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kRtBlock;
+          if (e < n4) *(float4 *)&Wt[e * 4] = v[i];
+        }
+      }
+      cur_tile = tile;
+      __syncthreads();
+    }
+    // H of depth >= 2 codes, level by level; a group per code
+    const int gidx = wave * kRtGroups + grp;
     for (int d = 2; d <= bt.n_levels; ++d) {
       const uint32_t a = lvl[d - 1], e = lvl[d];
-      for (uint32_t c = a + wave * 8 + grp; c < e; c += kRtWaves * 8) {
+      for (uint32_t c = a + gidx; c < e; c += kRtWaves * kRtGroups) {
         const uint32_t p = par[c];
+        const uint32_t cc = col[c];
+        const float vc = val[c];
         float4 base;
         if (p < n1) {
-          base = *(const float4 *)&Wt[col[p] * kRtKT + q];
           const float vp = val[p];
+          base = *(const float4 *)&Wt[col[p] * kRtKT + q];
           base = make_float4(vp * base.x, vp * base.y, vp * base.z, vp * base.w);
         } else if (DEEP_LDS) {
-          base = *(const float4 *)&lds[hl_base + (p - n1) * kRtKT + q];
+          base = *(const float4 *)&Wt[(m + 1 + (p - n1)) * kRtKT + q];
         } else {
           base = *(const float4 *)&Hg[(int64_t)(p - n1) * kRtKT + q];
         }
-        const float4 h = f4fma(val[c], *(const float4 *)&Wt[col[c] * kRtKT + q], base);
-        if (DEEP_LDS) *(float4 *)&lds[hl_base + (c - n1) * kRtKT + q] = h;
+        const float4 h = f4fma(vc, *(const float4 *)&Wt[cc * kRtKT + q], base);
+        if (DEEP_LDS) *(float4 *)&Wt[(m + 1 + (c - n1)) * kRtKT + q] = h;
         else *(float4 *)&Hg[(int64_t)(c - n1) * kRtKT + q] = h;
       }
       __syncthreads();
     }
-    // per-tuple sums, software-pipelined over pieces of tuples
-    auto piece_after = [&](RtPiece p) -> RtPiece {
-      if (p.j + kRtPiece < p.e) return RtPiece{p.r, p.j + kRtPiece, p.e};
-      const int r = p.r + kRtWaves;
-      if (r >= nrows) return RtPiece{nrows, 0, 0};
-      return RtPiece{r, span[r], span[r + 1]};
+    // per-tuple sums
+    const int n_tg = (nrows + kRtGroups - 1) / kRtGroups;
+    // rows past the end read span[nrows] twice: an empty tuple
+    auto spans_of = [&](int tg, uint32_t &st, uint32_t &en) {
+      const int r = min(tg * kRtGroups + grp, nrows);
+      st = span[r];
+      en = span[min(r + 1, nrows)];
     };
-    auto fetch = [&](RtPiece p, uint32_t half, uint32_t code) -> uint2 {
-      const uint32_t j = p.j + half * kWave + lane;
-      if (p.r >= nrows || j >= p.e || j >= p.j + kRtPiece) return make_uint2(0u, 0u);
-      if (code < n1) return make_uint2(col[code] * kRtKT, __float_as_uint(val[code]));
-      return make_uint2(DEEP_LDS ? hl_base + (code - n1) * kRtKT : (kRtGlobal | (code - n1)),
-                        __float_as_uint(1.0f));
+    auto wave_max = [&](uint32_t v) -> uint32_t {
+      v = max(v, (uint32_t)__shfl_xor((int)v, 8, kWave));
+      v = max(v, (uint32_t)__shfl_xor((int)v, 16, kWave));
+      v = max(v, (uint32_t)__shfl_xor((int)v, 32, kWave));
+      return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
     };
-    auto load_codes = [&](RtPiece p, uint32_t &d0, uint32_t &d1) {
-      const uint32_t j0 = p.j + lane, j1 = p.j + kWave + lane;
-      const uint32_t lim = min(p.e, p.j + kRtPiece);
-      d0 = p.r < nrows && j0 < lim ? dc[j0] : 0u;
-      d1 = p.r < nrows && j1 < lim ? dc[j1] : 0u;
+    // Tuple groups: wave w starts with group w, then takes the next free group
+    // from the item's counter, so waves that finish early take more groups.
+    auto grab = [&]() -> int {
+      uint32_t g = 0;
+      if (lane == 0) g = atomicAdd(&tg_next[parity], 1u);
+      return __builtin_amdgcn_readfirstlane((int)g);
     };
-    // pipeline: codes of pieces p3, p4 loading; their (row, multiplier) for p1, p2
-    // gathering; p0 staged and computed
-    auto next_piece = [&](RtPiece p) -> RtPiece { return p.r < nrows ? piece_after(p) : p; };
-    RtPiece p0{wave, 0, 0};
-    if (wave < nrows) p0 = RtPiece{wave, span[wave], span[wave + 1]};
-    else p0.r = nrows;
-    RtPiece p1 = next_piece(p0), p2 = next_piece(p1), p3 = next_piece(p2), p4 = next_piece(p3);
-    uint32_t x0, x1, dA0, dA1, dB0, dB1;
-    load_codes(p0, x0, x1);
-    uint2 c0 = fetch(p0, 0, x0), c1 = fetch(p0, 1, x1);
-    load_codes(p1, x0, x1);
-    uint2 cA0 = fetch(p1, 0, x0), cA1 = fetch(p1, 1, x1);
-    load_codes(p2, x0, x1);
-    uint2 cB0 = fetch(p2, 0, x0), cB1 = fetch(p2, 1, x1);
-    load_codes(p3, dA0, dA1);
-    load_codes(p4, dB0, dB1);
+    // load stage: tuple group ltg, entries [lj, lj + kRtChunk) of each tuple;
+    // ntg is the group after it, whose spans are in nst, nen
+    int ltg = wave, ntg = n_tg;
+    uint32_t lj = 0, lmax = 0, lst = 0, len = 0, nst = 0, nen = 0;
+    if (ltg < n_tg) {
+      spans_of(ltg, lst, len);
+      lmax = wave_max(len - lst);
+      ntg = grab();
+    }
+    spans_of(ntg, nst, nen);
+    auto chunk_of_l = [&]() -> RtChunk {
+      const uint32_t n = lmax > lj ? min((uint32_t)kRtChunk, lmax - lj) : 0u;
+      return RtChunk{ltg, (n + 3u) & ~3u, lj + kRtChunk >= lmax};
+    };
+    // the next group's spans are reloaded on every step (cache hits), so that a
+    // switch of group only moves values loaded a step earlier
+    auto advance = [&]() {
+      if (ltg < n_tg) {
+        lj += kRtChunk;
+        if (lj >= lmax) {
+          ltg = ntg;
+          lj = 0;
+          lst = nst;
+          len = nen;
+          lmax = 0u;
+          if (ltg < n_tg) {
+            lmax = wave_max(len - lst);
+            ntg = grab();
+          }
+        }
+      }
+      spans_of(ntg, nst, nen);
+    };
+    // Every load below is unconditional: the buffer range checks turn reads past
+    // the batch's arrays into zeros, and entries past the end of a tuple are
+    // marked in a wave mask and become (zero row, 0) when staged.
+    const BufRes rs_dc = buf_res(dc, (uint32_t)bt.n_d);
+    const BufRes rs_node = node_res(im.node + bt.code_base, (uint32_t)bt.n_codes);
+    auto load_codes = [&](uint32_t &d0, uint32_t &d1, uint64_t &ok0, uint64_t &ok1) {
+      const uint32_t j0 = lst + lj + (uint32_t)sub, j1 = j0 + 8u;
+      const bool live = ltg < n_tg;
+      ok0 = __ballot(live && j0 < len);
+      ok1 = __ballot(live && j1 < len);
+      d0 = buf_load(rs_dc, j0);
+      d1 = buf_load(rs_dc, j1);
+    };
+    auto entry = [&](uint32_t d, uint2 key, uint64_t ok) -> uint2 {
+      uint2 g;
+      if (d < n1) {
+        g = key;
+      } else {
+        g.x = DEEP_LDS ? (uint32_t)m + 1u + (d - n1) : (kRtGlobal | (d - n1));
+        g.y = __float_as_uint(1.0f);
+      }
+      if (!__builtin_amdgcn_inverse_ballot_w64(ok)) g = make_uint2(zrow, 0u);
+      return g;
+    };
+    // an H row in LDS or in the workspace; both loads are issued and the values
+    // selected (a select of the two pointers would make a flat pointer)
+    auto row_f4 = [&](uint32_t r) -> float4 {
+      if (DEEP_LDS) return *(const float4 *)(lds + qb + r * (kRtKT * 4));
+      const bool g = (r & kRtGlobal) != 0;
+      const float4 xl = *(const float4 *)(lds + qb + (g ? zrow : r) * (kRtKT * 4));
+      float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * kRtKT + q];
+      return g ? xg : xl;
+    };
+    // Pipeline: codes of chunk L load while chunk G's codes are translated and
+    // chunk C, staged in LDS, is summed.  Two register sets alternate between the
+    // roles of G and L, so no loaded value is ever copied.
+    RtChunk G = chunk_of_l();
+    RtChunk C{n_tg, 0u, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    while (p0.r < nrows) {
-      stage[lane] = c0;
-      stage[kWave + lane] = c1;
-      c0 = cA0;
-      c1 = cA1;
-      cA0 = cB0;
-      cA1 = cB1;
-      cB0 = fetch(p3, 0, dA0);
-      cB1 = fetch(p3, 1, dA1);
-      dA0 = dB0;
-      dA1 = dB1;
-      const RtPiece p5 = next_piece(p4);
-      load_codes(p5, dB0, dB1);
-      const uint32_t n = min(p0.e - p0.j, (uint32_t)kRtPiece);
-      const uint32_t steps = ((n + 31) / 32) * 4;
-      for (uint32_t t = 0; t < steps; t += 4) {
-        const uint2 e0 = stage[(t + 0) * 8 + grp], e1 = stage[(t + 1) * 8 + grp];
-        const uint2 e2 = stage[(t + 2) * 8 + grp], e3 = stage[(t + 3) * 8 + grp];
-        float4 x0, x1, x2, x3;
-        if (!DEEP_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
-          x0 = e0.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e0.x & ~kRtGlobal) * kRtKT + q]
-                                : *(const float4 *)&lds[e0.x + q];
-          x1 = e1.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e1.x & ~kRtGlobal) * kRtKT + q]
-                                : *(const float4 *)&lds[e1.x + q];
-          x2 = e2.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e2.x & ~kRtGlobal) * kRtKT + q]
-                                : *(const float4 *)&lds[e2.x + q];
-          x3 = e3.x & kRtGlobal ? *(const float4 *)&Hg[(int64_t)(e3.x & ~kRtGlobal) * kRtKT + q]
-                                : *(const float4 *)&lds[e3.x + q];
-        } else {
-          x0 = *(const float4 *)&lds[e0.x + q];
-          x1 = *(const float4 *)&lds[e1.x + q];
-          x2 = *(const float4 *)&lds[e2.x + q];
-          x3 = *(const float4 *)&lds[e3.x + q];
-        }
-        acc = f4fma(__uint_as_float(e0.y), x0, acc);
-        acc = f4fma(__uint_as_float(e1.y), x1, acc);
-        acc = f4fma(__uint_as_float(e2.y), x2, acc);
-        acc = f4fma(__uint_as_float(e3.y), x3, acc);
-      }
-      if (p0.j + kRtPiece >= p0.e) {   // last piece of the tuple
+    auto step = [&](uint32_t gd0, uint32_t gd1, uint64_t gok0, uint64_t gok1, uint32_t &ld0,
+                    uint32_t &ld1, uint64_t &lok0, uint64_t &lok1) {
+      advance();
+      const uint2 key0 = key_load(rs_node, gd0), key1 = key_load(rs_node, gd1);
+      const RtChunk L = chunk_of_l();
+      load_codes(ld0, ld1, lok0, lok1);
+      bool done = false;
+      if (C.tg < n_tg && C.steps == kRtChunk) {
+        // a full chunk: all staged entries first, then the rows, so that many
+        // LDS reads are in flight (rows in the workspace take the loop below)
+        uint2 e[kRtChunk];
 #pragma unroll
-        for (int o = 8; o < kWave; o <<= 1) {
-          acc.x += __shfl_xor(acc.x, o, kWave);
-          acc.y += __shfl_xor(acc.y, o, kWave);
-          acc.z += __shfl_xor(acc.z, o, kWave);
-          acc.w += __shfl_xor(acc.w, o, kWave);
+        for (int t = 0; t < kRtChunk; ++t) e[t] = stage[t * kRtGroups + grp];
+        uint32_t any = 0;
+        if (!DEEP_LDS) {
+#pragma unroll
+          for (int t = 0; t < kRtChunk; ++t) any |= e[t].x;
         }
-        if (grp == 0) {
-          float *rr = R + (bt.row_base + p0.r) * ldr + k0 + q;
-          if (q + 0 < kt) rr[0] = acc.x;
-          if (q + 1 < kt) rr[1] = acc.y;
-          if (q + 2 < kt) rr[2] = acc.z;
-          if (q + 3 < kt) rr[3] = acc.w;
+        if (!(any & kRtGlobal)) {
+          // rows in blocks of 8 reads issued back to back
+#pragma unroll
+          for (int h = 0; h < kRtChunk; h += 8) {
+            float4 xr[8];
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              xr[t] = *(const float4 *)(lds + qb + e[h + t].x * (kRtKT * 4));
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[h + t].y), xr[t], acc);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          done = true;
         }
-        acc = make_float4(0.f, 0.f, 0.f, 0.f);
       }
-      p0 = p1;
-      p1 = p2;
-      p2 = p3;
-      p3 = p4;
-      p4 = p5;
+      if (C.tg < n_tg && !done) {
+        for (uint32_t t = 0; t < C.steps; t += 4) {
+          const uint2 e0 = stage[(t + 0) * kRtGroups + grp], e1 = stage[(t + 1) * kRtGroups + grp];
+          const uint2 e2 = stage[(t + 2) * kRtGroups + grp], e3 = stage[(t + 3) * kRtGroups + grp];
+          float4 x0, x1, x2, x3;
+          if (!DEEP_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
+            x0 = row_f4(e0.x);
+            x1 = row_f4(e1.x);
+            x2 = row_f4(e2.x);
+            x3 = row_f4(e3.x);
+          } else {
+            x0 = *(const float4 *)(lds + qb + e0.x * (kRtKT * 4));
+            x1 = *(const float4 *)(lds + qb + e1.x * (kRtKT * 4));
+            x2 = *(const float4 *)(lds + qb + e2.x * (kRtKT * 4));
+            x3 = *(const float4 *)(lds + qb + e3.x * (kRtKT * 4));
+          }
+          acc = f4fma(__uint_as_float(e0.y), x0, acc);
+          acc = f4fma(__uint_as_float(e1.y), x1, acc);
+          acc = f4fma(__uint_as_float(e2.y), x2, acc);
+          acc = f4fma(__uint_as_float(e3.y), x3, acc);
+        }
+      }
+      if (C.tg < n_tg) {
+        if (C.last) {
+          const int r = C.tg * kRtGroups + grp;
+          if (r < nrows) {
+            float *rr = R + (bt.row_base + r) * ldr + k0 + q;
+            if (q + 3 < kt) {
+              rr[0] = acc.x;
+              rr[1] = acc.y;
+              rr[2] = acc.z;
+              rr[3] = acc.w;
+            } else {
+              if (q + 0 < kt) rr[0] = acc.x;
+              if (q + 1 < kt) rr[1] = acc.y;
+              if (q + 2 < kt) rr[2] = acc.z;
+            }
+          }
+          acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      // entries of chunk G: entry t of tuple grp goes to stage[t * 8 + grp]
+      stage[(sub + 0) * kRtGroups + grp] = entry(gd0, key0, gok0);
+      stage[(sub + 8) * kRtGroups + grp] = entry(gd1, key1, gok1);
+      __builtin_amdgcn_wave_barrier();
+      C = G;
+      G = L;
+    };
+    uint32_t dA0, dA1, dB0, dB1;
+    uint64_t okA0, okA1, okB0, okB1;
+    load_codes(dA0, dA1, okA0, okA1);
+    while (G.tg < n_tg || C.tg < n_tg) {
+      step(dA0, dA1, okA0, okA1, dB0, dB1, okB0, okB1);
+      if (!(G.tg < n_tg || C.tg < n_tg)) break;
+      step(dB0, dB1, okB0, okB1, dA0, dA1, okA0, okA1);
     }
   }
 }
@@ -625,9 +819,9 @@ __global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
   for (int64_t b = twk.first; b < nb; b += twk.stride) {
     const toc_batch bt = im.batches[b];
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const uint32_t *par = im.parent + bt.code_base;
-    const uint32_t *col = im.col + bt.code_base;
-    const float *val = im.val + bt.code_base;
+    const NodePar par{im.node + bt.code_base};
+    const NodeCol col{im.node + bt.code_base};
+    const NodeVal val{im.node + bt.code_base};
     const uint32_t *oo = occ_off_all + bt.code_base + b;
     const uint32_t *orow = occ_row_all + bt.d_base;
     const uint32_t *tl = tlist_all + bt.tree_base;
@@ -832,10 +1026,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   const int64_t t = t0 + slot;
   const uint4 dt = dtiles[t];                       // batch, first entry, pairs before, first row
   const toc_batch bt = im.batches[dt.x];
-  const uint32_t *par = im.parent + bt.code_base;
-  const uint32_t *col = im.col + bt.code_base;
-  const uint32_t *val = (const uint32_t *)im.val + bt.code_base;
-  const uint32_t *dep = im.depth + bt.code_base;
+  const toc_node *node = im.node + bt.code_base;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = wave_id();
@@ -847,11 +1038,15 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
     c[i] = j < nd ? dc[j] : 0u;
   }
+  // the node record of each entry's code: key pair, parent, depth
+  uint4 rec[kDecPer];
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) {
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
-    sh[i * kDecBlock + threadIdx.x] = j < nd ? dep[c[i]] : 0u;
+    rec[i] = j < nd ? node_load(node, c[i]) : make_uint4(0u, 0u, 0u, 0u);
   }
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) sh[i * kDecBlock + threadIdx.x] = rec[i].w;
   __syncthreads();
   // exclusive scan in entry order: thread t owns entries kDecPer*t .. +kDecPer-1
   uint32_t v[kDecPer], s = 0;
@@ -880,13 +1075,15 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   for (int i = 0; i < kDecPer; ++i) {
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
     if (j < nd) {
-      uint32_t x = c[i];
-      const uint32_t d = dep[x];
+      uint4 r = rec[i];
+      const uint32_t d = r.w;
       int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
-      for (uint32_t q = 0; q < d; ++q, --p) {
-        ocol[p] = (int32_t)col[x];
-        oval[p] = val[x];
-        x = par[x];
+      for (uint32_t q = 0;;) {
+        ocol[p] = (int32_t)r.x;
+        oval[p] = r.y;
+        if (++q >= d) break;
+        --p;
+        r = node_load(node, r.z);
       }
     }
   }
@@ -970,15 +1167,18 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
     return p;
   }
   if (right) {
-    const size_t fixed = ((size_t)m * kRtKT + (size_t)kRtWaves * kRtPiece * 2) * 4;
-    if (k >= 4 && fixed <= kLdsMax) {
+    const size_t fixed = kRtStageBytes + ((size_t)m + 1) * kRtKT * 4;
+    const size_t lds_max = kLdsMax - kRtStaticBytes;
+    if (k >= 4 && fixed <= lds_max) {
       p.path = kPathTiled;
       p.n_tiles = (k + kRtKT - 1) / kRtKT;
       p.tw = kRtKT;
-      p.deep_lds = fixed + (size_t)d->max_deep * kRtKT * 4 <= kLdsMax;
+      p.deep_lds = fixed + (size_t)d->max_deep * kRtKT * 4 <= lds_max;
       p.lds = p.deep_lds ? fixed + (size_t)d->max_deep * kRtKT * 4 : fixed;
-      p.spx = std::max(1, kCuPerXcd / p.n_tiles);
-      p.grid = (unsigned)(kXcd * p.spx * p.n_tiles);
+      // workers per XCD: one per CU, fewer when there are fewer items
+      const int64_t items = (d->info.n_batches + kXcd - 1) / kXcd * p.n_tiles;
+      p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
+      p.grid = (unsigned)(kXcd * p.spx);
       p.row_floats = p.deep_lds ? 0 : kRtKT;
       p.ws_floats = p.deep_lds ? 0 : (int64_t)p.grid * d->max_deep * kRtKT;
       return p;

@@ -32,6 +32,8 @@ void clear_error() { g_err.clear(); }
 // by one open-addressing table keyed by (node, column, value bits): the per-node
 // child maps of the paper folded into a single hash table.
 // ---------------------------------------------------------------------------
+static_assert(sizeof(toc_node) == 16, "toc_node is one 16-byte record");
+
 namespace {
 
 struct Slot {
@@ -486,31 +488,27 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       for (uint64_t kc : S.keys) S.newidx[(uint32_t)kc] = (uint32_t)at++;
     }
   }
-  uint32_t *parent = (uint32_t *)(dst + L.parent) + bt.code_base;
-  uint32_t *colv = (uint32_t *)(dst + L.col) + bt.code_base;
-  uint32_t *valv = (uint32_t *)(dst + L.val) + bt.code_base;
-  uint32_t *depv = (uint32_t *)(dst + L.depth) + bt.code_base;
+  toc_node *node = (toc_node *)(dst + L.node) + bt.code_base;
   for (int64_t c = 1; c < N; ++c) {
     if (!S.live[c]) continue;
     const uint32_t at = S.newidx[c];
-    parent[at] = S.depth[c] == 1 ? 0xFFFFFFFFu : S.newidx[S.parent[c]];
-    depv[at] = S.depth[c];
+    node[at].parent = S.depth[c] == 1 ? 0xFFFFFFFFu : S.newidx[S.parent[c]];
+    node[at].depth = S.depth[c];
   }
   // keys: node c <= |I| has key I[c-1]; node idx > |I| has the first pair of the
   // code that follows its parent in D (Algorithm 2).
-  for (int64_t c = 1; c <= nI; ++c) {
-    if (!S.live[c]) continue;
-    colv[S.newidx[c]] = (uint32_t)e->I_col[c - 1];
-    valv[S.newidx[c]] = e->I_bits[c - 1];
-  }
+  auto set_key = [&](uint32_t at, uint32_t fi) {
+    node[at].col = (uint32_t)e->I_col[fi - 1];
+    std::memcpy(&node[at].val, &e->I_bits[fi - 1], sizeof(float));
+  };
+  for (int64_t c = 1; c <= nI; ++c)
+    if (S.live[c]) set_key(S.newidx[c], (uint32_t)c);
   idx = nI + 1;
   for (int32_t r = 0; r < e->n_rows; ++r) {
     const int64_t a = e->D_rowptr[r], b = e->D_rowptr[r + 1];
     for (int64_t j = a; j + 1 < b; ++j, ++idx) {
       if (!S.live[idx]) continue;
-      const uint32_t fi = S.first[e->D_codes[j + 1]];  // index into I, 1-based
-      colv[S.newidx[idx]] = (uint32_t)e->I_col[fi - 1];
-      valv[S.newidx[idx]] = e->I_bits[fi - 1];
+      set_key(S.newidx[idx], S.first[e->D_codes[j + 1]]);   // index into I, 1-based
     }
   }
   // spans and renumbered D
@@ -540,7 +538,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   uint32_t *tlist = (uint32_t *)(dst + L.tlist) + bt.tree_base;
   S.keys.clear();
   for (int64_t c = 0; c < n_codes; ++c)
-    if (c < n_int1 || c >= n1) S.keys.push_back(((uint64_t)colv[c] << 32) | (uint64_t)c);
+    if (c < n_int1 || c >= n1) S.keys.push_back(((uint64_t)node[c].col << 32) | (uint64_t)c);
   std::sort(S.keys.begin(), S.keys.end());
   for (size_t t = 0; t < S.keys.size(); ++t) tlist[t] = (uint32_t)S.keys[t];
   // decode tiles: for every kDecodeTile entries of D, the batch, the first entry,
@@ -558,7 +556,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       dt[4 * t + 1] = (uint32_t)es;
       dt[4 * t + 2] = (uint32_t)pairs;
       dt[4 * t + 3] = (uint32_t)row;
-      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += depv[dcodes[j]];
+      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += node[dcodes[j]].depth;
     }
   }
   bt.n_codes = (int32_t)n_codes;
@@ -629,10 +627,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   int64_t off = 0;
   L.batches = off; off = align256(off + (int64_t)sizeof(toc_batch) * n_batches);
   L.level = off;   off = align256(off + 4 * levels);
-  L.parent = off;  off = align256(off + 4 * codes);
-  L.col = off;     off = align256(off + 4 * codes);
-  L.val = off;     off = align256(off + 4 * codes);
-  L.depth = off;   off = align256(off + 4 * codes);
+  L.node = off;    off = align256(off + (int64_t)sizeof(toc_node) * codes);
   L.span = off;    off = align256(off + 4 * spans);
   L.dcodes = off;  off = align256(off + 4 * d);
   L.occ_off = off; off = align256(off + 4 * (codes + n_batches));

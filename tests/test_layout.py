@@ -27,10 +27,7 @@ def read_image(dev, buf):
     img = dict(
         bt=bt, info=info,
         level=arr("level", np.uint32, n_levels),
-        parent=arr("parent", np.uint32, n_codes),
-        col=arr("col", np.uint32, n_codes),
-        val=arr("val", np.float32, n_codes),
-        depth=arr("depth", np.uint32, n_codes),
+        node=arr("node", T.NODE_DTYPE, n_codes),
         span=arr("span", np.uint32, int((bt["n_rows"] + 1).sum()) if nb else 0),
         dcodes=arr("dcodes", np.uint32, info["n_codes"]),
         occ_off=arr("occ_off", np.uint32, n_codes + nb),
@@ -38,6 +35,8 @@ def read_image(dev, buf):
         tlist=arr("tlist", np.uint32,
                   int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0),
     )
+    for f in ("parent", "col", "val", "depth"):
+        img[f] = img["node"][f]
     return img
 
 
