@@ -374,30 +374,14 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
 
 // ===========================================================================
 // ===========================================================================
-// Tiled kernels for wide k.  Persistent workgroups, one per CU: worker (x, s) on
-// XCD x (blocks are dealt to the 8 XCDs round-robin) keeps column tile
-// s % n_tiles resident in LDS and walks the batches of stream s / n_tiles, so the
-// n_tiles workers of a batch run together on one XCD and share its image in L2.
+// Tiled kernels for wide k.  Persistent workgroups, one per CU.  Blocks are dealt
+// to the 8 XCDs round-robin; worker s of XCD x takes items s, s + spw, ... of its
+// XCD's list, in which item i is column tile i % n_tiles of batch
+// x + 8 * (i / n_tiles).  The tiles of a batch are consecutive items, so they run
+// together on one XCD and share the batch's image in that XCD's L2.
 // ===========================================================================
 constexpr int kXcd = 8;
 constexpr int kCuPerXcd = 32;
-
-struct TileWorker {
-  int tile;
-  bool active;
-  int64_t first, stride;
-};
-
-__device__ inline TileWorker tile_worker(int n_tiles, int spx) {
-  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
-  TileWorker w;
-  w.tile = s % n_tiles;
-  const int stream = s / n_tiles;
-  w.active = stream < spx;
-  w.first = (int64_t)stream * kXcd + x;
-  w.stride = (int64_t)spx * kXcd;
-  return w;
-}
 
 __device__ inline float4 f4fma(float s, float4 x, float4 a) {
   return make_float4(fmaf(s, x.x, a.x), fmaf(s, x.y, a.y), fmaf(s, x.z, a.z), fmaf(s, x.w, a.w));
@@ -773,55 +757,87 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Left multiplication by pulling (Theorem 2 read as a definition): G(x) is the sum
-// of the G rows over the entries of D equal to x, which the inverted index
-// occ_off/occ_row lists per code.  A tile of up to 128 columns of the batch's G
-// sits in LDS (2 columns per lane).
-//  * Codes with children or of depth >= 2 ("tree codes", few): deepest level
-//    first, one wave per code, H = own occurrences + children's H (children of a
-//    code are contiguous because levels are sorted by parent); H rows go to this
-//    worker's workspace slot.
-//  * Depth-1 leaves (sorted by column): their occurrences form one flat stream in
-//    column order; each wave owns a contiguous range of columns (balanced by
-//    occurrence count), walks its part of the stream 64 entries at a time and
-//    writes each output row once: val(code) * G[row] summed per column, plus the
-//    tree codes of that column.  The code of an entry comes from the
-//    first-occurrence bit of occ_row through a ballot and a popcount.
+// Left multiplication by pulling (Theorem 2 read as a definition, Algorithm 8's
+// result): H(x) is the sum of the G rows over the entries of D equal to x (the
+// inverted index occ_off/occ_row lists them per code) plus the H of x's children,
+// and output row j is the sum of val(x) * H(x) over the codes x of key column j.
+// Work items are (batch, TW-column tile) pairs dealt per XCD as in the right
+// product.  A worker loads the batch's G tile into LDS (row nrows_max is all
+// zeros), then
+//  * tree codes (codes with children or of depth >= 2), deepest level first, a
+//    lane group per code: H = own occurrences + children's H (children of a code
+//    are contiguous, levels being sorted by parent); H rows follow the G tile in
+//    LDS, or go to the worker's workspace slot when they do not fit;
+//  * output columns: a group of TW/4 lanes owns one column j (a lane holds 4 of
+//    the tile's columns) and sums val * row over its entries: the occurrences of
+//    the column's leaf codes (depth-1 codes without children, sorted by column,
+//    so one contiguous stretch of occ_row) and then its tree codes.  The code of
+//    a leaf occurrence is recovered from the first-occurrence bits of occ_row by
+//    a popcount carried along the column.  Entries are loaded two chunks ahead,
+//    translated to (LDS row, multiplier) one chunk ahead and staged in LDS as in
+//    the right product; groups of columns are handed out from an LDS counter.
 // ---------------------------------------------------------------------------
-constexpr int kLpBlock = 1024;
-constexpr int kLpWaves = kLpBlock / kWave;
-constexpr int kLpMaxTW = 128;
+constexpr int kLtBlock = 1024;
+constexpr int kLtWaves = kLtBlock / kWave;
 constexpr uint32_t kFirstOcc = 0x80000000u;
+constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
 
-template <int DUMMY>
-__global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
+// LDS bytes of the per-wave stages and of the column tables
+template <int TW>
+constexpr uint32_t lt_stage_bytes() { return (uint32_t)kLtWaves * (TW / 4) * (kWave / (TW / 4)) * 8; }
+
+struct LtChunk {
+  int cg;           // column group (columns GPW*cg .. GPW*cg+GPW-1); >= n_cg: none
+  uint32_t steps;   // entries per column to process, rounded up to a multiple of 4
+  uint32_t first;   // first entry of the chunk (0: a column starts)
+  bool last;        // last chunk of the column group
+};
+
+template <int TW, bool TREE_LDS>
+__global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, int64_t nb, int n_tiles, int spx, int tw,
-    int max_rows, int m, const float *__restrict__ G, int64_t ldg, int k,
+    const uint32_t *__restrict__ tlist_all, int64_t nb, int n_tiles, int spw, int max_rows,
+    int max_tree, int m, const float *__restrict__ G, int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
     int64_t slot_floats) {
+  constexpr int LPG = TW / 4;                 // lanes per group (4 columns each)
+  constexpr int GPW = kWave / LPG;            // groups (output columns) per wave
+  constexpr int CH = LPG;                     // entries per column per chunk: one per lane
+  constexpr uint32_t RB = TW * 4;             // bytes of an LDS row
   extern __shared__ float4 smem4[];
-  __shared__ uint32_t jsplit[kLpWaves + 1];
-  const TileWorker twk = tile_worker(n_tiles, spx);
-  if (!twk.active) return;
-  const int k0 = twk.tile * tw;
-  const int kt = min(tw, k - k0);
+  __shared__ uint32_t cg_next[2];
+  char *lds = (char *)smem4;
+  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
   const int lane = threadIdx.x % kWave, wave = wave_id();
-  const int qq = 2 * lane;
-  const bool lane_on = qq < tw;
-  float *Gt = (float *)smem4;                                   // max_rows x tw
-  uint32_t *Loff = (uint32_t *)(Gt + (size_t)max_rows * tw);    // m + 1: first leaf code
-  uint32_t *Ost = Loff + m + 1;                                 // m + 1: first occurrence
-  uint32_t *Toff = Ost + m + 1;                                 // m + 1: tree-list start
-  uint32_t *Coff = Toff + m + 1;                                // children ranges
-  float *Ht = ws + blockIdx.x * slot_floats;
-  const float2 zero2 = make_float2(0.f, 0.f);
-  for (int64_t b = twk.first; b < nb; b += twk.stride) {
-    const toc_batch bt = im.batches[b];
+  const int grp = lane / LPG, sub = lane % LPG, q = 4 * sub;
+  // LDS: stages | Loff, Ost, Toff (m + 1 each) | Coff (max_tree + 1) | rows
+  uint2 *stage = (uint2 *)lds + wave * (CH * GPW);
+  uint32_t *Loff = (uint32_t *)(lds + lt_stage_bytes<TW>());
+  uint32_t *Ost = Loff + (m + 1);
+  uint32_t *Toff = Ost + (m + 1);
+  uint32_t *Coff = Toff + (m + 1);
+  const uint32_t rows_b = (uint32_t)((lt_stage_bytes<TW>() + 4u * (3u * (m + 1) + max_tree + 1) + 15u) & ~15u);
+  float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
+  const uint32_t qb = rows_b + 4u * (uint32_t)q;
+  const uint32_t zrow = (uint32_t)max_rows;
+  const uint32_t trow0 = zrow + 1u;
+  float *Hg = ws + blockIdx.x * slot_floats;
+  for (int e = threadIdx.x; e < TW; e += kLtBlock) Rw[zrow * TW + e] = 0.0f;
+  if (threadIdx.x < 2) cg_next[threadIdx.x] = kLtWaves;
+  const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
+  const int64_t n_items = nbx * n_tiles;
+  const int n_cg = (m + GPW - 1) / GPW;
+  uint32_t parity = 0;
+  for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
+    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
+    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
+    const int k0 = tile * TW;
+    const int kt = min(TW, k - k0);
+    const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const NodePar par{im.node + bt.code_base};
-    const NodeCol col{im.node + bt.code_base};
-    const NodeVal val{im.node + bt.code_base};
+    const toc_node *node = im.node + bt.code_base;
+    const NodePar par{node};
+    const NodeCol col{node};
     const uint32_t *oo = occ_off_all + bt.code_base + b;
     const uint32_t *orow = occ_row_all + bt.d_base;
     const uint32_t *tl = tlist_all + bt.tree_base;
@@ -829,15 +845,43 @@ __global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
     const uint32_t n_tree = ni + (nc - n1);
     const int nrows = bt.n_rows;
     auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
-    __syncthreads();   // previous batch done with the LDS tables
-    for (int e = threadIdx.x; e < nrows * (tw / 2); e += kLpBlock) {
-      const int r = e / (tw / 2), c2 = 2 * (e % (tw / 2));
-      const float *src = G + (bt.row_base + r) * ldg + k0 + c2;
-      *(float2 *)&Gt[r * tw + c2] =
-          make_float2(c2 < kt ? src[0] : 0.0f, c2 + 1 < kt ? src[1] : 0.0f);
+    __syncthreads();   // the previous item no longer reads the LDS rows and tables
+    if (threadIdx.x == 0) cg_next[parity ^ 1u] = kLtWaves;
+    // G tile: all loads of a pass first, then the stores
+    {
+      const int n4 = nrows * (TW / 4);
+      const bool vec = kt == TW && (ldg % 4) == 0 && (k0 % 4) == 0 &&
+                       ((((uintptr_t)G) & 15u) == 0);
+      for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * kLtBlock) {
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kLtBlock;
+          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e < n4) {
+            const int r = e / (TW / 4), q4 = 4 * (e % (TW / 4));
+            const float *src = G + (bt.row_base + r) * ldg + k0 + q4;
+            if (vec) {
+              v[i] = *(const float4 *)src;
+            } else {
+              if (q4 + 0 < kt) v[i].x = src[0];
+              if (q4 + 1 < kt) v[i].y = src[1];
+              if (q4 + 2 < kt) v[i].z = src[2];
+              if (q4 + 3 < kt) v[i].w = src[3];
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kLtBlock;
+          if (e < n4) *(float4 *)&Rw[e * 4] = v[i];
+        }
+      }
     }
+    // column tables: leaf codes and leaf occurrences before each column, tree
+    // list position of each column, children of each tree code
     const uint32_t obase = n1 > ni ? oo[ni] : 0u;
-    for (uint32_t i = ni + threadIdx.x; i < n1; i += kLpBlock) {
+    for (uint32_t i = ni + threadIdx.x; i < n1; i += kLtBlock) {
       const int64_t cc = col[i], cp = i > ni ? (int64_t)col[i - 1] : -1;
       if (cp < cc) {
         const uint32_t os = oo[i] - obase;
@@ -850,148 +894,216 @@ __global__ __launch_bounds__(kLpBlock) void left_pull_kernel(
     {
       const int64_t last = n1 > ni ? (int64_t)col[n1 - 1] : -1;
       const uint32_t oend = n1 > ni ? oo[n1] - obase : 0u;
-      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLpBlock) {
+      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLtBlock) {
         Loff[j] = n1;
         Ost[j] = oend;
       }
     }
-    for (uint32_t t = threadIdx.x; t < n_tree; t += kLpBlock) {
+    for (uint32_t t = threadIdx.x; t < n_tree; t += kLtBlock) {
       const int64_t cc = col[tl[t]], cp = t > 0 ? (int64_t)col[tl[t - 1]] : -1;
       for (int64_t j = cp + 1; j <= cc; ++j) Toff[j] = t;
     }
     {
       const int64_t last = n_tree > 0 ? (int64_t)col[tl[n_tree - 1]] : -1;
-      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLpBlock) Toff[j] = n_tree;
+      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLtBlock) Toff[j] = n_tree;
     }
-    for (uint32_t c = n1 + threadIdx.x; c < nc; c += kLpBlock) {
+    for (uint32_t c = n1 + threadIdx.x; c < nc; c += kLtBlock) {
       const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
       for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
     }
     {
       const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
-      for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kLpBlock) Coff[h] = nc;
+      for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = nc;
     }
     __syncthreads();
-    // column ranges of the waves, balanced by leaf occurrences
-    if (threadIdx.x <= kLpWaves) {
-      const uint32_t w = threadIdx.x, total = Ost[m];
-      uint32_t j;
-      if (w == 0) j = 0;
-      else if (w == kLpWaves) j = m;
-      else {
-        const uint32_t target = (uint32_t)(((uint64_t)total * w) / kLpWaves);
-        uint32_t lo = 0, hi = (uint32_t)m;
-        while (lo < hi) {
-          const uint32_t mid = (lo + hi) / 2;
-          if (Ost[mid] < target) lo = mid + 1;
-          else hi = mid;
-        }
-        j = lo;
-      }
-      jsplit[w] = j;
-    }
-    __syncthreads();
-    // tree codes, deepest level first
+    // tree codes, deepest level first; a group per code
+    auto tree_row = [&](uint32_t h) -> float * {
+      return TREE_LDS ? Rw + (size_t)(trow0 + h) * TW : Hg + (int64_t)h * TW;
+    };
+    const int gidx = wave * GPW + grp;
     for (int d = bt.n_levels; d >= 1; --d) {
-      const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
-      for (uint32_t c = a + wave; c < e; c += kLpWaves) {
+      const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+      for (uint32_t c = a + gidx; c < e; c += kLtWaves * GPW) {
         const uint32_t h = hrow(c);
-        float2 s = zero2;
-        for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) {
-          if (lane_on) {
-            const float2 g = *(const float2 *)&Gt[(orow[o] & ~kFirstOcc) * tw + qq];
-            s.x += g.x;
-            s.y += g.y;
-          }
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        const uint32_t o1 = oo[c + 1];
+        for (uint32_t o = oo[c]; o < o1; ++o) {
+          const float4 g = *(const float4 *)&Rw[(orow[o] & ~kFirstOcc) * TW + q];
+          acc.x += g.x;
+          acc.y += g.y;
+          acc.z += g.z;
+          acc.w += g.w;
         }
-        for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) {
-          if (lane_on) {
-            const float2 g = *(const float2 *)&Ht[(int64_t)hrow(ch) * tw + qq];
-            s.x += g.x;
-            s.y += g.y;
-          }
+        const uint32_t c1 = Coff[h + 1];
+        for (uint32_t ch = Coff[h]; ch < c1; ++ch) {
+          const float4 g = *(const float4 *)&tree_row(hrow(ch))[q];
+          acc.x += g.x;
+          acc.y += g.y;
+          acc.z += g.z;
+          acc.w += g.w;
         }
-        if (lane_on) *(float2 *)&Ht[(int64_t)h * tw + qq] = s;
+        *(float4 *)&tree_row(h)[q] = acc;
       }
       __syncthreads();
     }
-    // leaf stream, one column range per wave
-    const uint32_t J0 = jsplit[wave], J1 = jsplit[wave + 1];
-    float *ob = out + (b * m) * ldo + k0 + qq;
-    auto flush = [&](uint32_t j, float2 acc) {
-      for (uint32_t t = Toff[j]; t < Toff[j + 1]; ++t) {
-        const uint32_t c = tl[t];
-        const float v = val[c];
-        if (lane_on) {
-          const float2 h = *(const float2 *)&Ht[(int64_t)hrow(c) * tw + qq];
-          acc.x = fmaf(v, h.x, acc.x);
-          acc.y = fmaf(v, h.y, acc.y);
+    // output columns
+    auto grab = [&]() -> int {
+      uint32_t g = 0;
+      if (lane == 0) g = atomicAdd(&cg_next[parity], 1u);
+      return __builtin_amdgcn_readfirstlane((int)g);
+    };
+    auto wave_max = [&](uint32_t v) -> uint32_t {
+#pragma unroll
+      for (int o = LPG; o < kWave; o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+      return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+    };
+    // column j of group g of column group cg; past the last column: no entries
+    struct ColSpan { uint32_t ost, nl, nt, tof, lcode; };
+    auto col_of = [&](int cg) -> ColSpan {
+      const int j = min(cg * GPW + grp, m);
+      const int j1 = min(j + 1, m);
+      ColSpan c;
+      c.ost = Ost[j];
+      c.nl = Ost[j1] - c.ost;
+      c.tof = Toff[j];
+      c.nt = Toff[j1] - c.tof;
+      c.lcode = Loff[j];
+      return c;
+    };
+    // load stage: column group lcg, entries [lj, lj + CH) of each column
+    int lcg = wave, ncg = n_cg;
+    uint32_t lj = 0, lmax = 0;
+    ColSpan lc{0u, 0u, 0u, 0u, 0u};
+    if (lcg < n_cg) {
+      lc = col_of(lcg);
+      lmax = wave_max(lc.nl + lc.nt);
+      ncg = grab();
+    }
+    auto chunk_of_l = [&]() -> LtChunk {
+      const uint32_t n = lmax > lj ? min((uint32_t)CH, lmax - lj) : 0u;
+      return LtChunk{lcg, (n + 3u) & ~3u, lj, lj + CH >= lmax};
+    };
+    auto advance = [&]() {
+      if (lcg < n_cg) {
+        lj += CH;
+        if (lj >= lmax) {
+          lcg = ncg;
+          lj = 0;
+          lmax = 0u;
+          if (lcg < n_cg) {
+            lc = col_of(lcg);
+            lmax = wave_max(lc.nl + lc.nt);
+            ncg = grab();
+          }
         }
       }
-      float *p = ob + (int64_t)j * ldo;
-      if (qq < kt) p[0] = accumulate ? p[0] + acc.x : acc.x;
-      if (qq + 1 < kt) p[1] = accumulate ? p[1] + acc.y : acc.y;
     };
-    uint32_t cur = J0;
-    float2 acc = zero2;
-    if (J0 < J1) {
-      const uint32_t fend = Ost[J1];
-      uint32_t prev_code = Loff[J0] - 1;    // code of the entry before the stream
-      // chunk i is computed while chunk i+1's codes are gathered and chunk i+2's
-      // rows load
-      auto load_rows = [&](uint32_t f) -> uint32_t {
-        return f + lane < fend ? orow[obase + f + lane] : 0u;
-      };
-      uint32_t n_roff = 0, n_v = 0, n_cc = 0xFFFFFFFFu, n_n = 0;
-      auto decode_chunk = [&](uint32_t f, uint32_t w) {
-        const bool ok = f + lane < fend;
-        const uint64_t firsts = __ballot(ok && (w & kFirstOcc));
-        const uint32_t code = prev_code + (uint32_t)__popcll(firsts & (~0ull >> (63 - lane)));
-        prev_code += (uint32_t)__popcll(firsts);
-        n_roff = (w & ~kFirstOcc) * (uint32_t)tw * 4u;
-        n_v = ok ? __float_as_uint(val[code]) : 0u;
-        n_cc = ok ? col[code] : 0xFFFFFFFFu;
-        n_n = f < fend ? min((uint32_t)kWave, fend - f) : 0u;
-      };
-      uint32_t f0 = Ost[J0];
-      decode_chunk(f0, load_rows(f0));
-      uint32_t w_next = load_rows(f0 + kWave);
-      for (; f0 < fend; f0 += kWave) {
-        const uint32_t roff = n_roff, v = n_v, cc = n_cc, n = n_n;
-        if (f0 + kWave < fend) decode_chunk(f0 + kWave, w_next);
-        w_next = load_rows(f0 + 2 * kWave);
-        const uint32_t cprev = (uint32_t)__shfl_up((int)cc, 1, kWave);
-        const uint64_t bnd = __ballot((uint32_t)lane < n && (lane == 0 || cc != cprev));
-        for (uint32_t i0 = 0; i0 < n; i0 += 8) {
-          float2 x[8];
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const uint32_t ro = rdlane(roff, i0 + i);
-            x[i] = lane_on ? *(const float2 *)((const char *)Gt + ro + qq * 4) : zero2;
+    const BufRes rs_node = node_res(node, nc);
+    const uint32_t *dummy = lvl;   // a valid address for lanes without an entry
+    // L: the entry word of each lane (occ_row word of a leaf occurrence, or the
+    // code of a tree entry) and its kind: 0 leaf, 1 tree, 2 none
+    auto load_entry = [&](uint32_t &w, uint32_t &kind, uint32_t &lcode) {
+      const uint32_t e = lj + (uint32_t)sub;
+      const bool live = lcg < n_cg;
+      kind = !live || e >= lc.nl + lc.nt ? 2u : (e < lc.nl ? 0u : 1u);
+      const uint32_t *p = kind == 0u ? orow + obase + lc.ost + e
+                                     : (kind == 1u ? tl + lc.tof + (e - lc.nl) : dummy);
+      w = *p;
+      lcode = lc.lcode;
+    };
+    auto row_f4 = [&](uint32_t r) -> float4 {
+      if (TREE_LDS) return *(const float4 *)(lds + qb + r * RB);
+      const bool g = (r & kRtGlobal) != 0;
+      const float4 xl = *(const float4 *)(lds + qb + (g ? zrow : r) * RB);
+      float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
+      return g ? xg : xl;
+    };
+    const uint32_t gmask = LPG == 32 ? 0xFFFFFFFFu : ((1u << LPG) - 1u);
+    uint32_t gcode = 0;   // leaf code of the last occurrence translated in this column
+    LtChunk G = chunk_of_l();
+    LtChunk C{n_cg, 0u, 0u, false};
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto step = [&](uint32_t gw, uint32_t gkind, uint32_t glcode, uint32_t &lw, uint32_t &lkind,
+                    uint32_t &llcode) {
+      advance();
+      // G: codes of the chunk loaded a step ago, then their key pairs
+      const uint64_t firsts = __ballot(gkind == 0u && (gw & kFirstOcc));
+      const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
+      const uint32_t base = G.first == 0u ? glcode - 1u : gcode;
+      uint32_t code, row;
+      if (gkind == 0u) {
+        code = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
+        row = gw & ~kFirstOcc;
+      } else if (gkind == 1u) {
+        code = gw;
+        row = TREE_LDS ? trow0 + hrow(gw) : (kRtGlobal | hrow(gw));
+      } else {
+        code = 0xFFFFFFFFu;
+        row = zrow;
+      }
+      gcode = base + (uint32_t)__popc(gb);
+      const uint2 key = key_load(rs_node, code);
+      const LtChunk L = chunk_of_l();
+      load_entry(lw, lkind, llcode);
+      // C: the staged chunk
+      if (C.cg < n_cg) {
+        for (uint32_t t = 0; t < C.steps; t += 4) {
+          const uint2 e0 = stage[(t + 0) * GPW + grp], e1 = stage[(t + 1) * GPW + grp];
+          const uint2 e2 = stage[(t + 2) * GPW + grp], e3 = stage[(t + 3) * GPW + grp];
+          float4 x0, x1, x2, x3;
+          if (!TREE_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
+            x0 = row_f4(e0.x);
+            x1 = row_f4(e1.x);
+            x2 = row_f4(e2.x);
+            x3 = row_f4(e3.x);
+          } else {
+            x0 = *(const float4 *)(lds + qb + e0.x * RB);
+            x1 = *(const float4 *)(lds + qb + e1.x * RB);
+            x2 = *(const float4 *)(lds + qb + e2.x * RB);
+            x3 = *(const float4 *)(lds + qb + e3.x * RB);
           }
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            if (i0 + i < n) {
-              if ((bnd >> (i0 + i)) & 1) {
-                const uint32_t cj = rdlane(cc, i0 + i);
-                while (cur < cj) {
-                  flush(cur, acc);
-                  acc = zero2;
-                  ++cur;
-                }
-              }
-              const float vv = __uint_as_float(rdlane(v, i0 + i));
-              acc.x = fmaf(vv, x[i].x, acc.x);
-              acc.y = fmaf(vv, x[i].y, acc.y);
+          acc = f4fma(__uint_as_float(e0.y), x0, acc);
+          acc = f4fma(__uint_as_float(e1.y), x1, acc);
+          acc = f4fma(__uint_as_float(e2.y), x2, acc);
+          acc = f4fma(__uint_as_float(e3.y), x3, acc);
+        }
+        if (C.last) {
+          const int j = C.cg * GPW + grp;
+          if (j < m) {
+            float *o = out + (b * m + j) * ldo + k0 + q;
+            if (accumulate) {
+              if (q + 0 < kt) acc.x += o[0];
+              if (q + 1 < kt) acc.y += o[1];
+              if (q + 2 < kt) acc.z += o[2];
+              if (q + 3 < kt) acc.w += o[3];
+            }
+            if (q + 3 < kt) {
+              o[0] = acc.x;
+              o[1] = acc.y;
+              o[2] = acc.z;
+              o[3] = acc.w;
+            } else {
+              if (q + 0 < kt) o[0] = acc.x;
+              if (q + 1 < kt) o[1] = acc.y;
+              if (q + 2 < kt) o[2] = acc.z;
             }
           }
+          acc = make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
-    }
-    while (cur < J1) {
-      flush(cur, acc);
-      acc = zero2;
-      ++cur;
+      // S: entry sub of column grp goes to stage[sub * GPW + grp]
+      stage[sub * GPW + grp] = make_uint2(row, gkind == 2u ? 0u : key.y);
+      __builtin_amdgcn_wave_barrier();
+      C = G;
+      G = L;
+    };
+    uint32_t wA, kA, cA, wB, kB, cB;
+    load_entry(wA, kA, cA);
+    while (G.cg < n_cg || C.cg < n_cg) {
+      step(wA, kA, cA, wB, kB, cB);
+      if (!(G.cg < n_cg || C.cg < n_cg)) break;
+      step(wB, kB, cB, wA, kA, cA);
     }
   }
 }
@@ -1183,28 +1295,24 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
       p.ws_floats = p.deep_lds ? 0 : (int64_t)p.grid * d->max_deep * kRtKT;
       return p;
     }
-  } else {
-    // tile widths are multiples of 32 columns, so tiles of G rows and out rows
-    // start on 128-byte boundaries; the widest that fits LDS is taken
-    int tw = 0;
-    size_t lds = 0;
-    for (int cand = std::min(kLpMaxTW, (k + 31) / 32 * 32); cand >= 32; cand -= 32) {
-      lds = ((size_t)d->max_rows * cand + 3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) * 4;
-      if (lds <= kLdsMax - 256) {
-        tw = cand;
-        break;
-      }
-    }
-    const int n_tiles = tw ? (k + tw - 1) / tw : 1;
-    if (k >= 2 && tw > 0) {
+  } else if (k >= 2) {
+    // widest tile first; tree rows in LDS when they fit, else in the workspace
+    const size_t lds_max = kLdsMax - kLtStaticBytes;
+    for (int tw : {64, 32}) {
+      const size_t stage = tw == 64 ? lt_stage_bytes<64>() : lt_stage_bytes<32>();
+      const size_t head = (stage + 4 * (3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) + 15) & ~(size_t)15;
+      const size_t rows = ((size_t)d->max_rows + 1) * tw * 4;
+      if (head + rows > lds_max) continue;
       p.path = kPathTiled;
-      p.n_tiles = n_tiles;
       p.tw = tw;
-      p.lds = lds;
-      p.spx = std::max(1, kCuPerXcd / p.n_tiles);
-      p.grid = (unsigned)(kXcd * p.spx * p.n_tiles);
-      p.row_floats = tw;
-      p.ws_floats = (int64_t)p.grid * d->max_tree * tw;
+      p.n_tiles = (k + tw - 1) / tw;
+      p.deep_lds = head + rows + (size_t)d->max_tree * tw * 4 <= lds_max;
+      p.lds = head + rows + (p.deep_lds ? (size_t)d->max_tree * tw * 4 : 0);
+      const int64_t items = (d->info.n_batches + kXcd - 1) / kXcd * p.n_tiles;
+      p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
+      p.grid = (unsigned)(kXcd * p.spx);
+      p.row_floats = p.deep_lds ? 0 : tw;
+      p.ws_floats = p.deep_lds ? 0 : (int64_t)p.grid * d->max_tree * tw;
       return p;
     }
   }
@@ -1469,16 +1577,27 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     if (plan.ws_floats > 0 && (!ws || ws_bytes < (size_t)plan.ws_floats * 4))
       return fail(TOC_ESIZE, "workspace of %zu bytes below the %lld needed", ws_bytes,
                   (long long)plan.ws_floats * 4);
-    if ((st = allow_lds(left_pull_kernel<0>, plan.lds))) return st;
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
     const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
-    hipLaunchKernelGGL(left_pull_kernel<0>, dim3(plan.grid), dim3(kLpBlock), plan.lds, s, im,
-                       occ_off, occ_row, tlist, nb, plan.n_tiles, plan.spx, plan.tw,
-                       d->max_rows, m, G, ldg, k, out, ldo, accumulate, (float *)ws,
-                       (int64_t)d->max_tree * plan.tw);
-    return launch_status("left_pull_kernel");
+    const int64_t slot = plan.deep_lds ? 0 : (int64_t)d->max_tree * plan.tw;
+#define TOC_LT_LAUNCH(TW, TL)                                                                  \
+  do {                                                                                         \
+    if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
+    hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
+                       im, occ_off, occ_row, tlist, nb, plan.n_tiles, plan.spx, d->max_rows,      \
+                       (int)d->max_tree, m, G, ldg, k, out, ldo, accumulate, (float *)ws, slot);  \
+  } while (0)
+    if (plan.tw == 64) {
+      if (plan.deep_lds) TOC_LT_LAUNCH(64, true);
+      else TOC_LT_LAUNCH(64, false);
+    } else {
+      if (plan.deep_lds) TOC_LT_LAUNCH(32, true);
+      else TOC_LT_LAUNCH(32, false);
+    }
+#undef TOC_LT_LAUNCH
+    return launch_status("left_tiled_kernel");
   }
   int64_t cap_rows = 0;
   if ((st = ws_capacity(plan, ws, ws_bytes, cap_rows))) return st;
