@@ -445,6 +445,20 @@ __device__ inline uint2 key_load(BufRes r, uint32_t c) {
 
 __device__ inline uint4 node_load(const toc_node *n, int64_t c) { return *(const uint4 *)(n + c); }
 
+// LDS reads through address-space-3 pointers (byte addresses in LDS): the
+// compiler never merges such a read with a global one into a flat access.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) f32x4 lds_f32x4;
+
+__device__ inline uint32_t lds_base(float4 *smem) {
+  return (uint32_t)(size_t)(__attribute__((address_space(3))) float4 *)smem;
+}
+
+__device__ inline float4 lds_load4(uint32_t byte) {
+  const f32x4 v = *(const lds_f32x4 *)(size_t)byte;
+  return make_float4(v[0], v[1], v[2], v[3]);
+}
+
 // ---------------------------------------------------------------------------
 // Right multiplication (Theorem 1, Algorithm 7), tiled over the columns of W.
 // Work items are (batch, 32-column tile) pairs.  The items of one batch are
@@ -488,7 +502,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
   __shared__ uint32_t tg_next[2];                             // next free tuple group, by item parity
   uint2 *stage = (uint2 *)lds + wave * (kRtChunk * kRtGroups);
   float *Wt = (float *)(lds + kRtStageBytes);                 // (m + 1) x kRtKT, then deep rows
-  const uint32_t qb = kRtStageBytes + 4u * (uint32_t)q;       // byte offset of this lane's columns
+  const uint32_t qb = lds_base(smem4) + kRtStageBytes + 4u * (uint32_t)q;   // LDS address of this lane's columns
   const uint32_t zrow = (uint32_t)m;
   float *Hg = ws + blockIdx.x * slot_floats;
   for (int e = threadIdx.x; e < kRtKT; e += kRtBlock) Wt[m * kRtKT + e] = 0.0f;
@@ -651,9 +665,9 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // an H row in LDS or in the workspace; both loads are issued and the values
     // selected (a select of the two pointers would make a flat pointer)
     auto row_f4 = [&](uint32_t r) -> float4 {
-      if (DEEP_LDS) return *(const float4 *)(lds + qb + r * (kRtKT * 4));
+      if (DEEP_LDS) return lds_load4(qb + r * (kRtKT * 4));
       const bool g = (r & kRtGlobal) != 0;
-      const float4 xl = *(const float4 *)(lds + qb + (g ? zrow : r) * (kRtKT * 4));
+      const float4 xl = lds_load4(qb + (g ? zrow : r) * (kRtKT * 4));
       float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
       if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * kRtKT + q];
       return g ? xg : xl;
@@ -689,7 +703,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
             float4 xr[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
-              xr[t] = *(const float4 *)(lds + qb + e[h + t].x * (kRtKT * 4));
+              xr[t] = lds_load4(qb + e[h + t].x * (kRtKT * 4));
 #pragma unroll
             for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[h + t].y), xr[t], acc);
             __builtin_amdgcn_sched_barrier(0);
@@ -708,10 +722,10 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
             x2 = row_f4(e2.x);
             x3 = row_f4(e3.x);
           } else {
-            x0 = *(const float4 *)(lds + qb + e0.x * (kRtKT * 4));
-            x1 = *(const float4 *)(lds + qb + e1.x * (kRtKT * 4));
-            x2 = *(const float4 *)(lds + qb + e2.x * (kRtKT * 4));
-            x3 = *(const float4 *)(lds + qb + e3.x * (kRtKT * 4));
+            x0 = lds_load4(qb + e0.x * (kRtKT * 4));
+            x1 = lds_load4(qb + e1.x * (kRtKT * 4));
+            x2 = lds_load4(qb + e2.x * (kRtKT * 4));
+            x3 = lds_load4(qb + e3.x * (kRtKT * 4));
           }
           acc = f4fma(__uint_as_float(e0.y), x0, acc);
           acc = f4fma(__uint_as_float(e1.y), x1, acc);
@@ -818,7 +832,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   uint32_t *Coff = Toff + (m + 1);
   const uint32_t rows_b = (uint32_t)((lt_stage_bytes<TW>() + 4u * (3u * (m + 1) + max_tree + 1) + 15u) & ~15u);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
-  const uint32_t qb = rows_b + 4u * (uint32_t)q;
+  const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   const uint32_t zrow = (uint32_t)max_rows;
   const uint32_t trow0 = zrow + 1u;
   float *Hg = ws + blockIdx.x * slot_floats;
@@ -1012,9 +1026,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       lcode = lc.lcode;
     };
     auto row_f4 = [&](uint32_t r) -> float4 {
-      if (TREE_LDS) return *(const float4 *)(lds + qb + r * RB);
+      if (TREE_LDS) return lds_load4(qb + r * RB);
       const bool g = (r & kRtGlobal) != 0;
-      const float4 xl = *(const float4 *)(lds + qb + (g ? zrow : r) * RB);
+      const float4 xl = lds_load4(qb + (g ? zrow : r) * RB);
       float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
       if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
       return g ? xg : xl;
@@ -1058,10 +1072,10 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
             x2 = row_f4(e2.x);
             x3 = row_f4(e3.x);
           } else {
-            x0 = *(const float4 *)(lds + qb + e0.x * RB);
-            x1 = *(const float4 *)(lds + qb + e1.x * RB);
-            x2 = *(const float4 *)(lds + qb + e2.x * RB);
-            x3 = *(const float4 *)(lds + qb + e3.x * RB);
+            x0 = lds_load4(qb + e0.x * RB);
+            x1 = lds_load4(qb + e1.x * RB);
+            x2 = lds_load4(qb + e2.x * RB);
+            x3 = lds_load4(qb + e3.x * RB);
           }
           acc = f4fma(__uint_as_float(e0.y), x0, acc);
           acc = f4fma(__uint_as_float(e1.y), x1, acc);
