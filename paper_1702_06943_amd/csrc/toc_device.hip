@@ -805,6 +805,7 @@ struct LtChunk {
   uint32_t steps;   // entries per column to process, rounded up to a multiple of 4
   uint32_t first;   // first entry of the chunk (0: a column starts)
   bool last;        // last chunk of the column group
+  bool tree;        // the chunk holds tree entries
 };
 
 template <int TW, bool TREE_LDS>
@@ -995,7 +996,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     }
     auto chunk_of_l = [&]() -> LtChunk {
       const uint32_t n = lmax > lj ? min((uint32_t)CH, lmax - lj) : 0u;
-      return LtChunk{lcg, (n + 3u) & ~3u, lj, lj + CH >= lmax};
+      const bool tree = __ballot(lj + (uint32_t)sub >= lc.nl && lj + (uint32_t)sub < lc.nl + lc.nt) != 0;
+      return LtChunk{lcg, (n + 3u) & ~3u, lj, lj + CH >= lmax, tree};
     };
     auto advance = [&]() {
       if (lcg < n_cg) {
@@ -1036,7 +1038,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const uint32_t gmask = LPG == 32 ? 0xFFFFFFFFu : ((1u << LPG) - 1u);
     uint32_t gcode = 0;   // leaf code of the last occurrence translated in this column
     LtChunk G = chunk_of_l();
-    LtChunk C{n_cg, 0u, 0u, false};
+    LtChunk C{n_cg, 0u, 0u, false, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     auto step = [&](uint32_t gw, uint32_t gkind, uint32_t glcode, uint32_t &lw, uint32_t &lkind,
                     uint32_t &llcode) {
@@ -1045,28 +1047,36 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       const uint64_t firsts = __ballot(gkind == 0u && (gw & kFirstOcc));
       const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
       const uint32_t base = G.first == 0u ? glcode - 1u : gcode;
-      uint32_t code, row;
-      if (gkind == 0u) {
-        code = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
-        row = gw & ~kFirstOcc;
-      } else if (gkind == 1u) {
-        code = gw;
-        row = TREE_LDS ? trow0 + hrow(gw) : (kRtGlobal | hrow(gw));
-      } else {
-        code = 0xFFFFFFFFu;
-        row = zrow;
-      }
+      // branch-free: leaf, tree or no entry
+      const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
+      const uint32_t trow = TREE_LDS ? trow0 + hrow(gw) : (kRtGlobal | hrow(gw));
+      const uint32_t code = gkind == 0u ? lcode : (gkind == 1u ? gw : 0xFFFFFFFFu);
+      const uint32_t row = gkind == 0u ? (gw & ~kFirstOcc) : (gkind == 1u ? trow : zrow);
       gcode = base + (uint32_t)__popc(gb);
       const uint2 key = key_load(rs_node, code);
       const LtChunk L = chunk_of_l();
       load_entry(lw, lkind, llcode);
-      // C: the staged chunk
-      if (C.cg < n_cg) {
+      // C: the staged chunk; a full chunk of leaf entries reads only LDS rows, 8
+      // of them issued back to back
+      if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
+#pragma unroll
+        for (int h = 0; h < CH; h += 8) {
+          uint2 e[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) e[t] = stage[(h + t) * GPW + grp];
+          float4 xr[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) xr[t] = lds_load4(qb + e[t].x * RB);
+#pragma unroll
+          for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[t].y), xr[t], acc);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      } else if (C.cg < n_cg) {
         for (uint32_t t = 0; t < C.steps; t += 4) {
           const uint2 e0 = stage[(t + 0) * GPW + grp], e1 = stage[(t + 1) * GPW + grp];
           const uint2 e2 = stage[(t + 2) * GPW + grp], e3 = stage[(t + 3) * GPW + grp];
           float4 x0, x1, x2, x3;
-          if (!TREE_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
+          if (C.tree) {
             x0 = row_f4(e0.x);
             x1 = row_f4(e1.x);
             x2 = row_f4(e2.x);
@@ -1082,6 +1092,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           acc = f4fma(__uint_as_float(e2.y), x2, acc);
           acc = f4fma(__uint_as_float(e3.y), x3, acc);
         }
+      }
+      if (C.cg < n_cg) {
         if (C.last) {
           const int j = C.cg * GPW + grp;
           if (j < m) {
