@@ -795,10 +795,19 @@ constexpr int kLtBlock = 1024;
 constexpr int kLtWaves = kLtBlock / kWave;
 constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
+constexpr int kLtBuckets = 256;                   // columns are bucketed by chunk count
 
 // LDS bytes of the per-wave stages and of the column tables
 template <int TW>
 constexpr uint32_t lt_stage_bytes() { return (uint32_t)kLtWaves * (TW / 4) * (kWave / (TW / 4)) * 8; }
+
+// LDS byte offset of the rows: stages, then the tables Loff, Ost, Toff (m + 1
+// each), Coff (max_tree + 1), Ord (m) and the bucket counters
+template <int TW>
+constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree) {
+  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (3 * (m + 1) + max_tree + 1 + m + kLtBuckets + 1) + 15) &
+                    ~(int64_t)15);
+}
 
 struct LtChunk {
   int cg;           // column group (columns GPW*cg .. GPW*cg+GPW-1); >= n_cg: none
@@ -831,7 +840,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   uint32_t *Ost = Loff + (m + 1);
   uint32_t *Toff = Ost + (m + 1);
   uint32_t *Coff = Toff + (m + 1);
-  const uint32_t rows_b = (uint32_t)((lt_stage_bytes<TW>() + 4u * (3u * (m + 1) + max_tree + 1) + 15u) & ~15u);
+  uint32_t *Ord = Coff + (max_tree + 1);      // m: columns by decreasing chunk count
+  uint32_t *Hist = Ord + m;                   // kLtBuckets + 1 bucket counters
+  const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   const uint32_t zrow = (uint32_t)max_rows;
@@ -930,6 +941,33 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
       for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = nc;
     }
+    for (int t = threadIdx.x; t <= kLtBuckets; t += kLtBlock) Hist[t] = 0u;
+    __syncthreads();
+    // columns ordered by decreasing number of chunks (a counting sort over
+    // buckets), so that the columns of a wave need about as many steps
+    auto bucket_of = [&](int j) -> uint32_t {
+      const uint32_t n = (Ost[j + 1] - Ost[j]) + (Toff[j + 1] - Toff[j]);
+      return (uint32_t)(kLtBuckets - 1) - min((n + CH - 1) / CH, (uint32_t)(kLtBuckets - 1));
+    };
+    for (int j = threadIdx.x; j < m; j += kLtBlock) atomicAdd(&Hist[bucket_of(j)], 1u);
+    __syncthreads();
+    if (wave == 0) {
+      constexpr int per = kLtBuckets / kWave;
+      uint32_t v[per], t = 0;
+#pragma unroll
+      for (int u = 0; u < per; ++u) {
+        v[u] = Hist[lane * per + u];
+        t += v[u];
+      }
+      uint32_t run = wave_incl_scan(t, lane) - t;
+#pragma unroll
+      for (int u = 0; u < per; ++u) {
+        Hist[lane * per + u] = run;
+        run += v[u];
+      }
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < m; j += kLtBlock) Ord[atomicAdd(&Hist[bucket_of(j)], 1u)] = (uint32_t)j;
     __syncthreads();
     // tree codes, deepest level first; a group per code
     auto tree_row = [&](uint32_t h) -> float * {
@@ -975,7 +1013,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     // column j of group g of column group cg; past the last column: no entries
     struct ColSpan { uint32_t ost, nl, nt, tof, lcode; };
     auto col_of = [&](int cg) -> ColSpan {
-      const int j = min(cg * GPW + grp, m);
+      const int o = cg * GPW + grp;
+      const int j = o < m ? (int)Ord[o] : m;
       const int j1 = min(j + 1, m);
       ColSpan c;
       c.ost = Ost[j];
@@ -1095,8 +1134,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       }
       if (C.cg < n_cg) {
         if (C.last) {
-          const int j = C.cg * GPW + grp;
-          if (j < m) {
+          const int o = C.cg * GPW + grp;
+          if (o < m) {
+            const int j = (int)Ord[o];
             float *o = out + (b * m + j) * ldo + k0 + q;
             if (accumulate) {
               if (q + 0 < kt) acc.x += o[0];
@@ -1325,8 +1365,7 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
     // widest tile first; tree rows in LDS when they fit, else in the workspace
     const size_t lds_max = kLdsMax - kLtStaticBytes;
     for (int tw : {64, 32}) {
-      const size_t stage = tw == 64 ? lt_stage_bytes<64>() : lt_stage_bytes<32>();
-      const size_t head = (stage + 4 * (3 * ((size_t)m + 1) + (size_t)d->max_tree + 1) + 15) & ~(size_t)15;
+      const size_t head = tw == 64 ? lt_rows_offset<64>(m, d->max_tree) : lt_rows_offset<32>(m, d->max_tree);
       const size_t rows = ((size_t)d->max_rows + 1) * tw * 4;
       if (head + rows > lds_max) continue;
       p.path = kPathTiled;
