@@ -163,6 +163,15 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   dtiles  : uint32 x 4 per run of 1024 entries of D (at least one per batch):
  *             batch, first entry, pairs of the batch before that entry, first
  *             row whose span starts at or after that entry
+ *   cols    : uint32 per batch 4 (n_cols+1) entries (at b * 4 (n_cols+1)): for each
+ *             column j = 0..n_cols, the first depth-1 code without children whose
+ *             key column is >= j, the occurrences (occ_row entries) of such codes
+ *             before it, and the first tlist entry of key column >= j; then the
+ *             columns ordered by number of such occurrences plus tree codes, most
+ *             first (n_cols entries and one unused)
+ *   tchild  : uint32 per batch n_tree+1 entries (at tree_base + b): the children of
+ *             tree code h (h counting the codes with children at depth 1, then
+ *             the codes of depth >= 2) are the codes tchild[h] .. tchild[h+1]-1
  * Depth-1 codes without children are sorted by key column; the codes of each
  * level d >= 2 are sorted by parent.                                             */
 typedef struct {
@@ -182,7 +191,8 @@ typedef struct {
 } toc_node;
 
 typedef struct {
-  int64_t batches, level, node, span, dcodes, occ_off, occ_row, tlist, dtiles, end;
+  int64_t batches, level, node, span, dcodes, occ_off, occ_row, tlist, dtiles, cols, tchild,
+      end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

@@ -49,7 +49,7 @@ class DevInfo(C.Structure):
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
                 ("batches", "level", "node", "span", "dcodes", "occ_off", "occ_row",
-                 "tlist", "dtiles", "end")]
+                 "tlist", "dtiles", "cols", "tchild", "end")]
 
 
 # one record of the image's node array (toc_node)

@@ -795,18 +795,16 @@ constexpr int kLtBlock = 1024;
 constexpr int kLtWaves = kLtBlock / kWave;
 constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
-constexpr int kLtBuckets = 256;                   // columns are bucketed by chunk count
 
 // LDS bytes of the per-wave stages and of the column tables
 template <int TW>
 constexpr uint32_t lt_stage_bytes() { return (uint32_t)kLtWaves * (TW / 4) * (kWave / (TW / 4)) * 8; }
 
-// LDS byte offset of the rows: stages, then the tables Loff, Ost, Toff (m + 1
-// each), Coff (max_tree + 1), Ord (m) and the bucket counters
+// LDS byte offset of the rows: stages, then the batch's column index (Loff, Ost,
+// Toff, Ord: m + 1 entries each, as in the image) and Coff (max_tree + 1)
 template <int TW>
 constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree) {
-  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (3 * (m + 1) + max_tree + 1 + m + kLtBuckets + 1) + 15) &
-                    ~(int64_t)15);
+  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (4 * (m + 1) + max_tree + 1) + 15) & ~(int64_t)15);
 }
 
 struct LtChunk {
@@ -820,7 +818,8 @@ struct LtChunk {
 template <int TW, bool TREE_LDS>
 __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, int64_t nb, int n_tiles, int spw, int max_rows,
+    const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
+    const uint32_t *__restrict__ tchild_all, int64_t nb, int n_tiles, int spw, int max_rows,
     int max_tree, int m, const float *__restrict__ G, int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
     int64_t slot_floats) {
@@ -834,14 +833,13 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const int grp = lane / LPG, sub = lane % LPG, q = 4 * sub;
-  // LDS: stages | Loff, Ost, Toff (m + 1 each) | Coff (max_tree + 1) | rows
+  // LDS: stages | Loff, Ost, Toff, Ord (m + 1 each) | Coff (max_tree + 1) | rows
   uint2 *stage = (uint2 *)lds + wave * (CH * GPW);
   uint32_t *Loff = (uint32_t *)(lds + lt_stage_bytes<TW>());
   uint32_t *Ost = Loff + (m + 1);
   uint32_t *Toff = Ost + (m + 1);
-  uint32_t *Coff = Toff + (m + 1);
-  uint32_t *Ord = Coff + (max_tree + 1);      // m: columns by decreasing chunk count
-  uint32_t *Hist = Ord + m;                   // kLtBuckets + 1 bucket counters
+  uint32_t *Ord = Toff + (m + 1);             // columns by decreasing number of entries
+  uint32_t *Coff = Ord + (m + 1);
   const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
@@ -904,70 +902,14 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
       }
     }
-    // column tables: leaf codes and leaf occurrences before each column, tree
-    // list position of each column, children of each tree code
+    // the batch's column index and children ranges, from the image
+    {
+      const uint4 *src = (const uint4 *)(cols_all + b * 4 * (int64_t)(m + 1));
+      for (int e = threadIdx.x; e < m + 1; e += kLtBlock) ((uint4 *)Loff)[e] = src[e];
+      const uint32_t *tch = tchild_all + bt.tree_base + b;
+      for (uint32_t h = threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = tch[h];
+    }
     const uint32_t obase = n1 > ni ? oo[ni] : 0u;
-    for (uint32_t i = ni + threadIdx.x; i < n1; i += kLtBlock) {
-      const int64_t cc = col[i], cp = i > ni ? (int64_t)col[i - 1] : -1;
-      if (cp < cc) {
-        const uint32_t os = oo[i] - obase;
-        for (int64_t j = cp + 1; j <= cc; ++j) {
-          Loff[j] = i;
-          Ost[j] = os;
-        }
-      }
-    }
-    {
-      const int64_t last = n1 > ni ? (int64_t)col[n1 - 1] : -1;
-      const uint32_t oend = n1 > ni ? oo[n1] - obase : 0u;
-      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLtBlock) {
-        Loff[j] = n1;
-        Ost[j] = oend;
-      }
-    }
-    for (uint32_t t = threadIdx.x; t < n_tree; t += kLtBlock) {
-      const int64_t cc = col[tl[t]], cp = t > 0 ? (int64_t)col[tl[t - 1]] : -1;
-      for (int64_t j = cp + 1; j <= cc; ++j) Toff[j] = t;
-    }
-    {
-      const int64_t last = n_tree > 0 ? (int64_t)col[tl[n_tree - 1]] : -1;
-      for (int64_t j = last + 1 + threadIdx.x; j <= m; j += kLtBlock) Toff[j] = n_tree;
-    }
-    for (uint32_t c = n1 + threadIdx.x; c < nc; c += kLtBlock) {
-      const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
-      for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
-    }
-    {
-      const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
-      for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = nc;
-    }
-    for (int t = threadIdx.x; t <= kLtBuckets; t += kLtBlock) Hist[t] = 0u;
-    __syncthreads();
-    // columns ordered by decreasing number of chunks (a counting sort over
-    // buckets), so that the columns of a wave need about as many steps
-    auto bucket_of = [&](int j) -> uint32_t {
-      const uint32_t n = (Ost[j + 1] - Ost[j]) + (Toff[j + 1] - Toff[j]);
-      return (uint32_t)(kLtBuckets - 1) - min((n + CH - 1) / CH, (uint32_t)(kLtBuckets - 1));
-    };
-    for (int j = threadIdx.x; j < m; j += kLtBlock) atomicAdd(&Hist[bucket_of(j)], 1u);
-    __syncthreads();
-    if (wave == 0) {
-      constexpr int per = kLtBuckets / kWave;
-      uint32_t v[per], t = 0;
-#pragma unroll
-      for (int u = 0; u < per; ++u) {
-        v[u] = Hist[lane * per + u];
-        t += v[u];
-      }
-      uint32_t run = wave_incl_scan(t, lane) - t;
-#pragma unroll
-      for (int u = 0; u < per; ++u) {
-        Hist[lane * per + u] = run;
-        run += v[u];
-      }
-    }
-    __syncthreads();
-    for (int j = threadIdx.x; j < m; j += kLtBlock) Ord[atomicAdd(&Hist[bucket_of(j)], 1u)] = (uint32_t)j;
     __syncthreads();
     // tree codes, deepest level first; a group per code
     auto tree_row = [&](uint32_t h) -> float * {
@@ -1646,12 +1588,15 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
     const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
+    const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
+    const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     const int64_t slot = plan.deep_lds ? 0 : (int64_t)d->max_tree * plan.tw;
 #define TOC_LT_LAUNCH(TW, TL)                                                                  \
   do {                                                                                         \
     if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
     hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
-                       im, occ_off, occ_row, tlist, nb, plan.n_tiles, plan.spx, d->max_rows,      \
+                       im, occ_off, occ_row, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,     \
+                       d->max_rows,                                                             \
                        (int)d->max_tree, m, G, ldg, k, out, ldo, accumulate, (float *)ws, slot);  \
   } while (0)
     if (plan.tw == 64) {

@@ -541,6 +541,46 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     if (c < n_int1 || c >= n1) S.keys.push_back(((uint64_t)node[c].col << 32) | (uint64_t)c);
   std::sort(S.keys.begin(), S.keys.end());
   for (size_t t = 0; t < S.keys.size(); ++t) tlist[t] = (uint32_t)S.keys[t];
+  const int64_t n_tree = (int64_t)S.keys.size();
+  // column index of the left multiplication (out row j sums over the codes of key
+  // column j): per column the first leaf code (depth 1, no children) of a column
+  // >= j, the leaf occurrences before it, the first tree-list entry of a column
+  // >= j, and the columns ordered by number of entries (leaf occurrences + tree
+  // codes), most first
+  {
+    const int64_t m = e->n_cols;
+    uint32_t *cx = (uint32_t *)(dst + L.cols) + (int64_t)b * 4 * (m + 1);
+    uint32_t *c_code = cx, *c_occ = cx + (m + 1), *c_tree = cx + 2 * (m + 1), *c_ord = cx + 3 * (m + 1);
+    int64_t i = n_int1, t = 0;
+    for (int64_t j = 0; j <= m; ++j) {
+      while (i < n1 && (int64_t)node[i].col < j) ++i;
+      while (t < n_tree && (int64_t)node[tlist[t]].col < j) ++t;
+      c_code[j] = (uint32_t)i;
+      c_occ[j] = occ_off[i] - occ_off[n_int1];
+      c_tree[j] = (uint32_t)t;
+    }
+    S.keys.clear();
+    for (int64_t j = 0; j < m; ++j) {
+      const uint64_t cnt = (uint64_t)(c_occ[j + 1] - c_occ[j]) + (c_tree[j + 1] - c_tree[j]);
+      S.keys.push_back(((0xFFFFFFFFull - cnt) << 32) | (uint64_t)j);
+    }
+    std::sort(S.keys.begin(), S.keys.end());
+    for (int64_t k = 0; k < m; ++k) c_ord[k] = (uint32_t)S.keys[k];
+    c_ord[m] = 0;
+  }
+  // children of each tree code (their H rows are added to its H in the left
+  // multiplication): code h's children are codes tchild[h] .. tchild[h+1]-1, h
+  // numbering the tree codes as in tlist's row order (depth-1 codes with children,
+  // then deeper codes)
+  {
+    uint32_t *tch = (uint32_t *)(dst + L.tchild) + bt.tree_base + b;
+    auto hrow = [&](uint32_t c) -> int64_t { return c < n_int1 ? c : (int64_t)c - n1 + n_int1; };
+    int64_t c = n1;
+    for (int64_t h = 0; h <= n_tree; ++h) {
+      while (c < n_codes && hrow(node[c].parent) < h) ++c;
+      tch[h] = (uint32_t)c;
+    }
+  }
   // decode tiles: for every kDecodeTile entries of D, the batch, the first entry,
   // the number of pairs before it in the batch and the first row starting in it
   {
@@ -634,6 +674,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.occ_row = off; off = align256(off + 4 * d);
   L.tlist = off;   off = align256(off + 4 * tree);
   L.dtiles = off;  off = align256(off + 16 * dtiles);
+  L.cols = off;    off = align256(off + 16 * n_batches * ((int64_t)std::max(n_cols, 0) + 1));
+  L.tchild = off;  off = align256(off + 4 * (tree + n_batches));
   dev->n_dtiles = dtiles;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;

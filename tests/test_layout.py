@@ -34,6 +34,9 @@ def read_image(dev, buf):
         occ_row=arr("occ_row", np.uint32, info["n_codes"]),
         tlist=arr("tlist", np.uint32,
                   int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0),
+        cols=arr("cols", np.uint32, nb * 4 * (info["n_cols"] + 1)),
+        tchild=arr("tchild", np.uint32,
+                   int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"] + 1).sum()) if nb else 0),
     )
     for f in ("parent", "col", "val", "depth"):
         img[f] = img["node"][f]
@@ -42,6 +45,7 @@ def read_image(dev, buf):
 
 def batch_view(img, b):
     t = img["bt"][b]
+    m = int(img["info"]["n_cols"])
     cb, nc = int(t["code_base"]), int(t["n_codes"])
     return dict(
         t=t,
@@ -54,6 +58,9 @@ def batch_view(img, b):
         occ_row=img["occ_row"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
         tlist=img["tlist"][int(t["tree_base"]):int(t["tree_base"]) + int(t["n_int1"]) + nc
                            - int(t["n_lvl1"])],
+        cols=img["cols"][b * 4 * (m + 1):(b + 1) * 4 * (m + 1)].reshape(4, m + 1),
+        tchild=img["tchild"][int(t["tree_base"]) + b:int(t["tree_base"]) + b + int(t["n_int1"]) + nc
+                             - int(t["n_lvl1"]) + 1],
     )
 
 
@@ -104,6 +111,31 @@ def check_invariants(v):
     tl = v["tlist"]
     assert sorted(tl.tolist()) == tree
     assert np.all(np.diff(v["col"][tl].astype(np.int64)) >= 0)
+    # column index: first leaf code, leaf occurrences before it and first tree-list
+    # entry of each column j; columns by entry count, most first (ties by column)
+    cx = v["cols"]
+    m = cx.shape[1] - 1
+    leaf_cols = v["col"][ni:n1].astype(np.int64)
+    tree_cols = v["col"][tl].astype(np.int64)
+    for j in range(m + 1):
+        lc = ni + int(np.sum(leaf_cols < j))
+        assert cx[0, j] == lc
+        assert cx[1, j] == oo[lc] - oo[ni]
+        assert cx[2, j] == int(np.sum(tree_cols < j))
+    cnt = [int(cx[1, j + 1] - cx[1, j] + cx[2, j + 1] - cx[2, j]) for j in range(m)]
+    want = sorted(range(m), key=lambda j: (-cnt[j], j))
+    assert cx[3, :m].tolist() == want
+    # leaf occurrences of column j: those of its leaf codes; tree codes of column j
+    for j in range(m):
+        codes = [c for c in range(ni, n1) if v["col"][c] == j]
+        assert sum(int(oo[c + 1] - oo[c]) for c in codes) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
+    # children ranges: tree code h's children are tchild[h] .. tchild[h+1]-1
+    hrow = lambda c: c if c < ni else c - n1 + ni
+    tch = v["tchild"]
+    assert len(tch) == len(tree) + 1
+    for h, c in enumerate(tree):
+        kids = [x for x in range(n1, nc) if v["parent"][x] == c]
+        assert kids == list(range(int(tch[hrow(c)]), int(tch[hrow(c) + 1])))
 
 
 def walk_decode(v):
