@@ -921,21 +921,36 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       for (uint32_t c = a + gidx; c < e; c += kLtWaves * GPW) {
         const uint32_t h = hrow(c);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        const uint32_t o1 = oo[c + 1];
-        for (uint32_t o = oo[c]; o < o1; ++o) {
-          const float4 g = *(const float4 *)&Rw[(orow[o] & ~kFirstOcc) * TW + q];
-          acc.x += g.x;
-          acc.y += g.y;
-          acc.z += g.z;
-          acc.w += g.w;
+        // occurrences: the group's lanes load up to LPG of their rows at once and
+        // pass them round with lane shuffles
+        const uint32_t o0 = oo[c], o1 = oo[c + 1];
+        for (uint32_t ob = o0; ob < o1; ob += LPG) {
+          const uint32_t mine = ob + sub < o1 ? orow[ob + sub] & ~kFirstOcc : zrow;
+          const uint32_t n = min((uint32_t)LPG, o1 - ob);
+          for (uint32_t i = 0; i < n; ++i) {
+            const uint32_t r = (uint32_t)__shfl((int)mine, grp * LPG + (int)i, kWave);
+            const float4 g = lds_load4(qb + r * RB);
+            acc.x += g.x;
+            acc.y += g.y;
+            acc.z += g.z;
+            acc.w += g.w;
+          }
         }
-        const uint32_t c1 = Coff[h + 1];
-        for (uint32_t ch = Coff[h]; ch < c1; ++ch) {
-          const float4 g = *(const float4 *)&tree_row(hrow(ch))[q];
-          acc.x += g.x;
-          acc.y += g.y;
-          acc.z += g.z;
-          acc.w += g.w;
+        // children: H rows, four loads in flight
+        const uint32_t c0 = Coff[h], c1 = Coff[h + 1];
+        for (uint32_t ch = c0; ch < c1; ch += 4) {
+          float4 g[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            g[u] = ch + u < c1 ? *(const float4 *)&tree_row(hrow(ch + u))[q]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            acc.x += g[u].x;
+            acc.y += g[u].y;
+            acc.z += g[u].z;
+            acc.w += g[u].w;
+          }
         }
         *(float4 *)&tree_row(h)[q] = acc;
       }
