@@ -150,8 +150,9 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  * precede the others.
  *   batches : toc_batch[n_batches]
  *   level   : uint32 per batch n_levels+1 entries (lvl_base)
- *   node    : toc_node of each code (16 bytes: key pair, parent, depth), so that a
- *             code's fields come with one 16-byte read
+ *   key     : toc_key of each code (its key pair, 8 bytes), so that a code's key
+ *             comes with one 8-byte read
+ *   link    : toc_link of each code (its parent and depth, 8 bytes)
  *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
  *   dcodes  : uint32 local code of each entry of D (d_base)
  *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b)
@@ -181,18 +182,21 @@ typedef struct {
   int32_t pad[2];
 } toc_batch;
 
-/* One node of the decoding tree C' (Algorithm 2): its key pair (section 3.1) and
- * its place in the tree. */
+/* A node of the decoding tree C' (Algorithm 2): its key pair (section 3.1) ... */
 typedef struct {
   uint32_t col;      /* key column                                               */
   float val;         /* key value                                                */
+} toc_key;
+
+/* ... and its place in the tree. */
+typedef struct {
   uint32_t parent;   /* local code of the parent; 0xFFFFFFFF at depth 1           */
   uint32_t depth;    /* length of the node's sequence                            */
-} toc_node;
+} toc_link;
 
 typedef struct {
-  int64_t batches, level, node, span, dcodes, occ_off, occ_row, tlist, dtiles, cols, tchild,
-      end;
+  int64_t batches, level, key, link, span, dcodes, occ_off, occ_row, tlist, dtiles, cols,
+      tchild, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

@@ -5,7 +5,7 @@ The functions are those of include/toc.h, called through ctypes; see binding.py.
 """
 
 from .binding import (  # noqa: F401
-    TocError, Enc, Dev, lib, LIB_PATH, BATCH_DTYPE, NODE_DTYPE,
+    TocError, Enc, Dev, lib, LIB_PATH, BATCH_DTYPE, KEY_DTYPE, LINK_DTYPE,
     TOC_UPLOAD_KEEP_DEAD, TOC_UPLOAD_HOST, TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE,
     TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED,
     toc_encode, toc_encode_batches, toc_enc_info_get, toc_enc_export,

@@ -48,12 +48,13 @@ class DevInfo(C.Structure):
 
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
-                ("batches", "level", "node", "span", "dcodes", "occ_off", "occ_row",
+                ("batches", "level", "key", "link", "span", "dcodes", "occ_off", "occ_row",
                  "tlist", "dtiles", "cols", "tchild", "end")]
 
 
-# one record of the image's node array (toc_node)
-NODE_DTYPE = np.dtype([("col", "<u4"), ("val", "<f4"), ("parent", "<u4"), ("depth", "<u4")])
+# records of the image's key and link arrays (toc_key, toc_link)
+KEY_DTYPE = np.dtype([("col", "<u4"), ("val", "<f4")])
+LINK_DTYPE = np.dtype([("parent", "<u4"), ("depth", "<u4")])
 
 
 BATCH_DTYPE = np.dtype([

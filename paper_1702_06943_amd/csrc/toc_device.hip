@@ -27,7 +27,8 @@ constexpr size_t kLdsMax = 160 * 1024;        // gfx950 LDS per workgroup
 struct Img {
   const toc_batch *batches;
   const uint32_t *level;
-  const toc_node *node;
+  const toc_key *key;
+  const toc_link *link;
   const uint32_t *span;
   const uint32_t *dcodes;
 };
@@ -36,21 +37,22 @@ Img image_of(const toc_dev *d) {
   const uint8_t *b = (const uint8_t *)d->buf;
   const toc_layout &L = d->layout;
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
-             (const toc_node *)(b + L.node), (const uint32_t *)(b + L.span),
+             (const toc_key *)(b + L.key), (const toc_link *)(b + L.link),
+             (const uint32_t *)(b + L.span),
              (const uint32_t *)(b + L.dcodes)};
 }
 
 // Views of one field of a batch's node records, indexed by local code.
 struct NodeCol {
-  const toc_node *n;
+  const toc_key *n;
   __device__ uint32_t operator[](int64_t c) const { return n[c].col; }
 };
 struct NodeVal {
-  const toc_node *n;
+  const toc_key *n;
   __device__ float operator[](int64_t c) const { return n[c].val; }
 };
 struct NodePar {
-  const toc_node *n;
+  const toc_link *n;
   __device__ uint32_t operator[](int64_t c) const { return n[c].parent; }
 };
 
@@ -94,9 +96,9 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   extern __shared__ float H[];
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.node + bt.code_base};
-  const NodeCol col{im.node + bt.code_base};
-  const NodeVal val{im.node + bt.code_base};
+  const NodePar par{im.link + bt.code_base};
+  const NodeCol col{im.key + bt.code_base};
+  const NodeVal val{im.key + bt.code_base};
   for (int d = 1; d <= bt.n_levels; ++d) {
     const uint32_t a = lvl[d - 1], e = lvl[d];
     for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
@@ -134,9 +136,9 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = im.batches[b];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.node + bt.code_base};
-  const NodeCol col{im.node + bt.code_base};
-  const NodeVal val{im.node + bt.code_base};
+  const NodePar par{im.link + bt.code_base};
+  const NodeCol col{im.key + bt.code_base};
+  const NodeVal val{im.key + bt.code_base};
   const uint32_t *oo = occ_off_all + bt.code_base + b;
   const uint32_t *orow = occ_row_all + bt.d_base;
   const uint32_t *tl = tlist_all + bt.tree_base;
@@ -231,9 +233,9 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
     float *__restrict__ R, int64_t ldr, float *__restrict__ ws) {
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.node + bt.code_base};
-  const NodeCol col{im.node + bt.code_base};
-  const NodeVal val{im.node + bt.code_base};
+  const NodePar par{im.link + bt.code_base};
+  const NodeCol col{im.key + bt.code_base};
+  const NodeVal val{im.key + bt.code_base};
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
   float *Hd = ws + (bt.deep_base - ws_base) * kt;
@@ -302,9 +304,9 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = im.batches[b];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.node + bt.code_base};
-  const NodeCol col{im.node + bt.code_base};
-  const NodeVal val{im.node + bt.code_base};
+  const NodePar par{im.link + bt.code_base};
+  const NodeCol col{im.key + bt.code_base};
+  const NodeVal val{im.key + bt.code_base};
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = wave_id();
@@ -432,18 +434,16 @@ __device__ inline uint32_t buf_load(BufRes r, uint32_t i) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, i * 4u, 0, 0);
 }
 
-// Buffer over n node records; key_load reads the key pair (col, val bits) of one.
-__device__ inline BufRes node_res(const toc_node *p, uint32_t n) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<toc_node *>(p), (short)0,
-                                           (int)(n * (uint32_t)sizeof(toc_node)), kBufFlags);
+// Buffer over n keys; key_load reads the key pair (col, val bits) of one.
+__device__ inline BufRes key_res(const toc_key *p, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<toc_key *>(p), (short)0,
+                                           (int)(n * (uint32_t)sizeof(toc_key)), kBufFlags);
 }
 
 __device__ inline uint2 key_load(BufRes r, uint32_t c) {
-  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, c * (uint32_t)sizeof(toc_node), 0, 0);
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, c * (uint32_t)sizeof(toc_key), 0, 0);
   return make_uint2(v[0], v[1]);
 }
-
-__device__ inline uint4 node_load(const toc_node *n, int64_t c) { return *(const uint4 *)(n + c); }
 
 // LDS reads through address-space-3 pointers (byte addresses in LDS): the
 // compiler never merges such a read with a global one into a flat access.
@@ -518,9 +518,9 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     const int kt = min(kRtKT, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const NodePar par{im.node + bt.code_base};
-    const NodeCol col{im.node + bt.code_base};
-    const NodeVal val{im.node + bt.code_base};
+    const NodePar par{im.link + bt.code_base};
+    const NodeCol col{im.key + bt.code_base};
+    const NodeVal val{im.key + bt.code_base};
     const uint32_t *span = im.span + bt.span_base;
     const uint32_t *dc = im.dcodes + bt.d_base;
     const uint32_t n1 = (uint32_t)bt.n_lvl1;
@@ -642,7 +642,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // the batch's arrays into zeros, and entries past the end of a tuple are
     // marked in a wave mask and become (zero row, 0) when staged.
     const BufRes rs_dc = buf_res(dc, (uint32_t)bt.n_d);
-    const BufRes rs_node = node_res(im.node + bt.code_base, (uint32_t)bt.n_codes);
+    const BufRes rs_node = key_res(im.key + bt.code_base, (uint32_t)bt.n_codes);
     auto load_codes = [&](uint32_t &d0, uint32_t &d1, uint64_t &ok0, uint64_t &ok1) {
       const uint32_t j0 = lst + lj + (uint32_t)sub, j1 = j0 + 8u;
       const bool live = ltg < n_tg;
@@ -859,8 +859,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const int kt = min(TW, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const toc_node *node = im.node + bt.code_base;
-    const NodePar par{node};
+    const toc_key *node = im.key + bt.code_base;
+    const NodePar par{im.link + bt.code_base};
     const NodeCol col{node};
     const uint32_t *oo = occ_off_all + bt.code_base + b;
     const uint32_t *orow = occ_row_all + bt.d_base;
@@ -1010,7 +1010,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
       }
     };
-    const BufRes rs_node = node_res(node, nc);
+    const BufRes rs_node = key_res(node, nc);
     const uint32_t *dummy = lvl;   // a valid address for lanes without an entry
     // L: the entry word of each lane (occ_row word of a leaf occurrence, or the
     // code of a tree entry) and its kind: 0 leaf, 1 tree, 2 none
@@ -1161,7 +1161,9 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   const int64_t t = t0 + slot;
   const uint4 dt = dtiles[t];                       // batch, first entry, pairs before, first row
   const toc_batch bt = im.batches[dt.x];
-  const toc_node *node = im.node + bt.code_base;
+  const toc_key *key = im.key + bt.code_base;
+  const toc_link *link = im.link + bt.code_base;
+  const uint32_t n1 = (uint32_t)bt.n_lvl1;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % kWave, wave = wave_id();
@@ -1173,15 +1175,19 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
     c[i] = j < nd ? dc[j] : 0u;
   }
-  // the node record of each entry's code: key pair, parent, depth
-  uint4 rec[kDecPer];
+  // the key pair of each entry's code and its depth: 1 below n_lvl1 (depth-1
+  // codes come first), else from the code's link, which also holds its parent
+  uint2 kv[kDecPer];
+  uint2 lk[kDecPer];
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) {
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
-    rec[i] = j < nd ? node_load(node, c[i]) : make_uint4(0u, 0u, 0u, 0u);
+    kv[i] = j < nd ? *(const uint2 *)(key + c[i]) : make_uint2(0u, 0u);
+    lk[i] = make_uint2(0xFFFFFFFFu, j < nd ? 1u : 0u);
+    if (j < nd && c[i] >= n1) lk[i] = *(const uint2 *)(link + c[i]);
   }
 #pragma unroll
-  for (int i = 0; i < kDecPer; ++i) sh[i * kDecBlock + threadIdx.x] = rec[i].w;
+  for (int i = 0; i < kDecPer; ++i) sh[i * kDecBlock + threadIdx.x] = lk[i].y;
   __syncthreads();
   // exclusive scan in entry order: thread t owns entries kDecPer*t .. +kDecPer-1
   uint32_t v[kDecPer], s = 0;
@@ -1210,15 +1216,17 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   for (int i = 0; i < kDecPer; ++i) {
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
     if (j < nd) {
-      uint4 r = rec[i];
-      const uint32_t d = r.w;
+      uint2 kk = kv[i];
+      uint32_t par = lk[i].x;
+      const uint32_t d = lk[i].y;
       int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
       for (uint32_t q = 0;;) {
-        ocol[p] = (int32_t)r.x;
-        oval[p] = r.y;
+        ocol[p] = (int32_t)kk.x;
+        oval[p] = kk.y;
         if (++q >= d) break;
         --p;
-        r = node_load(node, r.z);
+        kk = *(const uint2 *)(key + par);
+        if (par >= n1) par = link[par].parent;
       }
     }
   }

@@ -32,7 +32,7 @@ void clear_error() { g_err.clear(); }
 // by one open-addressing table keyed by (node, column, value bits): the per-node
 // child maps of the paper folded into a single hash table.
 // ---------------------------------------------------------------------------
-static_assert(sizeof(toc_node) == 16, "toc_node is one 16-byte record");
+static_assert(sizeof(toc_key) == 8 && sizeof(toc_link) == 8, "toc_key and toc_link are 8 bytes");
 
 namespace {
 
@@ -488,12 +488,13 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       for (uint64_t kc : S.keys) S.newidx[(uint32_t)kc] = (uint32_t)at++;
     }
   }
-  toc_node *node = (toc_node *)(dst + L.node) + bt.code_base;
+  toc_key *node = (toc_key *)(dst + L.key) + bt.code_base;
+  toc_link *link = (toc_link *)(dst + L.link) + bt.code_base;
   for (int64_t c = 1; c < N; ++c) {
     if (!S.live[c]) continue;
     const uint32_t at = S.newidx[c];
-    node[at].parent = S.depth[c] == 1 ? 0xFFFFFFFFu : S.newidx[S.parent[c]];
-    node[at].depth = S.depth[c];
+    link[at].parent = S.depth[c] == 1 ? 0xFFFFFFFFu : S.newidx[S.parent[c]];
+    link[at].depth = S.depth[c];
   }
   // keys: node c <= |I| has key I[c-1]; node idx > |I| has the first pair of the
   // code that follows its parent in D (Algorithm 2).
@@ -577,7 +578,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     auto hrow = [&](uint32_t c) -> int64_t { return c < n_int1 ? c : (int64_t)c - n1 + n_int1; };
     int64_t c = n1;
     for (int64_t h = 0; h <= n_tree; ++h) {
-      while (c < n_codes && hrow(node[c].parent) < h) ++c;
+      while (c < n_codes && hrow(link[c].parent) < h) ++c;
       tch[h] = (uint32_t)c;
     }
   }
@@ -596,7 +597,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       dt[4 * t + 1] = (uint32_t)es;
       dt[4 * t + 2] = (uint32_t)pairs;
       dt[4 * t + 3] = (uint32_t)row;
-      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += node[dcodes[j]].depth;
+      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += link[dcodes[j]].depth;
     }
   }
   bt.n_codes = (int32_t)n_codes;
@@ -667,7 +668,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   int64_t off = 0;
   L.batches = off; off = align256(off + (int64_t)sizeof(toc_batch) * n_batches);
   L.level = off;   off = align256(off + 4 * levels);
-  L.node = off;    off = align256(off + (int64_t)sizeof(toc_node) * codes);
+  L.key = off;     off = align256(off + (int64_t)sizeof(toc_key) * codes);
+  L.link = off;    off = align256(off + (int64_t)sizeof(toc_link) * codes);
   L.span = off;    off = align256(off + 4 * spans);
   L.dcodes = off;  off = align256(off + 4 * d);
   L.occ_off = off; off = align256(off + 4 * (codes + n_batches));

@@ -27,7 +27,8 @@ def read_image(dev, buf):
     img = dict(
         bt=bt, info=info,
         level=arr("level", np.uint32, n_levels),
-        node=arr("node", T.NODE_DTYPE, n_codes),
+        key=arr("key", T.KEY_DTYPE, n_codes),
+        link=arr("link", T.LINK_DTYPE, n_codes),
         span=arr("span", np.uint32, int((bt["n_rows"] + 1).sum()) if nb else 0),
         dcodes=arr("dcodes", np.uint32, info["n_codes"]),
         occ_off=arr("occ_off", np.uint32, n_codes + nb),
@@ -38,8 +39,10 @@ def read_image(dev, buf):
         tchild=arr("tchild", np.uint32,
                    int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"] + 1).sum()) if nb else 0),
     )
-    for f in ("parent", "col", "val", "depth"):
-        img[f] = img["node"][f]
+    for f in ("col", "val"):
+        img[f] = img["key"][f]
+    for f in ("parent", "depth"):
+        img[f] = img["link"][f]
     return img
 
 
