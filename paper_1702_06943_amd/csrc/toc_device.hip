@@ -77,6 +77,33 @@ __device__ inline uint32_t wave_incl_scan(uint32_t x, int lane) {
   return x;
 }
 
+// A batch record read into wave-uniform (scalar) registers, so that pointers and
+// buffer descriptors derived from it stay scalar.
+__device__ inline int64_t uniform64(int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ inline toc_batch uniform_batch(const toc_batch *p) {
+  toc_batch t = *p;
+  t.code_base = uniform64(t.code_base);
+  t.d_base = uniform64(t.d_base);
+  t.row_base = uniform64(t.row_base);
+  t.span_base = uniform64(t.span_base);
+  t.nnz_base = uniform64(t.nnz_base);
+  t.deep_base = uniform64(t.deep_base);
+  t.tree_base = uniform64(t.tree_base);
+  t.lvl_base = uniform64(t.lvl_base);
+  t.n_rows = __builtin_amdgcn_readfirstlane(t.n_rows);
+  t.n_codes = __builtin_amdgcn_readfirstlane(t.n_codes);
+  t.n_lvl1 = __builtin_amdgcn_readfirstlane(t.n_lvl1);
+  t.n_int1 = __builtin_amdgcn_readfirstlane(t.n_int1);
+  t.n_levels = __builtin_amdgcn_readfirstlane(t.n_levels);
+  t.n_d = __builtin_amdgcn_readfirstlane(t.n_d);
+  return t;
+}
+
 // Load that bypasses the per-CU L1, for values other waves updated with atomics.
 __device__ inline float coherent_load(const float *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -120,55 +147,70 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
 }
 
 // Left multiplication (Theorem 2, Algorithm 5) without atomics: H[c] = G(c) is
-// pulled from the inverted index (the sum over the entries of D equal to c), each
+// pulled from the inverted index (the sum over the entries of D equal to c; a
+// thread takes 4 codes at a time and loads their occurrence rows together), each
 // code then adds its children's H (children are contiguous: levels are sorted by
-// parent), deepest level first; finally every key column has one writer, the
-// thread at the head of its run of depth-1 leaves (sorted by column) or, for a
-// column with no leaf, the head of its run in the column-sorted tree list.
+// parent), deepest level first; finally a thread per key column writes it once,
+// summing val * H over the column's depth-1 leaves (a contiguous code range) and
+// tree codes (a contiguous stretch of the tree list), both read from the image's
+// column index.
 constexpr uint32_t kFirstOccK1 = 0x80000000u;
+constexpr int kK1Codes = 4;      // codes per thread and pass
+constexpr int kK1Occ = 4;        // occurrences per code loaded together
+constexpr int kK1Cols = 8;       // output columns per thread and pass
+constexpr int kK1Tree = 4;       // tree-list entries per column loaded together
 
 __global__ __launch_bounds__(kBlock) void left_k1_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, int64_t b0, int32_t m, int32_t max_rows,
-    int32_t max_codes, int32_t max_tree, const float *__restrict__ G, int64_t ldg,
-    float *__restrict__ out, int64_t ldo, int accumulate) {
+    const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
+    const uint32_t *__restrict__ tchild_all, int64_t b0, int32_t m, int32_t max_rows,
+    int32_t max_codes, const float *__restrict__ G, int64_t ldg, float *__restrict__ out,
+    int64_t ldo, int accumulate) {
   extern __shared__ float sm[];
   const int64_t b = b0 + blockIdx.x;
-  const toc_batch bt = im.batches[b];
+  const toc_batch bt = uniform_batch(im.batches + b);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.link + bt.code_base};
-  const NodeCol col{im.key + bt.code_base};
-  const NodeVal val{im.key + bt.code_base};
+  const toc_key *key = im.key + bt.code_base;
   const uint32_t *oo = occ_off_all + bt.code_base + b;
   const uint32_t *orow = occ_row_all + bt.d_base;
   const uint32_t *tl = tlist_all + bt.tree_base;
+  const uint32_t *tch = tchild_all + bt.tree_base + b;
+  const uint32_t *cx = cols_all + b * 4 * (int64_t)(m + 1);   // Loff, Ost, Toff, Ord
   const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
-  const uint32_t n_tree = ni + (nc - n1);
   float *Gs = sm;                                     // max_rows
   float *H = sm + max_rows;                           // max_codes
-  uint32_t *Coff = (uint32_t *)(H + max_codes);       // n_tree + 1 children ranges
-  uint32_t *tcol = Coff + max_tree + 1;               // n_tree (column of each list entry)
   auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
   float *ob = out + b * (int64_t)m * ldo;
   for (int r = threadIdx.x; r < bt.n_rows; r += kBlock) Gs[r] = G[(bt.row_base + r) * ldg];
-  if (!accumulate)
-    for (int j = threadIdx.x; j < m; j += kBlock) ob[(int64_t)j * ldo] = 0.0f;
-  for (uint32_t c = n1 + threadIdx.x; c < nc; c += kBlock) {
-    const int64_t ph = hrow(par[c]), pp = c > n1 ? (int64_t)hrow(par[c - 1]) : -1;
-    for (int64_t h = pp + 1; h <= ph; ++h) Coff[h] = c;
-  }
-  {
-    const int64_t last = nc > n1 ? (int64_t)hrow(par[nc - 1]) : -1;
-    for (int64_t h = last + 1 + threadIdx.x; h <= n_tree; h += kBlock) Coff[h] = nc;
-  }
-  for (uint32_t t = threadIdx.x; t < n_tree; t += kBlock) tcol[t] = col[tl[t]];
-  __threadfence_block();
   __syncthreads();
   // G(c) for every code
-  for (uint32_t c = threadIdx.x; c < nc; c += kBlock) {
-    float s = 0.0f;
-    for (uint32_t o = oo[c]; o < oo[c + 1]; ++o) s += Gs[orow[o] & ~kFirstOccK1];
-    H[c] = s;
+  for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
+    uint32_t o0[kK1Codes], o1[kK1Codes];
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u) {
+      const uint32_t c = c0 + u * kBlock;
+      o0[u] = c < nc ? oo[c] : 0u;
+      o1[u] = c < nc ? oo[c + 1] : 0u;
+    }
+    float s[kK1Codes];
+    uint32_t w[kK1Codes][kK1Occ];
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u)
+#pragma unroll
+      for (int v = 0; v < kK1Occ; ++v) w[u][v] = o0[u] + v < o1[u] ? orow[o0[u] + v] : 0xFFFFFFFFu;
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u) {
+      s[u] = 0.0f;
+#pragma unroll
+      for (int v = 0; v < kK1Occ; ++v)
+        if (w[u][v] != 0xFFFFFFFFu) s[u] += Gs[w[u][v] & ~kFirstOccK1];
+      for (uint32_t o = o0[u] + kK1Occ; o < o1[u]; ++o) s[u] += Gs[orow[o] & ~kFirstOccK1];
+    }
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u) {
+      const uint32_t c = c0 + u * kBlock;
+      if (c < nc) H[c] = s[u];
+    }
   }
   __syncthreads();
   // children into parents, deepest parent level first
@@ -176,47 +218,63 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
     const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
     for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
       const uint32_t h = hrow(c);
-      float s = H[c];
-      for (uint32_t ch = Coff[h]; ch < Coff[h + 1]; ++ch) s += H[ch];
-      H[c] = s;
+      float sum = H[c];
+      const uint32_t ch1 = tch[h + 1];
+      for (uint32_t ch = tch[h]; ch < ch1; ++ch) sum += H[ch];
+      H[c] = sum;
     }
     __syncthreads();
   }
-  // first tree-list entry with column >= j
-  auto tree_lb = [&](uint32_t j) -> uint32_t {
-    uint32_t lo = 0, hi = n_tree;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) / 2;
-      if (tcol[mid] < j) lo = mid + 1;
-      else hi = mid;
+  // H[c] becomes val(c) * H[c]: a key column's output is the plain sum of these
+  // over the column's codes
+  for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
+    float v[kK1Codes];
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u) {
+      const uint32_t c = c0 + u * kBlock;
+      v[u] = c < nc ? key[c].val : 0.0f;
     }
-    return lo;
-  };
-  // columns owned by the head of a run of depth-1 leaves
-  for (uint32_t i = ni + threadIdx.x; i < n1; i += kBlock) {
-    const uint32_t j = col[i];
-    if (i > ni && col[i - 1] == j) continue;
-    float s = 0.0f;
-    for (uint32_t x = i; x < n1 && col[x] == j; ++x) s = fmaf(val[x], H[x], s);
-    for (uint32_t t = tree_lb(j); t < n_tree && tcol[t] == j; ++t) s = fmaf(val[tl[t]], H[tl[t]], s);
-    float *p = ob + (int64_t)j * ldo;
-    *p = accumulate ? *p + s : s;
+#pragma unroll
+    for (int u = 0; u < kK1Codes; ++u) {
+      const uint32_t c = c0 + u * kBlock;
+      if (c < nc) H[c] *= v[u];
+    }
   }
-  // columns that only tree codes have
-  for (uint32_t t = threadIdx.x; t < n_tree; t += kBlock) {
-    const uint32_t j = tcol[t];
-    if (t > 0 && tcol[t - 1] == j) continue;
-    uint32_t lo = ni, hi = n1;           // is there a leaf with column j?
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) / 2;
-      if (col[mid] < j) lo = mid + 1;
-      else hi = mid;
+  __syncthreads();
+  // each key column once: its depth-1 leaves (a code range), then its tree
+  // codes (a tree-list range); a thread has kK1Cols columns in flight and
+  // loads the first kK1Tree tree-list entries of each before summing
+  const uint32_t *Loff = cx, *Toff = cx + 2 * (m + 1);
+  for (int j0 = 0; j0 < m; j0 += kBlock * kK1Cols) {
+    uint32_t l0[kK1Cols], l1[kK1Cols], t0[kK1Cols], t1[kK1Cols];
+#pragma unroll
+    for (int u = 0; u < kK1Cols; ++u) {
+      const int j = j0 + u * kBlock + threadIdx.x;
+      const bool in = j < m;
+      l0[u] = in ? Loff[j] : 0u;
+      l1[u] = in ? Loff[j + 1] : 0u;
+      t0[u] = in ? Toff[j] : 0u;
+      t1[u] = in ? Toff[j + 1] : 0u;
     }
-    if (lo < n1 && col[lo] == j) continue;
-    float s = 0.0f;
-    for (uint32_t u = t; u < n_tree && tcol[u] == j; ++u) s = fmaf(val[tl[u]], H[tl[u]], s);
-    float *p = ob + (int64_t)j * ldo;
-    *p = accumulate ? *p + s : s;
+    uint32_t tc[kK1Cols][kK1Tree];
+#pragma unroll
+    for (int u = 0; u < kK1Cols; ++u)
+#pragma unroll
+      for (int v = 0; v < kK1Tree; ++v) tc[u][v] = t0[u] + v < t1[u] ? tl[t0[u] + v] : 0xFFFFFFFFu;
+#pragma unroll
+    for (int u = 0; u < kK1Cols; ++u) {
+      const int j = j0 + u * kBlock + threadIdx.x;
+      float sum = 0.0f;
+      for (uint32_t c = l0[u]; c < l1[u]; ++c) sum += H[c];
+#pragma unroll
+      for (int v = 0; v < kK1Tree; ++v)
+        if (tc[u][v] != 0xFFFFFFFFu) sum += H[tc[u][v]];
+      for (uint32_t t = t0[u] + kK1Tree; t < t1[u]; ++t) sum += H[tl[t]];
+      if (j < m) {
+        float *p = ob + (int64_t)j * ldo;
+        *p = accumulate ? *p + sum : sum;
+      }
+    }
   }
 }
 
@@ -393,32 +451,6 @@ __device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
 }
 
-// A batch record read into wave-uniform (scalar) registers, so that pointers and
-// buffer descriptors derived from it stay scalar.
-__device__ inline int64_t uniform64(int64_t v) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)v >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ inline toc_batch uniform_batch(const toc_batch *p) {
-  toc_batch t = *p;
-  t.code_base = uniform64(t.code_base);
-  t.d_base = uniform64(t.d_base);
-  t.row_base = uniform64(t.row_base);
-  t.span_base = uniform64(t.span_base);
-  t.nnz_base = uniform64(t.nnz_base);
-  t.deep_base = uniform64(t.deep_base);
-  t.tree_base = uniform64(t.tree_base);
-  t.lvl_base = uniform64(t.lvl_base);
-  t.n_rows = __builtin_amdgcn_readfirstlane(t.n_rows);
-  t.n_codes = __builtin_amdgcn_readfirstlane(t.n_codes);
-  t.n_lvl1 = __builtin_amdgcn_readfirstlane(t.n_lvl1);
-  t.n_int1 = __builtin_amdgcn_readfirstlane(t.n_int1);
-  t.n_levels = __builtin_amdgcn_readfirstlane(t.n_levels);
-  t.n_d = __builtin_amdgcn_readfirstlane(t.n_d);
-  return t;
-}
 
 // Raw buffer resource over n 32-bit elements: loads at an index >= n return 0
 // instead of touching memory (the range check of buffer instructions).
@@ -1279,7 +1311,7 @@ int lanes_per_row(const toc_dev *d) {
 // Whether the k = 1 kernels can keep a batch's H in LDS.
 size_t k1_lds(const toc_dev *d, int op) {
   if (op == TOC_OP_RIGHT) return std::max<size_t>(16, (size_t)d->max_codes * 4);
-  return ((size_t)d->max_rows + d->max_codes + 2 * (size_t)d->max_tree + 1) * 4;
+  return ((size_t)d->max_rows + d->max_codes) * 4;
 }
 
 bool k1_fits(const toc_dev *d, int op) { return k1_lds(d, op) <= kLdsMax; }
@@ -1593,11 +1625,13 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
     const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
+    const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
+    const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
       hipLaunchKernelGGL(left_k1_kernel, dim3(g), dim3(kBlock), lds, s, im, occ_off, occ_row,
-                         tlist, b0, m, d->max_rows, d->max_codes, (int32_t)d->max_tree, G, ldg,
-                         out, ldo, accumulate);
+                         tlist, cols, tchild, b0, m, d->max_rows, d->max_codes, G, ldg, out, ldo,
+                         accumulate);
       if ((st = launch_status("left_k1_kernel"))) return st;
     }
     return TOC_OK;
