@@ -9,6 +9,8 @@
 #include <algorithm>
 #include <cstring>
 #include <new>
+#include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "toc_internal.h"
@@ -498,31 +500,390 @@ __device__ inline float4 lds_load4(uint32_t byte) {
 // together there and share the batch's image in that XCD's L2.  A worker keeps
 // the tile of W it last used in LDS (rows 0..m-1; row m is all zeros) and the H
 // rows of the batch's depth >= 2 codes after it, built level by level.
-// An 8-lane group owns one tuple (a lane holds 4 columns), so a wave sums 8
-// tuples at once and needs no cross-lane reduction.  The codes of the wave's
-// entries are loaded two chunks ahead and translated to (LDS row, multiplier)
-// one chunk ahead; a chunk (16 entries of each of the 8 tuples) is staged in the
-// wave's part of LDS, where every lane of a group reads its tuple's entry by
-// broadcast.  Entries past the end of a tuple point at the zero row.
+// A 16-lane row of the wave owns one tuple (a lane holds 2 columns), so a wave
+// sums 4 tuples at once and needs no cross-lane reduction of sums.  Lane l of a
+// row loads the codes of entries l and l + 16 of its tuple's chunk two steps
+// ahead, gathers their keys one step ahead and translates them to (LDS address
+// of the H row, multiplier) in registers.  While a chunk is summed, the row
+// broadcast of the DPP cross-lane operations hands entry t of every tuple to
+// all 16 lanes of its row (the address through an add, the multiplier through
+// the FMA itself), so the only LDS reads are the H rows.  Entries past the end
+// of a tuple point at the zero row with multiplier 0.
 // ---------------------------------------------------------------------------
 constexpr int kRtKT = 32;
 constexpr int kRtBlock = 1024;
 constexpr int kRtWaves = kRtBlock / kWave;
-constexpr int kRtGroups = kWave / 8;              // tuples per wave
-constexpr int kRtChunk = 16;                      // entries per tuple per pipeline step
-constexpr uint32_t kRtStageBytes = kRtWaves * kRtChunk * kRtGroups * 8;
+constexpr int kRtLanes = 16;                      // lanes per tuple: one DPP row
+constexpr int kRtGroups = kWave / kRtLanes;       // tuples per wave
+constexpr int kRtPer = 2;                         // entries per lane and chunk
+constexpr int kRtChunk = kRtPer * kRtLanes;       // entries per tuple per pipeline step
+constexpr uint32_t kRtRowBytes = kRtKT * 4;
 constexpr uint32_t kRtStaticBytes = 16;           // static LDS: two tuple-group counters
-constexpr uint32_t kRtGlobal = 0x80000000u;       // H row lives in the workspace
-constexpr uint32_t kRtNone = 0xFFFFFFFFu;         // no entry
+constexpr uint32_t kRtGlobal = 0x80000000u;       // row index flag: the H row lives in the workspace
+constexpr int kRtDeepU = 2;                       // deep codes per 8-lane group and round
+
+// The value v of lane T of the caller's 16-lane row, in every lane of the row.
+template <int T>
+__device__ inline uint32_t row_bcast(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x150 + T, 0xF, 0xF, true);
+}
+
+// f(std::integral_constant<int, I>{}) for I = 0 .. N-1, unrolled.
+template <typename F, int... I>
+__device__ inline void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ inline void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) f32x2 lds_f32x2;
+
+__device__ inline float2 lds_load2(uint32_t byte) {
+  const f32x2 v = *(const lds_f32x2 *)(size_t)byte;
+  return make_float2(v[0], v[1]);
+}
+
+// acc += mu(lane L of the row) * x[i] for 8 entries, lanes L = T0 .. T0 + 7: the
+// FMA reads the multiplier across lanes itself.  A cross-lane read of a register
+// needs two wait states after a vector write of it; the s_nop provides them.
+#define TOC_FMAC2(I, L)                                                                  \
+  "v_fmac_f32_dpp %[ax], %[mu], %[x" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"                                          \
+  "v_fmac_f32_dpp %[ay], %[mu], %[y" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+#define TOC_FMA8(L0, L1, L2, L3, L4, L5, L6, L7)                                         \
+  asm volatile("s_nop 1\n\t" TOC_FMAC2(0, L0) TOC_FMAC2(1, L1) TOC_FMAC2(2, L2)          \
+                   TOC_FMAC2(3, L3) TOC_FMAC2(4, L4) TOC_FMAC2(5, L5) TOC_FMAC2(6, L6)   \
+                       TOC_FMAC2(7, L7)                                                   \
+               : [ax] "+v"(acc.x), [ay] "+v"(acc.y)                                       \
+               : [mu] "v"(mu), [x0] "v"(x[0].x), [y0] "v"(x[0].y), [x1] "v"(x[1].x),      \
+                 [y1] "v"(x[1].y), [x2] "v"(x[2].x), [y2] "v"(x[2].y), [x3] "v"(x[3].x),  \
+                 [y3] "v"(x[3].y), [x4] "v"(x[4].x), [y4] "v"(x[4].y), [x5] "v"(x[5].x),  \
+                 [y5] "v"(x[5].y), [x6] "v"(x[6].x), [y6] "v"(x[6].y), [x7] "v"(x[7].x),  \
+                 [y7] "v"(x[7].y))
+
+template <int T0>
+__device__ inline void fma8_bcast(float2 &acc, uint32_t mu, const float2 (&x)[8]) {
+  static_assert(T0 == 0 || T0 == 8, "lanes 0..7 or 8..15 of a row");
+  if constexpr (T0 == 0) {
+    TOC_FMA8(0, 1, 2, 3, 4, 5, 6, 7);
+  } else {
+    TOC_FMA8(8, 9, 10, 11, 12, 13, 14, 15);
+  }
+}
+#undef TOC_FMA8
+#undef TOC_FMAC2
+
+// The H rows of entries T0 .. T0 + 7 of a half chunk (rb: the row address held
+// by each lane, qoff: this lane's columns in a row).
+template <int T0>
+__device__ inline void load8_bcast(uint32_t rb, uint32_t qoff, float2 (&x)[8]) {
+  static_for<8>([&](auto i) { x[i] = lds_load2(row_bcast<T0 + decltype(i)::value>(rb) + qoff); });
+}
 
 struct RtChunk {
+  int tg;           // tuple group (tuples 4*tg .. 4*tg+3 of the batch); >= n_tg: none
+  uint32_t steps;   // entries per tuple to process, rounded up to a multiple of 8
+  bool last;        // last chunk of the tuple group
+};
+
+__global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
+    Img im, int64_t nb, int n_tiles, int spw, int m, const float *__restrict__ W,
+    int64_t ldw, int k, float *__restrict__ R, int64_t ldr) {
+  extern __shared__ float4 smem4[];
+  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
+  const int lane = threadIdx.x % kWave, wave = wave_id();
+  const int grp = lane / kRtLanes, sub = lane % kRtLanes, q = 2 * sub;
+  __shared__ uint32_t tg_next[2];                             // next free tuple group, by item parity
+  float *Wt = (float *)smem4;                                 // (m + 1) x kRtKT, then deep rows
+  const uint32_t wb = lds_base(smem4);                        // LDS address of row 0
+  const uint32_t qoff = 4u * (uint32_t)q;                     // this lane's columns in a row
+  const uint32_t zrow_b = wb + (uint32_t)m * kRtRowBytes;
+  for (int e = threadIdx.x; e < kRtKT; e += kRtBlock) Wt[m * kRtKT + e] = 0.0f;
+  if (threadIdx.x < 2) tg_next[threadIdx.x] = kRtWaves;
+  const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
+  const int64_t n_items = nbx * n_tiles;
+  int cur_tile = -1;
+  uint32_t parity = 0;
+  for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
+    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
+    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
+    const int k0 = tile * kRtKT;
+    const int kt = min(kRtKT, k - k0);
+    const toc_batch bt = uniform_batch(im.batches + b);
+    const uint32_t *lvl = im.level + bt.lvl_base;
+    const uint32_t *span = im.span + bt.span_base;
+    const uint32_t *dc = im.dcodes + bt.d_base;
+    const uint32_t n1 = (uint32_t)bt.n_lvl1;
+    const int nrows = bt.n_rows;
+    __syncthreads();   // the previous item no longer reads the W tile or the deep rows
+    // the counter of the previous item is free again: ready for the next one
+    if (threadIdx.x == 0) tg_next[parity ^ 1u] = kRtWaves;
+    if (tile != cur_tile) {
+      // all loads of a pass first, then the stores
+      const int n4 = m * (kRtKT / 4);
+      const bool vec = kt == kRtKT && (ldw % 4) == 0 && (((uintptr_t)(W + k0)) & 15u) == 0;
+      for (int e0 = threadIdx.x; e0 < n4; e0 += 8 * kRtBlock) {
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kRtBlock;
+          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e < n4) {
+            const int c = e / (kRtKT / 4), q4 = 4 * (e % (kRtKT / 4));
+            const float *src = W + (int64_t)c * ldw + k0 + q4;
+            if (vec) {
+              v[i] = *(const float4 *)src;
+            } else {
+              if (q4 + 0 < kt) v[i].x = src[0];
+              if (q4 + 1 < kt) v[i].y = src[1];
+              if (q4 + 2 < kt) v[i].z = src[2];
+              if (q4 + 3 < kt) v[i].w = src[3];
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = e0 + i * kRtBlock;
+          if (e < n4) *(float4 *)&Wt[e * 4] = v[i];
+        }
+      }
+      cur_tile = tile;
+      __syncthreads();
+    }
+    // H of depth >= 2 codes, level by level: 8 lanes per code (4 columns each,
+    // 16-byte accesses), kRtDeepU codes per group and round.  Every load is
+    // unconditional (indices are clamped to valid codes) so that the loads of a
+    // round are all in flight together.
+    {
+      const toc_key *key = im.key + bt.code_base;
+      const toc_link *link = im.link + bt.code_base;
+      const uint32_t g8 = threadIdx.x / 8u, q4 = 4u * (threadIdx.x % 8u);
+      constexpr uint32_t stride = kRtBlock / 8;
+      for (int d = 2; d <= bt.n_levels; ++d) {
+        const uint32_t a = lvl[d - 1], e = lvl[d];
+        for (uint32_t c0 = a + g8; c0 < e; c0 += kRtDeepU * stride) {
+          uint32_t cs[kRtDeepU], p[kRtDeepU];
+          uint2 kc[kRtDeepU], kp[kRtDeepU];
+#pragma unroll
+          for (int u = 0; u < kRtDeepU; ++u) {
+            cs[u] = c0 + u * stride;
+            const uint32_t cc = cs[u] < e ? cs[u] : c0;
+            p[u] = link[cc].parent;
+            kc[u] = *(const uint2 *)(key + cc);
+          }
+#pragma unroll
+          for (int u = 0; u < kRtDeepU; ++u) kp[u] = *(const uint2 *)(key + (p[u] < n1 ? p[u] : 0u));
+          float4 bl[kRtDeepU], w[kRtDeepU];
+#pragma unroll
+          for (int u = 0; u < kRtDeepU; ++u) {
+            const uint32_t lrow = p[u] < n1 ? kp[u].x : (uint32_t)m + 1u + (p[u] - n1);
+            bl[u] = *(const float4 *)&Wt[lrow * kRtKT + q4];
+            w[u] = *(const float4 *)&Wt[kc[u].x * kRtKT + q4];
+          }
+#pragma unroll
+          for (int u = 0; u < kRtDeepU; ++u) {
+            const float vp = p[u] < n1 ? __uint_as_float(kp[u].y) : 1.0f;
+            const float vc = __uint_as_float(kc[u].y);
+            const float4 h = make_float4(fmaf(vc, w[u].x, vp * bl[u].x), fmaf(vc, w[u].y, vp * bl[u].y),
+                                         fmaf(vc, w[u].z, vp * bl[u].z), fmaf(vc, w[u].w, vp * bl[u].w));
+            if (cs[u] < e) *(float4 *)&Wt[(m + 1 + (cs[u] - n1)) * kRtKT + q4] = h;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // per-tuple sums
+    const int n_tg = (nrows + kRtGroups - 1) / kRtGroups;
+    // rows past the end read span[nrows] twice: an empty tuple
+    auto spans_of = [&](int tg, uint32_t &st, uint32_t &en) {
+      const int r = min(tg * kRtGroups + grp, nrows);
+      st = span[r];
+      en = span[min(r + 1, nrows)];
+    };
+    auto wave_max = [&](uint32_t v) -> uint32_t {
+      v = max(v, (uint32_t)__shfl_xor((int)v, 16, kWave));
+      v = max(v, (uint32_t)__shfl_xor((int)v, 32, kWave));
+      return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+    };
+    // Tuple groups: wave w starts with group w, then takes the next free group
+    // from the item's counter, so waves that finish early take more groups.
+    auto grab = [&]() -> int {
+      uint32_t g = 0;
+      if (lane == 0) g = atomicAdd(&tg_next[parity], 1u);
+      return __builtin_amdgcn_readfirstlane((int)g);
+    };
+    // load stage: tuple group ltg, entries [lj, lj + kRtChunk) of each tuple;
+    // ntg is the group after it, whose spans are in nst, nen
+    int ltg = wave, ntg = n_tg;
+    uint32_t lj = 0, lmax = 0, lst = 0, len = 0, nst = 0, nen = 0;
+    if (ltg < n_tg) {
+      spans_of(ltg, lst, len);
+      lmax = wave_max(len - lst);
+      ntg = grab();
+    }
+    spans_of(ntg, nst, nen);
+    auto chunk_of_l = [&]() -> RtChunk {
+      const uint32_t n = lmax > lj ? min((uint32_t)kRtChunk, lmax - lj) : 0u;
+      return RtChunk{ltg, (n + 7u) & ~7u, lj + kRtChunk >= lmax};
+    };
+    // the next group's spans are reloaded on every step (cache hits), so that a
+    // switch of group only moves values loaded a step earlier
+    auto advance = [&]() {
+      if (ltg < n_tg) {
+        lj += kRtChunk;
+        if (lj >= lmax) {
+          ltg = ntg;
+          lj = 0;
+          lst = nst;
+          len = nen;
+          lmax = 0u;
+          if (ltg < n_tg) {
+            lmax = wave_max(len - lst);
+            ntg = grab();
+          }
+        }
+      }
+      spans_of(ntg, nst, nen);
+    };
+    // Every load below is unconditional: the buffer range checks turn reads past
+    // the batch's arrays into zeros, and entries past the end of a tuple are
+    // marked in a wave mask and become (zero row, 0) when translated.
+    const BufRes rs_dc = buf_res(dc, (uint32_t)bt.n_d);
+    const BufRes rs_node = key_res(im.key + bt.code_base, (uint32_t)bt.n_codes);
+    // codes of entries sub + 16 h (h < kRtPer) of the load stage's chunk
+    auto load_codes = [&](uint32_t (&d)[kRtPer], uint64_t (&ok)[kRtPer]) {
+      const bool live = ltg < n_tg;
+      static_for<kRtPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        const uint32_t j = lst + lj + (uint32_t)sub + (uint32_t)(h * kRtLanes);
+        ok[h] = __ballot(live && j < len);
+        d[h] = buf_load(rs_dc, j);
+      });
+    };
+    // (H row, multiplier) of an entry: a depth-1 code's row is its column of W
+    // times its value; a deeper code's row is its own H row, times 1
+    auto translate = [&](uint32_t d, uint2 key, uint64_t ok, uint32_t &rb, uint32_t &mu) {
+      if (d < n1) {
+        rb = wb + key.x * kRtRowBytes;
+        mu = key.y;
+      } else {
+        rb = wb + ((uint32_t)m + 1u + (d - n1)) * kRtRowBytes;
+        mu = __float_as_uint(1.0f);
+      }
+      if (!__builtin_amdgcn_inverse_ballot_w64(ok)) {
+        rb = zrow_b;
+        mu = 0u;
+      }
+    };
+    float2 acc = make_float2(0.f, 0.f);
+    // Pipeline: codes of chunk L load while chunk G's keys are gathered and
+    // chunk C, translated in registers, is summed; G is translated at the end of
+    // the step.  Two register sets of codes alternate between the roles of G and
+    // L, so no loaded value is ever copied.
+    RtChunk G = chunk_of_l();
+    RtChunk C{n_tg, 0u, false};
+    uint32_t crb[kRtPer], cmu[kRtPer];
+#pragma unroll
+    for (int h = 0; h < kRtPer; ++h) {
+      crb[h] = zrow_b;
+      cmu[h] = 0u;
+    }
+    auto step = [&](const uint32_t (&gd)[kRtPer], const uint64_t (&gok)[kRtPer],
+                    uint32_t (&ld)[kRtPer], uint64_t (&lok)[kRtPer]) {
+      advance();
+      uint2 key[kRtPer];
+      static_for<kRtPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        key[h] = key_load(rs_node, gd[h]);
+      });
+      const RtChunk L = chunk_of_l();
+      load_codes(ld, lok);
+      if (C.tg < n_tg) {
+        if (C.steps == kRtChunk) {
+          // each block's reads are issued before the previous block's FMAs
+          float2 x0[8], x1[8];
+          load8_bcast<0>(crb[0], qoff, x0);
+          static_for<kRtPer>([&](auto hc) {
+            constexpr int h = decltype(hc)::value;
+            load8_bcast<8>(crb[h], qoff, x1);
+            fma8_bcast<0>(acc, cmu[h], x0);
+            if constexpr (h + 1 < kRtPer) load8_bcast<0>(crb[h + 1], qoff, x0);
+            fma8_bcast<8>(acc, cmu[h], x1);
+          });
+        } else {
+          static_for<kRtPer>([&](auto hc) {
+            constexpr int h = decltype(hc)::value;
+            if (C.steps > (uint32_t)(16 * h)) {
+              float2 xr[8];
+              load8_bcast<0>(crb[h], qoff, xr);
+              fma8_bcast<0>(acc, cmu[h], xr);
+            }
+            if (C.steps > (uint32_t)(16 * h + 8)) {
+              float2 xr[8];
+              load8_bcast<8>(crb[h], qoff, xr);
+              fma8_bcast<8>(acc, cmu[h], xr);
+            }
+          });
+        }
+        if (C.last) {
+          const int r = C.tg * kRtGroups + grp;
+          if (r < nrows) {
+            float *rr = R + (bt.row_base + r) * ldr + k0 + q;
+            if (q + 1 < kt) {
+              rr[0] = acc.x;
+              rr[1] = acc.y;
+            } else if (q < kt) {
+              rr[0] = acc.x;
+            }
+          }
+          acc = make_float2(0.f, 0.f);
+        }
+      }
+      // chunk G becomes chunk C
+      static_for<kRtPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        translate(gd[h], key[h], gok[h], crb[h], cmu[h]);
+      });
+      C = G;
+      G = L;
+    };
+    uint32_t dA[kRtPer], dB[kRtPer];
+    uint64_t okA[kRtPer], okB[kRtPer];
+    load_codes(dA, okA);
+    while (G.tg < n_tg || C.tg < n_tg) {
+      step(dA, okA, dB, okB);
+      if (!(G.tg < n_tg || C.tg < n_tg)) break;
+      step(dB, okB, dA, okA);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Right multiplication, the same product for batches whose deep H rows do not
+// fit in LDS next to the W tile: those rows live in the worker's workspace
+// slot.  An 8-lane group owns one tuple (a lane holds 4 columns, so a workspace
+// row is read with 16-byte loads), so a wave sums 8 tuples at once.  The codes
+// of the wave's entries are loaded two chunks ahead and translated to (row,
+// multiplier) one chunk ahead; a chunk (16 entries of each of the 8 tuples) is
+// staged in the wave's part of LDS, where every lane of a group reads its
+// tuple's entry by broadcast.  Entries past the end of a tuple point at the
+// zero row.  Rows in the workspace are marked with kRtGlobal.
+// ---------------------------------------------------------------------------
+constexpr int kRsGroups = kWave / 8;              // tuples per wave
+constexpr int kRsChunk = 16;                      // entries per tuple per pipeline step
+constexpr uint32_t kRsStageBytes = kRtWaves * kRsChunk * kRsGroups * 8;
+
+struct RsChunk {
   int tg;           // tuple group (tuples 8*tg .. 8*tg+7 of the batch); >= n_tg: none
   uint32_t steps;   // entries per tuple to process, rounded up to a multiple of 4
   bool last;        // last chunk of the tuple group
 };
 
-template <bool DEEP_LDS>
-__global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
+__global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
     Img im, int64_t nb, int n_tiles, int spw, int m, const float *__restrict__ W,
     int64_t ldw, int k, float *__restrict__ R, int64_t ldr, float *__restrict__ ws,
     int64_t slot_floats) {
@@ -532,9 +893,9 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const int grp = lane / 8, sub = lane % 8, q = 4 * sub;
   __shared__ uint32_t tg_next[2];                             // next free tuple group, by item parity
-  uint2 *stage = (uint2 *)lds + wave * (kRtChunk * kRtGroups);
-  float *Wt = (float *)(lds + kRtStageBytes);                 // (m + 1) x kRtKT, then deep rows
-  const uint32_t qb = lds_base(smem4) + kRtStageBytes + 4u * (uint32_t)q;   // LDS address of this lane's columns
+  uint2 *stage = (uint2 *)lds + wave * (kRsChunk * kRsGroups);
+  float *Wt = (float *)(lds + kRsStageBytes);                 // (m + 1) x kRtKT, then deep rows
+  const uint32_t qb = lds_base(smem4) + kRsStageBytes + 4u * (uint32_t)q;   // LDS address of this lane's columns
   const uint32_t zrow = (uint32_t)m;
   float *Hg = ws + blockIdx.x * slot_floats;
   for (int e = threadIdx.x; e < kRtKT; e += kRtBlock) Wt[m * kRtKT + e] = 0.0f;
@@ -593,10 +954,10 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       __syncthreads();
     }
     // H of depth >= 2 codes, level by level; a group per code
-    const int gidx = wave * kRtGroups + grp;
+    const int gidx = wave * kRsGroups + grp;
     for (int d = 2; d <= bt.n_levels; ++d) {
       const uint32_t a = lvl[d - 1], e = lvl[d];
-      for (uint32_t c = a + gidx; c < e; c += kRtWaves * kRtGroups) {
+      for (uint32_t c = a + gidx; c < e; c += kRtWaves * kRsGroups) {
         const uint32_t p = par[c];
         const uint32_t cc = col[c];
         const float vc = val[c];
@@ -605,22 +966,19 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
           const float vp = val[p];
           base = *(const float4 *)&Wt[col[p] * kRtKT + q];
           base = make_float4(vp * base.x, vp * base.y, vp * base.z, vp * base.w);
-        } else if (DEEP_LDS) {
-          base = *(const float4 *)&Wt[(m + 1 + (p - n1)) * kRtKT + q];
         } else {
           base = *(const float4 *)&Hg[(int64_t)(p - n1) * kRtKT + q];
         }
         const float4 h = f4fma(vc, *(const float4 *)&Wt[cc * kRtKT + q], base);
-        if (DEEP_LDS) *(float4 *)&Wt[(m + 1 + (c - n1)) * kRtKT + q] = h;
-        else *(float4 *)&Hg[(int64_t)(c - n1) * kRtKT + q] = h;
+        *(float4 *)&Hg[(int64_t)(c - n1) * kRtKT + q] = h;
       }
       __syncthreads();
     }
     // per-tuple sums
-    const int n_tg = (nrows + kRtGroups - 1) / kRtGroups;
+    const int n_tg = (nrows + kRsGroups - 1) / kRsGroups;
     // rows past the end read span[nrows] twice: an empty tuple
     auto spans_of = [&](int tg, uint32_t &st, uint32_t &en) {
-      const int r = min(tg * kRtGroups + grp, nrows);
+      const int r = min(tg * kRsGroups + grp, nrows);
       st = span[r];
       en = span[min(r + 1, nrows)];
     };
@@ -637,7 +995,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       if (lane == 0) g = atomicAdd(&tg_next[parity], 1u);
       return __builtin_amdgcn_readfirstlane((int)g);
     };
-    // load stage: tuple group ltg, entries [lj, lj + kRtChunk) of each tuple;
+    // load stage: tuple group ltg, entries [lj, lj + kRsChunk) of each tuple;
     // ntg is the group after it, whose spans are in nst, nen
     int ltg = wave, ntg = n_tg;
     uint32_t lj = 0, lmax = 0, lst = 0, len = 0, nst = 0, nen = 0;
@@ -647,15 +1005,15 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       ntg = grab();
     }
     spans_of(ntg, nst, nen);
-    auto chunk_of_l = [&]() -> RtChunk {
-      const uint32_t n = lmax > lj ? min((uint32_t)kRtChunk, lmax - lj) : 0u;
-      return RtChunk{ltg, (n + 3u) & ~3u, lj + kRtChunk >= lmax};
+    auto chunk_of_l = [&]() -> RsChunk {
+      const uint32_t n = lmax > lj ? min((uint32_t)kRsChunk, lmax - lj) : 0u;
+      return RsChunk{ltg, (n + 3u) & ~3u, lj + kRsChunk >= lmax};
     };
     // the next group's spans are reloaded on every step (cache hits), so that a
     // switch of group only moves values loaded a step earlier
     auto advance = [&]() {
       if (ltg < n_tg) {
-        lj += kRtChunk;
+        lj += kRsChunk;
         if (lj >= lmax) {
           ltg = ntg;
           lj = 0;
@@ -688,7 +1046,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       if (d < n1) {
         g = key;
       } else {
-        g.x = DEEP_LDS ? (uint32_t)m + 1u + (d - n1) : (kRtGlobal | (d - n1));
+        g.x = kRtGlobal | (d - n1);
         g.y = __float_as_uint(1.0f);
       }
       if (!__builtin_amdgcn_inverse_ballot_w64(ok)) g = make_uint2(zrow, 0u);
@@ -697,7 +1055,6 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // an H row in LDS or in the workspace; both loads are issued and the values
     // selected (a select of the two pointers would make a flat pointer)
     auto row_f4 = [&](uint32_t r) -> float4 {
-      if (DEEP_LDS) return lds_load4(qb + r * (kRtKT * 4));
       const bool g = (r & kRtGlobal) != 0;
       const float4 xl = lds_load4(qb + (g ? zrow : r) * (kRtKT * 4));
       float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -707,31 +1064,29 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // Pipeline: codes of chunk L load while chunk G's codes are translated and
     // chunk C, staged in LDS, is summed.  Two register sets alternate between the
     // roles of G and L, so no loaded value is ever copied.
-    RtChunk G = chunk_of_l();
-    RtChunk C{n_tg, 0u, false};
+    RsChunk G = chunk_of_l();
+    RsChunk C{n_tg, 0u, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     auto step = [&](uint32_t gd0, uint32_t gd1, uint64_t gok0, uint64_t gok1, uint32_t &ld0,
                     uint32_t &ld1, uint64_t &lok0, uint64_t &lok1) {
       advance();
       const uint2 key0 = key_load(rs_node, gd0), key1 = key_load(rs_node, gd1);
-      const RtChunk L = chunk_of_l();
+      const RsChunk L = chunk_of_l();
       load_codes(ld0, ld1, lok0, lok1);
       bool done = false;
-      if (C.tg < n_tg && C.steps == kRtChunk) {
+      if (C.tg < n_tg && C.steps == kRsChunk) {
         // a full chunk: all staged entries first, then the rows, so that many
         // LDS reads are in flight (rows in the workspace take the loop below)
-        uint2 e[kRtChunk];
+        uint2 e[kRsChunk];
 #pragma unroll
-        for (int t = 0; t < kRtChunk; ++t) e[t] = stage[t * kRtGroups + grp];
+        for (int t = 0; t < kRsChunk; ++t) e[t] = stage[t * kRsGroups + grp];
         uint32_t any = 0;
-        if (!DEEP_LDS) {
 #pragma unroll
-          for (int t = 0; t < kRtChunk; ++t) any |= e[t].x;
-        }
+        for (int t = 0; t < kRsChunk; ++t) any |= e[t].x;
         if (!(any & kRtGlobal)) {
           // rows in blocks of 8 reads issued back to back
 #pragma unroll
-          for (int h = 0; h < kRtChunk; h += 8) {
+          for (int h = 0; h < kRsChunk; h += 8) {
             float4 xr[8];
 #pragma unroll
             for (int t = 0; t < 8; ++t)
@@ -745,10 +1100,10 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       }
       if (C.tg < n_tg && !done) {
         for (uint32_t t = 0; t < C.steps; t += 4) {
-          const uint2 e0 = stage[(t + 0) * kRtGroups + grp], e1 = stage[(t + 1) * kRtGroups + grp];
-          const uint2 e2 = stage[(t + 2) * kRtGroups + grp], e3 = stage[(t + 3) * kRtGroups + grp];
+          const uint2 e0 = stage[(t + 0) * kRsGroups + grp], e1 = stage[(t + 1) * kRsGroups + grp];
+          const uint2 e2 = stage[(t + 2) * kRsGroups + grp], e3 = stage[(t + 3) * kRsGroups + grp];
           float4 x0, x1, x2, x3;
-          if (!DEEP_LDS && ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal)) {
+          if ((e0.x | e1.x | e2.x | e3.x) & kRtGlobal) {
             x0 = row_f4(e0.x);
             x1 = row_f4(e1.x);
             x2 = row_f4(e2.x);
@@ -767,7 +1122,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       }
       if (C.tg < n_tg) {
         if (C.last) {
-          const int r = C.tg * kRtGroups + grp;
+          const int r = C.tg * kRsGroups + grp;
           if (r < nrows) {
             float *rr = R + (bt.row_base + r) * ldr + k0 + q;
             if (q + 3 < kt) {
@@ -785,8 +1140,8 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
         }
       }
       // entries of chunk G: entry t of tuple grp goes to stage[t * 8 + grp]
-      stage[(sub + 0) * kRtGroups + grp] = entry(gd0, key0, gok0);
-      stage[(sub + 8) * kRtGroups + grp] = entry(gd1, key1, gok1);
+      stage[(sub + 0) * kRsGroups + grp] = entry(gd0, key0, gok0);
+      stage[(sub + 8) * kRsGroups + grp] = entry(gd1, key1, gok1);
       __builtin_amdgcn_wave_barrier();
       C = G;
       G = L;
@@ -1342,14 +1697,17 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
     return p;
   }
   if (right) {
-    const size_t fixed = kRtStageBytes + ((size_t)m + 1) * kRtKT * 4;
+    // deep rows in LDS: right_tiled_kernel; else right_staged_kernel, with the
+    // deep rows in the workspace and a per-wave stage in LDS
+    const size_t tile = ((size_t)m + 1) * kRtKT * 4;
     const size_t lds_max = kLdsMax - kRtStaticBytes;
-    if (k >= 4 && fixed <= lds_max) {
+    const size_t with_deep = tile + (size_t)d->max_deep * kRtKT * 4;
+    if (k >= 4 && (with_deep <= lds_max || kRsStageBytes + tile <= lds_max)) {
       p.path = kPathTiled;
       p.n_tiles = (k + kRtKT - 1) / kRtKT;
       p.tw = kRtKT;
-      p.deep_lds = fixed + (size_t)d->max_deep * kRtKT * 4 <= lds_max;
-      p.lds = p.deep_lds ? fixed + (size_t)d->max_deep * kRtKT * 4 : fixed;
+      p.deep_lds = with_deep <= lds_max;
+      p.lds = p.deep_lds ? with_deep : kRsStageBytes + tile;
       // workers per XCD: one per CU, fewer when there are fewer items
       const int64_t items = (d->info.n_batches + kXcd - 1) / kXcd * p.n_tiles;
       p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
@@ -1576,14 +1934,13 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
                   (long long)plan.ws_floats * 4);
     const int m = d->info.n_cols;
     if (plan.deep_lds) {
-      if ((st = allow_lds(right_tiled_kernel<true>, plan.lds))) return st;
-      hipLaunchKernelGGL(right_tiled_kernel<true>, dim3(plan.grid), dim3(kRtBlock), plan.lds, s,
-                         im, nb, plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr, (float *)ws,
-                         (int64_t)0);
+      if ((st = allow_lds(right_tiled_kernel, plan.lds))) return st;
+      hipLaunchKernelGGL(right_tiled_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im, nb,
+                         plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr);
     } else {
-      if ((st = allow_lds(right_tiled_kernel<false>, plan.lds))) return st;
-      hipLaunchKernelGGL(right_tiled_kernel<false>, dim3(plan.grid), dim3(kRtBlock), plan.lds,
-                         s, im, nb, plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr, (float *)ws,
+      if ((st = allow_lds(right_staged_kernel, plan.lds))) return st;
+      hipLaunchKernelGGL(right_staged_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im,
+                         nb, plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr, (float *)ws,
                          (int64_t)d->max_deep * kRtKT);
     }
     return launch_status("right_tiled_kernel");
