@@ -577,11 +577,51 @@ __device__ inline void fma8_bcast(float2 &acc, uint32_t mu, const float2 (&x)[8]
 #undef TOC_FMA8
 #undef TOC_FMAC2
 
+// The same for 4 columns per lane: acc += mu(lane L) * x[i] for 4 entries.
+#define TOC_FMAC4(I, L)                                                                  \
+  "v_fmac_f32_dpp %[ax], %[mu], %[x" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"                                          \
+  "v_fmac_f32_dpp %[ay], %[mu], %[y" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"                                          \
+  "v_fmac_f32_dpp %[az], %[mu], %[z" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"                                          \
+  "v_fmac_f32_dpp %[aw], %[mu], %[w" #I "] row_newbcast:" #L                             \
+  " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+#define TOC_X4(I) [x##I] "v"(x[I].x), [y##I] "v"(x[I].y), [z##I] "v"(x[I].z), [w##I] "v"(x[I].w)
+#define TOC_FMA4X4(L0, L1, L2, L3)                                                       \
+  asm volatile("s_nop 1\n\t" TOC_FMAC4(0, L0) TOC_FMAC4(1, L1) TOC_FMAC4(2, L2)          \
+                   TOC_FMAC4(3, L3)                                                       \
+               : [ax] "+v"(acc.x), [ay] "+v"(acc.y), [az] "+v"(acc.z), [aw] "+v"(acc.w)   \
+               : [mu] "v"(mu), TOC_X4(0), TOC_X4(1), TOC_X4(2), TOC_X4(3))
+
+template <int T0>
+__device__ inline void fma4x4_bcast(float4 &acc, uint32_t mu, const float4 (&x)[4]) {
+  static_assert(T0 % 4 == 0 && T0 < 16, "lanes T0 .. T0 + 3 of a row");
+  if constexpr (T0 == 0) {
+    TOC_FMA4X4(0, 1, 2, 3);
+  } else if constexpr (T0 == 4) {
+    TOC_FMA4X4(4, 5, 6, 7);
+  } else if constexpr (T0 == 8) {
+    TOC_FMA4X4(8, 9, 10, 11);
+  } else {
+    TOC_FMA4X4(12, 13, 14, 15);
+  }
+}
+#undef TOC_FMA4X4
+#undef TOC_X4
+#undef TOC_FMAC4
+
 // The H rows of entries T0 .. T0 + 7 of a half chunk (rb: the row address held
 // by each lane, qoff: this lane's columns in a row).
 template <int T0>
 __device__ inline void load8_bcast(uint32_t rb, uint32_t qoff, float2 (&x)[8]) {
   static_for<8>([&](auto i) { x[i] = lds_load2(row_bcast<T0 + decltype(i)::value>(rb) + qoff); });
+}
+
+// The rows of entries T0 .. T0 + 3 with 4 columns per lane (16-byte reads).
+template <int T0>
+__device__ inline void load4x4_bcast(uint32_t rb, uint32_t qoff, float4 (&x)[4]) {
+  static_for<4>([&](auto i) { x[i] = lds_load4(row_bcast<T0 + decltype(i)::value>(rb) + qoff); });
 }
 
 struct RtChunk {
@@ -1184,8 +1224,11 @@ constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
 
 // LDS bytes of the per-wave stages and of the column tables
+// (groups of 16 lanes pass entries round with the DPP row broadcast: no stage)
 template <int TW>
-constexpr uint32_t lt_stage_bytes() { return (uint32_t)kLtWaves * (TW / 4) * (kWave / (TW / 4)) * 8; }
+constexpr uint32_t lt_stage_bytes() {
+  return TW / 4 == kRtLanes ? 0u : (uint32_t)kLtWaves * (TW / 4) * (kWave / (TW / 4)) * 8;
+}
 
 // LDS byte offset of the rows: stages, then the batch's column index (Loff, Ost,
 // Toff, Ord: m + 1 entries each, as in the image) and Coff (max_tree + 1)
@@ -1230,6 +1273,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
+  constexpr bool DPP = LPG == kRtLanes;       // a group is one 16-lane row: entries by broadcast
+  const uint32_t rb0 = lds_base(smem4) + rows_b;                      // LDS address of row 0
+  const uint32_t qoff = 4u * (uint32_t)q;
   const uint32_t zrow = (uint32_t)max_rows;
   const uint32_t trow0 = zrow + 1u;
   float *Hg = ws + blockIdx.x * slot_floats;
@@ -1423,6 +1469,11 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     LtChunk G = chunk_of_l();
     LtChunk C{n_cg, 0u, 0u, false, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    // 16-lane groups: chunk C's translated entries stay in registers (lane t
+    // holds entry t: LDS address of its row, or kRtGlobal | tree row in the
+    // workspace, and its multiplier) and are broadcast along the row
+    const uint32_t zaddr = rb0 + zrow * RB;
+    uint32_t cra = zaddr, cmu = 0u;
     auto step = [&](uint32_t gw, uint32_t gkind, uint32_t glcode, uint32_t &lw, uint32_t &lkind,
                     uint32_t &llcode) {
       advance();
@@ -1439,41 +1490,86 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       const uint2 key = key_load(rs_node, code);
       const LtChunk L = chunk_of_l();
       load_entry(lw, lkind, llcode);
-      // C: the staged chunk; a full chunk of leaf entries reads only LDS rows, 8
-      // of them issued back to back
-      if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
-#pragma unroll
-        for (int h = 0; h < CH; h += 8) {
-          uint2 e[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) e[t] = stage[(h + t) * GPW + grp];
-          float4 xr[8];
-#pragma unroll
-          for (int t = 0; t < 8; ++t) xr[t] = lds_load4(qb + e[t].x * RB);
-#pragma unroll
-          for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[t].y), xr[t], acc);
-          __builtin_amdgcn_sched_barrier(0);
+      if constexpr (DPP) {
+        if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
+          // a full chunk of leaf entries: LDS rows only, each block's reads
+          // issued before the previous block's FMAs
+          float4 x0[4], x1[4];
+          load4x4_bcast<0>(cra, qoff, x0);
+          load4x4_bcast<4>(cra, qoff, x1);
+          fma4x4_bcast<0>(acc, cmu, x0);
+          load4x4_bcast<8>(cra, qoff, x0);
+          fma4x4_bcast<4>(acc, cmu, x1);
+          load4x4_bcast<12>(cra, qoff, x1);
+          fma4x4_bcast<8>(acc, cmu, x0);
+          fma4x4_bcast<12>(acc, cmu, x1);
+        } else if (C.cg < n_cg) {
+          // blocks of 4 entries; tree rows may be in the workspace: both loads
+          // are issued and the values selected
+          const bool any_ws = !TREE_LDS && C.tree;
+          static_for<CH / 4>([&](auto bc) {
+            constexpr int t0 = 4 * decltype(bc)::value;
+            if (C.steps > (uint32_t)t0) {
+              float4 xv[4];
+              float mt[4];
+              static_for<4>([&](auto ic) {
+                constexpr int i = decltype(ic)::value;
+                const uint32_t r = row_bcast<t0 + i>(cra);
+                mt[i] = __uint_as_float(row_bcast<t0 + i>(cmu));
+                if (any_ws) {
+                  const bool g = (r & kRtGlobal) != 0;
+                  const float4 xl = lds_load4((g ? zaddr : r) + qoff);
+                  float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
+                  if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
+                  xv[i] = g ? xg : xl;
+                } else {
+                  xv[i] = lds_load4(r + qoff);
+                }
+              });
+              static_for<4>([&](auto ic) {
+                constexpr int i = decltype(ic)::value;
+                acc = f4fma(mt[i], xv[i], acc);
+              });
+            }
+          });
         }
-      } else if (C.cg < n_cg) {
-        for (uint32_t t = 0; t < C.steps; t += 4) {
-          const uint2 e0 = stage[(t + 0) * GPW + grp], e1 = stage[(t + 1) * GPW + grp];
-          const uint2 e2 = stage[(t + 2) * GPW + grp], e3 = stage[(t + 3) * GPW + grp];
-          float4 x0, x1, x2, x3;
-          if (C.tree) {
-            x0 = row_f4(e0.x);
-            x1 = row_f4(e1.x);
-            x2 = row_f4(e2.x);
-            x3 = row_f4(e3.x);
-          } else {
-            x0 = lds_load4(qb + e0.x * RB);
-            x1 = lds_load4(qb + e1.x * RB);
-            x2 = lds_load4(qb + e2.x * RB);
-            x3 = lds_load4(qb + e3.x * RB);
+      } else {
+        // C: the staged chunk; a full chunk of leaf entries reads only LDS rows, 8
+        // of them issued back to back
+        if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
+  #pragma unroll
+          for (int h = 0; h < CH; h += 8) {
+            uint2 e[8];
+  #pragma unroll
+            for (int t = 0; t < 8; ++t) e[t] = stage[(h + t) * GPW + grp];
+            float4 xr[8];
+  #pragma unroll
+            for (int t = 0; t < 8; ++t) xr[t] = lds_load4(qb + e[t].x * RB);
+  #pragma unroll
+            for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[t].y), xr[t], acc);
+            __builtin_amdgcn_sched_barrier(0);
           }
-          acc = f4fma(__uint_as_float(e0.y), x0, acc);
-          acc = f4fma(__uint_as_float(e1.y), x1, acc);
-          acc = f4fma(__uint_as_float(e2.y), x2, acc);
-          acc = f4fma(__uint_as_float(e3.y), x3, acc);
+        } else if (C.cg < n_cg) {
+          for (uint32_t t = 0; t < C.steps; t += 4) {
+            const uint2 e0 = stage[(t + 0) * GPW + grp], e1 = stage[(t + 1) * GPW + grp];
+            const uint2 e2 = stage[(t + 2) * GPW + grp], e3 = stage[(t + 3) * GPW + grp];
+            float4 x0, x1, x2, x3;
+            if (C.tree) {
+              x0 = row_f4(e0.x);
+              x1 = row_f4(e1.x);
+              x2 = row_f4(e2.x);
+              x3 = row_f4(e3.x);
+            } else {
+              x0 = lds_load4(qb + e0.x * RB);
+              x1 = lds_load4(qb + e1.x * RB);
+              x2 = lds_load4(qb + e2.x * RB);
+              x3 = lds_load4(qb + e3.x * RB);
+            }
+            acc = f4fma(__uint_as_float(e0.y), x0, acc);
+            acc = f4fma(__uint_as_float(e1.y), x1, acc);
+            acc = f4fma(__uint_as_float(e2.y), x2, acc);
+            acc = f4fma(__uint_as_float(e3.y), x3, acc);
+          }
         }
       }
       if (C.cg < n_cg) {
@@ -1502,9 +1598,15 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           acc = make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
-      // S: entry sub of column grp goes to stage[sub * GPW + grp]
-      stage[sub * GPW + grp] = make_uint2(row, gkind == 2u ? 0u : key.y);
-      __builtin_amdgcn_wave_barrier();
+      if constexpr (DPP) {
+        // entries of chunk G become chunk C
+        cra = gkind == 2u ? zaddr : ((row & kRtGlobal) ? row : rb0 + row * RB);
+        cmu = gkind == 2u ? 0u : key.y;
+      } else {
+        // S: entry sub of column grp goes to stage[sub * GPW + grp]
+        stage[sub * GPW + grp] = make_uint2(row, gkind == 2u ? 0u : key.y);
+        __builtin_amdgcn_wave_barrier();
+      }
       C = G;
       G = L;
     };
