@@ -106,6 +106,13 @@ __device__ inline toc_batch uniform_batch(const toc_batch *p) {
   return t;
 }
 
+// Maximum of v over the wave, as a wave-uniform value.
+__device__ inline uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
 // Load that bypasses the per-CU L1, for values other waves updated with atomics.
 __device__ inline float coherent_load(const float *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1222,6 +1229,7 @@ constexpr int kLtBlock = 1024;
 constexpr int kLtWaves = kLtBlock / kWave;
 constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
+constexpr int kLtU = 4;                           // tree codes per group at a time
 
 // LDS bytes of the per-wave stages and of the column tables
 // (groups of 16 lanes pass entries round with the DPP row broadcast: no stage)
@@ -1344,48 +1352,94 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     }
     const uint32_t obase = n1 > ni ? oo[ni] : 0u;
     __syncthreads();
-    // tree codes, deepest level first; a group per code
+    // Tree codes, deepest level first: H = own occurrences' G rows + children's
+    // H rows.  A group takes kLtU codes at a time and issues their loads
+    // together; a code's occurrence rows are broadcast along its group.
     auto tree_row = [&](uint32_t h) -> float * {
       return TREE_LDS ? Rw + (size_t)(trow0 + h) * TW : Hg + (int64_t)h * TW;
     };
+    // value v of lane i of the caller's group
+    auto gbcast = [&](uint32_t v, auto ic) -> uint32_t {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (LPG == kRtLanes) return row_bcast<i>(v);
+      else return (uint32_t)__shfl((int)v, grp * LPG + i, kWave);
+    };
     const int gidx = wave * GPW + grp;
+    constexpr uint32_t NG = kLtWaves * GPW;
     for (int d = bt.n_levels; d >= 1; --d) {
       const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
-      for (uint32_t c = a + gidx; c < e; c += kLtWaves * GPW) {
-        const uint32_t h = hrow(c);
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        // occurrences: the group's lanes load up to LPG of their rows at once and
-        // pass them round with lane shuffles
-        const uint32_t o0 = oo[c], o1 = oo[c + 1];
-        for (uint32_t ob = o0; ob < o1; ob += LPG) {
-          const uint32_t mine = ob + sub < o1 ? orow[ob + sub] & ~kFirstOcc : zrow;
-          const uint32_t n = min((uint32_t)LPG, o1 - ob);
-          for (uint32_t i = 0; i < n; ++i) {
-            const uint32_t r = (uint32_t)__shfl((int)mine, grp * LPG + (int)i, kWave);
-            const float4 g = lds_load4(qb + r * RB);
-            acc.x += g.x;
-            acc.y += g.y;
-            acc.z += g.z;
-            acc.w += g.w;
+      for (uint32_t c0 = a + gidx; c0 < e; c0 += kLtU * NG) {
+        uint32_t h[kLtU], o0[kLtU], o1[kLtU], k0[kLtU], k1[kLtU], mine[kLtU];
+        uint32_t nmax = 0, cmax = 0;
+#pragma unroll
+        for (int u = 0; u < kLtU; ++u) {
+          const uint32_t c = c0 + u * NG;
+          const bool in = c < e;
+          const uint32_t cc = in ? c : c0;
+          h[u] = hrow(cc);
+          o0[u] = oo[cc];
+          o1[u] = in ? oo[cc + 1] : o0[u];
+          k0[u] = Coff[h[u]];
+          k1[u] = in ? Coff[h[u] + 1] : k0[u];
+        }
+#pragma unroll
+        for (int u = 0; u < kLtU; ++u) {
+          mine[u] = o0[u] + sub < o1[u] ? orow[o0[u] + sub] & ~kFirstOcc : zrow;
+          nmax = max(nmax, min(o1[u] - o0[u], (uint32_t)LPG));
+          cmax = max(cmax, k1[u] - k0[u]);
+        }
+        nmax = wave_max_u32(nmax);
+        cmax = wave_max_u32(cmax);
+        float4 acc[kLtU];
+#pragma unroll
+        for (int u = 0; u < kLtU; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        // children: one per code at a time, all codes' loads in flight
+        for (uint32_t cb = 0; cb < cmax; ++cb) {
+          float4 g[kLtU];
+#pragma unroll
+          for (int u = 0; u < kLtU; ++u)
+            g[u] = k0[u] + cb < k1[u] ? *(const float4 *)&tree_row(hrow(k0[u] + cb))[q]
+                                      : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int u = 0; u < kLtU; ++u) {
+            acc[u].x += g[u].x;
+            acc[u].y += g[u].y;
+            acc[u].z += g[u].z;
+            acc[u].w += g[u].w;
           }
         }
-        // children: H rows, four loads in flight
-        const uint32_t c0 = Coff[h], c1 = Coff[h + 1];
-        for (uint32_t ch = c0; ch < c1; ch += 4) {
-          float4 g[4];
+        // occurrences: the first LPG of each code by broadcast
+        static_for<LPG>([&](auto ic) {
+          if (nmax > (uint32_t)decltype(ic)::value) {
+            float4 g[kLtU];
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            g[u] = ch + u < c1 ? *(const float4 *)&tree_row(hrow(ch + u))[q]
-                               : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int u = 0; u < kLtU; ++u) g[u] = lds_load4(qb + gbcast(mine[u], ic) * RB);
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            acc.x += g[u].x;
-            acc.y += g[u].y;
-            acc.z += g[u].z;
-            acc.w += g[u].w;
+            for (int u = 0; u < kLtU; ++u) {
+              acc[u].x += g[u].x;
+              acc[u].y += g[u].y;
+              acc[u].z += g[u].z;
+              acc[u].w += g[u].w;
+            }
           }
+        });
+#pragma unroll
+        for (int u = 0; u < kLtU; ++u) {
+          // occurrences past the first LPG (rare): one at a time
+          for (uint32_t ob = o0[u] + LPG; ob < o1[u]; ob += LPG) {
+            const uint32_t mo = ob + sub < o1[u] ? orow[ob + sub] & ~kFirstOcc : zrow;
+            const uint32_t n = min((uint32_t)LPG, o1[u] - ob);
+            for (uint32_t i = 0; i < n; ++i) {
+              const uint32_t r = (uint32_t)__shfl((int)mo, grp * LPG + (int)i, kWave);
+              const float4 g = lds_load4(qb + r * RB);
+              acc[u].x += g.x;
+              acc[u].y += g.y;
+              acc[u].z += g.z;
+              acc[u].w += g.w;
+            }
+          }
+          if (c0 + u * NG < e) *(float4 *)&tree_row(h[u])[q] = acc[u];
         }
-        *(float4 *)&tree_row(h)[q] = acc;
       }
       __syncthreads();
     }
