@@ -1282,6 +1282,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   constexpr bool DPP = LPG == kRtLanes;       // a group is one 16-lane row: entries by broadcast
+  constexpr int PER = 1;                      // entries per lane and chunk (2 measured slower on
+                                              // columns of ~50 entries)
+  constexpr int CHK = PER * LPG;              // entries per column per chunk
   const uint32_t rb0 = lds_base(smem4) + rows_b;                      // LDS address of row 0
   const uint32_t qoff = 4u * (uint32_t)q;
   const uint32_t zrow = (uint32_t)max_rows;
@@ -1468,7 +1471,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       c.lcode = Loff[j];
       return c;
     };
-    // load stage: column group lcg, entries [lj, lj + CH) of each column
+    // load stage: column group lcg, entries [lj, lj + CHK) of each column
     int lcg = wave, ncg = n_cg;
     uint32_t lj = 0, lmax = 0;
     ColSpan lc{0u, 0u, 0u, 0u, 0u};
@@ -1478,13 +1481,18 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       ncg = grab();
     }
     auto chunk_of_l = [&]() -> LtChunk {
-      const uint32_t n = lmax > lj ? min((uint32_t)CH, lmax - lj) : 0u;
-      const bool tree = __ballot(lj + (uint32_t)sub >= lc.nl && lj + (uint32_t)sub < lc.nl + lc.nt) != 0;
-      return LtChunk{lcg, (n + 3u) & ~3u, lj, lj + CH >= lmax, tree};
+      const uint32_t n = lmax > lj ? min((uint32_t)CHK, lmax - lj) : 0u;
+      bool tree = false;
+#pragma unroll
+      for (int h = 0; h < PER; ++h) {
+        const uint32_t e = lj + (uint32_t)(sub + h * LPG);
+        tree |= __ballot(e >= lc.nl && e < lc.nl + lc.nt) != 0;
+      }
+      return LtChunk{lcg, (n + 3u) & ~3u, lj, lj + CHK >= lmax, tree};
     };
     auto advance = [&]() {
       if (lcg < n_cg) {
-        lj += CH;
+        lj += CHK;
         if (lj >= lmax) {
           lcg = ncg;
           lj = 0;
@@ -1499,15 +1507,19 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     };
     const BufRes rs_node = key_res(node, nc);
     const uint32_t *dummy = lvl;   // a valid address for lanes without an entry
-    // L: the entry word of each lane (occ_row word of a leaf occurrence, or the
-    // code of a tree entry) and its kind: 0 leaf, 1 tree, 2 none
-    auto load_entry = [&](uint32_t &w, uint32_t &kind, uint32_t &lcode) {
-      const uint32_t e = lj + (uint32_t)sub;
+    // L: the entry words of each lane (entries sub + h * LPG of the chunk: the
+    // occ_row word of a leaf occurrence, or the code of a tree entry) and their
+    // kinds: 0 leaf, 1 tree, 2 none
+    auto load_entry = [&](uint32_t (&w)[PER], uint32_t (&kind)[PER], uint32_t &lcode) {
       const bool live = lcg < n_cg;
-      kind = !live || e >= lc.nl + lc.nt ? 2u : (e < lc.nl ? 0u : 1u);
-      const uint32_t *p = kind == 0u ? orow + obase + lc.ost + e
-                                     : (kind == 1u ? tl + lc.tof + (e - lc.nl) : dummy);
-      w = *p;
+#pragma unroll
+      for (int h = 0; h < PER; ++h) {
+        const uint32_t e = lj + (uint32_t)(sub + h * LPG);
+        kind[h] = !live || e >= lc.nl + lc.nt ? 2u : (e < lc.nl ? 0u : 1u);
+        const uint32_t *p = kind[h] == 0u ? orow + obase + lc.ost + e
+                                          : (kind[h] == 1u ? tl + lc.tof + (e - lc.nl) : dummy);
+        w[h] = *p;
+      }
       lcode = lc.lcode;
     };
     auto row_f4 = [&](uint32_t r) -> float4 {
@@ -1524,52 +1536,81 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     LtChunk C{n_cg, 0u, 0u, false, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     // 16-lane groups: chunk C's translated entries stay in registers (lane t
-    // holds entry t: LDS address of its row, or kRtGlobal | tree row in the
-    // workspace, and its multiplier) and are broadcast along the row
+    // holds entries t + 16 h: LDS address of the row, or kRtGlobal | tree row in
+    // the workspace, and the multiplier) and are broadcast along the row
     const uint32_t zaddr = rb0 + zrow * RB;
-    uint32_t cra = zaddr, cmu = 0u;
-    auto step = [&](uint32_t gw, uint32_t gkind, uint32_t glcode, uint32_t &lw, uint32_t &lkind,
-                    uint32_t &llcode) {
+    uint32_t cra[PER], cmu[PER];
+#pragma unroll
+    for (int h = 0; h < PER; ++h) {
+      cra[h] = zaddr;
+      cmu[h] = 0u;
+    }
+    auto step = [&](const uint32_t (&gw)[PER], const uint32_t (&gkind)[PER], uint32_t glcode,
+                    uint32_t (&lw)[PER], uint32_t (&lkind)[PER], uint32_t &llcode) {
       advance();
-      // G: codes of the chunk loaded a step ago, then their key pairs
-      const uint64_t firsts = __ballot(gkind == 0u && (gw & kFirstOcc));
-      const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
-      const uint32_t base = G.first == 0u ? glcode - 1u : gcode;
-      // branch-free: leaf, tree or no entry
-      const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
-      const uint32_t trow = TREE_LDS ? trow0 + hrow(gw) : (kRtGlobal | hrow(gw));
-      const uint32_t code = gkind == 0u ? lcode : (gkind == 1u ? gw : 0xFFFFFFFFu);
-      const uint32_t row = gkind == 0u ? (gw & ~kFirstOcc) : (gkind == 1u ? trow : zrow);
-      gcode = base + (uint32_t)__popc(gb);
-      const uint2 key = key_load(rs_node, code);
+      // G: entries of the chunk loaded a step ago; the code of a leaf occurrence
+      // is the column's first leaf code - 1 plus the first-occurrence bits up to
+      // it (carried along the column in gcode); then the key pairs
+      uint32_t base = G.first == 0u ? glcode - 1u : gcode;
+      uint32_t code[PER], row[PER];
+#pragma unroll
+      for (int h = 0; h < PER; ++h) {
+        const uint64_t firsts = __ballot(gkind[h] == 0u && (gw[h] & kFirstOcc));
+        const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
+        // branch-free: leaf, tree or no entry
+        const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
+        const uint32_t trow = TREE_LDS ? trow0 + hrow(gw[h]) : (kRtGlobal | hrow(gw[h]));
+        code[h] = gkind[h] == 0u ? lcode : (gkind[h] == 1u ? gw[h] : 0xFFFFFFFFu);
+        row[h] = gkind[h] == 0u ? (gw[h] & ~kFirstOcc) : (gkind[h] == 1u ? trow : zrow);
+        base += (uint32_t)__popc(gb);
+      }
+      gcode = base;
+      uint2 key[PER];
+#pragma unroll
+      for (int h = 0; h < PER; ++h) key[h] = key_load(rs_node, code[h]);
       const LtChunk L = chunk_of_l();
       load_entry(lw, lkind, llcode);
       if constexpr (DPP) {
-        if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
+        constexpr int NB = CHK / 4;             // blocks of 4 entries
+        if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CHK) {
           // a full chunk of leaf entries: LDS rows only, each block's reads
           // issued before the previous block's FMAs
-          float4 x0[4], x1[4];
-          load4x4_bcast<0>(cra, qoff, x0);
-          load4x4_bcast<4>(cra, qoff, x1);
-          fma4x4_bcast<0>(acc, cmu, x0);
-          load4x4_bcast<8>(cra, qoff, x0);
-          fma4x4_bcast<4>(acc, cmu, x1);
-          load4x4_bcast<12>(cra, qoff, x1);
-          fma4x4_bcast<8>(acc, cmu, x0);
-          fma4x4_bcast<12>(acc, cmu, x1);
+          float4 xa[4], xb[4];
+          load4x4_bcast<0>(cra[0], qoff, xa);
+          static_for<NB>([&](auto bc) {
+            constexpr int bk = decltype(bc)::value;
+            if constexpr (bk + 1 < NB) {
+              constexpr int nb = bk + 1;
+              if constexpr (bk % 2 == 0) load4x4_bcast<4 * (nb % 4)>(cra[nb / 4], qoff, xb);
+              else load4x4_bcast<4 * (nb % 4)>(cra[nb / 4], qoff, xa);
+            }
+            if constexpr (bk % 2 == 0) fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xa);
+            else fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xb);
+          });
+        } else if (C.cg < n_cg && (TREE_LDS || !C.tree)) {
+          // a partial chunk, rows in LDS: blocks of 4 entries
+          static_for<NB>([&](auto bc) {
+            constexpr int bk = decltype(bc)::value;
+            if (C.steps > (uint32_t)(4 * bk)) {
+              float4 xv[4];
+              load4x4_bcast<4 * (bk % 4)>(cra[bk / 4], qoff, xv);
+              fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xv);
+            }
+          });
         } else if (C.cg < n_cg) {
           // blocks of 4 entries; tree rows may be in the workspace: both loads
           // are issued and the values selected
           const bool any_ws = !TREE_LDS && C.tree;
-          static_for<CH / 4>([&](auto bc) {
-            constexpr int t0 = 4 * decltype(bc)::value;
-            if (C.steps > (uint32_t)t0) {
+          static_for<NB>([&](auto bc) {
+            constexpr int bk = decltype(bc)::value;
+            constexpr int t0 = 4 * (bk % 4), hh = bk / 4;
+            if (C.steps > (uint32_t)(4 * bk)) {
               float4 xv[4];
               float mt[4];
               static_for<4>([&](auto ic) {
                 constexpr int i = decltype(ic)::value;
-                const uint32_t r = row_bcast<t0 + i>(cra);
-                mt[i] = __uint_as_float(row_bcast<t0 + i>(cmu));
+                const uint32_t r = row_bcast<t0 + i>(cra[hh]);
+                mt[i] = __uint_as_float(row_bcast<t0 + i>(cmu[hh]));
                 if (any_ws) {
                   const bool g = (r & kRtGlobal) != 0;
                   const float4 xl = lds_load4((g ? zaddr : r) + qoff);
@@ -1588,6 +1629,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           });
         }
       } else {
+        static_assert(DPP || PER == 1, "the staged path takes one entry per lane");
         // C: the staged chunk; a full chunk of leaf entries reads only LDS rows, 8
         // of them issued back to back
         if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CH) {
@@ -1625,7 +1667,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
             acc = f4fma(__uint_as_float(e3.y), x3, acc);
           }
         }
-      }
+            }
       if (C.cg < n_cg) {
         if (C.last) {
           const int o = C.cg * GPW + grp;
@@ -1654,17 +1696,20 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       }
       if constexpr (DPP) {
         // entries of chunk G become chunk C
-        cra = gkind == 2u ? zaddr : ((row & kRtGlobal) ? row : rb0 + row * RB);
-        cmu = gkind == 2u ? 0u : key.y;
+#pragma unroll
+        for (int h = 0; h < PER; ++h) {
+          cra[h] = gkind[h] == 2u ? zaddr : ((row[h] & kRtGlobal) ? row[h] : rb0 + row[h] * RB);
+          cmu[h] = gkind[h] == 2u ? 0u : key[h].y;
+        }
       } else {
         // S: entry sub of column grp goes to stage[sub * GPW + grp]
-        stage[sub * GPW + grp] = make_uint2(row, gkind == 2u ? 0u : key.y);
+        stage[sub * GPW + grp] = make_uint2(row[0], gkind[0] == 2u ? 0u : key[0].y);
         __builtin_amdgcn_wave_barrier();
       }
       C = G;
       G = L;
     };
-    uint32_t wA, kA, cA, wB, kB, cB;
+    uint32_t wA[PER], kA[PER], wB[PER], kB[PER], cA, cB;
     load_entry(wA, kA, cA);
     while (G.cg < n_cg || C.cg < n_cg) {
       step(wA, kA, cA, wB, kB, cB);
