@@ -147,7 +147,9 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  * are local indices 0..n_codes-1, stored from code_base; local code c is at
  * depth d when level[lvl_base+d-1] <= c < level[lvl_base+d] (level[lvl_base] = 0).
  * Depth-1 codes come first; among them the n_int1 codes that have children
- * precede the others.
+ * precede the others.  The left multiplication reads codes at positions: a
+ * depth-1 code without children (a leaf) is at position n_int1 + its rank in
+ * (key column, code) order, every other code at its own index.
  *   batches : toc_batch[n_batches]
  *   level   : uint32 per batch n_levels+1 entries (lvl_base)
  *   key     : toc_key of each code (its key pair, 8 bytes), so that a code's key
@@ -155,26 +157,29 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   link    : toc_link of each code (its parent and depth, 8 bytes)
  *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
  *   dcodes  : uint32 local code of each entry of D (d_base)
- *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b)
- *   occ_row : uint32 row of each entry of D, grouped by code (d_base): D inverted,
- *             the index set of the sum that defines G(x) in Theorem 2; bit 31 is
- *             set on the first entry of each code
+ *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b),
+ *             by position
+ *   occ_row : uint32 row of each entry of D, grouped by position (d_base): D
+ *             inverted, the index set of the sum that defines G(x) in Theorem 2;
+ *             bit 31 is set on the first entry of each code
  *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
  *             by key column (tree_base)
  *   dtiles  : uint32 x 4 per run of 1024 entries of D (at least one per batch):
  *             batch, first entry, pairs of the batch before that entry, first
  *             row whose span starts at or after that entry
  *   cols    : uint32 per batch 4 (n_cols+1) entries (at b * 4 (n_cols+1)): for each
- *             column j = 0..n_cols, the first depth-1 code without children whose
- *             key column is >= j, the occurrences (occ_row entries) of such codes
- *             before it, and the first tlist entry of key column >= j; then the
- *             columns ordered by number of such occurrences plus tree codes, most
- *             first (n_cols entries and one unused)
+ *             column j = 0..n_cols, the first position of a leaf whose key column
+ *             is >= j, the occurrences (occ_row entries) of such leaves before
+ *             it, and the first tlist entry of key column >= j; then the columns
+ *             ordered by number of such occurrences plus tree codes, most first
+ *             (n_cols entries and one unused)
  *   tchild  : uint32 per batch n_tree+1 entries (at tree_base + b): the children of
  *             tree code h (h counting the codes with children at depth 1, then
  *             the codes of depth >= 2) are the codes tchild[h] .. tchild[h+1]-1
- * Depth-1 codes without children are sorted by key column; the codes of each
- * level d >= 2 are sorted by parent.                                             */
+ *   pval    : float per batch n_codes entries (code_base): the key value of the
+ *             code at each position
+ * Depth-1 codes without children are numbered in the order of their first entry
+ * in D; the codes of each level d >= 2 are sorted by parent.                    */
 typedef struct {
   int64_t code_base, d_base, row_base, span_base, nnz_base, deep_base, tree_base,
       lvl_base;
@@ -196,7 +201,7 @@ typedef struct {
 
 typedef struct {
   int64_t batches, level, key, link, span, dcodes, occ_off, occ_row, tlist, dtiles, cols,
-      tchild, end;
+      tchild, pval, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

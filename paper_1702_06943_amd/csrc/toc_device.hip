@@ -33,6 +33,7 @@ struct Img {
   const toc_link *link;
   const uint32_t *span;
   const uint32_t *dcodes;
+  const uint32_t *pval;     // key value bits by left-product position
 };
 
 Img image_of(const toc_dev *d) {
@@ -40,8 +41,8 @@ Img image_of(const toc_dev *d) {
   const toc_layout &L = d->layout;
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
              (const toc_key *)(b + L.key), (const toc_link *)(b + L.link),
-             (const uint32_t *)(b + L.span),
-             (const uint32_t *)(b + L.dcodes)};
+             (const uint32_t *)(b + L.span), (const uint32_t *)(b + L.dcodes),
+             (const uint32_t *)(b + L.pval)};
 }
 
 // Views of one field of a batch's node records, indexed by local code.
@@ -155,14 +156,15 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   }
 }
 
-// Left multiplication (Theorem 2, Algorithm 5) without atomics: H[c] = G(c) is
-// pulled from the inverted index (the sum over the entries of D equal to c; a
-// thread takes 4 codes at a time and loads their occurrence rows together), each
-// code then adds its children's H (children are contiguous: levels are sorted by
-// parent), deepest level first; finally a thread per key column writes it once,
-// summing val * H over the column's depth-1 leaves (a contiguous code range) and
-// tree codes (a contiguous stretch of the tree list), both read from the image's
-// column index.
+// Left multiplication (Theorem 2, Algorithm 5) without atomics, over the
+// image's left positions (a leaf's position orders it by column; every other
+// code is at its own index): H[p] = G(x) is pulled from the inverted index (the
+// sum over the entries of D equal to the code x at p; a thread takes 4 positions
+// at a time and loads their occurrence rows together), each code then adds its
+// children's H (children are contiguous: levels are sorted by parent), deepest
+// level first; finally a thread per key column writes it once, summing val * H
+// over the column's leaves (a contiguous range of positions) and tree codes (a
+// contiguous stretch of the tree list), both read from the image's column index.
 constexpr uint32_t kFirstOccK1 = 0x80000000u;
 constexpr int kK1Codes = 4;      // codes per thread and pass
 constexpr int kK1Occ = 4;        // occurrences per code loaded together
@@ -179,7 +181,7 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = uniform_batch(im.batches + b);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const toc_key *key = im.key + bt.code_base;
+  const uint32_t *pv = im.pval + bt.code_base;           // values by position
   const uint32_t *oo = occ_off_all + bt.code_base + b;
   const uint32_t *orow = occ_row_all + bt.d_base;
   const uint32_t *tl = tlist_all + bt.tree_base;
@@ -241,7 +243,7 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       const uint32_t c = c0 + u * kBlock;
-      v[u] = c < nc ? key[c].val : 0.0f;
+      v[u] = c < nc ? __uint_as_float(pv[c]) : 0.0f;
     }
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
@@ -1218,12 +1220,15 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
 //    LDS, or go to the worker's workspace slot when they do not fit;
 //  * output columns: a group of TW/4 lanes owns one column j (a lane holds 4 of
 //    the tile's columns) and sums val * row over its entries: the occurrences of
-//    the column's leaf codes (depth-1 codes without children, sorted by column,
-//    so one contiguous stretch of occ_row) and then its tree codes.  The code of
-//    a leaf occurrence is recovered from the first-occurrence bits of occ_row by
-//    a popcount carried along the column.  Entries are loaded two chunks ahead,
-//    translated to (LDS row, multiplier) one chunk ahead and staged in LDS as in
-//    the right product; groups of columns are handed out from an LDS counter.
+//    the column's leaf codes (depth-1 codes without children, whose left
+//    positions are ordered by column, so one contiguous stretch of occ_row) and
+//    then its tree codes.  The position of a leaf occurrence is recovered from
+//    the first-occurrence bits of occ_row by a popcount carried along the
+//    column, and its value read from pval.  Entries are loaded two chunks ahead
+//    and translated to (LDS row, multiplier) one chunk ahead; a group of 16
+//    lanes takes them from the lane that translated them by DPP row broadcast,
+//    a group of 8 from a per-wave stage in LDS.  Groups of columns are handed
+//    out from an LDS counter.
 // ---------------------------------------------------------------------------
 constexpr int kLtBlock = 1024;
 constexpr int kLtWaves = kLtBlock / kWave;
@@ -1303,9 +1308,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const int kt = min(TW, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const toc_key *node = im.key + bt.code_base;
-    const NodePar par{im.link + bt.code_base};
-    const NodeCol col{node};
     const uint32_t *oo = occ_off_all + bt.code_base + b;
     const uint32_t *orow = occ_row_all + bt.d_base;
     const uint32_t *tl = tlist_all + bt.tree_base;
@@ -1505,7 +1507,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
       }
     };
-    const BufRes rs_node = key_res(node, nc);
+    const BufRes rs_pval = buf_res(im.pval + bt.code_base, nc);
     const uint32_t *dummy = lvl;   // a valid address for lanes without an entry
     // L: the entry words of each lane (entries sub + h * LPG of the chunk: the
     // occ_row word of a leaf occurrence, or the code of a tree entry) and their
@@ -1565,9 +1567,9 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         base += (uint32_t)__popc(gb);
       }
       gcode = base;
-      uint2 key[PER];
+      uint32_t pv[PER];
 #pragma unroll
-      for (int h = 0; h < PER; ++h) key[h] = key_load(rs_node, code[h]);
+      for (int h = 0; h < PER; ++h) pv[h] = buf_load(rs_pval, code[h]);
       const LtChunk L = chunk_of_l();
       load_entry(lw, lkind, llcode);
       if constexpr (DPP) {
@@ -1699,11 +1701,11 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
 #pragma unroll
         for (int h = 0; h < PER; ++h) {
           cra[h] = gkind[h] == 2u ? zaddr : ((row[h] & kRtGlobal) ? row[h] : rb0 + row[h] * RB);
-          cmu[h] = gkind[h] == 2u ? 0u : key[h].y;
+          cmu[h] = gkind[h] == 2u ? 0u : pv[h];
         }
       } else {
         // S: entry sub of column grp goes to stage[sub * GPW + grp]
-        stage[sub * GPW + grp] = make_uint2(row[0], gkind[0] == 2u ? 0u : key[0].y);
+        stage[sub * GPW + grp] = make_uint2(row[0], gkind[0] == 2u ? 0u : pv[0]);
         __builtin_amdgcn_wave_barrier();
       }
       C = G;

@@ -384,7 +384,7 @@ Counts counts_of(const toc_enc *e, uint32_t flags) {
 }
 
 struct ImgScratch {
-  std::vector<uint32_t> parent, first, depth, newidx, bucket, fill;
+  std::vector<uint32_t> parent, first, depth, newidx, bucket, fill, fpos, lpos, at_lpos;
   std::vector<uint8_t> live, has_child;
   std::vector<int64_t> cnt, bucket_off;
   std::vector<uint64_t> keys;
@@ -445,7 +445,8 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     return fail(TOC_EINVAL, "corrupt encoding (tree counts disagree)");
   // Order of the stored codes (every order with parents before children is valid
   // for the scans of section 4; this one serves the kernels):
-  //   depth 1: codes with children (node order), then leaves sorted by column,
+  //   depth 1: codes with children (node order), then leaves in order of their
+  //   first entry in D (the entries of a tuple then read nearby keys),
   //   depth d >= 2: sorted by parent, so the children of a node are contiguous.
   S.cnt.assign((size_t)levels + 2, 0);
   int64_t n_int1 = 0;
@@ -469,10 +470,12 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       if (S.live[c]) S.bucket[fill[S.depth[c]]++] = (uint32_t)c;
     int64_t pos_int = 0;
     S.keys.clear();
+    S.fpos.assign((size_t)N, 0xFFFFFFFFu);
+    for (size_t j = e->D_codes.size(); j-- > 0;) S.fpos[e->D_codes[j]] = (uint32_t)j;
     for (int64_t i = S.bucket_off[1]; i < S.bucket_off[2]; ++i) {
       const uint32_t c = S.bucket[i];
       if (S.has_child[c]) S.newidx[c] = (uint32_t)pos_int++;
-      else S.keys.push_back(((uint64_t)(uint32_t)e->I_col[c - 1] << 32) | c);
+      else S.keys.push_back(((uint64_t)S.fpos[c] << 32) | c);   // a leaf is in D
     }
     std::sort(S.keys.begin(), S.keys.end());
     int64_t at = n_int1;
@@ -517,25 +520,38 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   uint32_t *dcodes = (uint32_t *)(dst + L.dcodes) + bt.d_base;
   for (int32_t r = 0; r <= e->n_rows; ++r) span[r] = (uint32_t)e->D_rowptr[r];
   for (size_t j = 0; j < e->D_codes.size(); ++j) dcodes[j] = S.newidx[e->D_codes[j]];
+  // Positions of the left multiplication: depth-1 leaves sorted by (column,
+  // code), so that the leaves of a column are contiguous; every other code is at
+  // its own index.  The inverted D, the column index and pval follow them.
+  const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;
+  S.lpos.resize((size_t)n_codes);
+  S.at_lpos.resize((size_t)n_codes);
+  for (int64_t c = 0; c < n_codes; ++c) S.lpos[c] = (uint32_t)c;
+  S.keys.clear();
+  for (int64_t c = n_int1; c < n1; ++c) S.keys.push_back(((uint64_t)node[c].col << 32) | (uint64_t)c);
+  std::sort(S.keys.begin(), S.keys.end());
+  for (size_t i = 0; i < S.keys.size(); ++i) S.lpos[(uint32_t)S.keys[i]] = (uint32_t)(n_int1 + (int64_t)i);
+  for (int64_t c = 0; c < n_codes; ++c) S.at_lpos[S.lpos[c]] = (uint32_t)c;
+  uint32_t *pval = (uint32_t *)(dst + L.pval) + bt.code_base;
+  for (int64_t p = 0; p < n_codes; ++p) std::memcpy(&pval[p], &node[S.at_lpos[p]].val, 4);
   // occurrences of each code (D inverted): rows of the entries of D equal to the
-  // code, ascending, grouped by code.  This is the index set of the sum that
+  // code, ascending, grouped by position.  This is the index set of the sum that
   // defines G(x) in Theorem 2.
   uint32_t *occ_off = (uint32_t *)(dst + L.occ_off) + bt.code_base + b;
   uint32_t *occ_row = (uint32_t *)(dst + L.occ_row) + bt.d_base;
   std::fill(occ_off, occ_off + n_codes + 1, 0u);
-  for (size_t j = 0; j < e->D_codes.size(); ++j) occ_off[dcodes[j] + 1]++;
+  for (size_t j = 0; j < e->D_codes.size(); ++j) occ_off[S.lpos[dcodes[j]] + 1]++;
   for (int64_t c = 0; c < n_codes; ++c) occ_off[c + 1] += occ_off[c];
   S.fill.assign(occ_off, occ_off + n_codes);
   for (int32_t r = 0; r < e->n_rows; ++r)
     for (int64_t j = e->D_rowptr[r]; j < e->D_rowptr[r + 1]; ++j)
-      occ_row[S.fill[dcodes[j]]++] = (uint32_t)r;
+      occ_row[S.fill[S.lpos[dcodes[j]]]++] = (uint32_t)r;
   // bit 31 marks the first occurrence of each code, so a scan over occ_row alone
   // can tell which code an entry belongs to
   for (int64_t c = 0; c < n_codes; ++c)
     if (occ_off[c] < occ_off[c + 1]) occ_row[occ_off[c]] |= 0x80000000u;
   // codes with an H row in the left multiplication (children or depth >= 2),
   // listed by column
-  const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;
   uint32_t *tlist = (uint32_t *)(dst + L.tlist) + bt.tree_base;
   S.keys.clear();
   for (int64_t c = 0; c < n_codes; ++c)
@@ -544,17 +560,17 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   for (size_t t = 0; t < S.keys.size(); ++t) tlist[t] = (uint32_t)S.keys[t];
   const int64_t n_tree = (int64_t)S.keys.size();
   // column index of the left multiplication (out row j sums over the codes of key
-  // column j): per column the first leaf code (depth 1, no children) of a column
-  // >= j, the leaf occurrences before it, the first tree-list entry of a column
-  // >= j, and the columns ordered by number of entries (leaf occurrences + tree
-  // codes), most first
+  // column j): per column the first position of a leaf (depth 1, no children) of
+  // a column >= j, the leaf occurrences before it, the first tree-list entry of a
+  // column >= j, and the columns ordered by number of entries (leaf occurrences +
+  // tree codes), most first
   {
     const int64_t m = e->n_cols;
     uint32_t *cx = (uint32_t *)(dst + L.cols) + (int64_t)b * 4 * (m + 1);
     uint32_t *c_code = cx, *c_occ = cx + (m + 1), *c_tree = cx + 2 * (m + 1), *c_ord = cx + 3 * (m + 1);
     int64_t i = n_int1, t = 0;
     for (int64_t j = 0; j <= m; ++j) {
-      while (i < n1 && (int64_t)node[i].col < j) ++i;
+      while (i < n1 && (int64_t)node[S.at_lpos[i]].col < j) ++i;
       while (t < n_tree && (int64_t)node[tlist[t]].col < j) ++t;
       c_code[j] = (uint32_t)i;
       c_occ[j] = occ_off[i] - occ_off[n_int1];
@@ -678,6 +694,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.dtiles = off;  off = align256(off + 16 * dtiles);
   L.cols = off;    off = align256(off + 16 * n_batches * ((int64_t)std::max(n_cols, 0) + 1));
   L.tchild = off;  off = align256(off + 4 * (tree + n_batches));
+  L.pval = off;    off = align256(off + 4 * codes);
   dev->n_dtiles = dtiles;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;

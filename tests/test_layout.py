@@ -38,6 +38,7 @@ def read_image(dev, buf):
         cols=arr("cols", np.uint32, nb * 4 * (info["n_cols"] + 1)),
         tchild=arr("tchild", np.uint32,
                    int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"] + 1).sum()) if nb else 0),
+        pval=arr("pval", np.float32, n_codes),
     )
     for f in ("col", "val"):
         img[f] = img["key"][f]
@@ -64,6 +65,7 @@ def batch_view(img, b):
         cols=img["cols"][b * 4 * (m + 1):(b + 1) * 4 * (m + 1)].reshape(4, m + 1),
         tchild=img["tchild"][int(t["tree_base"]) + b:int(t["tree_base"]) + b + int(t["n_int1"]) + nc
                              - int(t["n_lvl1"]) + 1],
+        pval=img["pval"][cb:cb + nc],
     )
 
 
@@ -94,28 +96,40 @@ def check_invariants(v):
         keys.add(k)
     assert np.all(v["dc"] < nc)
     assert v["span"][0] == 0 and v["span"][-1] == len(v["dc"])
-    # depth-1 leaves sorted by column; deeper levels sorted by parent
-    assert np.all(np.diff(v["col"][ni:n1].astype(np.int64)) >= 0)
+    # depth-1 leaves numbered by their first entry in D; deeper levels sorted by
+    # parent
+    first_entry = {}
+    for j, c in enumerate(v["dc"].tolist()):
+        first_entry.setdefault(c, j)
+    fe = [first_entry[c] for c in range(ni, n1)]
+    assert fe == sorted(fe)
     for d in range(2, nl + 1):
         assert np.all(np.diff(v["parent"][lv[d - 1]:lv[d]].astype(np.int64)) >= 0)
-    # inverted D: the rows listed for each code are exactly the rows using it
+    # left positions: leaves ordered by (column, code) after the codes with
+    # children; every other code at its own index
+    at = list(range(ni)) + sorted(range(ni, n1), key=lambda c: (int(v["col"][c]), c)) \
+        + list(range(n1, nc))
+    assert np.array_equal(v["pval"].view(np.uint32), v["val"].view(np.uint32)[at])
+    # inverted D: the rows listed at each position are exactly the rows using its
+    # code
     oo, orow = v["occ_off"], v["occ_row"]
     assert oo[0] == 0 and oo[-1] == len(v["dc"]) and np.all(np.diff(oo.astype(np.int64)) >= 0)
     row_of = np.repeat(np.arange(len(v["span"]) - 1), np.diff(v["span"].astype(np.int64)))
     first = (orow >> 31).astype(bool)
     assert np.array_equal(np.flatnonzero(first), oo[:-1][np.diff(oo.astype(np.int64)) > 0])
     orow = orow & 0x7FFFFFFF
-    for c in range(nc):
-        got = orow[oo[c]:oo[c + 1]]
+    for p in range(nc):
+        got = orow[oo[p]:oo[p + 1]]
         assert np.all(np.diff(got.astype(np.int64)) >= 0)
-        assert np.array_equal(got, row_of[v["dc"] == c])
+        assert np.array_equal(got, row_of[v["dc"] == at[p]])
     # tree list: codes with children or depth >= 2, sorted by column
     tree = [c for c in range(nc) if c < ni or c >= n1]
     tl = v["tlist"]
     assert sorted(tl.tolist()) == tree
     assert np.all(np.diff(v["col"][tl].astype(np.int64)) >= 0)
-    # column index: first leaf code, leaf occurrences before it and first tree-list
-    # entry of each column j; columns by entry count, most first (ties by column)
+    # column index: first leaf position, leaf occurrences before it and first
+    # tree-list entry of each column j; columns by entry count, most first (ties
+    # by column)
     cx = v["cols"]
     m = cx.shape[1] - 1
     leaf_cols = v["col"][ni:n1].astype(np.int64)
@@ -129,9 +143,11 @@ def check_invariants(v):
     want = sorted(range(m), key=lambda j: (-cnt[j], j))
     assert cx[3, :m].tolist() == want
     # leaf occurrences of column j: those of its leaf codes; tree codes of column j
+    pos = {c: p for p, c in enumerate(at)}
     for j in range(m):
-        codes = [c for c in range(ni, n1) if v["col"][c] == j]
-        assert sum(int(oo[c + 1] - oo[c]) for c in codes) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
+        ps = [pos[c] for c in range(ni, n1) if v["col"][c] == j]
+        assert ps == list(range(int(cx[0, j]), int(cx[0, j + 1])))
+        assert sum(int(oo[p + 1] - oo[p]) for p in ps) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
     # children ranges: tree code h's children are tchild[h] .. tchild[h+1]-1
     hrow = lambda c: c if c < ni else c - n1 + ni
     tch = v["tchild"]
