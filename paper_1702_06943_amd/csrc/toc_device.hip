@@ -1263,9 +1263,11 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
     const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
     const uint32_t *__restrict__ tchild_all, int64_t nb, int n_tiles, int spw, int max_rows,
-    int max_tree, int m, const float *__restrict__ G, int64_t ldg, int k,
+    int max_tree, int tree_cap, int m, const float *__restrict__ G, int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
     int64_t slot_floats) {
+  // TREE_LDS: every tree row is in LDS; else the first tree_cap are and the others
+  // are in the worker's workspace slot
   constexpr int LPG = TW / 4;                 // lanes per group (4 columns each)
   constexpr int GPW = kWave / LPG;            // groups (output columns) per wave
   constexpr int CH = LPG;                     // entries per column per chunk: one per lane
@@ -1360,8 +1362,21 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     // Tree codes, deepest level first: H = own occurrences' G rows + children's
     // H rows.  A group takes kLtU codes at a time and issues their loads
     // together; a code's occurrence rows are broadcast along its group.
-    auto tree_row = [&](uint32_t h) -> float * {
-      return TREE_LDS ? Rw + (size_t)(trow0 + h) * TW : Hg + (int64_t)h * TW;
+    // a tree row: in LDS (the first tree_cap) or in the workspace; both loads are
+    // issued and the values selected (a select of the two pointers would make a
+    // flat pointer)
+    const uint32_t cap = TREE_LDS ? 0xFFFFFFFFu : (uint32_t)tree_cap;
+    auto load_trow = [&](uint32_t h) -> float4 {
+      const bool inl = h < cap;
+      const float4 xl = lds_load4(qb + (inl ? trow0 + h : zrow) * RB);
+      if (TREE_LDS) return xl;
+      float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (!inl) xg = *(const float4 *)&Hg[(int64_t)h * TW + q];
+      return inl ? xl : xg;
+    };
+    auto store_trow = [&](uint32_t h, float4 v) {
+      if (h < cap) *(float4 *)&Rw[(size_t)(trow0 + h) * TW + q] = v;
+      else *(float4 *)&Hg[(int64_t)h * TW + q] = v;
     };
     // value v of lane i of the caller's group
     auto gbcast = [&](uint32_t v, auto ic) -> uint32_t {
@@ -1402,9 +1417,10 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         for (uint32_t cb = 0; cb < cmax; ++cb) {
           float4 g[kLtU];
 #pragma unroll
-          for (int u = 0; u < kLtU; ++u)
-            g[u] = k0[u] + cb < k1[u] ? *(const float4 *)&tree_row(hrow(k0[u] + cb))[q]
-                                      : make_float4(0.f, 0.f, 0.f, 0.f);
+          for (int u = 0; u < kLtU; ++u) {
+            g[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k0[u] + cb < k1[u]) g[u] = load_trow(hrow(k0[u] + cb));
+          }
 #pragma unroll
           for (int u = 0; u < kLtU; ++u) {
             acc[u].x += g[u].x;
@@ -1443,7 +1459,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
               acc[u].w += g.w;
             }
           }
-          if (c0 + u * NG < e) *(float4 *)&tree_row(h[u])[q] = acc[u];
+          if (c0 + u * NG < e) store_trow(h[u], acc[u]);
         }
       }
       __syncthreads();
@@ -1561,7 +1577,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
         // branch-free: leaf, tree or no entry
         const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
-        const uint32_t trow = TREE_LDS ? trow0 + hrow(gw[h]) : (kRtGlobal | hrow(gw[h]));
+        const uint32_t hr = hrow(gw[h]);
+        const uint32_t trow = hr < cap ? trow0 + hr : (kRtGlobal | hr);
         code[h] = gkind[h] == 0u ? lcode : (gkind[h] == 1u ? gw[h] : 0xFFFFFFFFu);
         row[h] = gkind[h] == 0u ? (gw[h] & ~kFirstOcc) : (gkind[h] == 1u ? trow : zrow);
         base += (uint32_t)__popc(gb);
@@ -1574,7 +1591,13 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       load_entry(lw, lkind, llcode);
       if constexpr (DPP) {
         constexpr int NB = CHK / 4;             // blocks of 4 entries
-        if (C.cg < n_cg && !C.tree && C.steps == (uint32_t)CHK) {
+        // does an entry of chunk C read a tree row in the workspace?
+        bool ws_chunk = false;
+        if (!TREE_LDS && C.tree) {
+#pragma unroll
+          for (int h = 0; h < PER; ++h) ws_chunk |= __ballot((cra[h] & kRtGlobal) != 0) != 0;
+        }
+        if (C.cg < n_cg && !ws_chunk && C.steps == (uint32_t)CHK) {
           // a full chunk of leaf entries: LDS rows only, each block's reads
           // issued before the previous block's FMAs
           float4 xa[4], xb[4];
@@ -1589,7 +1612,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
             if constexpr (bk % 2 == 0) fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xa);
             else fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xb);
           });
-        } else if (C.cg < n_cg && (TREE_LDS || !C.tree)) {
+        } else if (C.cg < n_cg && !ws_chunk) {
           // a partial chunk, rows in LDS: blocks of 4 entries
           static_for<NB>([&](auto bc) {
             constexpr int bk = decltype(bc)::value;
@@ -1602,7 +1625,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         } else if (C.cg < n_cg) {
           // blocks of 4 entries; tree rows may be in the workspace: both loads
           // are issued and the values selected
-          const bool any_ws = !TREE_LDS && C.tree;
           static_for<NB>([&](auto bc) {
             constexpr int bk = decltype(bc)::value;
             constexpr int t0 = 4 * (bk % 4), hh = bk / 4;
@@ -1613,15 +1635,11 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
                 constexpr int i = decltype(ic)::value;
                 const uint32_t r = row_bcast<t0 + i>(cra[hh]);
                 mt[i] = __uint_as_float(row_bcast<t0 + i>(cmu[hh]));
-                if (any_ws) {
-                  const bool g = (r & kRtGlobal) != 0;
-                  const float4 xl = lds_load4((g ? zaddr : r) + qoff);
-                  float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
-                  if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
-                  xv[i] = g ? xg : xl;
-                } else {
-                  xv[i] = lds_load4(r + qoff);
-                }
+                const bool g = (r & kRtGlobal) != 0;
+                const float4 xl = lds_load4((g ? zaddr : r) + qoff);
+                float4 xg = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
+                xv[i] = g ? xg : xl;
               });
               static_for<4>([&](auto ic) {
                 constexpr int i = decltype(ic)::value;
@@ -1887,6 +1905,7 @@ struct OpPlan {
   int64_t row_floats = 0;     // workspace floats per H row (0: no workspace)
   int64_t rows_max = 0, rows_total = 0;
   int64_t ws_floats = 0;      // tiled: whole workspace (one slot per worker)
+  int64_t lds_rows = 0;       // tiled left: tree rows in LDS
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -1929,8 +1948,10 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
       p.path = kPathTiled;
       p.tw = tw;
       p.n_tiles = (k + tw - 1) / tw;
-      p.deep_lds = head + rows + (size_t)d->max_tree * tw * 4 <= lds_max;
-      p.lds = head + rows + (p.deep_lds ? (size_t)d->max_tree * tw * 4 : 0);
+      // the tree rows that fit in LDS go there, the others to the workspace
+      p.lds_rows = std::min<int64_t>(d->max_tree, (int64_t)((lds_max - head - rows) / ((size_t)tw * 4)));
+      p.deep_lds = p.lds_rows == d->max_tree;
+      p.lds = head + rows + (size_t)p.lds_rows * tw * 4;
       const int64_t items = (d->info.n_batches + kXcd - 1) / kXcd * p.n_tiles;
       p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
       p.grid = (unsigned)(kXcd * p.spx);
@@ -2213,8 +2234,8 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
     hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
                        im, occ_off, occ_row, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,     \
-                       d->max_rows,                                                             \
-                       (int)d->max_tree, m, G, ldg, k, out, ldo, accumulate, (float *)ws, slot);  \
+                       d->max_rows, (int)d->max_tree, (int)plan.lds_rows, m, G, ldg, k, out, ldo,  \
+                       accumulate, (float *)ws, slot);                                          \
   } while (0)
     if (plan.tw == 64) {
       if (plan.deep_lds) TOC_LT_LAUNCH(64, true);
