@@ -20,6 +20,11 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
   dense_left     pinned: as dense_right, plus duality <G, A W> = <A^T G, W>
   toc_right      pinned: Theorem 1 (equals dense_right) + integer exactness
   toc_left       pinned: Theorem 2 (equals dense_left) + integer exactness
+  map_values     pinned: Algorithm 3's claim (decoding the modified I equals the
+                 element-wise op on the decoded batch), exact cases (c = 1, -1, 2),
+                 squares of integers
+  dense_plus     pinned: round trip to the CSR for c = 0, zeros become c,
+                 integer sums in closed form
   layout_stats   pinned: hand count on the worked example (live set, depths)
   physical_bytes parity unpinned (the paper prints sizes only in missing figures;
                  the formula of §3.3 is checked on the worked example by hand)
@@ -36,6 +41,10 @@ from .toc_oracle import (  # noqa: F401
     dense_left,
     toc_right,
     toc_left,
+    map_values,
+    dense_plus,
+    MAP_SCALE,
+    MAP_SQUARE,
     layout_stats,
     physical_bytes,
     f32_bits,

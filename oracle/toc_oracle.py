@@ -215,6 +215,47 @@ def _coo(rows):
 
 
 # ---------------------------------------------------------------------------
+# Sparse-safe element-wise operations (§4.2, Algorithm 3): every distinct
+# (column, value) pair of A is an entry of I, so A.*c (and A.^2, "similar" by the
+# same section) is computed by scanning I and changing each value.  Values are
+# binary32, so the new value is the binary32 rounding of the product; a product
+# that rounds to zero stays an entry (the structure of A is not revisited).
+# ---------------------------------------------------------------------------
+MAP_SCALE = 0
+MAP_SQUARE = 1
+
+
+def map_values(I, op, c=1.0):
+    """Algorithm 3: I -> I' with every value v replaced by v*c (MAP_SCALE) or v*v
+    (MAP_SQUARE), rounded to binary32."""
+    out = []
+    for col, b in I:
+        v = np.float32(bits_f32(b))
+        if op == MAP_SCALE:
+            w = np.float32(v * np.float32(c))
+        elif op == MAP_SQUARE:
+            w = np.float32(v * v)
+        else:
+            raise ValueError("unknown op")
+        out.append((col, int(np.asarray(w, dtype=np.float32).view(np.uint32))))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Sparse-unsafe element-wise plus (§4.5, Algorithm 9): decode A fully (the
+# backtracking of Algorithm 6), densify it, and add c to every element, the
+# zeros included.  In binary32: R[i, j] = a_ij + c rounded to binary32.
+# ---------------------------------------------------------------------------
+def dense_plus(rows, n_cols, c=0.0):
+    """Decoded rows -> dense (n_rows, n_cols) float32 array A .+ c."""
+    A = np.zeros((len(rows), n_cols), dtype=np.float32)
+    for i, r in enumerate(rows):
+        for col, b in r:
+            A[i, col] = np.float32(bits_f32(b))
+    return (A + np.float32(c)).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
 # Reference products.  Theorems 1 and 2 (and their matrix forms in the appendix)
 # state that the TOC algorithms compute exactly A.W and M.A; so the reference is the
 # plain definition over the nonzeros of the decoded batch, in fp64:

@@ -271,3 +271,84 @@ def test_scale_is_zero_only_for_structural_zeros():
     W = np.ones((3, 2), np.float32)
     R, S = O.dense_right(rows, 3, W)
     assert np.all(S[1] == 0) and np.all(R[1] == 0) and np.all(S[0] == 2)
+
+
+# --- sparse-safe element-wise ops (Algorithm 3) and A .+ c (Algorithm 9) ----------
+def _csr_arrays(rows):
+    """rows of (col, bits) -> (row index, col, float32 value) arrays."""
+    ri = np.asarray([i for i, r in enumerate(rows) for _ in r], dtype=np.int64)
+    ci = np.asarray([c for r in rows for c, _ in r], dtype=np.int64)
+    vi = np.asarray([b for r in rows for _, b in r], dtype=np.uint32).view(np.float32)
+    return ri, ci, vi
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("op,c", [(0, 1.0), (0, -1.0), (0, 2.0), (0, 0.37), (0, 0.0), (1, 0.0)])
+def test_map_values_commutes_with_decode(seed, case, op, c):
+    # Algorithm 3 changes only I; the section's claim is that this applies the
+    # element-wise op to every nonzero of A.  Checked against the op applied by
+    # numpy to the decoded values (vectorised binary32 arithmetic).
+    spec = CASES[case]
+    rp, col, val = tiny_batch(2000 + seed * 31 + case, **spec)
+    rows = O.canonicalize(spec["n_rows"], spec["n_cols"], rp, col, val)
+    I, D, _ = O.encode(rows)
+    got = _csr_arrays(O.decode(O.map_values(I, op, c), D))
+    ri, ci, vi = _csr_arrays(rows)
+    want = vi * np.float32(c) if op == O.MAP_SCALE else vi * vi
+    assert np.array_equal(got[0], ri) and np.array_equal(got[1], ci)
+    assert np.array_equal(got[2].view(np.uint32), want.astype(np.float32).view(np.uint32))
+
+
+def test_map_values_exact_cases():
+    rows = [[(0, O.f32_bits(1.5)), (3, O.f32_bits(-2.25))], [(1, O.f32_bits(3.0))]]
+    I, D, _ = O.encode(rows)
+    bits = np.asarray([b for _, b in I], dtype=np.uint32)
+    # c = 1: identical bits; c = -1: only the sign bit flips; c = 2: exponent + 1
+    assert [b for _, b in O.map_values(I, O.MAP_SCALE, 1.0)] == bits.tolist()
+    assert [b for _, b in O.map_values(I, O.MAP_SCALE, -1.0)] == (bits ^ 0x80000000).tolist()
+    assert [b for _, b in O.map_values(I, O.MAP_SCALE, 2.0)] == (bits + (1 << 23)).tolist()
+    # squares of small integers are exact
+    rows = [[(0, O.f32_bits(3.0)), (1, O.f32_bits(-7.0))], [(0, O.f32_bits(12.0))]]
+    I, D, _ = O.encode(rows)
+    sq = [O.bits_f32(b) for _, b in O.map_values(I, O.MAP_SQUARE)]
+    assert sq == [O.bits_f32(b) ** 2 for _, b in I]
+    assert [c for c, _ in O.map_values(I, O.MAP_SQUARE)] == [c for c, _ in I]
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_dense_plus(seed, case):
+    spec = CASES[case]
+    rp, col, val = tiny_batch(3000 + seed * 31 + case, zeros=True, **spec)
+    n, m = spec["n_rows"], spec["n_cols"]
+    rows = O.canonicalize(n, m, rp, col, val)
+    ri, ci, vi = _csr_arrays(rows)
+    # c = 0: the dense matrix has exactly the CSR's nonzeros
+    A = O.dense_plus(rows, m, 0.0)
+    assert A.dtype == np.float32 and A.shape == (n, m)
+    nz = np.nonzero(A)
+    assert np.array_equal(nz[0], ri) and np.array_equal(nz[1], ci)
+    assert np.array_equal(A[nz].view(np.uint32), vi.view(np.uint32))
+    # c != 0: zeros become c, every stored entry a + c
+    c = np.float32(-1.25)
+    B = O.dense_plus(rows, m, c)
+    mask = np.ones((n, m), bool)
+    mask[ri, ci] = False
+    assert np.all(B[mask] == c)
+    assert np.array_equal(B[ri, ci], (vi + c).astype(np.float32))
+
+
+def test_dense_plus_integer_sum():
+    # integer-valued A and c: every element is exact, so the total is closed-form
+    rng = np.random.default_rng(5)
+    n, m = 9, 13
+    dense = rng.integers(-4, 5, size=(n, m)).astype(np.float32)
+    dense[rng.random((n, m)) < 0.4] = 0
+    rp = np.concatenate([[0], np.cumsum((dense != 0).sum(1))]).astype(np.int64)
+    col = np.concatenate([np.flatnonzero(r) for r in dense]).astype(np.int32)
+    val = dense[dense != 0].astype(np.float32)
+    rows = O.canonicalize(n, m, rp, col, val)
+    I, D, _ = O.encode(rows)
+    B = O.dense_plus(O.decode(I, D), m, 3.0)
+    assert float(B.astype(np.float64).sum()) == float(dense.sum()) + 3.0 * n * m
