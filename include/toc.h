@@ -250,6 +250,29 @@ toc_status toc_left_mul(const toc_dev *dev, const float *G, int32_t k, int64_t l
 toc_status toc_decode_csr(const toc_dev *dev, int64_t *rowptr, int32_t *col,
                           float *val, void *stream);
 
+/* Sparse-safe element-wise operation on every batch, in place (section 4.2,
+ * Algorithm 3: every distinct key pair of A is a node key of the image, so
+ * changing the key values changes every nonzero of A alike).  Each key value v
+ * becomes v * c (TOC_MAP_SCALE) or v * v (TOC_MAP_SQUARE; c is ignored), rounded
+ * to binary32; the products and decodes that follow see the new matrix.  A value
+ * that becomes 0 stays a stored entry.  The image bytes in the caller's buffer are
+ * modified; the toc_dev descriptor is not.  Asynchronous on `stream`.
+ * Errors: TOC_EINVAL (unknown op, non-finite c, NULL or host-image toc_dev),
+ * TOC_EDEVICE. */
+#define TOC_MAP_SCALE 0
+#define TOC_MAP_SQUARE 1
+toc_status toc_map_values(const toc_dev *dev, int32_t op, float c, void *stream);
+
+/* Sparse-unsafe element-wise plus (section 4.5, Algorithm 9): every batch decoded
+ * to dense and c added to every element, the zeros included:
+ * A[i lda + j] = a_ij + c (binary32) for i < sum of rows (rows in batch order) and
+ * j < n_cols; columns n_cols .. lda-1 are left untouched.  A: caller-owned device
+ * memory of (sum of rows) x lda floats, lda >= n_cols.  With c = 0 this is the
+ * densify step of the algorithm alone.  Asynchronous on `stream`.
+ * Errors: TOC_EINVAL (NULL, lda < n_cols, non-finite c, host-image toc_dev),
+ * TOC_EDEVICE. */
+toc_status toc_decode_dense(const toc_dev *dev, float c, float *A, int64_t lda, void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *toc_last_error(void);
 

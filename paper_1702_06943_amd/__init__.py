@@ -1,5 +1,6 @@
 """MI355X-native tuple-oriented compression (TOC): encode on the host, run A.W,
-G^T.A and decode on the compressed mini-batches with hand-written gfx950 kernels.
+G^T.A, decode, sparse-safe element-wise ops and dense A .+ c on the compressed
+mini-batches with hand-written gfx950 kernels.
 
 The functions are those of include/toc.h, called through ctypes; see binding.py.
 """
@@ -7,8 +8,10 @@ The functions are those of include/toc.h, called through ctypes; see binding.py.
 from .binding import (  # noqa: F401
     TocError, Enc, Dev, lib, LIB_PATH, BATCH_DTYPE, KEY_DTYPE, LINK_DTYPE,
     TOC_UPLOAD_KEEP_DEAD, TOC_UPLOAD_HOST, TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE,
+    TOC_MAP_SCALE, TOC_MAP_SQUARE,
     TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED,
     toc_encode, toc_encode_batches, toc_enc_info_get, toc_enc_export,
     toc_upload_size, toc_upload, toc_dev_info_get, toc_dev_layout_get,
     toc_workspace_size, toc_right_mul, toc_left_mul, toc_decode_csr,
+    toc_map_values, toc_decode_dense,
 )

@@ -21,6 +21,7 @@ TOC_OK, TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED = range
 TOC_UPLOAD_KEEP_DEAD = 1
 TOC_UPLOAD_HOST = 2
 TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE = 0, 1, 2
+TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -95,6 +96,8 @@ def lib():
         "toc_right_mul": [P, P, I32, I64, P, I64, P, SZ, P],
         "toc_left_mul": [P, P, I32, I64, P, I64, I32, P, SZ, P],
         "toc_decode_csr": [P, P, P, P, P],
+        "toc_map_values": [P, I32, C.c_float, P],
+        "toc_decode_dense": [P, C.c_float, P, I64, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -284,3 +287,17 @@ def toc_decode_csr(dev, rowptr, col, val, stream=None):
         raise TocError(TOC_EINVAL, "rowptr/col/val sizes do not match the image")
     _check(lib().toc_decode_csr(dev.handle, rowptr.data_ptr(), _ptr(col), _ptr(val),
                                 _stream(stream)))
+
+
+def toc_map_values(dev, op, c=1.0, stream=None):
+    """In place: every key value v of the image becomes v*c (TOC_MAP_SCALE) or v*v."""
+    _check(lib().toc_map_values(dev.handle, int(op), float(c), _stream(stream)))
+
+
+def toc_decode_dense(dev, A, c=0.0, stream=None):
+    """A: n_rows x lda float32 (lda >= n_cols) receives the dense batches plus c."""
+    info = toc_dev_info_get(dev)
+    ap, lda, ncols = _mat(A, "A")
+    if A.shape[0] != info["n_rows"] or ncols < info["n_cols"]:
+        raise TocError(TOC_EINVAL, "A must be n_rows x (>= n_cols)")
+    _check(lib().toc_decode_dense(dev.handle, float(c), ap, lda, _stream(stream)))

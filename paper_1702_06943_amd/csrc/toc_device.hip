@@ -7,6 +7,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <new>
 #include <type_traits>
@@ -1849,6 +1850,66 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
 }
 
 // ===========================================================================
+// Sparse-safe element-wise operations (Algorithm 3): every key value of the
+// image, and its copy at the code's left position, changes alike.  Elementwise
+// over all stored codes; both arrays have one entry per stored code.
+// ===========================================================================
+constexpr int kMapBlock = 256;
+
+__global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restrict__ key,
+                                                               uint32_t *__restrict__ pval,
+                                                               int64_t n, int op, float c) {
+  const int64_t stride = (int64_t)gridDim.x * kMapBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kMapBlock + threadIdx.x; i < n; i += stride) {
+    const float v = key[i].val, w = __uint_as_float(pval[i]);
+    key[i].val = op == TOC_MAP_SCALE ? v * c : v * v;
+    pval[i] = __float_as_uint(op == TOC_MAP_SCALE ? w * c : w * w);
+  }
+}
+
+// ===========================================================================
+// Dense decode plus a scalar (Algorithm 9): one workgroup per batch fills the
+// batch's rows with c, then every entry of D writes its sequence's pairs,
+// a_ij + c, walking its chain to the root; a wave per tuple, a lane per entry.
+// The fill is made visible before the pairs are written (fence, barrier).
+// ===========================================================================
+constexpr int kDnBlock = 1024;
+constexpr int kDnWaves = kDnBlock / kWave;
+
+__global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t b0, int m,
+                                                                float c, float *__restrict__ A,
+                                                                int64_t lda) {
+  const int64_t b = b0 + blockIdx.x;
+  const toc_batch bt = uniform_batch(im.batches + b);
+  const int lane = threadIdx.x % kWave, wave = wave_id();
+  float *Ab = A + bt.row_base * lda;
+  for (int r = wave; r < bt.n_rows; r += kDnWaves) {
+    float *row = Ab + (int64_t)r * lda;
+    for (int j = lane; j < m; j += kWave) row[j] = c;
+  }
+  __threadfence();
+  __syncthreads();
+  const toc_key *key = im.key + bt.code_base;
+  const toc_link *link = im.link + bt.code_base;
+  const uint32_t *span = im.span + bt.span_base;
+  const uint32_t *dc = im.dcodes + bt.d_base;
+  const uint32_t n1 = (uint32_t)bt.n_lvl1;
+  for (int r = wave; r < bt.n_rows; r += kDnWaves) {
+    float *row = Ab + (int64_t)r * lda;
+    const uint32_t e = span[r + 1];
+    for (uint32_t j = span[r] + lane; j < e; j += kWave) {
+      uint32_t x = dc[j];
+      for (;;) {
+        const toc_key k = key[x];
+        row[k.col] = k.val + c;
+        if (x < n1) break;   // depth 1: the chain's first pair
+        x = link[x].parent;
+      }
+    }
+  }
+}
+
+// ===========================================================================
 // Host helpers
 // ===========================================================================
 toc_status check_device(const toc_dev *d) {
@@ -2286,6 +2347,40 @@ toc_status toc_decode_csr(const toc_dev *d, int64_t *rowptr, int32_t *col, float
     hipLaunchKernelGGL(decode_kernel, dim3(g), dim3(kDecBlock), 0, s, im, dtiles, t0, n, rowptr,
                        col, (uint32_t *)val);
     if ((st = launch_status("decode_kernel"))) return st;
+  }
+  return TOC_OK;
+}
+
+toc_status toc_map_values(const toc_dev *d, int32_t op, float c, void *stream) {
+  toc_status st = check_device(d);
+  if (st != TOC_OK) return st;
+  if (op != TOC_MAP_SCALE && op != TOC_MAP_SQUARE) return fail(TOC_EINVAL, "unknown op %d", op);
+  if (op == TOC_MAP_SCALE && !std::isfinite(c)) return fail(TOC_EINVAL, "c is not finite");
+  const int64_t n = d->info.n_stored;
+  if (n == 0) return TOC_OK;
+  uint8_t *bb = (uint8_t *)d->buf;
+  const int64_t blocks = std::min<int64_t>((n + kMapBlock - 1) / kMapBlock, 64 * 256);
+  hipLaunchKernelGGL(map_values_kernel, dim3((unsigned)blocks), dim3(kMapBlock), 0,
+                     (hipStream_t)stream, (toc_key *)(bb + d->layout.key),
+                     (uint32_t *)(bb + d->layout.pval), n, (int)op, c);
+  return launch_status("map_values_kernel");
+}
+
+toc_status toc_decode_dense(const toc_dev *d, float c, float *A, int64_t lda, void *stream) {
+  toc_status st = check_device(d);
+  if (st != TOC_OK) return st;
+  const int m = d->info.n_cols;
+  if (!std::isfinite(c)) return fail(TOC_EINVAL, "c is not finite");
+  if (lda < m) return fail(TOC_EINVAL, "lda %lld < n_cols %d", (long long)lda, m);
+  if (!A && d->info.n_rows > 0 && m > 0) return fail(TOC_EINVAL, "A is NULL");
+  const int64_t nb = d->info.n_batches;
+  if (nb == 0 || d->info.n_rows == 0 || m == 0) return TOC_OK;
+  const Img im = image_of(d);
+  hipStream_t s = (hipStream_t)stream;
+  for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
+    const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
+    hipLaunchKernelGGL(decode_dense_kernel, dim3(g), dim3(kDnBlock), 0, s, im, b0, m, c, A, lda);
+    if ((st = launch_status("decode_dense_kernel"))) return st;
   }
   return TOC_OK;
 }

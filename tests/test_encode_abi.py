@@ -152,3 +152,5 @@ def test_null_pointers_rejected():
     assert lib.toc_right_mul(None, None, 1, 1, None, 1, None, 0, None) == T.TOC_EINVAL
     assert lib.toc_left_mul(None, None, 1, 1, None, 1, 0, None, 0, None) == T.TOC_EINVAL
     assert lib.toc_decode_csr(None, None, None, None, None) == T.TOC_EINVAL
+    assert lib.toc_map_values(None, 0, 1.0, None) == T.TOC_EINVAL
+    assert lib.toc_decode_dense(None, 0.0, None, 1, None) == T.TOC_EINVAL

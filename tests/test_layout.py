@@ -281,3 +281,5 @@ def test_host_image_rejected_by_device_ops():
     assert lib.toc_right_mul(dev.handle, 8, 1, 1, 8, 1, None, 0, None) == T.TOC_EINVAL
     assert "host" in lib.toc_last_error().decode()
     assert lib.toc_decode_csr(dev.handle, 8, 8, 8, None) == T.TOC_EINVAL
+    assert lib.toc_map_values(dev.handle, 0, 2.0, None) == T.TOC_EINVAL
+    assert lib.toc_decode_dense(dev.handle, 0.0, 8, 3, None) == T.TOC_EINVAL
