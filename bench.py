@@ -152,6 +152,50 @@ def run_ops(w, which=("right", "left", "decode")):
         T.toc_decode_csr(w.dev, w.rowptr, w.ccol, w.cval)
 
 
+def time_elementwise(w, stream, reps=3):
+    """The element-wise operations on the same resident image, outside the step:
+    toc_map_values with c = 1 (the matrix is unchanged) and toc_decode_dense with
+    c = 0 into a dense n_rows x n_cols block when it fits in free memory.  HBM
+    fractions use algorithmic bytes: 4-byte read and write of every key value and
+    its position copy; the canonical bytes read plus the dense block written."""
+    import torch
+    import paper_1702_06943_amd as T
+    info = w.info
+    res = {}
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    T.toc_map_values(w.dev, T.TOC_MAP_SCALE, 1.0)
+    ev[0].record(stream)
+    for i in range(reps):
+        T.toc_map_values(w.dev, T.TOC_MAP_SCALE, 1.0)
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
+    b = 16.0 * info["n_stored"]
+    res["map_values"] = {"ms": round(ms, 4), "bytes": b, "GB/s": b / ms / 1e6,
+                         "hbm_frac": b / (ms / 1e3) / HBM_PEAK}
+    dense_bytes = 4 * info["n_rows"] * info["n_cols"]
+    free, _ = torch.cuda.mem_get_info()
+    if dense_bytes + (1 << 30) < free:
+        A = torch.empty((info["n_rows"], info["n_cols"]), dtype=torch.float32, device="cuda:0")
+        T.toc_decode_dense(w.dev, A, 0.0)
+        ev[0].record(stream)
+        for i in range(reps):
+            T.toc_decode_dense(w.dev, A, 0.0)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]))
+        b = float(info["canon_bytes"] + dense_bytes)
+        res["decode_dense"] = {"ms": round(ms, 4), "bytes": b, "GB/s": b / ms / 1e6,
+                               "hbm_frac": b / (ms / 1e3) / HBM_PEAK}
+        del A
+        torch.cuda.empty_cache()
+    else:
+        res["decode_dense"] = None
+    log("element-wise: " + ", ".join(f"{k} {v['ms']:.3f} ms ({v['hbm_frac']:.1%} of HBM peak)"
+                                     for k, v in res.items() if v))
+    return res
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -186,6 +230,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--workers", type=int, default=0)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip timing the element-wise operations after the step")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device three times "
                          "(reference dispatches for HBM byte counters)")
@@ -253,6 +299,7 @@ def main():
         del src, dst
 
     info = w.info
+    extras = None if args.no_extras else time_elementwise(w, stream)
     nnz = info["nnz"]
     canon = info["canon_bytes"]
     n_rows, m = info["n_rows"], info["n_cols"]
@@ -316,6 +363,7 @@ def main():
         "hbm_frac_compressed": {op: ops[op]["hbm_frac_compressed"] for op in names},
         "ops": ops,
         "roofline": roof,
+        "elementwise": extras,
         "cpu_baseline": cpu,
         "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
                  "cpu": host_cpu()},

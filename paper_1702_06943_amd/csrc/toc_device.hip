@@ -1868,34 +1868,32 @@ __global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restri
 }
 
 // ===========================================================================
-// Dense decode plus a scalar (Algorithm 9): one workgroup per batch fills the
-// batch's rows with c, then every entry of D writes its sequence's pairs,
-// a_ij + c, walking its chain to the root; a wave per tuple, a lane per entry.
-// The fill is made visible before the pairs are written (fence, barrier).
+// Dense decode plus a scalar (Algorithm 9): one workgroup per batch, a wave per
+// tuple.  When a row of the dense block fits (ROW_LDS: n_cols floats per wave in
+// LDS), the wave fills its row in LDS with c, every entry of the tuple (a lane
+// each) writes its sequence's pairs a_ij + c there while walking its chain to the
+// root, and the row goes to HBM once with 16-byte stores.  Otherwise the rows are
+// filled in HBM first, made visible (fence, barrier), then the pairs written.
 // ===========================================================================
 constexpr int kDnBlock = 1024;
 constexpr int kDnWaves = kDnBlock / kWave;
 
+template <bool ROW_LDS>
 __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t b0, int m,
                                                                 float c, float *__restrict__ A,
                                                                 int64_t lda) {
+  extern __shared__ float dn_rows[];
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = uniform_batch(im.batches + b);
   const int lane = threadIdx.x % kWave, wave = wave_id();
   float *Ab = A + bt.row_base * lda;
-  for (int r = wave; r < bt.n_rows; r += kDnWaves) {
-    float *row = Ab + (int64_t)r * lda;
-    for (int j = lane; j < m; j += kWave) row[j] = c;
-  }
-  __threadfence();
-  __syncthreads();
   const toc_key *key = im.key + bt.code_base;
   const toc_link *link = im.link + bt.code_base;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
-  for (int r = wave; r < bt.n_rows; r += kDnWaves) {
-    float *row = Ab + (int64_t)r * lda;
+  // the pairs of the tuple r into row (LDS or HBM)
+  auto scatter = [&](int r, float *row) {
     const uint32_t e = span[r + 1];
     for (uint32_t j = span[r] + lane; j < e; j += kWave) {
       uint32_t x = dc[j];
@@ -1906,6 +1904,33 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
         x = link[x].parent;
       }
     }
+  };
+  if constexpr (ROW_LDS) {
+    float *row = dn_rows + (size_t)wave * m;
+    const bool vec = (m % 4) == 0 && (lda % 4) == 0 && (((uintptr_t)A) & 15u) == 0;
+    for (int r = wave; r < bt.n_rows; r += kDnWaves) {
+      for (int j = lane; j < m; j += kWave) row[j] = c;
+      __builtin_amdgcn_wave_barrier();
+      scatter(r, row);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      float *dst = Ab + (int64_t)r * lda;
+      if (vec) {
+        for (int j = 4 * lane; j < m; j += 4 * kWave) *(float4 *)&dst[j] = *(const float4 *)&row[j];
+      } else {
+        for (int j = lane; j < m; j += kWave) dst[j] = row[j];
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    for (int r = wave; r < bt.n_rows; r += kDnWaves) {
+      float *row = Ab + (int64_t)r * lda;
+      for (int j = lane; j < m; j += kWave) row[j] = c;
+    }
+    __threadfence();
+    __syncthreads();
+    for (int r = wave; r < bt.n_rows; r += kDnWaves) scatter(r, Ab + (int64_t)r * lda);
   }
 }
 
@@ -2377,9 +2402,17 @@ toc_status toc_decode_dense(const toc_dev *d, float c, float *A, int64_t lda, vo
   if (nb == 0 || d->info.n_rows == 0 || m == 0) return TOC_OK;
   const Img im = image_of(d);
   hipStream_t s = (hipStream_t)stream;
+  const size_t lds = (size_t)kDnWaves * m * sizeof(float);
+  const bool row_lds = lds <= kLdsMax;
+  if (row_lds && (st = allow_lds(decode_dense_kernel<true>, lds))) return st;
   for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
     const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-    hipLaunchKernelGGL(decode_dense_kernel, dim3(g), dim3(kDnBlock), 0, s, im, b0, m, c, A, lda);
+    if (row_lds)
+      hipLaunchKernelGGL(decode_dense_kernel<true>, dim3(g), dim3(kDnBlock), lds, s, im, b0, m, c,
+                         A, lda);
+    else
+      hipLaunchKernelGGL(decode_dense_kernel<false>, dim3(g), dim3(kDnBlock), 0, s, im, b0, m, c,
+                         A, lda);
     if ((st = launch_status("decode_dense_kernel"))) return st;
   }
   return TOC_OK;
