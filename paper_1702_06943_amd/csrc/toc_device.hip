@@ -641,7 +641,7 @@ struct RtChunk {
 };
 
 __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
-    Img im, int64_t nb, int n_tiles, int spw, int m, const float *__restrict__ W,
+    Img im, int64_t nb, int n_tiles, int spw, int per, int m, const float *__restrict__ W,
     int64_t ldw, int k, float *__restrict__ R, int64_t ldr) {
   extern __shared__ float4 smem4[];
   const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
@@ -654,21 +654,26 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
   const uint32_t zrow_b = wb + (uint32_t)m * kRtRowBytes;
   for (int e = threadIdx.x; e < kRtKT; e += kRtBlock) Wt[m * kRtKT + e] = 0.0f;
   if (threadIdx.x < 2) tg_next[threadIdx.x] = kRtWaves;
+  // batches of this XCD, taken `per` (1 or 2) at a time
   const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
-  const int64_t n_items = nbx * n_tiles;
+  const int64_t n_items = (nbx + per - 1) / per * n_tiles;
   int cur_tile = -1;
   uint32_t parity = 0;
   for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
-    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
+    const int64_t gj = uniform64(per * (it / n_tiles));
+    const bool two = per == 2 && gj + 1 < nbx;               // a second batch B after A
     const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
     const int k0 = tile * kRtKT;
     const int kt = min(kRtKT, k - k0);
-    const toc_batch bt = uniform_batch(im.batches + b);
-    const uint32_t *lvl = im.level + bt.lvl_base;
-    const uint32_t *span = im.span + bt.span_base;
-    const uint32_t *dc = im.dcodes + bt.d_base;
-    const uint32_t n1 = (uint32_t)bt.n_lvl1;
-    const int nrows = bt.n_rows;
+    const toc_batch ba = uniform_batch(im.batches + x + kXcd * gj);
+    const toc_batch bb = uniform_batch(im.batches + x + kXcd * (two ? gj + 1 : gj));
+    const uint32_t *lvl_a = im.level + ba.lvl_base, *lvl_b = im.level + bb.lvl_base;
+    const uint32_t n1a = (uint32_t)ba.n_lvl1, n1b = (uint32_t)bb.n_lvl1;
+    const int nrows_a = ba.n_rows, nrows_b = two ? bb.n_rows : 0;
+    const int lev_a = ba.n_levels, lev_b = two ? bb.n_levels : 0;
+    // H row of deep code c: db + c (A's deep rows first, then B's)
+    const uint32_t db_a = (uint32_t)m + 1u - n1a;
+    const uint32_t db_b = (uint32_t)m + 1u + ((uint32_t)ba.n_codes - n1a) - n1b;
     __syncthreads();   // the previous item no longer reads the W tile or the deep rows
     // the counter of the previous item is free again: ready for the next one
     if (threadIdx.x == 0) tg_next[parity ^ 1u] = kRtWaves;
@@ -704,55 +709,72 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       cur_tile = tile;
       __syncthreads();
     }
-    // H of depth >= 2 codes, level by level: 8 lanes per code (4 columns each,
-    // 16-byte accesses), kRtDeepU codes per group and round.  Every load is
-    // unconditional (indices are clamped to valid codes) so that the loads of a
-    // round are all in flight together.
+    // H of depth >= 2 codes, level by level, both batches together: 8 lanes per
+    // code (4 columns each, 16-byte accesses), kRtDeepU codes per group and
+    // round.  Every load is unconditional (indices are clamped to valid codes)
+    // so that the loads of a round are all in flight together.
     {
-      const toc_key *key = im.key + bt.code_base;
-      const toc_link *link = im.link + bt.code_base;
+      const toc_key *key_a = im.key + ba.code_base, *key_b = im.key + bb.code_base;
+      const toc_link *link_a = im.link + ba.code_base, *link_b = im.link + bb.code_base;
       const uint32_t g8 = threadIdx.x / 8u, q4 = 4u * (threadIdx.x % 8u);
       constexpr uint32_t stride = kRtBlock / 8;
-      for (int d = 2; d <= bt.n_levels; ++d) {
-        const uint32_t a = lvl[d - 1], e = lvl[d];
-        for (uint32_t c0 = a + g8; c0 < e; c0 += kRtDeepU * stride) {
-          uint32_t cs[kRtDeepU], p[kRtDeepU];
+      const int n_lev = max(lev_a, lev_b);
+      for (int d = 2; d <= n_lev; ++d) {
+        // level d of A is codes [a0, a0 + na), of B [b0, b0 + (n - na))
+        const uint32_t a0 = d <= lev_a ? lvl_a[d - 1] : 0u;
+        const uint32_t na = d <= lev_a ? lvl_a[d] - a0 : 0u;
+        const uint32_t b0 = d <= lev_b ? lvl_b[d - 1] : 0u;
+        const uint32_t n = na + (d <= lev_b ? lvl_b[d] - b0 : 0u);
+        for (uint32_t i0 = g8; i0 < n; i0 += kRtDeepU * stride) {
+          uint32_t cs[kRtDeepU], p[kRtDeepU], n1[kRtDeepU], db[kRtDeepU];
+          bool live[kRtDeepU];
           uint2 kc[kRtDeepU], kp[kRtDeepU];
+          const toc_key *kb[kRtDeepU];
 #pragma unroll
           for (int u = 0; u < kRtDeepU; ++u) {
-            cs[u] = c0 + u * stride;
-            const uint32_t cc = cs[u] < e ? cs[u] : c0;
-            p[u] = link[cc].parent;
-            kc[u] = *(const uint2 *)(key + cc);
+            live[u] = i0 + u * stride < n;
+            const uint32_t i = live[u] ? i0 + u * stride : i0;
+            const bool in_b = i >= na;
+            cs[u] = in_b ? b0 + (i - na) : a0 + i;
+            kb[u] = in_b ? key_b : key_a;
+            n1[u] = in_b ? n1b : n1a;
+            db[u] = in_b ? db_b : db_a;
+            p[u] = (in_b ? link_b : link_a)[cs[u]].parent;
+            kc[u] = *(const uint2 *)(kb[u] + cs[u]);
           }
 #pragma unroll
-          for (int u = 0; u < kRtDeepU; ++u) kp[u] = *(const uint2 *)(key + (p[u] < n1 ? p[u] : 0u));
+          for (int u = 0; u < kRtDeepU; ++u) kp[u] = *(const uint2 *)(kb[u] + (p[u] < n1[u] ? p[u] : 0u));
           float4 bl[kRtDeepU], w[kRtDeepU];
 #pragma unroll
           for (int u = 0; u < kRtDeepU; ++u) {
-            const uint32_t lrow = p[u] < n1 ? kp[u].x : (uint32_t)m + 1u + (p[u] - n1);
+            const uint32_t lrow = p[u] < n1[u] ? kp[u].x : db[u] + p[u];
             bl[u] = *(const float4 *)&Wt[lrow * kRtKT + q4];
             w[u] = *(const float4 *)&Wt[kc[u].x * kRtKT + q4];
           }
 #pragma unroll
           for (int u = 0; u < kRtDeepU; ++u) {
-            const float vp = p[u] < n1 ? __uint_as_float(kp[u].y) : 1.0f;
+            const float vp = p[u] < n1[u] ? __uint_as_float(kp[u].y) : 1.0f;
             const float vc = __uint_as_float(kc[u].y);
             const float4 h = make_float4(fmaf(vc, w[u].x, vp * bl[u].x), fmaf(vc, w[u].y, vp * bl[u].y),
                                          fmaf(vc, w[u].z, vp * bl[u].z), fmaf(vc, w[u].w, vp * bl[u].w));
-            if (cs[u] < e) *(float4 *)&Wt[(m + 1 + (cs[u] - n1)) * kRtKT + q4] = h;
+            if (live[u]) *(float4 *)&Wt[(db[u] + cs[u]) * kRtKT + q4] = h;
           }
         }
         __syncthreads();
       }
     }
-    // per-tuple sums
-    const int n_tg = (nrows + kRtGroups - 1) / kRtGroups;
+    // per-tuple sums.  Tuple groups 0 .. n_tga - 1 are A's, then B's.
+    const int n_tga = (nrows_a + kRtGroups - 1) / kRtGroups;
+    const int n_tg = n_tga + (nrows_b + kRtGroups - 1) / kRtGroups;
+    const uint32_t *span_a = im.span + ba.span_base, *span_b = im.span + bb.span_base;
     // rows past the end read span[nrows] twice: an empty tuple
     auto spans_of = [&](int tg, uint32_t &st, uint32_t &en) {
-      const int r = min(tg * kRtGroups + grp, nrows);
+      const bool in_b = tg >= n_tga;
+      const uint32_t *span = in_b ? span_b : span_a;
+      const int nr = in_b ? nrows_b : nrows_a;
+      const int r = min((in_b ? tg - n_tga : tg) * kRtGroups + grp, nr);
       st = span[r];
-      en = span[min(r + 1, nrows)];
+      en = span[min(r + 1, nr)];
     };
     auto wave_max = [&](uint32_t v) -> uint32_t {
       v = max(v, (uint32_t)__shfl_xor((int)v, 16, kWave));
@@ -802,11 +824,14 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // Every load below is unconditional: the buffer range checks turn reads past
     // the batch's arrays into zeros, and entries past the end of a tuple are
     // marked in a wave mask and become (zero row, 0) when translated.
-    const BufRes rs_dc = buf_res(dc, (uint32_t)bt.n_d);
-    const BufRes rs_node = key_res(im.key + bt.code_base, (uint32_t)bt.n_codes);
+    const BufRes rs_dc_a = buf_res(im.dcodes + ba.d_base, (uint32_t)ba.n_d);
+    const BufRes rs_dc_b = buf_res(im.dcodes + bb.d_base, (uint32_t)bb.n_d);
+    const BufRes rs_node_a = key_res(im.key + ba.code_base, (uint32_t)ba.n_codes);
+    const BufRes rs_node_b = key_res(im.key + bb.code_base, (uint32_t)bb.n_codes);
     // codes of entries sub + 16 h (h < kRtPer) of the load stage's chunk
     auto load_codes = [&](uint32_t (&d)[kRtPer], uint64_t (&ok)[kRtPer]) {
       const bool live = ltg < n_tg;
+      const BufRes rs_dc = ltg >= n_tga ? rs_dc_b : rs_dc_a;
       static_for<kRtPer>([&](auto hc) {
         constexpr int h = decltype(hc)::value;
         const uint32_t j = lst + lj + (uint32_t)sub + (uint32_t)(h * kRtLanes);
@@ -816,12 +841,13 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     };
     // (H row, multiplier) of an entry: a depth-1 code's row is its column of W
     // times its value; a deeper code's row is its own H row, times 1
-    auto translate = [&](uint32_t d, uint2 key, uint64_t ok, uint32_t &rb, uint32_t &mu) {
+    auto translate = [&](uint32_t d, uint2 key, uint64_t ok, uint32_t n1, uint32_t db, uint32_t &rb,
+                         uint32_t &mu) {
       if (d < n1) {
         rb = wb + key.x * kRtRowBytes;
         mu = key.y;
       } else {
-        rb = wb + ((uint32_t)m + 1u + (d - n1)) * kRtRowBytes;
+        rb = wb + (db + d) * kRtRowBytes;
         mu = __float_as_uint(1.0f);
       }
       if (!__builtin_amdgcn_inverse_ballot_w64(ok)) {
@@ -845,6 +871,8 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     auto step = [&](const uint32_t (&gd)[kRtPer], const uint64_t (&gok)[kRtPer],
                     uint32_t (&ld)[kRtPer], uint64_t (&lok)[kRtPer]) {
       advance();
+      const bool g_in_b = G.tg >= n_tga;
+      const BufRes rs_node = g_in_b ? rs_node_b : rs_node_a;
       uint2 key[kRtPer];
       static_for<kRtPer>([&](auto hc) {
         constexpr int h = decltype(hc)::value;
@@ -880,9 +908,10 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
           });
         }
         if (C.last) {
-          const int r = C.tg * kRtGroups + grp;
-          if (r < nrows) {
-            float *rr = R + (bt.row_base + r) * ldr + k0 + q;
+          const bool in_b = C.tg >= n_tga;
+          const int r = (in_b ? C.tg - n_tga : C.tg) * kRtGroups + grp;
+          if (r < (in_b ? nrows_b : nrows_a)) {
+            float *rr = R + ((in_b ? bb.row_base : ba.row_base) + r) * ldr + k0 + q;
             if (q + 1 < kt) {
               rr[0] = acc.x;
               rr[1] = acc.y;
@@ -896,7 +925,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       // chunk G becomes chunk C
       static_for<kRtPer>([&](auto hc) {
         constexpr int h = decltype(hc)::value;
-        translate(gd[h], key[h], gok[h], crb[h], cmu[h]);
+        translate(gd[h], key[h], gok[h], g_in_b ? n1b : n1a, g_in_b ? db_b : db_a, crb[h], cmu[h]);
       });
       C = G;
       G = L;
@@ -1992,6 +2021,7 @@ struct OpPlan {
   int64_t rows_max = 0, rows_total = 0;
   int64_t ws_floats = 0;      // tiled: whole workspace (one slot per worker)
   int64_t lds_rows = 0;       // tiled left: tree rows in LDS
+  int per = 1;                // tiled right: batches per item
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -2010,14 +2040,18 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
     const size_t tile = ((size_t)m + 1) * kRtKT * 4;
     const size_t lds_max = kLdsMax - kRtStaticBytes;
     const size_t with_deep = tile + (size_t)d->max_deep * kRtKT * 4;
+    const size_t with_pair = tile + (size_t)d->max_pair_deep * kRtKT * 4;
     if (k >= 4 && (with_deep <= lds_max || kRsStageBytes + tile <= lds_max)) {
       p.path = kPathTiled;
       p.n_tiles = (k + kRtKT - 1) / kRtKT;
       p.tw = kRtKT;
       p.deep_lds = with_deep <= lds_max;
-      p.lds = p.deep_lds ? with_deep : kRsStageBytes + tile;
+      // two batches per item when every pair's deep rows fit next to the tile
+      p.per = p.deep_lds && with_pair <= lds_max ? 2 : 1;
+      p.lds = p.deep_lds ? (p.per == 2 ? with_pair : with_deep) : kRsStageBytes + tile;
       // workers per XCD: one per CU, fewer when there are fewer items
-      const int64_t items = (d->info.n_batches + kXcd - 1) / kXcd * p.n_tiles;
+      const int64_t per_xcd = (d->info.n_batches + kXcd - 1) / kXcd;
+      const int64_t items = (per_xcd + p.per - 1) / p.per * p.n_tiles;
       p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
       p.grid = (unsigned)(kXcd * p.spx);
       p.row_floats = p.deep_lds ? 0 : kRtKT;
@@ -2246,7 +2280,7 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
     if (plan.deep_lds) {
       if ((st = allow_lds(right_tiled_kernel, plan.lds))) return st;
       hipLaunchKernelGGL(right_tiled_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im, nb,
-                         plan.n_tiles, plan.spx, m, W, ldw, k, R, ldr);
+                         plan.n_tiles, plan.spx, plan.per, m, W, ldw, k, R, ldr);
     } else {
       if ((st = allow_lds(right_staged_kernel, plan.lds))) return st;
       hipLaunchKernelGGL(right_staged_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im,

@@ -634,7 +634,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   int32_t n_cols = -1, max_depth = 0;
   dev->batches.assign((size_t)n_batches, toc_batch{});
   dev->max_rows = dev->max_codes = dev->max_levels = 0;
-  dev->max_d = dev->max_deep = dev->max_tree = 0;
+  dev->max_d = dev->max_deep = dev->max_tree = dev->max_pair_deep = 0;
   dev->dtile_base.assign((size_t)n_batches, 0);
   int64_t dtiles = 0;
   for (int64_t b = 0; b < n_batches; ++b) {
@@ -699,6 +699,14 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;
   dev->total_tree = tree;
+  dev->max_pair_deep = 0;
+  for (int64_t b = 0; b < n_batches; ++b) {
+    auto nd = [&](int64_t i) {
+      return (i + 1 < n_batches ? dev->batches[i + 1].deep_base : deep) - dev->batches[i].deep_base;
+    };
+    const bool first = (b / 8) % 2 == 0 && b + 8 < n_batches;
+    dev->max_pair_deep = std::max(dev->max_pair_deep, nd(b) + (first ? nd(b + 8) : 0));
+  }
   toc_dev_info &I = dev->info;
   I = toc_dev_info{};
   I.n_batches = n_batches;

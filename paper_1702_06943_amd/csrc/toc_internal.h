@@ -35,6 +35,9 @@ struct toc_dev {
   std::vector<toc_batch> batches;  // host copy of the batch table
   int32_t max_rows = 0, max_codes = 0, max_levels = 0;
   int64_t max_deep = 0, max_tree = 0, max_d = 0;
+  // most deep codes of two batches b, b + 8 with b / 8 even (the batch pairs of
+  // the right product's tiled kernel)
+  int64_t max_pair_deep = 0;
   int64_t total_deep = 0, total_tree = 0;
   std::vector<int64_t> dtile_base;  // first decode tile of each batch
   int64_t n_dtiles = 0;

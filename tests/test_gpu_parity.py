@@ -196,6 +196,50 @@ def test_config_batches(cfg, nb, k):
     print(f"{cfg} nb={nb} k={k}: max err/S = {worst:.3e}")
 
 
+def test_right_batch_pairs():
+    """27 batches of the c3 shape: the tiled right product takes the batches of an
+    XCD (b, b + 8, ...) two per work item when both batches' deep H rows fit in
+    LDS beside the W tile, and the last batch of an XCD with an odd count alone."""
+    B = config_batches("c3", 11, 27)
+    k = 40
+    W = config_W("c3", k)
+    res = run_gpu(B, W=W, decode=False)
+    check_against_oracle(B, res, W=W)
+
+
+def _host_deep(B):
+    """Deep (depth >= 2) codes of each batch, from a host image of that batch."""
+    out = []
+    for b in range(B.n_batches):
+        n, rp, c, v = B.batch(b)
+        one = _batches_from_csrs([(n, rp, c, v)], B.n_cols)
+        encs = T.toc_encode_batches(one.n_rows, one.n_cols, one.rowptr, one.col, one.val)
+        buf = np.zeros(T.toc_upload_size(encs, T.TOC_UPLOAD_HOST), np.uint8)
+        out.append(T.toc_dev_info_get(T.toc_upload(encs, buf, T.TOC_UPLOAD_HOST))["n_deep"])
+    return out
+
+
+def test_right_pairs_that_do_not_fit():
+    """n_cols = 1100: a 32-column W tile leaves LDS room for 178 deep H rows.
+    Every batch fits alone and some pairs (b, b + 8) do not, so the tiled right
+    product takes one batch per work item."""
+    n_cols = 1100
+    csrs = []
+    for i in range(24):
+        rp, c, v = tiny_batch(300 + i, n_rows=40, n_cols=n_cols, density=0.04, n_values=3,
+                              prefix_copy=0.2)
+        csrs.append((40, rp, c, v))
+    B = _batches_from_csrs(csrs, n_cols)
+    deep = _host_deep(B)
+    room = (160 * 1024 - 16 - (n_cols + 1) * 128) // 128
+    assert max(deep) <= room
+    assert max(deep[b] + deep[b + 8] for b in range(16) if (b // 8) % 2 == 0) > room
+    k = 45
+    W = np.random.default_rng(4).standard_normal((n_cols, k)).astype(np.float32)
+    res = run_gpu(B, W=W, decode=False)
+    check_against_oracle(B, res, W=W)
+
+
 def test_accumulate_and_strides():
     B = _tiny_set(5)
     rng = np.random.default_rng(11)
