@@ -489,6 +489,17 @@ __device__ inline uint2 key_load(BufRes r, uint32_t c) {
   return make_uint2(v[0], v[1]);
 }
 
+// Buffer over n links; link_load reads the (parent, depth) pair of one.
+__device__ inline BufRes link_res(const toc_link *p, uint32_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<toc_link *>(p), (short)0,
+                                           (int)(n * (uint32_t)sizeof(toc_link)), kBufFlags);
+}
+
+__device__ inline uint2 link_load(BufRes r, uint32_t c) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, c * (uint32_t)sizeof(toc_link), 0, 0);
+  return make_uint2(v[0], v[1]);
+}
+
 // LDS reads through address-space-3 pointers (byte addresses in LDS): the
 // compiler never merges such a read with a global one into a flat access.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -1807,22 +1818,28 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t nd = (uint32_t)bt.n_d, es = dt.y;
   const int64_t base = bt.nnz_base + dt.z;
+  // every load is unconditional, so that all of a thread's gathers are in
+  // flight together: entries past the batch's end take the code 0xFFFFFFFF,
+  // whose key and link reads fall outside the buffers and return zeros (depth
+  // 0); depth-1 codes (below n_lvl1) read no link either
+  const BufRes rs_dc = buf_res(dc, nd);
+  const BufRes rs_key = key_res(key, (uint32_t)bt.n_codes);
+  const BufRes rs_link = link_res(link, (uint32_t)bt.n_codes);
   uint32_t c[kDecPer];
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) {
     const uint32_t j = es + i * kDecBlock + threadIdx.x;
-    c[i] = j < nd ? dc[j] : 0u;
+    c[i] = buf_load(rs_dc, j);
+    if (j >= nd) c[i] = 0xFFFFFFFFu;
   }
-  // the key pair of each entry's code and its depth: 1 below n_lvl1 (depth-1
-  // codes come first), else from the code's link, which also holds its parent
+  // the key pair of each entry's code and its link (parent, depth)
   uint2 kv[kDecPer];
   uint2 lk[kDecPer];
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) {
-    const uint32_t j = es + i * kDecBlock + threadIdx.x;
-    kv[i] = j < nd ? *(const uint2 *)(key + c[i]) : make_uint2(0u, 0u);
-    lk[i] = make_uint2(0xFFFFFFFFu, j < nd ? 1u : 0u);
-    if (j < nd && c[i] >= n1) lk[i] = *(const uint2 *)(link + c[i]);
+    kv[i] = key_load(rs_key, c[i]);
+    lk[i] = link_load(rs_link, c[i] < n1 ? 0xFFFFFFFFu : c[i]);
+    if (c[i] < n1) lk[i].y = 1u;
   }
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) sh[i * kDecBlock + threadIdx.x] = lk[i].y;
