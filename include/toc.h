@@ -178,6 +178,12 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *             the codes of depth >= 2) are the codes tchild[h] .. tchild[h+1]-1
  *   pval    : float per batch n_codes entries (code_base): the key value of the
  *             code at each position
+ *   centry  : uint32 per batch n_d + n_tree entries (at d_base + tree_base): for
+ *             each key column in turn, its leaf occurrences (the occ_row words of
+ *             the column's leaves, first-occurrence bit included) and then its
+ *             tree codes (tlist entries) with bit 30 set; column j starts at the
+ *             cols entries of j: leaf occurrences before it plus tlist entries
+ *             before it.  Needs rows and codes below 2^30 per batch.
  * Depth-1 codes without children are numbered in the order of their first entry
  * in D; the codes of each level d >= 2 are sorted by parent.                    */
 typedef struct {
@@ -201,7 +207,7 @@ typedef struct {
 
 typedef struct {
   int64_t batches, level, key, link, span, dcodes, occ_off, occ_row, tlist, dtiles, cols,
-      tchild, pval, end;
+      tchild, pval, centry, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

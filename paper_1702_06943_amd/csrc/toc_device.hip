@@ -35,6 +35,7 @@ struct Img {
   const uint32_t *span;
   const uint32_t *dcodes;
   const uint32_t *pval;     // key value bits by left-product position
+  const uint32_t *centry;   // left-product entries of each key column
 };
 
 Img image_of(const toc_dev *d) {
@@ -43,7 +44,7 @@ Img image_of(const toc_dev *d) {
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
              (const toc_key *)(b + L.key), (const toc_link *)(b + L.link),
              (const uint32_t *)(b + L.span), (const uint32_t *)(b + L.dcodes),
-             (const uint32_t *)(b + L.pval)};
+             (const uint32_t *)(b + L.pval), (const uint32_t *)(b + L.centry)};
 }
 
 // Views of one field of a batch's node records, indexed by local code.
@@ -1353,7 +1354,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const uint32_t *lvl = im.level + bt.lvl_base;
     const uint32_t *oo = occ_off_all + bt.code_base + b;
     const uint32_t *orow = occ_row_all + bt.d_base;
-    const uint32_t *tl = tlist_all + bt.tree_base;
     const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
     const uint32_t n_tree = ni + (nc - n1);
     const int nrows = bt.n_rows;
@@ -1398,7 +1398,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       const uint32_t *tch = tchild_all + bt.tree_base + b;
       for (uint32_t h = threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = tch[h];
     }
-    const uint32_t obase = n1 > ni ? oo[ni] : 0u;
     __syncthreads();
     // Tree codes, deepest level first: H = own occurrences' G rows + children's
     // H rows.  A group takes kLtU codes at a time and issues their loads
@@ -1516,24 +1515,25 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       for (int o = LPG; o < kWave; o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
       return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
     };
-    // column j of group g of column group cg; past the last column: no entries
-    struct ColSpan { uint32_t ost, nl, nt, tof, lcode; };
+    // column j of group g of column group cg; past the last column: no entries.
+    // Its entries (leaf occurrences, then tree codes) start at cst in centry.
+    struct ColSpan { uint32_t cst, nl, nt, lcode; };
     auto col_of = [&](int cg) -> ColSpan {
       const int o = cg * GPW + grp;
       const int j = o < m ? (int)Ord[o] : m;
       const int j1 = min(j + 1, m);
       ColSpan c;
-      c.ost = Ost[j];
-      c.nl = Ost[j1] - c.ost;
-      c.tof = Toff[j];
-      c.nt = Toff[j1] - c.tof;
+      const uint32_t ost = Ost[j], tof = Toff[j];
+      c.cst = ost + tof;
+      c.nl = Ost[j1] - ost;
+      c.nt = Toff[j1] - tof;
       c.lcode = Loff[j];
       return c;
     };
     // load stage: column group lcg, entries [lj, lj + CHK) of each column
     int lcg = wave, ncg = n_cg;
     uint32_t lj = 0, lmax = 0;
-    ColSpan lc{0u, 0u, 0u, 0u, 0u};
+    ColSpan lc{0u, 0u, 0u, 0u};
     if (lcg < n_cg) {
       lc = col_of(lcg);
       lmax = wave_max(lc.nl + lc.nt);
@@ -1565,19 +1565,19 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       }
     };
     const BufRes rs_pval = buf_res(im.pval + bt.code_base, nc);
-    const uint32_t *dummy = lvl;   // a valid address for lanes without an entry
+    const BufRes rs_cent = buf_res(im.centry + bt.d_base + bt.tree_base, (uint32_t)bt.n_d + n_tree);
     // L: the entry words of each lane (entries sub + h * LPG of the chunk: the
-    // occ_row word of a leaf occurrence, or the code of a tree entry) and their
-    // kinds: 0 leaf, 1 tree, 2 none
-    auto load_entry = [&](uint32_t (&w)[PER], uint32_t (&kind)[PER], uint32_t &lcode) {
+    // occ_row word of a leaf occurrence, or a tree code marked kTreeEntry) and the
+    // wave masks of lanes with an entry.  A lane without one reads past the
+    // buffer: its word is 0 and its code 0xFFFFFFFF, whose pval read gives 0.
+    auto load_entry = [&](uint32_t (&w)[PER], uint64_t (&ok)[PER], uint32_t &lcode) {
       const bool live = lcg < n_cg;
 #pragma unroll
       for (int h = 0; h < PER; ++h) {
         const uint32_t e = lj + (uint32_t)(sub + h * LPG);
-        kind[h] = !live || e >= lc.nl + lc.nt ? 2u : (e < lc.nl ? 0u : 1u);
-        const uint32_t *p = kind[h] == 0u ? orow + obase + lc.ost + e
-                                          : (kind[h] == 1u ? tl + lc.tof + (e - lc.nl) : dummy);
-        w[h] = *p;
+        const bool in = live && e < lc.nl + lc.nt;
+        ok[h] = __ballot(in);
+        w[h] = buf_load(rs_cent, in ? lc.cst + e : 0xFFFFFFFFu);
       }
       lcode = lc.lcode;
     };
@@ -1604,8 +1604,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       cra[h] = zaddr;
       cmu[h] = 0u;
     }
-    auto step = [&](const uint32_t (&gw)[PER], const uint32_t (&gkind)[PER], uint32_t glcode,
-                    uint32_t (&lw)[PER], uint32_t (&lkind)[PER], uint32_t &llcode) {
+    auto step = [&](const uint32_t (&gw)[PER], const uint64_t (&gok)[PER], uint32_t glcode,
+                    uint32_t (&lw)[PER], uint64_t (&lok)[PER], uint32_t &llcode) {
       advance();
       // G: entries of the chunk loaded a step ago; the code of a leaf occurrence
       // is the column's first leaf code - 1 plus the first-occurrence bits up to
@@ -1614,14 +1614,17 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       uint32_t code[PER], row[PER];
 #pragma unroll
       for (int h = 0; h < PER; ++h) {
-        const uint64_t firsts = __ballot(gkind[h] == 0u && (gw[h] & kFirstOcc));
+        const bool tree = (gw[h] & toc::kTreeEntry) != 0u;     // a lane without entry has word 0
+        const bool leaf = __builtin_amdgcn_inverse_ballot_w64(gok[h]) && !tree;
+        const uint64_t firsts = __ballot(leaf && (gw[h] & kFirstOcc));
         const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
         // branch-free: leaf, tree or no entry
         const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
-        const uint32_t hr = hrow(gw[h]);
+        const uint32_t tc = gw[h] & ~toc::kTreeEntry;
+        const uint32_t hr = hrow(tc);
         const uint32_t trow = hr < cap ? trow0 + hr : (kRtGlobal | hr);
-        code[h] = gkind[h] == 0u ? lcode : (gkind[h] == 1u ? gw[h] : 0xFFFFFFFFu);
-        row[h] = gkind[h] == 0u ? (gw[h] & ~kFirstOcc) : (gkind[h] == 1u ? trow : zrow);
+        code[h] = leaf ? lcode : (tree ? tc : 0xFFFFFFFFu);
+        row[h] = leaf ? (gw[h] & ~kFirstOcc) : (tree ? trow : zrow);
         base += (uint32_t)__popc(gb);
       }
       gcode = base;
@@ -1629,7 +1632,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
 #pragma unroll
       for (int h = 0; h < PER; ++h) pv[h] = buf_load(rs_pval, code[h]);
       const LtChunk L = chunk_of_l();
-      load_entry(lw, lkind, llcode);
+      load_entry(lw, lok, llcode);
       if constexpr (DPP) {
         constexpr int NB = CHK / 4;             // blocks of 4 entries
         // does an entry of chunk C read a tree row in the workspace?
@@ -1759,18 +1762,19 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         // entries of chunk G become chunk C
 #pragma unroll
         for (int h = 0; h < PER; ++h) {
-          cra[h] = gkind[h] == 2u ? zaddr : ((row[h] & kRtGlobal) ? row[h] : rb0 + row[h] * RB);
-          cmu[h] = gkind[h] == 2u ? 0u : pv[h];
+          cra[h] = (row[h] & kRtGlobal) ? row[h] : rb0 + row[h] * RB;
+          cmu[h] = pv[h];
         }
       } else {
         // S: entry sub of column grp goes to stage[sub * GPW + grp]
-        stage[sub * GPW + grp] = make_uint2(row[0], gkind[0] == 2u ? 0u : pv[0]);
+        stage[sub * GPW + grp] = make_uint2(row[0], pv[0]);
         __builtin_amdgcn_wave_barrier();
       }
       C = G;
       G = L;
     };
-    uint32_t wA[PER], kA[PER], wB[PER], kB[PER], cA, cB;
+    uint32_t wA[PER], wB[PER], cA, cB;
+    uint64_t kA[PER], kB[PER];
     load_entry(wA, kA, cA);
     while (G.cg < n_cg || C.cg < n_cg) {
       step(wA, kA, cA, wB, kB, cB);

@@ -584,6 +584,15 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     std::sort(S.keys.begin(), S.keys.end());
     for (int64_t k = 0; k < m; ++k) c_ord[k] = (uint32_t)S.keys[k];
     c_ord[m] = 0;
+    // the entries of each column in one stretch: leaf occurrences, then tree
+    // codes marked with kTreeEntry
+    uint32_t *ce = (uint32_t *)(dst + L.centry) + bt.d_base + bt.tree_base;
+    const uint32_t *lo = occ_row + occ_off[n_int1];
+    int64_t o = 0;
+    for (int64_t j = 0; j < m; ++j) {
+      for (uint32_t q = c_occ[j]; q < c_occ[j + 1]; ++q) ce[o++] = lo[q];
+      for (uint32_t q = c_tree[j]; q < c_tree[j + 1]; ++q) ce[o++] = tlist[q] | kTreeEntry;
+    }
   }
   // children of each tree code (their H rows are added to its H in the left
   // multiplication): code h's children are codes tchild[h] .. tchild[h+1]-1, h
@@ -643,7 +652,8 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
     if (n_cols < 0) n_cols = e->n_cols;
     if (e->n_cols != n_cols) return fail(TOC_EINVAL, "batches differ in n_cols");
     const Counts c = counts_of(e, flags);
-    if (c.codes > INT32_MAX || c.d > INT32_MAX) return fail(TOC_EUNSUPPORTED, "batch too large");
+    if (c.codes >= kMaxBatchDim || c.d > INT32_MAX || e->n_rows >= kMaxBatchDim)
+      return fail(TOC_EUNSUPPORTED, "batch too large");
     toc_batch &bt = dev->batches[b];
     bt.code_base = codes;
     bt.d_base = d;
@@ -695,6 +705,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.cols = off;    off = align256(off + 16 * n_batches * ((int64_t)std::max(n_cols, 0) + 1));
   L.tchild = off;  off = align256(off + 4 * (tree + n_batches));
   L.pval = off;    off = align256(off + 4 * codes);
+  L.centry = off;  off = align256(off + 4 * (d + tree));
   dev->n_dtiles = dtiles;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;

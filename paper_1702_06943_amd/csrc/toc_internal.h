@@ -48,6 +48,11 @@ namespace toc {
 // Entries of D per decode tile (one independent workgroup each).
 constexpr int64_t kDecodeTile = 1024;
 
+// Marks a tree code in the column entries (centry) of the image; leaf
+// occurrence words there hold a row below 2^30 and the first-occurrence bit.
+constexpr uint32_t kTreeEntry = 0x40000000u;
+constexpr int64_t kMaxBatchDim = (int64_t)1 << 30;   // rows and codes per batch
+
 // Records a message for toc_last_error() and returns s.
 toc_status fail(toc_status s, const char *fmt, ...);
 void clear_error();

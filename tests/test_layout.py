@@ -39,6 +39,8 @@ def read_image(dev, buf):
         tchild=arr("tchild", np.uint32,
                    int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"] + 1).sum()) if nb else 0),
         pval=arr("pval", np.float32, n_codes),
+        centry=arr("centry", np.uint32, info["n_codes"] + (
+            int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0)),
     )
     for f in ("col", "val"):
         img[f] = img["key"][f]
@@ -66,6 +68,9 @@ def batch_view(img, b):
         tchild=img["tchild"][int(t["tree_base"]) + b:int(t["tree_base"]) + b + int(t["n_int1"]) + nc
                              - int(t["n_lvl1"]) + 1],
         pval=img["pval"][cb:cb + nc],
+        centry=img["centry"][int(t["d_base"]) + int(t["tree_base"]):
+                             int(t["d_base"]) + int(t["tree_base"]) + int(t["n_d"]) + int(t["n_int1"])
+                             + nc - int(t["n_lvl1"])],
     )
 
 
@@ -148,6 +153,17 @@ def check_invariants(v):
         ps = [pos[c] for c in range(ni, n1) if v["col"][c] == j]
         assert ps == list(range(int(cx[0, j]), int(cx[0, j + 1])))
         assert sum(int(oo[p + 1] - oo[p]) for p in ps) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
+    # column entries: per column its leaf occurrence words, then its tree codes
+    # with bit 30 set, starting after the entries of the columns before it
+    ce = v["centry"]
+    orow_raw = v["occ_row"]
+    for j in range(m):
+        st = int(cx[1, j] + cx[2, j])
+        nlj, ntj = int(cx[1, j + 1] - cx[1, j]), int(cx[2, j + 1] - cx[2, j])
+        lo = int(oo[ni]) + int(cx[1, j])
+        assert np.array_equal(ce[st:st + nlj], orow_raw[lo:lo + nlj])
+        assert np.array_equal(ce[st + nlj:st + nlj + ntj],
+                              tl[int(cx[2, j]):int(cx[2, j + 1])] | np.uint32(0x40000000))
     # children ranges: tree code h's children are tchild[h] .. tchild[h+1]-1
     hrow = lambda c: c if c < ni else c - n1 + ni
     tch = v["tchild"]
