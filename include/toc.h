@@ -53,7 +53,7 @@ typedef struct {
   int64_t n_deep;       /* live codes whose sequence has two or more pairs        */
   int32_t max_depth;    /* longest live sequence                                  */
   int32_t reserved;
-  int64_t phys_bytes;   /* size of the paper's physical encoding (section 3.3)   */
+  int64_t phys_bytes;   /* size of the paper's physical encoding (section 3.2)   */
   int64_t canon_bytes;  /* canonical compressed bytes:
                            4|D| + 4(n_rows+1) + 10 n_live + 4(max_depth+1)       */
 } toc_enc_info;

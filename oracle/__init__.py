@@ -27,7 +27,12 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
                  integer sums in closed form
   layout_stats   pinned: hand count on the worked example (live set, depths)
   physical_bytes parity unpinned (the paper prints sizes only in missing figures;
-                 the formula of §3.3 is checked on the worked example by hand)
+                 the formula of §3.2 is checked on the worked example by hand)
+  pack_physical, unpack_physical
+                 pinned: the worked example's bytes derived by hand from Table 2's
+                 I and D under the byte-layout reading, the width rule of §3.2 at
+                 every byte boundary (its "max 4 needs 1 byte" example included),
+                 round trips, size equal to physical_bytes, malformed inputs
 """
 
 from .toc_oracle import (  # noqa: F401
@@ -47,6 +52,8 @@ from .toc_oracle import (  # noqa: F401
     MAP_SQUARE,
     layout_stats,
     physical_bytes,
+    pack_physical,
+    unpack_physical,
     f32_bits,
     bits_f32,
 )

@@ -372,7 +372,7 @@ def layout_stats(I, D):
 
 
 def _packed_array_bytes(values):
-    """Bit packing of §3.3: ceil(log2(max+1)/8) bytes per integer (at least one),
+    """Bit packing of §3.2: ceil(log2(max+1)/8) bytes per integer (at least one),
     plus a header holding the count (u32) and the bytes per integer (u8)."""
     mx = max(values, default=0)
     width = max(1, math.ceil(math.log2(mx + 1) / 8)) if mx > 0 else 1
@@ -380,7 +380,7 @@ def _packed_array_bytes(values):
 
 
 def physical_bytes(I, D):
-    """Physical encoding of §3.3: I's columns bit-packed, I's values replaced by
+    """Physical encoding of §3.2: I's columns bit-packed, I's values replaced by
     indices into an array of unique values (4 bytes each) which are bit-packed,
     D's codes concatenated and bit-packed, tuple start offsets bit-packed."""
     uniq = sorted(set(b for _, b in I))
@@ -394,3 +394,80 @@ def physical_bytes(I, D):
         starts.append(starts[-1] + len(d))
     size += _packed_array_bytes(starts)
     return size
+
+
+# ---------------------------------------------------------------------------
+# Physical encoding as bytes, §3.2.  The paper fixes the techniques -- bit packing
+# with ceil(log2(max+1)/8) bytes per integer behind a header that gives the count
+# and the bytes per integer, value indexing of I's values, D's codes of all tuples
+# concatenated, and the tuple starting indexes -- but not the byte layout.  The
+# reading taken here: five arrays in the order I's columns, the unique values,
+# I's value indexes, D's codes, the tuple starts (n_rows + 1 offsets into D, the
+# last one |D|); each behind a 5-byte header (count as a little-endian u32, then
+# the bytes per integer as a u8); integers little-endian in that many bytes; the
+# unique values are the distinct binary32 bit patterns of I's values in
+# ascending order, 4 bytes each.  §4.1.1 reads such integers back by copying
+# their bytes into a wider integer.
+# ---------------------------------------------------------------------------
+def _width(mx):
+    """Bytes per integer for an array whose largest value is mx: ceil(log2(mx+1)/8),
+    at least one (bit_length is ceil(log2(mx+1)) exactly)."""
+    return max(1, (int(mx).bit_length() + 7) // 8)
+
+
+def _pack_array(values, width=None):
+    w = _width(max(values, default=0)) if width is None else width
+    out = bytearray(struct.pack("<IB", len(values), w))
+    for v in values:
+        out += int(v).to_bytes(w, "little")
+    return bytes(out)
+
+
+def _unpack_array(blob, pos):
+    if pos + 5 > len(blob):
+        raise TocInputError("truncated array header")
+    n, w = struct.unpack_from("<IB", blob, pos)
+    pos += 5
+    if not 1 <= w <= 4:
+        raise TocInputError("bytes per integer must be 1..4")
+    if pos + n * w > len(blob):
+        raise TocInputError("truncated array")
+    vals = [int.from_bytes(blob[pos + q * w:pos + (q + 1) * w], "little") for q in range(n)]
+    return vals, pos + n * w
+
+
+def pack_physical(I, D):
+    """(I, D) -> bytes of the physical encoding (reading above)."""
+    uniq = sorted(set(b for _, b in I))
+    where = {b: q for q, b in enumerate(uniq)}
+    starts = [0]
+    for d in D:
+        starts.append(starts[-1] + len(d))
+    blob = _pack_array([c for c, _ in I])
+    blob += _pack_array(uniq, width=4)
+    blob += _pack_array([where[b] for _, b in I])
+    blob += _pack_array([c for d in D for c in d])
+    blob += _pack_array(starts)
+    return blob
+
+
+def unpack_physical(blob):
+    """Bytes of the physical encoding -> (I, D); raises TocInputError on a
+    malformed input."""
+    cols, p = _unpack_array(blob, 0)
+    if p + 5 <= len(blob) and blob[p + 4] != 4:
+        raise TocInputError("unique values are 4 bytes each")
+    uniq, p = _unpack_array(blob, p)
+    vidx, p = _unpack_array(blob, p)
+    codes, p = _unpack_array(blob, p)
+    starts, p = _unpack_array(blob, p)
+    if p != len(blob):
+        raise TocInputError("trailing bytes")
+    if len(vidx) != len(cols) or any(q >= len(uniq) for q in vidx):
+        raise TocInputError("bad value indexes")
+    if not starts or starts[0] != 0 or starts[-1] != len(codes) or \
+            any(b < a for a, b in zip(starts, starts[1:])):
+        raise TocInputError("bad tuple starts")
+    I = [(c, uniq[q]) for c, q in zip(cols, vidx)]
+    D = [codes[starts[r]:starts[r + 1]] for r in range(len(starts) - 1)]
+    return I, D

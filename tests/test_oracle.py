@@ -352,3 +352,91 @@ def test_dense_plus_integer_sum():
     I, D, _ = O.encode(rows)
     B = O.dense_plus(O.decode(I, D), m, 3.0)
     assert float(B.astype(np.float64).sum()) == float(dense.sum()) + 3.0 * n * m
+
+
+# --- physical encoding (Section 3.2) as bytes --------------------------------------
+PHYS = json.load(open(os.path.join(HERE, "golden", "physical_worked_example.json")))
+
+
+def test_physical_worked_example(example):
+    rows, I, D, N = example
+    want = bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"]))
+    assert len(want) == PHYS["total_bytes"] == GOLD["sizes"]["physical_bytes"]
+    assert O.pack_physical(I, D) == want
+    assert O.unpack_physical(want) == (I, D)
+
+
+# Section 3.2's width rule at each byte boundary; its own example: a largest column
+# index of 4 needs 1 byte
+@pytest.mark.parametrize("mx,width,tail", [
+    (0, 1, "00"), (4, 1, "04"), (255, 1, "ff"), (256, 2, "0001"), (65535, 2, "ffff"),
+    (65536, 3, "000001"), (0x123456, 3, "563412"), (2**24 - 1, 3, "ffffff"),
+    (2**24, 4, "00000001"), (2**32 - 1, 4, "ffffffff")])
+def test_physical_width_rule(mx, width, tail):
+    blob = O.pack_physical([(mx, O.f32_bits(1.0))], [])
+    # the I-column array: count 1, then the width, then the column in that many bytes
+    assert blob[:5 + width].hex() == "01000000" + "%02x" % width + tail
+    assert O.unpack_physical(blob) == ([(mx, O.f32_bits(1.0))], [])
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_physical_round_trip(seed, case):
+    spec = CASES[case]
+    rp, c, v = tiny_batch(3000 + seed * 31 + case, **spec)
+    rows = O.canonicalize(spec["n_rows"], spec["n_cols"], rp, c, v)
+    I, D, N = O.encode(rows)
+    blob = O.pack_physical(I, D)
+    assert len(blob) == O.physical_bytes(I, D)
+    assert O.unpack_physical(blob) == (I, D)
+    assert O.decode(*O.unpack_physical(blob)) == rows
+
+
+def test_physical_empty_batch():
+    blob = O.pack_physical([], [[], []])
+    assert O.unpack_physical(blob) == ([], [[], []])
+    assert O.build_cprime(*O.unpack_physical(blob))["n_nodes"] == 1
+
+
+def _phys_example():
+    return bytearray(bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"])))
+
+
+def _bad_truncated():
+    return _phys_example()[:-1]
+
+
+def _bad_trailing():
+    return _phys_example() + b"\x00"
+
+
+def _bad_width():
+    b = _phys_example()
+    b[4] = 5
+    return b
+
+
+def _bad_value_width():
+    b = _phys_example()
+    b[10 + 4] = 2
+    return b
+
+
+def _bad_value_index():
+    b = _phys_example()
+    b[10 + 21 + 5] = 4          # first value index -> 4, but only 4 unique values
+    return b
+
+
+def _bad_starts():
+    b = _phys_example()
+    b[-3] = 7                   # tuple starts 0,4,7,6,9: not monotone
+    b[-2] = 6
+    return b
+
+
+@pytest.mark.parametrize("make", [_bad_truncated, _bad_trailing, _bad_width,
+                                  _bad_value_width, _bad_value_index, _bad_starts])
+def test_physical_rejects(make):
+    with pytest.raises(O.TocInputError):
+        O.unpack_physical(bytes(make()))
