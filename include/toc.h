@@ -279,6 +279,73 @@ toc_status toc_map_values(const toc_dev *dev, int32_t op, float c, void *stream)
  * TOC_EDEVICE. */
 toc_status toc_decode_dense(const toc_dev *dev, float c, float *A, int64_t lda, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Physical encoding and the decoding tree on the device.
+ *
+ * Section 3.2 stores (I, D) as bytes: bit packing (ceil(log2(max+1)/8) bytes per
+ * integer, behind a header with the count and the bytes per integer) and value
+ * indexing of I's values.  The paper leaves the byte layout open; this library
+ * reads it as five arrays, in order: I's columns, the unique values (the distinct
+ * binary32 bit patterns of I's values, ascending, 4 bytes each), I's value
+ * indexes, D's codes of all tuples concatenated (paper numbering), the tuple
+ * starts (n_rows + 1 offsets into D, the last one |D|).  Each array is a 5-byte
+ * header (count: little-endian u32; bytes per integer: u8, 1..4, 4 for the
+ * values) followed by count little-endian integers of that many bytes.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int64_t n_rows;       /* tuples                                                 */
+  int64_t n_first;      /* |I|                                                    */
+  int64_t n_codes;      /* |D|                                                    */
+  int64_t n_unique;     /* distinct values of I                                   */
+  int64_t n_nodes;      /* |C'| including the root = 1 + |I| + sum(len(D_i)-1)    */
+} toc_phys_info;
+
+/* Bytes of the physical encoding of one encoded batch (host, synchronous). */
+toc_status toc_enc_pack_size(const toc_enc *enc, size_t *bytes);
+/* Writes them to dst (host memory of at least that many bytes): TOC_ESIZE if
+ * bytes is smaller. */
+toc_status toc_enc_pack(const toc_enc *enc, void *dst, size_t bytes);
+/* Reads the headers and tuple starts of one blob in host memory and checks the
+ * layout (sizes, widths, starts non-decreasing from 0 to |D|): TOC_EINVAL if it
+ * does not hold.  Codes and value indexes are checked by toc_cprime_build. */
+toc_status toc_phys_info_get(const void *blob, size_t bytes, toc_phys_info *info);
+
+/* Workspace bytes of toc_cprime_build for n_batches batches and n_nodes nodes in
+ * total. */
+toc_status toc_cprime_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *bytes);
+
+/* Algorithm 2 (BuildPrefixTree, section 4.1.2) on the device, one workgroup per
+ * batch, straight from physical bytes (section 4.1.1 reads them back).  Node 0
+ * is the root, nodes 1..|I| are I in order, and the entry at position j < len-1
+ * of tuple i of D makes the next node, whose parent is D_i[j] and whose key is
+ * the first pair of D_i[j+1]'s sequence; depth is the sequence length.  The
+ * first pair of a node and its depth are found by pointer jumping along parents.
+ *   blobs    device bytes holding the batches' blobs; batch b is bytes
+ *            blob_off[b] .. blob_off[b+1]-1 (blob_off: host, n_batches+1 entries,
+ *            non-decreasing)
+ *   node_off host, n_batches+1 entries: batch b's nodes are output entries
+ *            node_off[b] .. node_off[b+1]-1 (toc_phys_info_get's n_nodes each)
+ *   max_rows the most tuples of any batch (at most 16384; sizes LDS)
+ *   parent, col, val, depth  device outputs, one entry per node in paper
+ *            numbering: the root has parent 0xFFFFFFFF, col 0xFFFFFFFF, val +0.0,
+ *            depth 0; nodes 1..|I| have parent 0
+ *   status   device int32 per batch: 0, or TOC_CPRIME_* below when the blob is
+ *            malformed (the batch's outputs are then unspecified; nothing outside
+ *            its blob and node range is touched)
+ *   ws       device workspace of toc_cprime_workspace_size bytes
+ * Asynchronous on stream; blob_off and node_off are copied before returning.
+ * Checks the host arrays and sizes (TOC_EINVAL, TOC_ESIZE).                  */
+#define TOC_CPRIME_LAYOUT 1       /* headers, widths or sizes do not hold         */
+#define TOC_CPRIME_VALUE_INDEX 2  /* a value index is not below the unique count  */
+#define TOC_CPRIME_STARTS 3       /* tuple starts not non-decreasing from 0 to |D| */
+#define TOC_CPRIME_CODE 4         /* a code names no node existing at that point  */
+#define TOC_CPRIME_NODES 5        /* the node count differs from node_off's span  */
+#define TOC_CPRIME_ROWS 6         /* more tuples than max_rows                    */
+toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                            int64_t n_batches, int32_t max_rows, uint32_t *parent, uint32_t *col,
+                            float *val, uint32_t *depth, int32_t *status, void *ws,
+                            size_t ws_bytes, void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *toc_last_error(void);
 

@@ -1,6 +1,7 @@
 """MI355X-native tuple-oriented compression (TOC): encode on the host, run A.W,
 G^T.A, decode, sparse-safe element-wise ops and dense A .+ c on the compressed
-mini-batches with hand-written gfx950 kernels.
+mini-batches with hand-written gfx950 kernels; pack batches into the paper's
+physical encoding and build the decoding tree C' from it on the GPU.
 
 The functions are those of include/toc.h, called through ctypes; see binding.py.
 """
@@ -14,4 +15,7 @@ from .binding import (  # noqa: F401
     toc_upload_size, toc_upload, toc_dev_info_get, toc_dev_layout_get,
     toc_workspace_size, toc_right_mul, toc_left_mul, toc_decode_csr,
     toc_map_values, toc_decode_dense,
+    TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
+    TOC_CPRIME_NODES, TOC_CPRIME_ROWS,
+    toc_enc_pack, toc_phys_info_get, toc_cprime_workspace_size, toc_cprime_build,
 )

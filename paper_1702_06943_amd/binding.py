@@ -22,6 +22,8 @@ TOC_UPLOAD_KEEP_DEAD = 1
 TOC_UPLOAD_HOST = 2
 TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE = 0, 1, 2
 TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
+(TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
+ TOC_CPRIME_NODES, TOC_CPRIME_ROWS) = range(1, 7)
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -45,6 +47,11 @@ class DevInfo(C.Structure):
                 ("max_depth", C.c_int32), ("nnz", C.c_int64), ("n_codes", C.c_int64),
                 ("n_stored", C.c_int64), ("n_deep", C.c_int64), ("canon_bytes", C.c_int64),
                 ("image_bytes", C.c_int64)]
+
+
+class PhysInfo(C.Structure):
+    _fields_ = [(n, C.c_int64) for n in
+                ("n_rows", "n_first", "n_codes", "n_unique", "n_nodes")]
 
 
 class Layout(C.Structure):
@@ -98,6 +105,11 @@ def lib():
         "toc_decode_csr": [P, P, P, P, P],
         "toc_map_values": [P, I32, C.c_float, P],
         "toc_decode_dense": [P, C.c_float, P, I64, P],
+        "toc_enc_pack_size": [P, P],
+        "toc_enc_pack": [P, P, SZ],
+        "toc_phys_info_get": [P, SZ, P],
+        "toc_cprime_workspace_size": [I64, I64, P],
+        "toc_cprime_build": [P, P, P, I64, I32, P, P, P, P, P, P, SZ, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -301,3 +313,51 @@ def toc_decode_dense(dev, A, c=0.0, stream=None):
     if A.shape[0] != info["n_rows"] or ncols < info["n_cols"]:
         raise TocError(TOC_EINVAL, "A must be n_rows x (>= n_cols)")
     _check(lib().toc_decode_dense(dev.handle, float(c), ap, lda, _stream(stream)))
+
+
+def toc_enc_pack(enc):
+    """The physical encoding (section 3.2) of one encoded batch, as uint8 bytes."""
+    n = C.c_size_t()
+    _check(lib().toc_enc_pack_size(enc.handle, C.byref(n)))
+    out = np.empty(max(n.value, 1), np.uint8)
+    _check(lib().toc_enc_pack(enc.handle, _ptr(out), n.value))
+    return out[:n.value]
+
+
+def toc_phys_info_get(blob):
+    """Counts of one physical-encoding blob (numpy uint8, host)."""
+    blob = _arr(blob, np.uint8)
+    info = PhysInfo()
+    _check(lib().toc_phys_info_get(_ptr(blob), blob.size, C.byref(info)))
+    return {f: getattr(info, f) for f, _ in PhysInfo._fields_}
+
+
+def toc_cprime_workspace_size(n_batches, n_nodes):
+    n = C.c_size_t()
+    _check(lib().toc_cprime_workspace_size(int(n_batches), int(n_nodes), C.byref(n)))
+    return n.value
+
+
+def toc_cprime_build(blobs, blob_off, node_off, max_rows, parent, col, val, depth, status,
+                     ws, stream=None):
+    """blobs: device uint8 tensor of the concatenated blobs; blob_off, node_off: host
+    int64 arrays of n_batches + 1 offsets; parent, col, depth: device int32/uint32
+    tensors and val a float32 tensor of node_off[-1] entries; status: device int32
+    tensor of n_batches entries; ws: device tensor of toc_cprime_workspace_size
+    bytes."""
+    blob_off, node_off = _arr(blob_off, np.int64), _arr(node_off, np.int64)
+    nb = blob_off.size - 1
+    if node_off.size != nb + 1:
+        raise TocError(TOC_EINVAL, "blob_off and node_off differ in length")
+    n = int(node_off[-1]) if nb >= 0 else 0
+    for t, name in ((parent, "parent"), (col, "col"), (val, "val"), (depth, "depth")):
+        if t.numel() < n or t.element_size() != 4:
+            raise TocError(TOC_EINVAL, f"{name} must hold {n} 4-byte entries")
+    if status.numel() < nb or status.element_size() != 4:
+        raise TocError(TOC_EINVAL, "status must hold one int32 per batch")
+    if blobs.numel() < int(blob_off[-1]):
+        raise TocError(TOC_EINVAL, "blobs shorter than blob_off[-1]")
+    _check(lib().toc_cprime_build(_ptr(blobs), _ptr(blob_off), _ptr(node_off), nb, int(max_rows),
+                                  _ptr(parent), _ptr(col), _ptr(val), _ptr(depth), _ptr(status),
+                                  _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+                                  _stream(stream)))

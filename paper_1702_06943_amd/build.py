@@ -32,14 +32,19 @@ def _run(cmd, verbose):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    host_o = os.path.join(BUILD, "toc_host.o")
-    dev_o = os.path.join(BUILD, "toc_device.o")
-    _run(["g++", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE,
-          "-c", os.path.join(CSRC, "toc_host.cpp"), "-o", host_o], verbose)
-    _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32,
-          "-I", INCLUDE, "-c", os.path.join(CSRC, "toc_device.hip"), "-o", dev_o], verbose)
+    objs = []
+    for src in ("toc_host.cpp", "toc_phys.cpp"):
+        o = os.path.join(BUILD, src.replace(".cpp", ".o"))
+        _run(["g++", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE,
+              "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        objs.append(o)
+    for src in ("toc_device.hip", "toc_cprime.hip"):
+        o = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32,
+              "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        objs.append(o)
     tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", host_o, dev_o, "-o", tmp,
+    _run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp,
           "-lpthread"], verbose)
     os.replace(tmp, LIB)
     return LIB

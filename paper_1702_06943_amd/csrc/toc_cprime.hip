@@ -1,0 +1,292 @@
+// The decoding tree C' built on the device from the physical encoding: Algorithm 2
+// (BuildPrefixTree, section 4.1.2) over integers read back from bit-packed bytes
+// (section 4.1.1), one workgroup per batch, batches in parallel.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "toc_internal.h"
+
+namespace {
+
+constexpr int kCpBlock = 512;
+constexpr int kCpWave = 64;
+constexpr int kCpWaves = kCpBlock / kCpWave;
+constexpr int kCpMaxRows = 16384;
+constexpr int kCpMaxRounds = 48;            // pointer jumping: ceil(log2(nodes)) + 1 suffice
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+// Integer i of a packed array of w-byte little-endian integers (w = 1..4): its
+// bytes copied into a 32-bit integer, the upper bytes zero (section 4.1.1).
+__device__ inline uint32_t rd(const uint8_t *p, uint64_t i, uint32_t w) {
+  const uint8_t *q = p + i * w;
+  uint32_t v = q[0];
+  if (w > 1) v |= (uint32_t)q[1] << 8;
+  if (w > 2) v |= (uint32_t)q[2] << 16;
+  if (w > 3) v |= (uint32_t)q[3] << 24;
+  return v;
+}
+
+// Exclusive prefix sum of x over the workgroup; total gets the sum of all.
+__device__ uint32_t block_excl_scan(uint32_t x, uint32_t *wsum, uint32_t &total) {
+  const int lane = threadIdx.x % kCpWave, wave = threadIdx.x / kCpWave;
+  uint32_t v = x;
+#pragma unroll
+  for (int o = 1; o < kCpWave; o <<= 1) {
+    const uint32_t y = __shfl_up(v, o, kCpWave);
+    if (lane >= o) v += y;
+  }
+  if (lane == kCpWave - 1) wsum[wave] = v;
+  __syncthreads();
+  uint32_t before = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < kCpWaves; ++w) {
+    before += w < wave ? wsum[w] : 0u;
+    total += wsum[w];
+  }
+  __syncthreads();
+  return before + v - x;
+}
+
+// Header of array a of a blob: count, bytes per integer, byte offset of its data.
+struct Hdr {
+  uint32_t cnt[5], w[5], data[5];
+  int err;
+};
+
+__global__ __launch_bounds__(kCpBlock) void cprime_kernel(
+    const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
+    int max_rows, uint32_t *__restrict__ parent, uint32_t *__restrict__ col,
+    uint32_t *__restrict__ val, uint32_t *__restrict__ depth, int32_t *__restrict__ status,
+    uint32_t *__restrict__ anc0, uint32_t *__restrict__ dist0, uint32_t *__restrict__ anc1,
+    uint32_t *__restrict__ dist1, uint32_t *__restrict__ nxt) {
+  extern __shared__ uint32_t sm[];              // tuple starts, then nonempty tuples before each
+  __shared__ Hdr h;
+  __shared__ uint32_t wsum[kCpWaves];
+  __shared__ int errs;
+  uint32_t *st = sm, *nes = sm + (max_rows + 1);
+  const int64_t *node_off = offs + (n_batches + 1);
+  for (int64_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
+    const uint8_t *blob = blobs + offs[b];
+    const uint64_t size = (uint64_t)(offs[b + 1] - offs[b]);
+    const int64_t no = node_off[b];
+    const uint32_t n_decl = (uint32_t)(node_off[b + 1] - no);   // nodes node_off gives the batch
+    // headers, read by one thread; every later read stays inside the arrays
+    if (threadIdx.x == 0) {
+      int err = 0;
+      uint64_t pos = 0;
+      for (int a = 0; a < 5 && !err; ++a) {
+        if (size < pos + 5) {
+          err = TOC_CPRIME_LAYOUT;
+          break;
+        }
+        const uint32_t cnt = rd(blob + pos, 0, 4), w = blob[pos + 4];
+        if (w < 1 || w > 4 || (a == 1 && w != 4) || (size - pos - 5) / w < cnt) {
+          err = TOC_CPRIME_LAYOUT;
+          break;
+        }
+        h.cnt[a] = cnt;
+        h.w[a] = w;
+        h.data[a] = (uint32_t)(pos + 5);
+        pos += 5 + (uint64_t)cnt * w;
+      }
+      if (!err && (pos != size || h.cnt[2] != h.cnt[0] || h.cnt[4] < 1)) err = TOC_CPRIME_LAYOUT;
+      if (!err && h.cnt[4] - 1 > (uint32_t)max_rows) err = TOC_CPRIME_ROWS;
+      h.err = err;
+      errs = 0;
+    }
+    __syncthreads();
+    if (h.err) {
+      if (threadIdx.x == 0) status[b] = h.err;
+      __syncthreads();
+      continue;
+    }
+    const uint32_t nI = h.cnt[0], U = h.cnt[1], nD = h.cnt[3], nR = h.cnt[4] - 1;
+    const uint8_t *p_col = blob + h.data[0], *p_uni = blob + h.data[1], *p_vix = blob + h.data[2];
+    const uint8_t *p_d = blob + h.data[3], *p_st = blob + h.data[4];
+    const uint32_t w_col = h.w[0], w_vix = h.w[2], w_d = h.w[3], w_st = h.w[4];
+    // tuple starts, checked, and the number of nonempty tuples before each tuple:
+    // the entry at position p of tuple i matches against nI + 1 + p - nes[i] nodes
+    for (uint32_t r = threadIdx.x; r <= nR; r += kCpBlock) st[r] = rd(p_st, r, w_st);
+    __syncthreads();
+    bool bad = threadIdx.x == 0 && (st[0] != 0 || st[nR] != nD);
+    uint32_t carry = 0;
+    for (uint32_t r0 = 0; r0 < nR; r0 += kCpBlock) {
+      const uint32_t r = r0 + threadIdx.x;
+      const bool in = r < nR;
+      const uint32_t s0 = in ? st[r] : 0u, s1 = in ? st[r + 1] : 0u;
+      bad |= in && s1 < s0;
+      uint32_t tot;
+      const uint32_t ex = block_excl_scan(in && s1 > s0 ? 1u : 0u, wsum, tot);
+      if (in) nes[r] = carry + ex;
+      carry += tot;
+    }
+    if (__syncthreads_or(bad)) {
+      if (threadIdx.x == 0) status[b] = TOC_CPRIME_STARTS;
+      __syncthreads();
+      continue;
+    }
+    if ((uint64_t)1 + nI + (nD - carry) != (uint64_t)n_decl) {
+      if (threadIdx.x == 0) status[b] = TOC_CPRIME_NODES;
+      __syncthreads();
+      continue;
+    }
+    const uint32_t n_nodes = n_decl;
+    // the root and the first layer (nodes 1..nI are I in order); pointer-jumping
+    // state: a node's nearest first-layer ancestor (itself here) and its distance
+    for (uint32_t c = threadIdx.x; c <= nI; c += kCpBlock) {
+      const int64_t g = no + c;
+      if (c == 0) {
+        parent[g] = kNone;
+        col[g] = kNone;
+        val[g] = 0u;
+        depth[g] = 0u;
+      } else {
+        const uint32_t q = rd(p_vix, c - 1, w_vix);
+        if (q >= U) atomicOr(&errs, 1 << TOC_CPRIME_VALUE_INDEX);
+        parent[g] = 0u;
+        col[g] = rd(p_col, c - 1, w_col);
+        val[g] = q < U ? rd(p_uni, q, 4) : 0u;
+        depth[g] = 1u;
+      }
+      anc0[g] = anc1[g] = c;
+      dist0[g] = dist1[g] = 0u;
+    }
+    // the entries of D: entry p of tuple i matches one of the nI + 1 + p - nes[i]
+    // nodes existing at that point; unless it ends its tuple it makes that node,
+    // child of its code, keyed by the first pair of the next entry's code
+    for (uint32_t p = threadIdx.x; p < nD; p += kCpBlock) {
+      uint32_t lo = 0, hi = nR;                 // last tuple starting at or before p
+      while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) / 2;
+        if (st[mid] <= p) lo = mid;
+        else hi = mid;
+      }
+      const uint32_t i = lo, q = nI + 1u + p - nes[i];
+      const uint32_t code = rd(p_d, p, w_d);
+      if (code == 0u || code >= q) {
+        atomicOr(&errs, 1 << TOC_CPRIME_CODE);
+      } else if (p + 1 < st[i + 1]) {
+        const int64_t g = no + q;
+        parent[g] = code;
+        anc0[g] = code;
+        dist0[g] = 1u;
+        nxt[g] = rd(p_d, p + 1, w_d);
+      }
+    }
+    __syncthreads();
+    if (errs) {
+      if (threadIdx.x == 0) status[b] = (errs & (1 << TOC_CPRIME_VALUE_INDEX)) ? TOC_CPRIME_VALUE_INDEX
+                                                                              : TOC_CPRIME_CODE;
+      __syncthreads();
+      continue;
+    }
+    // pointer jumping over the new nodes: every node's parent has a smaller index,
+    // so each round halves the distance still to go to the first layer
+    uint32_t *ax = anc0, *dx = dist0, *ay = anc1, *dy = dist1;
+    for (int round = 0; round < kCpMaxRounds; ++round) {
+      bool changed = false;
+      for (uint32_t c = nI + 1 + threadIdx.x; c < n_nodes; c += kCpBlock) {
+        const int64_t g = no + c;
+        const uint32_t a = ax[g], d = dx[g];
+        if (a > nI) {
+          ay[g] = ax[no + a];
+          dy[g] = d + dx[no + a];
+          changed = true;
+        } else {
+          ay[g] = a;
+          dy[g] = d;
+        }
+      }
+      __syncthreads();                          // this round's writes, seen by the next
+      const bool any = __syncthreads_or(changed);
+      uint32_t *t = ax;
+      ax = ay;
+      ay = t;
+      t = dx;
+      dx = dy;
+      dy = t;
+      if (!any) break;
+    }
+    // depth = distance to the first layer + 1; key = first pair of the next
+    // entry's code, the key of its first-layer ancestor
+    for (uint32_t c = nI + 1 + threadIdx.x; c < n_nodes; c += kCpBlock) {
+      const int64_t g = no + c;
+      depth[g] = dx[g] + 1u;
+      const uint32_t f = ax[no + nxt[g]];
+      col[g] = col[no + f];
+      val[g] = val[no + f];
+    }
+    if (threadIdx.x == 0) status[b] = 0;
+    __syncthreads();
+  }
+}
+
+inline int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+int64_t ws_nodes_offset(int64_t n_batches) { return align256(16 * (n_batches + 1)); }
+
+}  // namespace
+
+using namespace toc;
+
+extern "C" {
+
+toc_status toc_cprime_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *bytes) {
+  clear_error();
+  if (!bytes || n_batches < 0 || n_nodes < 0) return fail(TOC_EINVAL, "bad argument");
+  *bytes = (size_t)(ws_nodes_offset(n_batches) + 5 * align256(4 * n_nodes));
+  return TOC_OK;
+}
+
+toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                            int64_t n_batches, int32_t max_rows, uint32_t *parent, uint32_t *col,
+                            float *val, uint32_t *depth, int32_t *status, void *ws,
+                            size_t ws_bytes, void *stream) {
+  clear_error();
+  if (n_batches < 0) return fail(TOC_EINVAL, "n_batches < 0");
+  if (n_batches == 0) return TOC_OK;
+  if (!blob_off || !node_off || !status || !ws) return fail(TOC_EINVAL, "NULL argument");
+  if (max_rows < 0 || max_rows > kCpMaxRows)
+    return fail(TOC_EUNSUPPORTED, "max_rows %d outside 0..%d", max_rows, kCpMaxRows);
+  if (blob_off[0] < 0 || node_off[0] < 0) return fail(TOC_EINVAL, "negative offset");
+  for (int64_t b = 0; b < n_batches; ++b) {
+    if (blob_off[b + 1] < blob_off[b] || blob_off[b + 1] - blob_off[b] > (int64_t)UINT32_MAX)
+      return fail(TOC_EINVAL, "blob_off not non-decreasing or a blob of 4 GiB or more at %lld",
+                  (long long)b);
+    if (node_off[b + 1] <= node_off[b] || node_off[b + 1] - node_off[b] > (int64_t)INT32_MAX)
+      return fail(TOC_EINVAL, "node_off[%lld] does not give 1..2^31-1 nodes", (long long)b);
+  }
+  const int64_t n_nodes = node_off[n_batches];
+  if (!parent || !col || !val || !depth) return fail(TOC_EINVAL, "NULL output");
+  if (blob_off[n_batches] > 0 && !blobs) return fail(TOC_EINVAL, "blobs is NULL");
+  size_t need = 0;
+  toc_cprime_workspace_size(n_batches, n_nodes, &need);
+  if (ws_bytes < need) return fail(TOC_ESIZE, "workspace of %zu bytes below the %zu needed", ws_bytes, need);
+  hipStream_t s = (hipStream_t)stream;
+  int64_t *offs = (int64_t *)ws;
+  if (hipMemcpyAsync(offs, blob_off, 8 * (n_batches + 1), hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + n_batches + 1, node_off, 8 * (n_batches + 1), hipMemcpyHostToDevice, s) !=
+          hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(TOC_EDEVICE, "copy of the offsets failed");
+  uint8_t *base = (uint8_t *)ws + ws_nodes_offset(n_batches);
+  const int64_t arr = align256(4 * n_nodes);
+  uint32_t *a0 = (uint32_t *)base, *d0 = (uint32_t *)(base + arr), *a1 = (uint32_t *)(base + 2 * arr);
+  uint32_t *d1 = (uint32_t *)(base + 3 * arr), *nx = (uint32_t *)(base + 4 * arr);
+  const size_t lds = 8 * ((size_t)max_rows + 1);
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute((const void *)cprime_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)lds) != hipSuccess)
+    return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
+  const unsigned g = (unsigned)std::min<int64_t>(n_batches, 1 << 20);
+  hipLaunchKernelGGL(cprime_kernel, dim3(g), dim3(kCpBlock), lds, s, (const uint8_t *)blobs, offs,
+                     n_batches, (int)max_rows, parent, col, (uint32_t *)val, depth, status, a0, d0,
+                     a1, d1, nx);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOC_EDEVICE, "cprime_kernel: %s", hipGetErrorString(e));
+  return TOC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,133 @@
+"""CPU tests of the physical encoding entry points (section 3.2): the library's
+bytes equal the oracle's, its header reader agrees with the oracle's counts and
+rejects malformed blobs.  No GPU needed."""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_1702_06943_amd as T
+from workloads import config_batches, tiny_batch, Batches
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+PHYS = json.load(open(os.path.join(HERE, "golden", "physical_worked_example.json")))
+GOLD = json.load(open(os.path.join(HERE, "golden", "worked_example.json")))
+
+
+def _encs(B):
+    return T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+
+
+def _oracle_ID(B, b):
+    n, rp, c, v = B.batch(b)
+    I, D, N = O.encode(O.canonicalize(n, B.n_cols, rp, c, v))
+    return I, D, N
+
+
+def test_worked_example_bytes():
+    rows = GOLD["rows_from_table2"]["rows"]
+    rp = np.cumsum([0] + [len(r) for r in rows])
+    col = np.array([c for r in rows for c, _ in r], np.int32)
+    val = np.array([v for r in rows for _, v in r], np.float32)
+    e = T.toc_encode(len(rows), GOLD["n_cols"], rp, col, val)
+    want = bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"]))
+    assert bytes(T.toc_enc_pack(e)) == want
+    info = T.toc_phys_info_get(np.frombuffer(want, np.uint8))
+    assert info == dict(n_rows=4, n_first=5, n_codes=9, n_unique=4, n_nodes=11)
+
+
+TINY = [dict(n_rows=0, density=0.5, n_values=2),
+        dict(n_rows=5, density=0.0, n_values=2),
+        dict(n_rows=1, density=1.0, n_values=1),
+        dict(n_rows=40, density=0.3, n_values=3, prefix_copy=0.6),
+        dict(n_rows=9, density=0.05, n_values=2)]
+
+
+@pytest.mark.parametrize("case", range(len(TINY)))
+@pytest.mark.parametrize("n_cols", [3, 300, 70000])
+def test_pack_equals_oracle_tiny(case, n_cols):
+    spec = TINY[case]
+    if n_cols == 70000 and spec["n_rows"] * n_cols * spec["density"] > 2e5:
+        pytest.skip("too large for a tiny case")
+    rp, c, v = tiny_batch(77 + case, n_cols=n_cols, **spec)
+    B = Batches(n_cols, [spec["n_rows"]], rp, c, v)
+    e = _encs(B)[0]
+    I, D, N = _oracle_ID(B, 0)
+    blob = T.toc_enc_pack(e)
+    assert bytes(blob) == O.pack_physical(I, D)
+    assert len(blob) == T.toc_enc_info_get(e)["phys_bytes"] == O.physical_bytes(I, D)
+    info = T.toc_phys_info_get(blob)
+    assert info["n_nodes"] == N and info["n_first"] == len(I)
+    assert info["n_codes"] == sum(len(d) for d in D) and info["n_rows"] == len(D)
+
+
+@pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c5"])
+def test_pack_equals_oracle_configs(cfg):
+    B = config_batches(cfg, 2, 1)
+    e = _encs(B)[0]
+    I, D, N = _oracle_ID(B, 0)
+    blob = T.toc_enc_pack(e)
+    assert bytes(blob) == O.pack_physical(I, D)
+    assert T.toc_phys_info_get(blob)["n_nodes"] == N
+
+
+def _example():
+    return bytearray(bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"])))
+
+
+def _mut(fn):
+    b = _example()
+    fn(b)
+    return b
+
+
+BAD = {
+    "truncated": lambda: _example()[:-1],
+    "trailing": lambda: _example() + b"\x00",
+    "width 5": lambda: _mut(lambda b: b.__setitem__(4, 5)),
+    "width 0": lambda: _mut(lambda b: b.__setitem__(4, 0)),
+    "value width 2": lambda: _mut(lambda b: b.__setitem__(14, 2)),
+    "count too large": lambda: _mut(lambda b: b.__setitem__(0, 200)),
+    "starts not monotone": lambda: _mut(lambda b: (b.__setitem__(-3, 7), b.__setitem__(-2, 6))),
+    "starts end early": lambda: _mut(lambda b: b.__setitem__(-1, 8)),
+    "starts begin late": lambda: _mut(lambda b: b.__setitem__(-5, 1)),
+    "empty": lambda: bytearray(),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BAD))
+def test_phys_info_rejects(name):
+    blob = np.frombuffer(bytes(BAD[name]()), np.uint8) if len(BAD[name]()) else np.zeros(0, np.uint8)
+    with pytest.raises(T.TocError) as ei:
+        T.toc_phys_info_get(blob)
+    assert ei.value.status == T.TOC_EINVAL
+    # the oracle's reader refuses them too
+    with pytest.raises(O.TocInputError):
+        O.unpack_physical(bytes(BAD[name]()))
+
+
+def test_pack_errors():
+    e = T.toc_encode(1, 2, np.array([0, 1]), np.array([1], np.int32), np.array([2.0], np.float32))
+    assert T.lib().toc_enc_pack(e.handle, np.zeros(4, np.uint8).ctypes.data, 4) == T.TOC_ESIZE
+    assert T.lib().toc_enc_pack_size(None, None) == T.TOC_EINVAL
+    assert T.lib().toc_cprime_build(None, None, None, 0, 0, None, None, None, None, None, None,
+                                    0, None) == 0
+    off = np.array([0, 5], np.int64)
+    assert T.lib().toc_cprime_build(None, off.ctypes.data, off.ctypes.data, 1, 0, None, None,
+                                    None, None, None, None, 0, None) == T.TOC_EINVAL
+    bad = np.array([5, 0], np.int64)
+    ws = np.zeros(1 << 12, np.uint8)
+    st = np.zeros(1, np.int32)
+    args = [ws.ctypes.data, bad.ctypes.data, off.ctypes.data, 1, 0, ws.ctypes.data, ws.ctypes.data,
+            ws.ctypes.data, ws.ctypes.data, st.ctypes.data, ws.ctypes.data, ws.size, None]
+    assert T.lib().toc_cprime_build(*args) == T.TOC_EINVAL          # blob_off decreasing
+    args[1] = off.ctypes.data
+    args[4] = 20000
+    assert T.lib().toc_cprime_build(*args) == T.TOC_EUNSUPPORTED    # max_rows beyond the limit
+    args[4] = 0
+    args[11] = 16
+    assert T.lib().toc_cprime_build(*args) == T.TOC_ESIZE           # workspace too small
+    assert T.toc_cprime_workspace_size(1, 5) > 0
