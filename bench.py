@@ -196,6 +196,60 @@ def time_elementwise(w, stream, reps=3):
     return res
 
 
+def pack_sample(w, n):
+    """Physical encodings (section 3.2) of n batches spread evenly over the workload,
+    packed on the host from the encodings before they are dropped."""
+    import paper_1702_06943_amd as T
+    if n <= 0:
+        return None
+    idx = np.linspace(0, len(w.encs) - 1, min(n, len(w.encs))).astype(np.int64)
+    t0 = time.perf_counter()
+    blobs = [T.toc_enc_pack(w.encs[i]) for i in idx]
+    return {"blobs": blobs, "pack_s": time.perf_counter() - t0}
+
+
+def time_cprime(sample, stream, reps=3):
+    """toc_cprime_build over the sampled batches' physical bytes, resident in HBM.
+    Algorithmic bytes: the blobs read once plus 16 bytes written per node."""
+    import torch
+    import paper_1702_06943_amd as T
+    blobs = sample["blobs"]
+    infos = [T.toc_phys_info_get(b) for b in blobs]
+    blob_off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
+    node_off = np.concatenate([[0], np.cumsum([i["n_nodes"] for i in infos])]).astype(np.int64)
+    n = int(node_off[-1])
+    dev = "cuda:0"
+    d_blobs = torch.from_numpy(np.concatenate(blobs)).to(dev)
+    outs = [torch.empty(n, dtype=torch.int32, device=dev) for _ in range(4)]
+    status = torch.empty(len(blobs), dtype=torch.int32, device=dev)
+    ws = torch.empty(T.toc_cprime_workspace_size(len(blobs), n), dtype=torch.uint8, device=dev)
+    max_rows = max(i["n_rows"] for i in infos)
+
+    def run():
+        T.toc_cprime_build(d_blobs, blob_off, node_off, max_rows, *outs, status, ws)
+
+    run()
+    torch.cuda.synchronize()
+    ok = bool((status == 0).all().item())
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+    for i in range(reps):
+        ev[2 * i].record(stream)
+        run()
+        ev[2 * i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.mean([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    b = float(blob_off[-1] + 16 * n)
+    res = {"batches": len(blobs), "nodes": n, "blob_bytes": int(blob_off[-1]), "ms": round(ms, 4),
+           "nodes_per_s": n / (ms / 1e3), "GB/s": b / ms / 1e6,
+           "hbm_frac": b / (ms / 1e3) / HBM_PEAK, "status_ok": ok,
+           "host_pack_s": round(sample["pack_s"], 3)}
+    log(f"C' build from physical bytes: {len(blobs)} batches, {n} nodes, {ms:.3f} ms "
+        f"({res['hbm_frac']:.1%} of HBM peak on algorithmic bytes), status ok: {ok}")
+    del d_blobs, outs, status, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -231,7 +285,11 @@ def main():
                     help="CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip timing the element-wise operations after the step")
+                    help="skip timing the element-wise operations and the C' build after "
+                         "the step")
+    ap.add_argument("--cprime-batches", type=int, default=4000,
+                    help="batches whose physical encoding is turned into C' on the GPU "
+                         "after the step (0 = skip)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device three times "
                          "(reference dispatches for HBM byte counters)")
@@ -264,6 +322,7 @@ def main():
 
     import torch
     upload_workload(w, k)
+    sample = None if args.no_extras else pack_sample(w, args.cprime_batches)
     w.encs = None
 
     stream = torch.cuda.current_stream()
@@ -300,6 +359,7 @@ def main():
 
     info = w.info
     extras = None if args.no_extras else time_elementwise(w, stream)
+    cprime = time_cprime(sample, stream) if sample else None
     nnz = info["nnz"]
     canon = info["canon_bytes"]
     n_rows, m = info["n_rows"], info["n_cols"]
@@ -364,6 +424,7 @@ def main():
         "ops": ops,
         "roofline": roof,
         "elementwise": extras,
+        "cprime_build": cprime,
         "cpu_baseline": cpu,
         "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
                  "cpu": host_cpu()},
