@@ -33,6 +33,12 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
                  I and D under the byte-layout reading, the width rule of §3.2 at
                  every byte boundary (its "max 4 needs 1 byte" example included),
                  round trips, size equal to physical_bytes, malformed inputs
+  mgd_loss, mgd_dloss, mgd_step
+                 pinned: central finite differences of the mean loss (the step is
+                 h - lr * its gradient) for all three losses on random batches,
+                 the paper's linear-regression gradient on the worked example by
+                 hand, closed forms (lr = 0, one entry, logistic at r = 0, hinge
+                 beyond the margin), an empty batch
 """
 
 from .toc_oracle import (  # noqa: F401
@@ -54,6 +60,12 @@ from .toc_oracle import (  # noqa: F401
     physical_bytes,
     pack_physical,
     unpack_physical,
+    MGD_LINEAR,
+    MGD_LOGISTIC,
+    MGD_HINGE,
+    mgd_loss,
+    mgd_dloss,
+    mgd_step,
     f32_bits,
     bits_f32,
 )

@@ -471,3 +471,55 @@ def unpack_physical(blob):
     I = [(c, uniq[q]) for c, q in zip(cols, vidx)]
     D = [codes[starts[r]:starts[r + 1]] for r in range(len(starts) - 1)]
     return I, D
+
+
+# ---------------------------------------------------------------------------
+# Mini-batch gradient descent on a TOC batch, §2.1: one step moves the model h by
+# the learning rate times the mean, over the batch's tuples, of the loss gradient
+# (the MGD update equation).  For the linear models of Table 1 the loss of a tuple
+# (x, y) depends on h through r = x^T h only, so the batch gradient is
+# A^T g / |B| with g_i = d loss / d r at r_i = (A h)_i: the paper's linear
+# regression example, ((A h - Y)^T A)^T, is the case g = r - y.  Losses (Table 1's
+# caption names them; the label convention is a reading): squared 1/2 (y - r)^2;
+# logistic log(1 + exp(-y r)) with y in {-1, +1}; hinge max(0, 1 - y r) with
+# y in {-1, +1}, whose subgradient at y r = 1 is taken as 0.
+# ---------------------------------------------------------------------------
+MGD_LINEAR, MGD_LOGISTIC, MGD_HINGE = 0, 1, 2
+
+
+def mgd_loss(loss, r, y):
+    """Per-tuple loss values (fp64 arrays)."""
+    r, y = np.asarray(r, np.float64), np.asarray(y, np.float64)
+    if loss == MGD_LINEAR:
+        return 0.5 * (y - r) ** 2
+    if loss == MGD_LOGISTIC:
+        return np.log1p(np.exp(-y * r))
+    if loss == MGD_HINGE:
+        return np.maximum(0.0, 1.0 - y * r)
+    raise TocInputError("unknown loss")
+
+
+def mgd_dloss(loss, r, y):
+    """d loss / d r per tuple (fp64 arrays)."""
+    r, y = np.asarray(r, np.float64), np.asarray(y, np.float64)
+    if loss == MGD_LINEAR:
+        return r - y
+    if loss == MGD_LOGISTIC:
+        return -y / (1.0 + np.exp(y * r))
+    if loss == MGD_HINGE:
+        return np.where(y * r < 1.0, -y, 0.0)
+    raise TocInputError("unknown loss")
+
+
+def mgd_step(rows, n_cols, h, y, loss, lr):
+    """One MGD step on a decoded batch: returns the new model (fp64) and the
+    tolerance scale |A|^T (|g| + |A||h|) of each component (sums of absolute
+    terms).  A batch without tuples leaves h unchanged."""
+    h = np.asarray(h, np.float64)
+    if len(rows) == 0:
+        return h.copy(), np.zeros_like(h)
+    r, s_r = dense_right(rows, n_cols, h[:, None])
+    g = mgd_dloss(loss, r[:, 0], y)
+    grad, _ = dense_left(rows, n_cols, g[:, None])
+    scale, _ = dense_left(rows, n_cols, (np.abs(g) + s_r[:, 0])[:, None])
+    return h - lr / len(rows) * grad[:, 0], scale[:, 0]

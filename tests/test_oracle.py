@@ -440,3 +440,59 @@ def _bad_starts():
 def test_physical_rejects(make):
     with pytest.raises(O.TocInputError):
         O.unpack_physical(bytes(make()))
+
+
+# --- mini-batch gradient descent step (section 2.1) --------------------------------
+def _mean_loss(A, h, y, loss):
+    return float(np.mean(O.mgd_loss(loss, A @ h, y)))
+
+
+@pytest.mark.parametrize("loss", [O.MGD_LINEAR, O.MGD_LOGISTIC, O.MGD_HINGE])
+@pytest.mark.parametrize("seed", range(4))
+def test_mgd_step_is_gradient_step(loss, seed):
+    """h - h_new = lr * grad of the mean loss, the gradient taken by central finite
+    differences of the loss definitions on the densified batch."""
+    spec = dict(n_rows=12, n_cols=7, density=0.6, n_values=3)
+    rp, c, v = tiny_batch(4000 + seed, **spec)
+    rows = O.canonicalize(12, 7, rp, c, v)
+    A = _dense(rows, 7)
+    rng = np.random.default_rng(seed)
+    for _ in range(100):                     # keep every margin away from the hinge's kink
+        h = rng.standard_normal(7) * 0.3
+        y = rng.choice([-1.0, 1.0], size=12)
+        if np.all(np.abs(y * (A @ h) - 1.0) > 1e-3):
+            break
+    lr = 0.37
+    h_new, _ = O.mgd_step(rows, 7, h, y, loss, lr)
+    eps = 1e-6
+    fd = np.array([(_mean_loss(A, h + eps * e, y, loss) - _mean_loss(A, h - eps * e, y, loss))
+                   / (2 * eps) for e in np.eye(7)])
+    assert np.allclose((h - h_new) / lr, fd, rtol=1e-6, atol=1e-8)
+
+
+def test_mgd_linear_worked_example(example):
+    """Section 2.1's linear-regression gradient ((A h - Y)^T A)^T on the example
+    table, summed by hand: h = 1, Y = (1, 2, 3, 4) give A h - Y = (6.5, 4.1, 2.5,
+    -0.9) and the gradient (10.67, 22.15, 39.3, 12.6); lr = 0.1 over 4 tuples."""
+    rows = example[0]
+    h_new, _ = O.mgd_step(rows, 4, np.ones(4), np.array([1.0, 2, 3, 4]), O.MGD_LINEAR, 0.1)
+    assert np.allclose(h_new, 1 - 0.025 * np.array([10.67, 22.15, 39.3, 12.6]), atol=2e-6)
+
+
+def test_mgd_closed_forms():
+    one = [[(2, O.f32_bits(1.5))]]
+    h = np.array([0.0, 0.0, 0.25])
+    # linear, one entry: h_j - lr (a h_j - y) a
+    h1, _ = O.mgd_step(one, 3, h, np.array([2.0]), O.MGD_LINEAR, 0.5)
+    assert h1.tolist() == [0.0, 0.0, 0.25 - 0.5 * (1.5 * 0.25 - 2.0) * 1.5]
+    # logistic at r = 0: g = -y / 2
+    h2, _ = O.mgd_step(one, 3, np.zeros(3), np.array([1.0]), O.MGD_LOGISTIC, 1.0)
+    assert h2.tolist() == [0.0, 0.0, 0.75]
+    # hinge beyond the margin: no change; inside: h + lr y a
+    h3, _ = O.mgd_step(one, 3, np.array([0.0, 0.0, 1.0]), np.array([1.0]), O.MGD_HINGE, 1.0)
+    assert h3.tolist() == [0.0, 0.0, 1.0]
+    h4, _ = O.mgd_step(one, 3, np.zeros(3), np.array([-1.0]), O.MGD_HINGE, 2.0)
+    assert h4.tolist() == [0.0, 0.0, -3.0]
+    # lr = 0 and an empty batch change nothing
+    assert O.mgd_step(one, 3, h, np.array([5.0]), O.MGD_LINEAR, 0.0)[0].tolist() == h.tolist()
+    assert O.mgd_step([], 3, h, np.array([]), O.MGD_LINEAR, 1.0)[0].tolist() == h.tolist()
