@@ -346,6 +346,29 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
                             float *val, uint32_t *depth, int32_t *status, void *ws,
                             size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Mini-batch gradient descent (section 2.1): h <- h - lr / |B| * sum over the
+ * tuples (x, y) of batch B of d loss(h, x, y) / d h, for the linear models of
+ * Table 1, whose loss depends on h through r = x^T h: the batch gradient is
+ * A^T g with g_i = d loss / d r at r_i = (A h)_i, so a step is the right
+ * product (Theorem 1), g, the left product (Theorem 2) and the update.
+ * ------------------------------------------------------------------------- */
+#define TOC_MGD_LINEAR 0     /* 1/2 (y - r)^2, linear regression                    */
+#define TOC_MGD_LOGISTIC 1   /* log(1 + exp(-y r)), y in {-1, +1}                   */
+#define TOC_MGD_HINGE 2      /* max(0, 1 - y r), y in {-1, +1}; subgradient 0 at 1  */
+
+/* Runs the steps of batches b0 .. b0+n_batches-1 of an uploaded image in order,
+ * in one launch of one workgroup (each step reads the model the previous step
+ * wrote; a batch without tuples changes nothing).
+ *   y  device float per row of the image (all batches' rows, stacked)
+ *   h  device float[n_cols], the model, updated in place
+ * Needs 4 (max rows + max stored codes of a batch) bytes of LDS, at most 160 KiB
+ * (TOC_EUNSUPPORTED beyond).  Asynchronous on stream.  TOC_EINVAL for a batch
+ * range outside the image, an unknown loss, a learning rate that is not finite
+ * or an image in host memory.                                                  */
+toc_status toc_mgd_epoch(const toc_dev *dev, int64_t b0, int64_t n_batches, int32_t loss,
+                         float lr, const float *y, float *h, void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *toc_last_error(void);
 

@@ -521,5 +521,5 @@ def mgd_step(rows, n_cols, h, y, loss, lr):
     r, s_r = dense_right(rows, n_cols, h[:, None])
     g = mgd_dloss(loss, r[:, 0], y)
     grad, _ = dense_left(rows, n_cols, g[:, None])
-    scale, _ = dense_left(rows, n_cols, (np.abs(g) + s_r[:, 0])[:, None])
+    _, scale = dense_left(rows, n_cols, (np.abs(g) + s_r[:, 0])[:, None])
     return h - lr / len(rows) * grad[:, 0], scale[:, 0]

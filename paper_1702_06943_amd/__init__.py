@@ -1,7 +1,8 @@
 """MI355X-native tuple-oriented compression (TOC): encode on the host, run A.W,
 G^T.A, decode, sparse-safe element-wise ops and dense A .+ c on the compressed
 mini-batches with hand-written gfx950 kernels; pack batches into the paper's
-physical encoding and build the decoding tree C' from it on the GPU.
+physical encoding and build the decoding tree C' from it on the GPU; run
+mini-batch gradient descent steps of linear models on the compressed batches.
 
 The functions are those of include/toc.h, called through ctypes; see binding.py.
 """
@@ -18,4 +19,5 @@ from .binding import (  # noqa: F401
     TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
     TOC_CPRIME_NODES, TOC_CPRIME_ROWS,
     toc_enc_pack, toc_phys_info_get, toc_cprime_workspace_size, toc_cprime_build,
+    TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE, toc_mgd_epoch,
 )

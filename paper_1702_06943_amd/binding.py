@@ -22,6 +22,7 @@ TOC_UPLOAD_KEEP_DEAD = 1
 TOC_UPLOAD_HOST = 2
 TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE = 0, 1, 2
 TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
+TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE = 0, 1, 2
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
  TOC_CPRIME_NODES, TOC_CPRIME_ROWS) = range(1, 7)
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
@@ -110,6 +111,7 @@ def lib():
         "toc_phys_info_get": [P, SZ, P],
         "toc_cprime_workspace_size": [I64, I64, P],
         "toc_cprime_build": [P, P, P, I64, I32, P, P, P, P, P, P, SZ, P],
+        "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -361,3 +363,18 @@ def toc_cprime_build(blobs, blob_off, node_off, max_rows, parent, col, val, dept
                                   _ptr(parent), _ptr(col), _ptr(val), _ptr(depth), _ptr(status),
                                   _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
                                   _stream(stream)))
+
+
+def toc_mgd_epoch(dev, y, h, loss, lr, b0=0, n_batches=None, stream=None):
+    """MGD steps over batches b0 .. b0+n_batches-1 (default: all from b0).  y: device
+    float32 tensor of one label per row of the image; h: device float32 tensor of
+    n_cols entries, updated in place."""
+    info = toc_dev_info_get(dev)
+    if n_batches is None:
+        n_batches = info["n_batches"] - b0
+    if y.numel() < info["n_rows"] or y.element_size() != 4:
+        raise TocError(TOC_EINVAL, "y must hold one float32 per row")
+    if h.numel() != info["n_cols"] or h.element_size() != 4:
+        raise TocError(TOC_EINVAL, "h must hold n_cols float32")
+    _check(lib().toc_mgd_epoch(dev.handle, int(b0), int(n_batches), int(loss), float(lr),
+                               _ptr(y), _ptr(h), _stream(stream)))

@@ -1,0 +1,167 @@
+// Mini-batch gradient descent on the uploaded image (section 2.1's update rule)
+// for the linear models of Table 1: per batch, the right product r = A.h
+// (Theorem 1, Algorithm 4), the loss gradient g_i at r_i, the left product g^T.A
+// (Theorem 2, Algorithm 5) and the update of h, all in one workgroup with H in
+// LDS.  The batches are consecutive steps of one launch: each step reads the
+// model the previous one wrote.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "toc_internal.h"
+
+namespace {
+
+constexpr int kMgBlock = 1024;
+constexpr int kMgLanes = 16;                   // lanes per tuple in the right product
+constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of occ_row
+constexpr size_t kMgLdsMax = 160 * 1024;
+
+struct MgImg {
+  const toc_batch *batches;
+  const uint32_t *level;
+  const toc_key *key;
+  const toc_link *link;
+  const uint32_t *span, *dcodes, *occ_off, *occ_row, *tlist, *cols, *tchild, *pval;
+};
+
+// d loss / d r of one tuple: squared 1/2 (y - r)^2, logistic log(1 + exp(-y r)),
+// hinge max(0, 1 - y r) (subgradient 0 at the kink)
+__device__ inline float dloss(int loss, float r, float y) {
+  if (loss == TOC_MGD_LINEAR) return r - y;
+  if (loss == TOC_MGD_LOGISTIC) return -y / (1.0f + expf(y * r));
+  return y * r < 1.0f ? -y : 0.0f;
+}
+
+__global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int64_t nb, int32_t m,
+                                                       int32_t max_rows, int loss, float lr,
+                                                       const float *__restrict__ y,
+                                                       float *__restrict__ h) {
+  extern __shared__ float sm[];
+  float *Gs = sm;                  // per tuple: d loss / d r
+  float *H = sm + max_rows;        // per code (right), then per left position (left)
+  for (int64_t b = b0; b < b0 + nb; ++b) {
+    const toc_batch bt = im.batches[b];
+    const int nr = bt.n_rows;
+    if (nr == 0) continue;          // no tuple: the step leaves h unchanged
+    const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+    const uint32_t *lvl = im.level + bt.lvl_base;
+    const toc_key *key = im.key + bt.code_base;
+    const toc_link *link = im.link + bt.code_base;
+    // right: H[c] = H[parent] + val * h[col], level by level
+    for (int d = 1; d <= bt.n_levels; ++d) {
+      const uint32_t a = lvl[d - 1], e = lvl[d];
+      for (uint32_t c = a + threadIdx.x; c < e; c += kMgBlock) {
+        const toc_key k = key[c];
+        const float base = d > 1 ? H[link[c].parent] : 0.0f;
+        H[c] = fmaf(k.val, h[k.col], base);
+      }
+      __syncthreads();
+    }
+    // r_i = sum of H over the tuple's codes; then the loss gradient at r_i
+    {
+      const uint32_t *span = im.span + bt.span_base;
+      const uint32_t *dc = im.dcodes + bt.d_base;
+      const int lane = threadIdx.x % kMgLanes, grp = threadIdx.x / kMgLanes;
+      for (int r = grp; r < nr; r += kMgBlock / kMgLanes) {
+        const uint32_t s = span[r], e = span[r + 1];
+        float acc = 0.0f;
+        for (uint32_t j = s + lane; j < e; j += kMgLanes) acc += H[dc[j]];
+#pragma unroll
+        for (int o = kMgLanes / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kMgLanes);
+        if (lane == 0) Gs[r] = dloss(loss, acc, y[bt.row_base + r]);
+      }
+    }
+    __syncthreads();
+    // left, by pulling: H at each left position = the gradients of the tuples
+    // holding its code, then children added into parents, deepest first
+    const uint32_t *oo = im.occ_off + bt.code_base + b;
+    const uint32_t *orow = im.occ_row + bt.d_base;
+    for (uint32_t p = threadIdx.x; p < nc; p += kMgBlock) {
+      float s = 0.0f;
+      const uint32_t o1 = oo[p + 1];
+      for (uint32_t o = oo[p]; o < o1; ++o) s += Gs[orow[o] & ~kMgFirst];
+      H[p] = s;
+    }
+    __syncthreads();
+    const uint32_t *tch = im.tchild + bt.tree_base + b;
+    for (int d = bt.n_levels - 1; d >= 1; --d) {
+      const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+      for (uint32_t c = a + threadIdx.x; c < e; c += kMgBlock) {
+        const uint32_t hr = c < ni ? c : c - n1 + ni;
+        float s = H[c];
+        const uint32_t c1 = tch[hr + 1];
+        for (uint32_t ch = tch[hr]; ch < c1; ++ch) s += H[ch];
+        H[c] = s;
+      }
+      __syncthreads();
+    }
+    // each key column once: its gradient is the sum of val * H over the column's
+    // leaves (a position range) and tree codes (a tree-list range); the step is
+    // h_j -= lr / |B| * gradient_j
+    const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
+    const uint32_t *Loff = cx, *Toff = cx + 2 * (m + 1);
+    const uint32_t *tl = im.tlist + bt.tree_base;
+    const uint32_t *pv = im.pval + bt.code_base;
+    const float step = lr / (float)nr;
+    for (int j = threadIdx.x; j < m; j += kMgBlock) {
+      float s = 0.0f;
+      const uint32_t l1 = Loff[j + 1], t1 = Toff[j + 1];
+      for (uint32_t p = Loff[j]; p < l1; ++p) s = fmaf(__uint_as_float(pv[p]), H[p], s);
+      for (uint32_t t = Toff[j]; t < t1; ++t) {
+        const uint32_t c = tl[t];
+        s = fmaf(__uint_as_float(pv[c]), H[c], s);
+      }
+      h[j] = fmaf(-step, s, h[j]);
+    }
+    __syncthreads();                // the next step's right product reads the new h
+  }
+}
+
+}  // namespace
+
+using namespace toc;
+
+extern "C" {
+
+toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_t loss, float lr,
+                         const float *y, float *h, void *stream) {
+  clear_error();
+  if (!d) return fail(TOC_EINVAL, "dev is NULL");
+  if (d->host) return fail(TOC_EINVAL, "image was uploaded to host memory");
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return fail(TOC_EDEVICE, "hipGetDevice failed");
+  if (cur != d->device) return fail(TOC_EINVAL, "current device %d differs from upload device %d", cur, d->device);
+  const int64_t nb = d->info.n_batches;
+  if (b0 < 0 || n_batches < 0 || b0 > nb || n_batches > nb - b0)
+    return fail(TOC_EINVAL, "batches %lld..%lld outside 0..%lld", (long long)b0,
+                (long long)(b0 + n_batches), (long long)nb);
+  if (loss != TOC_MGD_LINEAR && loss != TOC_MGD_LOGISTIC && loss != TOC_MGD_HINGE)
+    return fail(TOC_EINVAL, "unknown loss %d", loss);
+  if (!std::isfinite(lr)) return fail(TOC_EINVAL, "learning rate not finite");
+  if (n_batches == 0) return TOC_OK;
+  if (!h || (!y && d->info.n_rows > 0)) return fail(TOC_EINVAL, "NULL pointer");
+  const size_t lds = 4 * ((size_t)d->max_rows + (size_t)d->max_codes);
+  if (lds > kMgLdsMax)
+    return fail(TOC_EUNSUPPORTED, "a batch needs %zu bytes of LDS (max %zu)", lds, kMgLdsMax);
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute((const void *)mgd_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)lds) != hipSuccess)
+    return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
+  const uint8_t *base = (const uint8_t *)d->buf;
+  const toc_layout &L = d->layout;
+  const MgImg im{(const toc_batch *)(base + L.batches), (const uint32_t *)(base + L.level),
+                 (const toc_key *)(base + L.key), (const toc_link *)(base + L.link),
+                 (const uint32_t *)(base + L.span), (const uint32_t *)(base + L.dcodes),
+                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.occ_row),
+                 (const uint32_t *)(base + L.tlist), (const uint32_t *)(base + L.cols),
+                 (const uint32_t *)(base + L.tchild), (const uint32_t *)(base + L.pval)};
+  hipLaunchKernelGGL(mgd_kernel, dim3(1), dim3(kMgBlock), lds, (hipStream_t)stream, im, b0,
+                     n_batches, d->info.n_cols, d->max_rows, (int)loss, lr, y, h);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOC_EDEVICE, "mgd_kernel: %s", hipGetErrorString(e));
+  return TOC_OK;
+}
+
+}  // extern "C"

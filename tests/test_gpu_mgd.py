@@ -1,0 +1,126 @@
+"""GPU parity of toc_mgd_epoch (mini-batch gradient descent, section 2.1) with the
+oracle: every step from the same model agrees with the oracle's fp64 step within a
+bound derived from the fp32 arithmetic, and one launch over many batches equals
+the same steps launched one by one, bit for bit."""
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_1702_06943_amd as T
+from workloads import config_batches, tiny_batch, Batches
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+U = 2.0 ** -24
+
+
+def upload(B):
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    buf = torch.empty(T.toc_upload_size(encs), dtype=torch.uint8, device=DEV)
+    return T.toc_upload(encs, buf)
+
+
+def labels(B, loss, seed):
+    rng = np.random.default_rng(seed)
+    n = int(B.n_rows.sum())
+    if loss == T.TOC_MGD_LINEAR:
+        return rng.standard_normal(n).astype(np.float32)
+    return rng.choice(np.array([-1.0, 1.0], np.float32), size=n)
+
+
+def mixed_set():
+    parts = [config_batches("c5", 3, 3)]
+    for i, spec in enumerate([dict(n_rows=0, density=0.5, n_values=2),
+                              dict(n_rows=30, density=0.2, n_values=3, prefix_copy=0.6),
+                              dict(n_rows=4, density=0.0, n_values=2),
+                              dict(n_rows=120, density=0.05, n_values=2, prefix_copy=0.3)]):
+        rp, c, v = tiny_batch(60 + i, n_cols=900, **spec)
+        parts.append(Batches(900, [spec["n_rows"]], rp, c, v))
+    return Batches.concat(parts)
+
+
+def check_step(B, b, h_before, h_after, y, loss, lr):
+    n, rp, c, v = B.batch(b)
+    rows = O.canonicalize(n, B.n_cols, rp, c, v)
+    r0 = int(B.row_off[b])
+    want, scale = O.mgd_step(rows, B.n_cols, h_before.astype(np.float64),
+                             y[r0:r0 + n].astype(np.float64), loss, lr)
+    step = lr / max(n, 1)
+    tol = step * 1e-5 * scale + 4 * U * (np.abs(want) + np.abs(h_before))
+    if loss == T.TOC_MGD_HINGE and n:
+        # a tuple whose margin is within the fp32 error of 1 may take either side
+        A = np.zeros((n, B.n_cols))
+        for i, row in enumerate(rows):
+            for cc, bits in row:
+                A[i, cc] = O.bits_f32(bits)
+        r = A @ h_before.astype(np.float64)
+        s_r = np.abs(A) @ np.abs(h_before.astype(np.float64))
+        amb = np.abs(y[r0:r0 + n] * r - 1.0) <= 1e-5 * s_r + 1e-30
+        tol = tol + step * (np.abs(A[amb]).sum(axis=0))
+    err = np.abs(h_after.astype(np.float64) - want)
+    assert np.all(err <= tol), f"batch {b}: worst err/tol {np.max(err / np.maximum(tol, 1e-300))}"
+
+
+@pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
+@pytest.mark.parametrize("which", ["mixed", "c3", "c2"])
+def test_each_step_against_oracle(loss, which):
+    B = {"mixed": mixed_set, "c3": lambda: config_batches("c3", 4, 3),
+         "c2": lambda: config_batches("c2", 1, 2)}[which]()
+    dev = upload(B)
+    y = labels(B, loss, 7 + loss)
+    yd = torch.from_numpy(y).to(DEV)
+    rng = np.random.default_rng(loss)
+    h = (rng.standard_normal(B.n_cols) * 0.05).astype(np.float32)
+    hd = torch.from_numpy(h).to(DEV)
+    lr = 0.5
+    for b in range(B.n_batches):
+        before = hd.cpu().numpy().copy()
+        T.toc_mgd_epoch(dev, yd, hd, loss, lr, b0=b, n_batches=1)
+        torch.cuda.synchronize()
+        after = hd.cpu().numpy()
+        check_step(B, b, before, after, y, loss, lr)
+        if B.n_rows[b] == 0:
+            assert np.array_equal(after, before)
+
+
+@pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
+def test_one_launch_equals_steps(loss):
+    B = Batches.concat([config_batches("c5", 20, 40), mixed_set()])
+    dev = upload(B)
+    y = torch.from_numpy(labels(B, loss, 3)).to(DEV)
+    h0 = (np.random.default_rng(5).standard_normal(B.n_cols) * 0.05).astype(np.float32)
+    h1 = torch.from_numpy(h0).to(DEV)
+    T.toc_mgd_epoch(dev, y, h1, loss, 0.25)
+    h2 = torch.from_numpy(h0).to(DEV)
+    for b in range(B.n_batches):
+        T.toc_mgd_epoch(dev, y, h2, loss, 0.25, b0=b, n_batches=1)
+    torch.cuda.synchronize()
+    assert np.array_equal(h1.cpu().numpy().view(np.uint32), h2.cpu().numpy().view(np.uint32))
+    assert not np.array_equal(h1.cpu().numpy(), h0)
+
+
+def test_lr_zero_and_errors():
+    B = config_batches("c5", 0, 2)
+    dev = upload(B)
+    y = torch.ones(int(B.n_rows.sum()), device=DEV)
+    h = torch.randn(B.n_cols, device=DEV)
+    h0 = h.clone()
+    T.toc_mgd_epoch(dev, y, h, T.TOC_MGD_LINEAR, 0.0)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h0)
+    for kw, st in [(dict(b0=1, n_batches=2), T.TOC_EINVAL), (dict(b0=-1, n_batches=1), T.TOC_EINVAL)]:
+        with pytest.raises(T.TocError) as ei:
+            T.toc_mgd_epoch(dev, y, h, T.TOC_MGD_LINEAR, 0.1, **kw)
+        assert ei.value.status == st
+    for loss, lr in [(3, 0.1), (T.TOC_MGD_HINGE, float("nan")), (T.TOC_MGD_HINGE, float("inf"))]:
+        with pytest.raises(T.TocError) as ei:
+            T.toc_mgd_epoch(dev, y, h, loss, lr)
+        assert ei.value.status == T.TOC_EINVAL
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    hbuf = np.zeros(T.toc_upload_size(encs, T.TOC_UPLOAD_HOST), np.uint8)
+    hdev = T.toc_upload(encs, hbuf, T.TOC_UPLOAD_HOST)
+    with pytest.raises(T.TocError) as ei:
+        T.toc_mgd_epoch(hdev, y, h, T.TOC_MGD_LINEAR, 0.1)
+    assert ei.value.status == T.TOC_EINVAL

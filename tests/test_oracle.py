@@ -496,3 +496,16 @@ def test_mgd_closed_forms():
     # lr = 0 and an empty batch change nothing
     assert O.mgd_step(one, 3, h, np.array([5.0]), O.MGD_LINEAR, 0.0)[0].tolist() == h.tolist()
     assert O.mgd_step([], 3, h, np.array([]), O.MGD_LINEAR, 1.0)[0].tolist() == h.tolist()
+
+
+def test_mgd_tolerance_scale_is_absolute():
+    """The scale is |A|^T (|g| + |A||h|): nonnegative, and on one entry a at column j
+    equal to |a| (|g| + |a h_j|)."""
+    rows = [[(0, O.f32_bits(-2.0))], [(0, O.f32_bits(3.0)), (1, O.f32_bits(-1.0))]]
+    h = np.array([0.5, -4.0])
+    y = np.array([1.0, -2.0])
+    _, scale = O.mgd_step(rows, 2, h, y, O.MGD_LINEAR, 1.0)
+    g = np.array([-2.0 * 0.5 - 1.0, 3.0 * 0.5 + 4.0 + 2.0])
+    s_r = np.array([1.0, 1.5 + 4.0])
+    assert np.allclose(scale, [2.0 * (abs(g[0]) + s_r[0]) + 3.0 * (abs(g[1]) + s_r[1]),
+                               1.0 * (abs(g[1]) + s_r[1])])
