@@ -493,7 +493,7 @@ def mgd_loss(loss, r, y):
     if loss == MGD_LINEAR:
         return 0.5 * (y - r) ** 2
     if loss == MGD_LOGISTIC:
-        return np.log1p(np.exp(-y * r))
+        return np.logaddexp(0.0, -y * r)            # log(1 + exp(-y r)) without overflow
     if loss == MGD_HINGE:
         return np.maximum(0.0, 1.0 - y * r)
     raise TocInputError("unknown loss")
@@ -505,7 +505,8 @@ def mgd_dloss(loss, r, y):
     if loss == MGD_LINEAR:
         return r - y
     if loss == MGD_LOGISTIC:
-        return -y / (1.0 + np.exp(y * r))
+        # -y / (1 + exp(y r)) = -y * sigmoid(-y r), the sigmoid as (1 + tanh(z/2)) / 2
+        return -y * 0.5 * (1.0 + np.tanh(-0.5 * y * r))
     if loss == MGD_HINGE:
         return np.where(y * r < 1.0, -y, 0.0)
     raise TocInputError("unknown loss")
