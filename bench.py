@@ -250,6 +250,39 @@ def time_cprime(sample, stream, reps=3):
     return res
 
 
+def time_mgd(w, stream, lr=0.1):
+    """One epoch of mini-batch gradient descent for logistic regression (k = 1) over
+    every batch of the resident image, in one toc_mgd_epoch launch (each step
+    depends on the previous one), with seeded labels of +-1 and h = 0 at the start."""
+    import torch
+    import paper_1702_06943_amd as T
+    info = w.info
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(1702)
+    y = (torch.randint(0, 2, (info["n_rows"],), generator=gen, device="cuda:0") * 2 - 1).float()
+    h = torch.zeros(info["n_cols"], device="cuda:0")
+    try:
+        T.toc_mgd_epoch(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr, b0=0, n_batches=1)
+    except T.TocError as e:
+        log(f"MGD epoch skipped: {e}")
+        return None
+    h.zero_()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    T.toc_mgd_epoch(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1])
+    ok = bool(torch.isfinite(h).all().item())
+    res = {"loss": "logistic", "batches": info["n_batches"], "ms": round(ms, 3),
+           "batches_per_s": info["n_batches"] / (ms / 1e3),
+           "nnz_per_s": info["nnz"] / (ms / 1e3), "model_finite": ok}
+    log(f"MGD epoch (logistic, {info['n_batches']} steps in one launch): {ms:.1f} ms, "
+        f"{res['batches_per_s']:.0f} steps/s")
+    return res
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -285,8 +318,8 @@ def main():
                     help="CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--workers", type=int, default=0)
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip timing the element-wise operations and the C' build after "
-                         "the step")
+                    help="skip timing the element-wise operations, the C' build and the "
+                         "MGD epoch after the step")
     ap.add_argument("--cprime-batches", type=int, default=4000,
                     help="batches whose physical encoding is turned into C' on the GPU "
                          "after the step (0 = skip)")
@@ -360,6 +393,7 @@ def main():
     info = w.info
     extras = None if args.no_extras else time_elementwise(w, stream)
     cprime = time_cprime(sample, stream) if sample else None
+    mgd = None if args.no_extras else time_mgd(w, stream)
     nnz = info["nnz"]
     canon = info["canon_bytes"]
     n_rows, m = info["n_rows"], info["n_cols"]
@@ -425,6 +459,7 @@ def main():
         "roofline": roof,
         "elementwise": extras,
         "cprime_build": cprime,
+        "mgd_epoch": mgd,
         "cpu_baseline": cpu,
         "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
                  "cpu": host_cpu()},
