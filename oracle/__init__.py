@@ -28,6 +28,9 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
   layout_stats   pinned: hand count on the worked example (live set, depths)
   physical_bytes parity unpinned (the paper prints sizes only in missing figures;
                  the formula of §3.2 is checked on the worked example by hand)
+  dense_bytes, sparse_bytes, logical_bytes
+                 pinned: hand counts on the worked example (12 pairs, |I| = 5,
+                 |D| = 9); the byte layouts are a reading (the paper gives none)
   pack_physical, unpack_physical
                  pinned: the worked example's bytes derived by hand from Table 2's
                  I and D under the byte-layout reading, the width rule of §3.2 at
@@ -58,6 +61,9 @@ from .toc_oracle import (  # noqa: F401
     MAP_SQUARE,
     layout_stats,
     physical_bytes,
+    dense_bytes,
+    sparse_bytes,
+    logical_bytes,
     pack_physical,
     unpack_physical,
     MGD_LINEAR,

@@ -397,6 +397,27 @@ def physical_bytes(I, D):
 
 
 # ---------------------------------------------------------------------------
+# Sizes of the TOC variants compared in the ablation study of §5.2 (compression
+# ratios of TOC_SPARSE, TOC_SPARSE_AND_LOGICAL and TOC_FULL against the dense
+# encoding DEN).  The paper names the variants but not their byte layouts; the
+# reading taken here: DEN stores n x m binary32 values; the sparse encoding (§3)
+# stores each nonzero as a u32 column index and a binary32 value, plus n + 1 u32
+# tuple starts; the logical encoding (§3.1) stores I as such pairs, D's codes as
+# u32 and n + 1 u32 tuple starts; TOC_FULL is the physical encoding of §3.2.
+# ---------------------------------------------------------------------------
+def dense_bytes(n_rows, n_cols):
+    return 4 * n_rows * n_cols
+
+
+def sparse_bytes(rows):
+    return 8 * sum(len(t) for t in rows) + 4 * (len(rows) + 1)
+
+
+def logical_bytes(I, D):
+    return 8 * len(I) + 4 * sum(len(d) for d in D) + 4 * (len(D) + 1)
+
+
+# ---------------------------------------------------------------------------
 # Physical encoding as bytes, §3.2.  The paper fixes the techniques -- bit packing
 # with ceil(log2(max+1)/8) bytes per integer behind a header that gives the count
 # and the bytes per integer, value indexing of I's values, D's codes of all tuples

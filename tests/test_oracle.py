@@ -120,6 +120,14 @@ def test_worked_example_sizes(example):
     assert O.physical_bytes(I, D) == s["physical_bytes"]
 
 
+def test_worked_example_variant_sizes(example):
+    rows, I, D, N = example
+    v = GOLD["variant_sizes"]
+    assert O.dense_bytes(4, 4) == v["dense_bytes"]
+    assert O.sparse_bytes(rows) == v["sparse_bytes"]
+    assert O.logical_bytes(I, D) == v["logical_bytes"]
+
+
 # --- brute-force re-encoder -------------------------------------------------------
 def brute_force_encode(rows):
     """Greedy longest-prefix dictionary coding written from its definition, with a
