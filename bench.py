@@ -91,15 +91,19 @@ class Workload:
     pass
 
 
-def encode_workload(cfg, nb, pool, chunk=400):
+def encode_workload(cfg, nb, pool, chunk=400, keep_batches=0):
+    """Generates and host-encodes the workload; keeps the CSR of the first
+    keep_batches batches (w.kept) for the device encoder's measurement."""
     import paper_1702_06943_amd as T
     from workloads.parallel import iter_chunks
     w = Workload()
     w.cfg, w.nb = cfg, nb
-    w.encs, w.nnz, w.rows = [], 0, 0
+    w.encs, w.nnz, w.rows, w.kept = [], 0, 0, []
     t0 = time.perf_counter()
     last = t0
     for part in iter_chunks(cfg, nb, 0, chunk, pool):
+        if len(w.encs) < keep_batches:
+            w.kept.append(part)
         w.encs.extend(T.toc_encode_batches(part.n_rows, part.n_cols, part.rowptr, part.col,
                                            part.val))
         w.nnz += part.nnz
@@ -283,6 +287,86 @@ def time_mgd(w, stream, lr=0.1):
     return res
 
 
+def variant_sizes(infos, n_cols):
+    """Bytes of the ablation study's TOC variants (section 5.2) summed over the
+    batches, from the encoder's counts: DEN 4 n m; sparse encoding 8 nnz + 4 (n + 1);
+    logical encoding 8 |I| + 4 |D| + 4 (n + 1); TOC_FULL the physical encoding of
+    section 3.2.  Ratios are DEN over each."""
+    tot = {"dense": 0, "sparse": 0, "logical": 0, "full": 0}
+    for i in infos:
+        n = i["n_rows"]
+        tot["dense"] += 4 * n * n_cols
+        tot["sparse"] += 8 * i["nnz"] + 4 * (n + 1)
+        tot["logical"] += 8 * i["n_first"] + 4 * i["n_codes"] + 4 * (n + 1)
+        tot["full"] += i["phys_bytes"]
+    out = {f"{k}_bytes": v for k, v in tot.items()}
+    for k in ("sparse", "logical", "full"):
+        out[f"{k}_ratio"] = tot["dense"] / tot[k] if tot[k] else None
+    return out
+
+
+def time_encode_device(w, stream, reps=3):
+    """toc_encode_device (Algorithm 1 on the GPU) over the kept batches' CSR,
+    resident in HBM; counts checked against the host encoder's for every batch,
+    whose own time on the same batches (all host threads) is reported beside it.
+    Algorithmic bytes: the CSR read once, I, D and the tuple offsets written once."""
+    import torch
+    import paper_1702_06943_amd as T
+    from workloads import Batches
+    if not w.kept:
+        return None
+    B = Batches.concat(w.kept)
+    nb = B.n_batches
+    t0 = time.perf_counter()
+    T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    host_s = time.perf_counter() - t0
+    dev = "cuda:0"
+    max_nnz = int(np.diff(B.rowptr[B.row_off]).max())
+    d_rp = torch.from_numpy(B.rowptr).to(dev)
+    d_col = torch.from_numpy(B.col).to(dev)
+    d_val = torch.from_numpy(B.val).to(dev)
+    nnz = int(B.col.size)
+    I_col = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    I_val = torch.empty(max(nnz, 1), device=dev)
+    D = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+    D_rp = torch.empty(int(B.n_rows.sum()) + nb, dtype=torch.int64, device=dev)
+    counts = torch.empty(4 * nb, dtype=torch.int64, device=dev)
+    status = torch.empty(nb, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(T.toc_encode_device_workspace_size(nb, max_nnz), 1), dtype=torch.uint8,
+                     device=dev)
+
+    def run():
+        T.toc_encode_device(B.n_rows, B.n_cols, d_rp, d_col, d_val, max_nnz, I_col, I_val, D,
+                            D_rp, counts, status, ws)
+
+    run()
+    torch.cuda.synchronize()
+    c = counts.cpu().numpy().reshape(nb, 4)
+    ok = bool((status.cpu().numpy() == 0).all())
+    infos = [T.toc_enc_info_get(e) for e in w.encs[:nb]]
+    same = ok and all((c[b, 0], c[b, 1], c[b, 2]) == (infos[b]["n_first"], infos[b]["n_codes"],
+                                                      infos[b]["n_nodes"]) for b in range(nb))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+    for i in range(reps):
+        ev[2 * i].record(stream)
+        run()
+        ev[2 * i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    n_first, n_codes = int(c[:, 0].sum()), int(c[:, 1].sum())
+    b = 8.0 * (B.rowptr.size + nnz) + 8 * n_first + 4 * n_codes + 8 * (int(B.n_rows.sum()) + nb)
+    res = {"batches": nb, "nnz": nnz, "ms": round(ms, 3), "nnz_per_s": nnz / (ms / 1e3),
+           "hbm_frac": b / (ms / 1e3) / HBM_PEAK, "counts_equal_host": same,
+           "host_encoder_ms": round(host_s * 1e3, 1),
+           "host_encoder_nnz_per_s": nnz / host_s, "speedup_vs_host": host_s * 1e3 / ms,
+           "workspace_bytes": int(ws.numel())}
+    log(f"device encode: {nb} batches, {ms:.2f} ms ({res['nnz_per_s']:.3e} nnz/s); host "
+        f"encoder on the same batches {host_s * 1e3:.1f} ms; counts equal: {same}")
+    del d_rp, d_col, d_val, I_col, I_val, D, D_rp, counts, status, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -320,6 +404,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip timing the element-wise operations, the C' build and the "
                          "MGD epoch after the step")
+    ap.add_argument("--encode-batches", type=int, default=4000,
+                    help="batches for the device encoder's measurement (0: skip)")
     ap.add_argument("--cprime-batches", type=int, default=4000,
                     help="batches whose physical encoding is turned into C' on the GPU "
                          "after the step (0 = skip)")
@@ -349,14 +435,18 @@ def main():
         log(f"oracle CPU baseline on {workers} processes ...")
         cpu = cpu_baseline(pool, workers, cfg, nb, k, args.cpu_seconds)
         log(f"oracle: {cpu['value']:.3e} nnz/s ({cpu['sample']})")
-    w = encode_workload(cfg, nb, pool)
+    w = encode_workload(cfg, nb, pool,
+                        keep_batches=0 if args.no_extras else args.encode_batches)
     pool.close()
     pool.join()
 
     import torch
+    import paper_1702_06943_amd as T
     upload_workload(w, k)
     sample = None if args.no_extras else pack_sample(w, args.cprime_batches)
-    w.encs = None
+    ablation = variant_sizes([T.toc_enc_info_get(e) for e in w.encs], w.n_cols)
+    encode_dev = None if args.no_extras else time_encode_device(w, torch.cuda.current_stream())
+    w.encs = w.kept = None
 
     stream = torch.cuda.current_stream()
     log(f"warmup {args.warmup} steps")
@@ -460,6 +550,8 @@ def main():
         "elementwise": extras,
         "cprime_build": cprime,
         "mgd_epoch": mgd,
+        "encode_device": encode_dev,
+        "ablation_sizes": ablation,
         "cpu_baseline": cpu,
         "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
                  "cpu": host_cpu()},

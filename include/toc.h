@@ -347,6 +347,62 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
                             size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * Encoding on the device.  The logical encoding of Algorithm 1 (section 3.1)
+ * after the sparse encoding (section 3), for many mini-batches held in one
+ * concatenated CSR in device memory, each batch with its own prefix tree: the
+ * result is the (I, D) that toc_encode gives for the same batch, node for node.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes of toc_encode_device for n_batches batches of at most max_nnz
+ * entries each (max_nnz <= 2^30, else TOC_EUNSUPPORTED): one hash table of
+ * 16-byte slots (a power of two of them, at least 1.5 max_nnz + 1 and 64) for
+ * each of up to 1024 batches in phase I and for each of up to 16384 batches in
+ * phase II, each phase capped near 8 GiB, plus 8 (n_batches + 1) bytes. */
+toc_status toc_encode_device_workspace_size(int64_t n_batches, int64_t max_nnz, size_t *bytes);
+
+/* Algorithm 1 on the device: phase I numbers the distinct pairs of a batch in
+ * order of first appearance (one workgroup per batch), phase II encodes its
+ * tuples by greedy longest matches, growing the tree (one lane per batch, the
+ * tree's child links in a hash table in the workspace).
+ *   n_rows   host int32[n_batches]: batch b owns the n_rows[b] rows after those
+ *            of batches 0..b-1
+ *   rowptr   device int64[sum(n_rows) + 1], non-decreasing; entry e (rowptr[0]
+ *            <= e < rowptr[0] + nnz) is col[e - rowptr[0]], val[e - rowptr[0]]
+ *   col, val device int32 / float[nnz]; the same rules as toc_encode: columns in
+ *            [0, n_cols) strictly increasing inside a row, values finite; entries
+ *            equal to zero (either sign) are dropped
+ *   max_nnz  the most entries of any batch (sizes the workspace)
+ * Outputs (device, caller-owned).  Batch b's entries occupy indexes
+ * s_b = rowptr[r_b] - rowptr[0] onwards, r_b its first row; its slot there holds:
+ *   I_col, I_val  int32 / float[nnz]: I (nodes 1..|I| of Algorithm 1, in order)
+ *            at s_b .. s_b + |I| - 1
+ *   D_codes  uint32[nnz]: D's codes of all the batch's tuples, in paper
+ *            numbering, at s_b .. s_b + |D| - 1 (the rest of the slot is
+ *            overwritten with unspecified values)
+ *   D_rowptr int64[sum(n_rows) + n_batches]: at r_b + b, the batch's n_rows[b]+1
+ *            offsets of its tuples into its D (starting at 0)
+ *   counts   int64[4 n_batches]: |I|, |D|, the node count of the tree with its
+ *            root (1 + |I| + sum over tuples of (codes - 1)), nonzero entries
+ *   status   int32[n_batches]: 0, or TOC_ENCDEV_* below (then the batch's counts
+ *            are 0 and its outputs unspecified; nothing outside its slot is
+ *            written)
+ *   ws       device workspace of toc_encode_device_workspace_size bytes
+ * Asynchronous on stream (n_rows is copied before returning).  TOC_EINVAL for
+ * NULL or negative arguments, TOC_ESIZE for a small workspace, TOC_EUNSUPPORTED
+ * for max_nnz above 2^30 or 2^32-1 batches or more.  Not reentrant on one
+ * workspace: calls that share a workspace must be ordered on one stream.      */
+#define TOC_ENCDEV_ROWPTR 1   /* rowptr decreases at or inside the batch, or leaves
+                                 [rowptr[0], rowptr[0] + nnz]                     */
+#define TOC_ENCDEV_SIZE 2     /* more entries than max_nnz                        */
+#define TOC_ENCDEV_COLUMN 3   /* a column out of range or not increasing in a row */
+#define TOC_ENCDEV_VALUE 4    /* a value is NaN or infinite                       */
+toc_status toc_encode_device(int64_t n_batches, const int32_t *n_rows, int32_t n_cols,
+                             const int64_t *rowptr, const int32_t *col, const float *val,
+                             int64_t nnz, int64_t max_nnz, int32_t *I_col, float *I_val,
+                             uint32_t *D_codes, int64_t *D_rowptr, int64_t *counts,
+                             int32_t *status, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * Mini-batch gradient descent (section 2.1): h <- h - lr / |B| * sum over the
  * tuples (x, y) of batch B of d loss(h, x, y) / d h, for the linear models of
  * Table 1, whose loss depends on h through r = x^T h: the batch gradient is

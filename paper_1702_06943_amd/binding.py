@@ -23,6 +23,7 @@ TOC_UPLOAD_HOST = 2
 TOC_OP_RIGHT, TOC_OP_LEFT, TOC_OP_DECODE = 0, 1, 2
 TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
 TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE = 0, 1, 2
+TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(1, 5)
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
  TOC_CPRIME_NODES, TOC_CPRIME_ROWS) = range(1, 7)
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
@@ -112,6 +113,8 @@ def lib():
         "toc_cprime_workspace_size": [I64, I64, P],
         "toc_cprime_build": [P, P, P, I64, I32, P, P, P, P, P, P, SZ, P],
         "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
+        "toc_encode_device_workspace_size": [I64, I64, P],
+        "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -378,3 +381,40 @@ def toc_mgd_epoch(dev, y, h, loss, lr, b0=0, n_batches=None, stream=None):
         raise TocError(TOC_EINVAL, "h must hold n_cols float32")
     _check(lib().toc_mgd_epoch(dev.handle, int(b0), int(n_batches), int(loss), float(lr),
                                _ptr(y), _ptr(h), _stream(stream)))
+
+
+def toc_encode_device_workspace_size(n_batches, max_nnz):
+    n = C.c_size_t()
+    _check(lib().toc_encode_device_workspace_size(int(n_batches), int(max_nnz), C.byref(n)))
+    return n.value
+
+
+def toc_encode_device(n_rows, n_cols, rowptr, col, val, max_nnz, I_col, I_val, D_codes,
+                      D_rowptr, counts, status, ws, stream=None):
+    """Algorithm 1 on the device.  n_rows: host int32 array (one entry per batch);
+    rowptr (int64), col (int32), val (float32): device tensors of the concatenated
+    CSR; I_col, I_val, D_codes: device tensors of col.numel() entries; D_rowptr:
+    device int64 tensor of sum(n_rows) + n_batches entries; counts: device int64
+    tensor of 4 per batch; status: device int32 tensor of one per batch; ws: device
+    tensor of toc_encode_device_workspace_size bytes."""
+    n_rows = _arr(n_rows, np.int32)
+    nb, nr = n_rows.size, int(n_rows.sum())
+    nnz = col.numel()
+    if rowptr.numel() != nr + 1 or rowptr.element_size() != 8:
+        raise TocError(TOC_EINVAL, "rowptr must hold sum(n_rows) + 1 int64")
+    if val.numel() != nnz or col.element_size() != 4 or val.element_size() != 4:
+        raise TocError(TOC_EINVAL, "col and val must hold the same number of 4-byte entries")
+    for t, name in ((I_col, "I_col"), (I_val, "I_val"), (D_codes, "D_codes")):
+        if t.numel() < nnz or t.element_size() != 4:
+            raise TocError(TOC_EINVAL, f"{name} must hold {nnz} 4-byte entries")
+    if D_rowptr.numel() < nr + nb or D_rowptr.element_size() != 8:
+        raise TocError(TOC_EINVAL, "D_rowptr must hold sum(n_rows) + n_batches int64")
+    if counts.numel() < 4 * nb or counts.element_size() != 8:
+        raise TocError(TOC_EINVAL, "counts must hold 4 int64 per batch")
+    if status.numel() < nb or status.element_size() != 4:
+        raise TocError(TOC_EINVAL, "status must hold one int32 per batch")
+    _check(lib().toc_encode_device(nb, _ptr(n_rows), int(n_cols), _ptr(rowptr), _ptr(col),
+                                   _ptr(val), nnz, int(max_nnz), _ptr(I_col), _ptr(I_val),
+                                   _ptr(D_codes), _ptr(D_rowptr), _ptr(counts), _ptr(status),
+                                   _ptr(ws), ws.numel() * ws.element_size() if ws is not None
+                                   else 0, _stream(stream)))

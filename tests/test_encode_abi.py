@@ -154,3 +154,58 @@ def test_null_pointers_rejected():
     assert lib.toc_decode_csr(None, None, None, None, None) == T.TOC_EINVAL
     assert lib.toc_map_values(None, 0, 1.0, None) == T.TOC_EINVAL
     assert lib.toc_decode_dense(None, 0.0, None, 1, None) == T.TOC_EINVAL
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_bench_variant_sizes_match_oracle(seed):
+    """The benchmark's ablation sizes (section 5.2), computed from the encoder's
+    counts, equal the oracle's dense_bytes / sparse_bytes / logical_bytes /
+    physical_bytes on the same batches."""
+    import bench
+    infos, want = [], {"dense": 0, "sparse": 0, "logical": 0, "full": 0}
+    for k, spec in enumerate(TINY):
+        rp, c, v = tiny_batch(8800 + 7 * seed + k, zeros=(seed % 2 == 0), **spec)
+        rows, I, D, N = _oracle_encode(spec["n_rows"], spec["n_cols"], rp, c, v)
+        enc = T.toc_encode(spec["n_rows"], 40, rp, c, v)
+        infos.append(T.toc_enc_info_get(enc))
+        want["dense"] += O.dense_bytes(spec["n_rows"], 40)
+        want["sparse"] += O.sparse_bytes(rows)
+        want["logical"] += O.logical_bytes(I, D)
+        want["full"] += O.physical_bytes(I, D)
+    got = bench.variant_sizes(infos, 40)
+    for key, val in want.items():
+        assert got[f"{key}_bytes"] == val, key
+
+
+def test_encode_device_host_checks():
+    """Argument checks of the device encoder that return before any HIP call."""
+    import ctypes as C
+    lib = T.lib()
+    n = C.c_size_t()
+    assert lib.toc_encode_device_workspace_size(-1, 10, C.byref(n)) == T.TOC_EINVAL
+    assert lib.toc_encode_device_workspace_size(3, (1 << 30) + 1, C.byref(n)) == \
+        T.TOC_EUNSUPPORTED
+    assert lib.toc_encode_device_workspace_size(0, 100, C.byref(n)) == 0 and n.value == 0
+    assert lib.toc_encode_device_workspace_size(2, 1000, C.byref(n)) == 0
+    small = n.value
+    assert lib.toc_encode_device_workspace_size(2, 100000, C.byref(n)) == 0 and n.value > small
+    nr = np.array([3, 2], np.int32)
+    dummy = C.c_void_p(16)                     # never dereferenced: every check fails first
+    args = [2, nr.ctypes.data, 5, dummy, dummy, dummy, 10, 6, dummy, dummy, dummy, dummy,
+            dummy, dummy, dummy, 1, None]
+    assert lib.toc_encode_device(*args) == T.TOC_ESIZE          # workspace of 1 byte
+    bad = list(args)
+    bad[0] = -1
+    assert lib.toc_encode_device(*bad) == T.TOC_EINVAL
+    bad = list(args)
+    bad[7] = (1 << 30) + 1
+    assert lib.toc_encode_device(*bad) == T.TOC_EUNSUPPORTED
+    bad = list(args)
+    bad[3] = None
+    assert lib.toc_encode_device(*bad) == T.TOC_EINVAL
+    nr_bad = np.array([3, -2], np.int32)
+    bad = list(args)
+    bad[1] = nr_bad.ctypes.data
+    assert lib.toc_encode_device(*bad) == T.TOC_EINVAL
+    assert lib.toc_encode_device(0, None, 5, None, None, None, 0, 0, None, None, None, None,
+                                 None, None, None, 0, None) == 0
