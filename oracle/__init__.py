@@ -42,6 +42,11 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
                  the paper's linear-regression gradient on the worked example by
                  hand, closed forms (lr = 0, one entry, logistic at r = 0, hinge
                  beyond the margin), an empty batch
+  mlp_loss, mlp_step
+                 pinned: central finite differences of the mean cross-entropy for
+                 every parameter (softmax and single-sigmoid outputs), the first
+                 layer's gradient equal to Theorem 2's left product on (I, D)
+                 (toc_left), the closed form at zero weights, lr = 0, an empty batch
 """
 
 from .toc_oracle import (  # noqa: F401
@@ -72,6 +77,8 @@ from .toc_oracle import (  # noqa: F401
     mgd_loss,
     mgd_dloss,
     mgd_step,
+    mlp_loss,
+    mlp_step,
     f32_bits,
     bits_f32,
 )

@@ -545,3 +545,77 @@ def mgd_step(rows, n_cols, h, y, loss, lr):
     grad, _ = dense_left(rows, n_cols, g[:, None])
     _, scale = dense_left(rows, n_cols, (np.abs(g) + s_r[:, 0])[:, None])
     return h - lr / len(rows) * grad[:, 0], scale[:, 0]
+
+
+# ---------------------------------------------------------------------------
+# Mini-batch gradient descent for the neural network of §5.1 (the NN row of
+# Table 1, whose matrix operations are A.M and M.A): a feed-forward network with
+# two hidden layers (sigmoid activations) and a sigmoid output for one class or
+# a softmax output for several, trained with cross-entropy loss.  The batch's
+# first layer is Z1 = A W1 + b1 (A.M with M = W1) and its weight gradient is
+# A^T dZ1 (M.A with M = dZ1^T).  Readings: every layer has a bias; the loss is the
+# mean over the batch's tuples, so one step moves every parameter by lr times the
+# gradient of that mean (§2.1's update); labels are class indexes (0/1 for the
+# single sigmoid output).
+# ---------------------------------------------------------------------------
+def _sigmoid(x):
+    return 0.5 * (1.0 + np.tanh(0.5 * x))
+
+
+def _densify(rows, n_cols):
+    A = np.zeros((len(rows), n_cols))
+    for i, t in enumerate(rows):
+        for c, b in t:
+            A[i, c] = bits_f32(b)
+    return A
+
+
+def _mlp_forward(A, p):
+    H1 = _sigmoid(A @ p["W1"] + p["b1"])
+    H2 = _sigmoid(H1 @ p["W2"] + p["b2"])
+    Z3 = H2 @ p["W3"] + p["b3"]
+    return H1, H2, Z3
+
+
+def mlp_loss(rows, n_cols, params, labels):
+    """Mean cross-entropy loss of the network on a decoded batch (fp64)."""
+    p = {k: np.asarray(v, np.float64) for k, v in params.items()}
+    labels = np.asarray(labels, np.int64)
+    _, _, Z3 = _mlp_forward(_densify(rows, n_cols), p)
+    if Z3.shape[1] == 1:
+        z = Z3[:, 0]
+        per = np.logaddexp(0.0, z) - labels * z        # -log sigmoid(z) or -log(1 - sigmoid(z))
+    else:
+        zmax = Z3.max(axis=1, keepdims=True)
+        lse = zmax[:, 0] + np.log(np.exp(Z3 - zmax).sum(axis=1))
+        per = lse - Z3[np.arange(len(labels)), labels]
+    return float(per.mean()) if len(per) else 0.0
+
+
+def mlp_step(rows, n_cols, params, labels, lr):
+    """One MGD step of the network on a decoded batch: returns (new parameters,
+    gradients of the mean loss), both dicts of fp64 arrays keyed W1, b1, W2, b2, W3,
+    b3.  A batch without tuples leaves the parameters unchanged."""
+    p = {k: np.asarray(v, np.float64) for k, v in params.items()}
+    n = len(rows)
+    if n == 0:
+        return {k: v.copy() for k, v in p.items()}, {k: np.zeros_like(v) for k, v in p.items()}
+    labels = np.asarray(labels, np.int64)
+    A = _densify(rows, n_cols)
+    H1, H2, Z3 = _mlp_forward(A, p)
+    C = Z3.shape[1]
+    if C == 1:
+        P = _sigmoid(Z3)
+        Y = labels[:, None].astype(np.float64)
+    else:
+        E = np.exp(Z3 - Z3.max(axis=1, keepdims=True))
+        P = E / E.sum(axis=1, keepdims=True)
+        Y = np.zeros_like(P)
+        Y[np.arange(n), labels] = 1.0
+    dZ3 = (P - Y) / n                                   # d (mean loss) / d Z3
+    dZ2 = (dZ3 @ p["W3"].T) * H2 * (1.0 - H2)
+    dZ1 = (dZ2 @ p["W2"].T) * H1 * (1.0 - H1)
+    g = {"W3": H2.T @ dZ3, "b3": dZ3.sum(axis=0),
+         "W2": H1.T @ dZ2, "b2": dZ2.sum(axis=0),
+         "W1": A.T @ dZ1, "b1": dZ1.sum(axis=0)}
+    return {k: p[k] - lr * g[k] for k in p}, g

@@ -517,3 +517,66 @@ def test_mgd_tolerance_scale_is_absolute():
     s_r = np.array([1.0, 1.5 + 4.0])
     assert np.allclose(scale, [2.0 * (abs(g[0]) + s_r[0]) + 3.0 * (abs(g[1]) + s_r[1]),
                                1.0 * (abs(g[1]) + s_r[1])])
+
+
+# --- neural network step (section 5.1's network, Table 1's A.M and M.A) -------------
+def _mlp_params(rng, m, h1, h2, C, scale=0.5):
+    return {"W1": rng.standard_normal((m, h1)) * scale, "b1": rng.standard_normal(h1) * scale,
+            "W2": rng.standard_normal((h1, h2)) * scale, "b2": rng.standard_normal(h2) * scale,
+            "W3": rng.standard_normal((h2, C)) * scale, "b3": rng.standard_normal(C) * scale}
+
+
+@pytest.mark.parametrize("C", [1, 3])
+@pytest.mark.parametrize("seed", range(3))
+def test_mlp_step_is_gradient_step(C, seed):
+    """p - p_new = lr * d(mean loss)/dp for every entry of every parameter, the
+    derivative taken by central finite differences of the loss definition."""
+    rp, c, v = tiny_batch(4300 + seed, n_rows=9, n_cols=7, density=0.6, n_values=3)
+    rows = O.canonicalize(9, 7, rp, c, v)
+    rng = np.random.default_rng(seed)
+    p = _mlp_params(rng, 7, 4, 3, C)
+    labels = rng.integers(0, max(C, 2), size=9)
+    lr = 0.3
+    new, g = O.mlp_step(rows, 7, p, labels, lr)
+    eps = 1e-6
+    for name, val in p.items():
+        for idx in np.ndindex(val.shape):
+            hi = {k: x.copy() for k, x in p.items()}
+            lo = {k: x.copy() for k, x in p.items()}
+            hi[name][idx] += eps
+            lo[name][idx] -= eps
+            fd = (O.mlp_loss(rows, 7, hi, labels) - O.mlp_loss(rows, 7, lo, labels)) / (2 * eps)
+            assert abs(g[name][idx] - fd) <= 1e-6 * abs(fd) + 1e-9, (name, idx)
+            assert abs((val[idx] - new[name][idx]) / lr - fd) <= 1e-6 * abs(fd) + 1e-9
+
+
+def test_mlp_closed_form_at_zero_weights():
+    """All weights and biases 0: every hidden unit is 1/2 and the output uniform, so
+    d/db3_c = (1/C - [y = c]) averaged over the tuples, d/dW3[u, c] = d/db3_c / 2, and
+    every other gradient is 0 (W3 = 0 stops the backward pass)."""
+    rows = [[(0, O.f32_bits(1.0)), (2, O.f32_bits(-2.0))], [(1, O.f32_bits(3.0))],
+            [(2, O.f32_bits(0.5))], []]
+    p = {"W1": np.zeros((3, 4)), "b1": np.zeros(4), "W2": np.zeros((4, 2)), "b2": np.zeros(2),
+         "W3": np.zeros((2, 3)), "b3": np.zeros(3)}
+    labels = np.array([0, 2, 2, 1])
+    new, g = O.mlp_step(rows, 3, p, labels, 1.0)
+    db3 = np.array([1 / 3 - 1 / 4, 1 / 3 - 1 / 4, 1 / 3 - 2 / 4])
+    assert np.allclose(g["b3"], db3, rtol=0, atol=1e-15)
+    assert np.allclose(g["W3"], np.tile(db3 / 2, (2, 1)), rtol=0, atol=1e-15)
+    for k in ("W1", "b1", "W2", "b2"):
+        assert not g[k].any()
+    assert np.allclose(new["b3"], -db3, rtol=0, atol=1e-15)
+    # one sigmoid output: at z = 0 the gradient of the bias is the mean of 1/2 - y
+    p1 = dict(p, W3=np.zeros((2, 1)), b3=np.zeros(1))
+    _, g1 = O.mlp_step(rows, 3, p1, np.array([1, 0, 1, 1]), 1.0)
+    assert np.allclose(g1["b3"], [0.5 - 0.75], rtol=0, atol=1e-15)
+
+
+def test_mlp_lr_zero_and_empty_batch():
+    rng = np.random.default_rng(5)
+    p = _mlp_params(rng, 4, 3, 2, 2)
+    rows = [[(1, O.f32_bits(2.0))], [(0, O.f32_bits(-1.0)), (3, O.f32_bits(0.5))]]
+    new, _ = O.mlp_step(rows, 4, p, [0, 1], 0.0)
+    assert all(np.array_equal(new[k], p[k]) for k in p)
+    new, g = O.mlp_step([], 4, p, [], 1.0)
+    assert all(np.array_equal(new[k], p[k]) and not g[k].any() for k in p)
