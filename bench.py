@@ -367,6 +367,53 @@ def time_encode_device(w, stream, reps=3):
     return res
 
 
+def time_mlp(w, stream, n_steps, h1=200, h2=50, n_out=10, lr=0.1):
+    """n_steps mini-batch gradient descent steps of section 5.1's network (hidden
+    layers of h1 and h2 sigmoid units, a softmax over n_out classes, cross-entropy)
+    on the first batches of the resident image, in one toc_mlp_epoch call, with
+    seeded labels and weights."""
+    import torch
+    import paper_1702_06943_amd as T
+    info = w.info
+    n_steps = min(n_steps, info["n_batches"])
+    if n_steps <= 0:
+        return None
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(5101)
+    m = info["n_cols"]
+    labels = torch.randint(0, n_out, (info["n_rows"],), generator=gen, device="cuda:0",
+                           dtype=torch.int32)
+    scale1 = 1.0 / max(1.0, float(info["nnz"]) / info["n_rows"]) ** 0.5 / 100.0
+    p = {"W1": torch.randn((m, h1), generator=gen, device="cuda:0") * scale1,
+         "b1": torch.zeros(h1, device="cuda:0"),
+         "W2": torch.randn((h1, h2), generator=gen, device="cuda:0") * (1.0 / h1 ** 0.5),
+         "b2": torch.zeros(h2, device="cuda:0"),
+         "W3": torch.randn((h2, n_out), generator=gen, device="cuda:0") * (1.0 / h2 ** 0.5),
+         "b3": torch.zeros(n_out, device="cuda:0")}
+    ws = torch.empty(max(T.toc_mlp_workspace_size(w.dev, h1, h2, n_out), 16), dtype=torch.uint8,
+                     device="cuda:0")
+    try:
+        T.toc_mlp_epoch(w.dev, p, labels, lr, ws, b0=0, n_batches=1)
+    except T.TocError as e:
+        log(f"NN steps skipped: {e}")
+        return None
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    T.toc_mlp_epoch(w.dev, p, labels, lr, ws, b0=1, n_batches=n_steps)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1])
+    ok = all(bool(torch.isfinite(t).all().item()) for t in p.values())
+    res = {"layers": [m, h1, h2, n_out], "steps": n_steps, "ms": round(ms, 3),
+           "steps_per_s": n_steps / (ms / 1e3), "ms_per_step": ms / n_steps,
+           "epoch_s_extrapolated": info["n_batches"] * ms / n_steps / 1e3,
+           "model_finite": ok}
+    log(f"NN MGD ({m}-{h1}-{h2}-{n_out}, {n_steps} steps): {ms:.1f} ms, "
+        f"{res['steps_per_s']:.0f} steps/s")
+    return res
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -404,6 +451,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip timing the element-wise operations, the C' build and the "
                          "MGD epoch after the step")
+    ap.add_argument("--nn-steps", type=int, default=2000,
+                    help="neural-network MGD steps to time (0: skip)")
     ap.add_argument("--encode-batches", type=int, default=4000,
                     help="batches for the device encoder's measurement (0: skip)")
     ap.add_argument("--cprime-batches", type=int, default=4000,
@@ -484,6 +533,7 @@ def main():
     extras = None if args.no_extras else time_elementwise(w, stream)
     cprime = time_cprime(sample, stream) if sample else None
     mgd = None if args.no_extras else time_mgd(w, stream)
+    nn = None if args.no_extras else time_mlp(w, stream, args.nn_steps)
     nnz = info["nnz"]
     canon = info["canon_bytes"]
     n_rows, m = info["n_rows"], info["n_cols"]
@@ -550,6 +600,7 @@ def main():
         "elementwise": extras,
         "cprime_build": cprime,
         "mgd_epoch": mgd,
+        "nn_steps": nn,
         "encode_device": encode_dev,
         "ablation_sizes": ablation,
         "cpu_baseline": cpu,

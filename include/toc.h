@@ -425,6 +425,41 @@ toc_status toc_encode_device(int64_t n_batches, const int32_t *n_rows, int32_t n
 toc_status toc_mgd_epoch(const toc_dev *dev, int64_t b0, int64_t n_batches, int32_t loss,
                          float lr, const float *y, float *h, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Mini-batch gradient descent for the neural network of section 5.1 (Table 1's
+ * NN row, whose matrix operations are A.M and M.A): layers m -> h1 -> h2 ->
+ * n_out with sigmoid hidden units and a bias in every layer, a softmax output
+ * (n_out >= 2, labels 0..n_out-1) or one sigmoid output (n_out = 1, labels 0/1),
+ * cross-entropy loss; a step moves every parameter by -lr times the gradient of
+ * the batch's mean loss (section 2.1).  The first layer runs on the compressed
+ * batch: Z1 = A W1 + b1 by Theorem 1 and the gradient A^T dZ1 by Theorem 2.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes of toc_mlp_epoch: 4 (most rows of a batch) (2 h1 + 2 h2 +
+ * n_out) (each part rounded up to 4 floats), plus, when 16 bytes per code exceed
+ * 160 KiB of LDS (those table rows are then kept in the workspace), 16 h1 per
+ * tree code of the batch with the most and 4 h1 ceil(max rows / 64) per deep
+ * code of the batch with the most. */
+toc_status toc_mlp_workspace_size(const toc_dev *dev, int32_t h1, int32_t h2, int32_t n_out,
+                                  size_t *bytes);
+
+/* Runs the steps of batches b0 .. b0+n_batches-1 of an uploaded image in order
+ * (three launches per step on stream; a batch without tuples changes nothing).
+ *   W1 [m x h1], b1 [h1], W2 [h1 x h2], b2 [h2], W3 [h2 x n_out], b3 [n_out]:
+ *            device float, row-major, updated in place; W1 and b1 16-byte aligned
+ *   labels   device int32 per row of the image (all batches' rows, stacked); a
+ *            label outside the classes matches none (its target is all zeros)
+ *   ws       device workspace of toc_mlp_workspace_size bytes, 16-byte aligned
+ * h1 must be a multiple of 4 in 4..4096 (TOC_EUNSUPPORTED otherwise), h2 and
+ * n_out in 1..4096.  TOC_EINVAL for
+ * a batch range outside the image, NULL or misaligned pointers, a learning rate
+ * that is not finite or an image in host memory; TOC_ESIZE for a small
+ * workspace.  Asynchronous on stream.                                        */
+toc_status toc_mlp_epoch(const toc_dev *dev, int64_t b0, int64_t n_batches, int32_t h1,
+                         int32_t h2, int32_t n_out, float *W1, float *b1, float *W2, float *b2,
+                         float *W3, float *b3, const int32_t *labels, float lr, void *ws,
+                         size_t ws_bytes, void *stream);
+
 /* Message for the last non-OK status returned on this thread. */
 const char *toc_last_error(void);
 

@@ -2,7 +2,8 @@
 G^T.A, decode, sparse-safe element-wise ops and dense A .+ c on the compressed
 mini-batches with hand-written gfx950 kernels; pack batches into the paper's
 physical encoding and build the decoding tree C' from it on the GPU; run
-mini-batch gradient descent steps of linear models on the compressed batches;
+mini-batch gradient descent steps of linear models and of a feed-forward neural
+network on the compressed batches;
 encode many mini-batches at once on the GPU.
 
 The functions are those of include/toc.h, called through ctypes; see binding.py.
@@ -23,4 +24,5 @@ from .binding import (  # noqa: F401
     TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE, toc_mgd_epoch,
     TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE,
     toc_encode_device_workspace_size, toc_encode_device,
+    toc_mlp_workspace_size, toc_mlp_epoch,
 )

@@ -114,6 +114,8 @@ def lib():
         "toc_cprime_build": [P, P, P, I64, I32, P, P, P, P, P, P, SZ, P],
         "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
         "toc_encode_device_workspace_size": [I64, I64, P],
+        "toc_mlp_workspace_size": [P, I32, I32, I32, P],
+        "toc_mlp_epoch": [P, I64, I64, I32, I32, I32, P, P, P, P, P, P, P, C.c_float, P, SZ, P],
         "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
     }
     for name, args in sig.items():
@@ -418,3 +420,39 @@ def toc_encode_device(n_rows, n_cols, rowptr, col, val, max_nnz, I_col, I_val, D
                                    _ptr(D_codes), _ptr(D_rowptr), _ptr(counts), _ptr(status),
                                    _ptr(ws), ws.numel() * ws.element_size() if ws is not None
                                    else 0, _stream(stream)))
+
+
+def toc_mlp_workspace_size(dev, h1, h2, n_out):
+    n = C.c_size_t()
+    _check(lib().toc_mlp_workspace_size(dev.handle, int(h1), int(h2), int(n_out), C.byref(n)))
+    return n.value
+
+
+def toc_mlp_epoch(dev, params, labels, lr, ws, b0=0, n_batches=None, stream=None):
+    """Neural-network MGD steps over batches b0 .. b0+n_batches-1 (default: all
+    from b0).  params: dict of device float32 tensors W1 (m x h1), b1, W2 (h1 x
+    h2), b2, W3 (h2 x n_out), b3, updated in place; labels: device int32 tensor of
+    one label per row of the image; ws: device tensor of toc_mlp_workspace_size
+    bytes."""
+    info = toc_dev_info_get(dev)
+    if n_batches is None:
+        n_batches = info["n_batches"] - b0
+    W1, W2, W3 = params["W1"], params["W2"], params["W3"]
+    if W1.dim() != 2 or W2.dim() != 2 or W3.dim() != 2:
+        raise TocError(TOC_EINVAL, "W1, W2, W3 must be matrices")
+    m, h1 = W1.shape
+    h2, n_out = W3.shape
+    if m != info["n_cols"] or tuple(W2.shape) != (h1, h2):
+        raise TocError(TOC_EINVAL, "parameter shapes do not chain m -> h1 -> h2 -> n_out")
+    for name, t, n in (("W1", W1, m * h1), ("b1", params["b1"], h1), ("W2", W2, h1 * h2),
+                       ("b2", params["b2"], h2), ("W3", W3, h2 * n_out),
+                       ("b3", params["b3"], n_out)):
+        if t.numel() != n or t.element_size() != 4 or not t.is_contiguous():
+            raise TocError(TOC_EINVAL, f"{name} must be a contiguous float32 tensor of {n}")
+    if labels.numel() < info["n_rows"] or labels.element_size() != 4:
+        raise TocError(TOC_EINVAL, "labels must hold one int32 per row")
+    _check(lib().toc_mlp_epoch(dev.handle, int(b0), int(n_batches), int(h1), int(h2),
+                               int(n_out), _ptr(W1), _ptr(params["b1"]), _ptr(W2),
+                               _ptr(params["b2"]), _ptr(W3), _ptr(params["b3"]), _ptr(labels),
+                               float(lr), _ptr(ws), ws.numel() * ws.element_size(),
+                               _stream(stream)))

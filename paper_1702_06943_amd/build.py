@@ -38,7 +38,7 @@ def build(verbose=False):
         _run(["g++", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE,
               "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)
-    for src in ("toc_device.hip", "toc_cprime.hip", "toc_mgd.hip", "toc_encode.hip"):
+    for src in ("toc_device.hip", "toc_cprime.hip", "toc_mgd.hip", "toc_encode.hip", "toc_mlp.hip"):
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32,
               "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", o], verbose)

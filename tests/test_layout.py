@@ -299,3 +299,19 @@ def test_host_image_rejected_by_device_ops():
     assert lib.toc_decode_csr(dev.handle, 8, 8, 8, None) == T.TOC_EINVAL
     assert lib.toc_map_values(dev.handle, 0, 2.0, None) == T.TOC_EINVAL
     assert lib.toc_decode_dense(dev.handle, 0.0, 8, 3, None) == T.TOC_EINVAL
+
+
+def test_mlp_host_checks():
+    """The neural-network step's checks that need no GPU: an image in host memory
+    is rejected; the workspace size is 4 (max rows) (2 h1 + 2 h2 + n_out) bytes
+    when the table rows fit in LDS."""
+    import ctypes as C
+    B = config_batches("c5", 0, 2)
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    hbuf = np.zeros(T.toc_upload_size(encs, T.TOC_UPLOAD_HOST), np.uint8)
+    hdev = T.toc_upload(encs, hbuf, T.TOC_UPLOAD_HOST)
+    assert T.toc_mlp_workspace_size(hdev, 200, 50, 10) == 4 * 250 * (400 + 100 + 10)
+    dummy = C.c_void_p(16)
+    st = T.lib().toc_mlp_epoch(hdev.handle, 0, 2, 8, 3, 2, dummy, dummy, dummy, dummy, dummy,
+                               dummy, dummy, C.c_float(0.1), dummy, 1 << 20, None)
+    assert st == T.TOC_EINVAL
