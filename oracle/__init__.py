@@ -26,6 +26,10 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
   dense_plus     pinned: round trip to the CSR for c = 0, zeros become c,
                  integer sums in closed form
   layout_stats   pinned: hand count on the worked example (live set, depths)
+  level_order    pinned: the worked example's level order derived by hand from
+                 Table 4; invariants (parents first, depth steps of one, stable
+                 within a depth, exactly the live set) and decoding through the new
+                 numbering equal to Algorithm 6 on random tables
   physical_bytes parity unpinned (the paper prints sizes only in missing figures;
                  the formula of §3.2 is checked on the worked example by hand)
   dense_bytes, sparse_bytes, logical_bytes
@@ -65,6 +69,7 @@ from .toc_oracle import (  # noqa: F401
     MAP_SCALE,
     MAP_SQUARE,
     layout_stats,
+    level_order,
     physical_bytes,
     dense_bytes,
     sparse_bytes,

@@ -371,6 +371,38 @@ def layout_stats(I, D):
     }
 
 
+def level_order(I, D):
+    """The live codes in level order, as the operations of §4 can read them.
+
+    Live codes are those D references plus all their ancestors (the only codes
+    Algorithms 4-8 touch).  Sorted stably by (depth, index), every parent comes
+    before its children, which is all the forward scan of Algorithm 4 and the
+    backward scan of Algorithm 5 need.  Returns a dict: per live code in that order
+    parent (new index, None at depth 1), key (col, bits), depth; level_off[d] =
+    number of live codes of depth <= d (d = 0..max depth); D renumbered.
+    """
+    cp = build_cprime(I, D)
+    parent, depth = cp["parent"], cp["depth"]
+    live = set()
+    for d in D:
+        for c in d:
+            while c != 0 and c not in live:
+                live.add(c)
+                c = parent[c]
+    order = sorted(live, key=lambda c: (depth[c], c))
+    new = {c: i for i, c in enumerate(order)}
+    max_depth = max((depth[c] for c in order), default=0)
+    level_off = [sum(1 for c in order if depth[c] <= d) for d in range(max_depth + 1)]
+    return {
+        "parent": [new[parent[c]] if depth[c] > 1 else None for c in order],
+        "key": [cp["key"][c] for c in order],
+        "depth": [depth[c] for c in order],
+        "level_off": level_off,
+        "D": [[new[c] for c in d] for d in D],
+        "order": order,
+    }
+
+
 def _packed_array_bytes(values):
     """Bit packing of §3.2: ceil(log2(max+1)/8) bytes per integer (at least one),
     plus a header holding the count (u32) and the bytes per integer (u8)."""

@@ -580,3 +580,45 @@ def test_mlp_lr_zero_and_empty_batch():
     assert all(np.array_equal(new[k], p[k]) for k in p)
     new, g = O.mlp_step([], 4, p, [], 1.0)
     assert all(np.array_equal(new[k], p[k]) and not g[k].any() for k in p)
+
+
+# --- level order of the live codes -------------------------------------------------
+def test_level_order_worked_example(example):
+    rows, I, D, N = example
+    lo = O.level_order(I, D)
+    want = GOLD["level_order"]
+    for k in ("order", "parent", "depth", "level_off", "D"):
+        assert lo[k] == want[k], k
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_level_order_invariants_and_decode(seed):
+    spec = [dict(n_rows=30, n_cols=9, density=0.8, n_values=2, prefix_copy=0.7),
+            dict(n_rows=12, n_cols=25, density=0.4, n_values=3),
+            dict(n_rows=60, n_cols=6, density=1.0, n_values=1, prefix_copy=0.5)][seed % 3]
+    rp, c, v = tiny_batch(6100 + seed, zeros=(seed % 4 == 0), **spec)
+    rows = O.canonicalize(spec["n_rows"], spec["n_cols"], rp, c, v)
+    I, D, _ = O.encode(rows)
+    lo = O.level_order(I, D)
+    cp = O.build_cprime(I, D)
+    n = len(lo["order"])
+    assert n == O.layout_stats(I, D)["n_live"]
+    assert sorted(lo["order"]) == sorted(set(lo["order"]))
+    for i, (p, d) in enumerate(zip(lo["parent"], lo["depth"])):
+        if d == 1:
+            assert p is None
+        else:
+            assert p < i and lo["depth"][p] == d - 1
+            assert lo["order"][p] == cp["parent"][lo["order"][i]]
+        if i and lo["depth"][i - 1] == d:
+            assert lo["order"][i - 1] < lo["order"][i]          # stable inside a depth
+        assert lo["level_off"][d - 1] <= i < lo["level_off"][d]
+    assert lo["level_off"][-1] == n and lo["level_off"][0] == 0
+    # decoding through the new numbering gives Algorithm 6's rows
+    def chain(c):
+        out = []
+        while c is not None:
+            out.append(lo["key"][c])
+            c = lo["parent"][c]
+        return out[::-1]
+    assert [[p for c in d for p in chain(c)] for d in lo["D"]] == O.decode(I, D)
