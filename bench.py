@@ -242,14 +242,46 @@ def time_cprime(sample, stream, reps=3):
         ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
     ms = float(np.mean([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    # then the live codes in level order from that tree (toc_level_build)
+    d_off = np.concatenate([[0], np.cumsum([i["n_codes"] for i in infos])]).astype(np.int64)
+    max_levels = 64
+    lv = [torch.empty(n, dtype=torch.int32, device=dev) for _ in range(4)]
+    level = torch.empty(len(blobs) * (max_levels + 1), dtype=torch.int32, device=dev)
+    lD = torch.empty(max(int(d_off[-1]), 1), dtype=torch.int32, device=dev)
+    counts = torch.empty(2 * len(blobs), dtype=torch.int64, device=dev)
+    lst = torch.empty(len(blobs), dtype=torch.int32, device=dev)
+    ws2 = torch.empty(T.toc_level_workspace_size(len(blobs), n), dtype=torch.uint8, device=dev)
+
+    def run_level():
+        T.toc_level_build(d_blobs, blob_off, node_off, d_off, max_levels, status, *outs, *lv,
+                          level, lD, counts, lst, ws2)
+
+    run_level()
+    torch.cuda.synchronize()
+    lok = bool((lst == 0).all().item())
+    n_live = int(counts.view(-1, 2)[:, 0].sum().item())
+    for i in range(reps):
+        ev[2 * i].record(stream)
+        run_level()
+        ev[2 * i + 1].record(stream)
+    torch.cuda.synchronize()
+    lms = float(np.mean([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    # algorithmic bytes: the tree read once (16 B per node), D read from the blobs
+    # and written renumbered, 16 B per live code and the level offsets written
+    lb = float(16 * n + 8 * int(d_off[-1]) + 16 * n_live + 4 * level.numel())
     b = float(blob_off[-1] + 16 * n)
     res = {"batches": len(blobs), "nodes": n, "blob_bytes": int(blob_off[-1]), "ms": round(ms, 4),
            "nodes_per_s": n / (ms / 1e3), "GB/s": b / ms / 1e6,
            "hbm_frac": b / (ms / 1e3) / HBM_PEAK, "status_ok": ok,
-           "host_pack_s": round(sample["pack_s"], 3)}
+           "host_pack_s": round(sample["pack_s"], 3),
+           "level_order": {"ms": round(lms, 4), "live_codes": n_live,
+                           "hbm_frac": lb / (lms / 1e3) / HBM_PEAK, "status_ok": lok},
+           "ingest_ms": round(ms + lms, 4)}
     log(f"C' build from physical bytes: {len(blobs)} batches, {n} nodes, {ms:.3f} ms "
         f"({res['hbm_frac']:.1%} of HBM peak on algorithmic bytes), status ok: {ok}")
-    del d_blobs, outs, status, ws
+    log(f"level order from that tree: {lms:.3f} ms ({res['level_order']['hbm_frac']:.1%} of "
+        f"HBM peak on algorithmic bytes), {n_live} live codes, status ok: {lok}")
+    del d_blobs, outs, status, ws, lv, level, lD, counts, lst, ws2
     torch.cuda.empty_cache()
     return res
 

@@ -402,6 +402,41 @@ toc_status toc_encode_device(int64_t n_batches, const int32_t *n_rows, int32_t n
                              uint32_t *D_codes, int64_t *D_rowptr, int64_t *counts,
                              int32_t *status, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes of toc_level_build for n_batches batches and n_nodes nodes in
+ * total. */
+toc_status toc_level_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *bytes);
+
+/* The live codes of each batch in level order, on the device, from the tree of
+ * toc_cprime_build and the D of the same blobs: the codes D references and all
+ * their ancestors (the only codes the operations of section 4 touch), stably
+ * sorted by (depth, paper index), so that every parent precedes its children
+ * (all the forward scan of Algorithm 4 and the backward scan of Algorithm 5
+ * need); parents and D renumbered to that order.
+ *   blobs, blob_off, node_off  as for toc_cprime_build (the same launch's)
+ *   d_off    host, n_batches+1 entries: batch b's D is entries d_off[b] ..
+ *            d_off[b+1]-1 of l_D (toc_phys_info_get's n_codes each)
+ *   max_levels  deepest level kept, 1..4096 (sizes LDS and `level`)
+ *   cprime_status, parent, col, val, depth  toc_cprime_build's outputs
+ * Outputs (device, caller-owned):
+ *   l_parent, l_col, l_val, l_depth  at node_off[b] onwards, one entry per live
+ *            code in level order (parent as a level-order index, 0xFFFFFFFF at
+ *            depth 1); the rest of the batch's node range is left alone
+ *   level    uint32 (max_levels+1) per batch: level[d] = live codes of depth <= d
+ *   l_D      D renumbered
+ *   counts   int64 2 per batch: live codes, deepest live depth
+ *   status   int32 per batch: 0, the batch's nonzero cprime status, TOC_CPRIME_*
+ *            for a blob that does not hold, or TOC_LEVEL_* below
+ * Asynchronous on stream; the offsets are copied before returning.          */
+#define TOC_LEVEL_D 7             /* the blob's |D| differs from d_off's span       */
+#define TOC_LEVEL_DEPTH 8         /* a live code deeper than max_levels            */
+toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                           const int64_t *d_off, int64_t n_batches, int32_t max_levels,
+                           const int32_t *cprime_status, const uint32_t *parent,
+                           const uint32_t *col, const float *val, const uint32_t *depth,
+                           uint32_t *l_parent, uint32_t *l_col, float *l_val, uint32_t *l_depth,
+                           uint32_t *level, uint32_t *l_D, int64_t *counts, int32_t *status,
+                           void *ws, size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Mini-batch gradient descent (section 2.1): h <- h - lr / |B| * sum over the
  * tuples (x, y) of batch B of d loss(h, x, y) / d h, for the linear models of

@@ -25,7 +25,7 @@ TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
 TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE = 0, 1, 2
 TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(1, 5)
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
- TOC_CPRIME_NODES, TOC_CPRIME_ROWS) = range(1, 7)
+ TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH) = range(1, 9)
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -115,6 +115,8 @@ def lib():
         "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
         "toc_encode_device_workspace_size": [I64, I64, P],
         "toc_mlp_workspace_size": [P, I32, I32, I32, P],
+        "toc_level_workspace_size": [I64, I64, P],
+        "toc_level_build": [P, P, P, P, I64, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "toc_mlp_epoch": [P, I64, I64, I32, I32, I32, P, P, P, P, P, P, P, C.c_float, P, SZ, P],
         "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
     }
@@ -456,3 +458,48 @@ def toc_mlp_epoch(dev, params, labels, lr, ws, b0=0, n_batches=None, stream=None
                                _ptr(params["b2"]), _ptr(W3), _ptr(params["b3"]), _ptr(labels),
                                float(lr), _ptr(ws), ws.numel() * ws.element_size(),
                                _stream(stream)))
+
+
+def toc_level_workspace_size(n_batches, n_nodes):
+    n = C.c_size_t()
+    _check(lib().toc_level_workspace_size(int(n_batches), int(n_nodes), C.byref(n)))
+    return n.value
+
+
+def toc_level_build(blobs, blob_off, node_off, d_off, max_levels, cprime_status, parent, col,
+                    val, depth, l_parent, l_col, l_val, l_depth, level, l_D, counts, status, ws,
+                    stream=None):
+    """blobs, blob_off, node_off and the cprime_* tensors as for toc_cprime_build;
+    d_off: host int64 array of n_batches + 1 offsets into l_D; l_parent, l_col,
+    l_val, l_depth: device tensors of node_off[-1] 4-byte entries; level: device
+    int32/uint32 tensor of n_batches * (max_levels + 1); l_D: device tensor of
+    d_off[-1] entries; counts: device int64 tensor of 2 per batch; status: device
+    int32 tensor of one per batch; ws: toc_level_workspace_size bytes."""
+    blob_off, node_off, d_off = (_arr(x, np.int64) for x in (blob_off, node_off, d_off))
+    nb = blob_off.size - 1
+    if node_off.size != nb + 1 or d_off.size != nb + 1:
+        raise TocError(TOC_EINVAL, "offset arrays differ in length")
+    n = int(node_off[-1])
+    for t, name in ((parent, "parent"), (col, "col"), (val, "val"), (depth, "depth"),
+                    (l_parent, "l_parent"), (l_col, "l_col"), (l_val, "l_val"),
+                    (l_depth, "l_depth")):
+        if t.numel() < n or t.element_size() != 4:
+            raise TocError(TOC_EINVAL, f"{name} must hold {n} 4-byte entries")
+    if level.numel() < nb * (int(max_levels) + 1) or level.element_size() != 4:
+        raise TocError(TOC_EINVAL, "level must hold n_batches * (max_levels + 1) entries")
+    if l_D.numel() < int(d_off[-1]) or l_D.element_size() != 4:
+        raise TocError(TOC_EINVAL, "l_D shorter than d_off[-1]")
+    if counts.numel() < 2 * nb or counts.element_size() != 8:
+        raise TocError(TOC_EINVAL, "counts must hold 2 int64 per batch")
+    for t, name in ((status, "status"), (cprime_status, "cprime_status")):
+        if t.numel() < nb or t.element_size() != 4:
+            raise TocError(TOC_EINVAL, f"{name} must hold one int32 per batch")
+    if blobs.numel() < int(blob_off[-1]):
+        raise TocError(TOC_EINVAL, "blobs shorter than blob_off[-1]")
+    _check(lib().toc_level_build(_ptr(blobs), _ptr(blob_off), _ptr(node_off), _ptr(d_off), nb,
+                                 int(max_levels), _ptr(cprime_status), _ptr(parent), _ptr(col),
+                                 _ptr(val), _ptr(depth), _ptr(l_parent), _ptr(l_col),
+                                 _ptr(l_val), _ptr(l_depth), _ptr(level), _ptr(l_D),
+                                 _ptr(counts), _ptr(status), _ptr(ws),
+                                 ws.numel() * ws.element_size() if ws is not None else 0,
+                                 _stream(stream)))

@@ -55,6 +55,34 @@ struct Hdr {
   int err;
 };
 
+// Reads the five array headers of a blob of `size` bytes and checks that the
+// arrays fill it exactly (widths 1..4, unique values 4 bytes wide, as many value
+// indexes as columns, at least one tuple start, at most max_rows tuples); h.err
+// gets TOC_CPRIME_LAYOUT or TOC_CPRIME_ROWS, else 0.  Every later read of an array
+// stays inside the blob.
+__device__ void parse_headers(const uint8_t *blob, uint64_t size, int max_rows, Hdr &h) {
+  int err = 0;
+  uint64_t pos = 0;
+  for (int a = 0; a < 5 && !err; ++a) {
+    if (size < pos + 5) {
+      err = TOC_CPRIME_LAYOUT;
+      break;
+    }
+    const uint32_t cnt = rd(blob + pos, 0, 4), w = blob[pos + 4];
+    if (w < 1 || w > 4 || (a == 1 && w != 4) || (size - pos - 5) / w < cnt) {
+      err = TOC_CPRIME_LAYOUT;
+      break;
+    }
+    h.cnt[a] = cnt;
+    h.w[a] = w;
+    h.data[a] = (uint32_t)(pos + 5);
+    pos += 5 + (uint64_t)cnt * w;
+  }
+  if (!err && (pos != size || h.cnt[2] != h.cnt[0] || h.cnt[4] < 1)) err = TOC_CPRIME_LAYOUT;
+  if (!err && h.cnt[4] - 1 > (uint32_t)max_rows) err = TOC_CPRIME_ROWS;
+  h.err = err;
+}
+
 __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
     const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
     int max_rows, uint32_t *__restrict__ parent, uint32_t *__restrict__ col,
@@ -74,26 +102,7 @@ __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
     const uint32_t n_decl = (uint32_t)(node_off[b + 1] - no);   // nodes node_off gives the batch
     // headers, read by one thread; every later read stays inside the arrays
     if (threadIdx.x == 0) {
-      int err = 0;
-      uint64_t pos = 0;
-      for (int a = 0; a < 5 && !err; ++a) {
-        if (size < pos + 5) {
-          err = TOC_CPRIME_LAYOUT;
-          break;
-        }
-        const uint32_t cnt = rd(blob + pos, 0, 4), w = blob[pos + 4];
-        if (w < 1 || w > 4 || (a == 1 && w != 4) || (size - pos - 5) / w < cnt) {
-          err = TOC_CPRIME_LAYOUT;
-          break;
-        }
-        h.cnt[a] = cnt;
-        h.w[a] = w;
-        h.data[a] = (uint32_t)(pos + 5);
-        pos += 5 + (uint64_t)cnt * w;
-      }
-      if (!err && (pos != size || h.cnt[2] != h.cnt[0] || h.cnt[4] < 1)) err = TOC_CPRIME_LAYOUT;
-      if (!err && h.cnt[4] - 1 > (uint32_t)max_rows) err = TOC_CPRIME_ROWS;
-      h.err = err;
+      parse_headers(blob, size, max_rows, h);
       errs = 0;
     }
     __syncthreads();
@@ -223,6 +232,153 @@ __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
   }
 }
 
+// The live codes of each batch in level order, from the tree toc_cprime_build made
+// (parent, key, depth per node) and the blob's D: codes of D and their ancestors
+// are marked live (a walk up from each entry of D stops at the first node another
+// walk already marked, so each node is passed once); live codes are counted per
+// depth, and each gets its place in the stable (depth, index) order from a
+// per-depth running count, chunk by chunk in index order with the waves of a
+// chunk taking turns; parents and D are then renumbered.
+constexpr int kLvBlock = 512;
+constexpr int kLvWaves = kLvBlock / kCpWave;
+constexpr int kLvMaxLevels = 4096;
+
+__global__ __launch_bounds__(kLvBlock) void level_kernel(
+    const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
+    int max_levels, const int32_t *__restrict__ cp_status, const uint32_t *__restrict__ parent,
+    const uint32_t *__restrict__ col, const uint32_t *__restrict__ val,
+    const uint32_t *__restrict__ depth, uint32_t *__restrict__ l_parent,
+    uint32_t *__restrict__ l_col, uint32_t *__restrict__ l_val, uint32_t *__restrict__ l_depth,
+    uint32_t *__restrict__ level, uint32_t *__restrict__ l_D, int64_t *__restrict__ counts,
+    int32_t *__restrict__ status, uint32_t *__restrict__ live, uint32_t *__restrict__ newidx) {
+  extern __shared__ uint32_t run[];            // per depth: live codes placed so far
+  __shared__ Hdr h;
+  __shared__ int errs;
+  __shared__ uint32_t n_lv;
+  const int64_t *node_off = offs + (n_batches + 1), *d_off = offs + 2 * (n_batches + 1);
+  const int lane = threadIdx.x % kCpWave, wave = threadIdx.x / kCpWave;
+  for (int64_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
+    const uint8_t *blob = blobs + offs[b];
+    const uint64_t size = (uint64_t)(offs[b + 1] - offs[b]);
+    const int64_t no = node_off[b], dof = d_off[b];
+    const uint32_t n_nodes = (uint32_t)(node_off[b + 1] - no);
+    if (threadIdx.x == 0) {
+      h.err = cp_status[b];
+      if (h.err == 0) parse_headers(blob, size, 1 << 30, h);
+      if (h.err == 0 && (int64_t)h.cnt[3] != d_off[b + 1] - dof) h.err = TOC_LEVEL_D;
+      errs = 0;
+    }
+    __syncthreads();
+    if (h.err) {
+      if (threadIdx.x == 0) {
+        status[b] = h.err;
+        counts[2 * b] = counts[2 * b + 1] = 0;
+      }
+      __syncthreads();
+      continue;
+    }
+    const uint32_t nD = h.cnt[3], w_d = h.w[3];
+    const uint8_t *p_d = blob + h.data[3];
+    for (uint32_t c = threadIdx.x; c < n_nodes; c += kLvBlock) live[no + c] = 0u;
+    for (int d = threadIdx.x; d <= max_levels; d += kLvBlock) run[d] = 0u;
+    __threadfence();
+    __syncthreads();
+    // live marking: a walk up from every entry of D
+    for (uint32_t p = threadIdx.x; p < nD; p += kLvBlock) {
+      uint32_t c = rd(p_d, p, w_d);
+      if (c == 0u || c >= n_nodes) {
+        atomicOr(&errs, 1);
+        continue;
+      }
+      while (c != 0u && atomicOr(&live[no + c], 1u) == 0u) c = parent[no + c];
+    }
+    __threadfence();
+    __syncthreads();
+    if (errs) {
+      if (threadIdx.x == 0) {
+        status[b] = TOC_CPRIME_CODE;
+        counts[2 * b] = counts[2 * b + 1] = 0;
+      }
+      __syncthreads();
+      continue;
+    }
+    // live codes per depth
+    for (uint32_t c = 1 + threadIdx.x; c < n_nodes; c += kLvBlock) {
+      if (!__hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
+      const uint32_t d = depth[no + c];
+      if (d == 0u || d > (uint32_t)max_levels) atomicOr(&errs, 2);
+      else atomicAdd(&run[d], 1u);
+    }
+    __syncthreads();
+    if (errs) {
+      if (threadIdx.x == 0) {
+        status[b] = TOC_LEVEL_DEPTH;
+        counts[2 * b] = counts[2 * b + 1] = 0;
+      }
+      __syncthreads();
+      continue;
+    }
+    // level offsets; run[d] becomes the first place of depth d
+    if (threadIdx.x == 0) {
+      uint32_t *lv = level + b * (int64_t)(max_levels + 1);
+      uint32_t acc = 0, top = 0;
+      lv[0] = 0u;
+      for (int d = 1; d <= max_levels; ++d) {
+        const uint32_t n = run[d];
+        run[d] = acc;
+        acc += n;
+        if (n) top = (uint32_t)d;
+        lv[d] = acc;
+      }
+      n_lv = acc;
+      counts[2 * b] = acc;
+      counts[2 * b + 1] = top;
+    }
+    __syncthreads();
+    // places in (depth, index) order: chunks of kLvBlock nodes in index order, the
+    // waves of a chunk one after another, lanes of one depth ranked by a ballot
+    for (uint32_t c0 = 1; c0 < n_nodes; c0 += kLvBlock) {
+      const uint32_t c = c0 + threadIdx.x;
+      const bool in = c < n_nodes &&
+                      __hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t d = in ? depth[no + c] : 0u;
+      for (int w = 0; w < kLvWaves; ++w) {
+        if (wave == w) {
+          bool todo = in;
+          uint64_t left = __ballot(todo);
+          while (left) {
+            const int leader = __ffsll((unsigned long long)left) - 1;
+            const uint32_t dd = (uint32_t)__shfl((int)d, leader, kCpWave);
+            const bool mine = todo && d == dd;
+            const uint64_t m = __ballot(mine);
+            if (mine) {
+              newidx[no + c] = run[dd] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+              todo = false;
+            }
+            if (lane == leader) run[dd] += (uint32_t)__popcll(m);
+            left = __ballot(todo);
+          }
+        }
+        __syncthreads();
+      }
+    }
+    __threadfence();
+    __syncthreads();
+    // the live codes at their places, parents renumbered; D renumbered
+    for (uint32_t c = 1 + threadIdx.x; c < n_nodes; c += kLvBlock) {
+      if (!__hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
+      const uint32_t i = newidx[no + c], d = depth[no + c];
+      l_parent[no + i] = d == 1u ? kNone : newidx[no + parent[no + c]];
+      l_col[no + i] = col[no + c];
+      l_val[no + i] = val[no + c];
+      l_depth[no + i] = d;
+    }
+    for (uint32_t p = threadIdx.x; p < nD; p += kLvBlock) l_D[dof + p] = newidx[no + rd(p_d, p, w_d)];
+    if (threadIdx.x == 0) status[b] = 0;
+    __syncthreads();
+  }
+}
+
 inline int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 int64_t ws_nodes_offset(int64_t n_batches) { return align256(16 * (n_batches + 1)); }
@@ -286,6 +442,69 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
                      a1, d1, nx);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "cprime_kernel: %s", hipGetErrorString(e));
+  return TOC_OK;
+}
+
+toc_status toc_level_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *bytes) {
+  clear_error();
+  if (!bytes || n_batches < 0 || n_nodes < 0) return fail(TOC_EINVAL, "bad argument");
+  *bytes = (size_t)(align256(24 * (n_batches + 1)) + 2 * align256(4 * n_nodes));
+  return TOC_OK;
+}
+
+toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                           const int64_t *d_off, int64_t n_batches, int32_t max_levels,
+                           const int32_t *cprime_status, const uint32_t *parent,
+                           const uint32_t *col, const float *val, const uint32_t *depth,
+                           uint32_t *l_parent, uint32_t *l_col, float *l_val, uint32_t *l_depth,
+                           uint32_t *level, uint32_t *l_D, int64_t *counts, int32_t *status,
+                           void *ws, size_t ws_bytes, void *stream) {
+  clear_error();
+  if (n_batches < 0) return fail(TOC_EINVAL, "n_batches < 0");
+  if (n_batches == 0) return TOC_OK;
+  if (!blob_off || !node_off || !d_off || !cprime_status || !status || !counts || !level || !ws)
+    return fail(TOC_EINVAL, "NULL argument");
+  if (max_levels < 1 || max_levels > kLvMaxLevels)
+    return fail(TOC_EUNSUPPORTED, "max_levels %d outside 1..%d", max_levels, kLvMaxLevels);
+  if (blob_off[0] < 0 || node_off[0] < 0 || d_off[0] < 0) return fail(TOC_EINVAL, "negative offset");
+  for (int64_t b = 0; b < n_batches; ++b) {
+    if (blob_off[b + 1] < blob_off[b] || blob_off[b + 1] - blob_off[b] > (int64_t)UINT32_MAX)
+      return fail(TOC_EINVAL, "blob_off not non-decreasing or a blob of 4 GiB or more at %lld",
+                  (long long)b);
+    if (node_off[b + 1] <= node_off[b] || node_off[b + 1] - node_off[b] > (int64_t)INT32_MAX)
+      return fail(TOC_EINVAL, "node_off[%lld] does not give 1..2^31-1 nodes", (long long)b);
+    if (d_off[b + 1] < d_off[b]) return fail(TOC_EINVAL, "d_off not non-decreasing at %lld", (long long)b);
+  }
+  const int64_t n_nodes = node_off[n_batches];
+  if (!parent || !col || !val || !depth || !l_parent || !l_col || !l_val || !l_depth)
+    return fail(TOC_EINVAL, "NULL node array");
+  if (d_off[n_batches] > 0 && !l_D) return fail(TOC_EINVAL, "l_D is NULL");
+  if (blob_off[n_batches] > 0 && !blobs) return fail(TOC_EINVAL, "blobs is NULL");
+  size_t need = 0;
+  toc_level_workspace_size(n_batches, n_nodes, &need);
+  if (ws_bytes < need) return fail(TOC_ESIZE, "workspace of %zu bytes below the %zu needed", ws_bytes, need);
+  hipStream_t s = (hipStream_t)stream;
+  int64_t *offs = (int64_t *)ws;
+  const size_t ob = 8 * (size_t)(n_batches + 1);
+  if (hipMemcpyAsync(offs, blob_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + n_batches + 1, node_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + 2 * (n_batches + 1), d_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(TOC_EDEVICE, "copy of the offsets failed");
+  uint8_t *base = (uint8_t *)ws + align256(24 * (n_batches + 1));
+  uint32_t *live = (uint32_t *)base, *newidx = (uint32_t *)(base + align256(4 * n_nodes));
+  const size_t lds = 4 * ((size_t)max_levels + 1);
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute((const void *)level_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)lds) != hipSuccess)
+    return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
+  const unsigned g = (unsigned)std::min<int64_t>(n_batches, 1 << 20);
+  hipLaunchKernelGGL(level_kernel, dim3(g), dim3(kLvBlock), lds, s, (const uint8_t *)blobs, offs,
+                     n_batches, (int)max_levels, cprime_status, parent, col, (const uint32_t *)val,
+                     depth, l_parent, l_col, (uint32_t *)l_val, l_depth, level, l_D, counts,
+                     status, live, newidx);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOC_EDEVICE, "level_kernel: %s", hipGetErrorString(e));
   return TOC_OK;
 }
 

@@ -1,0 +1,165 @@
+"""GPU parity of the device level order (live codes of D and their ancestors,
+stably sorted by (depth, index), parents and D renumbered) built from the tree of
+toc_cprime_build, with the oracle's level_order on the oracle's unpacking of the
+same physical bytes: every array equal, bit for bit; malformed inputs get their
+status without disturbing the other batches of a launch."""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle as O
+import paper_1702_06943_amd as T
+from workloads import Batches, config_batches, tiny_batch
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLD = json.load(open(os.path.join(HERE, "golden", "worked_example.json")))
+PHYS = json.load(open(os.path.join(HERE, "golden", "physical_worked_example.json")))
+NONE = 0xFFFFFFFF
+
+
+def blobs_of(B):
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    return [T.toc_enc_pack(e) for e in encs]
+
+
+def level_gpu(blobs, max_levels=64, d_counts=None):
+    """toc_cprime_build then toc_level_build over the blobs in one launch each;
+    returns per batch (parent, col, val bits, depth, level offsets, D) host arrays
+    or None where the status is nonzero, and the status array."""
+    infos = [T.toc_phys_info_get(b) for b in blobs]
+    nb = len(blobs)
+    blob_off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
+    node_off = np.concatenate([[0], np.cumsum([i["n_nodes"] for i in infos])]).astype(np.int64)
+    if d_counts is None:
+        d_counts = [i["n_codes"] for i in infos]
+    d_off = np.concatenate([[0], np.cumsum(d_counts)]).astype(np.int64)
+    max_rows = max([i["n_rows"] for i in infos] + [0])
+    dblob = torch.from_numpy(np.concatenate([np.asarray(b, np.uint8) for b in blobs]
+                                            + [np.zeros(1, np.uint8)])).to(DEV)
+    n = int(node_off[-1])
+    cp = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
+    cst = torch.full((nb,), -1, dtype=torch.int32, device=DEV)
+    ws = torch.empty(T.toc_cprime_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
+    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, cp[0], cp[1], cp[2], cp[3], cst, ws)
+    lv = [torch.full((n,), -7, dtype=torch.int32, device=DEV) for _ in range(4)]
+    level = torch.full((nb * (max_levels + 1),), -7, dtype=torch.int32, device=DEV)
+    lD = torch.full((max(int(d_off[-1]), 1),), -7, dtype=torch.int32, device=DEV)
+    counts = torch.full((2 * nb,), -7, dtype=torch.int64, device=DEV)
+    st = torch.full((nb,), -1, dtype=torch.int32, device=DEV)
+    ws2 = torch.empty(T.toc_level_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
+    T.toc_level_build(dblob, blob_off, node_off, d_off, max_levels, cst, cp[0], cp[1], cp[2],
+                      cp[3], lv[0], lv[1], lv[2], lv[3], level, lD, counts, st, ws2)
+    torch.cuda.synchronize()
+    host = [x.cpu().numpy().view(np.uint32) for x in lv]
+    level = level.cpu().numpy().view(np.uint32).reshape(nb, max_levels + 1)
+    lD = lD.cpu().numpy().view(np.uint32)
+    counts, st = counts.cpu().numpy().reshape(nb, 2), st.cpu().numpy()
+    per = []
+    for b in range(nb):
+        if st[b] != 0:
+            per.append(None)
+            continue
+        n_live, top = int(counts[b, 0]), int(counts[b, 1])
+        o = int(node_off[b])
+        per.append(tuple(h[o:o + n_live] for h in host)
+                   + (level[b, :top + 1], lD[d_off[b]:d_off[b + 1]]))
+    return per, st
+
+
+def assert_same(got, blob):
+    I, D = O.unpack_physical(bytes(blob))
+    lo = O.level_order(I, D)
+    parent, col, val, depth, level, lD = got
+    assert parent.tolist() == [NONE if p is None else p for p in lo["parent"]]
+    assert col.tolist() == [k[0] for k in lo["key"]]
+    assert val.tolist() == [k[1] for k in lo["key"]]
+    assert depth.tolist() == lo["depth"]
+    assert level.tolist() == lo["level_off"]
+    assert lD.tolist() == [c for d in lo["D"] for c in d]
+
+
+def test_worked_example():
+    blob = np.frombuffer(bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"])), np.uint8)
+    (got,), st = level_gpu([blob])
+    assert st.tolist() == [0]
+    want = GOLD["level_order"]
+    assert got[3].tolist() == want["depth"]
+    assert got[4].tolist() == want["level_off"]
+    assert got[5].tolist() == [c for d in want["D"] for c in d]
+    assert got[0].tolist() == [NONE if p is None else p for p in want["parent"]]
+    assert_same(got, blob)
+
+
+TINY = [dict(n_rows=0, density=0.5, n_values=2),
+        dict(n_rows=5, density=0.0, n_values=2),
+        dict(n_rows=1, density=1.0, n_values=1),
+        dict(n_rows=40, density=0.3, n_values=3, prefix_copy=0.6),
+        dict(n_rows=9, density=0.05, n_values=2),
+        dict(n_rows=300, density=0.9, n_values=1, prefix_copy=0.9),
+        dict(n_rows=250, density=1.0, n_values=2, prefix_copy=0.5)]
+
+
+def test_tiny_batches_one_launch():
+    blobs = []
+    for n_cols in (3, 64, 400):
+        for i, spec in enumerate(TINY):
+            rp, c, v = tiny_batch(800 + i + n_cols, n_cols=n_cols, zeros=(i % 2 == 1), **spec)
+            blobs += blobs_of(Batches(n_cols, [spec["n_rows"]], rp, c, v))
+    per, st = level_gpu(blobs, max_levels=512)
+    assert st.tolist() == [0] * len(blobs)
+    for got, blob in zip(per, blobs):
+        assert_same(got, blob)
+
+
+@pytest.mark.parametrize("cfg,first,nb", [("c1", 0, 1), ("c2", 3, 3), ("c3", 5, 2),
+                                          ("c4", 0, 1), ("c5", 11, 8)])
+def test_config_batches(cfg, first, nb):
+    blobs = blobs_of(config_batches(cfg, first, nb))
+    per, st = level_gpu(blobs)
+    assert st.tolist() == [0] * nb
+    for got, blob in zip(per, blobs):
+        assert_same(got, blob)
+
+
+def test_statuses():
+    """A batch deeper than max_levels, a d_off span that is not the blob's |D| and
+    a blob cut short: each gets its status, the good batches their level order."""
+    good = blobs_of(config_batches("c5", 0, 2))
+    deep = blobs_of(config_batches("c1", 0, 1))               # depth 41 > 8
+    bad = np.asarray(good[0][:-3], np.uint8)                  # malformed: cprime rejects it
+    blobs = [good[0], deep[0], good[1], bad]
+    d_counts = [T.toc_phys_info_get(b)["n_codes"] for b in blobs[:3]] + [0]
+    # the malformed blob has no |D| of its own: give it 0 entries
+    per, st = level_gpu_checked(blobs, d_counts)
+    assert st[0] == 0 and st[2] == 0
+    assert st[1] == T.TOC_LEVEL_DEPTH
+    assert st[3] == T.TOC_CPRIME_LAYOUT
+    assert_same(per[0], good[0])
+    assert_same(per[2], good[1])
+    # |D| of batch 1 declared one short
+    d2 = [T.toc_phys_info_get(b)["n_codes"] for b in good]
+    per, st = level_gpu(good, d_counts=[d2[0], d2[1] - 1])
+    assert st.tolist() == [0, T.TOC_LEVEL_D]
+    assert_same(per[0], good[0])
+
+
+def level_gpu_checked(blobs, d_counts):
+    """level_gpu for a list holding a malformed last blob: its node count is taken
+    as 1 (the cprime status marks it; nothing of its range is read)."""
+    real_info = T.toc_phys_info_get
+    def info(b):
+        try:
+            return real_info(b)
+        except T.TocError:
+            return {"n_nodes": 1, "n_rows": 0, "n_codes": 0}
+    T.toc_phys_info_get = info
+    try:
+        return level_gpu(blobs, max_levels=8, d_counts=d_counts)
+    finally:
+        T.toc_phys_info_get = real_info
