@@ -127,8 +127,8 @@ __device__ inline float coherent_load(const float *p) {
 
 // Right multiplication (Theorem 1, Algorithm 4): H level by level, then one
 // group of LPR lanes per tuple sums H over the tuple's codes.
-template <int LPR>
-__global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
+template <int LPR, int BLK>
+__global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
                                                           const float *__restrict__ W,
                                                           int64_t ldw, float *__restrict__ R,
                                                           int64_t ldr) {
@@ -140,7 +140,8 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   const NodeVal val{im.key + bt.code_base};
   for (int d = 1; d <= bt.n_levels; ++d) {
     const uint32_t a = lvl[d - 1], e = lvl[d];
-    for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
+#pragma unroll 4
+    for (uint32_t c = a + threadIdx.x; c < e; c += BLK) {
       const float base = d > 1 ? H[par[c]] : 0.0f;
       H[c] = fmaf(val[c], W[(int64_t)col[c] * ldw], base);
     }
@@ -149,9 +150,10 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
-  for (int r = grp; r < bt.n_rows; r += kBlock / LPR) {
+  for (int r = grp; r < bt.n_rows; r += BLK / LPR) {
     const uint32_t s = span[r], e = span[r + 1];
     float acc = 0.0f;
+#pragma unroll 4
     for (uint32_t j = s + lane; j < e; j += LPR) acc += H[dc[j]];
     acc = group_sum<LPR>(acc);
     if (lane == 0) R[(bt.row_base + r) * ldr] = acc;
@@ -168,6 +170,9 @@ __global__ __launch_bounds__(kBlock) void right_k1_kernel(Img im, int64_t b0,
 // over the column's leaves (a contiguous range of positions) and tree codes (a
 // contiguous stretch of the tree list), both read from the image's column index.
 constexpr uint32_t kFirstOccK1 = 0x80000000u;
+// Workgroup of the k = 1 right product: small, so that many batches (each a chain
+// of dependent loads and barriers) are in flight on a CU at once.
+constexpr int kK1RightBlock = 256;
 constexpr int kK1Codes = 4;      // codes per thread and pass
 constexpr int kK1Occ = 4;        // occurrences per code loaded together
 constexpr int kK1Cols = 8;       // output columns per thread and pass
@@ -2012,11 +2017,16 @@ toc_status allow_lds(K kernel, size_t bytes) {
   return TOC_OK;
 }
 
+// Lanes that sum one tuple in the k = 1 right product: few, so that a workgroup
+// sums many tuples at once and each lane has several independent code loads in
+// flight (a tuple of c codes takes about c / lanes steps plus log2(lanes) for the
+// reduction, and the tuples of a batch take rows / (256 / lanes) rounds).
 int lanes_per_row(const toc_dev *d) {
   const double avg = d->info.n_rows ? (double)d->info.n_codes / (double)d->info.n_rows : 0.0;
-  if (avg <= 12) return 8;
-  if (avg <= 24) return 16;
-  if (avg <= 48) return 32;
+  if (avg <= 40) return 4;
+  if (avg <= 64) return 8;
+  if (avg <= 160) return 16;
+  if (avg <= 400) return 32;
   return 64;
 }
 
@@ -2279,14 +2289,18 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
       switch (lpr) {
-        case 8: if ((st = allow_lds(right_k1_kernel<8>, lds))) return st;
-          hipLaunchKernelGGL(right_k1_kernel<8>, dim3(g), dim3(kBlock), lds, s, im, b0, W, ldw, R, ldr); break;
-        case 16: if ((st = allow_lds(right_k1_kernel<16>, lds))) return st;
-          hipLaunchKernelGGL(right_k1_kernel<16>, dim3(g), dim3(kBlock), lds, s, im, b0, W, ldw, R, ldr); break;
-        case 32: if ((st = allow_lds(right_k1_kernel<32>, lds))) return st;
-          hipLaunchKernelGGL(right_k1_kernel<32>, dim3(g), dim3(kBlock), lds, s, im, b0, W, ldw, R, ldr); break;
-        default: if ((st = allow_lds(right_k1_kernel<64>, lds))) return st;
-          hipLaunchKernelGGL(right_k1_kernel<64>, dim3(g), dim3(kBlock), lds, s, im, b0, W, ldw, R, ldr); break;
+#define TOC_RK1(L)                                                                         \
+  case L:                                                                                  \
+    if ((st = allow_lds(right_k1_kernel<L, kK1RightBlock>, lds))) return st;               \
+    hipLaunchKernelGGL((right_k1_kernel<L, kK1RightBlock>), dim3(g), dim3(kK1RightBlock), lds, s, \
+                       im, b0, W, ldw, R, ldr);                                            \
+    break;
+        TOC_RK1(4)
+        TOC_RK1(8)
+        TOC_RK1(16)
+        TOC_RK1(32)
+        default: TOC_RK1(64)
+#undef TOC_RK1
       }
       if ((st = launch_status("right_k1_kernel"))) return st;
     }
