@@ -222,6 +222,7 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
 #pragma unroll
       for (int v = 0; v < kK1Occ; ++v)
         if (w[u][v] != 0xFFFFFFFFu) s[u] += Gs[w[u][v] & ~kFirstOccK1];
+#pragma unroll 8
       for (uint32_t o = o0[u] + kK1Occ; o < o1[u]; ++o) s[u] += Gs[orow[o] & ~kFirstOccK1];
     }
 #pragma unroll
