@@ -74,6 +74,25 @@ def cpu_baseline(pool, workers, cfg, nb, k, budget_s):
     }
 
 
+def cpu_baseline_single(cfg, nb, k, budget_s):
+    """The same oracle work on one core, in this process: batches evenly spaced
+    over the workload until about budget_s seconds of it are done."""
+    from threadpoolctl import threadpool_limits
+    t_all, nnz, done = 0.0, 0, 0
+    ids = np.linspace(0, nb - 1, min(nb, 400)).astype(int).tolist()
+    with threadpool_limits(limits=1):                 # numpy's BLAS on one thread too
+        for b in ids:
+            t, z = _oracle_batch((cfg, b, k))
+            t_all += t
+            nnz += z
+            done += 1
+            if t_all >= budget_s:
+                break
+    return {"value": nnz / t_all, "unit": "nnz/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} mini-batches evenly spaced over the workload, one process; "
+                      f"{t_all:.1f} s of oracle time"}
+
+
 def host_cpu():
     try:
         for line in open("/proc/cpuinfo"):
@@ -446,6 +465,28 @@ def time_mlp(w, stream, n_steps, h1=200, h2=50, n_out=10, lr=0.1):
     return res
 
 
+def measured_copy_bandwidth(stream, mib=4096, reps=5):
+    """Bytes moved per second (read + write) by a plain device-to-device copy of
+    `mib` MiB, the best of `reps`: the HBM rate a streaming kernel can reach here."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        dst.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * n * 4 / (best / 1e3)
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     for f in ("toc_device.hip", "toc_host.cpp", "toc_internal.h"):
@@ -511,11 +552,13 @@ def main():
 
     # everything that forks happens before the GPU is touched
     pool = make_pool(workers)
-    cpu = None
+    cpu = cpu1 = None
     if args.cpu_seconds > 0:
         log(f"oracle CPU baseline on {workers} processes ...")
         cpu = cpu_baseline(pool, workers, cfg, nb, k, args.cpu_seconds)
         log(f"oracle: {cpu['value']:.3e} nnz/s ({cpu['sample']})")
+        cpu1 = cpu_baseline_single(cfg, nb, k, args.cpu_seconds / 3)
+        log(f"oracle on one core: {cpu1['value']:.3e} nnz/s ({cpu1['sample']})")
     w = encode_workload(cfg, nb, pool,
                         keep_batches=0 if args.no_extras else args.encode_batches)
     pool.close()
@@ -561,6 +604,7 @@ def main():
         log(f"copy calibration: 3 copies of {n * 4} bytes")
         del src, dst
 
+    copy_bw = measured_copy_bandwidth(stream)
     info = w.info
     extras = None if args.no_extras else time_elementwise(w, stream)
     cprime = time_cprime(sample, stream) if sample else None
@@ -589,6 +633,8 @@ def main():
             "hbm_frac_compressed": canon / t / HBM_PEAK,
             "hbm_frac_whole_op": (canon + dense[op]) / t / HBM_PEAK,
             "tflops": flops[op] / t / 1e12,
+            "frac_of_measured_copy_compressed": canon / t / copy_bw,
+            "frac_of_measured_copy_whole_op": (canon + dense[op]) / t / copy_bw,
         }
     dom = max(("right", "left", "decode"), key=lambda o: op_ms[o])
     t_dom = op_ms[dom] / 1e3
@@ -636,6 +682,8 @@ def main():
         "encode_device": encode_dev,
         "ablation_sizes": ablation,
         "cpu_baseline": cpu,
+        "cpu_baseline_single_thread": cpu1,
+        "measured_copy_GBps": copy_bw / 1e9,
         "host": {"encode_s": round(w.encode_s, 2), "upload_s": round(w.upload_s, 2),
                  "cpu": host_cpu()},
     }
