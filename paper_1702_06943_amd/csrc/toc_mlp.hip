@@ -124,9 +124,10 @@ __global__ __launch_bounds__(kNnBlock) void mlp_fwd1_kernel(NnImg im, int64_t b,
 // gradient of the mean loss back to dZ1: every quantity here belongs to one tuple,
 // so workgroups split the tuples.  H2, dZ2 and dZ3 go to the workspace for the
 // weight gradients, dZ1 for the first layer's left product.
+template <bool kWlds>
 __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
     int n, int R, int64_t row_base, const float *__restrict__ act1, int h1, int h2, int C,
-    const float *__restrict__ W2, const float *__restrict__ b2, const float *__restrict__ W3,
+    const float *__restrict__ W2g, const float *__restrict__ b2, const float *__restrict__ W3g,
     const float *__restrict__ b3, const int32_t *__restrict__ labels, float *__restrict__ H2g,
     float *__restrict__ dZ2g, float *__restrict__ dZ3g, float *__restrict__ dz1) {
   extern __shared__ float sm[];
@@ -134,9 +135,16 @@ __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
   float *H = A + R * h1;               // R x h2
   float *G = H + R * h2;               // R x h2: dZ2
   float *Z = G + R * h2;               // R x C: Z3, then dZ3
+  // W2 and W3 staged in LDS when they fit (kWlds), else read from global memory
+  float *W2s = Z + R * C, *W3s = W2s + h1 * h2;
+  const float *W2 = kWlds ? W2s : W2g, *W3 = kWlds ? W3s : W3g;
   const int i0 = R * blockIdx.x, nr = min(R, n - i0);
   for (int idx = threadIdx.x; idx < nr * h1; idx += kNnBlock)
     A[idx] = act1[(int64_t)i0 * h1 + idx];
+  if (kWlds) {
+    for (int idx = threadIdx.x; idx < h1 * h2; idx += kNnBlock) W2s[idx] = W2g[idx];
+    for (int idx = threadIdx.x; idx < h2 * C; idx += kNnBlock) W3s[idx] = W3g[idx];
+  }
   __syncthreads();
   for (int idx = threadIdx.x; idx < nr * h2; idx += kNnBlock) {
     const int i = idx / h2, u = idx - i * h2;
@@ -461,7 +469,10 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   const size_t lds_f = rw.deep_global ? 0 : (size_t)std::max<int64_t>(rw.max_deep, 1) * 16;
   const size_t lds_b = rw.tree_global ? 0 : (size_t)std::max<int64_t>(rw.max_tree, 1) * 16;
   const int R = rows_per_group(h1, h2, n_out);
-  const size_t lds_r = (size_t)R * (h1 + 2 * h2 + n_out) * 4;
+  const size_t lds_r0 = (size_t)R * (h1 + 2 * h2 + n_out) * 4;
+  const size_t lds_w = ((size_t)h1 * h2 + (size_t)h2 * n_out) * 4;
+  const bool w_lds = lds_r0 + lds_w <= 96 * 1024;
+  const size_t lds_r = lds_r0 + (w_lds ? lds_w : 0);
   const int gU = std::min(h2, 256), gV = 256 / gU;
   const int n_w2 = ((h1 + gV - 1) / gV) * ((h2 + gU - 1) / gU);
   const int n_w3 = ((h2 + 1) * n_out + 255) / 256;
@@ -471,7 +482,8 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   toc_status st;
   if ((st = allow((const void *)mlp_fwd1_kernel<false>, lds_f)) ||
       (st = allow((const void *)mlp_bwd1_kernel<false>, lds_b)) ||
-      (st = allow((const void *)mlp_rows_kernel, lds_r)) ||
+      (st = allow(w_lds ? (const void *)mlp_rows_kernel<true> : (const void *)mlp_rows_kernel<false>,
+                  lds_r)) ||
       (st = allow((const void *)mlp_grad_kernel, lds_g)))
     return st;
   const uint8_t *base = (const uint8_t *)d->buf;
@@ -505,9 +517,14 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
     else
       hipLaunchKernelGGL(mlp_fwd1_kernel<false>, dim3(slices, row_groups), dim3(kNnBlock), lds_f, s, im, b, W1,
                          h1, b1, act1, nullptr, 0);
-    hipLaunchKernelGGL(mlp_rows_kernel, dim3((unsigned)((bt.n_rows + R - 1) / R)), dim3(kNnBlock),
-                       lds_r, s, bt.n_rows, R, bt.row_base, act1, h1, h2, n_out, W2, b2, W3, b3,
-                       labels, H2g, dZ2g, dZ3g, dz1);
+    if (w_lds)
+      hipLaunchKernelGGL(mlp_rows_kernel<true>, dim3((unsigned)((bt.n_rows + R - 1) / R)),
+                         dim3(kNnBlock), lds_r, s, bt.n_rows, R, bt.row_base, act1, h1, h2, n_out,
+                         W2, b2, W3, b3, labels, H2g, dZ2g, dZ3g, dz1);
+    else
+      hipLaunchKernelGGL(mlp_rows_kernel<false>, dim3((unsigned)((bt.n_rows + R - 1) / R)),
+                         dim3(kNnBlock), lds_r, s, bt.n_rows, R, bt.row_base, act1, h1, h2, n_out,
+                         W2, b2, W3, b3, labels, H2g, dZ2g, dZ3g, dz1);
     hipLaunchKernelGGL(mlp_grad_kernel, dim3((unsigned)(n_w2 + n_w3)), dim3(256), lds_g, s, bt.n_rows, n_w2,
                        act1, h1, h2, n_out, H2g, dZ2g, dZ3g, lr, W2, b2, W3, b3);
     if (rw.tree_global)

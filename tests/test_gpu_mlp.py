@@ -91,6 +91,8 @@ CASES = {
     "mixed_softmax": (lambda: mixed_set(16), 12, 5, 4, 0.3),
     "mixed_sigmoid": (lambda: mixed_set(16), 4, 1, 1, 0.3),
     "deep_rows_in_workspace": (deep_set, 8, 4, 3, 0.05),
+    # W2 and W3 too large to stage in LDS beside the tuples: read from global memory
+    "wide_hidden": (lambda: config_batches("c5", 3, 2), 400, 60, 3, 0.05),
 }
 
 
