@@ -472,7 +472,7 @@ toc_status toc_mgd_epoch(const toc_dev *dev, int64_t b0, int64_t n_batches, int3
 
 /* Workspace bytes of toc_mlp_epoch: 4 (most rows of a batch) (2 h1 + 2 h2 +
  * n_out) (each part rounded up to 4 floats), plus, when 16 bytes per code exceed
- * 160 KiB of LDS (those table rows are then kept in the workspace), 16 h1 per
+ * 160 KiB of LDS (those table rows are then kept in the workspace), 32 h1 per
  * tree code of the batch with the most and 4 h1 ceil(max rows / 64) per deep
  * code of the batch with the most. */
 toc_status toc_mlp_workspace_size(const toc_dev *dev, int32_t h1, int32_t h2, int32_t n_out,

@@ -26,7 +26,7 @@ constexpr int kNnBlock = 1024;
 constexpr int kNnLanes = 16;                 // lanes per tuple in the forward product
 constexpr uint32_t kNnFirst = 0x80000000u;   // first-occurrence bit of occ_row
 constexpr size_t kNnLdsMax = 160 * 1024;
-constexpr int kColGroups = 4;                // workgroups sharing a slice's key columns
+constexpr int kColGroups = 8;                // workgroups sharing a slice's key columns
 
 struct NnImg {
   const toc_batch *batches;
