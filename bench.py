@@ -228,7 +228,7 @@ def pack_sample(w, n):
     idx = np.linspace(0, len(w.encs) - 1, min(n, len(w.encs))).astype(np.int64)
     t0 = time.perf_counter()
     blobs = [T.toc_enc_pack(w.encs[i]) for i in idx]
-    return {"blobs": blobs, "pack_s": time.perf_counter() - t0}
+    return {"blobs": blobs, "pack_s": time.perf_counter() - t0, "cfg": w.cfg}
 
 
 def time_cprime(sample, stream, reps=3):
@@ -285,6 +285,34 @@ def time_cprime(sample, stream, reps=3):
         ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
     lms = float(np.mean([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    # and A.w (k = 1) from that level order (toc_level_right_mul): bytes to product
+    # without any host pass
+    from workloads import config_W
+    row_off = np.concatenate([[0], np.cumsum([i["n_rows"] for i in infos])]).astype(np.int64)
+    max_live = int(counts.view(-1, 2)[:, 0].max().item())
+    wv = torch.from_numpy(np.ascontiguousarray(config_W(sample["cfg"], 1)[:, 0])).to(dev)
+    rv = torch.empty(max(int(row_off[-1]), 1), device=dev)
+    rst = torch.empty(len(blobs), dtype=torch.int32, device=dev)
+    ws3 = torch.empty(32 * (len(blobs) + 1), dtype=torch.uint8, device=dev)
+
+    def run_right():
+        T.toc_level_right_mul(d_blobs, blob_off, node_off, d_off, row_off, max_levels, max_live,
+                              lst, counts, level, lv[0], lv[1], lv[2], lD, wv, rv, rst, ws3)
+
+    rms = None
+    try:
+        run_right()
+        torch.cuda.synchronize()
+        rok = bool((rst == 0).all().item())
+        for i in range(reps):
+            ev[2 * i].record(stream)
+            run_right()
+            ev[2 * i + 1].record(stream)
+        torch.cuda.synchronize()
+        rms = float(np.mean([ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps)]))
+    except T.TocError as e:
+        log(f"product from the level order skipped: {e}")
+        rok = False
     # algorithmic bytes: the tree read once (16 B per node), D read from the blobs
     # and written renumbered, 16 B per live code and the level offsets written
     lb = float(16 * n + 8 * int(d_off[-1]) + 16 * n_live + 4 * level.numel())
@@ -295,12 +323,18 @@ def time_cprime(sample, stream, reps=3):
            "host_pack_s": round(sample["pack_s"], 3),
            "level_order": {"ms": round(lms, 4), "live_codes": n_live,
                            "hbm_frac": lb / (lms / 1e3) / HBM_PEAK, "status_ok": lok},
-           "ingest_ms": round(ms + lms, 4)}
+           "ingest_ms": round(ms + lms, 4),
+           "right_k1_from_level_order": None if rms is None else
+           {"ms": round(rms, 4), "status_ok": rok,
+            "bytes_to_product_ms": round(ms + lms + rms, 4)}}
     log(f"C' build from physical bytes: {len(blobs)} batches, {n} nodes, {ms:.3f} ms "
         f"({res['hbm_frac']:.1%} of HBM peak on algorithmic bytes), status ok: {ok}")
     log(f"level order from that tree: {lms:.3f} ms ({res['level_order']['hbm_frac']:.1%} of "
         f"HBM peak on algorithmic bytes), {n_live} live codes, status ok: {lok}")
-    del d_blobs, outs, status, ws, lv, level, lD, counts, lst, ws2
+    if rms is not None:
+        log(f"A.w (k = 1) from that level order: {rms:.3f} ms; bytes to product "
+            f"{ms + lms + rms:.3f} ms, status ok: {rok}")
+    del d_blobs, outs, status, ws, lv, level, lD, counts, lst, ws2, wv, rv, rst, ws3
     torch.cuda.empty_cache()
     return res
 

@@ -437,6 +437,30 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
                            uint32_t *level, uint32_t *l_D, int64_t *counts, int32_t *status,
                            void *ws, size_t ws_bytes, void *stream);
 
+/* A.w for k = 1 (Theorem 1) straight from the output of toc_level_build, so that
+ * the whole path from physical bytes to a product runs on the device: per batch,
+ * H over the live codes level by level in LDS (parents first), then each tuple's
+ * sum of H over its renumbered codes (tuple starts read from the blob).
+ *   blobs, blob_off, node_off, d_off, max_levels  as for toc_level_build
+ *   row_off  host, n_batches+1 entries: batch b's tuples are rows row_off[b] ..
+ *            row_off[b+1]-1 of r
+ *   max_live the most live codes of a batch (4 max_live bytes of LDS, at most
+ *            160 KiB, else TOC_EUNSUPPORTED; a batch above it gets TOC_LEVEL_LIVE)
+ *   level_status, counts, level, l_parent, l_col, l_val, l_D  toc_level_build's
+ *   w        device float[n_cols];  r  device float per row (output)
+ *   status   device int32 per batch: 0, level_status when nonzero, or
+ *            TOC_LEVEL_D when the blob's tuples or |D| differ from the offsets
+ *   ws       device workspace of at least 32 (n_batches + 1) bytes
+ * Asynchronous on stream; the offsets are copied before returning.          */
+#define TOC_LEVEL_LIVE 9          /* more live codes than max_live                 */
+toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                               const int64_t *d_off, const int64_t *row_off, int64_t n_batches,
+                               int32_t max_levels, int64_t max_live, const int32_t *level_status,
+                               const int64_t *counts, const uint32_t *level,
+                               const uint32_t *l_parent, const uint32_t *l_col, const float *l_val,
+                               const uint32_t *l_D, const float *w, float *r, int32_t *status,
+                               void *ws, size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------------------
  * Mini-batch gradient descent (section 2.1): h <- h - lr / |B| * sum over the
  * tuples (x, y) of batch B of d loss(h, x, y) / d h, for the linear models of

@@ -25,7 +25,7 @@ TOC_MAP_SCALE, TOC_MAP_SQUARE = 0, 1
 TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE = 0, 1, 2
 TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(1, 5)
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
- TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH) = range(1, 9)
+ TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH, TOC_LEVEL_LIVE) = range(1, 10)
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -116,6 +116,7 @@ def lib():
         "toc_encode_device_workspace_size": [I64, I64, P],
         "toc_mlp_workspace_size": [P, I32, I32, I32, P],
         "toc_level_workspace_size": [I64, I64, P],
+        "toc_level_right_mul": [P, P, P, P, P, I64, I32, I64, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "toc_level_build": [P, P, P, P, I64, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "toc_mlp_epoch": [P, I64, I64, I32, I32, I32, P, P, P, P, P, P, P, C.c_float, P, SZ, P],
         "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
@@ -503,3 +504,27 @@ def toc_level_build(blobs, blob_off, node_off, d_off, max_levels, cprime_status,
                                  _ptr(counts), _ptr(status), _ptr(ws),
                                  ws.numel() * ws.element_size() if ws is not None else 0,
                                  _stream(stream)))
+
+
+def toc_level_right_mul(blobs, blob_off, node_off, d_off, row_off, max_levels, max_live,
+                        level_status, counts, level, l_parent, l_col, l_val, l_D, w, r, status,
+                        ws, stream=None):
+    """A.w from toc_level_build's outputs (same launch arguments); row_off: host
+    int64 array of n_batches + 1 row offsets into r; w: device float32 tensor of
+    n_cols; r: device float32 tensor of row_off[-1]; status: device int32 tensor of
+    one per batch; ws: device tensor of at least 32 (n_batches + 1) bytes."""
+    blob_off, node_off, d_off, row_off = (_arr(x, np.int64)
+                                          for x in (blob_off, node_off, d_off, row_off))
+    nb = blob_off.size - 1
+    if not (node_off.size == d_off.size == row_off.size == nb + 1):
+        raise TocError(TOC_EINVAL, "offset arrays differ in length")
+    if r.numel() < int(row_off[-1]) or r.element_size() != 4:
+        raise TocError(TOC_EINVAL, "r must hold one float32 per row")
+    if status.numel() < nb or status.element_size() != 4:
+        raise TocError(TOC_EINVAL, "status must hold one int32 per batch")
+    _check(lib().toc_level_right_mul(_ptr(blobs), _ptr(blob_off), _ptr(node_off), _ptr(d_off),
+                                     _ptr(row_off), nb, int(max_levels), int(max_live),
+                                     _ptr(level_status), _ptr(counts), _ptr(level),
+                                     _ptr(l_parent), _ptr(l_col), _ptr(l_val), _ptr(l_D), _ptr(w),
+                                     _ptr(r), _ptr(status), _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream(stream)))

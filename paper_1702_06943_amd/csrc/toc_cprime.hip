@@ -379,6 +379,67 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
   }
 }
 
+// A.w (k = 1, Theorem 1) straight from the device-built level order: per batch,
+// H over the live codes level by level in LDS (H[c] = H[parent] + val * w[col],
+// parents first), then each tuple's sum of H over its renumbered codes, the tuple
+// starts read back from the blob.  Completes ingest on the device: physical bytes
+// -> C' -> level order -> product, with no host pass over the batch.
+__global__ __launch_bounds__(kLvBlock) void level_right_k1_kernel(
+    const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
+    int max_levels, int64_t max_live, const int32_t *__restrict__ lv_status,
+    const int64_t *__restrict__ counts, const uint32_t *__restrict__ level,
+    const uint32_t *__restrict__ l_parent,
+    const uint32_t *__restrict__ l_col, const float *__restrict__ l_val,
+    const uint32_t *__restrict__ l_D, const float *__restrict__ w, float *__restrict__ r,
+    int32_t *__restrict__ status) {
+  extern __shared__ float H[];
+  __shared__ Hdr h;
+  const int64_t *node_off = offs + (n_batches + 1), *d_off = offs + 2 * (n_batches + 1);
+  const int64_t *row_off = offs + 3 * (n_batches + 1);
+  for (int64_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
+    const uint8_t *blob = blobs + offs[b];
+    const uint64_t size = (uint64_t)(offs[b + 1] - offs[b]);
+    const int64_t no = node_off[b], dof = d_off[b], r0 = row_off[b];
+    if (threadIdx.x == 0) {
+      h.err = lv_status[b];
+      if (h.err == 0) parse_headers(blob, size, 1 << 30, h);
+      if (h.err == 0 && ((int64_t)h.cnt[4] - 1 != row_off[b + 1] - r0 ||
+                         (int64_t)h.cnt[3] != d_off[b + 1] - dof))
+        h.err = TOC_LEVEL_D;
+      if (h.err == 0 && counts[2 * b] > max_live) h.err = TOC_LEVEL_LIVE;
+    }
+    __syncthreads();
+    if (h.err) {
+      if (threadIdx.x == 0) status[b] = h.err;
+      __syncthreads();
+      continue;
+    }
+    const uint32_t *lv = level + b * (int64_t)(max_levels + 1);
+    const int top = (int)counts[2 * b + 1];
+    for (int d = 1; d <= top; ++d) {
+      const uint32_t a = lv[d - 1], e = lv[d];
+      for (uint32_t c = a + threadIdx.x; c < e; c += kLvBlock) {
+        const float base = d > 1 ? H[l_parent[no + c]] : 0.0f;
+        H[c] = fmaf(l_val[no + c], w[l_col[no + c]], base);
+      }
+      __syncthreads();
+    }
+    const uint8_t *p_st = blob + h.data[4];
+    const uint32_t w_st = h.w[4], nR = h.cnt[4] - 1;
+    const int lane = threadIdx.x % 8, grp = threadIdx.x / 8;
+    for (uint32_t i = grp; i < nR; i += kLvBlock / 8) {
+      const uint32_t s0 = rd(p_st, i, w_st), s1 = rd(p_st, i + 1, w_st);
+      float acc = 0.0f;
+      for (uint32_t p = s0 + lane; p < s1; p += 8) acc += H[l_D[dof + p]];
+#pragma unroll
+      for (int o = 4; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 8);
+      if (lane == 0) r[r0 + i] = acc;
+    }
+    if (threadIdx.x == 0) status[b] = 0;
+    __syncthreads();
+  }
+}
+
 inline int64_t align256(int64_t x) { return (x + 255) & ~(int64_t)255; }
 
 int64_t ws_nodes_offset(int64_t n_batches) { return align256(16 * (n_batches + 1)); }
@@ -505,6 +566,56 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
                      status, live, newidx);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "level_kernel: %s", hipGetErrorString(e));
+  return TOC_OK;
+}
+
+toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
+                               const int64_t *d_off, const int64_t *row_off, int64_t n_batches,
+                               int32_t max_levels, int64_t max_live, const int32_t *level_status,
+                               const int64_t *counts, const uint32_t *level,
+                               const uint32_t *l_parent, const uint32_t *l_col, const float *l_val,
+                               const uint32_t *l_D, const float *w, float *r, int32_t *status,
+                               void *ws, size_t ws_bytes, void *stream) {
+  clear_error();
+  if (n_batches < 0) return fail(TOC_EINVAL, "n_batches < 0");
+  if (n_batches == 0) return TOC_OK;
+  if (!blob_off || !node_off || !d_off || !row_off || !level_status || !counts || !level ||
+      !status || !ws)
+    return fail(TOC_EINVAL, "NULL argument");
+  if (max_levels < 1 || max_levels > kLvMaxLevels)
+    return fail(TOC_EUNSUPPORTED, "max_levels %d outside 1..%d", max_levels, kLvMaxLevels);
+  if (max_live < 0 || max_live * 4 > 160 * 1024)
+    return fail(TOC_EUNSUPPORTED, "max_live %lld: H must fit 160 KiB of LDS", (long long)max_live);
+  for (int64_t b = 0; b < n_batches; ++b) {
+    if (blob_off[b + 1] < blob_off[b] || node_off[b + 1] <= node_off[b] ||
+        d_off[b + 1] < d_off[b] || row_off[b + 1] < row_off[b])
+      return fail(TOC_EINVAL, "offsets not non-decreasing at %lld", (long long)b);
+  }
+  if (!l_parent || !l_col || !l_val || !w || (row_off[n_batches] > 0 && !r) ||
+      (d_off[n_batches] > 0 && !l_D) || (blob_off[n_batches] > 0 && !blobs))
+    return fail(TOC_EINVAL, "NULL array");
+  const size_t need = (size_t)(32 * (n_batches + 1));
+  if (ws_bytes < need) return fail(TOC_ESIZE, "workspace of %zu bytes below the %zu needed", ws_bytes, need);
+  hipStream_t s = (hipStream_t)stream;
+  int64_t *offs = (int64_t *)ws;
+  const size_t ob = 8 * (size_t)(n_batches + 1);
+  if (hipMemcpyAsync(offs, blob_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + (n_batches + 1), node_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + 2 * (n_batches + 1), d_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(offs + 3 * (n_batches + 1), row_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(TOC_EDEVICE, "copy of the offsets failed");
+  const size_t lds = 4 * (size_t)std::max<int64_t>(max_live, 1);
+  if (lds > 64 * 1024 &&
+      hipFuncSetAttribute((const void *)level_right_k1_kernel,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
+  const unsigned g = (unsigned)std::min<int64_t>(n_batches, 1 << 20);
+  hipLaunchKernelGGL(level_right_k1_kernel, dim3(g), dim3(kLvBlock), lds, s, (const uint8_t *)blobs,
+                     offs, n_batches, (int)max_levels, max_live, level_status, counts, level, l_parent, l_col,
+                     l_val, l_D, w, r, status);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOC_EDEVICE, "level_right_k1_kernel: %s", hipGetErrorString(e));
   return TOC_OK;
 }
 

@@ -163,3 +163,73 @@ def level_gpu_checked(blobs, d_counts):
         return level_gpu(blobs, max_levels=8, d_counts=d_counts)
     finally:
         T.toc_phys_info_get = real_info
+
+
+def ingest_right(blobs, w_host, max_levels=64):
+    """Physical bytes -> toc_cprime_build -> toc_level_build -> toc_level_right_mul,
+    all on the device; returns R (host, one value per row) and the statuses."""
+    infos = [T.toc_phys_info_get(b) for b in blobs]
+    nb = len(blobs)
+    blob_off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
+    node_off = np.concatenate([[0], np.cumsum([i["n_nodes"] for i in infos])]).astype(np.int64)
+    d_off = np.concatenate([[0], np.cumsum([i["n_codes"] for i in infos])]).astype(np.int64)
+    row_off = np.concatenate([[0], np.cumsum([i["n_rows"] for i in infos])]).astype(np.int64)
+    max_rows = max([i["n_rows"] for i in infos] + [0])
+    dblob = torch.from_numpy(np.concatenate([np.asarray(b, np.uint8) for b in blobs]
+                                            + [np.zeros(1, np.uint8)])).to(DEV)
+    n = int(node_off[-1])
+    cp = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
+    cst = torch.empty(nb, dtype=torch.int32, device=DEV)
+    ws = torch.empty(T.toc_cprime_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
+    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, *cp, cst, ws)
+    lv = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
+    level = torch.empty(nb * (max_levels + 1), dtype=torch.int32, device=DEV)
+    lD = torch.empty(max(int(d_off[-1]), 1), dtype=torch.int32, device=DEV)
+    counts = torch.empty(2 * nb, dtype=torch.int64, device=DEV)
+    lst = torch.empty(nb, dtype=torch.int32, device=DEV)
+    ws2 = torch.empty(T.toc_level_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
+    T.toc_level_build(dblob, blob_off, node_off, d_off, max_levels, cst, *cp, *lv, level, lD,
+                      counts, lst, ws2)
+    max_live = int(counts.view(-1, 2)[:, 0].max().item())
+    wd = torch.from_numpy(np.asarray(w_host, np.float32)).to(DEV)
+    r = torch.full((max(int(row_off[-1]), 1),), float("nan"), device=DEV)
+    st = torch.full((nb,), -1, dtype=torch.int32, device=DEV)
+    ws3 = torch.empty(32 * (nb + 1), dtype=torch.uint8, device=DEV)
+    T.toc_level_right_mul(dblob, blob_off, node_off, d_off, row_off, max_levels, max_live, lst,
+                          counts, level, lv[0], lv[1], lv[2], lD, wd, r, st, ws3)
+    torch.cuda.synchronize()
+    return r.cpu().numpy()[:int(row_off[-1])], st.cpu().numpy(), row_off
+
+
+@pytest.mark.parametrize("cfg,first,nb", [("c1", 0, 1), ("c2", 3, 3), ("c3", 5, 2), ("c5", 11, 8)])
+def test_ingest_right_product(cfg, first, nb):
+    """A.w from physical bytes entirely on the device, within 1e-5 S of the oracle's
+    fp64 product on the decoded batch."""
+    from workloads import config_W
+    B = config_batches(cfg, first, nb)
+    blobs = blobs_of(B)
+    w = config_W(cfg, 1)[:, 0]
+    r, st, row_off = ingest_right(blobs, w)
+    assert st.tolist() == [0] * nb
+    for b in range(nb):
+        n, rp, c, v = B.batch(b)
+        rows = O.canonicalize(n, B.n_cols, rp, c, v)
+        want, S = O.dense_right(rows, B.n_cols, w[:, None].astype(np.float64))
+        got = r[row_off[b]:row_off[b + 1]]
+        assert np.all(np.abs(got - want[:, 0]) <= 1e-5 * S[:, 0]), f"batch {b}"
+
+
+def test_ingest_right_tiny_and_empty():
+    blobs = []
+    for i, spec in enumerate(TINY):
+        rp, c, v = tiny_batch(900 + i, n_cols=64, zeros=(i % 2 == 0), **spec)
+        blobs += blobs_of(Batches(64, [spec["n_rows"]], rp, c, v))
+    w = np.random.default_rng(3).standard_normal(64).astype(np.float32)
+    r, st, row_off = ingest_right(blobs, w, max_levels=512)
+    assert st.tolist() == [0] * len(blobs)
+    for b, blob in enumerate(blobs):
+        I, D = O.unpack_physical(bytes(blob))
+        rows = O.decode(I, D)
+        want, S = O.dense_right(rows, 64, w[:, None].astype(np.float64))
+        got = r[row_off[b]:row_off[b + 1]]
+        assert np.all(np.abs(got - want[:, 0]) <= 1e-5 * S[:, 0]), f"batch {b}"
