@@ -250,8 +250,9 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     const uint32_t *__restrict__ depth, uint32_t *__restrict__ l_parent,
     uint32_t *__restrict__ l_col, uint32_t *__restrict__ l_val, uint32_t *__restrict__ l_depth,
     uint32_t *__restrict__ level, uint32_t *__restrict__ l_D, int64_t *__restrict__ counts,
-    int32_t *__restrict__ status, uint32_t *__restrict__ live, uint32_t *__restrict__ newidx) {
+    int32_t *__restrict__ status, uint32_t *__restrict__ newidx) {
   extern __shared__ uint32_t run[];            // per depth: live codes placed so far
+  uint32_t *live = run + (max_levels + 1);     // then the batch's live codes, one bit each
   __shared__ Hdr h;
   __shared__ int errs;
   __shared__ uint32_t n_lv;
@@ -279,9 +280,8 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     }
     const uint32_t nD = h.cnt[3], w_d = h.w[3];
     const uint8_t *p_d = blob + h.data[3];
-    for (uint32_t c = threadIdx.x; c < n_nodes; c += kLvBlock) live[no + c] = 0u;
+    for (uint32_t x = threadIdx.x; x < (n_nodes + 31) / 32; x += kLvBlock) live[x] = 0u;
     for (int d = threadIdx.x; d <= max_levels; d += kLvBlock) run[d] = 0u;
-    __threadfence();
     __syncthreads();
     // live marking: a walk up from every entry of D
     for (uint32_t p = threadIdx.x; p < nD; p += kLvBlock) {
@@ -290,9 +290,9 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
         atomicOr(&errs, 1);
         continue;
       }
-      while (c != 0u && atomicOr(&live[no + c], 1u) == 0u) c = parent[no + c];
+      while (c != 0u && (atomicOr(&live[c / 32], 1u << (c % 32)) & (1u << (c % 32))) == 0u)
+        c = parent[no + c];
     }
-    __threadfence();
     __syncthreads();
     if (errs) {
       if (threadIdx.x == 0) {
@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     }
     // live codes per depth
     for (uint32_t c = 1 + threadIdx.x; c < n_nodes; c += kLvBlock) {
-      if (!__hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
+      if (!((live[c / 32] >> (c % 32)) & 1u)) continue;
       const uint32_t d = depth[no + c];
       if (d == 0u || d > (uint32_t)max_levels) atomicOr(&errs, 2);
       else atomicAdd(&run[d], 1u);
@@ -339,8 +339,7 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     // waves of a chunk one after another, lanes of one depth ranked by a ballot
     for (uint32_t c0 = 1; c0 < n_nodes; c0 += kLvBlock) {
       const uint32_t c = c0 + threadIdx.x;
-      const bool in = c < n_nodes &&
-                      __hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const bool in = c < n_nodes && ((live[c / 32] >> (c % 32)) & 1u);
       const uint32_t d = in ? depth[no + c] : 0u;
       for (int w = 0; w < kLvWaves; ++w) {
         if (wave == w) {
@@ -366,7 +365,7 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     __syncthreads();
     // the live codes at their places, parents renumbered; D renumbered
     for (uint32_t c = 1 + threadIdx.x; c < n_nodes; c += kLvBlock) {
-      if (!__hip_atomic_load(&live[no + c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) continue;
+      if (!((live[c / 32] >> (c % 32)) & 1u)) continue;
       const uint32_t i = newidx[no + c], d = depth[no + c];
       l_parent[no + i] = d == 1u ? kNone : newidx[no + parent[no + c]];
       l_col[no + i] = col[no + c];
@@ -509,7 +508,7 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
 toc_status toc_level_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *bytes) {
   clear_error();
   if (!bytes || n_batches < 0 || n_nodes < 0) return fail(TOC_EINVAL, "bad argument");
-  *bytes = (size_t)(align256(24 * (n_batches + 1)) + 2 * align256(4 * n_nodes));
+  *bytes = (size_t)(align256(24 * (n_batches + 1)) + align256(4 * n_nodes));
   return TOC_OK;
 }
 
@@ -552,9 +551,13 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
       hipMemcpyAsync(offs + 2 * (n_batches + 1), d_off, ob, hipMemcpyHostToDevice, s) != hipSuccess ||
       hipStreamSynchronize(s) != hipSuccess)
     return fail(TOC_EDEVICE, "copy of the offsets failed");
-  uint8_t *base = (uint8_t *)ws + align256(24 * (n_batches + 1));
-  uint32_t *live = (uint32_t *)base, *newidx = (uint32_t *)(base + align256(4 * n_nodes));
-  const size_t lds = 4 * ((size_t)max_levels + 1);
+  uint32_t *newidx = (uint32_t *)((uint8_t *)ws + align256(24 * (n_batches + 1)));
+  int64_t max_nodes = 0;
+  for (int64_t b = 0; b < n_batches; ++b) max_nodes = std::max(max_nodes, node_off[b + 1] - node_off[b]);
+  // per-depth counters and a bit per node of the batch (live marks) in LDS
+  const size_t lds = 4 * ((size_t)max_levels + 1) + 4 * (size_t)((max_nodes + 31) / 32);
+  if (lds > 160 * 1024)
+    return fail(TOC_EUNSUPPORTED, "a batch of %lld nodes: live marks beyond LDS", (long long)max_nodes);
   if (lds > 64 * 1024 &&
       hipFuncSetAttribute((const void *)level_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)lds) != hipSuccess)
@@ -563,7 +566,7 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
   hipLaunchKernelGGL(level_kernel, dim3(g), dim3(kLvBlock), lds, s, (const uint8_t *)blobs, offs,
                      n_batches, (int)max_levels, cprime_status, parent, col, (const uint32_t *)val,
                      depth, l_parent, l_col, (uint32_t *)l_val, l_depth, level, l_D, counts,
-                     status, live, newidx);
+                     status, newidx);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "level_kernel: %s", hipGetErrorString(e));
   return TOC_OK;
