@@ -427,7 +427,7 @@ toc_status toc_level_workspace_size(int64_t n_batches, int64_t n_nodes, size_t *
  *   status   int32 per batch: 0, the batch's nonzero cprime status, TOC_CPRIME_*
  *            for a blob that does not hold, or TOC_LEVEL_* below
  * Asynchronous on stream; the offsets are copied before returning.  Needs
- * 4 (max_levels + 1) + ceil(nodes / 32) * 4 bytes of LDS for the batch with the
+ * 36 (max_levels + 1) + ceil(nodes / 32) * 4 bytes of LDS for the batch with the
  * most nodes, at most 160 KiB (TOC_EUNSUPPORTED beyond).                     */
 #define TOC_LEVEL_D 7             /* the blob's |D| differs from d_off's span       */
 #define TOC_LEVEL_DEPTH 8         /* a live code deeper than max_levels            */

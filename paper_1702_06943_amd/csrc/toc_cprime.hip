@@ -252,10 +252,11 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     uint32_t *__restrict__ level, uint32_t *__restrict__ l_D, int64_t *__restrict__ counts,
     int32_t *__restrict__ status, uint32_t *__restrict__ newidx) {
   extern __shared__ uint32_t run[];            // per depth: live codes placed so far
-  uint32_t *live = run + (max_levels + 1);     // then the batch's live codes, one bit each
+  uint32_t *wcnt = run + (max_levels + 1);     // per wave and depth: a chunk's live codes
+  uint32_t *live = wcnt + kLvWaves * (max_levels + 1);   // the batch's live codes, a bit each
   __shared__ Hdr h;
   __shared__ int errs;
-  __shared__ uint32_t n_lv;
+  __shared__ uint32_t n_lv, top_d;
   const int64_t *node_off = offs + (n_batches + 1), *d_off = offs + 2 * (n_batches + 1);
   const int lane = threadIdx.x % kCpWave, wave = threadIdx.x / kCpWave;
   for (int64_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
@@ -281,7 +282,10 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
     const uint32_t nD = h.cnt[3], w_d = h.w[3];
     const uint8_t *p_d = blob + h.data[3];
     for (uint32_t x = threadIdx.x; x < (n_nodes + 31) / 32; x += kLvBlock) live[x] = 0u;
-    for (int d = threadIdx.x; d <= max_levels; d += kLvBlock) run[d] = 0u;
+    for (int d = threadIdx.x; d <= max_levels; d += kLvBlock) {
+      run[d] = 0u;
+      for (int v = 0; v < kLvWaves; ++v) wcnt[v * (max_levels + 1) + d] = 0u;
+    }
     __syncthreads();
     // live marking: a walk up from every entry of D
     for (uint32_t p = threadIdx.x; p < nD; p += kLvBlock) {
@@ -331,35 +335,51 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
         lv[d] = acc;
       }
       n_lv = acc;
+      top_d = top;
       counts[2 * b] = acc;
       counts[2 * b + 1] = top;
     }
     __syncthreads();
-    // places in (depth, index) order: chunks of kLvBlock nodes in index order, the
-    // waves of a chunk one after another, lanes of one depth ranked by a ballot
+    // places in (depth, index) order, chunk by chunk of kLvBlock nodes in index
+    // order: each wave ranks its lanes of one depth by a ballot and counts them per
+    // depth; a lane's place is the depth's running count, plus the counts of the
+    // waves before its own, plus its rank; then the running counts advance
+    const uint32_t L = top_d;
     for (uint32_t c0 = 1; c0 < n_nodes; c0 += kLvBlock) {
       const uint32_t c = c0 + threadIdx.x;
       const bool in = c < n_nodes && ((live[c / 32] >> (c % 32)) & 1u);
       const uint32_t d = in ? depth[no + c] : 0u;
-      for (int w = 0; w < kLvWaves; ++w) {
-        if (wave == w) {
-          bool todo = in;
-          uint64_t left = __ballot(todo);
-          while (left) {
-            const int leader = __ffsll((unsigned long long)left) - 1;
-            const uint32_t dd = (uint32_t)__shfl((int)d, leader, kCpWave);
-            const bool mine = todo && d == dd;
-            const uint64_t m = __ballot(mine);
-            if (mine) {
-              newidx[no + c] = run[dd] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-              todo = false;
-            }
-            if (lane == leader) run[dd] += (uint32_t)__popcll(m);
-            left = __ballot(todo);
-          }
+      uint32_t rank = 0;
+      bool todo = in;
+      uint64_t left = __ballot(todo);
+      while (left) {
+        const int leader = __ffsll((unsigned long long)left) - 1;
+        const uint32_t dd = (uint32_t)__shfl((int)d, leader, kCpWave);
+        const bool mine = todo && d == dd;
+        const uint64_t m = __ballot(mine);
+        if (mine) {
+          rank = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+          todo = false;
         }
-        __syncthreads();
+        if (lane == leader) wcnt[wave * (max_levels + 1) + dd] = (uint32_t)__popcll(m);
+        left = __ballot(todo);
       }
+      __syncthreads();
+      if (in) {
+        uint32_t at = run[d] + rank;
+        for (int v = 0; v < wave; ++v) at += wcnt[v * (max_levels + 1) + d];
+        newidx[no + c] = at;
+      }
+      __syncthreads();
+      for (uint32_t dd = 1 + threadIdx.x; dd <= L; dd += kLvBlock) {
+        uint32_t add = 0;
+        for (int v = 0; v < kLvWaves; ++v) {
+          add += wcnt[v * (max_levels + 1) + dd];
+          wcnt[v * (max_levels + 1) + dd] = 0u;
+        }
+        run[dd] += add;
+      }
+      __syncthreads();
     }
     __threadfence();
     __syncthreads();
@@ -555,7 +575,7 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
   int64_t max_nodes = 0;
   for (int64_t b = 0; b < n_batches; ++b) max_nodes = std::max(max_nodes, node_off[b + 1] - node_off[b]);
   // per-depth counters and a bit per node of the batch (live marks) in LDS
-  const size_t lds = 4 * ((size_t)max_levels + 1) + 4 * (size_t)((max_nodes + 31) / 32);
+  const size_t lds = 4 * ((size_t)max_levels + 1) * (1 + kLvWaves) + 4 * (size_t)((max_nodes + 31) / 32);
   if (lds > 160 * 1024)
     return fail(TOC_EUNSUPPORTED, "a batch of %lld nodes: live marks beyond LDS", (long long)max_nodes);
   if (lds > 64 * 1024 &&
