@@ -14,7 +14,7 @@
 namespace {
 
 constexpr int kMgBlock = 1024;
-constexpr int kMgLanes = 16;                   // lanes per tuple in the right product
+constexpr int kMgLanes = 8;                    // lanes per tuple in the right product
 constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of occ_row
 constexpr size_t kMgLdsMax = 160 * 1024;
 
@@ -52,6 +52,7 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     // right: H[c] = H[parent] + val * h[col], level by level
     for (int d = 1; d <= bt.n_levels; ++d) {
       const uint32_t a = lvl[d - 1], e = lvl[d];
+#pragma unroll 4
       for (uint32_t c = a + threadIdx.x; c < e; c += kMgBlock) {
         const toc_key k = key[c];
         const float base = d > 1 ? H[link[c].parent] : 0.0f;
@@ -67,6 +68,7 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
       for (int r = grp; r < nr; r += kMgBlock / kMgLanes) {
         const uint32_t s = span[r], e = span[r + 1];
         float acc = 0.0f;
+#pragma unroll 4
         for (uint32_t j = s + lane; j < e; j += kMgLanes) acc += H[dc[j]];
 #pragma unroll
         for (int o = kMgLanes / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kMgLanes);
@@ -78,9 +80,11 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     // holding its code, then children added into parents, deepest first
     const uint32_t *oo = im.occ_off + bt.code_base + b;
     const uint32_t *orow = im.occ_row + bt.d_base;
+#pragma unroll 2
     for (uint32_t p = threadIdx.x; p < nc; p += kMgBlock) {
       float s = 0.0f;
       const uint32_t o1 = oo[p + 1];
+#pragma unroll 4
       for (uint32_t o = oo[p]; o < o1; ++o) s += Gs[orow[o] & ~kMgFirst];
       H[p] = s;
     }
@@ -108,7 +112,9 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     for (int j = threadIdx.x; j < m; j += kMgBlock) {
       float s = 0.0f;
       const uint32_t l1 = Loff[j + 1], t1 = Toff[j + 1];
+#pragma unroll 4
       for (uint32_t p = Loff[j]; p < l1; ++p) s = fmaf(__uint_as_float(pv[p]), H[p], s);
+#pragma unroll 4
       for (uint32_t t = Toff[j]; t < t1; ++t) {
         const uint32_t c = tl[t];
         s = fmaf(__uint_as_float(pv[c]), H[c], s);
