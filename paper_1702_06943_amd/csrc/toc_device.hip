@@ -1886,8 +1886,8 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
       const uint32_t d = lk[i].y;
       int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
       for (uint32_t q = 0;;) {
-        ocol[p] = (int32_t)kk.x;
-        oval[p] = kk.y;
+        __builtin_nontemporal_store((int32_t)kk.x, &ocol[p]);
+        __builtin_nontemporal_store(kk.y, &oval[p]);
         if (++q >= d) break;
         --p;
         kk = *(const uint2 *)(key + par);
@@ -1972,10 +1972,13 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       float *dst = Ab + (int64_t)r * lda;
+      // streaming stores: the block is written once and not read back here
       if (vec) {
-        for (int j = 4 * lane; j < m; j += 4 * kWave) *(float4 *)&dst[j] = *(const float4 *)&row[j];
+        typedef float f4v __attribute__((ext_vector_type(4)));
+        for (int j = 4 * lane; j < m; j += 4 * kWave)
+          __builtin_nontemporal_store(*(const f4v *)&row[j], (f4v *)&dst[j]);
       } else {
-        for (int j = lane; j < m; j += kWave) dst[j] = row[j];
+        for (int j = lane; j < m; j += kWave) __builtin_nontemporal_store(row[j], &dst[j]);
       }
       __builtin_amdgcn_wave_barrier();
     }
