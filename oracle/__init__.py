@@ -18,6 +18,7 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
   dense_right    pinned: hand-computed worked-example sums, numpy dense matmul on the
                  densified batch, integer exactness
   dense_left     pinned: as dense_right, plus duality <G, A W> = <A^T G, W>
+  densify        pinned: equal to a dense matrix filled by the test itself
   toc_right      pinned: Theorem 1 (equals dense_right) + integer exactness
   toc_left       pinned: Theorem 2 (equals dense_left) + integer exactness
   map_values     pinned: Algorithm 3's claim (decoding the modified I equals the
@@ -59,6 +60,7 @@ from .toc_oracle import (  # noqa: F401
     encode,
     build_cprime,
     decode,
+    densify,
     decoded_to_csr,
     dense_right,
     dense_left,

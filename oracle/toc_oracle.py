@@ -18,6 +18,7 @@ import math
 import struct
 
 import numpy as np
+import scipy.sparse
 
 
 class TocInputError(ValueError):
@@ -263,33 +264,43 @@ def dense_plus(rows, n_cols, c=0.0):
 #   out[j, q] = sum_i a_ij g_iq         (left multiplication G^T.A, stored transposed)
 # The tolerance scales are the same sums of absolute values of the terms.
 # ---------------------------------------------------------------------------
+def densify(rows, n_cols):
+    """Decoded rows -> the dense fp64 (n_rows, n_cols) matrix A (zeros included),
+    on which A.W and A^T.G are plain matmuls."""
+    A = np.zeros((len(rows), n_cols))
+    for i, r in enumerate(rows):
+        for c, b in r:
+            A[i, c] = bits_f32(b)
+    return A
+
+
+def _sparse(rows, n_cols):
+    """The decoded batch as an fp64 sparse matrix A (n_rows x n_cols)."""
+    ri, ci, vi = _coo(rows)
+    return scipy.sparse.csr_matrix((vi, (ri, ci)), shape=(len(rows), n_cols))
+
+
 def dense_right(rows, n_cols, W):
-    """R = A.W and S_R = |A|.|W| in fp64.  W: (n_cols, k)."""
+    """R = A.W and S_R = |A|.|W| in fp64 (a sparse-times-dense matmul of the
+    decoded batch).  W: (n_cols, k)."""
     W = np.asarray(W, dtype=np.float64)
     if W.ndim != 2 or W.shape[0] != n_cols:
         raise TocInputError("W must be n_cols x k")
-    k = W.shape[1]
-    ri, ci, vi = _coo(rows)
-    R = np.zeros((len(rows), k))
-    S = np.zeros((len(rows), k))
-    terms = vi[:, None] * W[ci, :]
-    np.add.at(R, ri, terms)
-    np.add.at(S, ri, np.abs(terms))
+    A = _sparse(rows, n_cols)
+    R = np.asarray(A @ W, dtype=np.float64).reshape(len(rows), W.shape[1])
+    S = np.asarray(abs(A) @ np.abs(W), dtype=np.float64).reshape(len(rows), W.shape[1])
     return R, S
 
 
 def dense_left(rows, n_cols, G):
-    """out = (G^T.A)^T (n_cols x k) and S_out = |A|^T.|G| in fp64.  G: (n_rows, k)."""
+    """out = (G^T.A)^T = A^T.G (n_cols x k) and S_out = |A|^T.|G| in fp64 (a
+    sparse-times-dense matmul of the decoded batch).  G: (n_rows, k)."""
     G = np.asarray(G, dtype=np.float64)
     if G.ndim != 2 or G.shape[0] != len(rows):
         raise TocInputError("G must be n_rows x k")
-    k = G.shape[1]
-    ri, ci, vi = _coo(rows)
-    out = np.zeros((n_cols, k))
-    S = np.zeros((n_cols, k))
-    terms = vi[:, None] * G[ri, :]
-    np.add.at(out, ci, terms)
-    np.add.at(S, ci, np.abs(terms))
+    At = _sparse(rows, n_cols).T.tocsr()
+    out = np.asarray(At @ G, dtype=np.float64).reshape(n_cols, G.shape[1])
+    S = np.asarray(abs(At) @ np.abs(G), dtype=np.float64).reshape(n_cols, G.shape[1])
     return out, S
 
 

@@ -251,6 +251,7 @@ def test_products(seed, case, k):
         W = rng.standard_normal((spec["n_cols"], k)).astype(np.float32)
         G = rng.standard_normal((spec["n_rows"], k)).astype(np.float32)
     A = _dense(rows, spec["n_cols"])
+    assert np.array_equal(O.densify(rows, spec["n_cols"]), A)
     R, SR = O.dense_right(rows, spec["n_cols"], W)
     out, SO = O.dense_left(rows, spec["n_cols"], G)
     R_np = A @ W.astype(np.float64)
