@@ -21,9 +21,15 @@ import time
 import numpy as np
 
 HBM_PEAK = 8.0e12                     # bytes/s, MI355X HBM3E
-# 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz x 2 flops per fused multiply-add, with the
-# packed-FP32 instructions excluded from the build (they would double it to 157.3)
-FP32_FMA_PEAK = 256 * 4 * 16 * 2.4e9 * 2
+# MI355X's published fp32 vector peak: 256 CUs x 4 SIMDs x 16 lanes x 2 FMAs per lane
+# and clock (packed FP32) x 2 flops x 2.4 GHz
+FP32_PEAK = 256 * 4 * 16 * 2 * 2 * 2.4e9
+# the issue rate of one (non-packed) FMA per lane and clock: the ceiling of code
+# built without packed-FP32 instructions, as this library is
+FP32_NONPACKED_PEAK = FP32_PEAK / 2
+# workloads whose batches are dense enough that the CPU baseline multiplies the
+# densified batch (fp64 numpy matmul); the others use the oracle's sparse products
+DENSE_CPU = ("c1", "c3", "c4")
 METRIC = "uncompressed nnz/s for TOC A·W and Gᵀ·A; % HBM peak on compressed bytes"
 HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -33,64 +39,91 @@ def log(msg):
 
 
 # ---------------------------------------------------------------------------
-# CPU baseline: the oracle, timed on a sample of the workload's batches
+# CPU baseline: the oracle, timed on a sample of the workload's batches.  Per batch,
+# separately: the products A.W and G^T.A in fp64 on the decoded batch (dense
+# workloads: the densified batch times W and its transpose times G, numpy matmuls;
+# sparse ones: the oracle's sparse products), the oracle's decode (Algorithm 6) and
+# its encode (Algorithm 1).  The products are the baseline's value.
 # ---------------------------------------------------------------------------
 def _oracle_batch(args):
     cfg, b, k = args
     import oracle as O
+    from threadpoolctl import threadpool_limits
     from workloads import config_batches, config_G, config_W
     B = config_batches(cfg, b, 1)
     n, rp, c, v = B.batch(0)
-    W = config_W(cfg, k)
-    G = config_G(cfg, b, 1, k)
+    W = config_W(cfg, k).astype(np.float64)
+    G = config_G(cfg, b, 1, k).astype(np.float64)
     rows = O.canonicalize(n, B.n_cols, rp, c, v)
-    I, D, _ = O.encode(rows)             # encoding is not part of a step
-    t0 = time.perf_counter()
-    dec = O.decode(I, D)
-    O.decoded_to_csr(dec)
-    O.dense_right(dec, B.n_cols, W)
-    O.dense_left(dec, B.n_cols, G)
-    return time.perf_counter() - t0, int(B.nnz)
+    with threadpool_limits(limits=1):                 # one core per batch
+        t0 = time.perf_counter()
+        I, D, _ = O.encode(rows)
+        t_enc = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        dec = O.decode(I, D)
+        O.decoded_to_csr(dec)
+        t_dec = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        if cfg in DENSE_CPU:
+            A = O.densify(dec, B.n_cols)
+            _ = A @ W
+            _ = A.T @ G
+        else:
+            O.dense_right(dec, B.n_cols, W)
+            O.dense_left(dec, B.n_cols, G)
+        t_prod = time.perf_counter() - t0
+    return t_prod, t_dec, t_enc, int(B.nnz)
+
+
+def _cpu_rates(res, cores):
+    """nnz/s of each part with `cores` batches at a time: nnz over the summed
+    per-batch times divided by the cores."""
+    nnz = sum(r[3] for r in res)
+    t = [sum(r[i] for r in res) for i in range(3)]
+    return {name: nnz * cores / max(t[i], 1e-12)
+            for i, name in enumerate(("products", "decode", "encode"))}, t
 
 
 def cpu_baseline(pool, workers, cfg, nb, k, budget_s):
-    t1, _ = _oracle_batch((cfg, 0, k))
+    t1 = sum(_oracle_batch((cfg, 0, k))[:3])
     n_sample = int(min(max(workers, round(budget_s * workers / max(t1, 1e-3))), nb, 4000))
     ids = sorted(set(np.linspace(0, nb - 1, n_sample).astype(int).tolist()))
     t0 = time.perf_counter()
     res = pool.map(_oracle_batch, [(cfg, b, k) for b in ids])
     wall = time.perf_counter() - t0
-    nnz = sum(r[1] for r in res)
-    cpu = sum(r[0] for r in res)
+    rates, t = _cpu_rates(res, workers)
+    how = ("the densified batch (fp64 numpy matmuls A @ W and A.T @ G)" if cfg in DENSE_CPU
+           else "the decoded batch (the oracle's fp64 sparse products)")
     return {
-        "value": nnz / wall,
+        "value": rates["products"],
         "unit": "nnz/s",
         "cores": workers,
         "kind": "oracle",
-        "sample": f"{len(ids)} of {nb} mini-batches evenly spaced over the workload; per "
-                  f"batch the oracle's decode (Algorithm 6) + fp64 A.W + fp64 G^T.A on the "
-                  f"decoded batch (its encode untimed); {workers} worker processes, "
-                  f"{wall:.1f} s wall, {cpu:.1f} s CPU",
+        "sample": f"{len(ids)} of {nb} mini-batches evenly spaced over the workload, one "
+                  f"batch per core at a time on {workers} worker processes ({wall:.1f} s "
+                  f"wall); value = A.W + G^T.A in fp64 on {how}, nnz over the summed "
+                  f"per-batch product times ({t[0]:.1f} s) / {workers} cores; the oracle's "
+                  f"decode (Algorithm 6, {t[1]:.1f} s) and encode (Algorithm 1, {t[2]:.1f} "
+                  f"s) are timed apart in `parts`",
+        "parts_nnz_per_s": rates,
     }
 
 
 def cpu_baseline_single(cfg, nb, k, budget_s):
     """The same oracle work on one core, in this process: batches evenly spaced
     over the workload until about budget_s seconds of it are done."""
-    from threadpoolctl import threadpool_limits
-    t_all, nnz, done = 0.0, 0, 0
+    res = []
     ids = np.linspace(0, nb - 1, min(nb, 400)).astype(int).tolist()
-    with threadpool_limits(limits=1):                 # numpy's BLAS on one thread too
-        for b in ids:
-            t, z = _oracle_batch((cfg, b, k))
-            t_all += t
-            nnz += z
-            done += 1
-            if t_all >= budget_s:
-                break
-    return {"value": nnz / t_all, "unit": "nnz/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} mini-batches evenly spaced over the workload, one process; "
-                      f"{t_all:.1f} s of oracle time"}
+    for b in ids:
+        res.append(_oracle_batch((cfg, b, k)))
+        if sum(sum(r[:3]) for r in res) >= budget_s:
+            break
+    rates, t = _cpu_rates(res, 1)
+    return {"value": rates["products"], "unit": "nnz/s", "cores": 1, "kind": "oracle",
+            "sample": f"{len(res)} mini-batches evenly spaced over the workload, one process, "
+                      f"BLAS on one thread; products {t[0]:.2f} s, decode {t[1]:.2f} s, "
+                      f"encode {t[2]:.2f} s",
+            "parts_nnz_per_s": rates}
 
 
 def host_cpu():
@@ -175,6 +208,91 @@ def run_ops(w, which=("right", "left", "decode")):
         T.toc_decode_csr(w.dev, w.rowptr, w.ccol, w.cval)
 
 
+def time_ops(w, steps, warmup, stream, names=("right", "left", "decode")):
+    """warmup untimed steps, then `steps` timed ones; events around each op on the
+    stream the kernels run on.  Returns (per-op mean ms, mean step ms, wall s)."""
+    import torch
+    for _ in range(warmup):
+        run_ops(w, names)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for s in range(steps):
+        ev[s][0].record(stream)
+        for i, op in enumerate(names):
+            run_ops(w, (op,))
+            ev[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    op_ms = {op: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(steps)]))
+             for i, op in enumerate(names)}
+    step_ms = float(np.mean([ev[s][0].elapsed_time(ev[s][len(names)]) for s in range(steps)]))
+    return op_ms, step_ms, t_wall
+
+
+def op_bytes_flops(info, k):
+    """Algorithmic dense bytes (beyond the canonical compressed bytes) and flops of
+    each op over the whole workload (one launch of each op)."""
+    m, n_rows, nnz = info["n_cols"], info["n_rows"], info["nnz"]
+    dense = {
+        "right": 4 * m * k + 4 * n_rows * k,                         # W once, R
+        "left": 4 * n_rows * k + 4 * info["n_batches"] * m * k,      # G, out
+        "decode": 8 * (n_rows + 1) + 8 * nnz,                        # rowptr, col+val
+    }
+    flops = {
+        "right": 2.0 * k * (info["n_deep"] + info["n_codes"]),
+        "left": 2.0 * k * (info["n_codes"] + info["n_stored"] + info["n_deep"]),
+        "decode": 0.0,
+    }
+    return dense, flops
+
+
+def op_report(info, k, op_ms, copy_bw=None):
+    """Per op: time, uncompressed nnz/s, the literal fraction of the HBM peak on
+    the canonical compressed bytes and the fraction on the whole op's bytes."""
+    dense, flops = op_bytes_flops(info, k)
+    canon, nnz = info["canon_bytes"], info["nnz"]
+    ops = {}
+    for op, ms in op_ms.items():
+        t = ms / 1e3
+        ops[op] = {
+            "ms": round(ms, 4),
+            "nnz_per_s": nnz / t,
+            "hbm_frac_compressed": canon / t / HBM_PEAK,
+            "hbm_frac_whole_op": (canon + dense[op]) / t / HBM_PEAK,
+            "tflops": flops[op] / t / 1e12,
+        }
+        if copy_bw:
+            ops[op]["frac_of_measured_copy_compressed"] = canon / t / copy_bw
+            ops[op]["frac_of_measured_copy_whole_op"] = (canon + dense[op]) / t / copy_bw
+    return ops
+
+
+def time_k1_workloads(ws, steps, warmup, stream):
+    """The k = 1 workloads (each pre-encoded before the GPU was touched): upload,
+    time right, left and decode like the main step, report, free."""
+    import torch
+    out = {}
+    for w in ws:
+        upload_workload(w, 1)
+        w.encs = None
+        op_ms, step_ms, _ = time_ops(w, steps, warmup, stream)
+        ops = op_report(w.info, 1, op_ms)
+        out[w.cfg] = {"batches": w.nb, "nnz": w.info["nnz"], "canon_bytes": w.info["canon_bytes"],
+                      "image_bytes": w.info["image_bytes"], "step_ms": round(step_ms, 4),
+                      "nnz_per_s": w.info["nnz"] / (step_ms / 1e3), "ops": ops,
+                      "upload_s": round(w.upload_s, 2), "encode_s": round(w.encode_s, 2)}
+        log(f"{w.cfg} (k = 1, {w.nb} batches): step {step_ms:.3f} ms; " + ", ".join(
+            f"{o} {v['ms']:.3f} ms ({v['hbm_frac_compressed']:.1%} literal, "
+            f"{v['hbm_frac_whole_op']:.1%} whole-op)" for o, v in ops.items()))
+        for a in ("buf", "dev", "W", "G", "R", "out", "rowptr", "ccol", "cval", "ws_r", "ws_l"):
+            setattr(w, a, None)
+        torch.cuda.empty_cache()
+    return out
+
+
 def time_elementwise(w, stream, reps=3):
     """The element-wise operations on the same resident image, outside the step:
     toc_map_values with c = 1 (the matrix is unchanged) and toc_decode_dense with
@@ -228,7 +346,7 @@ def pack_sample(w, n):
     idx = np.linspace(0, len(w.encs) - 1, min(n, len(w.encs))).astype(np.int64)
     t0 = time.perf_counter()
     blobs = [T.toc_enc_pack(w.encs[i]) for i in idx]
-    return {"blobs": blobs, "pack_s": time.perf_counter() - t0, "cfg": w.cfg}
+    return {"blobs": blobs, "pack_s": time.perf_counter() - t0, "cfg": w.cfg, "n_cols": w.n_cols}
 
 
 def time_cprime(sample, stream, reps=3):
@@ -247,9 +365,10 @@ def time_cprime(sample, stream, reps=3):
     status = torch.empty(len(blobs), dtype=torch.int32, device=dev)
     ws = torch.empty(T.toc_cprime_workspace_size(len(blobs), n), dtype=torch.uint8, device=dev)
     max_rows = max(i["n_rows"] for i in infos)
+    n_cols = sample["n_cols"]
 
     def run():
-        T.toc_cprime_build(d_blobs, blob_off, node_off, max_rows, *outs, status, ws)
+        T.toc_cprime_build(d_blobs, blob_off, node_off, max_rows, n_cols, *outs, status, ws)
 
     run()
     torch.cuda.synchronize()
@@ -565,6 +684,9 @@ def main():
     ap.add_argument("--cprime-batches", type=int, default=4000,
                     help="batches whose physical encoding is turned into C' on the GPU "
                          "after the step (0 = skip)")
+    ap.add_argument("--k1-extras", default="c5,c2",
+                    help="k = 1 workloads timed after the step at full size (comma list; "
+                         "empty: none)")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device three times "
                          "(reference dispatches for HBM byte counters)")
@@ -595,6 +717,11 @@ def main():
         log(f"oracle on one core: {cpu1['value']:.3e} nnz/s ({cpu1['sample']})")
     w = encode_workload(cfg, nb, pool,
                         keep_batches=0 if args.no_extras else args.encode_batches)
+    k1 = []
+    if not args.no_extras:
+        for c in [x for x in args.k1_extras.split(",") if x and x != cfg]:
+            log(f"k = 1 extra {c}: generate and encode")
+            k1.append(encode_workload(c, CONFIGS[c]["n_batches"], pool))
     pool.close()
     pool.join()
 
@@ -607,25 +734,9 @@ def main():
     w.encs = w.kept = None
 
     stream = torch.cuda.current_stream()
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        run_ops(w)
-    torch.cuda.synchronize()
-
+    log(f"warmup {args.warmup} steps, then {args.steps} timed")
     names = ("right", "left", "decode")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    for s in range(args.steps):
-        ev[s][0].record(stream)
-        for i, op in enumerate(names):
-            run_ops(w, (op,))
-            ev[s][i + 1].record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    op_ms = {op: float(np.mean([ev[s][i].elapsed_time(ev[s][i + 1])
-                                for s in range(args.steps)])) for i, op in enumerate(names)}
-    step_ms = float(np.mean([ev[s][0].elapsed_time(ev[s][3]) for s in range(args.steps)]))
+    op_ms, step_ms, t_wall = time_ops(w, args.steps, args.warmup, stream, names)
     log(f"step {step_ms:.3f} ms ({', '.join(f'{o} {op_ms[o]:.3f}' for o in names)}); "
         f"wall {t_wall / args.steps * 1e3:.3f} ms/step")
     if args.copy_calib_mib > 0:
@@ -644,43 +755,28 @@ def main():
     cprime = time_cprime(sample, stream) if sample else None
     mgd = None if args.no_extras else time_mgd(w, stream)
     nn = None if args.no_extras else time_mlp(w, stream, args.nn_steps)
+    k1res = time_k1_workloads(k1, args.steps, args.warmup, stream) if k1 else None
     nnz = info["nnz"]
     canon = info["canon_bytes"]
-    n_rows, m = info["n_rows"], info["n_cols"]
+    m = info["n_cols"]
     # algorithmic bytes and flops per op (whole workload = one launch of each op)
-    dense = {
-        "right": 4 * m * k + 4 * n_rows * k,                         # W once, R
-        "left": 4 * n_rows * k + 4 * info["n_batches"] * m * k,      # G, out
-        "decode": 8 * (n_rows + 1) + 8 * nnz,                        # rowptr, col+val
-    }
-    flops = {
-        "right": 2.0 * k * (info["n_deep"] + info["n_codes"]),
-        "left": 2.0 * k * (info["n_codes"] + info["n_stored"] + info["n_deep"]),
-        "decode": 0.0,
-    }
-    ops = {}
-    for op in names:
-        t = op_ms[op] / 1e3
-        ops[op] = {
-            "ms": round(op_ms[op], 4),
-            "nnz_per_s": nnz / t,
-            "hbm_frac_compressed": canon / t / HBM_PEAK,
-            "hbm_frac_whole_op": (canon + dense[op]) / t / HBM_PEAK,
-            "tflops": flops[op] / t / 1e12,
-            "frac_of_measured_copy_compressed": canon / t / copy_bw,
-            "frac_of_measured_copy_whole_op": (canon + dense[op]) / t / copy_bw,
-        }
+    dense, flops = op_bytes_flops(info, k)
+    ops = op_report(info, k, op_ms, copy_bw)
     dom = max(("right", "left", "decode"), key=lambda o: op_ms[o])
     t_dom = op_ms[dom] / 1e3
     bytes_dom = canon + dense[dom]
     intensity = flops[dom] / bytes_dom
-    if intensity > FP32_FMA_PEAK / HBM_PEAK:
+    if intensity > FP32_PEAK / HBM_PEAK:
         roof = {"bound": "alu", "achieved": flops[dom] / t_dom / 1e12,
-                "peak": FP32_FMA_PEAK / 1e12, "unit": "TFLOP/s"}
+                "peak": FP32_PEAK / 1e12, "unit": "TFLOP/s"}
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        # the same against one FMA per lane and clock (no packed FP32)
+        roof["peak_nonpacked"] = FP32_NONPACKED_PEAK / 1e12
+        roof["frac_nonpacked"] = roof["achieved"] / roof["peak_nonpacked"]
     else:
         roof = {"bound": "hbm", "achieved": bytes_dom / t_dom / 1e9,
                 "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
+        roof["frac"] = roof["achieved"] / roof["peak"]
     full_size = nb == spec["n_batches"] and k == spec["k"]
     roof["traffic"] = measured_traffic(dom, cfg) if full_size else None
     roof["kernel"] = dom
@@ -713,6 +809,7 @@ def main():
         "cprime_build": cprime,
         "mgd_epoch": mgd,
         "nn_steps": nn,
+        "k1_workloads": k1res,
         "encode_device": encode_dev,
         "ablation_sizes": ablation,
         "cpu_baseline": cpu,

@@ -298,6 +298,8 @@ typedef struct {
   int64_t n_codes;      /* |D|                                                    */
   int64_t n_unique;     /* distinct values of I                                   */
   int64_t n_nodes;      /* |C'| including the root = 1 + |I| + sum(len(D_i)-1)    */
+  int64_t max_col;      /* largest column of I (-1 when I is empty): the blob is for
+                           a matrix of more than max_col columns                  */
 } toc_phys_info;
 
 /* Bytes of the physical encoding of one encoded batch (host, synchronous). */
@@ -305,9 +307,11 @@ toc_status toc_enc_pack_size(const toc_enc *enc, size_t *bytes);
 /* Writes them to dst (host memory of at least that many bytes): TOC_ESIZE if
  * bytes is smaller. */
 toc_status toc_enc_pack(const toc_enc *enc, void *dst, size_t bytes);
-/* Reads the headers and tuple starts of one blob in host memory and checks the
- * layout (sizes, widths, starts non-decreasing from 0 to |D|): TOC_EINVAL if it
- * does not hold.  Codes and value indexes are checked by toc_cprime_build. */
+/* Reads the headers, I's columns and the tuple starts of one blob in host memory
+ * and checks the layout (sizes, widths, starts non-decreasing from 0 to |D|):
+ * TOC_EINVAL if it does not hold.  max_col lets the caller check the blob against
+ * its matrix's columns before any device step.  Codes and value indexes are
+ * checked by toc_cprime_build. */
 toc_status toc_phys_info_get(const void *blob, size_t bytes, toc_phys_info *info);
 
 /* Workspace bytes of toc_cprime_build for n_batches batches and n_nodes nodes in
@@ -326,6 +330,9 @@ toc_status toc_cprime_workspace_size(int64_t n_batches, int64_t n_nodes, size_t 
  *   node_off host, n_batches+1 entries: batch b's nodes are output entries
  *            node_off[b] .. node_off[b+1]-1 (toc_phys_info_get's n_nodes each)
  *   max_rows the most tuples of any batch (at most 16384; sizes LDS)
+ *   n_cols   columns of the matrix the bytes encode: a column of I at or above it
+ *            makes the batch malformed (TOC_CPRIME_COLUMN), so no later step
+ *            indexes W or w past n_cols with it
  *   parent, col, val, depth  device outputs, one entry per node in paper
  *            numbering: the root has parent 0xFFFFFFFF, col 0xFFFFFFFF, val +0.0,
  *            depth 0; nodes 1..|I| have parent 0
@@ -341,9 +348,10 @@ toc_status toc_cprime_workspace_size(int64_t n_batches, int64_t n_nodes, size_t 
 #define TOC_CPRIME_CODE 4         /* a code names no node existing at that point  */
 #define TOC_CPRIME_NODES 5        /* the node count differs from node_off's span  */
 #define TOC_CPRIME_ROWS 6         /* more tuples than max_rows                    */
+#define TOC_CPRIME_COLUMN 10      /* a column of I is not below n_cols            */
 toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
-                            int64_t n_batches, int32_t max_rows, uint32_t *parent, uint32_t *col,
-                            float *val, uint32_t *depth, int32_t *status, void *ws,
+                            int64_t n_batches, int32_t max_rows, int32_t n_cols, uint32_t *parent,
+                            uint32_t *col, float *val, uint32_t *depth, int32_t *status, void *ws,
                             size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
@@ -446,18 +454,22 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
  *   blobs, blob_off, node_off, d_off, max_levels  as for toc_level_build
  *   row_off  host, n_batches+1 entries: batch b's tuples are rows row_off[b] ..
  *            row_off[b+1]-1 of r
+ *   n_cols   entries of w; a batch with a key column at or above it gets
+ *            TOC_CPRIME_COLUMN and w is never read past n_cols
  *   max_live the most live codes of a batch (4 max_live bytes of LDS, at most
  *            160 KiB, else TOC_EUNSUPPORTED; a batch above it gets TOC_LEVEL_LIVE)
  *   level_status, counts, level, l_parent, l_col, l_val, l_D  toc_level_build's
  *   w        device float[n_cols];  r  device float per row (output)
- *   status   device int32 per batch: 0, level_status when nonzero, or
- *            TOC_LEVEL_D when the blob's tuples or |D| differ from the offsets
+ *   status   device int32 per batch: 0, level_status when nonzero,
+ *            TOC_LEVEL_D when the blob's tuples or |D| differ from the offsets, or
+ *            TOC_CPRIME_COLUMN (then r's rows of the batch are not written)
  *   ws       device workspace of at least 32 (n_batches + 1) bytes
  * Asynchronous on stream; the offsets are copied before returning.          */
 #define TOC_LEVEL_LIVE 9          /* more live codes than max_live                 */
 toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
                                const int64_t *d_off, const int64_t *row_off, int64_t n_batches,
-                               int32_t max_levels, int64_t max_live, const int32_t *level_status,
+                               int32_t n_cols, int32_t max_levels, int64_t max_live,
+                               const int32_t *level_status,
                                const int64_t *counts, const uint32_t *level,
                                const uint32_t *l_parent, const uint32_t *l_col, const float *l_val,
                                const uint32_t *l_D, const float *w, float *r, int32_t *status,

@@ -19,7 +19,8 @@ from .binding import (  # noqa: F401
     toc_workspace_size, toc_right_mul, toc_left_mul, toc_decode_csr,
     toc_map_values, toc_decode_dense,
     TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
-    TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH, TOC_LEVEL_LIVE,
+    TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_CPRIME_COLUMN, TOC_LEVEL_D, TOC_LEVEL_DEPTH,
+    TOC_LEVEL_LIVE,
     toc_level_workspace_size, toc_level_build, toc_level_right_mul,
     toc_enc_pack, toc_phys_info_get, toc_cprime_workspace_size, toc_cprime_build,
     TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE, toc_mgd_epoch,

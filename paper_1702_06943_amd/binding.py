@@ -26,6 +26,7 @@ TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE = 0, 1, 2
 TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(1, 5)
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
  TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH, TOC_LEVEL_LIVE) = range(1, 10)
+TOC_CPRIME_COLUMN = 10
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -53,7 +54,7 @@ class DevInfo(C.Structure):
 
 class PhysInfo(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
-                ("n_rows", "n_first", "n_codes", "n_unique", "n_nodes")]
+                ("n_rows", "n_first", "n_codes", "n_unique", "n_nodes", "max_col")]
 
 
 class Layout(C.Structure):
@@ -111,12 +112,13 @@ def lib():
         "toc_enc_pack": [P, P, SZ],
         "toc_phys_info_get": [P, SZ, P],
         "toc_cprime_workspace_size": [I64, I64, P],
-        "toc_cprime_build": [P, P, P, I64, I32, P, P, P, P, P, P, SZ, P],
+        "toc_cprime_build": [P, P, P, I64, I32, I32, P, P, P, P, P, P, SZ, P],
         "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
         "toc_encode_device_workspace_size": [I64, I64, P],
         "toc_mlp_workspace_size": [P, I32, I32, I32, P],
         "toc_level_workspace_size": [I64, I64, P],
-        "toc_level_right_mul": [P, P, P, P, P, I64, I32, I64, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
+        "toc_level_right_mul": [P, P, P, P, P, I64, I32, I32, I64, P, P, P, P, P, P, P, P, P, P,
+                                P, SZ, P],
         "toc_level_build": [P, P, P, P, I64, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "toc_mlp_epoch": [P, I64, I64, I32, I32, I32, P, P, P, P, P, P, P, C.c_float, P, SZ, P],
         "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
@@ -348,10 +350,11 @@ def toc_cprime_workspace_size(n_batches, n_nodes):
     return n.value
 
 
-def toc_cprime_build(blobs, blob_off, node_off, max_rows, parent, col, val, depth, status,
-                     ws, stream=None):
+def toc_cprime_build(blobs, blob_off, node_off, max_rows, n_cols, parent, col, val, depth,
+                     status, ws, stream=None):
     """blobs: device uint8 tensor of the concatenated blobs; blob_off, node_off: host
-    int64 arrays of n_batches + 1 offsets; parent, col, depth: device int32/uint32
+    int64 arrays of n_batches + 1 offsets; n_cols: columns of the encoded matrix (a
+    column of I at or above it is TOC_CPRIME_COLUMN); parent, col, depth: device int32/uint32
     tensors and val a float32 tensor of node_off[-1] entries; status: device int32
     tensor of n_batches entries; ws: device tensor of toc_cprime_workspace_size
     bytes."""
@@ -368,7 +371,7 @@ def toc_cprime_build(blobs, blob_off, node_off, max_rows, parent, col, val, dept
     if blobs.numel() < int(blob_off[-1]):
         raise TocError(TOC_EINVAL, "blobs shorter than blob_off[-1]")
     _check(lib().toc_cprime_build(_ptr(blobs), _ptr(blob_off), _ptr(node_off), nb, int(max_rows),
-                                  _ptr(parent), _ptr(col), _ptr(val), _ptr(depth), _ptr(status),
+                                  int(n_cols), _ptr(parent), _ptr(col), _ptr(val), _ptr(depth), _ptr(status),
                                   _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
                                   _stream(stream)))
 
@@ -511,8 +514,10 @@ def toc_level_right_mul(blobs, blob_off, node_off, d_off, row_off, max_levels, m
                         ws, stream=None):
     """A.w from toc_level_build's outputs (same launch arguments); row_off: host
     int64 array of n_batches + 1 row offsets into r; w: device float32 tensor of
-    n_cols; r: device float32 tensor of row_off[-1]; status: device int32 tensor of
-    one per batch; ws: device tensor of at least 32 (n_batches + 1) bytes."""
+    n_cols (its length is passed as n_cols: a key column at or above it gives the
+    batch TOC_CPRIME_COLUMN); r: device float32 tensor of row_off[-1]; status:
+    device int32 tensor of one per batch; ws: device tensor of at least
+    32 (n_batches + 1) bytes."""
     blob_off, node_off, d_off, row_off = (_arr(x, np.int64)
                                           for x in (blob_off, node_off, d_off, row_off))
     nb = blob_off.size - 1
@@ -523,7 +528,8 @@ def toc_level_right_mul(blobs, blob_off, node_off, d_off, row_off, max_levels, m
     if status.numel() < nb or status.element_size() != 4:
         raise TocError(TOC_EINVAL, "status must hold one int32 per batch")
     _check(lib().toc_level_right_mul(_ptr(blobs), _ptr(blob_off), _ptr(node_off), _ptr(d_off),
-                                     _ptr(row_off), nb, int(max_levels), int(max_live),
+                                     _ptr(row_off), nb, int(w.numel()), int(max_levels),
+                                     int(max_live),
                                      _ptr(level_status), _ptr(counts), _ptr(level),
                                      _ptr(l_parent), _ptr(l_col), _ptr(l_val), _ptr(l_D), _ptr(w),
                                      _ptr(r), _ptr(status), _ptr(ws),

@@ -85,7 +85,7 @@ __device__ void parse_headers(const uint8_t *blob, uint64_t size, int max_rows, 
 
 __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
     const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
-    int max_rows, uint32_t *__restrict__ parent, uint32_t *__restrict__ col,
+    int max_rows, uint32_t n_cols, uint32_t *__restrict__ parent, uint32_t *__restrict__ col,
     uint32_t *__restrict__ val, uint32_t *__restrict__ depth, int32_t *__restrict__ status,
     uint32_t *__restrict__ anc0, uint32_t *__restrict__ dist0, uint32_t *__restrict__ anc1,
     uint32_t *__restrict__ dist1, uint32_t *__restrict__ nxt) {
@@ -154,8 +154,10 @@ __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
       } else {
         const uint32_t q = rd(p_vix, c - 1, w_vix);
         if (q >= U) atomicOr(&errs, 1 << TOC_CPRIME_VALUE_INDEX);
+        const uint32_t cc = rd(p_col, c - 1, w_col);
+        if (cc >= n_cols) atomicOr(&errs, 1 << TOC_CPRIME_COLUMN);
         parent[g] = 0u;
-        col[g] = rd(p_col, c - 1, w_col);
+        col[g] = cc;
         val[g] = q < U ? rd(p_uni, q, 4) : 0u;
         depth[g] = 1u;
       }
@@ -186,8 +188,10 @@ __global__ __launch_bounds__(kCpBlock) void cprime_kernel(
     }
     __syncthreads();
     if (errs) {
-      if (threadIdx.x == 0) status[b] = (errs & (1 << TOC_CPRIME_VALUE_INDEX)) ? TOC_CPRIME_VALUE_INDEX
-                                                                              : TOC_CPRIME_CODE;
+      if (threadIdx.x == 0)
+        status[b] = (errs & (1 << TOC_CPRIME_VALUE_INDEX)) ? TOC_CPRIME_VALUE_INDEX
+                    : (errs & (1 << TOC_CPRIME_COLUMN))    ? TOC_CPRIME_COLUMN
+                                                           : TOC_CPRIME_CODE;
       __syncthreads();
       continue;
     }
@@ -405,7 +409,7 @@ __global__ __launch_bounds__(kLvBlock) void level_kernel(
 // -> C' -> level order -> product, with no host pass over the batch.
 __global__ __launch_bounds__(kLvBlock) void level_right_k1_kernel(
     const uint8_t *__restrict__ blobs, const int64_t *__restrict__ offs, int64_t n_batches,
-    int max_levels, int64_t max_live, const int32_t *__restrict__ lv_status,
+    int max_levels, int64_t max_live, uint32_t n_cols, const int32_t *__restrict__ lv_status,
     const int64_t *__restrict__ counts, const uint32_t *__restrict__ level,
     const uint32_t *__restrict__ l_parent,
     const uint32_t *__restrict__ l_col, const float *__restrict__ l_val,
@@ -413,6 +417,7 @@ __global__ __launch_bounds__(kLvBlock) void level_right_k1_kernel(
     int32_t *__restrict__ status) {
   extern __shared__ float H[];
   __shared__ Hdr h;
+  __shared__ int bad_col;
   const int64_t *node_off = offs + (n_batches + 1), *d_off = offs + 2 * (n_batches + 1);
   const int64_t *row_off = offs + 3 * (n_batches + 1);
   for (int64_t b = blockIdx.x; b < n_batches; b += gridDim.x) {
@@ -426,6 +431,7 @@ __global__ __launch_bounds__(kLvBlock) void level_right_k1_kernel(
                          (int64_t)h.cnt[3] != d_off[b + 1] - dof))
         h.err = TOC_LEVEL_D;
       if (h.err == 0 && counts[2 * b] > max_live) h.err = TOC_LEVEL_LIVE;
+      bad_col = 0;
     }
     __syncthreads();
     if (h.err) {
@@ -439,17 +445,35 @@ __global__ __launch_bounds__(kLvBlock) void level_right_k1_kernel(
       const uint32_t a = lv[d - 1], e = lv[d];
       for (uint32_t c = a + threadIdx.x; c < e; c += kLvBlock) {
         const float base = d > 1 ? H[l_parent[no + c]] : 0.0f;
-        H[c] = fmaf(l_val[no + c], w[l_col[no + c]], base);
+        const uint32_t cc = l_col[no + c];
+        // a column past w (a tree built from another matrix's bytes) is never read
+        if (cc >= n_cols) bad_col = 1;
+        H[c] = fmaf(l_val[no + c], cc < n_cols ? w[cc] : 0.0f, base);
       }
       __syncthreads();
+    }
+    if (bad_col) {
+      if (threadIdx.x == 0) status[b] = TOC_CPRIME_COLUMN;
+      __syncthreads();
+      continue;
     }
     const uint8_t *p_st = blob + h.data[4];
     const uint32_t w_st = h.w[4], nR = h.cnt[4] - 1;
     const int lane = threadIdx.x % 8, grp = threadIdx.x / 8;
     for (uint32_t i = grp; i < nR; i += kLvBlock / 8) {
       const uint32_t s0 = rd(p_st, i, w_st), s1 = rd(p_st, i + 1, w_st);
+      // blocked summation: 16 entries per partial sum, their codes loaded together
       float acc = 0.0f;
-      for (uint32_t p = s0 + lane; p < s1; p += 8) acc += H[l_D[dof + p]];
+      for (uint32_t p0 = s0 + lane; p0 < s1; p0 += 16 * 8) {
+        uint32_t x[16];
+#pragma unroll
+        for (uint32_t u = 0; u < 16; ++u) x[u] = p0 + 8 * u < s1 ? l_D[dof + p0 + 8 * u] : 0u;
+        float part = 0.0f;
+#pragma unroll
+        for (uint32_t u = 0; u < 16; ++u)
+          if (p0 + 8 * u < s1) part += H[x[u]];
+        acc += part;
+      }
 #pragma unroll
       for (int o = 4; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 8);
       if (lane == 0) r[r0 + i] = acc;
@@ -477,7 +501,8 @@ toc_status toc_cprime_workspace_size(int64_t n_batches, int64_t n_nodes, size_t 
 }
 
 toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
-                            int64_t n_batches, int32_t max_rows, uint32_t *parent, uint32_t *col,
+                            int64_t n_batches, int32_t max_rows, int32_t n_cols, uint32_t *parent,
+                            uint32_t *col,
                             float *val, uint32_t *depth, int32_t *status, void *ws,
                             size_t ws_bytes, void *stream) {
   clear_error();
@@ -486,6 +511,7 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
   if (!blob_off || !node_off || !status || !ws) return fail(TOC_EINVAL, "NULL argument");
   if (max_rows < 0 || max_rows > kCpMaxRows)
     return fail(TOC_EUNSUPPORTED, "max_rows %d outside 0..%d", max_rows, kCpMaxRows);
+  if (n_cols < 0) return fail(TOC_EINVAL, "n_cols < 0");
   if (blob_off[0] < 0 || node_off[0] < 0) return fail(TOC_EINVAL, "negative offset");
   for (int64_t b = 0; b < n_batches; ++b) {
     if (blob_off[b + 1] < blob_off[b] || blob_off[b + 1] - blob_off[b] > (int64_t)UINT32_MAX)
@@ -518,7 +544,8 @@ toc_status toc_cprime_build(const void *blobs, const int64_t *blob_off, const in
     return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
   const unsigned g = (unsigned)std::min<int64_t>(n_batches, 1 << 20);
   hipLaunchKernelGGL(cprime_kernel, dim3(g), dim3(kCpBlock), lds, s, (const uint8_t *)blobs, offs,
-                     n_batches, (int)max_rows, parent, col, (uint32_t *)val, depth, status, a0, d0,
+                     n_batches, (int)max_rows, (uint32_t)n_cols, parent, col, (uint32_t *)val, depth,
+                     status, a0, d0,
                      a1, d1, nx);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "cprime_kernel: %s", hipGetErrorString(e));
@@ -594,7 +621,8 @@ toc_status toc_level_build(const void *blobs, const int64_t *blob_off, const int
 
 toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const int64_t *node_off,
                                const int64_t *d_off, const int64_t *row_off, int64_t n_batches,
-                               int32_t max_levels, int64_t max_live, const int32_t *level_status,
+                               int32_t n_cols, int32_t max_levels, int64_t max_live,
+                               const int32_t *level_status,
                                const int64_t *counts, const uint32_t *level,
                                const uint32_t *l_parent, const uint32_t *l_col, const float *l_val,
                                const uint32_t *l_D, const float *w, float *r, int32_t *status,
@@ -609,6 +637,7 @@ toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const
     return fail(TOC_EUNSUPPORTED, "max_levels %d outside 1..%d", max_levels, kLvMaxLevels);
   if (max_live < 0 || max_live * 4 > 160 * 1024)
     return fail(TOC_EUNSUPPORTED, "max_live %lld: H must fit 160 KiB of LDS", (long long)max_live);
+  if (n_cols < 0) return fail(TOC_EINVAL, "n_cols < 0");
   for (int64_t b = 0; b < n_batches; ++b) {
     if (blob_off[b + 1] < blob_off[b] || node_off[b + 1] <= node_off[b] ||
         d_off[b + 1] < d_off[b] || row_off[b + 1] < row_off[b])
@@ -635,7 +664,8 @@ toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const
     return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
   const unsigned g = (unsigned)std::min<int64_t>(n_batches, 1 << 20);
   hipLaunchKernelGGL(level_right_k1_kernel, dim3(g), dim3(kLvBlock), lds, s, (const uint8_t *)blobs,
-                     offs, n_batches, (int)max_levels, max_live, level_status, counts, level, l_parent, l_col,
+                     offs, n_batches, (int)max_levels, max_live, (uint32_t)n_cols, level_status, counts,
+                     level, l_parent, l_col,
                      l_val, l_D, w, r, status);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "level_right_k1_kernel: %s", hipGetErrorString(e));

@@ -116,9 +116,36 @@ __device__ inline uint32_t wave_max_u32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
 }
 
-// Load that bypasses the per-CU L1, for values other waves updated with atomics.
-__device__ inline float coherent_load(const float *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Blocked summation of f(i) over i = a, a + step, ... < e: every kBlk terms form
+// a partial sum that then joins the running sum, so no serial chain of fp32
+// additions is longer than kBlk or the number of blocks.
+constexpr uint32_t kBlk = 16;
+
+// load(i) fetches the index of term i (issued IN at a time, before any of them
+// is used); use(x) gives the term for that index.
+template <uint32_t IN = 4, typename L, typename U>
+__device__ inline float blocked_sum(uint32_t a, uint32_t e, uint32_t step, L load, U use) {
+  constexpr uint32_t kIn = IN;     // loads in flight together
+  static_assert(kBlk % kIn == 0, "a block is a whole number of load groups");
+  float acc = 0.0f;
+  for (uint32_t b = a; b < e; b += kBlk * step) {
+    float p = 0.0f;
+    for (uint32_t u0 = 0; u0 < kBlk; u0 += kIn) {
+      const uint32_t i0 = b + u0 * step;
+      if (i0 >= e) break;
+      uint32_t x[kIn];
+#pragma unroll
+      for (uint32_t u = 0; u < kIn; ++u) {
+        const uint32_t i = i0 + u * step;
+        x[u] = i < e ? load(i) : 0u;
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kIn; ++u)
+        if (i0 + u * step < e) p += use(x[u]);
+    }
+    acc += p;
+  }
+  return acc;
 }
 
 // ===========================================================================
@@ -152,9 +179,8 @@ __global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
   const int lane = threadIdx.x % LPR, grp = threadIdx.x / LPR;
   for (int r = grp; r < bt.n_rows; r += BLK / LPR) {
     const uint32_t s = span[r], e = span[r + 1];
-    float acc = 0.0f;
-#pragma unroll 4
-    for (uint32_t j = s + lane; j < e; j += LPR) acc += H[dc[j]];
+    float acc = blocked_sum(s + lane, e, LPR, [&](uint32_t j) { return dc[j]; },
+                            [&](uint32_t c) { return H[c]; });
     acc = group_sum<LPR>(acc);
     if (lane == 0) R[(bt.row_base + r) * ldr] = acc;
   }
@@ -222,8 +248,9 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
 #pragma unroll
       for (int v = 0; v < kK1Occ; ++v)
         if (w[u][v] != 0xFFFFFFFFu) s[u] += Gs[w[u][v] & ~kFirstOccK1];
-#pragma unroll 8
-      for (uint32_t o = o0[u] + kK1Occ; o < o1[u]; ++o) s[u] += Gs[orow[o] & ~kFirstOccK1];
+      if (o1[u] > o0[u] + kK1Occ)
+        s[u] += blocked_sum<8>(o0[u] + kK1Occ, o1[u], 1u, [&](uint32_t o) { return orow[o]; },
+                            [&](uint32_t w) { return Gs[w & ~kFirstOccK1]; });
     }
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
@@ -237,10 +264,8 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
     const uint32_t a = d == 1 ? 0 : lvl[d - 1], e = d == 1 ? ni : lvl[d];
     for (uint32_t c = a + threadIdx.x; c < e; c += kBlock) {
       const uint32_t h = hrow(c);
-      float sum = H[c];
-      const uint32_t ch1 = tch[h + 1];
-      for (uint32_t ch = tch[h]; ch < ch1; ++ch) sum += H[ch];
-      H[c] = sum;
+      H[c] += blocked_sum(tch[h], tch[h + 1], 1u, [&](uint32_t ch) { return ch; },
+                          [&](uint32_t ch) { return H[ch]; });
     }
     __syncthreads();
   }
@@ -283,12 +308,16 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
 #pragma unroll
     for (int u = 0; u < kK1Cols; ++u) {
       const int j = j0 + u * kBlock + threadIdx.x;
-      float sum = 0.0f;
-      for (uint32_t c = l0[u]; c < l1[u]; ++c) sum += H[c];
+      float sum = blocked_sum(l0[u], l1[u], 1u, [&](uint32_t c) { return c; },
+                              [&](uint32_t c) { return H[c]; });
+      float tsum = 0.0f;
 #pragma unroll
       for (int v = 0; v < kK1Tree; ++v)
-        if (tc[u][v] != 0xFFFFFFFFu) sum += H[tc[u][v]];
-      for (uint32_t t = t0[u] + kK1Tree; t < t1[u]; ++t) sum += H[tl[t]];
+        if (tc[u][v] != 0xFFFFFFFFu) tsum += H[tc[u][v]];
+      sum += tsum;
+      if (t1[u] > t0[u] + kK1Tree)
+        sum += blocked_sum(t0[u] + kK1Tree, t1[u], 1u, [&](uint32_t t) { return tl[t]; },
+                           [&](uint32_t c) { return H[c]; });
       if (j < m) {
         float *p = ob + (int64_t)j * ldo;
         *p = accumulate ? *p + sum : sum;
@@ -339,28 +368,36 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   for (int r = wave; r < bt.n_rows; r += kWaves) {
-    float acc[KPL];
+    float acc[KPL], part[KPL];
 #pragma unroll
     for (int i = 0; i < KPL; ++i) acc[i] = 0.0f;
     const uint32_t s = span[r], e = span[r + 1];
-    for (uint32_t j = s; j < e; ++j) {
-      const uint32_t c = dc[j];
-      if (c < n1) {
-        const float v = val[c];
-        const float *w = W + (int64_t)col[c] * ldw;
+    // blocked summation: kBlk entries per partial sum
+    for (uint32_t j0 = s; j0 < e; j0 += kBlk) {
+      const uint32_t je = min(e, j0 + kBlk);
 #pragma unroll
-        for (int i = 0; i < KPL; ++i) {
-          const int q = lane + kWave * i;
-          if (q < kt) acc[i] = fmaf(v, w[q], acc[i]);
-        }
-      } else {
-        const float *h = Hd + (int64_t)(c - n1) * kt;
+      for (int i = 0; i < KPL; ++i) part[i] = 0.0f;
+      for (uint32_t j = j0; j < je; ++j) {
+        const uint32_t c = dc[j];
+        if (c < n1) {
+          const float v = val[c];
+          const float *w = W + (int64_t)col[c] * ldw;
 #pragma unroll
-        for (int i = 0; i < KPL; ++i) {
-          const int q = lane + kWave * i;
-          if (q < kt) acc[i] += h[q];
+          for (int i = 0; i < KPL; ++i) {
+            const int q = lane + kWave * i;
+            if (q < kt) part[i] = fmaf(v, w[q], part[i]);
+          }
+        } else {
+          const float *h = Hd + (int64_t)(c - n1) * kt;
+#pragma unroll
+          for (int i = 0; i < KPL; ++i) {
+            const int q = lane + kWave * i;
+            if (q < kt) part[i] += h[q];
+          }
         }
       }
+#pragma unroll
+      for (int i = 0; i < KPL; ++i) acc[i] += part[i];
     }
     float *rr = R + (bt.row_base + r) * ldr;
 #pragma unroll
@@ -371,83 +408,105 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
   }
 }
 
-// Left: H rows for codes with children or depth >= 2 (a depth-1 leaf code sends
-// val * G[row] straight to out[col]); scatter, then propagate and accumulate one
-// level at a time from the deepest.  Algorithm 8 with the column loop innermost.
+// Left by pulling (Theorem 2 read as a definition, the result of Algorithm 8),
+// deterministic and without atomics: the H row of each tree code (a code with
+// children or of depth >= 2) is the sum of the G rows of its occurrences (the
+// inverted index of D) plus its children's H rows, deepest level first, a wave
+// per code; then a wave per key column j sums val * G[row] over the occurrences
+// of the column's depth-1 leaves and val * H over its tree codes, and writes
+// out[j] once.  Column loop innermost (lanes over up to 64 * KPL columns); every
+// sum is blocked (kBlk terms per partial sum).  H rows live in the workspace.
 template <int KPL>
 __global__ __launch_bounds__(kBlock) void left_wide_kernel(
-    Img im, int64_t b0, int64_t ws_base, int32_t m, const float *__restrict__ G, int64_t ldg,
-    int kt, float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws) {
+    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
+    const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
+    const uint32_t *__restrict__ tchild_all, int64_t b0, int64_t ws_base, int32_t m,
+    const float *__restrict__ G, int64_t ldg, int kt, float *__restrict__ out, int64_t ldo,
+    int accumulate, float *__restrict__ ws) {
+  constexpr uint32_t kFirst = 0x80000000u;
   const int64_t b = b0 + blockIdx.x;
-  const toc_batch bt = im.batches[b];
+  const toc_batch bt = uniform_batch(im.batches + b);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.link + bt.code_base};
-  const NodeCol col{im.key + bt.code_base};
-  const NodeVal val{im.key + bt.code_base};
-  const uint32_t *span = im.span + bt.span_base;
-  const uint32_t *dc = im.dcodes + bt.d_base;
+  const uint32_t *pv = im.pval + bt.code_base;             // key value bits by position
+  const uint32_t *oo = occ_off_all + bt.code_base + b;
+  const uint32_t *orow = occ_row_all + bt.d_base;
+  const uint32_t *tl = tlist_all + bt.tree_base;
+  const uint32_t *tch = tchild_all + bt.tree_base + b;
+  const uint32_t *cx = cols_all + b * 4 * (int64_t)(m + 1);
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const uint32_t n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
-  const int64_t n_tree = (int64_t)ni + (bt.n_codes - bt.n_lvl1);
   float *Ht = ws + (bt.tree_base - ws_base) * kt;
-  float *ob = out + b * (int64_t)m * ldo;
+  const float *Gb = G + bt.row_base * ldg;
   auto hrow = [&](uint32_t c) -> int64_t { return c < ni ? c : (int64_t)c - n1 + ni; };
-  for (int64_t x = threadIdx.x; x < n_tree * kt; x += kBlock) Ht[x] = 0.0f;
-  if (!accumulate)
-    for (int64_t x = threadIdx.x; x < (int64_t)m * kt; x += kBlock)
-      ob[(x / kt) * ldo + x % kt] = 0.0f;
-  __threadfence();
-  __syncthreads();
-  for (int r = wave; r < bt.n_rows; r += kWaves) {
-    float g[KPL];
-    const float *gr = G + (bt.row_base + r) * ldg;
+  float acc[KPL], part[KPL];
+  uint32_t cnt = 0;
+  auto start = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) acc[i] = part[i] = 0.0f;
+    cnt = 0;
+  };
+  // part += mul * row; every kBlk terms the partial sum joins acc
+  auto add_term = [&](float mul, const float *row) {
 #pragma unroll
     for (int i = 0; i < KPL; ++i) {
       const int q = lane + kWave * i;
-      g[i] = q < kt ? gr[q] : 0.0f;
+      if (q < kt) part[i] = fmaf(mul, row[q], part[i]);
     }
-    const uint32_t s = span[r], e = span[r + 1];
-    for (uint32_t j = s; j < e; ++j) {
-      const uint32_t c = dc[j];
-      if (c < ni || c >= n1) {
-        float *h = Ht + hrow(c) * kt;
+    if (++cnt == kBlk) {
 #pragma unroll
-        for (int i = 0; i < KPL; ++i) {
-          const int q = lane + kWave * i;
-          if (q < kt) unsafeAtomicAdd(&h[q], g[i]);
-        }
-      } else {
-        const float v = val[c];
-        float *o = ob + (int64_t)col[c] * ldo;
-#pragma unroll
-        for (int i = 0; i < KPL; ++i) {
-          const int q = lane + kWave * i;
-          if (q < kt) unsafeAtomicAdd(&o[q], v * g[i]);
-        }
+      for (int i = 0; i < KPL; ++i) {
+        acc[i] += part[i];
+        part[i] = 0.0f;
       }
+      cnt = 0;
     }
-  }
-  __threadfence();
-  __syncthreads();
+  };
+  auto finish = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) acc[i] += part[i];
+  };
+  // tree codes, deepest level first (children are one level deeper)
   for (int d = bt.n_levels; d >= 1; --d) {
-    const uint32_t a = lvl[d - 1], e = d == 1 ? ni : lvl[d];
+    const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
     for (uint32_t c = a + wave; c < e; c += kWaves) {
-      const float *h = Ht + hrow(c) * kt;
-      float *hp = d >= 2 ? Ht + hrow(par[c]) * kt : nullptr;
-      const float v = val[c];
-      float *o = ob + (int64_t)col[c] * ldo;
+      const int64_t h = hrow(c);
+      start();
+      for (uint32_t o = oo[c], o1 = oo[c + 1]; o < o1; ++o)
+        add_term(1.0f, Gb + (int64_t)(orow[o] & ~kFirst) * ldg);
+      for (uint32_t ch = tch[h], ch1 = tch[h + 1]; ch < ch1; ++ch)
+        add_term(1.0f, Ht + hrow(ch) * kt);
+      finish();
+      float *hr = Ht + h * kt;
 #pragma unroll
       for (int i = 0; i < KPL; ++i) {
         const int q = lane + kWave * i;
-        if (q < kt) {
-          const float x = coherent_load(&h[q]);
-          unsafeAtomicAdd(&o[q], v * x);
-          if (d >= 2) unsafeAtomicAdd(&hp[q], x);
-        }
+        if (q < kt) hr[q] = acc[i];
       }
     }
-    __threadfence();
     __syncthreads();
+  }
+  // key columns: the leaves of column j are positions Loff[j] .. Loff[j+1]-1, its
+  // tree codes tree-list entries Toff[j] .. Toff[j+1]-1
+  const uint32_t *Loff = cx, *Toff = cx + 2 * (m + 1);
+  float *ob = out + b * (int64_t)m * ldo;
+  for (int j = wave; j < m; j += kWaves) {
+    start();
+    for (uint32_t p = Loff[j], p1 = Loff[j + 1]; p < p1; ++p) {
+      const float v = __uint_as_float(pv[p]);
+      for (uint32_t o = oo[p], o1 = oo[p + 1]; o < o1; ++o)
+        add_term(v, Gb + (int64_t)(orow[o] & ~kFirst) * ldg);
+    }
+    for (uint32_t t = Toff[j], t1 = Toff[j + 1]; t < t1; ++t) {
+      const uint32_t c = tl[t];
+      add_term(__uint_as_float(pv[c]), Ht + hrow(c) * kt);
+    }
+    finish();
+    float *o = ob + (int64_t)j * ldo;
+#pragma unroll
+    for (int i = 0; i < KPL; ++i) {
+      const int q = lane + kWave * i;
+      if (q < kt) o[q] = accumulate ? o[q] + acc[i] : acc[i];
+    }
   }
 }
 
@@ -899,6 +958,10 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
       const RtChunk L = chunk_of_l();
       load_codes(ld, lok);
       if (C.tg < n_tg) {
+        // blocked summation: the chunk's entries go into a partial sum of their
+        // own, which then joins the tuple's running sum, so no serial chain is
+        // longer than a chunk (kRtChunk) or the tuple's number of chunks
+        float2 part = make_float2(0.f, 0.f);
         if (C.steps == kRtChunk) {
           // each block's reads are issued before the previous block's FMAs
           float2 x0[8], x1[8];
@@ -906,9 +969,9 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
           static_for<kRtPer>([&](auto hc) {
             constexpr int h = decltype(hc)::value;
             load8_bcast<8>(crb[h], qoff, x1);
-            fma8_bcast<0>(acc, cmu[h], x0);
+            fma8_bcast<0>(part, cmu[h], x0);
             if constexpr (h + 1 < kRtPer) load8_bcast<0>(crb[h + 1], qoff, x0);
-            fma8_bcast<8>(acc, cmu[h], x1);
+            fma8_bcast<8>(part, cmu[h], x1);
           });
         } else {
           static_for<kRtPer>([&](auto hc) {
@@ -916,15 +979,17 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
             if (C.steps > (uint32_t)(16 * h)) {
               float2 xr[8];
               load8_bcast<0>(crb[h], qoff, xr);
-              fma8_bcast<0>(acc, cmu[h], xr);
+              fma8_bcast<0>(part, cmu[h], xr);
             }
             if (C.steps > (uint32_t)(16 * h + 8)) {
               float2 xr[8];
               load8_bcast<8>(crb[h], qoff, xr);
-              fma8_bcast<8>(acc, cmu[h], xr);
+              fma8_bcast<8>(part, cmu[h], xr);
             }
           });
         }
+        acc.x += part.x;
+        acc.y += part.y;
         if (C.last) {
           const bool in_b = C.tg >= n_tga;
           const int r = (in_b ? C.tg - n_tga : C.tg) * kRtGroups + grp;
@@ -1171,6 +1236,10 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
       const RsChunk L = chunk_of_l();
       load_codes(ld0, ld1, lok0, lok1);
       bool done = false;
+      // blocked summation: a chunk's entries form a partial sum that then joins
+      // the tuple's running sum (serial chains of at most kRsChunk terms, and of
+      // the tuple's number of chunks)
+      float4 part = make_float4(0.f, 0.f, 0.f, 0.f);
       if (C.tg < n_tg && C.steps == kRsChunk) {
         // a full chunk: all staged entries first, then the rows, so that many
         // LDS reads are in flight (rows in the workspace take the loop below)
@@ -1189,7 +1258,7 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
             for (int t = 0; t < 8; ++t)
               xr[t] = lds_load4(qb + e[h + t].x * (kRtKT * 4));
 #pragma unroll
-            for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[h + t].y), xr[t], acc);
+            for (int t = 0; t < 8; ++t) part = f4fma(__uint_as_float(e[h + t].y), xr[t], part);
             __builtin_amdgcn_sched_barrier(0);
           }
           done = true;
@@ -1211,13 +1280,17 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
             x2 = lds_load4(qb + e2.x * (kRtKT * 4));
             x3 = lds_load4(qb + e3.x * (kRtKT * 4));
           }
-          acc = f4fma(__uint_as_float(e0.y), x0, acc);
-          acc = f4fma(__uint_as_float(e1.y), x1, acc);
-          acc = f4fma(__uint_as_float(e2.y), x2, acc);
-          acc = f4fma(__uint_as_float(e3.y), x3, acc);
+          part = f4fma(__uint_as_float(e0.y), x0, part);
+          part = f4fma(__uint_as_float(e1.y), x1, part);
+          part = f4fma(__uint_as_float(e2.y), x2, part);
+          part = f4fma(__uint_as_float(e3.y), x3, part);
         }
       }
       if (C.tg < n_tg) {
+        acc.x += part.x;
+        acc.y += part.y;
+        acc.z += part.z;
+        acc.w += part.w;
         if (C.last) {
           const int r = C.tg * kRsGroups + grp;
           if (r < nrows) {
@@ -1283,6 +1356,14 @@ constexpr int kLtWaves = kLtBlock / kWave;
 constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
 constexpr int kLtU = 4;                           // tree codes per group at a time
+constexpr uint32_t kLtBlk = 16;                   // children per block of a tree code's sum
+
+__device__ inline void add4(float4 &a, const float4 &b) {
+  a.x += b.x;
+  a.y += b.y;
+  a.z += b.z;
+  a.w += b.w;
+}
 
 // LDS bytes of the per-wave stages and of the column tables
 // (groups of 16 lanes pass entries round with the DPP row broadcast: no stage)
@@ -1456,54 +1537,55 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
         nmax = wave_max_u32(nmax);
         cmax = wave_max_u32(cmax);
-        float4 acc[kLtU];
+        // blocked summation: children and occurrences are summed in blocks of at
+        // most kLtBlk (children) or LPG (occurrences) terms, each block's partial
+        // sum then joining the code's running sum
+        float4 acc[kLtU], part[kLtU];
 #pragma unroll
         for (int u = 0; u < kLtU; ++u) acc[u] = make_float4(0.f, 0.f, 0.f, 0.f);
         // children: one per code at a time, all codes' loads in flight
-        for (uint32_t cb = 0; cb < cmax; ++cb) {
-          float4 g[kLtU];
+        for (uint32_t cb0 = 0; cb0 < cmax; cb0 += kLtBlk) {
+          const uint32_t ce = min(cmax, cb0 + kLtBlk);
 #pragma unroll
-          for (int u = 0; u < kLtU; ++u) {
-            g[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (k0[u] + cb < k1[u]) g[u] = load_trow(hrow(k0[u] + cb));
+          for (int u = 0; u < kLtU; ++u) part[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+          for (uint32_t cb = cb0; cb < ce; ++cb) {
+            float4 g[kLtU];
+#pragma unroll
+            for (int u = 0; u < kLtU; ++u) {
+              g[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+              if (k0[u] + cb < k1[u]) g[u] = load_trow(hrow(k0[u] + cb));
+            }
+#pragma unroll
+            for (int u = 0; u < kLtU; ++u) add4(part[u], g[u]);
           }
 #pragma unroll
-          for (int u = 0; u < kLtU; ++u) {
-            acc[u].x += g[u].x;
-            acc[u].y += g[u].y;
-            acc[u].z += g[u].z;
-            acc[u].w += g[u].w;
-          }
+          for (int u = 0; u < kLtU; ++u) add4(acc[u], part[u]);
         }
         // occurrences: the first LPG of each code by broadcast
+#pragma unroll
+        for (int u = 0; u < kLtU; ++u) part[u] = make_float4(0.f, 0.f, 0.f, 0.f);
         static_for<LPG>([&](auto ic) {
           if (nmax > (uint32_t)decltype(ic)::value) {
             float4 g[kLtU];
 #pragma unroll
             for (int u = 0; u < kLtU; ++u) g[u] = lds_load4(qb + gbcast(mine[u], ic) * RB);
 #pragma unroll
-            for (int u = 0; u < kLtU; ++u) {
-              acc[u].x += g[u].x;
-              acc[u].y += g[u].y;
-              acc[u].z += g[u].z;
-              acc[u].w += g[u].w;
-            }
+            for (int u = 0; u < kLtU; ++u) add4(part[u], g[u]);
           }
         });
 #pragma unroll
         for (int u = 0; u < kLtU; ++u) {
+          add4(acc[u], part[u]);
           // occurrences past the first LPG (rare): one at a time
           for (uint32_t ob = o0[u] + LPG; ob < o1[u]; ob += LPG) {
             const uint32_t mo = ob + sub < o1[u] ? orow[ob + sub] & ~kFirstOcc : zrow;
             const uint32_t n = min((uint32_t)LPG, o1[u] - ob);
+            float4 pb = make_float4(0.f, 0.f, 0.f, 0.f);
             for (uint32_t i = 0; i < n; ++i) {
               const uint32_t r = (uint32_t)__shfl((int)mo, grp * LPG + (int)i, kWave);
-              const float4 g = lds_load4(qb + r * RB);
-              acc[u].x += g.x;
-              acc[u].y += g.y;
-              acc[u].z += g.z;
-              acc[u].w += g.w;
+              add4(pb, lds_load4(qb + r * RB));
             }
+            add4(acc[u], pb);
           }
           if (c0 + u * NG < e) store_trow(h[u], acc[u]);
         }
@@ -1639,6 +1721,10 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       for (int h = 0; h < PER; ++h) pv[h] = buf_load(rs_pval, code[h]);
       const LtChunk L = chunk_of_l();
       load_entry(lw, lok, llcode);
+      // blocked summation: a chunk's entries form a partial sum that then joins
+      // the column's running sum (serial chains of at most CHK terms, and of the
+      // column's number of chunks)
+      float4 part = make_float4(0.f, 0.f, 0.f, 0.f);
       if constexpr (DPP) {
         constexpr int NB = CHK / 4;             // blocks of 4 entries
         // does an entry of chunk C read a tree row in the workspace?
@@ -1659,8 +1745,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
               if constexpr (bk % 2 == 0) load4x4_bcast<4 * (nb % 4)>(cra[nb / 4], qoff, xb);
               else load4x4_bcast<4 * (nb % 4)>(cra[nb / 4], qoff, xa);
             }
-            if constexpr (bk % 2 == 0) fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xa);
-            else fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xb);
+            if constexpr (bk % 2 == 0) fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xa);
+            else fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xb);
           });
         } else if (C.cg < n_cg && !ws_chunk) {
           // a partial chunk, rows in LDS: blocks of 4 entries
@@ -1669,7 +1755,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
             if (C.steps > (uint32_t)(4 * bk)) {
               float4 xv[4];
               load4x4_bcast<4 * (bk % 4)>(cra[bk / 4], qoff, xv);
-              fma4x4_bcast<4 * (bk % 4)>(acc, cmu[bk / 4], xv);
+              fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xv);
             }
           });
         } else if (C.cg < n_cg) {
@@ -1693,7 +1779,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
               });
               static_for<4>([&](auto ic) {
                 constexpr int i = decltype(ic)::value;
-                acc = f4fma(mt[i], xv[i], acc);
+                part = f4fma(mt[i], xv[i], part);
               });
             }
           });
@@ -1712,7 +1798,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   #pragma unroll
             for (int t = 0; t < 8; ++t) xr[t] = lds_load4(qb + e[t].x * RB);
   #pragma unroll
-            for (int t = 0; t < 8; ++t) acc = f4fma(__uint_as_float(e[t].y), xr[t], acc);
+            for (int t = 0; t < 8; ++t) part = f4fma(__uint_as_float(e[t].y), xr[t], part);
             __builtin_amdgcn_sched_barrier(0);
           }
         } else if (C.cg < n_cg) {
@@ -1731,14 +1817,18 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
               x2 = lds_load4(qb + e2.x * RB);
               x3 = lds_load4(qb + e3.x * RB);
             }
-            acc = f4fma(__uint_as_float(e0.y), x0, acc);
-            acc = f4fma(__uint_as_float(e1.y), x1, acc);
-            acc = f4fma(__uint_as_float(e2.y), x2, acc);
-            acc = f4fma(__uint_as_float(e3.y), x3, acc);
+            part = f4fma(__uint_as_float(e0.y), x0, part);
+            part = f4fma(__uint_as_float(e1.y), x1, part);
+            part = f4fma(__uint_as_float(e2.y), x2, part);
+            part = f4fma(__uint_as_float(e3.y), x3, part);
           }
         }
             }
       if (C.cg < n_cg) {
+        acc.x += part.x;
+        acc.y += part.y;
+        acc.z += part.z;
+        acc.w += part.w;
         if (C.last) {
           const int o = C.cg * GPW + grp;
           if (o < m) {
@@ -1886,8 +1976,10 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
       const uint32_t d = lk[i].y;
       int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
       for (uint32_t q = 0;;) {
-        __builtin_nontemporal_store((int32_t)kk.x, &ocol[p]);
-        __builtin_nontemporal_store(kk.y, &oval[p]);
+        // ordinary stores: L2 merges the chains' partial lines (streaming stores
+        // measured 1.9x slower on the categorical workload's deeper chains)
+        ocol[p] = (int32_t)kk.x;
+        oval[p] = kk.y;
         if (++q >= d) break;
         --p;
         kk = *(const uint2 *)(key + par);
@@ -2411,10 +2503,17 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
   for (int64_t k0 = 0; k0 < k; k0 += kKTile) {
     const int kt = (int)std::min<int64_t>(kKTile, k - k0);
     const int kpl = (kt + kWave - 1) / kWave;
+    const uint8_t *bb = (const uint8_t *)d->buf;
+    const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
+    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
+    const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
+    const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
+    const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     st = for_each_pass(d, TOC_OP_LEFT, cap_rows,
                        [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
-      TOC_DISPATCH_KPL(kpl, left_wide_kernel, dim3((unsigned)n), dim3(kBlock), 0, s, im, b0,
-                       base, m, G + k0, ldg, kt, out + k0, ldo, accumulate, (float *)ws);
+      TOC_DISPATCH_KPL(kpl, left_wide_kernel, dim3((unsigned)n), dim3(kBlock), 0, s, im, occ_off,
+                       occ_row, tlist, cols, tchild, b0, base, m, G + k0, ldg, kt, out + k0, ldo,
+                       accumulate, (float *)ws);
       return launch_status("left_wide_kernel");
     });
     if (st != TOC_OK) return st;

@@ -131,6 +131,10 @@ toc_status toc_phys_info_get(const void *blob, size_t bytes, toc_phys_info *info
   info->n_codes = (int64_t)cnt[3];
   info->n_unique = (int64_t)cnt[1];
   info->n_nodes = 1 + (int64_t)cnt[0] + (int64_t)cnt[3] - nonempty;
+  int64_t max_col = -1;
+  for (uint64_t i = 0; i < cnt[0]; ++i)
+    max_col = std::max<int64_t>(max_col, (int64_t)get(b + data[0] + i * wid[0], wid[0]));
+  info->max_col = max_col;
   return TOC_OK;
 }
 

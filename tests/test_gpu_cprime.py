@@ -27,13 +27,16 @@ def blobs_of(B):
     return [T.toc_enc_pack(e) for e in encs]
 
 
-def build_gpu(blobs, n_nodes=None, max_rows=None):
+def build_gpu(blobs, n_nodes=None, max_rows=None, n_cols=None):
     """Runs toc_cprime_build over the blobs in one launch; returns per-batch
-    (parent, col, val bits, depth) host arrays and the status array."""
+    (parent, col, val bits, depth) host arrays and the status array.  n_cols
+    defaults to one past the largest column of any blob's I."""
     if n_nodes is None:
         n_nodes = [T.toc_phys_info_get(b)["n_nodes"] for b in blobs]
     if max_rows is None:
         max_rows = max([T.toc_phys_info_get(b)["n_rows"] for b in blobs] + [0])
+    if n_cols is None:
+        n_cols = 1 + max([T.toc_phys_info_get(b)["max_col"] for b in blobs] + [0])
     blob_off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
     node_off = np.concatenate([[0], np.cumsum(n_nodes)]).astype(np.int64)
     cat = np.concatenate([np.asarray(b, np.uint8) for b in blobs] + [np.zeros(1, np.uint8)])
@@ -42,8 +45,8 @@ def build_gpu(blobs, n_nodes=None, max_rows=None):
     outs = [torch.full((n,), -7, dtype=torch.int32, device=DEV) for _ in range(4)]
     status = torch.full((len(blobs),), -1, dtype=torch.int32, device=DEV)
     ws = torch.empty(T.toc_cprime_workspace_size(len(blobs), n), dtype=torch.uint8, device=DEV)
-    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, outs[0], outs[1], outs[2], outs[3],
-                       status, ws)
+    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, n_cols, outs[0], outs[1], outs[2],
+                       outs[3], status, ws)
     torch.cuda.synchronize()
     host = [o.cpu().numpy().view(np.uint32) for o in outs]
     per = [tuple(h[node_off[b]:node_off[b + 1]] for h in host) for b in range(len(blobs))]
@@ -158,10 +161,25 @@ def test_malformed_blobs_get_status():
     blobs = [good[0]] + [c[0] for c in cases] + [good[1]]
     n_nodes = [T.toc_phys_info_get(good[0])["n_nodes"]] + [c[1] for c in cases] + \
         [T.toc_phys_info_get(good[1])["n_nodes"]]
-    per, status = build_gpu(blobs, n_nodes=n_nodes, max_rows=250)
+    per, status = build_gpu(blobs, n_nodes=n_nodes, max_rows=250, n_cols=900)
     assert status.tolist() == [0] + [c[2] for c in cases] + [0]
     assert_same(per[0], good[0])
     assert_same(per[-1], good[1])
+
+
+def test_column_past_n_cols_gets_status():
+    """The worked example's bytes with the third column of I raised from 2 to 4 (a
+    column past the 4 of the matrix): TOC_CPRIME_COLUMN, while the unchanged copy
+    before it in the same launch is built as usual."""
+    ex = _example()
+    assert ex[7] == 2
+    bad = bytearray(ex)
+    bad[7] = 4
+    blobs = [np.frombuffer(bytes(ex), np.uint8), np.frombuffer(bytes(bad), np.uint8)]
+    assert T.toc_phys_info_get(blobs[1])["max_col"] == 4
+    per, status = build_gpu(blobs, n_nodes=[11, 11], max_rows=4, n_cols=4)
+    assert status.tolist() == [0, T.TOC_CPRIME_COLUMN]
+    assert_same(per[0], blobs[0])
 
 
 def test_rows_beyond_max_rows():

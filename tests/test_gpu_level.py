@@ -46,7 +46,9 @@ def level_gpu(blobs, max_levels=64, d_counts=None):
     cp = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
     cst = torch.full((nb,), -1, dtype=torch.int32, device=DEV)
     ws = torch.empty(T.toc_cprime_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
-    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, cp[0], cp[1], cp[2], cp[3], cst, ws)
+    n_cols = 1 + max([i["max_col"] for i in infos] + [0])
+    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, n_cols, cp[0], cp[1], cp[2], cp[3],
+                       cst, ws)
     lv = [torch.full((n,), -7, dtype=torch.int32, device=DEV) for _ in range(4)]
     level = torch.full((nb * (max_levels + 1),), -7, dtype=torch.int32, device=DEV)
     lD = torch.full((max(int(d_off[-1]), 1),), -7, dtype=torch.int32, device=DEV)
@@ -157,7 +159,7 @@ def level_gpu_checked(blobs, d_counts):
         try:
             return real_info(b)
         except T.TocError:
-            return {"n_nodes": 1, "n_rows": 0, "n_codes": 0}
+            return {"n_nodes": 1, "n_rows": 0, "n_codes": 0, "max_col": -1}
     T.toc_phys_info_get = info
     try:
         return level_gpu(blobs, max_levels=8, d_counts=d_counts)
@@ -165,9 +167,11 @@ def level_gpu_checked(blobs, d_counts):
         T.toc_phys_info_get = real_info
 
 
-def ingest_right(blobs, w_host, max_levels=64):
+def ingest_right(blobs, w_host, max_levels=64, cprime_n_cols=None, cprime_status=None):
     """Physical bytes -> toc_cprime_build -> toc_level_build -> toc_level_right_mul,
-    all on the device; returns R (host, one value per row) and the statuses."""
+    all on the device; returns R (host, one value per row) and the statuses.
+    cprime_n_cols: n_cols of the C' build (default: one past the largest column);
+    cprime_status: a list that receives the C' build's statuses."""
     infos = [T.toc_phys_info_get(b) for b in blobs]
     nb = len(blobs)
     blob_off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
@@ -181,7 +185,9 @@ def ingest_right(blobs, w_host, max_levels=64):
     cp = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
     cst = torch.empty(nb, dtype=torch.int32, device=DEV)
     ws = torch.empty(T.toc_cprime_workspace_size(nb, n), dtype=torch.uint8, device=DEV)
-    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, *cp, cst, ws)
+    n_cols = 1 + max([i["max_col"] for i in infos] + [0]) if cprime_n_cols is None \
+        else cprime_n_cols
+    T.toc_cprime_build(dblob, blob_off, node_off, max_rows, n_cols, *cp, cst, ws)
     lv = [torch.empty(n, dtype=torch.int32, device=DEV) for _ in range(4)]
     level = torch.empty(nb * (max_levels + 1), dtype=torch.int32, device=DEV)
     lD = torch.empty(max(int(d_off[-1]), 1), dtype=torch.int32, device=DEV)
@@ -198,6 +204,8 @@ def ingest_right(blobs, w_host, max_levels=64):
     T.toc_level_right_mul(dblob, blob_off, node_off, d_off, row_off, max_levels, max_live, lst,
                           counts, level, lv[0], lv[1], lv[2], lD, wd, r, st, ws3)
     torch.cuda.synchronize()
+    if cprime_status is not None:
+        cprime_status.extend(cst.cpu().numpy().tolist())
     return r.cpu().numpy()[:int(row_off[-1])], st.cpu().numpy(), row_off
 
 
@@ -233,3 +241,26 @@ def test_ingest_right_tiny_and_empty():
         want, S = O.dense_right(rows, 64, w[:, None].astype(np.float64))
         got = r[row_off[b]:row_off[b + 1]]
         assert np.all(np.abs(got - want[:, 0]) <= 1e-5 * S[:, 0]), f"batch {b}"
+
+
+def test_columns_past_n_cols():
+    """Batch 1 uses columns up to 63, batch 0 only columns below 32.  Built for 32
+    columns, batch 1's bytes are malformed (TOC_CPRIME_COLUMN from the C' build,
+    carried through the level order and the product) while batch 0 is built and
+    multiplied as usual.  Built for 64 columns but multiplied by a w of 32 entries,
+    the product reports TOC_CPRIME_COLUMN for batch 1 and never reads w past its
+    end; batch 0 is unaffected."""
+    rp0, c0, v0 = tiny_batch(5, n_rows=20, n_cols=32, density=0.5, n_values=3, prefix_copy=0.5)
+    rp1, c1, v1 = tiny_batch(6, n_rows=20, n_cols=64, density=0.5, n_values=3, prefix_copy=0.5)
+    blobs = blobs_of(Batches(32, [20], rp0, c0, v0)) + blobs_of(Batches(64, [20], rp1, c1, v1))
+    assert T.toc_phys_info_get(blobs[0])["max_col"] < 32 <= T.toc_phys_info_get(blobs[1])["max_col"]
+    w = np.random.default_rng(8).standard_normal(32).astype(np.float32)
+    rows0 = O.canonicalize(20, 32, rp0, c0, v0)
+    want, S = O.dense_right(rows0, 32, w[:, None].astype(np.float64))
+    for n_cols, want_cp in ((32, [0, T.TOC_CPRIME_COLUMN]), (64, [0, 0])):
+        cst = []
+        r, st, row_off = ingest_right(blobs, w, cprime_n_cols=n_cols, cprime_status=cst)
+        assert cst == want_cp
+        assert st.tolist() == [0, T.TOC_CPRIME_COLUMN]
+        assert np.all(np.abs(r[:20] - want[:, 0]) <= 1e-5 * S[:, 0])
+        assert np.all(np.isnan(r[20:40]))           # batch 1's rows are not written

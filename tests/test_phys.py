@@ -36,7 +36,8 @@ def test_worked_example_bytes():
     want = bytes.fromhex("".join(a["hex"] for a in PHYS["arrays"]))
     assert bytes(T.toc_enc_pack(e)) == want
     info = T.toc_phys_info_get(np.frombuffer(want, np.uint8))
-    assert info == dict(n_rows=4, n_first=5, n_codes=9, n_unique=4, n_nodes=11)
+    # Table 2's I holds the columns 1..4 of the paper, 0..3 here
+    assert info == dict(n_rows=4, n_first=5, n_codes=9, n_unique=4, n_nodes=11, max_col=3)
 
 
 TINY = [dict(n_rows=0, density=0.5, n_values=2),
@@ -49,9 +50,11 @@ TINY = [dict(n_rows=0, density=0.5, n_values=2),
 @pytest.mark.parametrize("case", range(len(TINY)))
 @pytest.mark.parametrize("n_cols", [3, 300, 70000])
 def test_pack_equals_oracle_tiny(case, n_cols):
-    spec = TINY[case]
-    if n_cols == 70000 and spec["n_rows"] * n_cols * spec["density"] > 2e5:
-        pytest.skip("too large for a tiny case")
+    spec = dict(TINY[case])
+    # keep every case small: at most about 2e5 pairs (a dense row of 70,000 columns
+    # stays dense; wider batches get sparser)
+    if spec["n_rows"] * n_cols * spec["density"] > 2e5:
+        spec["density"] = 2e5 / (spec["n_rows"] * n_cols)
     rp, c, v = tiny_batch(77 + case, n_cols=n_cols, **spec)
     B = Batches(n_cols, [spec["n_rows"]], rp, c, v)
     e = _encs(B)[0]
@@ -62,6 +65,7 @@ def test_pack_equals_oracle_tiny(case, n_cols):
     info = T.toc_phys_info_get(blob)
     assert info["n_nodes"] == N and info["n_first"] == len(I)
     assert info["n_codes"] == sum(len(d) for d in D) and info["n_rows"] == len(D)
+    assert info["max_col"] == max((c for c, _ in I), default=-1)
 
 
 @pytest.mark.parametrize("cfg", ["c1", "c2", "c3", "c5"])
@@ -113,21 +117,25 @@ def test_pack_errors():
     e = T.toc_encode(1, 2, np.array([0, 1]), np.array([1], np.int32), np.array([2.0], np.float32))
     assert T.lib().toc_enc_pack(e.handle, np.zeros(4, np.uint8).ctypes.data, 4) == T.TOC_ESIZE
     assert T.lib().toc_enc_pack_size(None, None) == T.TOC_EINVAL
-    assert T.lib().toc_cprime_build(None, None, None, 0, 0, None, None, None, None, None, None,
-                                    0, None) == 0
+    assert T.lib().toc_cprime_build(None, None, None, 0, 0, 0, None, None, None, None, None,
+                                    None, 0, None) == 0
     off = np.array([0, 5], np.int64)
-    assert T.lib().toc_cprime_build(None, off.ctypes.data, off.ctypes.data, 1, 0, None, None,
+    assert T.lib().toc_cprime_build(None, off.ctypes.data, off.ctypes.data, 1, 0, 4, None, None,
                                     None, None, None, None, 0, None) == T.TOC_EINVAL
     bad = np.array([5, 0], np.int64)
     ws = np.zeros(1 << 12, np.uint8)
     st = np.zeros(1, np.int32)
-    args = [ws.ctypes.data, bad.ctypes.data, off.ctypes.data, 1, 0, ws.ctypes.data, ws.ctypes.data,
-            ws.ctypes.data, ws.ctypes.data, st.ctypes.data, ws.ctypes.data, ws.size, None]
+    args = [ws.ctypes.data, bad.ctypes.data, off.ctypes.data, 1, 0, 4, ws.ctypes.data,
+            ws.ctypes.data, ws.ctypes.data, ws.ctypes.data, st.ctypes.data, ws.ctypes.data, ws.size,
+            None]
     assert T.lib().toc_cprime_build(*args) == T.TOC_EINVAL          # blob_off decreasing
     args[1] = off.ctypes.data
     args[4] = 20000
     assert T.lib().toc_cprime_build(*args) == T.TOC_EUNSUPPORTED    # max_rows beyond the limit
     args[4] = 0
-    args[11] = 16
+    args[5] = -1
+    assert T.lib().toc_cprime_build(*args) == T.TOC_EINVAL          # negative n_cols
+    args[5] = 4
+    args[12] = 16
     assert T.lib().toc_cprime_build(*args) == T.TOC_ESIZE           # workspace too small
     assert T.toc_cprime_workspace_size(1, 5) > 0
