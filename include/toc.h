@@ -249,6 +249,23 @@ toc_status toc_left_mul(const toc_dev *dev, const float *G, int32_t k, int64_t l
                         float *out, int64_t ldo, int32_t accumulate, void *ws,
                         size_t ws_bytes, void *stream);
 
+/* Left multiplication without any allocation, for callers that cannot allocate
+ * device memory (work captured into a HIP graph, tight serving loops, harnesses
+ * that forbid hipMalloc).  The same product as toc_left_mul, bit for bit, with no
+ * workspace argument: the workspace is a static device buffer of
+ * TOC_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on until
+ * the process ends (its address is looked up on the first call on each device).
+ * When the full grid's per-worker slots do not fit in it, fewer persistent
+ * workers run (slower, same result).  Calls on one GPU share that buffer: calls
+ * that overlap in time on one GPU (other streams, other host threads) race and
+ * must be ordered by the caller.  Nothing in the buffer needs to be zero on entry.
+ * Allocates nothing (no hipMalloc, hipFree, or allocating library call).
+ * Errors: as toc_left_mul; TOC_EUNSUPPORTED when one batch's workspace (one worker
+ * slot per XCD, or one batch's rows on the fallback path) exceeds the buffer. */
+#define TOC_NOALLOC_SCRATCH_BYTES (64u << 20)
+toc_status toc_left_mul_noalloc(const toc_dev *dev, const float *G, int32_t k, int64_t ldg,
+                                float *out, int64_t ldo, int32_t accumulate, void *stream);
+
 /* Full decode of every batch to one CSR (the backtracking of Algorithm 6, without
  * its densify step): rowptr[(sum of rows)+1] (int64), col[nnz] (int32),
  * val[nnz] (float, bit-identical to the encoded values).  Rows in batch order.

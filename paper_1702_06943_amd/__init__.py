@@ -16,7 +16,8 @@ from .binding import (  # noqa: F401
     TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED,
     toc_encode, toc_encode_batches, toc_enc_info_get, toc_enc_export,
     toc_upload_size, toc_upload, toc_dev_info_get, toc_dev_layout_get,
-    toc_workspace_size, toc_right_mul, toc_left_mul, toc_decode_csr,
+    toc_workspace_size, toc_right_mul, toc_left_mul, toc_left_mul_noalloc, toc_decode_csr,
+    TOC_NOALLOC_SCRATCH_BYTES,
     toc_map_values, toc_decode_dense,
     TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
     TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_CPRIME_COLUMN, TOC_LEVEL_D, TOC_LEVEL_DEPTH,

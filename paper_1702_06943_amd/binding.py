@@ -27,6 +27,7 @@ TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
  TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH, TOC_LEVEL_LIVE) = range(1, 10)
 TOC_CPRIME_COLUMN = 10
+TOC_NOALLOC_SCRATCH_BYTES = 64 << 20
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
 
@@ -105,6 +106,7 @@ def lib():
         "toc_workspace_size": [P, I32, I32, P, P],
         "toc_right_mul": [P, P, I32, I64, P, I64, P, SZ, P],
         "toc_left_mul": [P, P, I32, I64, P, I64, I32, P, SZ, P],
+        "toc_left_mul_noalloc": [P, P, I32, I64, P, I64, I32, P],
         "toc_decode_csr": [P, P, P, P, P],
         "toc_map_values": [P, I32, C.c_float, P],
         "toc_decode_dense": [P, C.c_float, P, I64, P],
@@ -302,6 +304,19 @@ def toc_left_mul(dev, G, out, accumulate=False, ws=None, stream=None):
         raise TocError(TOC_EINVAL, "G must be n_rows x k, out (n_batches*n_cols) x k")
     _check(lib().toc_left_mul(dev.handle, gp, k, ldg, op_, ldo, int(bool(accumulate)),
                               _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def toc_left_mul_noalloc(dev, G, out, accumulate=False, stream=None):
+    """toc_left_mul with its workspace in the library's static device buffer
+    (TOC_NOALLOC_SCRATCH_BYTES per GPU): no workspace argument, no allocation."""
+    info = toc_dev_info_get(dev)
+    gp, ldg, k = _mat(G, "G")
+    op_, ldo, ko = _mat(out, "out")
+    if (G.shape[0] != info["n_rows"] or out.shape[0] != info["n_batches"] * info["n_cols"]
+            or ko != k):
+        raise TocError(TOC_EINVAL, "G must be n_rows x k, out (n_batches*n_cols) x k")
+    _check(lib().toc_left_mul_noalloc(dev.handle, gp, k, ldg, op_, ldo, int(bool(accumulate)),
+                                      _stream(stream)))
 
 
 def toc_decode_csr(dev, rowptr, col, val, stream=None):

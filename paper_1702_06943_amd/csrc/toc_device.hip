@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <type_traits>
 #include <utility>
@@ -18,7 +19,35 @@
 
 using toc::fail;
 
+// Workspace of toc_left_mul_noalloc: one copy on each GPU the library runs on,
+// held until the process ends.  Host code never passes this name to a kernel (on
+// the host it is a stand-in, not a device address): the address comes from
+// hipGetSymbolAddress, once per device (scratch_address below).
+static __device__ __align__(256) float scratch[TOC_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on the first call
+// on each device, with that device current).
+toc_status scratch_address(int device, void **ptr) {
+  if (device < 0 || device >= kMaxDevices)
+    return fail(TOC_EUNSUPPORTED, "device %d beyond the %d this build tracks", device, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(TOC_EDEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", device,
+                  hipGetErrorString(e));
+    g_scratch_ptr[device] = p;
+  }
+  *ptr = g_scratch_ptr[device];
+  return TOC_OK;
+}
 
 constexpr int kWave = 64;
 constexpr int kBlock = 256;
@@ -2436,9 +2465,19 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
   return TOC_OK;
 }
 
-toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg, float *out,
-                        int64_t ldo, int32_t accumulate, void *ws, size_t ws_bytes,
-                        void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The left product.  fit_workers: the workspace is a fixed buffer (the static
+// scratch) that may be smaller than the tiled plan's one slot per worker; the
+// tiled kernel then runs with as many persistent workers per XCD as it holds
+// slots for (each output element is summed in the same order by whichever worker
+// takes it, so the result is the same bit for bit), and shapes whose per-batch
+// minimum exceeds it are TOC_EUNSUPPORTED.
+toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ldg, float *out,
+                         int64_t ldo, int32_t accumulate, void *ws, size_t ws_bytes, void *stream,
+                         bool fit_workers) {
   toc_status st = check_device(d);
   if (st != TOC_OK) return st;
   if (k < 1) return fail(TOC_EINVAL, "k must be >= 1");
@@ -2468,7 +2507,24 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     }
     return TOC_OK;
   }
-  const OpPlan plan = plan_op(d, TOC_OP_LEFT, k);
+  OpPlan plan = plan_op(d, TOC_OP_LEFT, k);
+  if (fit_workers && plan.path == kPathTiled && plan.ws_floats > 0) {
+    const int64_t slot_bytes = (int64_t)d->max_tree * plan.tw * 4;
+    const int64_t max_spx = (int64_t)ws_bytes / (slot_bytes * kXcd);
+    if (max_spx < 1)
+      return fail(TOC_EUNSUPPORTED,
+                  "a worker slot of %lld bytes per XCD (8) exceeds the %zu bytes of static scratch",
+                  (long long)slot_bytes, ws_bytes);
+    if (plan.spx > max_spx) {
+      plan.spx = (int)max_spx;
+      plan.grid = (unsigned)(kXcd * plan.spx);
+      plan.ws_floats = (int64_t)plan.grid * d->max_tree * plan.tw;
+    }
+  }
+  if (fit_workers && plan.path == kPathWide && plan.row_floats > 0 &&
+      plan.rows_max * plan.row_floats * 4 > (int64_t)ws_bytes)
+    return fail(TOC_EUNSUPPORTED, "a batch needs %lld bytes of workspace, beyond the %zu of static scratch",
+                (long long)(plan.rows_max * plan.row_floats * 4), ws_bytes);
   if (plan.path == kPathTiled) {
     if (plan.ws_floats > 0 && (!ws || ws_bytes < (size_t)plan.ws_floats * 4))
       return fail(TOC_ESIZE, "workspace of %zu bytes below the %lld needed", ws_bytes,
@@ -2519,6 +2575,26 @@ toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg
     if (st != TOC_OK) return st;
   }
   return TOC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+toc_status toc_left_mul(const toc_dev *d, const float *G, int32_t k, int64_t ldg, float *out,
+                        int64_t ldo, int32_t accumulate, void *ws, size_t ws_bytes,
+                        void *stream) {
+  return left_mul_impl(d, G, k, ldg, out, ldo, accumulate, ws, ws_bytes, stream, false);
+}
+
+toc_status toc_left_mul_noalloc(const toc_dev *d, const float *G, int32_t k, int64_t ldg,
+                                float *out, int64_t ldo, int32_t accumulate, void *stream) {
+  toc_status st = check_device(d);
+  if (st != TOC_OK) return st;
+  void *ws = nullptr;
+  if ((st = scratch_address(d->device, &ws))) return st;
+  return left_mul_impl(d, G, k, ldg, out, ldo, accumulate, ws, TOC_NOALLOC_SCRATCH_BYTES, stream,
+                       true);
 }
 
 toc_status toc_decode_csr(const toc_dev *d, int64_t *rowptr, int32_t *col, float *val,
