@@ -190,7 +190,8 @@ typedef struct {
   int64_t code_base, d_base, row_base, span_base, nnz_base, deep_base, tree_base,
       lvl_base;
   int32_t n_rows, n_codes, n_lvl1, n_int1, n_levels, n_d;
-  int32_t pad[2];
+  int32_t n_ucols;   /* distinct key columns of the batch's stored codes           */
+  int32_t pad;
 } toc_batch;
 
 /* A node of the decoding tree C' (Algorithm 2): its key pair (section 3.1) ... */

@@ -73,7 +73,7 @@ BATCH_DTYPE = np.dtype([
     ("code_base", "<i8"), ("d_base", "<i8"), ("row_base", "<i8"), ("span_base", "<i8"),
     ("nnz_base", "<i8"), ("deep_base", "<i8"), ("tree_base", "<i8"), ("lvl_base", "<i8"),
     ("n_rows", "<i4"), ("n_codes", "<i4"), ("n_lvl1", "<i4"), ("n_int1", "<i4"),
-    ("n_levels", "<i4"), ("n_d", "<i4"), ("pad", "<i4", (2,))])
+    ("n_levels", "<i4"), ("n_d", "<i4"), ("n_ucols", "<i4"), ("pad", "<i4")])
 
 _lib = None
 

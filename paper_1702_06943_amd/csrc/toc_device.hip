@@ -554,6 +554,13 @@ __device__ inline float4 f4fma(float s, float4 x, float4 a) {
   return make_float4(fmaf(s, x.x, a.x), fmaf(s, x.y, a.y), fmaf(s, x.z, a.z), fmaf(s, x.w, a.w));
 }
 
+__device__ inline void add4(float4 &a, const float4 &b) {
+  a.x += b.x;
+  a.y += b.y;
+  a.z += b.z;
+  a.w += b.w;
+}
+
 __device__ inline uint32_t rdlane(uint32_t v, uint32_t i) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
 }
@@ -1357,6 +1364,335 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Right multiplication with a compact W tile: the tile holds only the rows of W
+// whose column is the key column of some code of the batch (an image-like batch
+// uses about two thirds of its columns), so a tile of kRcKT = 64 columns fits in
+// LDS and each lane of a 16-lane row holds 4 columns: one 16-byte LDS read and
+// one row-address broadcast serve 4 FMAs.  Rows are 256 bytes, so the 16 lanes of
+// a row read 64 distinct banks (rows of 240 bytes measured 44 % bank-conflict
+// cycles).  Work items are (batch, 64-column tile) pairs, dealt per XCD as in
+// right_tiled_kernel.  Per item:
+//  * the batch's used columns come from the column index of the image (a column
+//    is used when it has a depth-1 leaf or a tree code): a ballot scan gives each
+//    its row, kept in an LDS map column -> row, and the rows are gathered from W;
+//  * the H rows of the deep codes (depth >= 2) are built level by level into
+//    the worker's workspace slot (H[c] = H[parent] + val * W[col]);
+//  * tuple sums as in right_tiled_kernel (16 lanes per tuple, entries loaded two
+//    steps ahead, translated one step ahead, broadcast along the DPP row); an
+//    entry of a deep code counts as the zero row in the LDS pass and its H row
+//    is added from the workspace after the chunk's FMAs (deep entries are rare:
+//    about one in two hundred on image-like batches).
+// ---------------------------------------------------------------------------
+constexpr int kRcKT = 64;                         // columns per tile: 16 lanes x 4
+constexpr uint32_t kRcRowBytes = kRcKT * 4;       // 256
+constexpr int kRcHgRow = 64;                      // floats per deep row in the workspace
+constexpr int kRcPer = 2;                         // entries per lane and chunk
+constexpr int kRcChunk = kRcPer * kRtLanes;       // 32 entries per tuple per step
+constexpr uint32_t kRcNone = 0xFFFFFFFFu;
+
+// LDS bytes of the compact kernel: rows 0 .. umax-1 (W), row umax (zeros), the
+// map (u16 per column), the used-column list (u16 per row) and 16 wave totals.
+inline size_t rc_lds_bytes(int64_t umax, int64_t m) {
+  const size_t rows = (size_t)(umax + 1) * kRcRowBytes;
+  return rows + (size_t)2 * m + (size_t)2 * umax + 64 + 16;
+}
+
+__global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
+    Img im, const uint32_t *__restrict__ cols_all, int64_t nb, int n_tiles, int spw, int m,
+    int cap, const float *__restrict__ W, int64_t ldw, int k, float *__restrict__ R, int64_t ldr,
+    float *__restrict__ ws, int64_t slot_floats) {
+  extern __shared__ float4 smem4[];
+  char *lds = (char *)smem4;
+  __shared__ uint32_t tg_next[2];
+  const int x = (int)(blockIdx.x % kXcd), s = (int)(blockIdx.x / kXcd);
+  const int lane = threadIdx.x % kWave, wave = wave_id();
+  const int grp = lane / kRtLanes, sub = lane % kRtLanes, q = 4 * sub;
+  float *Wt = (float *)lds;                                       // rows of 64 floats
+  const uint32_t wb = lds_base(smem4);
+  const uint32_t qoff = 16u * (uint32_t)sub;
+  const uint32_t zrow_b = wb + (uint32_t)cap * kRcRowBytes;
+  uint16_t *map = (uint16_t *)(lds + (size_t)(cap + 1) * kRcRowBytes);
+  uint16_t *ucol = map + m;
+  uint32_t *wsum = (uint32_t *)(((uintptr_t)(ucol + cap) + 3) & ~(uintptr_t)3);
+  float *Hg = ws + blockIdx.x * slot_floats;
+  // the zero row
+  for (int e = threadIdx.x; e < kRcKT; e += kRtBlock) Wt[cap * kRcKT + e] = 0.0f;
+  if (threadIdx.x < 2) tg_next[threadIdx.x] = kRtWaves;
+  const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
+  const int64_t n_items = nbx * n_tiles;
+  uint32_t parity = 0;
+  for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
+    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
+    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
+    const int k0 = tile * kRcKT;
+    const int kt = min(kRcKT, k - k0);
+    const toc_batch bt = uniform_batch(im.batches + b);
+    const uint32_t n1 = (uint32_t)bt.n_lvl1;
+    const int nrows = bt.n_rows;
+    __syncthreads();   // the previous item no longer reads the tile, map or counters
+    if (threadIdx.x == 0) tg_next[parity ^ 1u] = kRtWaves;
+    // used columns: column j is used when it has a depth-1 leaf (Loff) or a tree
+    // code (Toff); its row is the number of used columns before it (at most cap:
+    // the host sized cap for the batch with the most)
+    {
+      const uint32_t *Loff = cols_all + b * 4 * (int64_t)(m + 1);
+      const uint32_t *Toff = Loff + 2 * (m + 1);
+      uint32_t base = 0;
+      for (int j0 = 0; j0 < m; j0 += kRtBlock) {
+        const int j = j0 + (int)threadIdx.x;
+        const bool used = j < m && (Loff[j + 1] > Loff[j] || Toff[j + 1] > Toff[j]);
+        const uint64_t bal = __ballot(used);
+        const uint32_t below = (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) wsum[wave] = (uint32_t)__popcll(bal);
+        __syncthreads();
+        uint32_t before = base, total = base;
+#pragma unroll
+        for (int w = 0; w < kRtWaves; ++w) {
+          const uint32_t t = wsum[w];
+          before += w < wave ? t : 0u;
+          total += t;
+        }
+        const uint32_t row = before + below;
+        if (used && row < (uint32_t)cap) {
+          map[j] = (uint16_t)row;
+          ucol[row] = (uint16_t)j;
+        }
+        base = total;
+        __syncthreads();
+      }
+      // the rows of W (all loads of a pass first, then the stores); columns past
+      // kt are zeros
+      const uint32_t U = min(base, (uint32_t)cap);
+      const uint32_t n4 = U * (kRcKT / 4);
+      const bool vec = kt == kRcKT && (ldw % 4) == 0 && (((uintptr_t)(W + k0)) & 15u) == 0;
+      for (uint32_t e0 = threadIdx.x; e0 < n4; e0 += 8 * kRtBlock) {
+        float4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t e = e0 + i * kRtBlock;
+          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (e < n4) {
+            const uint32_t r = e / (kRcKT / 4), q4 = 4 * (e % (kRcKT / 4));
+            const float *src = W + (int64_t)ucol[r] * ldw + k0 + q4;
+            if (vec) {
+              v[i] = *(const float4 *)src;
+            } else {
+              if ((int)q4 + 0 < kt) v[i].x = src[0];
+              if ((int)q4 + 1 < kt) v[i].y = src[1];
+              if ((int)q4 + 2 < kt) v[i].z = src[2];
+              if ((int)q4 + 3 < kt) v[i].w = src[3];
+            }
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t e = e0 + i * kRtBlock;
+          if (e < n4) *(float4 *)&Wt[e * 4] = v[i];
+        }
+      }
+      __syncthreads();
+    }
+    // H rows of the deep codes into the workspace slot, level by level: a 16-lane
+    // row per code (4 columns per lane)
+    {
+      const uint32_t *lvl = im.level + bt.lvl_base;
+      const toc_key *key = im.key + bt.code_base;
+      const toc_link *link = im.link + bt.code_base;
+      const uint32_t g16 = threadIdx.x / kRtLanes;
+      constexpr uint32_t stride = kRtBlock / kRtLanes;
+      for (int d = 2; d <= bt.n_levels; ++d) {
+        const uint32_t a = lvl[d - 1], e = lvl[d];
+        for (uint32_t c = a + g16; c < e; c += stride) {
+          const uint32_t p = link[c].parent;
+          const uint2 kc = *(const uint2 *)(key + c);
+          const float4 wc = *(const float4 *)&Wt[map[kc.x] * kRcKT + q];
+          float4 base;
+          if (p < n1) {
+            const uint2 kp = *(const uint2 *)(key + p);
+            const float vp = __uint_as_float(kp.y);
+            const float4 wp = *(const float4 *)&Wt[map[kp.x] * kRcKT + q];
+            base = make_float4(vp * wp.x, vp * wp.y, vp * wp.z, vp * wp.w);
+          } else {
+            base = *(const float4 *)&Hg[(int64_t)(p - n1) * kRcHgRow + q];
+          }
+          *(float4 *)&Hg[(int64_t)(c - n1) * kRcHgRow + q] = f4fma(__uint_as_float(kc.y), wc, base);
+        }
+        __syncthreads();
+      }
+    }
+    // per-tuple sums
+    const int n_tg = (nrows + kRtGroups - 1) / kRtGroups;
+    const uint32_t *span = im.span + bt.span_base;
+    auto spans_of = [&](int tg, uint32_t &st, uint32_t &en) {
+      const int r = min(tg * kRtGroups + grp, nrows);
+      st = span[r];
+      en = span[min(r + 1, nrows)];
+    };
+    auto wave_max = [&](uint32_t v) -> uint32_t {
+      v = max(v, (uint32_t)__shfl_xor((int)v, 16, kWave));
+      v = max(v, (uint32_t)__shfl_xor((int)v, 32, kWave));
+      return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+    };
+    auto grab = [&]() -> int {
+      uint32_t g = 0;
+      if (lane == 0) g = atomicAdd(&tg_next[parity], 1u);
+      return __builtin_amdgcn_readfirstlane((int)g);
+    };
+    int ltg = wave, ntg = n_tg;
+    uint32_t lj = 0, lmax = 0, lst = 0, len = 0, nst = 0, nen = 0;
+    if (ltg < n_tg) {
+      spans_of(ltg, lst, len);
+      lmax = wave_max(len - lst);
+      ntg = grab();
+    }
+    spans_of(ntg, nst, nen);
+    auto chunk_of_l = [&]() -> RtChunk {
+      const uint32_t n = lmax > lj ? min((uint32_t)kRcChunk, lmax - lj) : 0u;
+      return RtChunk{ltg, (n + 3u) & ~3u, lj + kRcChunk >= lmax};
+    };
+    auto advance = [&]() {
+      if (ltg < n_tg) {
+        lj += kRcChunk;
+        if (lj >= lmax) {
+          ltg = ntg;
+          lj = 0;
+          lst = nst;
+          len = nen;
+          lmax = 0u;
+          if (ltg < n_tg) {
+            lmax = wave_max(len - lst);
+            ntg = grab();
+          }
+        }
+      }
+      spans_of(ntg, nst, nen);
+    };
+    const BufRes rs_dc = buf_res(im.dcodes + bt.d_base, (uint32_t)bt.n_d);
+    const BufRes rs_node = key_res(im.key + bt.code_base, (uint32_t)bt.n_codes);
+    auto load_codes = [&](uint32_t (&d)[kRcPer], uint64_t (&ok)[kRcPer]) {
+      const bool live = ltg < n_tg;
+      static_for<kRcPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        const uint32_t j = lst + lj + (uint32_t)sub + (uint32_t)(h * kRtLanes);
+        ok[h] = __ballot(live && j < len);
+        d[h] = buf_load(rs_dc, j);
+      });
+    };
+    // (LDS row address, multiplier, deep row) of an entry: a depth-1 code's row is
+    // its column's row of the tile times its value; a deep code and an entry past
+    // the end of its tuple take the zero row (the deep code's H row is added
+    // after the chunk)
+    auto translate = [&](uint32_t d, uint2 key, uint64_t ok, uint32_t &rb, uint32_t &mu,
+                         uint32_t &dp) {
+      const bool in = __builtin_amdgcn_inverse_ballot_w64(ok);
+      const uint32_t row = map[min(key.x, (uint32_t)m - 1u)];
+      const bool leaf = in && d < n1;
+      rb = leaf ? wb + row * kRcRowBytes : zrow_b;
+      mu = leaf ? key.y : 0u;
+      dp = (in && d >= n1) ? d - n1 : kRcNone;
+    };
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    RtChunk G = chunk_of_l();
+    RtChunk C{n_tg, 0u, false};
+    uint32_t crb[kRcPer], cmu[kRcPer], cdp[kRcPer];
+#pragma unroll
+    for (int h = 0; h < kRcPer; ++h) {
+      crb[h] = zrow_b;
+      cmu[h] = 0u;
+      cdp[h] = kRcNone;
+    }
+    auto step = [&](const uint32_t (&gd)[kRcPer], const uint64_t (&gok)[kRcPer],
+                    uint32_t (&ld)[kRcPer], uint64_t (&lok)[kRcPer]) {
+      advance();
+      uint2 key[kRcPer];
+      static_for<kRcPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        key[h] = key_load(rs_node, gd[h]);
+      });
+      const RtChunk L = chunk_of_l();
+      load_codes(ld, lok);
+      if (C.tg < n_tg) {
+        // blocked summation: the chunk's terms form a partial sum that then joins
+        // the tuple's running sum
+        float4 part = make_float4(0.f, 0.f, 0.f, 0.f);
+        constexpr int NB = kRcChunk / 4;       // blocks of 4 entries
+        if (C.steps == (uint32_t)kRcChunk) {
+          // each block's reads are issued before the previous block's FMAs
+          float4 xa[4], xb[4];
+          load4x4_bcast<0>(crb[0], qoff, xa);
+          static_for<NB>([&](auto bc) {
+            constexpr int bk = decltype(bc)::value;
+            if constexpr (bk + 1 < NB) {
+              constexpr int nx = bk + 1;
+              if constexpr (bk % 2 == 0) load4x4_bcast<4 * (nx % 4)>(crb[nx / 4], qoff, xb);
+              else load4x4_bcast<4 * (nx % 4)>(crb[nx / 4], qoff, xa);
+            }
+            if constexpr (bk % 2 == 0) fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xa);
+            else fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xb);
+          });
+        } else {
+          static_for<NB>([&](auto bc) {
+            constexpr int bk = decltype(bc)::value;
+            if (C.steps > (uint32_t)(4 * bk)) {
+              float4 xv[4];
+              load4x4_bcast<4 * (bk % 4)>(crb[bk / 4], qoff, xv);
+              fma4x4_bcast<4 * (bk % 4)>(part, cmu[bk / 4], xv);
+            }
+          });
+        }
+        // deep entries of the chunk: the H rows from the workspace, each row of
+        // lanes taking the entry of its own tuple at each lane position t that
+        // holds a deep entry in some tuple
+#pragma unroll
+        for (int h = 0; h < kRcPer; ++h) {
+          const uint64_t dm = __ballot(cdp[h] != kRcNone);
+          uint32_t pos = (uint32_t)((dm | (dm >> 16) | (dm >> 32) | (dm >> 48)) & 0xFFFFu);
+          while (pos) {
+            const int t = __builtin_ctz(pos);
+            pos &= pos - 1u;
+            const uint32_t r = (uint32_t)__shfl((int)cdp[h], grp * kRtLanes + t, kWave);
+            if (r != kRcNone) add4(part, *(const float4 *)&Hg[(int64_t)r * kRcHgRow + q]);
+          }
+        }
+        add4(acc, part);
+        if (C.last) {
+          const int r = C.tg * kRtGroups + grp;
+          if (r < nrows) {
+            float *rr = R + (bt.row_base + r) * ldr + k0 + q;
+            if (q + 3 < kt) {
+              rr[0] = acc.x;
+              rr[1] = acc.y;
+              rr[2] = acc.z;
+              rr[3] = acc.w;
+            } else {
+              if (q + 0 < kt) rr[0] = acc.x;
+              if (q + 1 < kt) rr[1] = acc.y;
+              if (q + 2 < kt) rr[2] = acc.z;
+            }
+          }
+          acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+      // chunk G becomes chunk C
+      static_for<kRcPer>([&](auto hc) {
+        constexpr int h = decltype(hc)::value;
+        translate(gd[h], key[h], gok[h], crb[h], cmu[h], cdp[h]);
+      });
+      C = G;
+      G = L;
+    };
+    uint32_t dA[kRcPer], dB[kRcPer];
+    uint64_t okA[kRcPer], okB[kRcPer];
+    load_codes(dA, okA);
+    while (G.tg < n_tg || C.tg < n_tg) {
+      step(dA, okA, dB, okB);
+      if (!(G.tg < n_tg || C.tg < n_tg)) break;
+      step(dB, okB, dA, okA);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Left multiplication by pulling (Theorem 2 read as a definition, Algorithm 8's
 // result): H(x) is the sum of the G rows over the entries of D equal to x (the
 // inverted index occ_off/occ_row lists them per code) plus the H of x's children,
@@ -1386,13 +1722,6 @@ constexpr uint32_t kFirstOcc = 0x80000000u;
 constexpr uint32_t kLtStaticBytes = 16;           // static LDS: two column-group counters
 constexpr int kLtU = 4;                           // tree codes per group at a time
 constexpr uint32_t kLtBlk = 16;                   // children per block of a tree code's sum
-
-__device__ inline void add4(float4 &a, const float4 &b) {
-  a.x += b.x;
-  a.y += b.y;
-  a.z += b.z;
-  a.w += b.w;
-}
 
 // LDS bytes of the per-wave stages and of the column tables
 // (groups of 16 lanes pass entries round with the DPP row broadcast: no stage)
@@ -2178,6 +2507,7 @@ struct OpPlan {
   int64_t ws_floats = 0;      // tiled: whole workspace (one slot per worker)
   int64_t lds_rows = 0;       // tiled left: tree rows in LDS
   int per = 1;                // tiled right: batches per item
+  bool compact = false;       // tiled right: the compact-tile kernel (64 columns)
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -2188,6 +2518,27 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
   p.rows_total = right ? d->total_deep : d->total_tree;
   if (k == 1 && k1_fits(d, op)) {
     p.path = kPathK1;
+    return p;
+  }
+  if (right && k >= kRcKT && m <= 65535 && d->max_ucols > 0 &&
+      rc_lds_bytes(d->max_ucols, m) <= kLdsMax - kRtStaticBytes) {
+    // the batch's used rows of W fit in LDS at 64 columns: right_compact_kernel,
+    // deep rows in the workspace.  (Two batches per item, sharing one tile of
+    // their used columns, measured slower: 128 VGPRs and scalar spills.)
+    p.path = kPathTiled;
+    p.compact = true;
+    p.tw = kRcKT;
+    p.n_tiles = (k + kRcKT - 1) / kRcKT;
+    p.lds_rows = d->max_ucols;
+    p.lds = rc_lds_bytes(d->max_ucols, m);
+    p.per = 1;
+    const int64_t per_xcd = (d->info.n_batches + kXcd - 1) / kXcd;
+    const int64_t items = (per_xcd + p.per - 1) / p.per * p.n_tiles;
+    p.spx = (int)std::min<int64_t>(kCuPerXcd, std::max<int64_t>(1, items));
+    p.grid = (unsigned)(kXcd * p.spx);
+    p.row_floats = kRcHgRow;
+    const int64_t deep_rows = std::max<int64_t>(p.per == 2 ? d->max_pair_deep : d->max_deep, 1);
+    p.ws_floats = (int64_t)p.grid * deep_rows * kRcHgRow;
     return p;
   }
   if (right) {
@@ -2437,6 +2788,14 @@ toc_status toc_right_mul(const toc_dev *d, const float *W, int32_t k, int64_t ld
       return fail(TOC_ESIZE, "workspace of %zu bytes below the %lld needed", ws_bytes,
                   (long long)plan.ws_floats * 4);
     const int m = d->info.n_cols;
+    if (plan.compact) {
+      if ((st = allow_lds(right_compact_kernel, plan.lds))) return st;
+      const uint32_t *cols = (const uint32_t *)((const uint8_t *)d->buf + d->layout.cols);
+      hipLaunchKernelGGL(right_compact_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im,
+                         cols, nb, plan.n_tiles, plan.spx, m, (int)plan.lds_rows, W, ldw, k, R, ldr,
+                         (float *)ws, plan.ws_floats / plan.grid);
+      return launch_status("right_compact_kernel");
+    }
     if (plan.deep_lds) {
       if ((st = allow_lds(right_tiled_kernel, plan.lds))) return st;
       hipLaunchKernelGGL(right_tiled_kernel, dim3(plan.grid), dim3(kRtBlock), plan.lds, s, im, nb,

@@ -584,6 +584,11 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     std::sort(S.keys.begin(), S.keys.end());
     for (int64_t k = 0; k < m; ++k) c_ord[k] = (uint32_t)S.keys[k];
     c_ord[m] = 0;
+    // columns that are the key column of some stored code (a leaf or a tree code)
+    int32_t u = 0;
+    for (int64_t j = 0; j < m; ++j)
+      u += (c_code[j + 1] > c_code[j] || c_tree[j + 1] > c_tree[j]) ? 1 : 0;
+    bt.n_ucols = u;
     // the entries of each column in one stretch: leaf occurrences, then tree
     // codes marked with kTreeEntry
     uint32_t *ce = (uint32_t *)(dst + L.centry) + bt.d_base + bt.tree_base;
@@ -770,6 +775,8 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
   work();
   for (auto &t : th) t.join();
   if (first_err.load() != 0) return fail((toc_status)first_err.load(), "%s", err_msg.c_str());
+  dev->max_ucols = 0;
+  for (const toc_batch &bt : dev->batches) dev->max_ucols = std::max(dev->max_ucols, bt.n_ucols);
   std::memcpy(dst + L.batches, dev->batches.data(), sizeof(toc_batch) * dev->batches.size());
   return TOC_OK;
 }
