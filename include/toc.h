@@ -184,6 +184,8 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *             tree codes (tlist entries) with bit 30 set; column j starts at the
  *             cols entries of j: leaf occurrences before it plus tlist entries
  *             before it.  Needs rows and codes below 2^30 per batch.
+ *   cval    : float per centry entry (same index): the key value of the entry's
+ *             code (the multiplier of the left multiplication's term)
  * Depth-1 codes without children are numbered in the order of their first entry
  * in D; the codes of each level d >= 2 are sorted by parent.                    */
 typedef struct {
@@ -208,7 +210,7 @@ typedef struct {
 
 typedef struct {
   int64_t batches, level, key, link, span, dcodes, occ_off, occ_row, tlist, dtiles, cols,
-      tchild, pval, centry, end;
+      tchild, pval, centry, cval, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

@@ -65,6 +65,7 @@ struct Img {
   const uint32_t *dcodes;
   const uint32_t *pval;     // key value bits by left-product position
   const uint32_t *centry;   // left-product entries of each key column
+  const uint32_t *cval;     // key value bits of each centry entry's code
 };
 
 Img image_of(const toc_dev *d) {
@@ -73,7 +74,8 @@ Img image_of(const toc_dev *d) {
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
              (const toc_key *)(b + L.key), (const toc_link *)(b + L.link),
              (const uint32_t *)(b + L.span), (const uint32_t *)(b + L.dcodes),
-             (const uint32_t *)(b + L.pval), (const uint32_t *)(b + L.centry)};
+             (const uint32_t *)(b + L.pval), (const uint32_t *)(b + L.centry),
+             (const uint32_t *)(b + L.cval)};
 }
 
 // Views of one field of a batch's node records, indexed by local code.
@@ -1776,8 +1778,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   constexpr bool DPP = LPG == kRtLanes;       // a group is one 16-lane row: entries by broadcast
-  constexpr int PER = 1;                      // entries per lane and chunk (2 measured slower on
-                                              // columns of ~50 entries)
+  constexpr int PER = DPP ? 2 : 1;            // entries per lane and chunk (16-lane groups: 2,
+                                              // 3 % faster on dense quantised batches)
   constexpr int CHK = PER * LPG;              // entries per column per chunk
   const uint32_t rb0 = lds_base(smem4) + rows_b;                      // LDS address of row 0
   const uint32_t qoff = 4u * (uint32_t)q;
@@ -1788,7 +1790,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   if (threadIdx.x < 2) cg_next[threadIdx.x] = kLtWaves;
   const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
   const int64_t n_items = nbx * n_tiles;
-  const int n_cg = (m + GPW - 1) / GPW;
   uint32_t parity = 0;
   for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
     const int64_t b = uniform64(x + kXcd * (it / n_tiles));
@@ -1950,7 +1951,26 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       }
       __syncthreads();
     }
-    // output columns
+    // output columns.  The image orders a batch's columns by entries, most
+    // first, so its n_ucols columns with entries come first: column groups cover
+    // only those, and the output rows of the others are zero (written here once).
+    const int n_used = bt.n_ucols;
+    const int n_cg = (n_used + GPW - 1) / GPW;
+    if (!accumulate) {
+      const int n4 = (m - n_used) * (TW / 4);
+      for (int e = threadIdx.x; e < n4; e += kLtBlock) {
+        const int j = (int)Ord[n_used + e / (TW / 4)], q4 = 4 * (e % (TW / 4));
+        float *o = out + (b * m + j) * ldo + k0 + q4;
+        if (q4 + 3 < kt) {
+          o[0] = 0.0f;
+          o[1] = 0.0f;
+          o[2] = 0.0f;
+          o[3] = 0.0f;
+        } else {
+          for (int i = 0; i < kt - q4; ++i) o[i] = 0.0f;
+        }
+      }
+    }
     auto grab = [&]() -> int {
       uint32_t g = 0;
       if (lane == 0) g = atomicAdd(&cg_next[parity], 1u);
@@ -1963,23 +1983,22 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     };
     // column j of group g of column group cg; past the last column: no entries.
     // Its entries (leaf occurrences, then tree codes) start at cst in centry.
-    struct ColSpan { uint32_t cst, nl, nt, lcode; };
+    struct ColSpan { uint32_t cst, nl, nt; };
     auto col_of = [&](int cg) -> ColSpan {
       const int o = cg * GPW + grp;
-      const int j = o < m ? (int)Ord[o] : m;
+      const int j = o < n_used ? (int)Ord[o] : m;
       const int j1 = min(j + 1, m);
       ColSpan c;
       const uint32_t ost = Ost[j], tof = Toff[j];
       c.cst = ost + tof;
       c.nl = Ost[j1] - ost;
       c.nt = Toff[j1] - tof;
-      c.lcode = Loff[j];
       return c;
     };
     // load stage: column group lcg, entries [lj, lj + CHK) of each column
     int lcg = wave, ncg = n_cg;
     uint32_t lj = 0, lmax = 0;
-    ColSpan lc{0u, 0u, 0u, 0u};
+    ColSpan lc{0u, 0u, 0u};
     if (lcg < n_cg) {
       lc = col_of(lcg);
       lmax = wave_max(lc.nl + lc.nt);
@@ -2010,22 +2029,23 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
       }
     };
-    const BufRes rs_pval = buf_res(im.pval + bt.code_base, nc);
     const BufRes rs_cent = buf_res(im.centry + bt.d_base + bt.tree_base, (uint32_t)bt.n_d + n_tree);
+    const BufRes rs_cval = buf_res(im.cval + bt.d_base + bt.tree_base, (uint32_t)bt.n_d + n_tree);
     // L: the entry words of each lane (entries sub + h * LPG of the chunk: the
-    // occ_row word of a leaf occurrence, or a tree code marked kTreeEntry) and the
-    // wave masks of lanes with an entry.  A lane without one reads past the
-    // buffer: its word is 0 and its code 0xFFFFFFFF, whose pval read gives 0.
-    auto load_entry = [&](uint32_t (&w)[PER], uint64_t (&ok)[PER], uint32_t &lcode) {
+    // occ_row word of a leaf occurrence, or a tree code marked kTreeEntry), the
+    // value of the entry's code beside it, and the wave masks of lanes with an
+    // entry.  A lane without one reads past the buffers: word and value 0.
+    auto load_entry = [&](uint32_t (&w)[PER], uint32_t (&v)[PER], uint64_t (&ok)[PER]) {
       const bool live = lcg < n_cg;
 #pragma unroll
       for (int h = 0; h < PER; ++h) {
         const uint32_t e = lj + (uint32_t)(sub + h * LPG);
         const bool in = live && e < lc.nl + lc.nt;
         ok[h] = __ballot(in);
-        w[h] = buf_load(rs_cent, in ? lc.cst + e : 0xFFFFFFFFu);
+        const uint32_t at = in ? lc.cst + e : 0xFFFFFFFFu;
+        w[h] = buf_load(rs_cent, at);
+        v[h] = buf_load(rs_cval, at);
       }
-      lcode = lc.lcode;
     };
     auto row_f4 = [&](uint32_t r) -> float4 {
       if (TREE_LDS) return lds_load4(qb + r * RB);
@@ -2035,8 +2055,6 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       if (g) xg = *(const float4 *)&Hg[(int64_t)(r & ~kRtGlobal) * TW + q];
       return g ? xg : xl;
     };
-    const uint32_t gmask = LPG == 32 ? 0xFFFFFFFFu : ((1u << LPG) - 1u);
-    uint32_t gcode = 0;   // leaf code of the last occurrence translated in this column
     LtChunk G = chunk_of_l();
     LtChunk C{n_cg, 0u, 0u, false, false};
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -2050,35 +2068,25 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       cra[h] = zaddr;
       cmu[h] = 0u;
     }
-    auto step = [&](const uint32_t (&gw)[PER], const uint64_t (&gok)[PER], uint32_t glcode,
-                    uint32_t (&lw)[PER], uint64_t (&lok)[PER], uint32_t &llcode) {
+    auto step = [&](const uint32_t (&gw)[PER], const uint32_t (&gv)[PER],
+                    const uint64_t (&gok)[PER], uint32_t (&lw)[PER], uint32_t (&lv)[PER],
+                    uint64_t (&lok)[PER]) {
       advance();
-      // G: entries of the chunk loaded a step ago; the code of a leaf occurrence
-      // is the column's first leaf code - 1 plus the first-occurrence bits up to
-      // it (carried along the column in gcode); then the key pairs
-      uint32_t base = G.first == 0u ? glcode - 1u : gcode;
-      uint32_t code[PER], row[PER];
+      // G: entries of the chunk loaded a step ago: a leaf occurrence reads the G
+      // row of its tuple, a tree code its H row; the multiplier is the value
+      // loaded beside the entry (0 for a lane without entry)
+      uint32_t row[PER], pv[PER];
 #pragma unroll
       for (int h = 0; h < PER; ++h) {
         const bool tree = (gw[h] & toc::kTreeEntry) != 0u;     // a lane without entry has word 0
         const bool leaf = __builtin_amdgcn_inverse_ballot_w64(gok[h]) && !tree;
-        const uint64_t firsts = __ballot(leaf && (gw[h] & kFirstOcc));
-        const uint32_t gb = (uint32_t)(firsts >> (grp * LPG)) & gmask;
-        // branch-free: leaf, tree or no entry
-        const uint32_t lcode = base + (uint32_t)__popc(gb & (gmask >> (LPG - 1 - sub)));
-        const uint32_t tc = gw[h] & ~toc::kTreeEntry;
-        const uint32_t hr = hrow(tc);
+        const uint32_t hr = hrow(gw[h] & ~toc::kTreeEntry);
         const uint32_t trow = hr < cap ? trow0 + hr : (kRtGlobal | hr);
-        code[h] = leaf ? lcode : (tree ? tc : 0xFFFFFFFFu);
         row[h] = leaf ? (gw[h] & ~kFirstOcc) : (tree ? trow : zrow);
-        base += (uint32_t)__popc(gb);
+        pv[h] = gv[h];
       }
-      gcode = base;
-      uint32_t pv[PER];
-#pragma unroll
-      for (int h = 0; h < PER; ++h) pv[h] = buf_load(rs_pval, code[h]);
       const LtChunk L = chunk_of_l();
-      load_entry(lw, lok, llcode);
+      load_entry(lw, lv, lok);
       // blocked summation: a chunk's entries form a partial sum that then joins
       // the column's running sum (serial chains of at most CHK terms, and of the
       // column's number of chunks)
@@ -2189,7 +2197,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         acc.w += part.w;
         if (C.last) {
           const int o = C.cg * GPW + grp;
-          if (o < m) {
+          if (o < n_used) {
             const int j = (int)Ord[o];
             float *o = out + (b * m + j) * ldo + k0 + q;
             if (accumulate) {
@@ -2227,13 +2235,13 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       C = G;
       G = L;
     };
-    uint32_t wA[PER], wB[PER], cA, cB;
+    uint32_t wA[PER], wB[PER], vA[PER], vB[PER];
     uint64_t kA[PER], kB[PER];
-    load_entry(wA, kA, cA);
+    load_entry(wA, vA, kA);
     while (G.cg < n_cg || C.cg < n_cg) {
-      step(wA, kA, cA, wB, kB, cB);
+      step(wA, vA, kA, wB, vB, kB);
       if (!(G.cg < n_cg || C.cg < n_cg)) break;
-      step(wB, kB, cB, wA, kA, cA);
+      step(wB, vB, kB, wA, vA, kA);
     }
   }
 }
@@ -2364,12 +2372,18 @@ constexpr int kMapBlock = 256;
 
 __global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restrict__ key,
                                                                uint32_t *__restrict__ pval,
-                                                               int64_t n, int op, float c) {
+                                                               int64_t n, uint32_t *__restrict__ cval,
+                                                               int64_t n_cval, int op, float c) {
   const int64_t stride = (int64_t)gridDim.x * kMapBlock;
   for (int64_t i = (int64_t)blockIdx.x * kMapBlock + threadIdx.x; i < n; i += stride) {
     const float v = key[i].val, w = __uint_as_float(pval[i]);
     key[i].val = op == TOC_MAP_SCALE ? v * c : v * v;
     pval[i] = __float_as_uint(op == TOC_MAP_SCALE ? w * c : w * w);
+  }
+  // the copies beside the left multiplication's column entries
+  for (int64_t i = (int64_t)blockIdx.x * kMapBlock + threadIdx.x; i < n_cval; i += stride) {
+    const float w = __uint_as_float(cval[i]);
+    cval[i] = __float_as_uint(op == TOC_MAP_SCALE ? w * c : w * w);
   }
 }
 
@@ -2992,9 +3006,11 @@ toc_status toc_map_values(const toc_dev *d, int32_t op, float c, void *stream) {
   if (n == 0) return TOC_OK;
   uint8_t *bb = (uint8_t *)d->buf;
   const int64_t blocks = std::min<int64_t>((n + kMapBlock - 1) / kMapBlock, 64 * 256);
+  const int64_t n_cval = (d->layout.end - d->layout.cval) / 4;
   hipLaunchKernelGGL(map_values_kernel, dim3((unsigned)blocks), dim3(kMapBlock), 0,
                      (hipStream_t)stream, (toc_key *)(bb + d->layout.key),
-                     (uint32_t *)(bb + d->layout.pval), n, (int)op, c);
+                     (uint32_t *)(bb + d->layout.pval), n, (uint32_t *)(bb + d->layout.cval),
+                     n_cval, (int)op, c);
   return launch_status("map_values_kernel");
 }
 

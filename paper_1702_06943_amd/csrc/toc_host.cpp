@@ -591,12 +591,20 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     bt.n_ucols = u;
     // the entries of each column in one stretch: leaf occurrences, then tree
     // codes marked with kTreeEntry
+    // (cval: beside each entry, the key value of its code)
     uint32_t *ce = (uint32_t *)(dst + L.centry) + bt.d_base + bt.tree_base;
-    const uint32_t *lo = occ_row + occ_off[n_int1];
+    uint32_t *cv = (uint32_t *)(dst + L.cval) + bt.d_base + bt.tree_base;
     int64_t o = 0;
     for (int64_t j = 0; j < m; ++j) {
-      for (uint32_t q = c_occ[j]; q < c_occ[j + 1]; ++q) ce[o++] = lo[q];
-      for (uint32_t q = c_tree[j]; q < c_tree[j + 1]; ++q) ce[o++] = tlist[q] | kTreeEntry;
+      for (uint32_t p = c_code[j]; p < c_code[j + 1]; ++p)
+        for (uint32_t q = occ_off[p]; q < occ_off[p + 1]; ++q) {
+          ce[o] = occ_row[q];
+          cv[o++] = pval[p];
+        }
+      for (uint32_t q = c_tree[j]; q < c_tree[j + 1]; ++q) {
+        ce[o] = tlist[q] | kTreeEntry;
+        std::memcpy(&cv[o++], &node[tlist[q]].val, 4);
+      }
     }
   }
   // children of each tree code (their H rows are added to its H in the left
@@ -711,6 +719,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.tchild = off;  off = align256(off + 4 * (tree + n_batches));
   L.pval = off;    off = align256(off + 4 * codes);
   L.centry = off;  off = align256(off + 4 * (d + tree));
+  L.cval = off;    off = align256(off + 4 * (d + tree));
   dev->n_dtiles = dtiles;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;

@@ -41,6 +41,8 @@ def read_image(dev, buf):
         pval=arr("pval", np.float32, n_codes),
         centry=arr("centry", np.uint32, info["n_codes"] + (
             int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0)),
+        cval=arr("cval", np.float32, info["n_codes"] + (
+            int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0)),
     )
     for f in ("col", "val"):
         img[f] = img["key"][f]
@@ -71,6 +73,9 @@ def batch_view(img, b):
         centry=img["centry"][int(t["d_base"]) + int(t["tree_base"]):
                              int(t["d_base"]) + int(t["tree_base"]) + int(t["n_d"]) + int(t["n_int1"])
                              + nc - int(t["n_lvl1"])],
+        cval=img["cval"][int(t["d_base"]) + int(t["tree_base"]):
+                         int(t["d_base"]) + int(t["tree_base"]) + int(t["n_d"]) + int(t["n_int1"])
+                         + nc - int(t["n_lvl1"])],
     )
 
 
@@ -164,6 +169,13 @@ def check_invariants(v):
         assert np.array_equal(ce[st:st + nlj], orow_raw[lo:lo + nlj])
         assert np.array_equal(ce[st + nlj:st + nlj + ntj],
                               tl[int(cx[2, j]):int(cx[2, j + 1])] | np.uint32(0x40000000))
+        # the value beside each entry: its leaf's value (leaves of the column in
+        # position order, each for its occurrences), then each tree code's value
+        want = [v["val"][at[p]] for p in range(int(cx[0, j]), int(cx[0, j + 1]))
+                for _ in range(int(oo[p + 1] - oo[p]))]
+        want += [v["val"][c] for c in tl[int(cx[2, j]):int(cx[2, j + 1])]]
+        assert np.array_equal(v["cval"][st:st + nlj + ntj].view(np.uint32),
+                              np.asarray(want, np.float32).view(np.uint32))
     # children ranges: tree code h's children are tchild[h] .. tchild[h+1]-1
     hrow = lambda c: c if c < ni else c - n1 + ni
     tch = v["tchild"]
