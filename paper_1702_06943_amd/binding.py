@@ -16,6 +16,9 @@ import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtoc.so")
+# A host-sanitizer build of the same library (tests only, see sanitize.py) is
+# loaded instead when TOC_LIB_PATH names it.
+LIB_PATH = os.environ.get("TOC_LIB_PATH", LIB_PATH)
 
 TOC_OK, TOC_EINVAL, TOC_ENOMEM, TOC_ESIZE, TOC_EDEVICE, TOC_EUNSUPPORTED = range(6)
 TOC_UPLOAD_KEEP_DEAD = 1
