@@ -47,6 +47,9 @@ Parity status of each function (what pins it, see ``tests/test_oracle.py``):
                  the paper's linear-regression gradient on the worked example by
                  hand, closed forms (lr = 0, one entry, logistic at r = 0, hinge
                  beyond the margin), an empty batch
+  mlp_grad_scale pinned: at least |gradient| for every entry; at zero weights
+                 the closed form (only the output layer's scales are nonzero, the
+                 bias's being the mean of |1/C - [y = c]|)
   mlp_loss, mlp_step
                  pinned: central finite differences of the mean cross-entropy for
                  every parameter (softmax and single-sigmoid outputs), the first
@@ -61,6 +64,7 @@ from .toc_oracle import (  # noqa: F401
     build_cprime,
     decode,
     densify,
+    mlp_grad_scale,
     decoded_to_csr,
     dense_right,
     dense_left,

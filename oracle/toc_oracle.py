@@ -605,14 +605,6 @@ def _sigmoid(x):
     return 0.5 * (1.0 + np.tanh(0.5 * x))
 
 
-def _densify(rows, n_cols):
-    A = np.zeros((len(rows), n_cols))
-    for i, t in enumerate(rows):
-        for c, b in t:
-            A[i, c] = bits_f32(b)
-    return A
-
-
 def _mlp_forward(A, p):
     H1 = _sigmoid(A @ p["W1"] + p["b1"])
     H2 = _sigmoid(H1 @ p["W2"] + p["b2"])
@@ -624,7 +616,7 @@ def mlp_loss(rows, n_cols, params, labels):
     """Mean cross-entropy loss of the network on a decoded batch (fp64)."""
     p = {k: np.asarray(v, np.float64) for k, v in params.items()}
     labels = np.asarray(labels, np.int64)
-    _, _, Z3 = _mlp_forward(_densify(rows, n_cols), p)
+    _, _, Z3 = _mlp_forward(densify(rows, n_cols), p)
     if Z3.shape[1] == 1:
         z = Z3[:, 0]
         per = np.logaddexp(0.0, z) - labels * z        # -log sigmoid(z) or -log(1 - sigmoid(z))
@@ -644,7 +636,7 @@ def mlp_step(rows, n_cols, params, labels, lr):
     if n == 0:
         return {k: v.copy() for k, v in p.items()}, {k: np.zeros_like(v) for k, v in p.items()}
     labels = np.asarray(labels, np.int64)
-    A = _densify(rows, n_cols)
+    A = densify(rows, n_cols)
     H1, H2, Z3 = _mlp_forward(A, p)
     C = Z3.shape[1]
     if C == 1:
@@ -662,3 +654,44 @@ def mlp_step(rows, n_cols, params, labels, lr):
          "W2": H1.T @ dZ2, "b2": dZ2.sum(axis=0),
          "W1": A.T @ dZ1, "b1": dZ1.sum(axis=0)}
     return {k: p[k] - lr * g[k] for k in p}, g
+
+
+def mlp_grad_scale(rows, n_cols, params, labels):
+    """Scale S of each gradient entry of mlp_step, for the tolerance eps * S of a
+    binary32 gradient (like the products' 1e-5 * sum |a_ij w_jq|).  S is the
+    backward pass with every factor replaced by its magnitude (|P - Y| for the
+    output error, |W| for the weights), each factor weighted by its sensitivity to
+    the forward pass's rounding: c_l, the sum of the absolute values of the terms
+    of the pre-activations Z_l (with the previous layer's c carried through the
+    sigmoid's slope, at most 1/4), bounds the absolute error of Z_l in units of
+    eps; an activation H then carries error c/4, the slope H (1 - H) and the
+    softmax output relative error of order c.  So every term of every gradient
+    entry counts |term| (1 + its factors' c).  Returns a dict keyed like the
+    gradients."""
+    p = {k: np.asarray(v, np.float64) for k, v in params.items()}
+    n = len(rows)
+    if n == 0:
+        return {k: np.zeros_like(v) for k, v in p.items()}
+    labels = np.asarray(labels, np.int64)
+    A = densify(rows, n_cols)
+    H1, H2, Z3 = _mlp_forward(A, p)
+    aW1, aW2, aW3 = np.abs(p["W1"]), np.abs(p["W2"]), np.abs(p["W3"])
+    # forward sensitivities (absolute error bounds of Z_l, in units of eps)
+    c1 = np.abs(A) @ aW1 + np.abs(p["b1"])
+    c2 = H1 @ aW2 + np.abs(p["b2"]) + 0.25 * (c1 @ aW2)
+    c3 = H2 @ aW3 + np.abs(p["b3"]) + 0.25 * (c2 @ aW3)
+    if Z3.shape[1] == 1:
+        P = _sigmoid(Z3)
+        Y = labels[:, None].astype(np.float64)
+    else:
+        E = np.exp(Z3 - Z3.max(axis=1, keepdims=True))
+        P = E / E.sum(axis=1, keepdims=True)
+        Y = np.zeros_like(P)
+        Y[np.arange(n), labels] = 1.0
+    # the output error and its sensitivity (a softmax moves by at most 2 P max|dZ|)
+    M3 = (np.abs(P - Y) + 2.0 * P * c3.max(axis=1, keepdims=True)) / n
+    M2 = (M3 @ aW3.T) * H2 * (1.0 - H2) * (1.0 + c2)
+    M1 = (M2 @ aW2.T) * H1 * (1.0 - H1) * (1.0 + c1)
+    return {"W3": (H2 + 0.25 * c2).T @ M3, "b3": M3.sum(axis=0),
+            "W2": (H1 + 0.25 * c1).T @ M2, "b2": M2.sum(axis=0),
+            "W1": np.abs(A).T @ M1, "b1": M1.sum(axis=0)}

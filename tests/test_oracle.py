@@ -573,6 +573,44 @@ def test_mlp_closed_form_at_zero_weights():
     assert np.allclose(g1["b3"], [0.5 - 0.75], rtol=0, atol=1e-15)
 
 
+@pytest.mark.parametrize("C", [1, 3])
+@pytest.mark.parametrize("seed", range(3))
+def test_mlp_grad_scale_bounds_the_gradient(C, seed):
+    """S >= |g| for every entry of every gradient (the scale sums the absolute
+    values of the terms the gradient sums)."""
+    rp, c, v = tiny_batch(4400 + seed, n_rows=11, n_cols=6, density=0.6, n_values=3)
+    rows = O.canonicalize(11, 6, rp, c, v)
+    rng = np.random.default_rng(seed)
+    p = _mlp_params(rng, 6, 5, 3, C)
+    labels = rng.integers(0, max(C, 2), size=11)
+    _, g = O.mlp_step(rows, 6, p, labels, 1.0)
+    S = O.mlp_grad_scale(rows, 6, p, labels)
+    for k in g:
+        assert S[k].shape == g[k].shape
+        assert np.all(S[k] >= np.abs(g[k]) * (1 - 1e-12)), k
+        assert np.any(S[k] > np.abs(g[k]) * (1 + 1e-9)) or not g[k].any() or C == 1, k
+
+
+def test_mlp_grad_scale_at_zero_weights():
+    """Zero weights and biases: no forward rounding (c = 0), hidden units 1/2, the
+    output uniform, and W3 = 0 stops the backward pass; so only the output layer
+    has a scale, that of b3_c being the mean over the tuples of |1/C - [y = c]|
+    and that of W3[u, c] half of it."""
+    rows = [[(0, O.f32_bits(1.0)), (2, O.f32_bits(-2.0))], [(1, O.f32_bits(3.0))],
+            [(2, O.f32_bits(0.5))], []]
+    p = {"W1": np.zeros((3, 4)), "b1": np.zeros(4), "W2": np.zeros((4, 2)), "b2": np.zeros(2),
+         "W3": np.zeros((2, 3)), "b3": np.zeros(3)}
+    labels = np.array([0, 2, 2, 1])
+    S = O.mlp_grad_scale(rows, 3, p, labels)
+    # class 0: one tuple of it (|1/3 - 1|) and three others (1/3 each); class 1
+    # likewise; class 2: two tuples of it and two others
+    sb3 = np.array([(2 / 3 + 3 * 1 / 3) / 4, (2 / 3 + 3 * 1 / 3) / 4, (2 * 2 / 3 + 2 * 1 / 3) / 4])
+    assert np.allclose(S["b3"], sb3, rtol=0, atol=1e-15)
+    assert np.allclose(S["W3"], np.tile(sb3 / 2, (2, 1)), rtol=0, atol=1e-15)
+    for k in ("W1", "b1", "W2", "b2"):
+        assert not S[k].any()
+
+
 def test_mlp_lr_zero_and_empty_batch():
     rng = np.random.default_rng(5)
     p = _mlp_params(rng, 4, 3, 2, 2)
