@@ -1,7 +1,7 @@
 """GPU parity of toc_mlp_epoch (mini-batch gradient descent for the neural network
 of section 5.1, first layer on the compressed batch) with the oracle: every step
 taken from the GPU's current parameters agrees with the oracle's fp64 step within
-a bound derived from the fp32 arithmetic; one launch over many batches equals the
+1e-5 times each gradient entry's sum of absolute terms; one launch over many batches equals the
 same steps launched one by one, bit for bit; argument errors are reported."""
 
 import numpy as np
@@ -41,18 +41,21 @@ def to_host(pd):
 
 
 def check_step(B, b, before, after, labels, lr, worst):
-    """after must equal the oracle's step from before: per parameter,
-    |after - (before - lr g)| <= lr * 1e-4 * max|g of that parameter| + 4u (|before|
-    + |after|), g the oracle's fp64 gradient of the mean loss."""
+    """after must equal the oracle's step from before, element by element:
+    |after - (before - lr g)| <= lr * 1e-5 * S + 4u (|before| + |after|), g the
+    oracle's fp64 gradient of the mean loss and S its scale (the sum of the
+    absolute values of the terms each gradient entry sums, through the backward
+    pass), as 1e-5 * sum |a_ij w_jq| for the products; 4u covers the rounding of
+    the update itself."""
     n, rp, c, v = B.batch(b)
     rows = O.canonicalize(n, B.n_cols, rp, c, v)
     r0 = int(B.row_off[b])
-    want, g = O.mlp_step(rows, B.n_cols, {k: x.astype(np.float64) for k, x in before.items()},
-                         labels[r0:r0 + n], lr)
+    p64 = {k: x.astype(np.float64) for k, x in before.items()}
+    want, g = O.mlp_step(rows, B.n_cols, p64, labels[r0:r0 + n], lr)
+    S = O.mlp_grad_scale(rows, B.n_cols, p64, labels[r0:r0 + n])
     for k in NAMES:
         a = after[k].astype(np.float64)
-        tol = lr * 1e-4 * np.max(np.abs(g[k]), initial=0.0) + \
-            4 * U * (np.abs(before[k]) + np.abs(a))
+        tol = lr * 1e-5 * S[k] + 4 * U * (np.abs(before[k]) + np.abs(a))
         err = np.abs(a - want[k])
         ratio = float(np.max(err / np.maximum(tol, 1e-300), initial=0.0))
         worst[k] = max(worst.get(k, 0.0), ratio)
