@@ -109,8 +109,11 @@ void toc_enc_free(toc_enc *enc);
  * structure-of-arrays image laid out as described by toc_layout below.
  *
  * All batches must have the same n_cols.  toc_upload_size gives the bytes `buf`
- * needs; toc_upload copies the image with hipMemcpyAsync on `stream` and waits
- * for it, so the handles in `encs` may be freed afterwards.  `buf` must stay
+ * needs; toc_upload builds the image range of batches by range of batches into
+ * two pinned host staging buffers of 256 MiB (or of the largest batch, if
+ * larger) in turn, copying each range with hipMemcpyAsync on `stream` while the
+ * next is built, and waits for the copies, so the handles in `encs` may be freed
+ * afterwards and host memory never holds the whole image.  `buf` must stay
  * allocated for as long as the returned toc_dev is used.
  * flags: TOC_UPLOAD_KEEP_DEAD keeps every node of C' (results are identical);
  *        TOC_UPLOAD_HOST writes the image into host memory `buf` without any HIP

@@ -2658,6 +2658,115 @@ toc_status ws_capacity(const OpPlan &p, void *ws, size_t ws_bytes, int64_t &cap_
 
 extern "C" {
 
+}  // extern "C"
+
+namespace {
+
+// The per-batch arrays of the image: offset in the layout, bytes per element and
+// the element at which batch b's slice starts (slices are in batch order).
+struct ImgArr {
+  int64_t toc_layout::*off;
+  int64_t elem;
+  int64_t (*start)(const toc::ArrStarts &);
+};
+
+const ImgArr kImgArrs[] = {
+    {&toc_layout::level, 4, [](const toc::ArrStarts &a) { return a.level; }},
+    {&toc_layout::key, 8, [](const toc::ArrStarts &a) { return a.code; }},
+    {&toc_layout::link, 8, [](const toc::ArrStarts &a) { return a.code; }},
+    {&toc_layout::span, 4, [](const toc::ArrStarts &a) { return a.span; }},
+    {&toc_layout::dcodes, 4, [](const toc::ArrStarts &a) { return a.d; }},
+    {&toc_layout::occ_off, 4, [](const toc::ArrStarts &a) { return a.code + a.b; }},
+    {&toc_layout::occ_row, 4, [](const toc::ArrStarts &a) { return a.d; }},
+    {&toc_layout::tlist, 4, [](const toc::ArrStarts &a) { return a.tree; }},
+    {&toc_layout::dtiles, 16, [](const toc::ArrStarts &a) { return a.dtile; }},
+    {&toc_layout::cols, 4, [](const toc::ArrStarts &a) { return a.cols; }},
+    {&toc_layout::tchild, 4, [](const toc::ArrStarts &a) { return a.tree + a.b; }},
+    {&toc_layout::pval, 4, [](const toc::ArrStarts &a) { return a.code; }},
+    {&toc_layout::centry, 4, [](const toc::ArrStarts &a) { return a.d + a.tree; }},
+    {&toc_layout::cval, 4, [](const toc::ArrStarts &a) { return a.d + a.tree; }},
+};
+constexpr int kNumImgArrs = (int)(sizeof(kImgArrs) / sizeof(kImgArrs[0]));
+constexpr size_t kStageBytes = (size_t)256 << 20;   // each of the two pinned buffers
+
+inline int64_t round256(int64_t x) { return (x + 255) & ~(int64_t)255; }
+
+// Builds the image batch range by batch range into two pinned host buffers in
+// turn and copies each range's slices of every array to the device while the
+// next range is built, so host memory holds two buffers, never the whole image.
+toc_status upload_chunked(const toc_enc *const *encs, int64_t n, uint32_t flags, toc_dev *d,
+                          uint8_t *dbuf, hipStream_t s) {
+  std::vector<toc::ArrStarts> st((size_t)n + 1);
+  for (int64_t b = 0; b <= n; ++b) st[(size_t)b] = toc::arr_starts(d, b);
+  auto range_bytes = [&](int64_t b0, int64_t b1) {
+    int64_t t = 0;
+    for (const ImgArr &a : kImgArrs)
+      t += round256((a.start(st[(size_t)b1]) - a.start(st[(size_t)b0])) * a.elem);
+    return t;
+  };
+  size_t cap = kStageBytes;
+  for (int64_t b = 0; b < n; ++b) cap = std::max(cap, (size_t)range_bytes(b, b + 1));
+  uint8_t *stage[2] = {nullptr, nullptr};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  toc_status ret = TOC_OK;
+  for (int i = 0; i < 2 && ret == TOC_OK; ++i) {
+    if (hipHostMalloc((void **)&stage[i], cap, hipHostMallocDefault) != hipSuccess)
+      ret = fail(TOC_ENOMEM, "pinned staging buffer of %zu bytes failed", cap);
+    else if (hipEventCreateWithFlags(&done[i], hipEventDisableTiming) != hipSuccess)
+      ret = fail(TOC_EDEVICE, "hipEventCreate failed");
+  }
+  int64_t b0 = 0;
+  for (int i = 0; ret == TOC_OK && b0 < n; ++i) {
+    uint8_t *buf = stage[i % 2];
+    if (i >= 2 && hipEventSynchronize(done[i % 2]) != hipSuccess) {
+      ret = fail(TOC_EDEVICE, "staging copy failed");
+      break;
+    }
+    int64_t b1 = b0 + 1;
+    while (b1 < n && range_bytes(b0, b1 + 1) <= (int64_t)cap) ++b1;
+    // each array's slice for batches b0 .. b1-1, packed; the layout shifted so
+    // that the batch writer lands in those slices
+    toc_layout Ls = d->layout;
+    int64_t so = 0, at[kNumImgArrs], len[kNumImgArrs];
+    for (int a = 0; a < kNumImgArrs; ++a) {
+      const ImgArr &A = kImgArrs[a];
+      const int64_t e0 = A.start(st[(size_t)b0]) * A.elem;
+      len[a] = A.start(st[(size_t)b1]) * A.elem - e0;
+      at[a] = so;
+      Ls.*(A.off) = so - e0;
+      so = round256(so + len[a]);
+    }
+    std::memset(buf, 0, (size_t)so);
+    if ((ret = toc::write_batches(encs, b0, b1, flags, Ls, d, buf)) != TOC_OK) break;
+    for (int a = 0; a < kNumImgArrs && ret == TOC_OK; ++a) {
+      if (len[a] == 0) continue;
+      const ImgArr &A = kImgArrs[a];
+      uint8_t *dst = dbuf + d->layout.*(A.off) + A.start(st[(size_t)b0]) * A.elem;
+      if (hipMemcpyAsync(dst, buf + at[a], (size_t)len[a], hipMemcpyHostToDevice, s) != hipSuccess)
+        ret = fail(TOC_EDEVICE, "upload copy failed");
+    }
+    if (ret == TOC_OK && hipEventRecord(done[i % 2], s) != hipSuccess)
+      ret = fail(TOC_EDEVICE, "hipEventRecord failed");
+    b0 = b1;
+  }
+  if (ret == TOC_OK) {
+    toc::finish_image(d);
+    if (n > 0 && hipMemcpyAsync(dbuf + d->layout.batches, d->batches.data(),
+                                sizeof(toc_batch) * (size_t)n, hipMemcpyHostToDevice, s) != hipSuccess)
+      ret = fail(TOC_EDEVICE, "upload copy failed");
+  }
+  if (hipStreamSynchronize(s) != hipSuccess && ret == TOC_OK) ret = fail(TOC_EDEVICE, "upload copy failed");
+  for (int i = 0; i < 2; ++i) {
+    if (done[i]) hipEventDestroy(done[i]);
+    if (stage[i]) hipHostFree(stage[i]);
+  }
+  return ret;
+}
+
+}  // namespace
+
+extern "C" {
+
 toc_status toc_upload_size(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
                            size_t *bytes) {
   if (!bytes) return fail(TOC_EINVAL, "bytes is NULL");
@@ -2704,18 +2813,10 @@ toc_status toc_upload(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
         delete d;
         return fail(TOC_EDEVICE, "hipGetDevice failed");
       }
-      std::vector<uint8_t> staging((size_t)d->layout.end);
-      st = toc::build_image(encs, n_batches, flags, d, staging.data());
+      st = upload_chunked(encs, n_batches, flags, d, (uint8_t *)buf, (hipStream_t)stream);
       if (st != TOC_OK) {
         delete d;
         return st;
-      }
-      hipStream_t s = (hipStream_t)stream;
-      if (hipMemcpyAsync(buf, staging.data(), staging.size(), hipMemcpyHostToDevice, s) !=
-              hipSuccess ||
-          hipStreamSynchronize(s) != hipSuccess) {
-        delete d;
-        return fail(TOC_EDEVICE, "upload copy failed");
       }
     }
   } catch (const std::bad_alloc &) {

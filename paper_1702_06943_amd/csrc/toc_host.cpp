@@ -721,6 +721,7 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   L.centry = off;  off = align256(off + 4 * (d + tree));
   L.cval = off;    off = align256(off + 4 * (d + tree));
   dev->n_dtiles = dtiles;
+  dev->tot_levels = levels;
   L.end = std::max<int64_t>(off, 256);
   dev->total_deep = deep;
   dev->total_tree = tree;
@@ -748,13 +749,11 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   return TOC_OK;
 }
 
-toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
-                       toc_dev *dev, uint8_t *dst) {
-  const toc_layout &L = dev->layout;
-  std::memset(dst, 0, (size_t)L.end);
-  const int nt = (int)std::min<int64_t>(
-      std::max(1u, std::thread::hardware_concurrency()), std::max<int64_t>(n_batches, 1));
-  std::atomic<int64_t> next{0};
+toc_status write_batches(const toc_enc *const *encs, int64_t b0, int64_t b1, uint32_t flags,
+                         const toc_layout &L, toc_dev *dev, uint8_t *dst) {
+  const int nt = (int)std::min<int64_t>(std::max(1u, std::thread::hardware_concurrency()),
+                                        std::max<int64_t>(b1 - b0, 1));
+  std::atomic<int64_t> next{b0};
   std::atomic<int> first_err{0};
   std::string err_msg;
   std::atomic<int> err_taken{0};
@@ -762,7 +761,7 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
     ImgScratch S;
     for (;;) {
       const int64_t b = next.fetch_add(1);
-      if (b >= n_batches || first_err.load() != 0) return;
+      if (b >= b1 || first_err.load() != 0) return;
       toc_status st;
       try {
         st = write_batch(encs[b], b, flags, L, dst, dev->batches[b], dev->dtile_base[b], S);
@@ -784,10 +783,48 @@ toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t f
   work();
   for (auto &t : th) t.join();
   if (first_err.load() != 0) return fail((toc_status)first_err.load(), "%s", err_msg.c_str());
+  return TOC_OK;
+}
+
+void finish_image(toc_dev *dev) {
   dev->max_ucols = 0;
   for (const toc_batch &bt : dev->batches) dev->max_ucols = std::max(dev->max_ucols, bt.n_ucols);
+}
+
+toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
+                       toc_dev *dev, uint8_t *dst) {
+  const toc_layout &L = dev->layout;
+  std::memset(dst, 0, (size_t)L.end);
+  toc_status st = write_batches(encs, 0, n_batches, flags, L, dev, dst);
+  if (st != TOC_OK) return st;
+  finish_image(dev);
   std::memcpy(dst + L.batches, dev->batches.data(), sizeof(toc_batch) * dev->batches.size());
   return TOC_OK;
+}
+
+ArrStarts arr_starts(const toc_dev *dev, int64_t b) {
+  ArrStarts a;
+  const int64_t n = (int64_t)dev->batches.size();
+  const int64_t m1 = 4 * ((int64_t)std::max(dev->info.n_cols, 0) + 1);
+  if (b < n) {
+    const toc_batch &t = dev->batches[b];
+    a.level = t.lvl_base;
+    a.code = t.code_base;
+    a.span = t.span_base;
+    a.d = t.d_base;
+    a.tree = t.tree_base;
+    a.dtile = dev->dtile_base[b];
+  } else {
+    a.level = dev->tot_levels;
+    a.code = dev->info.n_stored;
+    a.span = dev->info.n_rows + n;
+    a.d = dev->info.n_codes;
+    a.tree = dev->total_tree;
+    a.dtile = dev->n_dtiles;
+  }
+  a.cols = b * m1;
+  a.b = b;
+  return a;
 }
 
 }  // namespace toc

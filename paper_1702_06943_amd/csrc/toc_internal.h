@@ -42,6 +42,7 @@ struct toc_dev {
   int64_t total_deep = 0, total_tree = 0;
   std::vector<int64_t> dtile_base;  // first decode tile of each batch
   int64_t n_dtiles = 0;
+  int64_t tot_levels = 0;           // level entries over all batches
 };
 
 namespace toc {
@@ -61,6 +62,19 @@ void clear_error();
 // Builds the upload image into `dst` (host memory of layout.end bytes).
 toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
                        toc_dev *dev, uint8_t *dst);
+// Writes the arrays of batches b0 .. b1-1 (host threads) at the offsets of layout
+// L from dst: with L shifted per array, into a staging area holding only those
+// batches' slices.  The batch table is not written.
+toc_status write_batches(const toc_enc *const *encs, int64_t b0, int64_t b1, uint32_t flags,
+                         const toc_layout &L, toc_dev *dev, uint8_t *dst);
+// After every batch is written: maxima only the build computes.
+void finish_image(toc_dev *dev);
+// Element index at which batch b's slice of each per-batch array starts (b equal
+// to the batch count: the arrays' ends).
+struct ArrStarts {
+  int64_t level, code, span, d, tree, dtile, cols, b;
+};
+ArrStarts arr_starts(const toc_dev *dev, int64_t b);
 // Computes layout and totals only.
 toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
                       toc_dev *dev);
