@@ -176,7 +176,9 @@ def upload_workload(w, k, device="cuda:0", seed_G=None):
     spec = CONFIGS[w.cfg]
     t0 = time.perf_counter()
     size = T.toc_upload_size(w.encs)
-    w.buf = torch.empty(size, dtype=torch.uint8, device=device)
+    # zeroed, so that the padding between arrays is defined (the device-built
+    # image is compared with this one byte for byte)
+    w.buf = torch.zeros(size, dtype=torch.uint8, device=device)
     w.dev = T.toc_upload(w.encs, w.buf)
     w.upload_s = time.perf_counter() - t0
     w.info = T.toc_dev_info_get(w.dev)
@@ -347,6 +349,66 @@ def pack_sample(w, n):
     t0 = time.perf_counter()
     blobs = [T.toc_enc_pack(w.encs[i]) for i in idx]
     return {"blobs": blobs, "pack_s": time.perf_counter() - t0, "cfg": w.cfg, "n_cols": w.n_cols}
+
+
+def _host_map(fn, items, threads=16):
+    """fn over items on host threads (the library's calls release the GIL)."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        return list(ex.map(fn, items, chunksize=64))
+
+
+def pack_all(w):
+    """Physical encodings (section 3.2) of every batch, packed on the host."""
+    import paper_1702_06943_amd as T
+    t0 = time.perf_counter()
+    blobs = _host_map(T.toc_enc_pack, w.encs)
+    infos = _host_map(T.toc_phys_info_get, blobs)
+    off = np.concatenate([[0], np.cumsum([len(b) for b in blobs])]).astype(np.int64)
+    cat = np.concatenate(blobs + [np.zeros(1, np.uint8)])
+    return {"cat": cat, "off": off, "infos": infos, "pack_s": time.perf_counter() - t0}
+
+
+def time_ingest(w, packed, ws_gib=8):
+    """The whole workload's image built on the device from its physical bytes
+    (toc_ingest_plan + toc_ingest_build), after copying only those bytes to HBM; the
+    result is compared byte for byte with the image toc_upload built on the host."""
+    import torch
+    import paper_1702_06943_amd as T
+    dev = "cuda:0"
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    d_blobs = torch.from_numpy(packed["cat"]).to(dev)
+    torch.cuda.synchronize()
+    h2d_s = time.perf_counter() - t0
+    full, least = T.toc_ingest_workspace_size(packed["infos"], w.n_cols)
+    ws_bytes = max(least, min(full, ws_gib << 30))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    t0 = time.perf_counter()
+    size, idev = T.toc_ingest_plan(d_blobs, packed["off"], packed["infos"], w.n_cols, ws)
+    plan_s = time.perf_counter() - t0
+    buf = torch.empty(size, dtype=torch.uint8, device=dev)
+    t0 = time.perf_counter()
+    T.toc_ingest_build(idev, d_blobs, packed["off"], buf, ws)
+    build_s = time.perf_counter() - t0
+    same = size == w.info["image_bytes"]
+    step = 1 << 30
+    for a in range(0, size if same else 0, step):
+        bsz = min(step, size - a)
+        if not torch.equal(buf[a:a + bsz], w.buf[a:a + bsz]):
+            same = False
+            break
+    del buf, ws, d_blobs, idev
+    torch.cuda.empty_cache()
+    phys = int(packed["off"][-1])
+    log(f"device ingest: {phys / 1e9:.2f} GB of physical bytes -> {size / 1e9:.2f} GB image: "
+        f"copy {h2d_s:.2f} s, plan {plan_s:.2f} s, build {build_s:.2f} s, "
+        f"identical to the host-built image: {same}")
+    return {"phys_bytes": phys, "image_bytes": int(size), "canon_bytes": w.info["canon_bytes"],
+            "pack_s": round(packed["pack_s"], 2), "h2d_s": round(h2d_s, 3),
+            "plan_s": round(plan_s, 3), "build_s": round(build_s, 3),
+            "ws_bytes": int(ws_bytes), "identical_to_host_image": bool(same),
+            "host_path_s": round(w.encode_s + w.upload_s, 2)}
 
 
 def time_cprime(sample, stream, reps=3):
@@ -687,6 +749,9 @@ def main():
     ap.add_argument("--k1-extras", default="c5,c2",
                     help="k = 1 workloads timed after the step at full size (comma list; "
                          "empty: none)")
+    ap.add_argument("--ingest", type=int, default=1,
+                    help="1: after the step, build the whole image on the device from its "
+                         "physical bytes and compare it with the host-built one")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device three times "
                          "(reference dispatches for HBM byte counters)")
@@ -729,7 +794,8 @@ def main():
     import paper_1702_06943_amd as T
     upload_workload(w, k)
     sample = None if args.no_extras else pack_sample(w, args.cprime_batches)
-    ablation = variant_sizes([T.toc_enc_info_get(e) for e in w.encs], w.n_cols)
+    packed = pack_all(w) if args.ingest and not args.no_extras else None
+    ablation = variant_sizes(_host_map(T.toc_enc_info_get, w.encs), w.n_cols)
     encode_dev = None if args.no_extras else time_encode_device(w, torch.cuda.current_stream())
     w.encs = w.kept = None
 
@@ -756,6 +822,8 @@ def main():
     mgd = None if args.no_extras else time_mgd(w, stream)
     nn = None if args.no_extras else time_mlp(w, stream, args.nn_steps)
     k1res = time_k1_workloads(k1, args.steps, args.warmup, stream) if k1 else None
+    ingest = time_ingest(w, packed) if packed else None
+    packed = None
     nnz = info["nnz"]
     canon = info["canon_bytes"]
     m = info["n_cols"]
@@ -807,6 +875,7 @@ def main():
         "roofline": roof,
         "elementwise": extras,
         "cprime_build": cprime,
+        "device_ingest": ingest,
         "mgd_epoch": mgd,
         "nn_steps": nn,
         "k1_workloads": k1res,

@@ -499,6 +499,55 @@ toc_status toc_level_right_mul(const void *blobs, const int64_t *blob_off, const
                                void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------------------------
+ * The upload image built on the device from physical bytes, so that only the
+ * compressed bytes of section 3.2 cross from the host.  Per batch, C' is built as
+ * by toc_cprime_build (Algorithm 2 over the integers read back as in section
+ * 4.1.1), its live codes are put in level order (parents first, as the scans of
+ * Algorithms 4 and 5 need) and the arrays the operations read are derived from it
+ * (toc_dev_layout_get lists them).  The image equals the one toc_upload builds on
+ * the host from the same batches (flags 0), word for word, so every operation gives
+ * the same results, bit for bit, on either.  Two steps: toc_ingest_plan counts what
+ * the layout needs (a census on the device, read back) and gives the image size;
+ * toc_ingest_build writes the image into a caller buffer of that size.  Batches go
+ * through the workspace in ranges that fit it.  Needs codes to occur at most once
+ * in a tuple (true of every encoding of Algorithm 1: a code's sequence begins at a
+ * column, and a tuple holds each column once).
+ * ------------------------------------------------------------------------- */
+#define TOC_INGEST_CHANGED 11     /* the bytes differ from those the plan counted  */
+
+/* Workspace bytes for the batches described by info (toc_phys_info_get of each
+ * blob, n_batches entries): *bytes to take all batches in one range, *min_bytes
+ * (when not NULL) the least that takes the largest batch alone.  TOC_EINVAL for
+ * counts out of range or a column of I at or above n_cols, TOC_EUNSUPPORTED for a
+ * batch of more than 16384 tuples. */
+toc_status toc_ingest_workspace_size(const toc_phys_info *info, int64_t n_batches, int32_t n_cols,
+                                     size_t *bytes, size_t *min_bytes);
+
+/* Reads the blobs on the device and plans the image.
+ *   blobs     device bytes; batch b's blob is bytes blob_off[b] .. blob_off[b+1]-1
+ *             (blob_off: host, n_batches + 1 entries, non-decreasing)
+ *   info      host, the toc_phys_info of each blob (its node and code counts size
+ *             the workspace ranges)
+ *   n_cols    columns of the encoded matrix
+ *   ws        device workspace (at least toc_ingest_workspace_size's *min_bytes)
+ * Synchronises `stream`.  On success *dev is a planned image (operations on it
+ * fail until toc_ingest_build) and *image_bytes the bytes it needs; free it with
+ * toc_dev_free.  TOC_EINVAL names the first batch whose blob is malformed (the
+ * status toc_cprime_build would give it), TOC_ESIZE a workspace below the need of
+ * one batch. */
+toc_status toc_ingest_plan(const void *blobs, const int64_t *blob_off, const toc_phys_info *info,
+                           int64_t n_batches, int32_t n_cols, void *ws, size_t ws_bytes,
+                           void *stream, size_t *image_bytes, toc_dev **dev);
+
+/* Builds the planned image into buf (device memory of at least *image_bytes from
+ * the plan) from the same blobs; afterwards dev is an ordinary device image bound
+ * to buf on the current device.  Synchronises `stream`.  TOC_EINVAL for a dev that
+ * is not planned-and-unbuilt, or for blobs that differ from those planned (the
+ * batch is named; dev stays unbuilt), TOC_ESIZE for a small buf or workspace. */
+toc_status toc_ingest_build(toc_dev *dev, const void *blobs, const int64_t *blob_off, void *buf,
+                            size_t bytes, void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
  * Mini-batch gradient descent (section 2.1): h <- h - lr / |B| * sum over the
  * tuples (x, y) of batch B of d loss(h, x, y) / d h, for the linear models of
  * Table 1, whose loss depends on h through r = x^T h: the batch gradient is

@@ -1,7 +1,8 @@
 """MI355X-native tuple-oriented compression (TOC): encode on the host, run A.W,
 G^T.A, decode, sparse-safe element-wise ops and dense A .+ c on the compressed
 mini-batches with hand-written gfx950 kernels; pack batches into the paper's
-physical encoding and build the decoding tree C' from it on the GPU; run
+physical encoding and build the decoding tree C' and the whole upload image from
+it on the GPU; run
 mini-batch gradient descent steps of linear models and of a feed-forward neural
 network on the compressed batches;
 encode many mini-batches at once on the GPU.
@@ -28,4 +29,5 @@ from .binding import (  # noqa: F401
     TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE,
     toc_encode_device_workspace_size, toc_encode_device,
     toc_mlp_workspace_size, toc_mlp_epoch,
+    TOC_INGEST_CHANGED, toc_ingest_workspace_size, toc_ingest_plan, toc_ingest_build,
 )

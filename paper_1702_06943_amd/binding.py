@@ -30,6 +30,7 @@ TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE = range(
 (TOC_CPRIME_LAYOUT, TOC_CPRIME_VALUE_INDEX, TOC_CPRIME_STARTS, TOC_CPRIME_CODE,
  TOC_CPRIME_NODES, TOC_CPRIME_ROWS, TOC_LEVEL_D, TOC_LEVEL_DEPTH, TOC_LEVEL_LIVE) = range(1, 10)
 TOC_CPRIME_COLUMN = 10
+TOC_INGEST_CHANGED = 11
 TOC_NOALLOC_SCRATCH_BYTES = 64 << 20
 STATUS_NAMES = {0: "TOC_OK", 1: "TOC_EINVAL", 2: "TOC_ENOMEM", 3: "TOC_ESIZE",
                 4: "TOC_EDEVICE", 5: "TOC_EUNSUPPORTED"}
@@ -127,6 +128,9 @@ def lib():
         "toc_level_build": [P, P, P, P, I64, I32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
         "toc_mlp_epoch": [P, I64, I64, I32, I32, I32, P, P, P, P, P, P, P, C.c_float, P, SZ, P],
         "toc_encode_device": [I64, P, I32, P, P, P, I64, I64, P, P, P, P, P, P, P, SZ, P],
+        "toc_ingest_workspace_size": [P, I64, I32, P, P],
+        "toc_ingest_plan": [P, P, P, I64, I32, P, SZ, P, P, P],
+        "toc_ingest_build": [P, P, P, P, SZ, P, SZ, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -392,6 +396,48 @@ def toc_cprime_build(blobs, blob_off, node_off, max_rows, n_cols, parent, col, v
                                   int(n_cols), _ptr(parent), _ptr(col), _ptr(val), _ptr(depth), _ptr(status),
                                   _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
                                   _stream(stream)))
+
+
+def _phys_infos(infos):
+    arr = (PhysInfo * max(len(infos), 1))()
+    for i, f in enumerate(infos):
+        for name, _ in PhysInfo._fields_:
+            setattr(arr[i], name, int(f[name]))
+    return arr
+
+
+def toc_ingest_workspace_size(infos, n_cols):
+    """infos: toc_phys_info_get of each blob.  Returns (bytes for one range of all
+    batches, least bytes that take the largest batch)."""
+    n, mn = C.c_size_t(), C.c_size_t()
+    _check(lib().toc_ingest_workspace_size(_phys_infos(infos), len(infos), int(n_cols),
+                                           C.byref(n), C.byref(mn)))
+    return n.value, mn.value
+
+
+def toc_ingest_plan(blobs, blob_off, infos, n_cols, ws, stream=None):
+    """blobs: device uint8 tensor of the concatenated blobs; blob_off: host int64
+    array of len(infos) + 1 offsets; ws: device workspace tensor.  Returns
+    (image bytes, planned Dev); build it with toc_ingest_build."""
+    blob_off = _arr(blob_off, np.int64)
+    if blob_off.size != len(infos) + 1:
+        raise TocError(TOC_EINVAL, "blob_off must have one entry per blob plus one")
+    if blobs.numel() < int(blob_off[-1]):
+        raise TocError(TOC_EINVAL, "blobs shorter than blob_off[-1]")
+    n, h = C.c_size_t(), C.c_void_p()
+    _check(lib().toc_ingest_plan(_ptr(blobs), _ptr(blob_off), _phys_infos(infos), len(infos),
+                                 int(n_cols), _ptr(ws), _nbytes(ws) if ws is not None else 0,
+                                 _stream(stream), C.byref(n), C.byref(h)))
+    return n.value, Dev(h.value, None)
+
+
+def toc_ingest_build(dev, blobs, blob_off, buf, ws, stream=None):
+    """Builds the planned image into buf (device uint8 tensor of at least the
+    plan's bytes); dev then keeps buf alive."""
+    blob_off = _arr(blob_off, np.int64)
+    _check(lib().toc_ingest_build(dev.handle, _ptr(blobs), _ptr(blob_off), _ptr(buf), _nbytes(buf),
+                                  _ptr(ws), _nbytes(ws) if ws is not None else 0, _stream(stream)))
+    dev.buf = buf
 
 
 def toc_mgd_epoch(dev, y, h, loss, lr, b0=0, n_batches=None, stream=None):

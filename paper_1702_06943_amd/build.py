@@ -18,6 +18,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # packed FP32 instructions are kept out of every kernel
 NO_PACKED_FP32 = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+HOST_SOURCES = ("toc_host.cpp", "toc_phys.cpp")
+HIP_SOURCES = ("toc_device.hip", "toc_cprime.hip", "toc_mgd.hip", "toc_encode.hip", "toc_mlp.hip",
+               "toc_ingest.hip")
 
 
 def _run(cmd, verbose):
@@ -33,12 +36,12 @@ def _run(cmd, verbose):
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     objs = []
-    for src in ("toc_host.cpp", "toc_phys.cpp"):
+    for src in HOST_SOURCES:
         o = os.path.join(BUILD, src.replace(".cpp", ".o"))
         _run(["g++", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE,
               "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)
-    for src in ("toc_device.hip", "toc_cprime.hip", "toc_mgd.hip", "toc_encode.hip", "toc_mlp.hip"):
+    for src in HIP_SOURCES:
         o = os.path.join(BUILD, src.replace(".hip", ".o"))
         _run([HIPCC, "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", *NO_PACKED_FP32,
               "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", o], verbose)

@@ -2462,6 +2462,7 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
 // ===========================================================================
 toc_status check_device(const toc_dev *d) {
   if (!d) return fail(TOC_EINVAL, "dev is NULL");
+  if (d->pending) return fail(TOC_EINVAL, "image planned but not built");
   if (d->host) return fail(TOC_EINVAL, "image was uploaded to host memory");
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return fail(TOC_EDEVICE, "hipGetDevice failed");

@@ -651,21 +651,41 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
   if (n_batches < 0) return fail(TOC_EINVAL, "n_batches < 0");
   if (n_batches > 0 && !encs) return fail(TOC_EINVAL, "encs is NULL");
   if (flags & ~(TOC_UPLOAD_KEEP_DEAD | TOC_UPLOAD_HOST)) return fail(TOC_EINVAL, "unknown flag");
-  int64_t codes = 0, levels = 0, rows = 0, d = 0, spans = 0, nnz = 0, canon = 0, deep = 0,
-          tree = 0;
-  int32_t n_cols = -1, max_depth = 0;
-  dev->batches.assign((size_t)n_batches, toc_batch{});
-  dev->max_rows = dev->max_codes = dev->max_levels = 0;
-  dev->max_d = dev->max_deep = dev->max_tree = dev->max_pair_deep = 0;
-  dev->dtile_base.assign((size_t)n_batches, 0);
-  int64_t dtiles = 0;
+  int32_t n_cols = -1;
+  std::vector<BatchCounts> bc((size_t)n_batches);
+  const bool keep = flags & TOC_UPLOAD_KEEP_DEAD;
   for (int64_t b = 0; b < n_batches; ++b) {
     const toc_enc *e = encs[b];
     if (!e) return fail(TOC_EINVAL, "encs[%lld] is NULL", (long long)b);
     if (n_cols < 0) n_cols = e->n_cols;
     if (e->n_cols != n_cols) return fail(TOC_EINVAL, "batches differ in n_cols");
     const Counts c = counts_of(e, flags);
-    if (c.codes >= kMaxBatchDim || c.d > INT32_MAX || e->n_rows >= kMaxBatchDim)
+    BatchCounts &k = bc[(size_t)b];
+    k.rows = c.rows;
+    k.codes = c.codes;
+    k.levels = c.levels;
+    k.d = c.d;
+    k.deep = keep ? e->n_deep_all : e->n_deep_live;
+    k.int1 = keep ? e->n_int1_all : e->n_int1_live;
+    k.nnz = e->nnz;
+    k.canon = 4 * c.d + 4 * (c.rows + 1) + 10 * e->n_live + 4 * ((int64_t)e->max_depth_live + 1);
+  }
+  return plan_layout(bc.data(), n_batches, n_cols, flags, dev);
+}
+
+toc_status plan_layout(const BatchCounts *bc, int64_t n_batches, int32_t n_cols, uint32_t flags,
+                       toc_dev *dev) {
+  int64_t codes = 0, levels = 0, rows = 0, d = 0, spans = 0, nnz = 0, canon = 0, deep = 0,
+          tree = 0;
+  int32_t max_depth = 0;
+  dev->batches.assign((size_t)n_batches, toc_batch{});
+  dev->max_rows = dev->max_codes = dev->max_levels = 0;
+  dev->max_d = dev->max_deep = dev->max_tree = dev->max_pair_deep = 0;
+  dev->dtile_base.assign((size_t)n_batches, 0);
+  int64_t dtiles = 0;
+  for (int64_t b = 0; b < n_batches; ++b) {
+    const BatchCounts &c = bc[b];
+    if (c.codes >= kMaxBatchDim || c.d > INT32_MAX || c.rows >= kMaxBatchDim)
       return fail(TOC_EUNSUPPORTED, "batch too large");
     toc_batch &bt = dev->batches[b];
     bt.code_base = codes;
@@ -674,13 +694,12 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
     bt.span_base = spans;
     bt.nnz_base = nnz;
     bt.lvl_base = levels;
-    bt.n_rows = e->n_rows;
+    bt.n_rows = (int32_t)c.rows;
     bt.n_codes = (int32_t)c.codes;
     bt.n_levels = (int32_t)c.levels;
     bt.n_d = (int32_t)c.d;
-    const bool keep = flags & TOC_UPLOAD_KEEP_DEAD;
-    const int64_t nd = keep ? e->n_deep_all : e->n_deep_live;
-    const int64_t ni = keep ? e->n_int1_all : e->n_int1_live;
+    const int64_t nd = c.deep;
+    const int64_t ni = c.int1;
     bt.n_int1 = (int32_t)ni;
     bt.deep_base = deep;
     bt.tree_base = tree;
@@ -694,11 +713,11 @@ toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t fl
     rows += c.rows;
     spans += c.rows + 1;
     d += c.d;
-    nnz += e->nnz;
+    nnz += c.nnz;
     deep += nd;
-    canon += 4 * c.d + 4 * (c.rows + 1) + 10 * e->n_live + 4 * ((int64_t)e->max_depth_live + 1);
+    canon += c.canon;
     max_depth = std::max<int32_t>(max_depth, (int32_t)c.levels);
-    dev->max_rows = std::max<int32_t>(dev->max_rows, e->n_rows);
+    dev->max_rows = std::max<int32_t>(dev->max_rows, (int32_t)c.rows);
     dev->max_codes = std::max<int32_t>(dev->max_codes, (int32_t)c.codes);
     dev->max_levels = std::max<int32_t>(dev->max_levels, (int32_t)c.levels);
     dev->max_d = std::max<int64_t>(dev->max_d, c.d);

@@ -43,6 +43,10 @@ struct toc_dev {
   std::vector<int64_t> dtile_base;  // first decode tile of each batch
   int64_t n_dtiles = 0;
   int64_t tot_levels = 0;           // level entries over all batches
+  // image planned from physical bytes on the device and not yet built (the
+  // per-batch counts of those bytes, kept for the build)
+  bool pending = false;
+  std::vector<toc_phys_info> phys;
 };
 
 namespace toc {
@@ -78,5 +82,15 @@ ArrStarts arr_starts(const toc_dev *dev, int64_t b);
 // Computes layout and totals only.
 toc_status plan_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,
                       toc_dev *dev);
+// The counts of one batch that the layout depends on: tuples, stored codes, depth
+// of the deepest stored code, |D|, stored codes of depth >= 2, depth-1 codes with
+// children, nonzeros, and the canonical bytes (toc_dev_info.canon_bytes).
+struct BatchCounts {
+  int64_t rows, codes, levels, d, deep, int1, nnz, canon;
+};
+// Layout, batch table bases and totals from per-batch counts (the tables' n_lvl1
+// and n_ucols are left to the writer).
+toc_status plan_layout(const BatchCounts *bc, int64_t n_batches, int32_t n_cols, uint32_t flags,
+                       toc_dev *dev);
 
 }  // namespace toc

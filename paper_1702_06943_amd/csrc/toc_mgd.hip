@@ -135,6 +135,7 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                          const float *y, float *h, void *stream) {
   clear_error();
   if (!d) return fail(TOC_EINVAL, "dev is NULL");
+  if (d->pending) return fail(TOC_EINVAL, "image planned but not built");
   if (d->host) return fail(TOC_EINVAL, "image was uploaded to host memory");
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return fail(TOC_EDEVICE, "hipGetDevice failed");

@@ -17,51 +17,56 @@ int width_of(uint64_t mx) {
   return std::max(1, (bits + 7) / 8);
 }
 
-struct Packer {
-  uint8_t *out;   // null: count bytes only
-  size_t n = 0;
-  void put(uint64_t v, int w) {
-    for (int q = 0; q < w; ++q, ++n)
-      if (out) out[n] = (uint8_t)(v >> (8 * q));
-  }
-  void header(uint64_t count, int w) {
-    put(count, 4);
-    put((uint64_t)w, 1);
-  }
+// Widths and unique values of one batch's arrays, computed once per call.
+struct PackPlan {
+  std::vector<uint32_t> u;   // unique values of I (ascending bit patterns)
+  int w_col = 1, w_vix = 1, w_d = 1, w_st = 1;
+  size_t bytes = 0;
 };
 
-// unique values of I (ascending bit patterns)
-std::vector<uint32_t> uniques(const toc_enc *e) {
-  std::vector<uint32_t> u(e->I_bits);
-  std::sort(u.begin(), u.end());
-  u.erase(std::unique(u.begin(), u.end()), u.end());
-  return u;
-}
-
-toc_status pack(const toc_enc *e, Packer &pk) {
+toc_status plan(const toc_enc *e, PackPlan &pl) {
   const size_t nI = e->I_col.size(), nD = e->D_codes.size();
   if (nI > 0xFFFFFFFFu || nD > 0xFFFFFFFFu || (uint64_t)e->n_rows + 1 > 0xFFFFFFFFu)
     return fail(TOC_EUNSUPPORTED, "array longer than a u32 count");
-  const std::vector<uint32_t> u = uniques(e);
+  pl.u.assign(e->I_bits.begin(), e->I_bits.end());
+  std::sort(pl.u.begin(), pl.u.end());
+  pl.u.erase(std::unique(pl.u.begin(), pl.u.end()), pl.u.end());
   uint64_t mc = 0, md = 0;
   for (int32_t c : e->I_col) mc = std::max<uint64_t>(mc, (uint64_t)c);
   for (uint32_t c : e->D_codes) md = std::max<uint64_t>(md, c);
-  int w = width_of(mc);
-  pk.header(nI, w);
-  for (int32_t c : e->I_col) pk.put((uint64_t)c, w);
-  pk.header(u.size(), 4);
-  for (uint32_t b : u) pk.put(b, 4);
-  w = width_of(u.empty() ? 0 : u.size() - 1);
-  pk.header(nI, w);
-  for (uint32_t b : e->I_bits)
-    pk.put((uint64_t)(std::lower_bound(u.begin(), u.end(), b) - u.begin()), w);
-  w = width_of(md);
-  pk.header(nD, w);
-  for (uint32_t c : e->D_codes) pk.put(c, w);
-  w = width_of((uint64_t)nD);
-  pk.header((uint64_t)e->n_rows + 1, w);
-  for (int64_t s : e->D_rowptr) pk.put((uint64_t)s, w);
+  pl.w_col = width_of(mc);
+  pl.w_vix = width_of(pl.u.empty() ? 0 : pl.u.size() - 1);
+  pl.w_d = width_of(md);
+  pl.w_st = width_of((uint64_t)nD);
+  pl.bytes = 25 + nI * (size_t)(pl.w_col + pl.w_vix) + 4 * pl.u.size() + nD * (size_t)pl.w_d +
+             ((size_t)e->n_rows + 1) * (size_t)pl.w_st;
   return TOC_OK;
+}
+
+// v as w little-endian bytes at p; returns the byte after them
+inline uint8_t *put(uint8_t *p, uint64_t v, int w) {
+  for (int q = 0; q < w; ++q) p[q] = (uint8_t)(v >> (8 * q));
+  return p + w;
+}
+
+inline uint8_t *header(uint8_t *p, uint64_t count, int w) {
+  p = put(p, count, 4);
+  return put(p, (uint64_t)w, 1);
+}
+
+void write(const toc_enc *e, const PackPlan &pl, uint8_t *p) {
+  const size_t nI = e->I_col.size();
+  p = header(p, nI, pl.w_col);
+  for (int32_t c : e->I_col) p = put(p, (uint64_t)c, pl.w_col);
+  p = header(p, pl.u.size(), 4);
+  for (uint32_t b : pl.u) p = put(p, b, 4);
+  p = header(p, nI, pl.w_vix);
+  for (uint32_t b : e->I_bits)
+    p = put(p, (uint64_t)(std::lower_bound(pl.u.begin(), pl.u.end(), b) - pl.u.begin()), pl.w_vix);
+  p = header(p, e->D_codes.size(), pl.w_d);
+  for (uint32_t c : e->D_codes) p = put(p, c, pl.w_d);
+  p = header(p, (uint64_t)e->n_rows + 1, pl.w_st);
+  for (int64_t s : e->D_rowptr) p = put(p, (uint64_t)s, pl.w_st);
 }
 
 uint64_t get(const uint8_t *p, int w) {
@@ -80,21 +85,21 @@ extern "C" {
 toc_status toc_enc_pack_size(const toc_enc *enc, size_t *bytes) {
   clear_error();
   if (!enc || !bytes) return fail(TOC_EINVAL, "NULL argument");
-  Packer pk{nullptr};
-  const toc_status st = pack(enc, pk);
-  if (st == TOC_OK) *bytes = pk.n;
+  PackPlan pl;
+  const toc_status st = plan(enc, pl);
+  if (st == TOC_OK) *bytes = pl.bytes;
   return st;
 }
 
 toc_status toc_enc_pack(const toc_enc *enc, void *dst, size_t bytes) {
   clear_error();
   if (!enc || !dst) return fail(TOC_EINVAL, "NULL argument");
-  Packer cnt{nullptr};
-  toc_status st = pack(enc, cnt);
+  PackPlan pl;
+  toc_status st = plan(enc, pl);
   if (st != TOC_OK) return st;
-  if (bytes < cnt.n) return fail(TOC_ESIZE, "%zu bytes given, %zu needed", bytes, cnt.n);
-  Packer pk{(uint8_t *)dst};
-  return pack(enc, pk);
+  if (bytes < pl.bytes) return fail(TOC_ESIZE, "%zu bytes given, %zu needed", bytes, pl.bytes);
+  write(enc, pl, (uint8_t *)dst);
+  return TOC_OK;
 }
 
 toc_status toc_phys_info_get(const void *blob, size_t bytes, toc_phys_info *info) {

@@ -20,7 +20,8 @@ from . import build as B
 ASAN_DIR = os.path.join(B.BUILD, "asan")
 ASAN_LIB = os.path.join(ASAN_DIR, "libtoc.so")
 SAN = ["-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=undefined"]
-TESTS = ["tests/test_encode_abi.py", "tests/test_layout.py", "tests/test_phys.py"]
+TESTS = ["tests/test_encode_abi.py", "tests/test_layout.py", "tests/test_phys.py",
+         "tests/test_ingest_host.py"]
 
 
 def runtime():
@@ -34,13 +35,13 @@ def build_asan(verbose=False):
     os.makedirs(ASAN_DIR, exist_ok=True)
     clang = "/opt/rocm/llvm/bin/clang++"
     objs = []
-    for src in ("toc_host.cpp", "toc_phys.cpp"):
+    for src in B.HOST_SOURCES:
         o = os.path.join(ASAN_DIR, src.replace(".cpp", ".o"))
         B._run([clang, "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC", *SAN,
                 "-I", B.INCLUDE, "-c", os.path.join(B.CSRC, src), "-o", o], verbose)
         objs.append(o)
     host_san = [x for f in SAN for x in ("-Xarch_host", f)]
-    for src in ("toc_device.hip", "toc_cprime.hip", "toc_mgd.hip", "toc_encode.hip", "toc_mlp.hip"):
+    for src in B.HIP_SOURCES:
         o = os.path.join(ASAN_DIR, src.replace(".hip", ".o"))
         B._run([B.HIPCC, "-O1", "-g", "-std=c++17", "-fPIC", f"--offload-arch={B.ARCH}",
                 *B.NO_PACKED_FP32, *host_san, "-I", B.INCLUDE, "-c", os.path.join(B.CSRC, src),

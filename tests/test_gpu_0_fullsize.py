@@ -7,6 +7,9 @@ every batch of a workload, one launch of each op over all of them.
   1,000 columns, k = 200 (a 145 GB image, uploaded in chunks through pinned
   staging buffers).
 
+For the first, the image is also built on the device from the batches' physical
+bytes (section 3.2) and must equal the host-built one byte for byte.
+
 The oracle checks sampled batches one by one (products within 1e-5 * S, decode
 bit-exact against the regenerated batch); properties that hold at any size are
 checked on the whole output.
@@ -59,6 +62,7 @@ def test_fullsize_sampled(cfg):
 
 def _check_workload(bench, w, cfg, spec, nb, k):
     bench.upload_workload(w, k)
+    packed = bench.pack_all(w) if cfg == "c3" else None
     w.encs = None
     info = w.info
     assert info["n_batches"] == nb and info["n_rows"] == nb * spec["rows"]
@@ -100,3 +104,7 @@ def _check_workload(bench, w, cfg, spec, nb, k):
         assert np.array_equal(w.ccol[p0:p1].cpu().numpy(), c)
         assert np.array_equal(w.cval[p0:p1].cpu().numpy().view(np.uint32), v.view(np.uint32))
     print(f"{cfg} sampled batches {sample}: max |err|/S = {worst:.3e}", flush=True)
+    if packed is not None:
+        ing = bench.time_ingest(w, packed)
+        print(f"{cfg} device ingest: {ing}", flush=True)
+        assert ing["identical_to_host_image"]
