@@ -157,14 +157,15 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   level   : uint32 per batch n_levels+1 entries (lvl_base)
  *   key     : toc_key of each code (its key pair, 8 bytes), so that a code's key
  *             comes with one 8-byte read
- *   link    : toc_link of each code (its parent and depth, 8 bytes)
+ *   link    : toc_link of each code of depth >= 2 (its parent and depth, 8 bytes),
+ *             code c of batch b at deep_base + c - n_lvl1; a depth-1 code has none
+ *             (no parent, depth 1)
  *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
  *   dcodes  : uint32 local code of each entry of D (d_base)
- *   occ_off : uint32 per batch n_codes+1 offsets into occ_row (at code_base + b),
- *             by position
- *   occ_row : uint32 row of each entry of D, grouped by position (d_base): D
- *             inverted, the index set of the sum that defines G(x) in Theorem 2;
- *             bit 31 is set on the first entry of each code
+ *   occ_off : uint32 per batch n_tree+1 entries (at tree_base + b): tree code h's
+ *             occurrences (the tuples holding its code: D inverted, the index set
+ *             of the sum that defines G(x) in Theorem 2) are centry entries
+ *             occ_off[h] .. occ_off[h+1]-1 of the batch (h as in tchild)
  *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
  *             by key column (tree_base)
  *   dtiles  : uint32 x 4 per run of 1024 entries of D (at least one per batch):
@@ -179,16 +180,18 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *   tchild  : uint32 per batch n_tree+1 entries (at tree_base + b): the children of
  *             tree code h (h counting the codes with children at depth 1, then
  *             the codes of depth >= 2) are the codes tchild[h] .. tchild[h+1]-1
- *   pval    : float per batch n_codes entries (code_base): the key value of the
- *             code at each position
  *   centry  : uint32 per batch n_d + n_tree entries (at d_base + tree_base): for
- *             each key column in turn, its leaf occurrences (the occ_row words of
- *             the column's leaves, first-occurrence bit included) and then its
- *             tree codes (tlist entries) with bit 30 set; column j starts at the
- *             cols entries of j: leaf occurrences before it plus tlist entries
- *             before it.  Needs rows and codes below 2^30 per batch.
- *   cval    : float per centry entry (same index): the key value of the entry's
- *             code (the multiplier of the left multiplication's term)
+ *             each key column in turn, its leaf occurrences (the tuple of each
+ *             entry of D whose code is one of the column's leaves, the leaves in
+ *             position order, each leaf's tuples ascending, bit 31 on a leaf's
+ *             first) and then its tree codes (tlist entries) with bit 30 set;
+ *             column j starts at the cols entries of j: leaf occurrences before it
+ *             plus tlist entries before it.  After the last column, the tree
+ *             codes' occurrences (plain tuple indexes, ascending per code), where
+ *             occ_off points.  Needs rows and codes below 2^30 per batch.
+ *   cval    : float per centry entry of a column (same index): the key value of
+ *             the entry's code (the multiplier of the left multiplication's term);
+ *             0 beside the tree codes' occurrences
  * Depth-1 codes without children are numbered in the order of their first entry
  * in D; the codes of each level d >= 2 are sorted by parent.                    */
 typedef struct {
@@ -212,8 +215,8 @@ typedef struct {
 } toc_link;
 
 typedef struct {
-  int64_t batches, level, key, link, span, dcodes, occ_off, occ_row, tlist, dtiles, cols,
-      tchild, pval, centry, cval, end;
+  int64_t batches, level, key, link, span, dcodes, occ_off, tlist, dtiles, cols, tchild, centry,
+      cval, end;
 } toc_layout;
 
 toc_status toc_dev_layout_get(const toc_dev *dev, toc_layout *layout);

@@ -64,8 +64,8 @@ class PhysInfo(C.Structure):
 
 class Layout(C.Structure):
     _fields_ = [(n, C.c_int64) for n in
-                ("batches", "level", "key", "link", "span", "dcodes", "occ_off", "occ_row",
-                 "tlist", "dtiles", "cols", "tchild", "pval", "centry", "cval", "end")]
+                ("batches", "level", "key", "link", "span", "dcodes", "occ_off", "tlist",
+                 "dtiles", "cols", "tchild", "centry", "cval", "end")]
 
 
 # records of the image's key and link arrays (toc_key, toc_link)

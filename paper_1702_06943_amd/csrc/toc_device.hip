@@ -63,8 +63,7 @@ struct Img {
   const toc_link *link;
   const uint32_t *span;
   const uint32_t *dcodes;
-  const uint32_t *pval;     // key value bits by left-product position
-  const uint32_t *centry;   // left-product entries of each key column
+  const uint32_t *centry;   // left-product entries: leaf occurrences, tree codes, tree occurrences
   const uint32_t *cval;     // key value bits of each centry entry's code
 };
 
@@ -74,8 +73,7 @@ Img image_of(const toc_dev *d) {
   return Img{(const toc_batch *)(b + L.batches), (const uint32_t *)(b + L.level),
              (const toc_key *)(b + L.key), (const toc_link *)(b + L.link),
              (const uint32_t *)(b + L.span), (const uint32_t *)(b + L.dcodes),
-             (const uint32_t *)(b + L.pval), (const uint32_t *)(b + L.centry),
-             (const uint32_t *)(b + L.cval)};
+             (const uint32_t *)(b + L.centry), (const uint32_t *)(b + L.cval)};
 }
 
 // Views of one field of a batch's node records, indexed by local code.
@@ -91,6 +89,12 @@ struct NodePar {
   const toc_link *n;
   __device__ uint32_t operator[](int64_t c) const { return n[c].parent; }
 };
+
+// The links of a batch's codes of depth >= 2 (the image stores none for depth-1
+// codes), as a view indexed by local code: valid for codes n_lvl1 .. n_codes-1.
+__device__ inline const toc_link *deep_links(const toc_link *all, const toc_batch &bt) {
+  return all + (bt.deep_base - (int64_t)bt.n_lvl1);
+}
 
 // Index of the calling wave in its workgroup, as a wave-uniform (scalar) value.
 __device__ inline int wave_id() {
@@ -193,7 +197,7 @@ __global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
   extern __shared__ float H[];
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.link + bt.code_base};
+  const NodePar par{deep_links(im.link, bt)};
   const NodeCol col{im.key + bt.code_base};
   const NodeVal val{im.key + bt.code_base};
   for (int d = 1; d <= bt.n_levels; ++d) {
@@ -220,12 +224,13 @@ __global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
 // Left multiplication (Theorem 2, Algorithm 5) without atomics, over the
 // image's left positions (a leaf's position orders it by column; every other
 // code is at its own index): H[p] = G(x) is pulled from the inverted index (the
-// sum over the entries of D equal to the code x at p; a thread takes 4 positions
-// at a time and loads their occurrence rows together), each code then adds its
-// children's H (children are contiguous: levels are sorted by parent), deepest
-// level first; finally a thread per key column writes it once, summing val * H
-// over the column's leaves (a contiguous range of positions) and tree codes (a
-// contiguous stretch of the tree list), both read from the image's column index.
+// sum over the entries of D equal to the code x at p, whose tuples are listed in
+// the batch's entry array; a thread takes 4 positions at a time and loads their
+// occurrence rows together), each code then adds its children's H (children are
+// contiguous: levels are sorted by parent), deepest level first; finally a thread
+// per key column writes it once, summing val * H over the column's leaves (a
+// contiguous range of positions) and tree codes (a contiguous stretch of the tree
+// list), both read from the image's column index.
 constexpr uint32_t kFirstOccK1 = 0x80000000u;
 // Workgroup of the k = 1 right product: small, so that many batches (each a chain
 // of dependent loads and barriers) are in flight on a CU at once.
@@ -235,44 +240,79 @@ constexpr int kK1Occ = 4;        // occurrences per code loaded together
 constexpr int kK1Cols = 8;       // output columns per thread and pass
 constexpr int kK1Tree = 4;       // tree-list entries per column loaded together
 
+// Where a batch's left positions find their occurrences: a leaf position p
+// (n_int1 <= p < n_lvl1) at entries lo[p - n_int1] .. lo[p - n_int1 + 1]-1 of the
+// batch's entry array, a tree code (its own position) at to[h] .. to[h+1]-1, h its
+// tree row; a leaf's value beside its first occurrence, a tree code's in its key.
+struct OccIndex {
+  const uint32_t *lo, *to, *ce, *cv;
+  const toc_key *key;
+  uint32_t ni, n1;
+  __device__ uint32_t hrow(uint32_t c) const { return c < ni ? c : c - n1 + ni; }
+  __device__ bool leaf(uint32_t p) const { return p >= ni && p < n1; }
+  __device__ uint32_t start(uint32_t p) const { return leaf(p) ? lo[p - ni] : to[hrow(p)]; }
+  __device__ uint32_t end(uint32_t p) const { return leaf(p) ? lo[p - ni + 1] : to[hrow(p) + 1]; }
+  // (0 for a leaf without occurrences, a kept dead code, whose sum is 0 anyway)
+  __device__ float val(uint32_t p) const {
+    if (!leaf(p)) return key[p].val;
+    const uint32_t o = lo[p - ni];
+    return o < lo[p - ni + 1] ? __uint_as_float(cv[o]) : 0.0f;
+  }
+};
+
+__device__ inline OccIndex occ_index(const Img &im, const uint32_t *occ_off_all, const toc_batch &bt,
+                                     int64_t b) {
+  OccIndex x;
+  x.ni = (uint32_t)bt.n_int1;
+  x.n1 = (uint32_t)bt.n_lvl1;
+  x.lo = occ_off_all + bt.code_base + 2 * b;
+  x.to = x.lo + (x.n1 - x.ni) + 1;
+  x.ce = im.centry + bt.d_base + bt.tree_base;
+  x.cv = im.cval + bt.d_base + bt.tree_base;
+  x.key = im.key + bt.code_base;
+  return x;
+}
+
 __global__ __launch_bounds__(kBlock) void left_k1_kernel(
-    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
-    const uint32_t *__restrict__ tchild_all, int64_t b0, int32_t m, int32_t max_rows,
-    int32_t max_codes, const float *__restrict__ G, int64_t ldg, float *__restrict__ out,
-    int64_t ldo, int accumulate) {
+    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ tlist_all,
+    const uint32_t *__restrict__ cols_all, const uint32_t *__restrict__ tchild_all, int64_t b0,
+    int32_t m, int32_t max_rows, int32_t max_codes, const float *__restrict__ G, int64_t ldg,
+    float *__restrict__ out, int64_t ldo, int accumulate) {
   extern __shared__ float sm[];
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = uniform_batch(im.batches + b);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *pv = im.pval + bt.code_base;           // values by position
-  const uint32_t *oo = occ_off_all + bt.code_base + b;
-  const uint32_t *orow = occ_row_all + bt.d_base;
+  const OccIndex ox = occ_index(im, occ_off_all, bt, b);
   const uint32_t *tl = tlist_all + bt.tree_base;
   const uint32_t *tch = tchild_all + bt.tree_base + b;
   const uint32_t *cx = cols_all + b * 4 * (int64_t)(m + 1);   // Loff, Ost, Toff, Ord
-  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+  const uint32_t nc = (uint32_t)bt.n_codes, ni = (uint32_t)bt.n_int1;
   float *Gs = sm;                                     // max_rows
   float *H = sm + max_rows;                           // max_codes
-  auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
+  auto hrow = [&](uint32_t c) -> uint32_t { return ox.hrow(c); };
   float *ob = out + b * (int64_t)m * ldo;
   for (int r = threadIdx.x; r < bt.n_rows; r += kBlock) Gs[r] = G[(bt.row_base + r) * ldg];
   __syncthreads();
-  // G(c) for every code
+  // G(c) for every code; a leaf's times its value (read beside its first
+  // occurrence), since a leaf has no children to add first
   for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
-    uint32_t o0[kK1Codes], o1[kK1Codes];
+    uint32_t o0[kK1Codes], o1[kK1Codes], vb[kK1Codes];
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       const uint32_t c = c0 + u * kBlock;
-      o0[u] = c < nc ? oo[c] : 0u;
-      o1[u] = c < nc ? oo[c + 1] : 0u;
+      o0[u] = c < nc ? ox.start(c) : 0u;
+      o1[u] = c < nc ? ox.end(c) : 0u;
     }
     float s[kK1Codes];
     uint32_t w[kK1Codes][kK1Occ];
 #pragma unroll
-    for (int u = 0; u < kK1Codes; ++u)
+    for (int u = 0; u < kK1Codes; ++u) {
+      const uint32_t c = c0 + u * kBlock;
+      // 1.0 for a tree code; a leaf without occurrences (kept dead code) sums to 0
+      vb[u] = c < nc && ox.leaf(c) && o1[u] > o0[u] ? ox.cv[o0[u]] : 0x3F800000u;
 #pragma unroll
-      for (int v = 0; v < kK1Occ; ++v) w[u][v] = o0[u] + v < o1[u] ? orow[o0[u] + v] : 0xFFFFFFFFu;
+      for (int v = 0; v < kK1Occ; ++v) w[u][v] = o0[u] + v < o1[u] ? ox.ce[o0[u] + v] : 0xFFFFFFFFu;
+    }
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       s[u] = 0.0f;
@@ -280,13 +320,13 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
       for (int v = 0; v < kK1Occ; ++v)
         if (w[u][v] != 0xFFFFFFFFu) s[u] += Gs[w[u][v] & ~kFirstOccK1];
       if (o1[u] > o0[u] + kK1Occ)
-        s[u] += blocked_sum<8>(o0[u] + kK1Occ, o1[u], 1u, [&](uint32_t o) { return orow[o]; },
+        s[u] += blocked_sum<8>(o0[u] + kK1Occ, o1[u], 1u, [&](uint32_t o) { return ox.ce[o]; },
                             [&](uint32_t w) { return Gs[w & ~kFirstOccK1]; });
     }
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       const uint32_t c = c0 + u * kBlock;
-      if (c < nc) H[c] = s[u];
+      if (c < nc) H[c] = ox.leaf(c) ? __uint_as_float(vb[u]) * s[u] : s[u];
     }
   }
   __syncthreads();
@@ -300,19 +340,20 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
     }
     __syncthreads();
   }
-  // H[c] becomes val(c) * H[c]: a key column's output is the plain sum of these
-  // over the column's codes
-  for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
+  // a tree code's H becomes val * H (the leaves' already are): a key column's
+  // output is the plain sum of these over the column's codes
+  const uint32_t n_tree = ni + (nc - ox.n1);
+  for (uint32_t t0 = threadIdx.x; t0 < n_tree; t0 += kBlock * kK1Codes) {
     float v[kK1Codes];
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
-      const uint32_t c = c0 + u * kBlock;
-      v[u] = c < nc ? __uint_as_float(pv[c]) : 0.0f;
+      const uint32_t t = t0 + u * kBlock, c = t < ni ? t : t - ni + ox.n1;
+      v[u] = t < n_tree ? ox.key[c].val : 0.0f;
     }
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
-      const uint32_t c = c0 + u * kBlock;
-      if (c < nc) H[c] *= v[u];
+      const uint32_t t = t0 + u * kBlock, c = t < ni ? t : t - ni + ox.n1;
+      if (t < n_tree) H[c] *= v[u];
     }
   }
   __syncthreads();
@@ -370,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
     float *__restrict__ R, int64_t ldr, float *__restrict__ ws) {
   const toc_batch bt = im.batches[b0 + blockIdx.x];
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const NodePar par{im.link + bt.code_base};
+  const NodePar par{deep_links(im.link, bt)};
   const NodeCol col{im.key + bt.code_base};
   const NodeVal val{im.key + bt.code_base};
   const int lane = threadIdx.x % kWave, wave = wave_id();
@@ -449,7 +490,7 @@ __global__ __launch_bounds__(kBlock) void right_wide_kernel(
 // sum is blocked (kBlk terms per partial sum).  H rows live in the workspace.
 template <int KPL>
 __global__ __launch_bounds__(kBlock) void left_wide_kernel(
-    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
+    Img im, const uint32_t *__restrict__ occ_off_all,
     const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
     const uint32_t *__restrict__ tchild_all, int64_t b0, int64_t ws_base, int32_t m,
     const float *__restrict__ G, int64_t ldg, int kt, float *__restrict__ out, int64_t ldo,
@@ -458,9 +499,7 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
   const int64_t b = b0 + blockIdx.x;
   const toc_batch bt = uniform_batch(im.batches + b);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *pv = im.pval + bt.code_base;             // key value bits by position
-  const uint32_t *oo = occ_off_all + bt.code_base + b;
-  const uint32_t *orow = occ_row_all + bt.d_base;
+  const OccIndex ox = occ_index(im, occ_off_all, bt, b);
   const uint32_t *tl = tlist_all + bt.tree_base;
   const uint32_t *tch = tchild_all + bt.tree_base + b;
   const uint32_t *cx = cols_all + b * 4 * (int64_t)(m + 1);
@@ -502,8 +541,8 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
     for (uint32_t c = a + wave; c < e; c += kWaves) {
       const int64_t h = hrow(c);
       start();
-      for (uint32_t o = oo[c], o1 = oo[c + 1]; o < o1; ++o)
-        add_term(1.0f, Gb + (int64_t)(orow[o] & ~kFirst) * ldg);
+      for (uint32_t o = ox.start(c), o1 = ox.end(c); o < o1; ++o)
+        add_term(1.0f, Gb + (int64_t)(ox.ce[o] & ~kFirst) * ldg);
       for (uint32_t ch = tch[h], ch1 = tch[h + 1]; ch < ch1; ++ch)
         add_term(1.0f, Ht + hrow(ch) * kt);
       finish();
@@ -523,13 +562,13 @@ __global__ __launch_bounds__(kBlock) void left_wide_kernel(
   for (int j = wave; j < m; j += kWaves) {
     start();
     for (uint32_t p = Loff[j], p1 = Loff[j + 1]; p < p1; ++p) {
-      const float v = __uint_as_float(pv[p]);
-      for (uint32_t o = oo[p], o1 = oo[p + 1]; o < o1; ++o)
-        add_term(v, Gb + (int64_t)(orow[o] & ~kFirst) * ldg);
+      const float v = ox.val(p);
+      for (uint32_t o = ox.start(p), o1 = ox.end(p); o < o1; ++o)
+        add_term(v, Gb + (int64_t)(ox.ce[o] & ~kFirst) * ldg);
     }
     for (uint32_t t = Toff[j], t1 = Toff[j + 1]; t < t1; ++t) {
       const uint32_t c = tl[t];
-      add_term(__uint_as_float(pv[c]), Ht + hrow(c) * kt);
+      add_term(ox.val(c), Ht + hrow(c) * kt);
     }
     finish();
     float *o = ob + (int64_t)j * ldo;
@@ -830,7 +869,7 @@ __global__ __launch_bounds__(kRtBlock) void right_tiled_kernel(
     // so that the loads of a round are all in flight together.
     {
       const toc_key *key_a = im.key + ba.code_base, *key_b = im.key + bb.code_base;
-      const toc_link *link_a = im.link + ba.code_base, *link_b = im.link + bb.code_base;
+      const toc_link *link_a = deep_links(im.link, ba), *link_b = deep_links(im.link, bb);
       const uint32_t g8 = threadIdx.x / 8u, q4 = 4u * (threadIdx.x % 8u);
       constexpr uint32_t stride = kRtBlock / 8;
       const int n_lev = max(lev_a, lev_b);
@@ -1111,7 +1150,7 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
     const int kt = min(kRtKT, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const NodePar par{im.link + bt.code_base};
+    const NodePar par{deep_links(im.link, bt)};
     const NodeCol col{im.key + bt.code_base};
     const NodeVal val{im.key + bt.code_base};
     const uint32_t *span = im.span + bt.span_base;
@@ -1499,7 +1538,7 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
     {
       const uint32_t *lvl = im.level + bt.lvl_base;
       const toc_key *key = im.key + bt.code_base;
-      const toc_link *link = im.link + bt.code_base;
+      const toc_link *link = deep_links(im.link, bt);
       const uint32_t g16 = threadIdx.x / kRtLanes;
       constexpr uint32_t stride = kRtBlock / kRtLanes;
       for (int d = 2; d <= bt.n_levels; ++d) {
@@ -1697,11 +1736,11 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
 // ---------------------------------------------------------------------------
 // Left multiplication by pulling (Theorem 2 read as a definition, Algorithm 8's
 // result): H(x) is the sum of the G rows over the entries of D equal to x (the
-// inverted index occ_off/occ_row lists them per code) plus the H of x's children,
-// and output row j is the sum of val(x) * H(x) over the codes x of key column j.
-// Work items are (batch, TW-column tile) pairs dealt per XCD as in the right
-// product.  A worker loads the batch's G tile into LDS (row nrows_max is all
-// zeros), then
+// image lists each tree code's tuples after the column entries, where occ_off
+// points) plus the H of x's children, and output row j is the sum of
+// val(x) * H(x) over the codes x of key column j.  Work items are (batch,
+// TW-column tile) pairs dealt per XCD as in the right product.  A worker loads the
+// batch's G tile into LDS (row nrows_max is all zeros), then
 //  * tree codes (codes with children or of depth >= 2), deepest level first, a
 //    lane group per code: H = own occurrences + children's H (children of a code
 //    are contiguous, levels being sorted by parent); H rows follow the G tile in
@@ -1709,10 +1748,9 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
 //  * output columns: a group of TW/4 lanes owns one column j (a lane holds 4 of
 //    the tile's columns) and sums val * row over its entries: the occurrences of
 //    the column's leaf codes (depth-1 codes without children, whose left
-//    positions are ordered by column, so one contiguous stretch of occ_row) and
-//    then its tree codes.  The position of a leaf occurrence is recovered from
-//    the first-occurrence bits of occ_row by a popcount carried along the
-//    column, and its value read from pval.  Entries are loaded two chunks ahead
+//    positions are ordered by column, so one contiguous stretch of the entry
+//    array) and then its tree codes (a stretch after all leaf occurrences), the
+//    multiplier loaded beside each entry.  Entries are loaded two chunks ahead
 //    and translated to (LDS row, multiplier) one chunk ahead; a group of 16
 //    lanes takes them from the lane that translated them by DPP row broadcast,
 //    a group of 8 from a per-wave stage in LDS.  Groups of columns are handed
@@ -1749,8 +1787,7 @@ struct LtChunk {
 
 template <int TW, bool TREE_LDS>
 __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
-    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ occ_row_all,
-    const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
+    Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
     const uint32_t *__restrict__ tchild_all, int64_t nb, int n_tiles, int spw, int max_rows,
     int max_tree, int tree_cap, int m, const float *__restrict__ G, int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
@@ -1798,9 +1835,10 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const int kt = min(TW, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
-    const uint32_t *oo = occ_off_all + bt.code_base + b;
-    const uint32_t *orow = occ_row_all + bt.d_base;
     const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+    // tree row h's occurrences: entries to[h] .. to[h+1]-1 of the batch's entry array
+    const uint32_t *to = occ_off_all + bt.code_base + 2 * b + (n1 - ni) + 1;
+    const uint32_t *orow = im.centry + bt.d_base + bt.tree_base;
     const uint32_t n_tree = ni + (nc - n1);
     const int nrows = bt.n_rows;
     auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
@@ -1883,8 +1921,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           const bool in = c < e;
           const uint32_t cc = in ? c : c0;
           h[u] = hrow(cc);
-          o0[u] = oo[cc];
-          o1[u] = in ? oo[cc + 1] : o0[u];
+          o0[u] = to[h[u]];
+          o1[u] = in ? to[h[u] + 1] : o0[u];
           k0[u] = Coff[h[u]];
           k1[u] = in ? Coff[h[u] + 1] : k0[u];
         }
@@ -1983,14 +2021,18 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     };
     // column j of group g of column group cg; past the last column: no entries.
     // Its entries (leaf occurrences, then tree codes) start at cst in centry.
-    struct ColSpan { uint32_t cst, nl, nt; };
+    // Its leaf occurrences start at lst in centry, its tree codes at tst (after all
+    // the batch's leaf occurrences).
+    struct ColSpan { uint32_t lst, tst, nl, nt; };
+    const uint32_t n_lo = Ost[m];
     auto col_of = [&](int cg) -> ColSpan {
       const int o = cg * GPW + grp;
       const int j = o < n_used ? (int)Ord[o] : m;
       const int j1 = min(j + 1, m);
       ColSpan c;
       const uint32_t ost = Ost[j], tof = Toff[j];
-      c.cst = ost + tof;
+      c.lst = ost;
+      c.tst = n_lo + tof;
       c.nl = Ost[j1] - ost;
       c.nt = Toff[j1] - tof;
       return c;
@@ -1998,7 +2040,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     // load stage: column group lcg, entries [lj, lj + CHK) of each column
     int lcg = wave, ncg = n_cg;
     uint32_t lj = 0, lmax = 0;
-    ColSpan lc{0u, 0u, 0u};
+    ColSpan lc{0u, 0u, 0u, 0u};
     if (lcg < n_cg) {
       lc = col_of(lcg);
       lmax = wave_max(lc.nl + lc.nt);
@@ -2032,7 +2074,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const BufRes rs_cent = buf_res(im.centry + bt.d_base + bt.tree_base, (uint32_t)bt.n_d + n_tree);
     const BufRes rs_cval = buf_res(im.cval + bt.d_base + bt.tree_base, (uint32_t)bt.n_d + n_tree);
     // L: the entry words of each lane (entries sub + h * LPG of the chunk: the
-    // occ_row word of a leaf occurrence, or a tree code marked kTreeEntry), the
+    // tuple of a leaf occurrence, or a tree code marked kTreeEntry), the
     // value of the entry's code beside it, and the wave masks of lanes with an
     // entry.  A lane without one reads past the buffers: word and value 0.
     auto load_entry = [&](uint32_t (&w)[PER], uint32_t (&v)[PER], uint64_t (&ok)[PER]) {
@@ -2042,7 +2084,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         const uint32_t e = lj + (uint32_t)(sub + h * LPG);
         const bool in = live && e < lc.nl + lc.nt;
         ok[h] = __ballot(in);
-        const uint32_t at = in ? lc.cst + e : 0xFFFFFFFFu;
+        const uint32_t at = in ? e + (e < lc.nl ? lc.lst : lc.tst - lc.nl) : 0xFFFFFFFFu;
         w[h] = buf_load(rs_cent, at);
         v[h] = buf_load(rs_cval, at);
       }
@@ -2277,7 +2319,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
   const uint4 dt = dtiles[t];                       // batch, first entry, pairs before, first row
   const toc_batch bt = im.batches[dt.x];
   const toc_key *key = im.key + bt.code_base;
-  const toc_link *link = im.link + bt.code_base;
+  const toc_link *link = deep_links(im.link, bt);
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
@@ -2365,20 +2407,17 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
 
 // ===========================================================================
 // Sparse-safe element-wise operations (Algorithm 3): every key value of the
-// image, and its copy at the code's left position, changes alike.  Elementwise
-// over all stored codes; both arrays have one entry per stored code.
+// image, and its copies beside the left multiplication's entries, changes alike.
 // ===========================================================================
 constexpr int kMapBlock = 256;
 
-__global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restrict__ key,
-                                                               uint32_t *__restrict__ pval,
-                                                               int64_t n, uint32_t *__restrict__ cval,
+__global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restrict__ key, int64_t n,
+                                                               uint32_t *__restrict__ cval,
                                                                int64_t n_cval, int op, float c) {
   const int64_t stride = (int64_t)gridDim.x * kMapBlock;
   for (int64_t i = (int64_t)blockIdx.x * kMapBlock + threadIdx.x; i < n; i += stride) {
-    const float v = key[i].val, w = __uint_as_float(pval[i]);
+    const float v = key[i].val;
     key[i].val = op == TOC_MAP_SCALE ? v * c : v * v;
-    pval[i] = __float_as_uint(op == TOC_MAP_SCALE ? w * c : w * w);
   }
   // the copies beside the left multiplication's column entries
   for (int64_t i = (int64_t)blockIdx.x * kMapBlock + threadIdx.x; i < n_cval; i += stride) {
@@ -2408,7 +2447,7 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
   const int lane = threadIdx.x % kWave, wave = wave_id();
   float *Ab = A + bt.row_base * lda;
   const toc_key *key = im.key + bt.code_base;
-  const toc_link *link = im.link + bt.code_base;
+  const toc_link *link = deep_links(im.link, bt);
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
@@ -2674,16 +2713,14 @@ struct ImgArr {
 const ImgArr kImgArrs[] = {
     {&toc_layout::level, 4, [](const toc::ArrStarts &a) { return a.level; }},
     {&toc_layout::key, 8, [](const toc::ArrStarts &a) { return a.code; }},
-    {&toc_layout::link, 8, [](const toc::ArrStarts &a) { return a.code; }},
+    {&toc_layout::link, 8, [](const toc::ArrStarts &a) { return a.deep; }},
     {&toc_layout::span, 4, [](const toc::ArrStarts &a) { return a.span; }},
     {&toc_layout::dcodes, 4, [](const toc::ArrStarts &a) { return a.d; }},
-    {&toc_layout::occ_off, 4, [](const toc::ArrStarts &a) { return a.code + a.b; }},
-    {&toc_layout::occ_row, 4, [](const toc::ArrStarts &a) { return a.d; }},
+    {&toc_layout::occ_off, 4, [](const toc::ArrStarts &a) { return a.code + 2 * a.b; }},
     {&toc_layout::tlist, 4, [](const toc::ArrStarts &a) { return a.tree; }},
     {&toc_layout::dtiles, 16, [](const toc::ArrStarts &a) { return a.dtile; }},
     {&toc_layout::cols, 4, [](const toc::ArrStarts &a) { return a.cols; }},
     {&toc_layout::tchild, 4, [](const toc::ArrStarts &a) { return a.tree + a.b; }},
-    {&toc_layout::pval, 4, [](const toc::ArrStarts &a) { return a.code; }},
     {&toc_layout::centry, 4, [](const toc::ArrStarts &a) { return a.d + a.tree; }},
     {&toc_layout::cval, 4, [](const toc::ArrStarts &a) { return a.d + a.tree; }},
 };
@@ -2969,13 +3006,12 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
     if ((st = allow_lds(left_k1_kernel, lds))) return st;
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
-    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
     const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
     const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-      hipLaunchKernelGGL(left_k1_kernel, dim3(g), dim3(kBlock), lds, s, im, occ_off, occ_row,
+      hipLaunchKernelGGL(left_k1_kernel, dim3(g), dim3(kBlock), lds, s, im, occ_off,
                          tlist, cols, tchild, b0, m, d->max_rows, d->max_codes, G, ldg, out, ldo,
                          accumulate);
       if ((st = launch_status("left_k1_kernel"))) return st;
@@ -3006,7 +3042,6 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
                   (long long)plan.ws_floats * 4);
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
-    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
     const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
     const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
@@ -3015,7 +3050,7 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
   do {                                                                                         \
     if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
     hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
-                       im, occ_off, occ_row, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,     \
+                       im, occ_off, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,              \
                        d->max_rows, (int)d->max_tree, (int)plan.lds_rows, m, G, ldg, k, out, ldo,  \
                        accumulate, (float *)ws, slot);                                          \
   } while (0)
@@ -3036,14 +3071,13 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
     const int kpl = (kt + kWave - 1) / kWave;
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
-    const uint32_t *occ_row = (const uint32_t *)(bb + d->layout.occ_row);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
     const uint32_t *cols = (const uint32_t *)(bb + d->layout.cols);
     const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     st = for_each_pass(d, TOC_OP_LEFT, cap_rows,
                        [&](int64_t b0, int64_t n, int64_t base) -> toc_status {
       TOC_DISPATCH_KPL(kpl, left_wide_kernel, dim3((unsigned)n), dim3(kBlock), 0, s, im, occ_off,
-                       occ_row, tlist, cols, tchild, b0, base, m, G + k0, ldg, kt, out + k0, ldo,
+                       tlist, cols, tchild, b0, base, m, G + k0, ldg, kt, out + k0, ldo,
                        accumulate, (float *)ws);
       return launch_status("left_wide_kernel");
     });
@@ -3110,9 +3144,8 @@ toc_status toc_map_values(const toc_dev *d, int32_t op, float c, void *stream) {
   const int64_t blocks = std::min<int64_t>((n + kMapBlock - 1) / kMapBlock, 64 * 256);
   const int64_t n_cval = (d->layout.end - d->layout.cval) / 4;
   hipLaunchKernelGGL(map_values_kernel, dim3((unsigned)blocks), dim3(kMapBlock), 0,
-                     (hipStream_t)stream, (toc_key *)(bb + d->layout.key),
-                     (uint32_t *)(bb + d->layout.pval), n, (uint32_t *)(bb + d->layout.cval),
-                     n_cval, (int)op, c);
+                     (hipStream_t)stream, (toc_key *)(bb + d->layout.key), n,
+                     (uint32_t *)(bb + d->layout.cval), n_cval, (int)op, c);
   return launch_status("map_values_kernel");
 }
 

@@ -384,7 +384,7 @@ Counts counts_of(const toc_enc *e, uint32_t flags) {
 }
 
 struct ImgScratch {
-  std::vector<uint32_t> parent, first, depth, newidx, bucket, fill, fpos, lpos, at_lpos;
+  std::vector<uint32_t> parent, first, depth, newidx, bucket, fill, fpos, lpos, at_lpos, poff, prow;
   std::vector<uint8_t> live, has_child;
   std::vector<int64_t> cnt, bucket_off;
   std::vector<uint64_t> keys;
@@ -491,14 +491,18 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       for (uint64_t kc : S.keys) S.newidx[(uint32_t)kc] = (uint32_t)at++;
     }
   }
+  // links of the codes of depth >= 2 (a depth-1 code has no parent), by code - n1
+  const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;
   toc_key *node = (toc_key *)(dst + L.key) + bt.code_base;
-  toc_link *link = (toc_link *)(dst + L.link) + bt.code_base;
+  toc_link *link = (toc_link *)(dst + L.link) + bt.deep_base;
   for (int64_t c = 1; c < N; ++c) {
-    if (!S.live[c]) continue;
+    if (!S.live[c] || S.depth[c] == 1) continue;
     const uint32_t at = S.newidx[c];
-    link[at].parent = S.depth[c] == 1 ? 0xFFFFFFFFu : S.newidx[S.parent[c]];
-    link[at].depth = S.depth[c];
+    link[at - n1].parent = S.newidx[S.parent[c]];
+    link[at - n1].depth = S.depth[c];
   }
+  auto parent_of = [&](int64_t c) -> uint32_t { return c < n1 ? 0xFFFFFFFFu : link[c - n1].parent; };
+  auto depth_of = [&](int64_t c) -> uint32_t { return c < n1 ? 1u : link[c - n1].depth; };
   // keys: node c <= |I| has key I[c-1]; node idx > |I| has the first pair of the
   // code that follows its parent in D (Algorithm 2).
   auto set_key = [&](uint32_t at, uint32_t fi) {
@@ -522,8 +526,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   for (size_t j = 0; j < e->D_codes.size(); ++j) dcodes[j] = S.newidx[e->D_codes[j]];
   // Positions of the left multiplication: depth-1 leaves sorted by (column,
   // code), so that the leaves of a column are contiguous; every other code is at
-  // its own index.  The inverted D, the column index and pval follow them.
-  const int64_t n1 = levels >= 1 ? S.cnt[1] : 0;
+  // its own index.  The column index and the column stretches follow them.
   S.lpos.resize((size_t)n_codes);
   S.at_lpos.resize((size_t)n_codes);
   for (int64_t c = 0; c < n_codes; ++c) S.lpos[c] = (uint32_t)c;
@@ -532,24 +535,25 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
   std::sort(S.keys.begin(), S.keys.end());
   for (size_t i = 0; i < S.keys.size(); ++i) S.lpos[(uint32_t)S.keys[i]] = (uint32_t)(n_int1 + (int64_t)i);
   for (int64_t c = 0; c < n_codes; ++c) S.at_lpos[S.lpos[c]] = (uint32_t)c;
-  uint32_t *pval = (uint32_t *)(dst + L.pval) + bt.code_base;
-  for (int64_t p = 0; p < n_codes; ++p) std::memcpy(&pval[p], &node[S.at_lpos[p]].val, 4);
-  // occurrences of each code (D inverted): rows of the entries of D equal to the
-  // code, ascending, grouped by position.  This is the index set of the sum that
-  // defines G(x) in Theorem 2.
-  uint32_t *occ_off = (uint32_t *)(dst + L.occ_off) + bt.code_base + b;
-  uint32_t *occ_row = (uint32_t *)(dst + L.occ_row) + bt.d_base;
-  std::fill(occ_off, occ_off + n_codes + 1, 0u);
-  for (size_t j = 0; j < e->D_codes.size(); ++j) occ_off[S.lpos[dcodes[j]] + 1]++;
-  for (int64_t c = 0; c < n_codes; ++c) occ_off[c + 1] += occ_off[c];
-  S.fill.assign(occ_off, occ_off + n_codes);
+  auto val_bits = [&](int64_t c) {
+    uint32_t v;
+    std::memcpy(&v, &node[c].val, 4);
+    return v;
+  };
+  // D inverted (scratch): the rows of the entries of D equal to the code at each
+  // position, ascending, grouped by position; bit 31 marks the first of each.
+  // This is the index set of the sum that defines G(x) in Theorem 2.
+  std::vector<uint32_t> &poff = S.poff, &prow = S.prow;
+  poff.assign((size_t)n_codes + 1, 0u);
+  prow.assign(e->D_codes.size(), 0u);
+  for (size_t j = 0; j < e->D_codes.size(); ++j) poff[S.lpos[dcodes[j]] + 1]++;
+  for (int64_t c = 0; c < n_codes; ++c) poff[c + 1] += poff[c];
+  S.fill.assign(poff.begin(), poff.begin() + n_codes);
   for (int32_t r = 0; r < e->n_rows; ++r)
     for (int64_t j = e->D_rowptr[r]; j < e->D_rowptr[r + 1]; ++j)
-      occ_row[S.fill[S.lpos[dcodes[j]]]++] = (uint32_t)r;
-  // bit 31 marks the first occurrence of each code, so a scan over occ_row alone
-  // can tell which code an entry belongs to
+      prow[S.fill[S.lpos[dcodes[j]]]++] = (uint32_t)r;
   for (int64_t c = 0; c < n_codes; ++c)
-    if (occ_off[c] < occ_off[c + 1]) occ_row[occ_off[c]] |= 0x80000000u;
+    if (poff[c] < poff[c + 1]) prow[poff[c]] |= 0x80000000u;
   // codes with an H row in the left multiplication (children or depth >= 2),
   // listed by column
   uint32_t *tlist = (uint32_t *)(dst + L.tlist) + bt.tree_base;
@@ -573,7 +577,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       while (i < n1 && (int64_t)node[S.at_lpos[i]].col < j) ++i;
       while (t < n_tree && (int64_t)node[tlist[t]].col < j) ++t;
       c_code[j] = (uint32_t)i;
-      c_occ[j] = occ_off[i] - occ_off[n_int1];
+      c_occ[j] = poff[i] - poff[n_int1];
       c_tree[j] = (uint32_t)t;
     }
     S.keys.clear();
@@ -589,23 +593,36 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     for (int64_t j = 0; j < m; ++j)
       u += (c_code[j + 1] > c_code[j] || c_tree[j + 1] > c_tree[j]) ? 1 : 0;
     bt.n_ucols = u;
-    // the entries of each column in one stretch: leaf occurrences, then tree
-    // codes marked with kTreeEntry
-    // (cval: beside each entry, the key value of its code)
+    // the left multiplication's entries, in three parts: the leaf occurrences by
+    // position (so those of a column are one stretch, from c_occ[j]), the tree
+    // codes by column marked with kTreeEntry (column j's from n_lo + c_tree[j]),
+    // then the tree codes' own occurrences by tree row (plain tuple indexes).
+    // cval beside each: the key value of the entry's code (0 in the third part).
+    // occ_off: the start of each leaf position's occurrences (n_int1 .. n1-1,
+    // then the end), then of each tree row's (and the end).
     uint32_t *ce = (uint32_t *)(dst + L.centry) + bt.d_base + bt.tree_base;
     uint32_t *cv = (uint32_t *)(dst + L.cval) + bt.d_base + bt.tree_base;
+    uint32_t *lo = (uint32_t *)(dst + L.occ_off) + bt.code_base + 2 * b;
+    uint32_t *to = lo + (n1 - n_int1) + 1;
     int64_t o = 0;
-    for (int64_t j = 0; j < m; ++j) {
-      for (uint32_t p = c_code[j]; p < c_code[j + 1]; ++p)
-        for (uint32_t q = occ_off[p]; q < occ_off[p + 1]; ++q) {
-          ce[o] = occ_row[q];
-          cv[o++] = pval[p];
-        }
-      for (uint32_t q = c_tree[j]; q < c_tree[j + 1]; ++q) {
-        ce[o] = tlist[q] | kTreeEntry;
-        std::memcpy(&cv[o++], &node[tlist[q]].val, 4);
+    for (int64_t p = n_int1; p < n1; ++p) {
+      lo[p - n_int1] = (uint32_t)o;
+      for (uint32_t q = poff[p]; q < poff[p + 1]; ++q) {
+        ce[o] = prow[q];
+        cv[o++] = val_bits(S.at_lpos[p]);
       }
     }
+    lo[n1 - n_int1] = (uint32_t)o;
+    for (int64_t t = 0; t < n_tree; ++t) {
+      ce[o] = tlist[t] | kTreeEntry;
+      cv[o++] = val_bits(tlist[t]);
+    }
+    for (int64_t h = 0; h < n_tree; ++h) {
+      const int64_t c = h < n_int1 ? h : h - n_int1 + n1;   // tree row h's code (and position)
+      to[h] = (uint32_t)o;
+      for (uint32_t q = poff[c]; q < poff[c + 1]; ++q) ce[o++] = prow[q] & 0x7FFFFFFFu;
+    }
+    to[n_tree] = (uint32_t)o;
   }
   // children of each tree code (their H rows are added to its H in the left
   // multiplication): code h's children are codes tchild[h] .. tchild[h+1]-1, h
@@ -616,7 +633,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
     auto hrow = [&](uint32_t c) -> int64_t { return c < n_int1 ? c : (int64_t)c - n1 + n_int1; };
     int64_t c = n1;
     for (int64_t h = 0; h <= n_tree; ++h) {
-      while (c < n_codes && hrow(link[c].parent) < h) ++c;
+      while (c < n_codes && hrow(parent_of(c)) < h) ++c;
       tch[h] = (uint32_t)c;
     }
   }
@@ -635,7 +652,7 @@ toc_status write_batch(const toc_enc *e, int64_t b, uint32_t flags, const toc_la
       dt[4 * t + 1] = (uint32_t)es;
       dt[4 * t + 2] = (uint32_t)pairs;
       dt[4 * t + 3] = (uint32_t)row;
-      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += link[dcodes[j]].depth;
+      for (int64_t j = es; j < std::min(nd, es + kDecodeTile); ++j) pairs += depth_of(dcodes[j]);
     }
   }
   bt.n_codes = (int32_t)n_codes;
@@ -727,16 +744,14 @@ toc_status plan_layout(const BatchCounts *bc, int64_t n_batches, int32_t n_cols,
   L.batches = off; off = align256(off + (int64_t)sizeof(toc_batch) * n_batches);
   L.level = off;   off = align256(off + 4 * levels);
   L.key = off;     off = align256(off + (int64_t)sizeof(toc_key) * codes);
-  L.link = off;    off = align256(off + (int64_t)sizeof(toc_link) * codes);
+  L.link = off;    off = align256(off + (int64_t)sizeof(toc_link) * deep);
   L.span = off;    off = align256(off + 4 * spans);
   L.dcodes = off;  off = align256(off + 4 * d);
-  L.occ_off = off; off = align256(off + 4 * (codes + n_batches));
-  L.occ_row = off; off = align256(off + 4 * d);
+  L.occ_off = off; off = align256(off + 4 * (codes + 2 * n_batches));
   L.tlist = off;   off = align256(off + 4 * tree);
   L.dtiles = off;  off = align256(off + 16 * dtiles);
   L.cols = off;    off = align256(off + 16 * n_batches * ((int64_t)std::max(n_cols, 0) + 1));
   L.tchild = off;  off = align256(off + 4 * (tree + n_batches));
-  L.pval = off;    off = align256(off + 4 * codes);
   L.centry = off;  off = align256(off + 4 * (d + tree));
   L.cval = off;    off = align256(off + 4 * (d + tree));
   dev->n_dtiles = dtiles;
@@ -829,6 +844,7 @@ ArrStarts arr_starts(const toc_dev *dev, int64_t b) {
     const toc_batch &t = dev->batches[b];
     a.level = t.lvl_base;
     a.code = t.code_base;
+    a.deep = t.deep_base;
     a.span = t.span_base;
     a.d = t.d_base;
     a.tree = t.tree_base;
@@ -836,6 +852,7 @@ ArrStarts arr_starts(const toc_dev *dev, int64_t b) {
   } else {
     a.level = dev->tot_levels;
     a.code = dev->info.n_stored;
+    a.deep = dev->total_deep;
     a.span = dev->info.n_rows + n;
     a.d = dev->info.n_codes;
     a.tree = dev->total_tree;

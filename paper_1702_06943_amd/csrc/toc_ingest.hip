@@ -447,20 +447,23 @@ __global__ __launch_bounds__(kIgBlock) void image_kernel(IgParams P) {
       if (tid == 0) tch[ntree] = nc;
       __syncthreads();
 
-      // keys and links by place; tuple starts; D renumbered
+      // keys by place, links of the codes of depth >= 2 (by place - n1); tuple
+      // starts; D renumbered
       {
         toc_key *key = (toc_key *)(P.img + P.L.key) + bt.code_base;
-        toc_link *lk = (toc_link *)(P.img + P.L.link) + bt.code_base;
+        toc_link *lk = (toc_link *)(P.img + P.L.link) + bt.deep_base;
         for (uint32_t q = tid; q < nc; q += kIgBlock) {
           const uint32_t c = at[q], d = dep[c];
           toc_key k;
           k.col = cl[c];
           k.val = __uint_as_float(vl[c]);
           key[q] = k;
-          toc_link l;
-          l.parent = d == 1u ? kNone : nx[par[c]];
-          l.depth = d;
-          lk[q] = l;
+          if (q >= n1) {
+            toc_link l;
+            l.parent = nx[par[c]];
+            l.depth = d;
+            lk[q - n1] = l;
+          }
         }
         uint32_t *span = (uint32_t *)(P.img + P.L.span) + bt.span_base;
         for (uint32_t r = tid; r <= n_r; r += kIgBlock) span[r] = st[r];
@@ -480,25 +483,29 @@ __global__ __launch_bounds__(kIgBlock) void image_kernel(IgParams P) {
         for (uint32_t q = tid; q < nc; q += kIgBlock) atl[q] = (q >= ni && q < n1) ? srt[q - ni] : q;
       }
       __syncthreads();
-      uint32_t *pval = (uint32_t *)(P.img + P.L.pval) + bt.code_base;
-      for (uint32_t q = tid; q < nc; q += kIgBlock) pval[q] = vl[at[atl[q]]];
-      // D inverted by position: the tuples of each position's entries, ascending,
-      // bit 31 on the first
-      uint32_t *oo = (uint32_t *)(P.img + P.L.occ_off) + bt.code_base + b;
-      uint32_t *orow = (uint32_t *)(P.img + P.L.occ_row) + bt.d_base;
+      // the left multiplication's entries (centry, cval), first part: the tuples of
+      // each leaf position's entries of D, ascending, bit 31 on the first, the
+      // key value beside each; lo: where each leaf position's start
+      uint32_t *ce = (uint32_t *)(P.img + P.L.centry) + bt.d_base + bt.tree_base;
+      uint32_t *cv = (uint32_t *)(P.img + P.L.cval) + bt.d_base + bt.tree_base;
+      uint32_t *lo = (uint32_t *)(P.img + P.L.occ_off) + bt.code_base + 2 * b;
+      uint32_t *to = lo + (n1 - ni) + 1;
       carry = 0;
-      for (uint32_t q0 = 0; q0 < nc; q0 += kIgBlock) {
+      for (uint32_t q0 = ni; q0 < n1; q0 += kIgBlock) {
         const uint32_t q = q0 + tid;
-        const uint32_t c = q < nc ? at[atl[q]] : 0u, cnt = q < nc ? gz[c] : 0u;
+        const uint32_t c = q < n1 ? at[atl[q]] : 0u, cnt = q < n1 ? gz[c] : 0u;
         const uint32_t v = scan_step(cnt, wsum, carry);
-        if (q < nc) {
-          oo[q] = v;
+        if (q < n1) {
+          lo[q - ni] = v;
           const uint32_t ga = gs[c];
-          for (uint32_t x = 0; x < cnt; ++x)
-            orow[v + x] = tuple_of(st, n_r, occ[ga + x]) | (x == 0 ? 0x80000000u : 0u);
+          for (uint32_t x = 0; x < cnt; ++x) {
+            ce[v + x] = tuple_of(st, n_r, occ[ga + x]) | (x == 0 ? 0x80000000u : 0u);
+            cv[v + x] = vl[c];
+          }
         }
       }
-      if (tid == 0) oo[nc] = carry;
+      const uint32_t n_lo = carry;      // leaf occurrences; the tree codes' entries follow
+      if (tid == 0) lo[n1 - ni] = n_lo;
       // tree codes (depth-1 codes with children, codes of depth >= 2) by (key
       // column, place)
       for (uint32_t t = tid; t < ntree; t += kIgBlock) {
@@ -511,8 +518,29 @@ __global__ __launch_bounds__(kIgBlock) void image_kernel(IgParams P) {
       {
         const uint32_t *srt =
             block_radix_sort(sk0, sv0, sk1, sv1, ntree, cbits, run, wcnt, wsum) ? sv1 : sv0;
-        for (uint32_t t = tid; t < ntree; t += kIgBlock) tl[t] = srt[t];
+        for (uint32_t t = tid; t < ntree; t += kIgBlock) {
+          const uint32_t q = srt[t];
+          tl[t] = q;
+          // second part of the entries: the tree codes by (column, place)
+          ce[n_lo + t] = q | toc::kTreeEntry;
+          cv[n_lo + t] = vl[at[q]];
+        }
       }
+      // third part: the tuples of each tree code's entries of D, ascending, by tree
+      // row; to: where each tree row's start
+      carry = n_lo + ntree;
+      for (uint32_t h0 = 0; h0 < ntree; h0 += kIgBlock) {
+        const uint32_t h = h0 + tid;
+        const uint32_t c = h < ntree ? at[h < ni ? h : n1 + (h - ni)] : 0u;
+        const uint32_t cnt = h < ntree ? gz[c] : 0u;
+        const uint32_t v = scan_step(cnt, wsum, carry);
+        if (h < ntree) {
+          to[h] = v;
+          const uint32_t ga = gs[c];
+          for (uint32_t x = 0; x < cnt; ++x) ce[v + x] = tuple_of(st, n_r, occ[ga + x]);
+        }
+      }
+      if (tid == 0) to[ntree] = carry;
       __syncthreads();
 
       // column index: per key column its leaves, their occurrences and its tree
@@ -557,27 +585,6 @@ __global__ __launch_bounds__(kIgBlock) void image_kernel(IgParams P) {
         const uint32_t *srt =
             block_radix_sort(sk0, sv0, sk1, sv1, m, key_bits(top + 1u), run, wcnt, wsum) ? sv1 : sv0;
         for (uint32_t j = tid; j < m; j += kIgBlock) c_ord[j] = srt[j];
-      }
-      // the entries of each key column in one stretch: its leaves' occurrences (by
-      // position), then its tree codes marked with kTreeEntry; beside each, the key
-      // value of its code
-      {
-        uint32_t *ce = (uint32_t *)(P.img + P.L.centry) + bt.d_base + bt.tree_base;
-        uint32_t *cv = (uint32_t *)(P.img + P.L.cval) + bt.d_base + bt.tree_base;
-        const uint32_t o_ni = oo[ni];
-        for (uint32_t q = ni + tid; q < n1; q += kIgBlock) {
-          const uint32_t c = at[atl[q]], cnt = gz[c], o = oo[q];
-          const uint32_t base = (o - o_ni) + c_tree[cl[c]];
-          for (uint32_t x = 0; x < cnt; ++x) {
-            ce[base + x] = orow[o + x];
-            cv[base + x] = vl[c];
-          }
-        }
-        for (uint32_t t = tid; t < ntree; t += kIgBlock) {
-          const uint32_t q = tl[t], c = at[q], o = c_occ[cl[c] + 1] + t;
-          ce[o] = q | toc::kTreeEntry;
-          cv[o] = vl[c];
-        }
       }
       // decode tiles: per run of kDecodeTile entries of D, the batch, the first
       // entry, the pairs before it in the batch, the first tuple starting at or

@@ -76,7 +76,7 @@ void finish_image(toc_dev *dev);
 // Element index at which batch b's slice of each per-batch array starts (b equal
 // to the batch count: the arrays' ends).
 struct ArrStarts {
-  int64_t level, code, span, d, tree, dtile, cols, b;
+  int64_t level, code, deep, span, d, tree, dtile, cols, b;
 };
 ArrStarts arr_starts(const toc_dev *dev, int64_t b);
 // Computes layout and totals only.

@@ -15,7 +15,7 @@ namespace {
 
 constexpr int kMgBlock = 1024;
 constexpr int kMgLanes = 8;                    // lanes per tuple in the right product
-constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of occ_row
+constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of a leaf occurrence
 constexpr size_t kMgLdsMax = 160 * 1024;
 
 struct MgImg {
@@ -23,7 +23,7 @@ struct MgImg {
   const uint32_t *level;
   const toc_key *key;
   const toc_link *link;
-  const uint32_t *span, *dcodes, *occ_off, *occ_row, *tlist, *cols, *tchild, *pval;
+  const uint32_t *span, *dcodes, *occ_off, *tlist, *cols, *tchild, *centry, *cval;
 };
 
 // d loss / d r of one tuple: squared 1/2 (y - r)^2, logistic log(1 + exp(-y r)),
@@ -48,7 +48,7 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
     const uint32_t *lvl = im.level + bt.lvl_base;
     const toc_key *key = im.key + bt.code_base;
-    const toc_link *link = im.link + bt.code_base;
+    const toc_link *link = im.link + (bt.deep_base - (int64_t)bt.n_lvl1);   // depth >= 2 only
     // right: H[c] = H[parent] + val * h[col], level by level
     for (int d = 1; d <= bt.n_levels; ++d) {
       const uint32_t a = lvl[d - 1], e = lvl[d];
@@ -78,15 +78,29 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     __syncthreads();
     // left, by pulling: H at each left position = the gradients of the tuples
     // holding its code, then children added into parents, deepest first
-    const uint32_t *oo = im.occ_off + bt.code_base + b;
-    const uint32_t *orow = im.occ_row + bt.d_base;
+    // a leaf position p's tuples: entries lo[p - ni] .. of the batch's entry array
+    // (its value beside the first); a tree code's: entries to[tree row] ..
+    const uint32_t *lo = im.occ_off + bt.code_base + 2 * b, *to = lo + (n1 - ni) + 1;
+    const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
+    const uint32_t *cv = im.cval + bt.d_base + bt.tree_base;
+    auto occ = [&](uint32_t p, uint32_t &o0, uint32_t &o1) {
+      const bool leaf = p >= ni && p < n1;
+      const uint32_t hr = p < ni ? p : p - n1 + ni;
+      o0 = leaf ? lo[p - ni] : to[hr];
+      o1 = leaf ? lo[p - ni + 1] : to[hr + 1];
+    };
 #pragma unroll 2
     for (uint32_t p = threadIdx.x; p < nc; p += kMgBlock) {
       float s = 0.0f;
-      const uint32_t o1 = oo[p + 1];
+      uint32_t o0, o1;
+      occ(p, o0, o1);
+      // a leaf's sum times its value (beside its first occurrence) right away: it
+      // has no children to add first
+      const bool lv = p >= ni && p < n1 && o1 > o0;
+      const float v = lv ? __uint_as_float(cv[o0]) : 1.0f;
 #pragma unroll 4
-      for (uint32_t o = oo[p]; o < o1; ++o) s += Gs[orow[o] & ~kMgFirst];
-      H[p] = s;
+      for (uint32_t o = o0; o < o1; ++o) s += Gs[ce[o] & ~kMgFirst];
+      H[p] = lv ? v * s : s;
     }
     __syncthreads();
     const uint32_t *tch = im.tchild + bt.tree_base + b;
@@ -107,17 +121,16 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
     const uint32_t *Loff = cx, *Toff = cx + 2 * (m + 1);
     const uint32_t *tl = im.tlist + bt.tree_base;
-    const uint32_t *pv = im.pval + bt.code_base;
     const float step = lr / (float)nr;
     for (int j = threadIdx.x; j < m; j += kMgBlock) {
       float s = 0.0f;
       const uint32_t l1 = Loff[j + 1], t1 = Toff[j + 1];
 #pragma unroll 4
-      for (uint32_t p = Loff[j]; p < l1; ++p) s = fmaf(__uint_as_float(pv[p]), H[p], s);
+      for (uint32_t p = Loff[j]; p < l1; ++p) s += H[p];      // leaves: val * H already
 #pragma unroll 4
       for (uint32_t t = Toff[j]; t < t1; ++t) {
         const uint32_t c = tl[t];
-        s = fmaf(__uint_as_float(pv[c]), H[c], s);
+        s = fmaf(key[c].val, H[c], s);
       }
       h[j] = fmaf(-step, s, h[j]);
     }
@@ -161,9 +174,9 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   const MgImg im{(const toc_batch *)(base + L.batches), (const uint32_t *)(base + L.level),
                  (const toc_key *)(base + L.key), (const toc_link *)(base + L.link),
                  (const uint32_t *)(base + L.span), (const uint32_t *)(base + L.dcodes),
-                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.occ_row),
-                 (const uint32_t *)(base + L.tlist), (const uint32_t *)(base + L.cols),
-                 (const uint32_t *)(base + L.tchild), (const uint32_t *)(base + L.pval)};
+                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.tlist),
+                 (const uint32_t *)(base + L.cols), (const uint32_t *)(base + L.tchild),
+                 (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
   hipLaunchKernelGGL(mgd_kernel, dim3(1), dim3(kMgBlock), lds, (hipStream_t)stream, im, b0,
                      n_batches, d->info.n_cols, d->max_rows, (int)loss, lr, y, h);
   const hipError_t e = hipGetLastError();

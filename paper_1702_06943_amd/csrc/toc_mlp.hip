@@ -24,7 +24,7 @@ namespace {
 
 constexpr int kNnBlock = 1024;
 constexpr int kNnLanes = 16;                 // lanes per tuple in the forward product
-constexpr uint32_t kNnFirst = 0x80000000u;   // first-occurrence bit of occ_row
+constexpr uint32_t kNnFirst = 0x80000000u;   // first-occurrence bit of a leaf occurrence
 constexpr size_t kNnLdsMax = 160 * 1024;
 constexpr int kColGroups = 8;                // workgroups sharing a slice's key columns
 
@@ -33,7 +33,7 @@ struct NnImg {
   const uint32_t *level;
   const toc_key *key;
   const toc_link *link;
-  const uint32_t *span, *dcodes, *occ_off, *occ_row, *tlist, *cols, *tchild, *pval, *centry;
+  const uint32_t *span, *dcodes, *occ_off, *tlist, *cols, *tchild, *centry, *cval;
 };
 
 __device__ inline float sigm(float x) { return 1.0f / (1.0f + expf(-x)); }
@@ -71,7 +71,7 @@ __global__ __launch_bounds__(kNnBlock) void mlp_fwd1_kernel(NnImg im, int64_t b,
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
   const uint32_t *lvl = im.level + bt.lvl_base;
   const toc_key *key = im.key + bt.code_base;
-  const toc_link *link = im.link + bt.code_base;
+  const toc_link *link = im.link + (bt.deep_base - (int64_t)bt.n_lvl1);   // depth >= 2 only
   auto wrow = [&](uint32_t col) { return *(const float4 *)(W1 + (int64_t)col * h1 + u0); };
   for (int d = 2; d <= bt.n_levels; ++d) {
     const uint32_t a = lvl[d - 1], e = lvl[d];
@@ -287,8 +287,10 @@ __global__ __launch_bounds__(kNnBlock) void mlp_bwd1_kernel(NnImg im, int64_t b,
   const uint32_t n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1, nc = (uint32_t)bt.n_codes;
   const uint32_t n_tree = ni + (nc - n1);
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *oo = im.occ_off + bt.code_base + b;
-  const uint32_t *orow = im.occ_row + bt.d_base;
+  // tree row t's tuples: entries to[t] .. to[t+1]-1 of the batch's entry array
+  const uint32_t *to = im.occ_off + bt.code_base + 2 * b + (n1 - ni) + 1;
+  const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
+  const uint32_t *cv = im.cval + bt.d_base + bt.tree_base;
   const int lane = threadIdx.x % kNnLanes, grp = threadIdx.x / kNnLanes;
   constexpr int kGroups = kNnBlock / kNnLanes;
   auto grow = [&](uint32_t row) { return *(const float4 *)(dz1 + (int64_t)row * h1 + u0); };
@@ -306,9 +308,8 @@ __global__ __launch_bounds__(kNnBlock) void mlp_bwd1_kernel(NnImg im, int64_t b,
     const uint32_t t = t0 + grp;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     if (t < n_tree) {
-      const uint32_t c = t < ni ? t : t - ni + n1;
-      const uint32_t o1 = oo[c + 1];
-      for (uint32_t o = oo[c] + lane; o < o1; o += kNnLanes) s = add4(s, grow(orow[o] & ~kNnFirst));
+      const uint32_t o1 = to[t + 1];
+      for (uint32_t o = to[t] + lane; o < o1; o += kNnLanes) s = add4(s, grow(ce[o]));
     }
     s = group_sum(s);
     if (t < n_tree && lane == 0) Ht[t] = s;
@@ -327,29 +328,26 @@ __global__ __launch_bounds__(kNnBlock) void mlp_bwd1_kernel(NnImg im, int64_t b,
     rows_barrier<kGlobal>();
   }
   const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
-  const uint32_t *Loff = cx, *Ost = cx + (m + 1), *Toff = cx + 2 * (m + 1), *Ord = cx + 3 * (m + 1);
-  const uint32_t *pv = im.pval + bt.code_base;
-  const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
-  const int gshift = (threadIdx.x % 64) / kNnLanes * kNnLanes;   // the group's bits in a ballot
+  const uint32_t *Ost = cx + (m + 1), *Toff = cx + 2 * (m + 1), *Ord = cx + 3 * (m + 1);
+  const uint32_t n_lo = Ost[m];   // leaf occurrences; the tree codes' entries follow
   for (int k = blockIdx.y * kGroups + grp; k < m; k += kGroups * gridDim.y) {
     const uint32_t j = Ord[k];
-    const uint32_t st = Ost[j] + Toff[j], nl = Ost[j + 1] - Ost[j], nt = Toff[j + 1] - Toff[j];
+    const uint32_t lst = Ost[j], tst = n_lo + Toff[j];
+    const uint32_t nl = Ost[j + 1] - Ost[j], nt = Toff[j + 1] - Toff[j];
     if (nl + nt == 0) continue;                // no entry: the column's gradient is 0
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    uint32_t pos = Loff[j];                    // leaf position of the next first occurrence
-    for (uint32_t q0 = 0; q0 < nl + nt; q0 += kNnLanes) {
-      const uint32_t q = q0 + lane;
-      const uint32_t w = q < nl + nt ? ce[st + q] : 0u;
-      const bool leaf = q < nl, first = leaf && (w & kNnFirst);
-      const uint32_t gm = (uint32_t)(__ballot(first) >> gshift) & 0xFFFFu;
-      if (leaf) {
-        const uint32_t p = pos + __popc(gm & ((2u << lane) - 1u)) - 1u;
-        s = fma4(__uint_as_float(pv[p]), grow(w & ~kNnFirst), s);
-      } else if (q < nl + nt) {
+    // the column's leaf occurrences (val * dZ1 row of the tuple), then its tree
+    // codes (val * tree row), the multiplier beside each entry
+    for (uint32_t q = lane; q < nl + nt; q += kNnLanes) {
+      const uint32_t at = q < nl ? lst + q : tst + (q - nl);
+      const uint32_t w = ce[at];
+      const float v = __uint_as_float(cv[at]);
+      if (q < nl) {
+        s = fma4(v, grow(w & ~kNnFirst), s);
+      } else {
         const uint32_t c = w & ~toc::kTreeEntry;
-        s = fma4(__uint_as_float(pv[c]), Ht[c < ni ? c : c - n1 + ni], s);
+        s = fma4(v, Ht[c < ni ? c : c - n1 + ni], s);
       }
-      pos += __popc(gm);
     }
     s = group_sum(s);
     if (lane == 0) {
@@ -492,10 +490,9 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   const NnImg im{(const toc_batch *)(base + L.batches), (const uint32_t *)(base + L.level),
                  (const toc_key *)(base + L.key), (const toc_link *)(base + L.link),
                  (const uint32_t *)(base + L.span), (const uint32_t *)(base + L.dcodes),
-                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.occ_row),
-                 (const uint32_t *)(base + L.tlist), (const uint32_t *)(base + L.cols),
-                 (const uint32_t *)(base + L.tchild), (const uint32_t *)(base + L.pval),
-                 (const uint32_t *)(base + L.centry)};
+                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.tlist),
+                 (const uint32_t *)(base + L.cols), (const uint32_t *)(base + L.tchild),
+                 (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
   const int64_t nr = d->max_rows;
   float *act1 = (float *)ws;
   float *dz1 = act1 + align4(nr * h1);

@@ -28,17 +28,15 @@ def read_image(dev, buf):
         bt=bt, info=info,
         level=arr("level", np.uint32, n_levels),
         key=arr("key", T.KEY_DTYPE, n_codes),
-        link=arr("link", T.LINK_DTYPE, n_codes),
+        link=arr("link", T.LINK_DTYPE, info["n_deep"]),
         span=arr("span", np.uint32, int((bt["n_rows"] + 1).sum()) if nb else 0),
         dcodes=arr("dcodes", np.uint32, info["n_codes"]),
-        occ_off=arr("occ_off", np.uint32, n_codes + nb),
-        occ_row=arr("occ_row", np.uint32, info["n_codes"]),
+        occ_off=arr("occ_off", np.uint32, n_codes + 2 * nb),
         tlist=arr("tlist", np.uint32,
                   int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0),
         cols=arr("cols", np.uint32, nb * 4 * (info["n_cols"] + 1)),
         tchild=arr("tchild", np.uint32,
                    int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"] + 1).sum()) if nb else 0),
-        pval=arr("pval", np.float32, n_codes),
         centry=arr("centry", np.uint32, info["n_codes"] + (
             int((bt["n_int1"] + bt["n_codes"] - bt["n_lvl1"]).sum()) if nb else 0)),
         cval=arr("cval", np.float32, info["n_codes"] + (
@@ -46,8 +44,6 @@ def read_image(dev, buf):
     )
     for f in ("col", "val"):
         img[f] = img["key"][f]
-    for f in ("parent", "depth"):
-        img[f] = img["link"][f]
     return img
 
 
@@ -55,21 +51,26 @@ def batch_view(img, b):
     t = img["bt"][b]
     m = int(img["info"]["n_cols"])
     cb, nc = int(t["code_base"]), int(t["n_codes"])
+    # links are stored for the codes of depth >= 2 only; a depth-1 code has no
+    # parent and depth 1
+    n1, db = int(t["n_lvl1"]), int(t["deep_base"])
+    parent = np.full(nc, 0xFFFFFFFF, np.uint32)
+    depth = np.ones(nc, np.uint32)
+    parent[n1:] = img["link"]["parent"][db:db + nc - n1]
+    depth[n1:] = img["link"]["depth"][db:db + nc - n1]
     return dict(
         t=t,
         level=img["level"][int(t["lvl_base"]):int(t["lvl_base"]) + int(t["n_levels"]) + 1],
-        parent=img["parent"][cb:cb + nc], col=img["col"][cb:cb + nc],
-        val=img["val"][cb:cb + nc], depth=img["depth"][cb:cb + nc],
+        parent=parent, col=img["col"][cb:cb + nc],
+        val=img["val"][cb:cb + nc], depth=depth,
         span=img["span"][int(t["span_base"]):int(t["span_base"]) + int(t["n_rows"]) + 1],
         dc=img["dcodes"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
-        occ_off=img["occ_off"][cb + b:cb + b + nc + 1],
-        occ_row=img["occ_row"][int(t["d_base"]):int(t["d_base"]) + int(t["n_d"])],
+        occ_off=img["occ_off"][cb + 2 * b:cb + 2 * b + nc + 2],
         tlist=img["tlist"][int(t["tree_base"]):int(t["tree_base"]) + int(t["n_int1"]) + nc
                            - int(t["n_lvl1"])],
         cols=img["cols"][b * 4 * (m + 1):(b + 1) * 4 * (m + 1)].reshape(4, m + 1),
         tchild=img["tchild"][int(t["tree_base"]) + b:int(t["tree_base"]) + b + int(t["n_int1"]) + nc
                              - int(t["n_lvl1"]) + 1],
-        pval=img["pval"][cb:cb + nc],
         centry=img["centry"][int(t["d_base"]) + int(t["tree_base"]):
                              int(t["d_base"]) + int(t["tree_base"]) + int(t["n_d"]) + int(t["n_int1"])
                              + nc - int(t["n_lvl1"])],
@@ -119,24 +120,41 @@ def check_invariants(v):
     # children; every other code at its own index
     at = list(range(ni)) + sorted(range(ni, n1), key=lambda c: (int(v["col"][c]), c)) \
         + list(range(n1, nc))
-    assert np.array_equal(v["pval"].view(np.uint32), v["val"].view(np.uint32)[at])
-    # inverted D: the rows listed at each position are exactly the rows using its
-    # code
-    oo, orow = v["occ_off"], v["occ_row"]
-    assert oo[0] == 0 and oo[-1] == len(v["dc"]) and np.all(np.diff(oo.astype(np.int64)) >= 0)
+    # the tuples holding each position's code (the index set of the sum that
+    # defines G(x) in Theorem 2), ascending
     row_of = np.repeat(np.arange(len(v["span"]) - 1), np.diff(v["span"].astype(np.int64)))
-    first = (orow >> 31).astype(bool)
-    assert np.array_equal(np.flatnonzero(first), oo[:-1][np.diff(oo.astype(np.int64)) > 0])
-    orow = orow & 0x7FFFFFFF
-    for p in range(nc):
-        got = orow[oo[p]:oo[p + 1]]
-        assert np.all(np.diff(got.astype(np.int64)) >= 0)
-        assert np.array_equal(got, row_of[v["dc"] == at[p]])
+    occ = [row_of[v["dc"] == at[p]] for p in range(nc)]
+    bits = v["val"].view(np.uint32)
     # tree list: codes with children or depth >= 2, sorted by column
     tree = [c for c in range(nc) if c < ni or c >= n1]
     tl = v["tlist"]
     assert sorted(tl.tolist()) == tree
     assert np.all(np.diff(v["col"][tl].astype(np.int64)) >= 0)
+    # the entries of the left multiplication, in three parts, with the value of
+    # the entry's code beside each (0 in the third part)
+    ce, cvb = v["centry"], v["cval"].view(np.uint32)
+    oo = v["occ_off"]
+    lo, to = oo[:n1 - ni + 1], oo[n1 - ni + 1:]
+    assert len(to) == len(tree) + 1
+    o = 0
+    for p in range(ni, n1):           # 1: leaf occurrences by position, bit 31 on the first
+        k = len(occ[p])
+        assert lo[p - ni] == o
+        assert np.array_equal(ce[o:o + k] & 0x7FFFFFFF, occ[p])
+        assert k == 0 or (ce[o] >> 31 == 1 and np.all(ce[o + 1:o + k] >> 31 == 0))
+        assert np.all(cvb[o:o + k] == bits[at[p]])
+        o += k
+    assert lo[n1 - ni] == o
+    n_lo = o
+    assert np.array_equal(ce[o:o + len(tl)], tl | np.uint32(0x40000000))   # 2: tree codes
+    assert np.array_equal(cvb[o:o + len(tl)], bits[tl])
+    o += len(tl)
+    for h, c in enumerate(tree):      # 3: the tree codes' tuples, by tree row
+        k = len(occ[c])
+        assert to[h] == o
+        assert np.array_equal(ce[o:o + k], occ[c]) and not cvb[o:o + k].any()
+        o += k
+    assert to[len(tree)] == o == len(v["dc"]) + len(tree) == len(ce)
     # column index: first leaf position, leaf occurrences before it and first
     # tree-list entry of each column j; columns by entry count, most first (ties
     # by column)
@@ -147,35 +165,18 @@ def check_invariants(v):
     for j in range(m + 1):
         lc = ni + int(np.sum(leaf_cols < j))
         assert cx[0, j] == lc
-        assert cx[1, j] == oo[lc] - oo[ni]
+        assert cx[1, j] == lo[lc - ni]
         assert cx[2, j] == int(np.sum(tree_cols < j))
+    assert cx[1, m] == n_lo
     cnt = [int(cx[1, j + 1] - cx[1, j] + cx[2, j + 1] - cx[2, j]) for j in range(m)]
     want = sorted(range(m), key=lambda j: (-cnt[j], j))
     assert cx[3, :m].tolist() == want
-    # leaf occurrences of column j: those of its leaf codes; tree codes of column j
+    # leaf positions of column j are contiguous, and so its leaf occurrences
     pos = {c: p for p, c in enumerate(at)}
     for j in range(m):
         ps = [pos[c] for c in range(ni, n1) if v["col"][c] == j]
         assert ps == list(range(int(cx[0, j]), int(cx[0, j + 1])))
-        assert sum(int(oo[p + 1] - oo[p]) for p in ps) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
-    # column entries: per column its leaf occurrence words, then its tree codes
-    # with bit 30 set, starting after the entries of the columns before it
-    ce = v["centry"]
-    orow_raw = v["occ_row"]
-    for j in range(m):
-        st = int(cx[1, j] + cx[2, j])
-        nlj, ntj = int(cx[1, j + 1] - cx[1, j]), int(cx[2, j + 1] - cx[2, j])
-        lo = int(oo[ni]) + int(cx[1, j])
-        assert np.array_equal(ce[st:st + nlj], orow_raw[lo:lo + nlj])
-        assert np.array_equal(ce[st + nlj:st + nlj + ntj],
-                              tl[int(cx[2, j]):int(cx[2, j + 1])] | np.uint32(0x40000000))
-        # the value beside each entry: its leaf's value (leaves of the column in
-        # position order, each for its occurrences), then each tree code's value
-        want = [v["val"][at[p]] for p in range(int(cx[0, j]), int(cx[0, j + 1]))
-                for _ in range(int(oo[p + 1] - oo[p]))]
-        want += [v["val"][c] for c in tl[int(cx[2, j]):int(cx[2, j + 1])]]
-        assert np.array_equal(v["cval"][st:st + nlj + ntj].view(np.uint32),
-                              np.asarray(want, np.float32).view(np.uint32))
+        assert sum(len(occ[p]) for p in ps) == cnt[j] - int(cx[2, j + 1] - cx[2, j])
     # children ranges: tree code h's children are tchild[h] .. tchild[h+1]-1
     hrow = lambda c: c if c < ni else c - n1 + ni
     tch = v["tchild"]
