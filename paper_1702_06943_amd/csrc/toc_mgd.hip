@@ -3,9 +3,12 @@
 // (Theorem 1, Algorithm 4), the loss gradient g_i at r_i, the left product g^T.A
 // (Theorem 2, Algorithm 5) and the update of h, all in one workgroup with H in
 // LDS.  The batches are consecutive steps of one launch: each step reads the
-// model the previous one wrote.
+// model the previous one wrote.  A step's reads of the image do not depend on the
+// model, so helper workgroups on the stepping workgroup's XCD read the next
+// batches' arrays ahead of it, and its loads find them in that XCD's L2.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 
@@ -17,6 +20,17 @@ constexpr int kMgBlock = 1024;
 constexpr int kMgLanes = 8;                    // lanes per tuple in the right product
 constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of a leaf occurrence
 constexpr size_t kMgLdsMax = 160 * 1024;
+constexpr int kMgXcds = 8;                     // workgroups are dealt to the XCDs in turn
+constexpr int kMgHelpers = 1;                  // workgroups reading ahead of the steps (more
+                                               // measured slower: the XCD's L2 overflows)
+constexpr int64_t kMgAheadMax = (int64_t)1280 << 10;   // larger batches are not read ahead
+constexpr uint32_t kMgSpinMax = 1u << 20;      // a helper's wait for the steps is bounded
+
+// The step the stepping workgroup of the latest launch works on: the launch's tag
+// in the upper half, the batch (from b0) in the lower.  Only the helpers read it,
+// to stay at most kMgHelpers batches ahead; a stale or foreign value only moves
+// their reads in time.
+__device__ uint64_t mgd_progress;
 
 struct MgImg {
   const toc_batch *batches;
@@ -34,14 +48,74 @@ __device__ inline float dloss(int loss, float r, float y) {
   return y * r < 1.0f ? -y : 0.0f;
 }
 
+// A helper: reads the batches b0 + role - 1 + i * kMgHelpers of the launch, each
+// once the steps are at most kMgHelpers batches behind it, touching one word of
+// every 128-byte line of the arrays the step reads.
+__device__ void mgd_read_ahead(const MgImg &im, int64_t b0, int64_t nb, int32_t m,
+                               const float *y, int role, uint32_t tag) {
+  __shared__ int s_go;
+  uint32_t acc = 0;
+  for (int64_t rt = role - 1; rt < nb; rt += kMgHelpers) {
+    if (threadIdx.x == 0) {
+      uint32_t spins = 0;
+      for (; spins < kMgSpinMax; ++spins) {
+        const uint64_t v = __hip_atomic_load(&mgd_progress, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((uint32_t)(v >> 32) == tag && (int64_t)(uint32_t)v + kMgHelpers >= rt) break;
+        __builtin_amdgcn_s_sleep(8);
+      }
+      s_go = spins < kMgSpinMax;
+    }
+    __syncthreads();
+    const bool go = s_go;
+    __syncthreads();
+    if (!go) return;                // the steps went quiet: leave them alone
+    const int64_t b = b0 + rt;
+    const toc_batch bt = im.batches[b];
+    const int64_t nc = bt.n_codes, n1 = bt.n_lvl1, nd = bt.n_d, nr = bt.n_rows;
+    const int64_t nt = bt.n_int1 + nc - n1;
+    struct Range { const void *p; int64_t bytes; };
+    const Range r[] = {
+        {im.dcodes + bt.d_base, 4 * nd},
+        {im.key + bt.code_base, 8 * nc},
+        {im.link + bt.deep_base, 8 * (nc - n1)},
+        {im.span + bt.span_base, 4 * (nr + 1)},
+        {im.occ_off + bt.code_base + 2 * b, 4 * (nc + 2)},
+        {im.centry + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+        {im.cval + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+        {im.cols + b * 4 * (int64_t)(m + 1), 4 * 3 * (int64_t)(m + 1)},
+        {im.tlist + bt.tree_base, 4 * nt},
+        {im.tchild + bt.tree_base + b, 4 * (nt + 1)},
+        {im.level + bt.lvl_base, 4 * ((int64_t)bt.n_levels + 1)},
+        {y + bt.row_base, 4 * nr},
+    };
+    int64_t total = 0;
+    for (const Range &x : r) total += x.bytes;
+    if (total > kMgAheadMax) continue;
+    for (const Range &x : r)
+      for (int64_t o = (int64_t)threadIdx.x * 128; o < x.bytes; o += (int64_t)kMgBlock * 128)
+        acc += *(const uint32_t *)((const char *)x.p + o);
+  }
+  asm volatile("" : : "v"(acc));    // the loads are the point: keep them
+}
+
 __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int64_t nb, int32_t m,
                                                        int32_t max_rows, int loss, float lr,
                                                        const float *__restrict__ y,
-                                                       float *__restrict__ h) {
+                                                       float *__restrict__ h, uint32_t tag) {
+  // workgroup 0 steps; workgroups kMgXcds, 2 kMgXcds, ... (on its XCD) read ahead;
+  // the others have nothing to do
+  if (blockIdx.x % kMgXcds != 0) return;
+  if (blockIdx.x != 0) {
+    mgd_read_ahead(im, b0, nb, m, y, (int)(blockIdx.x / kMgXcds), tag);
+    return;
+  }
   extern __shared__ float sm[];
   float *Gs = sm;                  // per tuple: d loss / d r
   float *H = sm + max_rows;        // per code (right), then per left position (left)
   for (int64_t b = b0; b < b0 + nb; ++b) {
+    if (threadIdx.x == 0)
+      __hip_atomic_store(&mgd_progress, ((uint64_t)tag << 32) | (uint32_t)(b - b0), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     const toc_batch bt = im.batches[b];
     const int nr = bt.n_rows;
     if (nr == 0) continue;          // no tuple: the step leaves h unchanged
@@ -177,8 +251,11 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                  (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.tlist),
                  (const uint32_t *)(base + L.cols), (const uint32_t *)(base + L.tchild),
                  (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
-  hipLaunchKernelGGL(mgd_kernel, dim3(1), dim3(kMgBlock), lds, (hipStream_t)stream, im, b0,
-                     n_batches, d->info.n_cols, d->max_rows, (int)loss, lr, y, h);
+  static std::atomic<uint32_t> launches{0};
+  const uint32_t tag = launches.fetch_add(1) + 1;
+  hipLaunchKernelGGL(mgd_kernel, dim3(kMgXcds * (1 + kMgHelpers)), dim3(kMgBlock), lds,
+                     (hipStream_t)stream, im, b0, n_batches, d->info.n_cols, d->max_rows, (int)loss,
+                     lr, y, h, tag);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "mgd_kernel: %s", hipGetErrorString(e));
   return TOC_OK;
