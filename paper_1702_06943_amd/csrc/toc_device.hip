@@ -237,7 +237,9 @@ constexpr uint32_t kFirstOccK1 = 0x80000000u;
 constexpr int kK1RightBlock = 256;
 constexpr int kK1Codes = 4;      // codes per thread and pass
 constexpr int kK1Occ = 4;        // occurrences per code loaded together
-constexpr int kK1Cols = 8;       // output columns per thread and pass
+// output columns per thread and pass: 4 or 8 (template argument NCOL of
+// left_k1_kernel: 8 only for wide matrices, as 4 keeps the kernel at 50 VGPRs and
+// 8 waves per SIMD, 8 needs 82)
 constexpr int kK1Tree = 4;       // tree-list entries per column loaded together
 
 // Where a batch's left positions find their occurrences: a leaf position p
@@ -273,6 +275,7 @@ __device__ inline OccIndex occ_index(const Img &im, const uint32_t *occ_off_all,
   return x;
 }
 
+template <int NCOL>
 __global__ __launch_bounds__(kBlock) void left_k1_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ tlist_all,
     const uint32_t *__restrict__ cols_all, const uint32_t *__restrict__ tchild_all, int64_t b0,
@@ -358,13 +361,13 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
   }
   __syncthreads();
   // each key column once: its depth-1 leaves (a code range), then its tree
-  // codes (a tree-list range); a thread has kK1Cols columns in flight and
+  // codes (a tree-list range); a thread has NCOL columns in flight and
   // loads the first kK1Tree tree-list entries of each before summing
   const uint32_t *Loff = cx, *Toff = cx + 2 * (m + 1);
-  for (int j0 = 0; j0 < m; j0 += kBlock * kK1Cols) {
-    uint32_t l0[kK1Cols], l1[kK1Cols], t0[kK1Cols], t1[kK1Cols];
+  for (int j0 = 0; j0 < m; j0 += kBlock * NCOL) {
+    uint32_t l0[NCOL], l1[NCOL], t0[NCOL], t1[NCOL];
 #pragma unroll
-    for (int u = 0; u < kK1Cols; ++u) {
+    for (int u = 0; u < NCOL; ++u) {
       const int j = j0 + u * kBlock + threadIdx.x;
       const bool in = j < m;
       l0[u] = in ? Loff[j] : 0u;
@@ -372,13 +375,13 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
       t0[u] = in ? Toff[j] : 0u;
       t1[u] = in ? Toff[j + 1] : 0u;
     }
-    uint32_t tc[kK1Cols][kK1Tree];
+    uint32_t tc[NCOL][kK1Tree];
 #pragma unroll
-    for (int u = 0; u < kK1Cols; ++u)
+    for (int u = 0; u < NCOL; ++u)
 #pragma unroll
       for (int v = 0; v < kK1Tree; ++v) tc[u][v] = t0[u] + v < t1[u] ? tl[t0[u] + v] : 0xFFFFFFFFu;
 #pragma unroll
-    for (int u = 0; u < kK1Cols; ++u) {
+    for (int u = 0; u < NCOL; ++u) {
       const int j = j0 + u * kBlock + threadIdx.x;
       float sum = blocked_sum(l0[u], l1[u], 1u, [&](uint32_t c) { return c; },
                               [&](uint32_t c) { return H[c]; });
@@ -3003,7 +3006,8 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
   const Img im = image_of(d);
   if (k == 1 && k1_fits(d, TOC_OP_LEFT)) {
     const size_t lds = k1_lds(d, TOC_OP_LEFT);
-    if ((st = allow_lds(left_k1_kernel, lds))) return st;
+    const bool wide_m = m > 4 * kBlock;      // a pass of 4 columns per thread covers 4 kBlock
+    if ((st = allow_lds(wide_m ? left_k1_kernel<8> : left_k1_kernel<4>, lds))) return st;
     const uint8_t *bb = (const uint8_t *)d->buf;
     const uint32_t *occ_off = (const uint32_t *)(bb + d->layout.occ_off);
     const uint32_t *tlist = (const uint32_t *)(bb + d->layout.tlist);
@@ -3011,9 +3015,12 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
     const uint32_t *tchild = (const uint32_t *)(bb + d->layout.tchild);
     for (int64_t b0 = 0; b0 < nb; b0 += (1 << 30)) {
       const unsigned g = (unsigned)std::min<int64_t>(nb - b0, 1 << 30);
-      hipLaunchKernelGGL(left_k1_kernel, dim3(g), dim3(kBlock), lds, s, im, occ_off,
-                         tlist, cols, tchild, b0, m, d->max_rows, d->max_codes, G, ldg, out, ldo,
-                         accumulate);
+      if (wide_m)
+        hipLaunchKernelGGL(left_k1_kernel<8>, dim3(g), dim3(kBlock), lds, s, im, occ_off, tlist, cols,
+                           tchild, b0, m, d->max_rows, d->max_codes, G, ldg, out, ldo, accumulate);
+      else
+        hipLaunchKernelGGL(left_k1_kernel<4>, dim3(g), dim3(kBlock), lds, s, im, occ_off, tlist, cols,
+                           tchild, b0, m, d->max_rows, d->max_codes, G, ldg, out, ldo, accumulate);
       if ((st = launch_status("left_k1_kernel"))) return st;
     }
     return TOC_OK;
