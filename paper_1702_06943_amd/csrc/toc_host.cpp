@@ -822,7 +822,11 @@ toc_status write_batches(const toc_enc *const *encs, int64_t b0, int64_t b1, uin
 
 void finish_image(toc_dev *dev) {
   dev->max_ucols = 0;
-  for (const toc_batch &bt : dev->batches) dev->max_ucols = std::max(dev->max_ucols, bt.n_ucols);
+  dev->max_keylinks = 0;
+  for (const toc_batch &bt : dev->batches) {
+    dev->max_ucols = std::max(dev->max_ucols, bt.n_ucols);
+    dev->max_keylinks = std::max<int64_t>(dev->max_keylinks, 2 * (int64_t)bt.n_codes - bt.n_lvl1);
+  }
 }
 
 toc_status build_image(const toc_enc *const *encs, int64_t n_batches, uint32_t flags,

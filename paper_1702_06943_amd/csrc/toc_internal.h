@@ -35,6 +35,7 @@ struct toc_dev {
   std::vector<toc_batch> batches;  // host copy of the batch table
   int32_t max_rows = 0, max_codes = 0, max_levels = 0;
   int32_t max_ucols = 0;           // most distinct key columns of a batch (after build)
+  int64_t max_keylinks = 0;        // most keys plus deep links of a batch (after build)
   int64_t max_deep = 0, max_tree = 0, max_d = 0;
   // most deep codes of two batches b, b + 8 with b / 8 even (the batch pairs of
   // the right product's tiled kernel)
