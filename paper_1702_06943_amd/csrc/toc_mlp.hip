@@ -270,15 +270,51 @@ __global__ __launch_bounds__(256) void mlp_grad_kernel(
 // children are added into parents deepest first; each key column's gradient sums
 // val * (dZ1 row) over its leaf occurrences and val * (tree row) over its tree
 // codes.  16-lane groups take one tree code, then one column, at a time (columns
-// with the most entries first, dealt round-robin to the gridDim.y workgroups of
+// with the most entries first, dealt round-robin to the kColGroups workgroups of
 // the slice), so a code or column with many occurrences is summed by 16 lanes;
 // sums are reduced in a fixed order.
+// Reads the arrays of batch b that the next step's kernels read (one word of every
+// 128-byte line), so that they find them in L2: the step's kernels gather from
+// them with little else to overlap.  One workgroup per XCD runs it, each reading
+// the whole batch into its XCD's L2.
+__device__ void nn_read_ahead(const NnImg &im, int64_t b, int32_t m, const int32_t *labels) {
+  const toc_batch bt = im.batches[b];
+  const int64_t nc = bt.n_codes, n1 = bt.n_lvl1, nd = bt.n_d, nr = bt.n_rows;
+  const int64_t nt = bt.n_int1 + nc - n1;
+  struct Range { const void *p; int64_t bytes; };
+  const Range r[] = {
+      {im.dcodes + bt.d_base, 4 * nd},
+      {im.key + bt.code_base, 8 * nc},
+      {im.link + bt.deep_base, 8 * (nc - n1)},
+      {im.span + bt.span_base, 4 * (nr + 1)},
+      {im.occ_off + bt.code_base + 2 * b, 4 * (nc + 2)},
+      {im.centry + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+      {im.cval + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+      {im.cols + b * 4 * (int64_t)(m + 1), 4 * 4 * (int64_t)(m + 1)},
+      {im.tchild + bt.tree_base + b, 4 * (nt + 1)},
+      {im.level + bt.lvl_base, 4 * ((int64_t)bt.n_levels + 1)},
+      {labels + bt.row_base, 4 * nr},
+  };
+  uint32_t acc = 0;
+  for (const Range &x : r)
+    for (int64_t o = (int64_t)threadIdx.x * 128; o < x.bytes; o += (int64_t)kNnBlock * 128)
+      acc += *(const uint32_t *)((const char *)x.p + o);
+  asm volatile("" : : "v"(acc));    // the loads are the point: keep them
+}
+
 template <bool kGlobal>
 __global__ __launch_bounds__(kNnBlock) void mlp_bwd1_kernel(NnImg im, int64_t b, int32_t m,
                                                             const float *__restrict__ dz1, int h1,
                                                             float lr, float *__restrict__ W1,
                                                             float *__restrict__ b1, float4 *rows_g,
-                                                            int64_t rows_stride) {
+                                                            int64_t rows_stride, int64_t next,
+                                                            const int32_t *__restrict__ labels) {
+  // the grid's last row: the first 8 workgroups (one per XCD) read the next
+  // step's batch ahead, the others have nothing to do
+  if (blockIdx.y == kColGroups) {
+    if (next >= 0 && blockIdx.x < 8) nn_read_ahead(im, next, m, labels);
+    return;
+  }
   extern __shared__ float4 rows_l[];
   // tree code c at Ht[c < ni ? c : c - n1 + ni]; each workgroup builds its own copy
   float4 *Ht = kGlobal ? rows_g + (blockIdx.y * gridDim.x + blockIdx.x) * rows_stride : rows_l;
@@ -330,7 +366,7 @@ __global__ __launch_bounds__(kNnBlock) void mlp_bwd1_kernel(NnImg im, int64_t b,
   const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
   const uint32_t *Ost = cx + (m + 1), *Toff = cx + 2 * (m + 1), *Ord = cx + 3 * (m + 1);
   const uint32_t n_lo = Ost[m];   // leaf occurrences; the tree codes' entries follow
-  for (int k = blockIdx.y * kGroups + grp; k < m; k += kGroups * gridDim.y) {
+  for (int k = blockIdx.y * kGroups + grp; k < m; k += kGroups * kColGroups) {
     const uint32_t j = Ord[k];
     const uint32_t lst = Ost[j], tst = n_lo + Toff[j];
     const uint32_t nl = Ost[j + 1] - Ost[j], nt = Toff[j + 1] - Toff[j];
@@ -525,12 +561,17 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                          W2, b2, W3, b3, labels, H2g, dZ2g, dZ3g, dz1);
     hipLaunchKernelGGL(mlp_grad_kernel, dim3((unsigned)(n_w2 + n_w3)), dim3(256), lds_g, s, bt.n_rows, n_w2,
                        act1, h1, h2, n_out, H2g, dZ2g, dZ3g, lr, W2, b2, W3, b3);
+    // the next step's batch with rows (its arrays are read ahead by the last
+    // kernel of this step)
+    int64_t next = b + 1;
+    while (next < b0 + n_batches && d->batches[next].n_rows == 0) ++next;
+    if (next >= b0 + n_batches) next = -1;
     if (rw.tree_global)
-      hipLaunchKernelGGL(mlp_bwd1_kernel<true>, dim3(slices, kColGroups), dim3(kNnBlock), 0, s, im,
-                         b, m, dz1, h1, lr, W1, b1, tree_rows, rw.max_tree);
+      hipLaunchKernelGGL(mlp_bwd1_kernel<true>, dim3(slices, kColGroups + 1), dim3(kNnBlock), 0, s, im,
+                         b, m, dz1, h1, lr, W1, b1, tree_rows, rw.max_tree, next, labels);
     else
-      hipLaunchKernelGGL(mlp_bwd1_kernel<false>, dim3(slices, kColGroups), dim3(kNnBlock), lds_b, s,
-                         im, b, m, dz1, h1, lr, W1, b1, nullptr, 0);
+      hipLaunchKernelGGL(mlp_bwd1_kernel<false>, dim3(slices, kColGroups + 1), dim3(kNnBlock), lds_b, s,
+                         im, b, m, dz1, h1, lr, W1, b1, nullptr, 0, next, labels);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(TOC_EDEVICE, "mlp step kernels: %s", hipGetErrorString(e));
   }
