@@ -162,10 +162,13 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *             (no parent, depth 1)
  *   span    : uint32 per batch n_rows+1 offsets into the batch's D (span_base)
  *   dcodes  : uint32 local code of each entry of D (d_base)
- *   occ_off : uint32 per batch n_tree+1 entries (at tree_base + b): tree code h's
- *             occurrences (the tuples holding its code: D inverted, the index set
- *             of the sum that defines G(x) in Theorem 2) are centry entries
- *             occ_off[h] .. occ_off[h+1]-1 of the batch (h as in tchild)
+ *   occ_off : uint32 per batch n_codes+2 entries (at code_base + 2 b): first,
+ *             for each leaf position p = n_int1 .. n_lvl1 (the last one the end),
+ *             where position p's leaf occurrences start in the batch's centry;
+ *             then, for each tree row h = 0 .. n_tree (h as in tchild, the last
+ *             the end), where tree code h's occurrences start.  A code's
+ *             occurrences are the tuples holding it: D inverted, the index set of
+ *             the sum that defines G(x) in Theorem 2
  *   tlist   : uint32 per batch the codes with children or of depth >= 2, sorted
  *             by key column (tree_base)
  *   dtiles  : uint32 x 4 per run of 1024 entries of D (at least one per batch):
@@ -173,25 +176,25 @@ toc_status toc_dev_info_get(const toc_dev *dev, toc_dev_info *info);
  *             row whose span starts at or after that entry
  *   cols    : uint32 per batch 4 (n_cols+1) entries (at b * 4 (n_cols+1)): for each
  *             column j = 0..n_cols, the first position of a leaf whose key column
- *             is >= j, the occurrences (occ_row entries) of such leaves before
- *             it, and the first tlist entry of key column >= j; then the columns
+ *             is >= j, the leaf occurrences (centry entries) of such leaves
+ *             before it, and the first tlist entry of key column >= j; then the columns
  *             ordered by number of such occurrences plus tree codes, most first
  *             (n_cols entries and one unused)
  *   tchild  : uint32 per batch n_tree+1 entries (at tree_base + b): the children of
  *             tree code h (h counting the codes with children at depth 1, then
  *             the codes of depth >= 2) are the codes tchild[h] .. tchild[h+1]-1
- *   centry  : uint32 per batch n_d + n_tree entries (at d_base + tree_base): for
- *             each key column in turn, its leaf occurrences (the tuple of each
- *             entry of D whose code is one of the column's leaves, the leaves in
- *             position order, each leaf's tuples ascending, bit 31 on a leaf's
- *             first) and then its tree codes (tlist entries) with bit 30 set;
- *             column j starts at the cols entries of j: leaf occurrences before it
- *             plus tlist entries before it.  After the last column, the tree
- *             codes' occurrences (plain tuple indexes, ascending per code), where
- *             occ_off points.  Needs rows and codes below 2^30 per batch.
- *   cval    : float per centry entry of a column (same index): the key value of
- *             the entry's code (the multiplier of the left multiplication's term);
- *             0 beside the tree codes' occurrences
+ *   centry  : uint32 per batch n_d + n_tree entries (at d_base + tree_base), in
+ *             three parts: (1) the leaf occurrences, leaf by leaf in position
+ *             order (so a column's leaves are one stretch, from its cols entry),
+ *             each leaf's tuples ascending with bit 31 set on its first; (2) the
+ *             tree codes (tlist entries) by key column, each with bit 30 set,
+ *             column j's from (1)'s end plus its cols tlist entry; (3) the tree
+ *             codes' own occurrences, tree row by tree row (plain tuple indexes,
+ *             ascending), where occ_off points.  Needs rows and codes below 2^30
+ *             per batch.
+ *   cval    : float per centry entry (same index): in parts (1) and (2) the key
+ *             value of the entry's code (the multiplier of the left
+ *             multiplication's term), 0 in part (3)
  * Depth-1 codes without children are numbered in the order of their first entry
  * in D; the codes of each level d >= 2 are sorted by parent.                    */
 typedef struct {

@@ -1418,7 +1418,11 @@ __global__ __launch_bounds__(kRtBlock) void right_staged_kernel(
 // right_tiled_kernel.  Per item:
 //  * the batch's used columns come from the column index of the image (a column
 //    is used when it has a depth-1 leaf or a tree code): a ballot scan gives each
-//    its row, kept in an LDS map column -> row, and the rows are gathered from W;
+//    its row, kept in an LDS map column -> row, and the rows are gathered from W.
+//    This is pipelined one item ahead: the map of the next item is built (into a
+//    second map) while the current item starts, from column-index words loaded
+//    one item earlier still, and a wave that has no tuples left loads its share
+//    of the next item's rows of W into registers before it waits for the others;
 //  * the H rows of the deep codes (depth >= 2) are built level by level into
 //    the worker's workspace slot (H[c] = H[parent] + val * W[col]);
 //  * tuple sums as in right_tiled_kernel (16 lanes per tuple, entries loaded two
@@ -1433,12 +1437,13 @@ constexpr int kRcHgRow = 64;                      // floats per deep row in the 
 constexpr int kRcPer = 2;                         // entries per lane and chunk
 constexpr int kRcChunk = kRcPer * kRtLanes;       // 32 entries per tuple per step
 constexpr uint32_t kRcNone = 0xFFFFFFFFu;
+constexpr int kRcWv = 10;                         // float4 of W rows per thread held across the barrier
 
-// LDS bytes of the compact kernel: rows 0 .. umax-1 (W), row umax (zeros), the
-// map (u16 per column), the used-column list (u16 per row) and 16 wave totals.
+// LDS bytes of the compact kernel: rows 0 .. umax-1 (W), row umax (zeros), two
+// maps (u16 per column), two used-column lists (u16 per row) and 16 wave totals.
 inline size_t rc_lds_bytes(int64_t umax, int64_t m) {
   const size_t rows = (size_t)(umax + 1) * kRcRowBytes;
-  return rows + (size_t)2 * m + (size_t)2 * umax + 64 + 16;
+  return rows + (size_t)4 * m + (size_t)4 * umax + 64 + 16;
 }
 
 __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
@@ -1455,85 +1460,145 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
   const uint32_t wb = lds_base(smem4);
   const uint32_t qoff = 16u * (uint32_t)sub;
   const uint32_t zrow_b = wb + (uint32_t)cap * kRcRowBytes;
-  uint16_t *map = (uint16_t *)(lds + (size_t)(cap + 1) * kRcRowBytes);
-  uint16_t *ucol = map + m;
-  uint32_t *wsum = (uint32_t *)(((uintptr_t)(ucol + cap) + 3) & ~(uintptr_t)3);
+  uint16_t *maps = (uint16_t *)(lds + (size_t)(cap + 1) * kRcRowBytes);   // two maps of m
+  uint16_t *ucols = maps + 2 * m;                                         // two lists of cap
+  uint32_t *wsum = (uint32_t *)(((uintptr_t)(ucols + 2 * cap) + 3) & ~(uintptr_t)3);
   float *Hg = ws + blockIdx.x * slot_floats;
   // the zero row
   for (int e = threadIdx.x; e < kRcKT; e += kRtBlock) Wt[cap * kRcKT + e] = 0.0f;
   if (threadIdx.x < 2) tg_next[threadIdx.x] = kRtWaves;
   const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
   const int64_t n_items = nbx * n_tiles;
+  auto batch_of = [&](int64_t it) -> int64_t { return uniform64(x + kXcd * (it / n_tiles)); };
+  auto tile_of = [&](int64_t it) -> int {
+    return __builtin_amdgcn_readfirstlane((int)(it % n_tiles)) * kRcKT;
+  };
+  // column-index words of column j = threadIdx.x of batch b (leaf positions and
+  // tree-list entries of columns j and j + 1), loaded ahead of the map build
+  auto load_cols = [&](int64_t b, uint32_t (&cw)[4]) {
+    const uint32_t *Loff = cols_all + b * 4 * (int64_t)(m + 1);
+    const uint32_t *Toff = Loff + 2 * (m + 1);
+    const int j = (int)threadIdx.x;
+    cw[0] = cw[1] = cw[2] = cw[3] = 0u;
+    if (j < m) {
+      cw[0] = Loff[j];
+      cw[1] = Loff[j + 1];
+      cw[2] = Toff[j];
+      cw[3] = Toff[j + 1];
+    }
+  };
+  // used columns: column j is used when it has a depth-1 leaf or a tree code; its
+  // row is the number of used columns before it (at most cap: the host sized cap
+  // for the batch with the most).  Columns from kRtBlock on (wide matrices) are
+  // loaded here.  Returns the number of rows; the map and the list are complete
+  // for every thread on return.
+  auto build_map = [&](int64_t b, const uint32_t (&cw)[4], uint16_t *map, uint16_t *ucol) -> uint32_t {
+    const uint32_t *Loff = cols_all + b * 4 * (int64_t)(m + 1);
+    const uint32_t *Toff = Loff + 2 * (m + 1);
+    uint32_t base = 0;
+    for (int j0 = 0; j0 < m; j0 += kRtBlock) {
+      const int j = j0 + (int)threadIdx.x;
+      bool used;
+      if (j0 == 0) {
+        used = cw[1] > cw[0] || cw[3] > cw[2];
+      } else {
+        used = j < m && (Loff[j + 1] > Loff[j] || Toff[j + 1] > Toff[j]);
+      }
+      const uint64_t bal = __ballot(used);
+      const uint32_t below = (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+      if (lane == 0) wsum[wave] = (uint32_t)__popcll(bal);
+      __syncthreads();
+      uint32_t before = base, total = base;
+#pragma unroll
+      for (int w = 0; w < kRtWaves; ++w) {
+        const uint32_t t = wsum[w];
+        before += w < wave ? t : 0u;
+        total += t;
+      }
+      const uint32_t row = before + below;
+      if (used && row < (uint32_t)cap) {
+        map[j] = (uint16_t)row;
+        ucol[row] = (uint16_t)j;
+      }
+      base = total;
+      __syncthreads();
+    }
+    return min(base, (uint32_t)cap);
+  };
+  // this thread's share of the item's rows of W (float4 e = threadIdx.x + i *
+  // kRtBlock of the U rows of 16 float4); columns past kt are zeros
+  auto w_at = [&](uint32_t e, int k0, int kt, bool vec, const uint16_t *ucol) -> float4 {
+    const uint32_t r = e / (kRcKT / 4), q4 = 4 * (e % (kRcKT / 4));
+    const float *src = W + (int64_t)ucol[r] * ldw + k0 + q4;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (vec) {
+      v = *(const float4 *)src;
+    } else {
+      if ((int)q4 + 0 < kt) v.x = src[0];
+      if ((int)q4 + 1 < kt) v.y = src[1];
+      if ((int)q4 + 2 < kt) v.z = src[2];
+      if ((int)q4 + 3 < kt) v.w = src[3];
+    }
+    return v;
+  };
+  auto is_vec = [&](int k0, int kt) {
+    return kt == kRcKT && (ldw % 4) == 0 && (((uintptr_t)(W + k0)) & 15u) == 0;
+  };
+  auto load_w = [&](uint32_t U, int k0, const uint16_t *ucol, float4 (&wv)[kRcWv]) {
+    const int kt = min(kRcKT, k - k0);
+    const bool vec = is_vec(k0, kt);
+    const uint32_t n4 = U * (kRcKT / 4);
+#pragma unroll
+    for (int i = 0; i < kRcWv; ++i) {
+      const uint32_t e = threadIdx.x + (uint32_t)(i * kRtBlock);
+      wv[i] = e < n4 ? w_at(e, k0, kt, vec, ucol) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  // the held share into the tile, and rows past kRcWv * kRtBlock float4 (more
+  // than 640 used columns) straight from W
+  auto store_w = [&](uint32_t U, int k0, const uint16_t *ucol, const float4 (&wv)[kRcWv]) {
+    const uint32_t n4 = U * (kRcKT / 4);
+#pragma unroll
+    for (int i = 0; i < kRcWv; ++i) {
+      const uint32_t e = threadIdx.x + (uint32_t)(i * kRtBlock);
+      if (e < n4) *(float4 *)&Wt[e * 4] = wv[i];
+    }
+    const int kt = min(kRcKT, k - k0);
+    const bool vec = is_vec(k0, kt);
+    for (uint32_t e = threadIdx.x + (uint32_t)(kRcWv * kRtBlock); e < n4; e += kRtBlock)
+      *(float4 *)&Wt[e * 4] = w_at(e, k0, kt, vec, ucol);
+  };
+  // the first item's map and rows, and the column-index words of the second
+  uint32_t cw[4];
+  float4 wv[kRcWv];
+  uint32_t U = 0;
+  if (s < n_items) {
+    load_cols(batch_of(s), cw);
+    U = build_map(batch_of(s), cw, maps, ucols);
+    if (s + spw < n_items) load_cols(batch_of(s + spw), cw);
+    load_w(U, tile_of(s), ucols, wv);
+  }
   uint32_t parity = 0;
   for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
-    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
-    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
-    const int k0 = tile * kRcKT;
+    const int64_t b = batch_of(it);
+    const int k0 = tile_of(it);
     const int kt = min(kRcKT, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t n1 = (uint32_t)bt.n_lvl1;
     const int nrows = bt.n_rows;
-    __syncthreads();   // the previous item no longer reads the tile, map or counters
+    const uint16_t *map = maps + parity * (uint32_t)m;
+    __syncthreads();   // the previous item no longer reads the tile, the other map or counters
     if (threadIdx.x == 0) tg_next[parity ^ 1u] = kRtWaves;
-    // used columns: column j is used when it has a depth-1 leaf (Loff) or a tree
-    // code (Toff); its row is the number of used columns before it (at most cap:
-    // the host sized cap for the batch with the most)
-    {
-      const uint32_t *Loff = cols_all + b * 4 * (int64_t)(m + 1);
-      const uint32_t *Toff = Loff + 2 * (m + 1);
-      uint32_t base = 0;
-      for (int j0 = 0; j0 < m; j0 += kRtBlock) {
-        const int j = j0 + (int)threadIdx.x;
-        const bool used = j < m && (Loff[j + 1] > Loff[j] || Toff[j + 1] > Toff[j]);
-        const uint64_t bal = __ballot(used);
-        const uint32_t below = (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
-        if (lane == 0) wsum[wave] = (uint32_t)__popcll(bal);
-        __syncthreads();
-        uint32_t before = base, total = base;
-#pragma unroll
-        for (int w = 0; w < kRtWaves; ++w) {
-          const uint32_t t = wsum[w];
-          before += w < wave ? t : 0u;
-          total += t;
-        }
-        const uint32_t row = before + below;
-        if (used && row < (uint32_t)cap) {
-          map[j] = (uint16_t)row;
-          ucol[row] = (uint16_t)j;
-        }
-        base = total;
-        __syncthreads();
-      }
-      // the rows of W (all loads of a pass first, then the stores); columns past
-      // kt are zeros
-      const uint32_t U = min(base, (uint32_t)cap);
-      const uint32_t n4 = U * (kRcKT / 4);
-      const bool vec = kt == kRcKT && (ldw % 4) == 0 && (((uintptr_t)(W + k0)) & 15u) == 0;
-      for (uint32_t e0 = threadIdx.x; e0 < n4; e0 += 8 * kRtBlock) {
-        float4 v[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t e = e0 + i * kRtBlock;
-          v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (e < n4) {
-            const uint32_t r = e / (kRcKT / 4), q4 = 4 * (e % (kRcKT / 4));
-            const float *src = W + (int64_t)ucol[r] * ldw + k0 + q4;
-            if (vec) {
-              v[i] = *(const float4 *)src;
-            } else {
-              if ((int)q4 + 0 < kt) v[i].x = src[0];
-              if ((int)q4 + 1 < kt) v[i].y = src[1];
-              if ((int)q4 + 2 < kt) v[i].z = src[2];
-              if ((int)q4 + 3 < kt) v[i].w = src[3];
-            }
-          }
-        }
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t e = e0 + i * kRtBlock;
-          if (e < n4) *(float4 *)&Wt[e * 4] = v[i];
-        }
-      }
+    store_w(U, k0, ucols + parity * (uint32_t)cap, wv);
+    // the next item's map (its barriers also publish the tile), then the
+    // column-index words of the item after it
+    const int64_t itn = it + spw;
+    uint32_t U_next = 0;
+    if (itn < n_items) {
+      U_next = build_map(batch_of(itn), cw, maps + (parity ^ 1u) * (uint32_t)m,
+                         ucols + (parity ^ 1u) * (uint32_t)cap);
+      if (itn + spw < n_items) load_cols(batch_of(itn + spw), cw);
+    } else {
       __syncthreads();
     }
     // H rows of the deep codes into the workspace slot, level by level: a 16-lane
@@ -1607,9 +1672,9 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
             lmax = wave_max(len - lst);
             ntg = grab();
           }
+          spans_of(ntg, nst, nen);
         }
       }
-      spans_of(ntg, nst, nen);
     };
     const BufRes rs_dc = buf_res(im.dcodes + bt.d_base, (uint32_t)bt.n_d);
     const BufRes rs_node = key_res(im.key + bt.code_base, (uint32_t)bt.n_codes);
@@ -1733,6 +1798,11 @@ __global__ __launch_bounds__(kRtBlock) void right_compact_kernel(
       if (!(G.tg < n_tg || C.tg < n_tg)) break;
       step(dB, okB, dA, okA);
     }
+    // no tuples left for this wave: its share of the next item's rows of W, held
+    // until every wave is done with the tile
+    // (none after the last item: U_next is 0 there)
+    load_w(U_next, tile_of(itn), ucols + (parity ^ 1u) * (uint32_t)cap, wv);
+    U = U_next;
   }
 }
 
