@@ -1844,10 +1844,13 @@ constexpr uint32_t lt_stage_bytes() {
 }
 
 // LDS byte offset of the rows: stages, then the batch's column index (Loff, Ost,
-// Toff, Ord: m + 1 entries each, as in the image) and Coff (max_tree + 1)
+// Toff, Ord: m + 1 entries each, as in the image), the children offsets Coff of
+// the tree rows and, when toc is set, their occurrence offsets Toc (max_tree + 1
+// each)
 template <int TW>
-constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree) {
-  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (4 * (m + 1) + max_tree + 1) + 15) & ~(int64_t)15);
+constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree, bool toc) {
+  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (4 * (m + 1) + (toc ? 2 : 1) * (max_tree + 1)) +
+                     15) & ~(int64_t)15);
 }
 
 struct LtChunk {
@@ -1862,7 +1865,7 @@ template <int TW, bool TREE_LDS>
 __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
     const uint32_t *__restrict__ tchild_all, int64_t nb, int n_tiles, int spw, int max_rows,
-    int max_tree, int tree_cap, int m, const float *__restrict__ G, int64_t ldg, int k,
+    int max_tree, int tree_cap, int toc_lds, int m, const float *__restrict__ G, int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
     int64_t slot_floats) {
   // TREE_LDS: every tree row is in LDS; else the first tree_cap are and the others
@@ -1884,7 +1887,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   uint32_t *Toff = Ost + (m + 1);
   uint32_t *Ord = Toff + (m + 1);             // columns by decreasing number of entries
   uint32_t *Coff = Ord + (m + 1);
-  const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree);
+  uint32_t *Toc = Coff + (max_tree + 1);     // (toc_lds only)
+  const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree, toc_lds != 0);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   constexpr bool DPP = LPG == kRtLanes;       // a group is one 16-lane row: entries by broadcast
@@ -1900,17 +1904,25 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   if (threadIdx.x < 2) cg_next[threadIdx.x] = kLtWaves;
   const int64_t nbx = nb > x ? (nb - x + kXcd - 1) / kXcd : 0;
   const int64_t n_items = nbx * n_tiles;
+  auto item_batch = [&](int64_t it) -> int64_t { return uniform64(x + kXcd * (it / n_tiles)); };
+  auto item_k0 = [&](int64_t it) -> int {
+    return __builtin_amdgcn_readfirstlane((int)(it % n_tiles)) * TW;
+  };
   uint32_t parity = 0;
   for (int64_t it = s; it < n_items; it += spw, parity ^= 1u) {
-    const int64_t b = uniform64(x + kXcd * (it / n_tiles));
-    const int tile = __builtin_amdgcn_readfirstlane((int)(it % n_tiles));
-    const int k0 = tile * TW;
+    const int64_t b = item_batch(it);
+    const int k0 = item_k0(it);
     const int kt = min(TW, k - k0);
     const toc_batch bt = uniform_batch(im.batches + b);
     const uint32_t *lvl = im.level + bt.lvl_base;
     const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
     // tree row h's occurrences: entries to[h] .. to[h+1]-1 of the batch's entry array
+    // (copied to Toc in LDS when toc_lds is set)
     const uint32_t *to = occ_off_all + bt.code_base + 2 * b + (n1 - ni) + 1;
+    auto occ_at = [&](uint32_t h) -> uint32_t {
+      if (toc_lds) return Toc[h];
+      return to[h];
+    };
     const uint32_t *orow = im.centry + bt.d_base + bt.tree_base;
     const uint32_t n_tree = ni + (nc - n1);
     const int nrows = bt.n_rows;
@@ -1948,12 +1960,16 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
       }
     }
-    // the batch's column index and children ranges, from the image
+    // the batch's column index, children ranges and (when they fit) occurrence
+    // offsets, from the image
     {
       const uint4 *src = (const uint4 *)(cols_all + b * 4 * (int64_t)(m + 1));
       for (int e = threadIdx.x; e < m + 1; e += kLtBlock) ((uint4 *)Loff)[e] = src[e];
       const uint32_t *tch = tchild_all + bt.tree_base + b;
-      for (uint32_t h = threadIdx.x; h <= n_tree; h += kLtBlock) Coff[h] = tch[h];
+      for (uint32_t h = threadIdx.x; h <= n_tree; h += kLtBlock) {
+        Coff[h] = tch[h];
+        if (toc_lds) Toc[h] = to[h];
+      }
     }
     __syncthreads();
     // Tree codes, deepest level first: H = own occurrences' G rows + children's
@@ -1994,8 +2010,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           const bool in = c < e;
           const uint32_t cc = in ? c : c0;
           h[u] = hrow(cc);
-          o0[u] = to[h[u]];
-          o1[u] = in ? to[h[u] + 1] : o0[u];
+          o0[u] = occ_at(h[u]);
+          o1[u] = in ? occ_at(h[u] + 1) : o0[u];
           k0[u] = Coff[h[u]];
           k1[u] = in ? Coff[h[u] + 1] : k0[u];
         }
@@ -2737,6 +2753,7 @@ struct OpPlan {
   int64_t lds_rows = 0;       // tiled left: tree rows in LDS
   int per = 1;                // tiled right: batches per item
   bool compact = false;       // tiled right: the compact-tile kernel (64 columns)
+  bool toc_lds = false;       // tiled left: tree rows' occurrence offsets in LDS
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -2797,12 +2814,16 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
   } else if (k >= 2) {
     // widest tile first; tree rows in LDS when they fit, else in the workspace
     const size_t lds_max = kLdsMax - kLtStaticBytes;
-    for (int tw : {64, 32}) {
-      const size_t head = tw == 64 ? lt_rows_offset<64>(m, d->max_tree) : lt_rows_offset<32>(m, d->max_tree);
+    for (int tw_toc : {64 * 2 + 1, 64 * 2, 32 * 2 + 1, 32 * 2}) {
+      const int tw = tw_toc / 2;
+      const bool toc = (tw_toc & 1) != 0;
+      const size_t head = tw == 64 ? lt_rows_offset<64>(m, d->max_tree, toc)
+                                   : lt_rows_offset<32>(m, d->max_tree, toc);
       const size_t rows = ((size_t)d->max_rows + 1) * tw * 4;
       if (head + rows > lds_max) continue;
       p.path = kPathTiled;
       p.tw = tw;
+      p.toc_lds = toc;
       p.n_tiles = (k + tw - 1) / tw;
       // the tree rows that fit in LDS go there, the others to the workspace
       p.lds_rows = std::min<int64_t>(d->max_tree, (int64_t)((lds_max - head - rows) / ((size_t)tw * 4)));
@@ -3230,7 +3251,8 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
     if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
     hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
                        im, occ_off, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,              \
-                       d->max_rows, (int)d->max_tree, (int)plan.lds_rows, m, G, ldg, k, out, ldo,  \
+                       d->max_rows, (int)d->max_tree, (int)plan.lds_rows, (int)plan.toc_lds, m, G, \
+                       ldg, k, out, ldo,                                                            \
                        accumulate, (float *)ws, slot);                                          \
   } while (0)
     if (plan.tw == 64) {
