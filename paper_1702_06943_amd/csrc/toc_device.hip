@@ -1846,12 +1846,14 @@ constexpr uint32_t lt_stage_bytes() {
 // LDS byte offset of the rows: stages, then the batch's column index (Loff, Ost,
 // Toff, Ord: m + 1 entries each, as in the image), the children offsets Coff of
 // the tree rows and, when toc is set, their occurrence offsets Toc (max_tree + 1
-// each)
+// each) and ocr words for the tree rows' occurrences themselves
 template <int TW>
-constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree, bool toc) {
-  return (uint32_t)((lt_stage_bytes<TW>() + 4 * (4 * (m + 1) + (toc ? 2 : 1) * (max_tree + 1)) +
-                     15) & ~(int64_t)15);
+constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree, bool toc, int64_t ocr) {
+  return (uint32_t)((lt_stage_bytes<TW>() +
+                     4 * (4 * (m + 1) + (toc ? 2 : 1) * (max_tree + 1) + (toc ? ocr : 0)) + 15) &
+                    ~(int64_t)15);
 }
+constexpr int kLtOcr = 1024;   // LDS words for a batch's tree-row occurrences
 
 struct LtChunk {
   int cg;           // column group (columns GPW*cg .. GPW*cg+GPW-1); >= n_cg: none
@@ -1865,7 +1867,8 @@ template <int TW, bool TREE_LDS>
 __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     Img im, const uint32_t *__restrict__ occ_off_all, const uint32_t *__restrict__ tlist_all, const uint32_t *__restrict__ cols_all,
     const uint32_t *__restrict__ tchild_all, int64_t nb, int n_tiles, int spw, int max_rows,
-    int max_tree, int tree_cap, int toc_lds, int m, const float *__restrict__ G, int64_t ldg, int k,
+    int max_tree, int tree_cap, int toc_lds, int ocr_cap, int m, const float *__restrict__ G,
+    int64_t ldg, int k,
     float *__restrict__ out, int64_t ldo, int accumulate, float *__restrict__ ws,
     int64_t slot_floats) {
   // TREE_LDS: every tree row is in LDS; else the first tree_cap are and the others
@@ -1888,7 +1891,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
   uint32_t *Ord = Toff + (m + 1);             // columns by decreasing number of entries
   uint32_t *Coff = Ord + (m + 1);
   uint32_t *Toc = Coff + (max_tree + 1);     // (toc_lds only)
-  const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree, toc_lds != 0);
+  uint32_t *Ocr = Toc + (max_tree + 1);      // (toc_lds only: ocr_cap words)
+  const uint32_t rows_b = lt_rows_offset<TW>(m, max_tree, toc_lds != 0, ocr_cap);
   float *Rw = (float *)(lds + rows_b);        // G rows, zero row, then tree rows
   const uint32_t qb = lds_base(smem4) + rows_b + 4u * (uint32_t)q;   // LDS address of this lane's columns
   constexpr bool DPP = LPG == kRtLanes;       // a group is one 16-lane row: entries by broadcast
@@ -1927,6 +1931,15 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     const uint32_t n_tree = ni + (nc - n1);
     const int nrows = bt.n_rows;
     auto hrow = [&](uint32_t c) -> uint32_t { return c < ni ? c : c - n1 + ni; };
+    // the tree rows' occurrences are the last entries of the batch's entry array,
+    // from to[0]; they are copied to LDS when they fit in ocr_cap words
+    const uint32_t p3 = toc_lds && ocr_cap ? (uint32_t)__builtin_amdgcn_readfirstlane((int)to[0]) : 0u;
+    const uint32_t n_p3 = (uint32_t)bt.n_d + n_tree - p3;
+    const bool use_ocr = toc_lds && ocr_cap && n_p3 <= (uint32_t)ocr_cap;
+    auto occ_row = [&](uint32_t o) -> uint32_t {
+      if (use_ocr) return Ocr[o - p3];
+      return orow[o];
+    };
     __syncthreads();   // the previous item no longer reads the LDS rows and tables
     if (threadIdx.x == 0) cg_next[parity ^ 1u] = kLtWaves;
     // G tile: all loads of a pass first, then the stores
@@ -1970,6 +1983,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         Coff[h] = tch[h];
         if (toc_lds) Toc[h] = to[h];
       }
+      if (use_ocr)
+        for (uint32_t t = threadIdx.x; t < n_p3; t += kLtBlock) Ocr[t] = orow[p3 + t];
     }
     __syncthreads();
     // Tree codes, deepest level first: H = own occurrences' G rows + children's
@@ -2017,7 +2032,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
         }
 #pragma unroll
         for (int u = 0; u < kLtU; ++u) {
-          mine[u] = o0[u] + sub < o1[u] ? orow[o0[u] + sub] & ~kFirstOcc : zrow;
+          mine[u] = o0[u] + sub < o1[u] ? occ_row(o0[u] + sub) & ~kFirstOcc : zrow;
           nmax = max(nmax, min(o1[u] - o0[u], (uint32_t)LPG));
           cmax = max(cmax, k1[u] - k0[u]);
         }
@@ -2064,7 +2079,7 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           add4(acc[u], part[u]);
           // occurrences past the first LPG (rare): one at a time
           for (uint32_t ob = o0[u] + LPG; ob < o1[u]; ob += LPG) {
-            const uint32_t mo = ob + sub < o1[u] ? orow[ob + sub] & ~kFirstOcc : zrow;
+            const uint32_t mo = ob + sub < o1[u] ? occ_row(ob + sub) & ~kFirstOcc : zrow;
             const uint32_t n = min((uint32_t)LPG, o1[u] - ob);
             float4 pb = make_float4(0.f, 0.f, 0.f, 0.f);
             for (uint32_t i = 0; i < n; ++i) {
@@ -2754,6 +2769,7 @@ struct OpPlan {
   int per = 1;                // tiled right: batches per item
   bool compact = false;       // tiled right: the compact-tile kernel (64 columns)
   bool toc_lds = false;       // tiled left: tree rows' occurrence offsets in LDS
+  int ocr_cap = 0;            // tiled left: LDS words for the tree rows' occurrences
 };
 
 OpPlan plan_op(const toc_dev *d, int op, int k) {
@@ -2814,16 +2830,20 @@ OpPlan plan_op(const toc_dev *d, int op, int k) {
   } else if (k >= 2) {
     // widest tile first; tree rows in LDS when they fit, else in the workspace
     const size_t lds_max = kLdsMax - kLtStaticBytes;
-    for (int tw_toc : {64 * 2 + 1, 64 * 2, 32 * 2 + 1, 32 * 2}) {
-      const int tw = tw_toc / 2;
-      const bool toc = (tw_toc & 1) != 0;
-      const size_t head = tw == 64 ? lt_rows_offset<64>(m, d->max_tree, toc)
-                                   : lt_rows_offset<32>(m, d->max_tree, toc);
+    // widest tile first, then with the tree rows' occurrence offsets and (kLtOcr
+    // words of) occurrences in LDS, then with the offsets only, then neither
+    for (int cfg = 0; cfg < 6; ++cfg) {
+      const int tw = cfg < 3 ? 64 : 32;
+      const bool toc = cfg % 3 != 2;
+      const int ocr = cfg % 3 == 0 ? kLtOcr : 0;
+      const size_t head = tw == 64 ? lt_rows_offset<64>(m, d->max_tree, toc, ocr)
+                                   : lt_rows_offset<32>(m, d->max_tree, toc, ocr);
       const size_t rows = ((size_t)d->max_rows + 1) * tw * 4;
       if (head + rows > lds_max) continue;
       p.path = kPathTiled;
       p.tw = tw;
       p.toc_lds = toc;
+      p.ocr_cap = ocr;
       p.n_tiles = (k + tw - 1) / tw;
       // the tree rows that fit in LDS go there, the others to the workspace
       p.lds_rows = std::min<int64_t>(d->max_tree, (int64_t)((lds_max - head - rows) / ((size_t)tw * 4)));
@@ -3251,7 +3271,8 @@ toc_status left_mul_impl(const toc_dev *d, const float *G, int32_t k, int64_t ld
     if ((st = allow_lds(left_tiled_kernel<TW, TL>, plan.lds))) return st;                       \
     hipLaunchKernelGGL((left_tiled_kernel<TW, TL>), dim3(plan.grid), dim3(kLtBlock), plan.lds, s, \
                        im, occ_off, tlist, cols, tchild, nb, plan.n_tiles, plan.spx,              \
-                       d->max_rows, (int)d->max_tree, (int)plan.lds_rows, (int)plan.toc_lds, m, G, \
+                       d->max_rows, (int)d->max_tree, (int)plan.lds_rows, (int)plan.toc_lds,       \
+                       plan.ocr_cap, m, G,                                                          \
                        ldg, k, out, ldo,                                                            \
                        accumulate, (float *)ws, slot);                                          \
   } while (0)
