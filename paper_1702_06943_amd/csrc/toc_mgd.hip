@@ -98,10 +98,14 @@ __device__ void mgd_read_ahead(const MgImg &im, int64_t b0, int64_t nb, int32_t 
   asm volatile("" : : "v"(acc));    // the loads are the point: keep them
 }
 
+// HL: the model h is kept in LDS for the whole launch (read at the start, written
+// back at the end), else every step reads and writes it in memory
+template <bool HL>
 __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int64_t nb, int32_t m,
-                                                       int32_t max_rows, int loss, float lr,
+                                                       int32_t max_rows, int32_t max_codes,
+                                                       int loss, float lr,
                                                        const float *__restrict__ y,
-                                                       float *__restrict__ h, uint32_t tag) {
+                                                       float *__restrict__ hg, uint32_t tag) {
   // workgroup 0 steps; workgroups kMgXcds, 2 kMgXcds, ... (on its XCD) read ahead;
   // the others have nothing to do
   if (blockIdx.x % kMgXcds != 0) return;
@@ -112,6 +116,11 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
   extern __shared__ float sm[];
   float *Gs = sm;                  // per tuple: d loss / d r
   float *H = sm + max_rows;        // per code (right), then per left position (left)
+  float *h = HL ? H + max_codes : hg;
+  if (HL) {
+    for (int j = threadIdx.x; j < m; j += kMgBlock) h[j] = hg[j];
+    __syncthreads();
+  }
   for (int64_t b = b0; b < b0 + nb; ++b) {
     if (threadIdx.x == 0)
       __hip_atomic_store(&mgd_progress, ((uint64_t)tag << 32) | (uint32_t)(b - b0), __ATOMIC_RELAXED,
@@ -126,7 +135,7 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     // right: H[c] = H[parent] + val * h[col], level by level
     for (int d = 1; d <= bt.n_levels; ++d) {
       const uint32_t a = lvl[d - 1], e = lvl[d];
-#pragma unroll 4
+#pragma unroll 8
       for (uint32_t c = a + threadIdx.x; c < e; c += kMgBlock) {
         const toc_key k = key[c];
         const float base = d > 1 ? H[link[c].parent] : 0.0f;
@@ -210,6 +219,8 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     }
     __syncthreads();                // the next step's right product reads the new h
   }
+  if (HL)
+    for (int j = threadIdx.x; j < m; j += kMgBlock) hg[j] = h[j];
 }
 
 }  // namespace
@@ -236,12 +247,15 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   if (!std::isfinite(lr)) return fail(TOC_EINVAL, "learning rate not finite");
   if (n_batches == 0) return TOC_OK;
   if (!h || (!y && d->info.n_rows > 0)) return fail(TOC_EINVAL, "NULL pointer");
-  const size_t lds = 4 * ((size_t)d->max_rows + (size_t)d->max_codes);
-  if (lds > kMgLdsMax)
-    return fail(TOC_EUNSUPPORTED, "a batch needs %zu bytes of LDS (max %zu)", lds, kMgLdsMax);
+  const size_t lds0 = 4 * ((size_t)d->max_rows + (size_t)d->max_codes);
+  if (lds0 > kMgLdsMax)
+    return fail(TOC_EUNSUPPORTED, "a batch needs %zu bytes of LDS (max %zu)", lds0, kMgLdsMax);
+  // the model in LDS too when it fits
+  const bool hl = lds0 + 4 * (size_t)d->info.n_cols <= kMgLdsMax;
+  const size_t lds = hl ? lds0 + 4 * (size_t)d->info.n_cols : lds0;
+  const void *fn = hl ? (const void *)mgd_kernel<true> : (const void *)mgd_kernel<false>;
   if (lds > 64 * 1024 &&
-      hipFuncSetAttribute((const void *)mgd_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                          (int)lds) != hipSuccess)
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
   const uint8_t *base = (const uint8_t *)d->buf;
   const toc_layout &L = d->layout;
@@ -253,9 +267,14 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                  (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
   static std::atomic<uint32_t> launches{0};
   const uint32_t tag = launches.fetch_add(1) + 1;
-  hipLaunchKernelGGL(mgd_kernel, dim3(kMgXcds * (1 + kMgHelpers)), dim3(kMgBlock), lds,
-                     (hipStream_t)stream, im, b0, n_batches, d->info.n_cols, d->max_rows, (int)loss,
-                     lr, y, h, tag);
+  if (hl)
+    hipLaunchKernelGGL(mgd_kernel<true>, dim3(kMgXcds * (1 + kMgHelpers)), dim3(kMgBlock), lds,
+                       (hipStream_t)stream, im, b0, n_batches, d->info.n_cols, d->max_rows,
+                       d->max_codes, (int)loss, lr, y, h, tag);
+  else
+    hipLaunchKernelGGL(mgd_kernel<false>, dim3(kMgXcds * (1 + kMgHelpers)), dim3(kMgBlock), lds,
+                       (hipStream_t)stream, im, b0, n_batches, d->info.n_cols, d->max_rows,
+                       d->max_codes, (int)loss, lr, y, h, tag);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "mgd_kernel: %s", hipGetErrorString(e));
   return TOC_OK;
