@@ -2520,6 +2520,8 @@ constexpr size_t kDecLdsMax = 64 * 1024;
 constexpr int kDbBlock = 1024;                    // 16 waves: two or more workgroups per CU
 constexpr int kDbWaves = kDbBlock / kWave;
 constexpr int kDbPer = (int)toc::kDecodeTile / kDbBlock;   // 1
+constexpr int kDbAhead = 8;                       // runs whose codes are loaded together
+static_assert(kDbPer == 1, "one entry per thread and run");
 
 __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t b0,
                                                                  int64_t *__restrict__ rowptr,
@@ -2546,13 +2548,23 @@ __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t 
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const int64_t base = bt.nnz_base;
   uint32_t carry = 0;                               // pairs of the runs before
+  // the codes of kDbAhead runs are loaded at once, so one load latency serves them
+  // (loading the first ones before the tables measured slower)
+  uint32_t ahead[kDbAhead];
   for (uint32_t es = 0; es < nd; es += (uint32_t)toc::kDecodeTile) {
-    uint32_t c[kDbPer], dd[kDbPer];
+    const uint32_t r_in = (es / (uint32_t)toc::kDecodeTile) % kDbAhead;
+    if (r_in == 0) {
 #pragma unroll
-    for (int i = 0; i < kDbPer; ++i) {
-      const uint32_t j = es + i * kDbBlock + threadIdx.x;
-      c[i] = j < nd ? dc[j] : 0xFFFFFFFFu;
+      for (int a = 0; a < kDbAhead; ++a) {
+        const uint32_t j = es + a * (uint32_t)toc::kDecodeTile + threadIdx.x;
+        ahead[a] = j < nd ? dc[j] : 0xFFFFFFFFu;
+      }
     }
+    uint32_t c[kDbPer], dd[kDbPer];
+    c[0] = ahead[0];
+#pragma unroll
+    for (int a = 1; a < kDbAhead; ++a)
+      if (r_in == (uint32_t)a) c[0] = ahead[a];
 #pragma unroll
     for (int i = 0; i < kDbPer; ++i) {
       dd[i] = c[i] == 0xFFFFFFFFu ? 0u : (c[i] < n1 ? 1u : lk[c[i] - n1].y);
