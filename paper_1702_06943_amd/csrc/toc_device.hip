@@ -189,6 +189,8 @@ __device__ inline float blocked_sum(uint32_t a, uint32_t e, uint32_t step, L loa
 
 // Right multiplication (Theorem 1, Algorithm 4): H level by level, then one
 // group of LPR lanes per tuple sums H over the tuple's codes.
+constexpr int kK1RegCodes = 12;  // codes per thread held in registers by the k = 1 right product
+
 template <int LPR, int BLK>
 __global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
                                                           const float *__restrict__ W,
@@ -200,14 +202,50 @@ __global__ __launch_bounds__(BLK) void right_k1_kernel(Img im, int64_t b0,
   const NodePar par{deep_links(im.link, bt)};
   const NodeCol col{im.key + bt.code_base};
   const NodeVal val{im.key + bt.code_base};
-  for (int d = 1; d <= bt.n_levels; ++d) {
-    const uint32_t a = lvl[d - 1], e = lvl[d];
-#pragma unroll 4
-    for (uint32_t c = a + threadIdx.x; c < e; c += BLK) {
-      const float base = d > 1 ? H[par[c]] : 0.0f;
-      H[c] = fmaf(val[c], W[(int64_t)col[c] * ldw], base);
+  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1;
+  if (nc <= (uint32_t)(kK1RegCodes * BLK)) {
+    // every code's key, W entry and parent are loaded at once (thread t holds
+    // codes t, t + BLK, ...); depth-1 codes' H is written right away, and each
+    // deeper level then needs only LDS: H[c] = H[parent] + val * W[col]
+    float v[kK1RegCodes], w[kK1RegCodes];
+    uint32_t pr[kK1RegCodes];
+#pragma unroll
+    for (int i = 0; i < kK1RegCodes; ++i) {
+      const uint32_t c = threadIdx.x + (uint32_t)(i * BLK);
+      v[i] = 0.0f;
+      w[i] = 0.0f;
+      pr[i] = 0u;
+      if (c < nc) {
+        v[i] = val[c];
+        w[i] = W[(int64_t)col[c] * ldw];
+        if (c >= n1) pr[i] = par[c];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kK1RegCodes; ++i) {
+      const uint32_t c = threadIdx.x + (uint32_t)(i * BLK);
+      if (c < n1) H[c] = fmaf(v[i], w[i], 0.0f);
     }
     __syncthreads();
+    for (int d = 2; d <= bt.n_levels; ++d) {
+      const uint32_t a = lvl[d - 1], e = lvl[d];
+#pragma unroll
+      for (int i = 0; i < kK1RegCodes; ++i) {
+        const uint32_t c = threadIdx.x + (uint32_t)(i * BLK);
+        if (c >= a && c < e) H[c] = fmaf(v[i], w[i], H[pr[i]]);
+      }
+      __syncthreads();
+    }
+  } else {
+    for (int d = 1; d <= bt.n_levels; ++d) {
+      const uint32_t a = lvl[d - 1], e = lvl[d];
+#pragma unroll 4
+      for (uint32_t c = a + threadIdx.x; c < e; c += BLK) {
+        const float base = d > 1 ? H[par[c]] : 0.0f;
+        H[c] = fmaf(val[c], W[(int64_t)col[c] * ldw], base);
+      }
+      __syncthreads();
+    }
   }
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;

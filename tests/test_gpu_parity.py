@@ -283,6 +283,45 @@ def test_huge_single_row_and_large_batch():
         check_against_oracle(B, res, W=W, G=G)
 
 
+def _tree_occurrences(B):
+    """Per batch: (tree codes, entries of the tree codes' own occurrences), read
+    from the host-built image (toc_upload to host memory)."""
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    buf = np.zeros(T.toc_upload_size(encs), np.uint8)
+    dev = T.toc_upload(encs, buf, T.TOC_UPLOAD_HOST)
+    L = T.toc_dev_layout_get(dev)
+    recs = np.frombuffer(buf[L["batches"]:L["batches"] + 96 * B.n_batches].tobytes(), np.uint8)
+    out = []
+    for b in range(B.n_batches):
+        rec = recs[96 * b:96 * (b + 1)].tobytes()
+        code_base = int(np.frombuffer(rec[:8], np.int64)[0])
+        _, n_codes, n1, ni, _, n_d, _, _ = (int(x) for x in np.frombuffer(rec[64:], np.int32))
+        n_tree = ni + n_codes - n1
+        off = np.frombuffer(buf[L["occ_off"] + 4 * (code_base + 2 * b):][:4 * (n_codes + 2)]
+                            .tobytes(), np.uint32)
+        out.append((n_tree, n_d + n_tree - int(off[n1 - ni + 1])))
+    return out
+
+
+def test_left_tree_occurrences_in_and_beyond_lds():
+    """The tiled left product copies a batch's tree-code occurrences into LDS when
+    they fit in 1,024 words and reads them from memory otherwise: one batch of
+    each kind (rows copying long prefixes of earlier rows make many tree codes
+    with many occurrences) in one launch, right and left against the oracle."""
+    m = 40
+    heavy = tiny_batch(7, 480, m, density=0.9, n_values=1, prefix_copy=0.99)
+    light = tiny_batch(8, 480, m, density=0.2, n_values=30)
+    B = _batches_from_csrs([(480,) + heavy, (480,) + light], m)
+    occ = _tree_occurrences(B)
+    assert occ[0][1] > 1024 >= occ[1][1], occ
+    rng = np.random.default_rng(31)
+    for k in (64, 40):
+        W = rng.standard_normal((m, k)).astype(np.float32)
+        G = rng.standard_normal((960, k)).astype(np.float32)
+        res = run_gpu(B, W=W, G=G)
+        check_against_oracle(B, res, W=W, G=G)
+
+
 def test_many_batches():
     csrs = []
     for i in range(2500):
