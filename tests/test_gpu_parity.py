@@ -322,6 +322,21 @@ def test_left_tree_occurrences_in_and_beyond_lds():
         check_against_oracle(B, res, W=W, G=G)
 
 
+def test_decode_batch_of_many_runs():
+    """A batch of 8,000 short rows over 6 columns: few codes (its keys and links fit
+    the batch decode's LDS) but more than eight runs of 1,024 entries of D, so the
+    batch decode loads its codes in more than one group of runs."""
+    rp, c, v = tiny_batch(21, 8000, 6, density=0.7, n_values=2)
+    B = _batches_from_csrs([(8000, rp, c, v)], 6)
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    assert T.toc_enc_info_get(encs[0])["n_codes"] > 8 * 1024
+    rng = np.random.default_rng(12)
+    W = rng.standard_normal((6, 1)).astype(np.float32)
+    G = rng.standard_normal((8000, 1)).astype(np.float32)
+    res = run_gpu(B, W=W, G=G)
+    check_against_oracle(B, res, W=W, G=G)
+
+
 def test_many_batches():
     csrs = []
     for i in range(2500):
