@@ -18,6 +18,7 @@ namespace {
 
 constexpr int kMgBlock = 1024;
 constexpr int kMgLanes = 8;                    // lanes per tuple in the right product
+constexpr int kMgTup = 24;                     // a lane's codes of a tuple loaded at once
 constexpr uint32_t kMgFirst = 0x80000000u;     // first-occurrence bit of a leaf occurrence
 constexpr size_t kMgLdsMax = 160 * 1024;
 constexpr int kMgXcds = 8;                     // workgroups are dealt to the XCDs in turn
@@ -147,12 +148,31 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     {
       const uint32_t *span = im.span + bt.span_base;
       const uint32_t *dc = im.dcodes + bt.d_base;
+      const bool long_tuples = bt.n_d >= (int64_t)kMgLanes * 8 * nr;   // 8 codes a lane on average
       const int lane = threadIdx.x % kMgLanes, grp = threadIdx.x / kMgLanes;
       for (int r = grp; r < nr; r += kMgBlock / kMgLanes) {
         const uint32_t s = span[r], e = span[r + 1];
+        // long tuples (image-like batches): a lane's codes of the tuple (up to
+        // kMgTup of them) are loaded together and summed as one block; short ones
+        // (categorical batches) a few at a time
         float acc = 0.0f;
+        if (!long_tuples) {
 #pragma unroll 4
-        for (uint32_t j = s + lane; j < e; j += kMgLanes) acc += H[dc[j]];
+          for (uint32_t j = s + lane; j < e; j += kMgLanes) acc += H[dc[j]];
+        } else
+        for (uint32_t j0 = s + lane; j0 < e; j0 += kMgLanes * kMgTup) {
+          uint32_t cc[kMgTup];
+#pragma unroll
+          for (int q = 0; q < kMgTup; ++q) {
+            const uint32_t j = j0 + (uint32_t)(q * kMgLanes);
+            cc[q] = j < e ? dc[j] : 0xFFFFFFFFu;
+          }
+          float part = 0.0f;
+#pragma unroll
+          for (int q = 0; q < kMgTup; ++q)
+            if (cc[q] != 0xFFFFFFFFu) part += H[cc[q]];
+          acc += part;
+        }
 #pragma unroll
         for (int o = kMgLanes / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kMgLanes);
         if (lane == 0) Gs[r] = dloss(loss, acc, y[bt.row_base + r]);
