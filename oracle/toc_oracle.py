@@ -77,116 +77,97 @@ def canonicalize(n_rows, n_cols, rowptr, col, val):
 
 
 # ---------------------------------------------------------------------------
-# Logical encoding: Algorithm 1 (PrefixTreeEncode with LongestMatchFromTree), §3.1.
-# The prefix tree C is kept as one dict mapping (node, key) -> child index: this is
-# the per-node child hash map of §3.1.1 with the node folded into the dict key.
-# AddNode hands out indices from a sequence number; the root is node 0.
+# Logical encoding (§3.1, Algorithm 1), written from its two rules:
+#  * the tree C starts with every distinct pair of the batch as a child of the
+#    root, numbered 1, 2, ... in order of first appearance;
+#  * each tuple is cut greedily into the longest sequences C already holds
+#    (read from the root down); the code of a piece is the node it ends at, and
+#    after every piece that does not end the tuple, C learns that piece followed
+#    by the tuple's next pair as a new node (the next number in turn).
+# C is one dict (node, pair) -> child: §3.1.1's per-node child map with the node
+# folded into the key.
 # ---------------------------------------------------------------------------
-def _longest_match(t, i, children):
-    """LongestMatchFromTree (Alg. 1): greedy longest tree sequence starting at t[i].
-
-    Returns (n, j): the node of the longest match and the next start position.
-    The match has length >= 1 because phase I put every pair under the root.
-    """
-    j = i
-    n_next = children[(0, t[j])]
-    while True:
-        n = n_next
-        j = j + 1
-        if j < len(t):
-            n_next = children.get((n, t[j]), -1)
-        else:
-            n_next = -1
-        if n_next == -1:
-            return n, j
+def _deepest_prefix(children, t, start):
+    """The node of the longest sequence of C that t[start:] begins with, and the
+    position just past it.  Every pair is a child of the root, so the sequence
+    has at least one pair."""
+    node, end = 0, start
+    while end < len(t) and (node, t[end]) in children:
+        node = children[(node, t[end])]
+        end += 1
+    return node, end
 
 
 def encode(rows):
-    """Algorithm 1.  rows -> (I, D, N).
+    """§3.1 encoding.  rows -> (I, D, N).
 
     I: list of (col, bits), the first layer of C in node-index order (nodes 1..|I|).
     D: list (one per row) of lists of node indices.
     N: number of nodes of C including the root (= next sequence number).
     """
     children = {}
-    next_index = 1
     I = []
-    # phase I: every distinct pair becomes a child of the root, first appearance first
     for t in rows:
         for pair in t:
             if (0, pair) not in children:
-                children[(0, pair)] = next_index
-                next_index += 1
                 I.append(pair)
-    # phase II: encode each tuple by greedy longest matches, growing the tree
+                children[(0, pair)] = len(I)
+    n_nodes = len(I) + 1
     D = []
     for t in rows:
-        i = 0
-        codes = []
-        while i < len(t):
-            n, j = _longest_match(t, i, children)
-            codes.append(n)
-            if j < len(t):
-                children[(n, t[j])] = next_index
-                next_index += 1
-            i = j
+        codes, start = [], 0
+        while start < len(t):
+            node, start = _deepest_prefix(children, t, start)
+            codes.append(node)
+            if start < len(t):            # the piece plus the next pair becomes a node
+                children[(node, t[start])] = n_nodes
+                n_nodes += 1
         D.append(codes)
-    return I, D, next_index
+    return I, D, n_nodes
 
 
 # ---------------------------------------------------------------------------
-# Decoding tree C': Algorithm 2 (BuildPrefixTree), §4.1.2, Table 4.
-# Each node keeps its key and its parent; F holds the first pair of each node's
-# sequence.  depth (the length of a node's sequence) is derived alongside:
-# a new node extends its parent's sequence by one pair.
+# Decoding tree C' (§4.1.2, Algorithm 2, Table 4), from the same node-creation
+# rule: node 1..|I| is the root's child with pair I[i-1]; each later node was made
+# when a tuple's code p was followed by a code q, as p's sequence extended by the
+# first pair of q's sequence, so it is p's child with that pair as its key.  Nodes
+# are numbered in creation order, which D replays tuple by tuple, code by code.
+# depth is the length of a node's sequence.
 # ---------------------------------------------------------------------------
 def build_cprime(I, D):
-    """Algorithm 2.  Returns dict with lists parent, key (pairs), depth; index 0 = root."""
-    n_nodes = 1 + len(I) + sum(max(len(d) - 1, 0) for d in D)
-    parent = [None] * n_nodes
-    key = [None] * n_nodes
-    first = [None] * n_nodes
-    depth = [0] * n_nodes
-    # phase I: initialise with I
-    for i in range(1, len(I) + 1):
-        key[i] = I[i - 1]
-        parent[i] = 0
-        first[i] = I[i - 1]
-        depth[i] = 1
-    # phase II: replay the node creations of Algorithm 1 from D
-    idx = len(I) + 1
-    for d in D:
-        for j in range(0, len(d) - 1):
-            parent[idx] = d[j]
-            first[idx] = first[d[j]]
-            key[idx] = first[d[j + 1]]
-            depth[idx] = depth[d[j]] + 1
-            idx += 1
-    assert idx == n_nodes
-    return {"parent": parent, "key": key, "depth": depth, "n_nodes": n_nodes}
+    """Returns dict with lists parent, key (pairs), depth; index 0 = root."""
+    parent, key, depth = [None], [None], [0]
+    first = [None]                        # first pair of each node's sequence
+    for pair in I:
+        parent.append(0)
+        key.append(pair)
+        depth.append(1)
+        first.append(pair)
+    for codes in D:
+        for p, q in zip(codes[:-1], codes[1:]):
+            parent.append(p)
+            depth.append(depth[p] + 1)
+            first.append(first[p])
+            # q may be the node made right here (a tuple repeating its pair): its
+            # first pair is then p's, appended just above
+            key.append(first[q])
+    return {"parent": parent, "key": key, "depth": depth, "n_nodes": len(parent)}
 
 
 # ---------------------------------------------------------------------------
-# Full decode: the backtracking loop of Algorithm 6 (§4.5), without the final
-# densify-and-add-c step.
+# Full decode (§4.5, Algorithm 6 without its densify-and-add-c step): a code
+# stands for the pairs on the path from the root of C' down to it; a tuple is
+# its codes' sequences one after another.  A parent is made before its children,
+# so the sequences fill in index order.
 # ---------------------------------------------------------------------------
 def decode(I, D):
     """(I, D) -> rows of (col, bits) pairs."""
     cp = build_cprime(I, D)
     parent, key = cp["parent"], cp["key"]
-    rows = []
-    for d in D:
-        row = []
-        for code in d:
-            reverse_seq = []
-            node = code
-            while node != 0:
-                reverse_seq.append(key[node])
-                node = parent[node]
-            for q in range(len(reverse_seq) - 1, -1, -1):
-                row.append(reverse_seq[q])
-        rows.append(row)
-    return rows
+    seq = [()] * cp["n_nodes"]
+    for node in range(1, cp["n_nodes"]):
+        seq[node] = seq[parent[node]] + (key[node],)
+    return [[pair for code in d for pair in seq[code]] for d in D]
 
 
 def decoded_to_csr(rows):
@@ -243,8 +224,8 @@ def map_values(I, op, c=1.0):
 
 
 # ---------------------------------------------------------------------------
-# Sparse-unsafe element-wise plus (§4.5, Algorithm 9): decode A fully (the
-# backtracking of Algorithm 6), densify it, and add c to every element, the
+# Sparse-unsafe element-wise plus (§4.5, Algorithm 9): decode A fully (decode
+# above), densify it, and add c to every element, the
 # zeros included.  In binary32: R[i, j] = a_ij + c rounded to binary32.
 # ---------------------------------------------------------------------------
 def dense_plus(rows, n_cols, c=0.0):
@@ -305,42 +286,48 @@ def dense_left(rows, n_cols, G):
 
 
 # ---------------------------------------------------------------------------
-# The TOC algorithms themselves, in fp64 and in the paper's order, used to check
-# Theorems 1 and 2 against the plain products above.
+# The products through C' (Theorems 1 and 2, the content of Algorithms 4, 5, 7
+# and 8), in fp64, used to check those theorems against the plain products above.
+# Both rest on two objects:
+#  * H[n]: node n's sequence applied to W, i.e. the sum of val * W[col] over the
+#    pairs on the path from the root to n; a parent is made before its children,
+#    so H fills in index order from H[parent];
+#  * M: the tuple-by-node count matrix of D (M[i, n] = how often tuple i uses n).
+# Right (Theorem 1): A W = M H.  Left (Theorem 2): a pair of node n's sequence is
+# used by every tuple that uses n or one of n's descendants, so column col(n) of
+# A^T G gains val(n) times the sum of (M^T G) over n and its descendants.
 # ---------------------------------------------------------------------------
+def _occurrences(D, n_nodes):
+    """M as a scipy sparse matrix (duplicates summed)."""
+    rows = [i for i, d in enumerate(D) for _ in d]
+    codes = [c for d in D for c in d]
+    return scipy.sparse.csr_matrix((np.ones(len(codes)), (rows, codes)), shape=(len(D), n_nodes))
+
+
 def toc_right(I, D, W):
-    """Algorithm 4 / Algorithm 7: scan C' forward computing H, then scan D summing H."""
+    """Theorem 1: R = M H."""
     W = np.asarray(W, dtype=np.float64)
-    k = W.shape[1]
     cp = build_cprime(I, D)
     parent, key = cp["parent"], cp["key"]
-    H = np.zeros((cp["n_nodes"], k))
-    for i in range(1, cp["n_nodes"]):
-        c, b = key[i]
-        H[i, :] = bits_f32(b) * W[c, :] + H[parent[i], :]
-    R = np.zeros((len(D), k))
-    for i, d in enumerate(D):
-        for code in d:
-            R[i, :] = R[i, :] + H[code, :]
-    return R
+    H = np.zeros((cp["n_nodes"], W.shape[1]))
+    for n in range(1, cp["n_nodes"]):
+        col, bits = key[n]
+        H[n] = H[parent[n]] + bits_f32(bits) * W[col]
+    return np.asarray(_occurrences(D, cp["n_nodes"]) @ H)
 
 
 def toc_left(I, D, G, n_cols):
-    """Algorithm 5 / Algorithm 8: scan D scattering G rows into H, then scan C'
-    backwards adding key * H[i] into the result and H[i] into H[parent]."""
+    """Theorem 2: out[col(n)] += val(n) * (sum of M^T G over n's subtree)."""
     G = np.asarray(G, dtype=np.float64)
-    k = G.shape[1]
     cp = build_cprime(I, D)
     parent, key = cp["parent"], cp["key"]
-    H = np.zeros((cp["n_nodes"], k))
-    for i, d in enumerate(D):
-        for code in d:
-            H[code, :] = G[i, :] + H[code, :]
-    out = np.zeros((n_cols, k))
-    for i in range(cp["n_nodes"] - 1, 0, -1):
-        c, b = key[i]
-        out[c, :] = out[c, :] + bits_f32(b) * H[i, :]
-        H[parent[i], :] = H[parent[i], :] + H[i, :]
+    sub = np.asarray(_occurrences(D, cp["n_nodes"]).T @ G)
+    for n in range(cp["n_nodes"] - 1, 0, -1):   # children before their parents
+        sub[parent[n]] += sub[n]
+    out = np.zeros((n_cols, G.shape[1]))
+    for n in range(1, cp["n_nodes"]):
+        col, bits = key[n]
+        out[col] += bits_f32(bits) * sub[n]
     return out
 
 
