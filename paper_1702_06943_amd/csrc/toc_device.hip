@@ -2600,46 +2600,27 @@ __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t 
         ahead[a] = j < nd ? dc[j] : 0xFFFFFFFFu;
       }
     }
-    uint32_t c[kDbPer], dd[kDbPer];
-    c[0] = ahead[0];
+    // thread t owns entry es + t of the run: its depth, then an exclusive scan
+    // of the depths in entry order gives its output position
+    uint32_t c = ahead[0];
 #pragma unroll
     for (int a = 1; a < kDbAhead; ++a)
-      if (r_in == (uint32_t)a) c[0] = ahead[a];
-#pragma unroll
-    for (int i = 0; i < kDbPer; ++i) {
-      dd[i] = c[i] == 0xFFFFFFFFu ? 0u : (c[i] < n1 ? 1u : lk[c[i] - n1].y);
-      sh[i * kDbBlock + threadIdx.x] = dd[i];
-    }
-    __syncthreads();
-    // exclusive scan in entry order: thread t owns entries kDbPer*t .. +kDbPer-1
-    uint32_t v[kDbPer], sum = 0;
-#pragma unroll
-    for (int i = 0; i < kDbPer; ++i) {
-      v[i] = sh[kDbPer * threadIdx.x + i];
-      sum += v[i];
-    }
-    const uint32_t incl = wave_incl_scan(sum, lane);
+      if (r_in == (uint32_t)a) c = ahead[a];
+    const uint32_t dd = c == 0xFFFFFFFFu ? 0u : (c < n1 ? 1u : lk[c - n1].y);
+    const uint32_t incl = wave_incl_scan(dd, lane);
     if (lane == kWave - 1) wave_tot[wave] = incl;
     __syncthreads();
-    uint32_t off = 0, total = 0;
-#pragma unroll
-    for (int w = 0; w < kDbWaves; ++w) {
-      off += w < wave ? wave_tot[w] : 0u;
-      total += wave_tot[w];
-    }
-    uint32_t run = off + incl - sum;
-#pragma unroll
-    for (int i = 0; i < kDbPer; ++i) {
-      sh[kDbPer * threadIdx.x + i] = run;
-      run += v[i];
-    }
-    __syncthreads();
+    // the waves' totals: lane w holds wave w's, scanned across the wave
+    const uint32_t wt = lane < kDbWaves ? wave_tot[lane] : 0u;
+    const uint32_t wi = wave_incl_scan(wt, lane);
+    const uint32_t off = (uint32_t)__shfl((int)(wi - wt), wave, kWave);
+    const uint32_t total = (uint32_t)__shfl((int)wi, kDbWaves - 1, kWave);
+    const uint32_t pos = off + incl - dd;
+    sh[threadIdx.x] = pos;
     // each entry writes its sequence backwards, walking to the root in LDS
-#pragma unroll
-    for (int i = 0; i < kDbPer; ++i) {
-      if (c[i] == 0xFFFFFFFFu) continue;
-      uint32_t x = c[i];
-      int64_t p = base + carry + sh[i * kDbBlock + threadIdx.x] + dd[i] - 1;
+    if (c != 0xFFFFFFFFu) {
+      uint32_t x = c;
+      int64_t p = base + carry + pos + dd - 1;
       for (;;) {
         const uint2 kk = kl[x];
         ocol[p] = (int32_t)kk.x;
@@ -2649,6 +2630,9 @@ __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t 
         --p;
       }
     }
+    // every position is in sh, and every wave has read wave_tot (the next run
+    // writes wave_tot before its first barrier and sh only after it)
+    __syncthreads();
     // tuples starting in this run
     for (uint32_t r = threadIdx.x; r <= nr; r += kDbBlock) {
       const uint32_t sr = sp[r];
@@ -2656,7 +2640,6 @@ __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t 
         rowptr[bt.row_base + r] = base + carry + sh[sr - es];
     }
     carry += total;
-    __syncthreads();                                // sh and wave_tot are reused
   }
   // tuples starting at the end of D, and the end mark
   for (uint32_t r = threadIdx.x; r <= nr; r += kDbBlock)
