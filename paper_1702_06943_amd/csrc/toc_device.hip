@@ -2441,7 +2441,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
 // entries' depths inside the run gives every position (and rowptr at row
 // starts), then each entry writes its sequence backwards while walking to the
 // root.  Entries are dealt to threads with stride kDecBlock, so loads and
-// depth-1 stores are coalesced; the scan runs on a transposed copy in LDS.
+// depth-1 stores are coalesced; the scan takes each wave's part of every row of
+// kDecBlock entries, then the row-and-wave totals in one wave.
 // ===========================================================================
 constexpr int kDecBlock = 256;
 constexpr int kDecWaves = kDecBlock / kWave;
@@ -2453,7 +2454,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
                                                            int32_t *__restrict__ ocol,
                                                            uint32_t *__restrict__ oval) {
   __shared__ uint32_t sh[toc::kDecodeTile];
-  __shared__ uint32_t wave_tot[kDecWaves];
+  __shared__ uint32_t wave_tot[kDecPer * kDecWaves];
   // blocks are dealt to the 8 XCDs round-robin; the grid is a multiple of 8 and
   // each XCD gets a contiguous range of runs, so the runs of a batch share its L2
   const int64_t per_xcd = (int64_t)gridDim.x / kXcd;
@@ -2493,30 +2494,24 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
     lk[i] = link_load(rs_link, c[i] < n1 ? 0xFFFFFFFFu : c[i]);
     if (c[i] < n1) lk[i].y = 1u;
   }
-#pragma unroll
-  for (int i = 0; i < kDecPer; ++i) sh[i * kDecBlock + threadIdx.x] = lk[i].y;
-  __syncthreads();
-  // exclusive scan in entry order: thread t owns entries kDecPer*t .. +kDecPer-1
-  uint32_t v[kDecPer], s = 0;
-#pragma unroll
-  for (int i = 0; i < kDecPer; ++i) {
-    v[i] = sh[kDecPer * threadIdx.x + i];
-    s += v[i];
-  }
-  const uint32_t incl = wave_incl_scan(s, lane);
-  if (lane == kWave - 1) wave_tot[wave] = incl;
-  __syncthreads();
-  uint32_t off = 0, total = 0;
-#pragma unroll
-  for (int w = 0; w < kDecWaves; ++w) {
-    off += w < wave ? wave_tot[w] : 0u;
-    total += wave_tot[w];
-  }
-  uint32_t run = off + incl - s;
+  // exclusive scan of the depths in entry order: entry i * kDecBlock + t is row
+  // i, position t; each wave scans its 64 positions of every row, then the
+  // (row, wave) totals, in entry order, are scanned across one wave
+  uint32_t incl[kDecPer];
 #pragma unroll
   for (int i = 0; i < kDecPer; ++i) {
-    sh[kDecPer * threadIdx.x + i] = run;
-    run += v[i];
+    incl[i] = wave_incl_scan(lk[i].y, lane);
+    if (lane == kWave - 1) wave_tot[i * kDecWaves + wave] = incl[i];
+  }
+  __syncthreads();
+  const uint32_t wt = lane < kDecPer * kDecWaves ? wave_tot[lane] : 0u;
+  const uint32_t wi = wave_incl_scan(wt, lane);
+  const uint32_t total = (uint32_t)__shfl((int)wi, kDecPer * kDecWaves - 1, kWave);
+  uint32_t pos[kDecPer];
+#pragma unroll
+  for (int i = 0; i < kDecPer; ++i) {
+    pos[i] = (uint32_t)__shfl((int)(wi - wt), i * kDecWaves + wave, kWave) + incl[i] - lk[i].y;
+    sh[i * kDecBlock + threadIdx.x] = pos[i];
   }
   __syncthreads();
 #pragma unroll
@@ -2526,7 +2521,7 @@ __global__ __launch_bounds__(kDecBlock) void decode_kernel(Img im, const uint4 *
       uint2 kk = kv[i];
       uint32_t par = lk[i].x;
       const uint32_t d = lk[i].y;
-      int64_t p = base + sh[i * kDecBlock + threadIdx.x] + d - 1;
+      int64_t p = base + pos[i] + d - 1;
       for (uint32_t q = 0;;) {
         // ordinary stores: L2 merges the chains' partial lines (streaming stores
         // measured 1.9x slower on the categorical workload's deeper chains)
