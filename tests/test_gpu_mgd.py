@@ -41,6 +41,18 @@ def mixed_set():
     return Batches.concat(parts)
 
 
+def long_set():
+    """Batches whose tuples run to several hundred codes: each lane of a tuple's
+    8-lane group takes its codes in chunks of 24, so these take 2 to 5 chunks (the
+    image-like batches never take a second); the second has deep codes."""
+    parts = []
+    for i, spec in enumerate([dict(n_rows=40, density=0.5, n_values=30),
+                              dict(n_rows=20, density=0.9, n_values=4, prefix_copy=0.5)]):
+        rp, c, v = tiny_batch(91 + i, n_cols=900, **spec)
+        parts.append(Batches(900, [spec["n_rows"]], rp, c, v))
+    return Batches.concat(parts)
+
+
 def check_step(B, b, h_before, h_after, y, loss, lr):
     n, rp, c, v = B.batch(b)
     rows = O.canonicalize(n, B.n_cols, rp, c, v)
@@ -64,10 +76,10 @@ def check_step(B, b, h_before, h_after, y, loss, lr):
 
 
 @pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
-@pytest.mark.parametrize("which", ["mixed", "c3", "c2"])
+@pytest.mark.parametrize("which", ["mixed", "c3", "c2", "long"])
 def test_each_step_against_oracle(loss, which):
     B = {"mixed": mixed_set, "c3": lambda: config_batches("c3", 4, 3),
-         "c2": lambda: config_batches("c2", 1, 2)}[which]()
+         "c2": lambda: config_batches("c2", 1, 2), "long": long_set}[which]()
     dev = upload(B)
     y = labels(B, loss, 7 + loss)
     yd = torch.from_numpy(y).to(DEV)
@@ -87,7 +99,7 @@ def test_each_step_against_oracle(loss, which):
 
 @pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
 def test_one_launch_equals_steps(loss):
-    B = Batches.concat([config_batches("c5", 20, 40), mixed_set()])
+    B = Batches.concat([config_batches("c5", 20, 40), mixed_set(), long_set()])
     dev = upload(B)
     y = torch.from_numpy(labels(B, loss, 3)).to(DEV)
     h0 = (np.random.default_rng(5).standard_normal(B.n_cols) * 0.05).astype(np.float32)
