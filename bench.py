@@ -759,8 +759,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see DESIGN.md for how the batches would shard).", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: there is no multi-GPU path (batches are "
+              "independent, so each GPU would take a contiguous range of them with W "
+              "replicated).", file=sys.stderr)
         sys.exit(2)
 
     from workloads import CONFIGS
