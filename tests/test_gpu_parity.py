@@ -337,6 +337,40 @@ def test_decode_batch_of_many_runs():
     check_against_oracle(B, res, W=W, G=G)
 
 
+def _one_pair_rows(lengths, n_cols, n_values, offset=0):
+    """A batch whose rows hold one pair each (or none, where lengths has 0), so
+    that its D has exactly one entry per non-empty row; pair i is column
+    i % n_cols with value 1 + (i // n_cols) % n_values."""
+    lengths = np.asarray(lengths, np.int64)
+    rp = np.concatenate([[0], np.cumsum(lengths)])
+    i = np.arange(int(rp[-1])) + offset
+    c = (i % n_cols).astype(np.int32)
+    v = (1 + (i // n_cols) % n_values).astype(np.float32)
+    return len(lengths), rp, c, v
+
+
+def test_decode_runs_of_exact_length():
+    """D of 2,048, 8,192 and 8,193 entries (whole runs of 1,024, a whole group of
+    eight runs, one entry past it), with empty tuples starting at a run boundary
+    and at the end of D, through the batch decode; then 9,216 distinct pairs
+    (keys beyond the batch decode's LDS) through the CSR decode."""
+    few = [_one_pair_rows([1] * 1024 + [0] * 3 + [1] * 1024 + [0] * 2, 6, 2),
+           _one_pair_rows([1] * 8192, 6, 2),
+           _one_pair_rows([0] + [1] * 8193, 6, 2)]
+    B = _batches_from_csrs(few, 6)
+    rng = np.random.default_rng(13)
+    W = rng.standard_normal((6, 1)).astype(np.float32)
+    G = rng.standard_normal((int(B.n_rows.sum()), 1)).astype(np.float32)
+    check_against_oracle(B, run_gpu(B, W=W, G=G), W=W, G=G)
+    many = [_one_pair_rows([1] * 4096 + [0] + [1] * 5120 + [0], 96, 96)]
+    B = _batches_from_csrs(many, 96)
+    encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
+    assert 8 * T.toc_enc_info_get(encs[0])["n_live"] > 64 * 1024   # keys beyond 64 KiB
+    W = rng.standard_normal((96, 1)).astype(np.float32)
+    G = rng.standard_normal((int(B.n_rows.sum()), 1)).astype(np.float32)
+    check_against_oracle(B, run_gpu(B, W=W, G=G), W=W, G=G)
+
+
 def test_many_batches():
     csrs = []
     for i in range(2500):
