@@ -124,6 +124,26 @@ __global__ __launch_bounds__(kNnBlock) void mlp_fwd1_kernel(NnImg im, int64_t b,
 // gradient of the mean loss back to dZ1: every quantity here belongs to one tuple,
 // so workgroups split the tuples.  H2, dZ2 and dZ3 go to the workspace for the
 // weight gradients, dZ1 for the first layer's left product.
+// n floats src(x) into LDS dst[x] by a workgroup of NT threads, each with kStagePer
+// loads in flight before its stores (one load latency per pass, not per element)
+constexpr int kStagePer = 8;
+template <int NT, typename F>
+__device__ inline void stage(float *dst, int n, F src) {
+  for (int x0 = threadIdx.x; x0 < n; x0 += kStagePer * NT) {
+    float t[kStagePer];
+#pragma unroll
+    for (int k = 0; k < kStagePer; ++k) {
+      const int x = x0 + k * NT;
+      t[k] = x < n ? src(x) : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < kStagePer; ++k) {
+      const int x = x0 + k * NT;
+      if (x < n) dst[x] = t[k];
+    }
+  }
+}
+
 template <bool kWlds>
 __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
     int n, int R, int64_t row_base, const float *__restrict__ act1, int h1, int h2, int C,
@@ -139,11 +159,10 @@ __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
   float *W2s = Z + R * C, *W3s = W2s + h1 * h2;
   const float *W2 = kWlds ? W2s : W2g, *W3 = kWlds ? W3s : W3g;
   const int i0 = R * blockIdx.x, nr = min(R, n - i0);
-  for (int idx = threadIdx.x; idx < nr * h1; idx += kNnBlock)
-    A[idx] = act1[(int64_t)i0 * h1 + idx];
+  stage<kNnBlock>(A, nr * h1, [&](int x) { return act1[(int64_t)i0 * h1 + x]; });
   if (kWlds) {
-    for (int idx = threadIdx.x; idx < h1 * h2; idx += kNnBlock) W2s[idx] = W2g[idx];
-    for (int idx = threadIdx.x; idx < h2 * C; idx += kNnBlock) W3s[idx] = W3g[idx];
+    stage<kNnBlock>(W2s, h1 * h2, [&](int x) { return W2g[x]; });
+    stage<kNnBlock>(W3s, h2 * C, [&](int x) { return W3g[x]; });
   }
   __syncthreads();
   for (int idx = threadIdx.x; idx < nr * h2; idx += kNnBlock) {
@@ -210,6 +229,7 @@ __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
 // H1 and dZ2 staged in LDS (the blocks of W2's first rows also sum b2's gradient);
 // the workgroups after them take 256 entries each of W3 and b3.  Runs after every
 // tuple's dZ1 was computed from the old W2.
+
 __global__ __launch_bounds__(256) void mlp_grad_kernel(
     int n, int n_w2, const float *__restrict__ act1, int h1, int h2, int C,
     const float *__restrict__ H2g, const float *__restrict__ dZ2g, const float *__restrict__ dZ3g,
@@ -225,14 +245,14 @@ __global__ __launch_bounds__(256) void mlp_grad_kernel(
     float g = 0.0f, gb = 0.0f;                  // gb: b2's gradient, by the first row of blocks
     for (int i0 = 0; i0 < n; i0 += 64) {
       const int ni = min(64, n - i0);
-      for (int x = threadIdx.x; x < ni * V; x += 256) {
+      stage<256>(As, ni * V, [&](int x) {
         const int ii = x / V, vv = v0 + (x - ii * V);
-        As[x] = vv < h1 ? act1[(int64_t)(i0 + ii) * h1 + vv] : 0.0f;
-      }
-      for (int x = threadIdx.x; x < ni * U; x += 256) {
+        return vv < h1 ? act1[(int64_t)(i0 + ii) * h1 + vv] : 0.0f;
+      });
+      stage<256>(Gs, ni * U, [&](int x) {
         const int ii = x / U, uu = u0 + (x - ii * U);
-        Gs[x] = uu < h2 ? dZ2g[(int64_t)(i0 + ii) * h2 + uu] : 0.0f;
-      }
+        return uu < h2 ? dZ2g[(int64_t)(i0 + ii) * h2 + uu] : 0.0f;
+      });
       __syncthreads();
       if (lv < V)
         for (int ii = 0; ii < ni; ++ii) g = fmaf(As[ii * V + lv], Gs[ii * U + lu], g);
@@ -253,8 +273,8 @@ __global__ __launch_bounds__(256) void mlp_grad_kernel(
     float g = 0.0f;
     for (int i0 = 0; i0 < n; i0 += TI) {
       const int ni = min(TI, n - i0);
-      for (int x = threadIdx.x; x < ni * h2; x += 256) Hs[x] = H2g[(int64_t)i0 * h2 + x];
-      for (int x = threadIdx.x; x < ni * C; x += 256) Zs[x] = dZ3g[(int64_t)i0 * C + x];
+      stage<256>(Hs, ni * h2, [&](int x) { return H2g[(int64_t)i0 * h2 + x]; });
+      stage<256>(Zs, ni * C, [&](int x) { return dZ3g[(int64_t)i0 * C + x]; });
       __syncthreads();
       if (idx < n_out3)
         for (int ii = 0; ii < ni; ++ii) g = fmaf(u < h2 ? Hs[ii * h2 + u] : 1.0f, Zs[ii * C + c], g);
