@@ -24,6 +24,7 @@ namespace {
 
 constexpr int kNnBlock = 1024;
 constexpr int kNnLanes = 16;                 // lanes per tuple in the forward product
+constexpr int kNnCodes = 8;                  // a lane's codes whose loads fly together there
 constexpr uint32_t kNnFirst = 0x80000000u;   // first-occurrence bit of a leaf occurrence
 constexpr size_t kNnLdsMax = 160 * 1024;
 constexpr int kColGroups = 8;                // workgroups sharing a slice's key columns
@@ -97,13 +98,29 @@ __global__ __launch_bounds__(kNnBlock) void mlp_fwd1_kernel(NnImg im, int64_t b,
   if (r < bt.n_rows) {
     const uint32_t s = span[r], e = span[r + 1];
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (uint32_t j = s + lane; j < e; j += kNnLanes) {
-      const uint32_t c = dc[j];
-      if (c < n1) {
-        const toc_key k = key[c];
-        acc = fma4(k.val, wrow(k.col), acc);
-      } else {
-        acc = add4(acc, Hd[c - n1]);
+    // kNnCodes of the lane's codes at a time: their codes, then their keys, then
+    // their rows are loaded together, and summed in order
+    for (uint32_t j0 = s + lane; j0 < e; j0 += kNnLanes * kNnCodes) {
+      uint32_t c[kNnCodes];
+      toc_key k[kNnCodes];
+      float4 w[kNnCodes];
+#pragma unroll
+      for (int q = 0; q < kNnCodes; ++q) {
+        const uint32_t j = j0 + (uint32_t)(q * kNnLanes);
+        c[q] = j < e ? dc[j] : 0xFFFFFFFFu;
+      }
+#pragma unroll
+      for (int q = 0; q < kNnCodes; ++q) k[q] = c[q] < n1 ? key[c[q]] : toc_key{0u, 0.0f};
+#pragma unroll
+      for (int q = 0; q < kNnCodes; ++q) {
+        w[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (c[q] < n1) w[q] = wrow(k[q].col);
+        else if (c[q] != 0xFFFFFFFFu) w[q] = Hd[c[q] - n1];
+      }
+#pragma unroll
+      for (int q = 0; q < kNnCodes; ++q) {
+        if (c[q] < n1) acc = fma4(k[q].val, w[q], acc);
+        else if (c[q] != 0xFFFFFFFFu) acc = add4(acc, w[q]);
       }
     }
 #pragma unroll
