@@ -2556,6 +2556,7 @@ constexpr int kDbBlock = 1024;                    // 16 waves: two or more workg
 constexpr int kDbWaves = kDbBlock / kWave;
 constexpr int kDbPer = (int)toc::kDecodeTile / kDbBlock;   // 1
 constexpr int kDbAhead = 8;                       // runs whose codes are loaded together
+constexpr int kDbCopy = 4;                        // keys, links and tuple starts per thread in flight
 static_assert(kDbPer == 1, "one entry per thread and run");
 
 __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t b0,
@@ -2576,9 +2577,27 @@ __global__ __launch_bounds__(kDbBlock) void decode_batch_kernel(Img im, int64_t 
   const uint2 *link = (const uint2 *)(im.link + bt.deep_base);
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
-  for (uint32_t i = threadIdx.x; i < nc; i += kDbBlock) kl[i] = key[i];
-  for (uint32_t i = threadIdx.x; i < nc - n1; i += kDbBlock) lk[i] = link[i];
-  for (uint32_t r = threadIdx.x; r <= nr; r += kDbBlock) sp[r] = span[r];
+  // keys, deep links and tuple starts into LDS: a thread's loads of a pass (up to
+  // kDbCopy of each) are all issued before its stores
+  const uint32_t nlk = nc - n1;
+  for (uint32_t i0 = threadIdx.x; i0 < nc || i0 < nlk || i0 <= nr; i0 += kDbCopy * kDbBlock) {
+    uint2 kt[kDbCopy], lt[kDbCopy];
+    uint32_t st[kDbCopy];
+#pragma unroll
+    for (int q = 0; q < kDbCopy; ++q) {
+      const uint32_t i = i0 + (uint32_t)(q * kDbBlock);
+      kt[q] = i < nc ? key[i] : make_uint2(0u, 0u);
+      lt[q] = i < nlk ? link[i] : make_uint2(0u, 0u);
+      st[q] = i <= nr ? span[i] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < kDbCopy; ++q) {
+      const uint32_t i = i0 + (uint32_t)(q * kDbBlock);
+      if (i < nc) kl[i] = kt[q];
+      if (i < nlk) lk[i] = lt[q];
+      if (i <= nr) sp[i] = st[q];
+    }
+  }
   __syncthreads();
   const int lane = threadIdx.x % kWave, wave = wave_id();
   const int64_t base = bt.nnz_base;
