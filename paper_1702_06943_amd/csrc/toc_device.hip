@@ -1894,6 +1894,7 @@ constexpr uint32_t lt_rows_offset(int64_t m, int64_t max_tree, bool toc, int64_t
                     ~(int64_t)15);
 }
 constexpr int kLtOcr = 1024;   // LDS words for a batch's tree-row occurrences
+constexpr int kLtCopy = 4;     // children (and occurrence) offsets per thread in flight
 
 struct LtChunk {
   int cg;           // column group (columns GPW*cg .. GPW*cg+GPW-1); >= n_cg: none
@@ -2019,9 +2020,23 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
       const uint4 *src = (const uint4 *)(cols_all + b * 4 * (int64_t)(m + 1));
       for (int e = threadIdx.x; e < m + 1; e += kLtBlock) ((uint4 *)Loff)[e] = src[e];
       const uint32_t *tch = tchild_all + bt.tree_base + b;
-      for (uint32_t h = threadIdx.x; h <= n_tree; h += kLtBlock) {
-        Coff[h] = tch[h];
-        if (toc_lds) Toc[h] = to[h];
+      // (a thread's loads of a pass, up to kLtCopy of each table, before its stores)
+      for (uint32_t h0 = threadIdx.x; h0 <= n_tree; h0 += kLtCopy * kLtBlock) {
+        uint32_t ct[kLtCopy], ot[kLtCopy];
+#pragma unroll
+        for (int q = 0; q < kLtCopy; ++q) {
+          const uint32_t h = h0 + (uint32_t)(q * kLtBlock);
+          ct[q] = h <= n_tree ? tch[h] : 0u;
+          ot[q] = toc_lds && h <= n_tree ? to[h] : 0u;
+        }
+#pragma unroll
+        for (int q = 0; q < kLtCopy; ++q) {
+          const uint32_t h = h0 + (uint32_t)(q * kLtBlock);
+          if (h <= n_tree) {
+            Coff[h] = ct[q];
+            if (toc_lds) Toc[h] = ot[q];
+          }
+        }
       }
       if (use_ocr)
         for (uint32_t t = threadIdx.x; t < n_p3; t += kLtBlock) Ocr[t] = orow[p3 + t];
