@@ -2706,6 +2706,7 @@ __global__ __launch_bounds__(kMapBlock) void map_values_kernel(toc_key *__restri
 // ===========================================================================
 constexpr int kDnBlock = 1024;
 constexpr int kDnWaves = kDnBlock / kWave;
+constexpr int kDnPer = 4;        // a lane's entries of a tuple whose loads fly together
 
 template <bool ROW_LDS>
 __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t b0, int m,
@@ -2721,23 +2722,51 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
   const uint32_t *span = im.span + bt.span_base;
   const uint32_t *dc = im.dcodes + bt.d_base;
   const uint32_t n1 = (uint32_t)bt.n_lvl1;
-  // the pairs of the tuple r into row (LDS or HBM)
+  // the wave's tuples' starts and ends, one tuple per lane (tuple wave + 16 i in
+  // lane i), loaded once
+  const int nrows = bt.n_rows;
+  uint32_t ps = 0u, pe = 0u;
+  {
+    const int rl = wave + kDnWaves * lane;
+    if (rl < nrows) {
+      ps = span[rl];
+      pe = span[rl + 1];
+    }
+  }
+  // the pairs of the tuple r into row (LDS or HBM): kDnPer of a lane's entries at
+  // a time, their codes and then their keys loaded together; deeper codes walk
+  // the rest of their chain to the root
   auto scatter = [&](int r, float *row) {
-    const uint32_t e = span[r + 1];
-    for (uint32_t j = span[r] + lane; j < e; j += kWave) {
-      uint32_t x = dc[j];
-      for (;;) {
-        const toc_key k = key[x];
-        row[k.col] = k.val + c;
-        if (x < n1) break;   // depth 1: the chain's first pair
-        x = link[x].parent;
+    const int i = (r - wave) / kDnWaves;
+    const uint32_t s0 = i < kWave ? (uint32_t)__shfl((int)ps, i, kWave) : span[r];
+    const uint32_t e = i < kWave ? (uint32_t)__shfl((int)pe, i, kWave) : span[r + 1];
+    for (uint32_t j0 = s0 + lane; j0 < e; j0 += kWave * kDnPer) {
+      uint32_t x[kDnPer];
+      toc_key kk[kDnPer];
+#pragma unroll
+      for (int q = 0; q < kDnPer; ++q) {
+        const uint32_t j = j0 + (uint32_t)(q * kWave);
+        x[q] = j < e ? dc[j] : 0xFFFFFFFFu;
+      }
+#pragma unroll
+      for (int q = 0; q < kDnPer; ++q) kk[q] = x[q] != 0xFFFFFFFFu ? key[x[q]] : toc_key{0u, 0.0f};
+#pragma unroll
+      for (int q = 0; q < kDnPer; ++q) {
+        if (x[q] == 0xFFFFFFFFu) continue;
+        row[kk[q].col] = kk[q].val + c;
+        uint32_t xx = x[q];
+        while (xx >= n1) {   // depth 1 ends the chain
+          xx = link[xx].parent;
+          const toc_key k = key[xx];
+          row[k.col] = k.val + c;
+        }
       }
     }
   };
   if constexpr (ROW_LDS) {
     float *row = dn_rows + (size_t)wave * m;
     const bool vec = (m % 4) == 0 && (lda % 4) == 0 && (((uintptr_t)A) & 15u) == 0;
-    for (int r = wave; r < bt.n_rows; r += kDnWaves) {
+    for (int r = wave; r < nrows; r += kDnWaves) {
       for (int j = lane; j < m; j += kWave) row[j] = c;
       __builtin_amdgcn_wave_barrier();
       scatter(r, row);
@@ -2762,7 +2791,7 @@ __global__ __launch_bounds__(kDnBlock) void decode_dense_kernel(Img im, int64_t 
     }
     __threadfence();
     __syncthreads();
-    for (int r = wave; r < bt.n_rows; r += kDnWaves) scatter(r, Ab + (int64_t)r * lda);
+    for (int r = wave; r < nrows; r += kDnWaves) scatter(r, Ab + (int64_t)r * lda);
   }
 }
 
