@@ -576,6 +576,30 @@ toc_status toc_ingest_build(toc_dev *dev, const void *blobs, const int64_t *blob
 toc_status toc_mgd_epoch(const toc_dev *dev, int64_t b0, int64_t n_batches, int32_t loss,
                          float lr, const float *y, float *h, void *stream);
 
+/* Device workspace bytes toc_mgd_epoch_split needs for the image in *bytes: one
+ * float per row of its largest batch (a step's loss derivatives g).
+ * TOC_EINVAL for NULL arguments.                                                */
+toc_status toc_mgd_workspace_size(const toc_dev *dev, size_t *bytes);
+
+/* The steps of toc_mgd_epoch (section 2.1: the right product of Theorem 1, g,
+ * the left product of Theorem 2, the update) with each step split over many
+ * workgroups: two launches per step on stream, in batch order.  The first sums
+ * each tuple's r = x^T h over the pairs of its codes and writes g_i = d loss / d r
+ * to ws; the second forms each tree code's sum of g (its own tuples, then its
+ * children's sums) and, column by column over the batch's used columns, the
+ * gradient (val * g over the column's leaf occurrences, val * sum over its tree
+ * codes) and h_j -= lr / |B| * gradient.  y, h, loss, lr and the errors as for
+ * toc_mgd_epoch; ws is caller-owned device memory of at least the bytes
+ * toc_mgd_workspace_size gives (TOC_EINVAL if NULL, TOC_ESIZE if smaller), which
+ * calls on other streams must not share while this call runs.  Needs
+ * 4 (max rows + max tree codes of a batch + 1) bytes of LDS, at most 160 KiB
+ * (TOC_EUNSUPPORTED beyond).  The sums run in a fixed order: one call over many
+ * batches equals one call per batch, bit for bit (the order differs from
+ * toc_mgd_epoch's, so the two agree within rounding, not bit for bit).          */
+toc_status toc_mgd_epoch_split(const toc_dev *dev, int64_t b0, int64_t n_batches, int32_t loss,
+                               float lr, const float *y, float *h, void *ws, size_t ws_bytes,
+                               void *stream);
+
 /* ---------------------------------------------------------------------------
  * Mini-batch gradient descent for the neural network of section 5.1 (Table 1's
  * NN row, whose matrix operations are A.M and M.A): layers m -> h1 -> h2 ->

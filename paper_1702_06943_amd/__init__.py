@@ -25,7 +25,8 @@ from .binding import (  # noqa: F401
     TOC_LEVEL_LIVE,
     toc_level_workspace_size, toc_level_build, toc_level_right_mul,
     toc_enc_pack, toc_phys_info_get, toc_cprime_workspace_size, toc_cprime_build,
-    TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE, toc_mgd_epoch,
+    TOC_MGD_LINEAR, TOC_MGD_LOGISTIC, TOC_MGD_HINGE, toc_mgd_epoch, toc_mgd_workspace_size,
+    toc_mgd_epoch_split,
     TOC_ENCDEV_ROWPTR, TOC_ENCDEV_SIZE, TOC_ENCDEV_COLUMN, TOC_ENCDEV_VALUE,
     toc_encode_device_workspace_size, toc_encode_device,
     toc_mlp_workspace_size, toc_mlp_epoch,

@@ -120,6 +120,8 @@ def lib():
         "toc_cprime_workspace_size": [I64, I64, P],
         "toc_cprime_build": [P, P, P, I64, I32, I32, P, P, P, P, P, P, SZ, P],
         "toc_mgd_epoch": [P, I64, I64, I32, C.c_float, P, P, P],
+        "toc_mgd_workspace_size": [P, P],
+        "toc_mgd_epoch_split": [P, I64, I64, I32, C.c_float, P, P, P, SZ, P],
         "toc_encode_device_workspace_size": [I64, I64, P],
         "toc_mlp_workspace_size": [P, I32, I32, I32, P],
         "toc_level_workspace_size": [I64, I64, P],
@@ -453,6 +455,28 @@ def toc_mgd_epoch(dev, y, h, loss, lr, b0=0, n_batches=None, stream=None):
         raise TocError(TOC_EINVAL, "h must hold n_cols float32")
     _check(lib().toc_mgd_epoch(dev.handle, int(b0), int(n_batches), int(loss), float(lr),
                                _ptr(y), _ptr(h), _stream(stream)))
+
+
+def toc_mgd_workspace_size(dev):
+    """Device workspace bytes toc_mgd_epoch_split needs for this image."""
+    n = C.c_size_t()
+    _check(lib().toc_mgd_workspace_size(dev.handle, C.byref(n)))
+    return n.value
+
+
+def toc_mgd_epoch_split(dev, y, h, loss, lr, ws, b0=0, n_batches=None, stream=None):
+    """toc_mgd_epoch's steps, each split over many workgroups; ws: a device uint8
+    tensor of at least toc_mgd_workspace_size(dev) bytes."""
+    info = toc_dev_info_get(dev)
+    if n_batches is None:
+        n_batches = info["n_batches"] - b0
+    if y.numel() < info["n_rows"] or y.element_size() != 4:
+        raise TocError(TOC_EINVAL, "y must hold one float32 per row")
+    if h.numel() != info["n_cols"] or h.element_size() != 4:
+        raise TocError(TOC_EINVAL, "h must hold n_cols float32")
+    _check(lib().toc_mgd_epoch_split(dev.handle, int(b0), int(n_batches), int(loss), float(lr),
+                                     _ptr(y), _ptr(h), _ptr(ws), ws.numel() * ws.element_size(),
+                                     _stream(stream)))
 
 
 def toc_encode_device_workspace_size(n_batches, max_nnz):

@@ -243,15 +243,204 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
     for (int j = threadIdx.x; j < m; j += kMgBlock) hg[j] = h[j];
 }
 
+// ---------------------------------------------------------------------------
+// The same steps split over many workgroups, two launches per step (the stream
+// orders them: a step's update is seen by the next step's forward pass):
+//  * mgds_fwd_kernel: a 16-lane group per tuple sums val * h[col] over the pairs
+//    of its codes (a deeper code walks its chain to the root: its sequence's
+//    pairs), kMsCodes of a lane's codes and then their keys loaded together, and
+//    writes the tuple's loss derivative g to the workspace; the model is staged in
+//    LDS when the matrix has at most kMsHlds columns;
+//  * mgds_bwd_kernel: every workgroup stages g, sums each tree code's own
+//    occurrences (its tree row) and adds children into parents deepest level
+//    first in LDS, then takes kMsColPasses x 16 of the batch's used columns (a
+//    16-lane group per column): the gradient of column j sums val * g over its
+//    leaf occurrences and val * (tree row) over its tree codes, the multipliers
+//    beside the entries, and h_j -= lr / |B| * gradient.
+// Every sum has a fixed order, so one call over many batches equals the batches
+// one call each, bit for bit.
+// ---------------------------------------------------------------------------
+constexpr int kMsBlock = 256;
+constexpr int kMsLanes = 16;                   // lanes per tuple or column
+constexpr int kMsGroups = kMsBlock / kMsLanes;
+constexpr int kMsCodes = 8;                    // a lane's codes (or entries) loaded together
+constexpr int kMsHlds = 8192;                  // most columns whose model the forward pass stages
+constexpr int kMsColPasses = 4;                // column passes of a backward workgroup
+constexpr uint32_t kMsNone = 0xFFFFFFFFu;
+
+template <bool HLDS>
+__global__ __launch_bounds__(kMsBlock) void mgds_fwd_kernel(MgImg im, int64_t b, int32_t m, int loss,
+                                                            const float *__restrict__ y,
+                                                            const float *__restrict__ hg,
+                                                            float *__restrict__ g) {
+  __shared__ float hs[HLDS ? kMsHlds : 1];
+  const toc_batch bt = im.batches[b];
+  if (HLDS) {
+    for (int j0 = threadIdx.x; j0 < m; j0 += kMsCodes * kMsBlock) {
+      float t[kMsCodes];
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) {
+        const int j = j0 + q * kMsBlock;
+        t[q] = j < m ? hg[j] : 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) {
+        const int j = j0 + q * kMsBlock;
+        if (j < m) hs[j] = t[q];
+      }
+    }
+    __syncthreads();
+  }
+  const float *h = HLDS ? hs : hg;
+  const int lane = threadIdx.x % kMsLanes, grp = threadIdx.x / kMsLanes;
+  const int r = (int)blockIdx.x * kMsGroups + grp;
+  const uint32_t n1 = (uint32_t)bt.n_lvl1;
+  const toc_key *key = im.key + bt.code_base;
+  const toc_link *link = im.link + (bt.deep_base - (int64_t)bt.n_lvl1);   // depth >= 2 only
+  float acc = 0.0f;
+  if (r < bt.n_rows) {
+    const uint32_t *span = im.span + bt.span_base;
+    const uint32_t *dc = im.dcodes + bt.d_base;
+    const uint32_t s = span[r], e = span[r + 1];
+    for (uint32_t j0 = s + lane; j0 < e; j0 += kMsLanes * kMsCodes) {
+      uint32_t c[kMsCodes];
+      toc_key k[kMsCodes];
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) {
+        const uint32_t j = j0 + (uint32_t)(q * kMsLanes);
+        c[q] = j < e ? dc[j] : kMsNone;
+      }
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) k[q] = c[q] != kMsNone ? key[c[q]] : toc_key{0u, 0.0f};
+      float part = 0.0f;
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) {
+        if (c[q] == kMsNone) continue;
+        float v = k[q].val * h[k[q].col];
+        for (uint32_t x = c[q]; x >= n1;) {        // a deeper code: the rest of its chain
+          x = link[x].parent;
+          const toc_key kp = key[x];
+          v = fmaf(kp.val, h[kp.col], v);
+        }
+        part += v;
+      }
+      acc += part;
+    }
+  }
+#pragma unroll
+  for (int o = kMsLanes / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o, kMsLanes);
+  if (r < bt.n_rows && lane == 0) g[r] = dloss(loss, acc, y[bt.row_base + r]);
+}
+
+__global__ __launch_bounds__(kMsBlock) void mgds_bwd_kernel(MgImg im, int64_t b, int32_t m,
+                                                            int32_t max_rows, float lr,
+                                                            const float *__restrict__ g,
+                                                            float *__restrict__ h) {
+  extern __shared__ float sm[];
+  float *Gs = sm;                  // per tuple: d loss / d r
+  float *Ht = sm + max_rows;       // per tree row (tree code c: row c < ni ? c : c - n1 + ni)
+  const toc_batch bt = im.batches[b];
+  const int nr = bt.n_rows;
+  const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
+  const uint32_t n_tree = ni + (nc - n1);
+  for (int r0 = threadIdx.x; r0 < nr; r0 += kMsCodes * kMsBlock) {
+    float t[kMsCodes];
+#pragma unroll
+    for (int q = 0; q < kMsCodes; ++q) {
+      const int r = r0 + q * kMsBlock;
+      t[q] = r < nr ? g[r] : 0.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < kMsCodes; ++q) {
+      const int r = r0 + q * kMsBlock;
+      if (r < nr) Gs[r] = t[q];
+    }
+  }
+  __syncthreads();
+  // tree rows: the gradients of the tuples holding the code, then the children's
+  // rows added into their parents, deepest level first
+  const uint32_t *to = im.occ_off + bt.code_base + 2 * b + (n1 - ni) + 1;
+  const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
+  const uint32_t *cv = im.cval + bt.d_base + bt.tree_base;
+  for (uint32_t t = threadIdx.x; t < n_tree; t += kMsBlock) {
+    const uint32_t o1 = to[t + 1];
+    float s = 0.0f;
+#pragma unroll 4
+    for (uint32_t o = to[t]; o < o1; ++o) s += Gs[ce[o] & ~kMgFirst];
+    Ht[t] = s;
+  }
+  __syncthreads();
+  const uint32_t *lvl = im.level + bt.lvl_base;
+  const uint32_t *tch = im.tchild + bt.tree_base + b;
+  for (int d = bt.n_levels - 1; d >= 1; --d) {
+    const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
+    for (uint32_t c = a + threadIdx.x; c < e; c += kMsBlock) {
+      const uint32_t t = c < ni ? c : c - n1 + ni;
+      float s = Ht[t];
+      const uint32_t c1 = tch[t + 1];
+      for (uint32_t ch = tch[t]; ch < c1; ++ch) s += Ht[ch - n1 + ni];
+      Ht[t] = s;
+    }
+    __syncthreads();
+  }
+  // this workgroup's used columns
+  const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
+  const uint32_t *Ost = cx + (m + 1), *Toff = cx + 2 * (m + 1), *Ord = cx + 3 * (m + 1);
+  const uint32_t n_lo = Ost[m];      // leaf occurrences; the tree entries follow them
+  const int n_used = bt.n_ucols;
+  const float step = lr / (float)nr;
+  const int lane = threadIdx.x % kMsLanes, grp = threadIdx.x / kMsLanes;
+  for (int pass = 0; pass < kMsColPasses; ++pass) {
+    const int u = ((int)blockIdx.x * kMsColPasses + pass) * kMsGroups + grp;
+    uint32_t j = 0, lst = 0, tst = 0, nl = 0, nt = 0;
+    if (u < n_used) {
+      j = Ord[u];
+      lst = Ost[j];
+      nl = Ost[j + 1] - lst;
+      tst = n_lo + Toff[j];
+      nt = Toff[j + 1] - Toff[j];
+    }
+    float s = 0.0f;
+    for (uint32_t q0 = lane; q0 < nl + nt; q0 += kMsLanes * kMsCodes) {
+      uint32_t w[kMsCodes];
+      float v[kMsCodes];
+#pragma unroll
+      for (int i = 0; i < kMsCodes; ++i) {
+        const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
+        const uint32_t at = q < nl ? lst + q : tst + (q - nl);
+        w[i] = q < nl + nt ? ce[at] : 0u;
+        v[i] = q < nl + nt ? __uint_as_float(cv[at]) : 0.0f;
+      }
+      float part = 0.0f;
+#pragma unroll
+      for (int i = 0; i < kMsCodes; ++i) {
+        const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
+        if (q < nl) {
+          part = fmaf(v[i], Gs[w[i] & ~kMgFirst], part);
+        } else if (q < nl + nt) {
+          const uint32_t c = w[i] & ~toc::kTreeEntry;
+          part = fmaf(v[i], Ht[c < ni ? c : c - n1 + ni], part);
+        }
+      }
+      s += part;
+    }
+#pragma unroll
+    for (int o = kMsLanes / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, kMsLanes);
+    if (u < n_used && lane == 0) h[j] = fmaf(-step, s, h[j]);
+  }
+}
+
 }  // namespace
 
 using namespace toc;
 
-extern "C" {
+namespace {
 
-toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_t loss, float lr,
-                         const float *y, float *h, void *stream) {
-  clear_error();
+// Argument checks shared by the two entry points; *done is set when there is
+// nothing to do.
+toc_status mgd_check(const toc_dev *d, int64_t b0, int64_t n_batches, int32_t loss, float lr,
+                     const float *y, const float *h, bool *done) {
+  *done = false;
   if (!d) return fail(TOC_EINVAL, "dev is NULL");
   if (d->pending) return fail(TOC_EINVAL, "image planned but not built");
   if (d->host) return fail(TOC_EINVAL, "image was uploaded to host memory");
@@ -265,8 +454,35 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   if (loss != TOC_MGD_LINEAR && loss != TOC_MGD_LOGISTIC && loss != TOC_MGD_HINGE)
     return fail(TOC_EINVAL, "unknown loss %d", loss);
   if (!std::isfinite(lr)) return fail(TOC_EINVAL, "learning rate not finite");
-  if (n_batches == 0) return TOC_OK;
+  if (n_batches == 0) {
+    *done = true;
+    return TOC_OK;
+  }
   if (!h || (!y && d->info.n_rows > 0)) return fail(TOC_EINVAL, "NULL pointer");
+  return TOC_OK;
+}
+
+MgImg mgd_image(const toc_dev *d) {
+  const uint8_t *base = (const uint8_t *)d->buf;
+  const toc_layout &L = d->layout;
+  return MgImg{(const toc_batch *)(base + L.batches), (const uint32_t *)(base + L.level),
+               (const toc_key *)(base + L.key), (const toc_link *)(base + L.link),
+               (const uint32_t *)(base + L.span), (const uint32_t *)(base + L.dcodes),
+               (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.tlist),
+               (const uint32_t *)(base + L.cols), (const uint32_t *)(base + L.tchild),
+               (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
+}
+
+}  // namespace
+
+extern "C" {
+
+toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_t loss, float lr,
+                         const float *y, float *h, void *stream) {
+  clear_error();
+  bool done = false;
+  const toc_status st = mgd_check(d, b0, n_batches, loss, lr, y, h, &done);
+  if (st != TOC_OK || done) return st;
   const size_t lds0 = 4 * ((size_t)d->max_rows + (size_t)d->max_codes);
   if (lds0 > kMgLdsMax)
     return fail(TOC_EUNSUPPORTED, "a batch needs %zu bytes of LDS (max %zu)", lds0, kMgLdsMax);
@@ -277,14 +493,7 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   if (lds > 64 * 1024 &&
       hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
     return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
-  const uint8_t *base = (const uint8_t *)d->buf;
-  const toc_layout &L = d->layout;
-  const MgImg im{(const toc_batch *)(base + L.batches), (const uint32_t *)(base + L.level),
-                 (const toc_key *)(base + L.key), (const toc_link *)(base + L.link),
-                 (const uint32_t *)(base + L.span), (const uint32_t *)(base + L.dcodes),
-                 (const uint32_t *)(base + L.occ_off), (const uint32_t *)(base + L.tlist),
-                 (const uint32_t *)(base + L.cols), (const uint32_t *)(base + L.tchild),
-                 (const uint32_t *)(base + L.centry), (const uint32_t *)(base + L.cval)};
+  const MgImg im = mgd_image(d);
   static std::atomic<uint32_t> launches{0};
   const uint32_t tag = launches.fetch_add(1) + 1;
   if (hl)
@@ -297,6 +506,57 @@ toc_status toc_mgd_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                        d->max_codes, (int)loss, lr, y, h, tag);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "mgd_kernel: %s", hipGetErrorString(e));
+  return TOC_OK;
+}
+
+toc_status toc_mgd_workspace_size(const toc_dev *d, size_t *bytes) {
+  clear_error();
+  if (!d || !bytes) return fail(TOC_EINVAL, "NULL pointer");
+  *bytes = 4 * (size_t)std::max<int32_t>(d->max_rows, 1);
+  return TOC_OK;
+}
+
+toc_status toc_mgd_epoch_split(const toc_dev *d, int64_t b0, int64_t n_batches, int32_t loss,
+                               float lr, const float *y, float *h, void *ws, size_t ws_bytes,
+                               void *stream) {
+  clear_error();
+  bool done = false;
+  const toc_status st = mgd_check(d, b0, n_batches, loss, lr, y, h, &done);
+  if (st != TOC_OK || done) return st;
+  const size_t need = 4 * (size_t)std::max<int32_t>(d->max_rows, 1);
+  if (!ws) return fail(TOC_EINVAL, "workspace is NULL");
+  if (ws_bytes < need) return fail(TOC_ESIZE, "workspace of %zu bytes below the %zu needed", ws_bytes, need);
+  const size_t lds = 4 * ((size_t)d->max_rows + (size_t)d->max_tree + 1);
+  if (lds > kMgLdsMax)
+    return fail(TOC_EUNSUPPORTED, "a batch needs %zu bytes of LDS (max %zu)", lds, kMgLdsMax);
+  if (lds > 64 * 1024 && hipFuncSetAttribute((const void *)mgds_bwd_kernel,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)lds) != hipSuccess)
+    return fail(TOC_EDEVICE, "cannot raise dynamic LDS to %zu bytes", lds);
+  const MgImg im = mgd_image(d);
+  const int32_t m = d->info.n_cols;
+  const bool hl = m <= kMsHlds;
+  float *g = (float *)ws;
+  hipStream_t s = (hipStream_t)stream;
+  for (int64_t b = b0; b < b0 + n_batches; ++b) {
+    const toc_batch &bt = d->batches[(size_t)b];
+    if (bt.n_rows == 0) continue;             // no tuple: the step leaves h unchanged
+    const unsigned gf = (unsigned)((bt.n_rows + kMsGroups - 1) / kMsGroups);
+    if (hl)
+      hipLaunchKernelGGL(mgds_fwd_kernel<true>, dim3(gf), dim3(kMsBlock), 0, s, im, b, m, (int)loss, y,
+                         (const float *)h, g);
+    else
+      hipLaunchKernelGGL(mgds_fwd_kernel<false>, dim3(gf), dim3(kMsBlock), 0, s, im, b, m, (int)loss,
+                         y, (const float *)h, g);
+    if (bt.n_ucols > 0) {                     // no used column: no entry of h changes
+      const int per = kMsGroups * kMsColPasses;
+      const unsigned gb = (unsigned)((bt.n_ucols + per - 1) / per);
+      hipLaunchKernelGGL(mgds_bwd_kernel, dim3(gb), dim3(kMsBlock), lds, s, im, b, m, d->max_rows, lr,
+                         (const float *)g, h);
+    }
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TOC_EDEVICE, "mgds kernels: %s", hipGetErrorString(e));
   return TOC_OK;
 }
 

@@ -1,7 +1,7 @@
-"""GPU parity of toc_mgd_epoch (mini-batch gradient descent, section 2.1) with the
-oracle: every step from the same model agrees with the oracle's fp64 step within a
-bound derived from the fp32 arithmetic, and one launch over many batches equals
-the same steps launched one by one, bit for bit."""
+"""GPU parity of toc_mgd_epoch and toc_mgd_epoch_split (mini-batch gradient
+descent, section 2.1) with the oracle: every step from the same model agrees with
+the oracle's fp64 step within a bound derived from the fp32 arithmetic, and one
+call over many batches equals the same steps called one by one, bit for bit."""
 
 import numpy as np
 import pytest
@@ -20,6 +20,15 @@ def upload(B):
     encs = T.toc_encode_batches(B.n_rows, B.n_cols, B.rowptr, B.col, B.val)
     buf = torch.empty(T.toc_upload_size(encs), dtype=torch.uint8, device=DEV)
     return T.toc_upload(encs, buf)
+
+
+def run_epoch(kind, dev, y, h, loss, lr, b0=0, n_batches=None):
+    """One call of the single-workgroup entry point ("one") or of the split one."""
+    if kind == "one":
+        T.toc_mgd_epoch(dev, y, h, loss, lr, b0=b0, n_batches=n_batches)
+    else:
+        ws = torch.empty(T.toc_mgd_workspace_size(dev), dtype=torch.uint8, device=DEV)
+        T.toc_mgd_epoch_split(dev, y, h, loss, lr, ws, b0=b0, n_batches=n_batches)
 
 
 def labels(B, loss, seed):
@@ -77,7 +86,8 @@ def check_step(B, b, h_before, h_after, y, loss, lr):
 
 @pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
 @pytest.mark.parametrize("which", ["mixed", "c3", "c2", "long"])
-def test_each_step_against_oracle(loss, which):
+@pytest.mark.parametrize("kind", ["one", "split"])
+def test_each_step_against_oracle(loss, which, kind):
     B = {"mixed": mixed_set, "c3": lambda: config_batches("c3", 4, 3),
          "c2": lambda: config_batches("c2", 1, 2), "long": long_set}[which]()
     dev = upload(B)
@@ -89,7 +99,7 @@ def test_each_step_against_oracle(loss, which):
     lr = 0.5
     for b in range(B.n_batches):
         before = hd.cpu().numpy().copy()
-        T.toc_mgd_epoch(dev, yd, hd, loss, lr, b0=b, n_batches=1)
+        run_epoch(kind, dev, yd, hd, loss, lr, b0=b, n_batches=1)
         torch.cuda.synchronize()
         after = hd.cpu().numpy()
         check_step(B, b, before, after, y, loss, lr)
@@ -98,16 +108,17 @@ def test_each_step_against_oracle(loss, which):
 
 
 @pytest.mark.parametrize("loss", [T.TOC_MGD_LINEAR, T.TOC_MGD_LOGISTIC, T.TOC_MGD_HINGE])
-def test_one_launch_equals_steps(loss):
+@pytest.mark.parametrize("kind", ["one", "split"])
+def test_one_launch_equals_steps(loss, kind):
     B = Batches.concat([config_batches("c5", 20, 40), mixed_set(), long_set()])
     dev = upload(B)
     y = torch.from_numpy(labels(B, loss, 3)).to(DEV)
     h0 = (np.random.default_rng(5).standard_normal(B.n_cols) * 0.05).astype(np.float32)
     h1 = torch.from_numpy(h0).to(DEV)
-    T.toc_mgd_epoch(dev, y, h1, loss, 0.25)
+    run_epoch(kind, dev, y, h1, loss, 0.25)
     h2 = torch.from_numpy(h0).to(DEV)
     for b in range(B.n_batches):
-        T.toc_mgd_epoch(dev, y, h2, loss, 0.25, b0=b, n_batches=1)
+        run_epoch(kind, dev, y, h2, loss, 0.25, b0=b, n_batches=1)
     torch.cuda.synchronize()
     assert np.array_equal(h1.cpu().numpy().view(np.uint32), h2.cpu().numpy().view(np.uint32))
     assert not np.array_equal(h1.cpu().numpy(), h0)
@@ -136,3 +147,25 @@ def test_lr_zero_and_errors():
     with pytest.raises(T.TocError) as ei:
         T.toc_mgd_epoch(hdev, y, h, T.TOC_MGD_LINEAR, 0.1)
     assert ei.value.status == T.TOC_EINVAL
+
+
+def test_split_workspace_and_agreement():
+    """The split entry point refuses a short workspace; over a whole epoch it stays
+    close to the single-workgroup one (same steps, sums in another order)."""
+    B = Batches.concat([config_batches("c5", 0, 30), mixed_set()])
+    dev = upload(B)
+    y = torch.from_numpy(labels(B, T.TOC_MGD_LOGISTIC, 9)).to(DEV)
+    h0 = (np.random.default_rng(9).standard_normal(B.n_cols) * 0.05).astype(np.float32)
+    need = T.toc_mgd_workspace_size(dev)
+    assert need == 4 * int(max(B.n_rows.max(), 1))
+    h = torch.from_numpy(h0).to(DEV)
+    with pytest.raises(T.TocError) as ei:
+        T.toc_mgd_epoch_split(dev, y, h, T.TOC_MGD_LOGISTIC, 0.1,
+                              torch.empty(need - 4, dtype=torch.uint8, device=DEV))
+    assert ei.value.status == T.TOC_ESIZE
+    run_epoch("split", dev, y, h, T.TOC_MGD_LOGISTIC, 0.1)
+    h1 = torch.from_numpy(h0).to(DEV)
+    run_epoch("one", dev, y, h1, T.TOC_MGD_LOGISTIC, 0.1)
+    torch.cuda.synchronize()
+    a, b = h.cpu().numpy().astype(np.float64), h1.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(a - b) <= 1e-4 * (np.abs(b) + 1e-3))
