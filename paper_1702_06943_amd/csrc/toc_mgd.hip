@@ -253,8 +253,9 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
 //    LDS when the matrix has at most kMsHlds columns;
 //  * mgds_bwd_kernel: every workgroup stages g, sums each tree code's own
 //    occurrences (its tree row) and adds children into parents deepest level
-//    first in LDS, then takes kMsColPasses x 16 of the batch's used columns (a
-//    16-lane group per column): the gradient of column j sums val * g over its
+//    first in LDS (a thread holds the ranges of its first kMbRows rows), then
+//    takes 64 of the batch's used columns (a 16-lane group per column): the
+//    gradient of column j sums val * g over its
 //    leaf occurrences and val * (tree row) over its tree codes, the multipliers
 //    beside the entries, and h_j -= lr / |B| * gradient.
 // Every sum has a fixed order, so one call over many batches equals the batches
@@ -265,7 +266,9 @@ constexpr int kMsLanes = 16;                   // lanes per tuple or column
 constexpr int kMsGroups = kMsBlock / kMsLanes;
 constexpr int kMsCodes = 8;                    // a lane's codes (or entries) loaded together
 constexpr int kMsHlds = 8192;                  // most columns whose model the forward pass stages
-constexpr int kMsColPasses = 4;                // column passes of a backward workgroup
+constexpr int kMbBlock = 1024;                 // backward workgroup
+constexpr int kMbGroups = kMbBlock / kMsLanes; // its columns: one per 16-lane group
+constexpr int kMbRows = 4;                     // tree rows per thread whose ranges it holds
 constexpr uint32_t kMsNone = 0xFFFFFFFFu;
 
 template <bool HLDS>
@@ -332,7 +335,7 @@ __global__ __launch_bounds__(kMsBlock) void mgds_fwd_kernel(MgImg im, int64_t b,
   if (r < bt.n_rows && lane == 0) g[r] = dloss(loss, acc, y[bt.row_base + r]);
 }
 
-__global__ __launch_bounds__(kMsBlock) void mgds_bwd_kernel(MgImg im, int64_t b, int32_t m,
+__global__ __launch_bounds__(kMbBlock) void mgds_bwd_kernel(MgImg im, int64_t b, int32_t m,
                                                             int32_t max_rows, float lr,
                                                             const float *__restrict__ g,
                                                             float *__restrict__ h) {
@@ -343,39 +346,80 @@ __global__ __launch_bounds__(kMsBlock) void mgds_bwd_kernel(MgImg im, int64_t b,
   const int nr = bt.n_rows;
   const uint32_t nc = (uint32_t)bt.n_codes, n1 = (uint32_t)bt.n_lvl1, ni = (uint32_t)bt.n_int1;
   const uint32_t n_tree = ni + (nc - n1);
-  for (int r0 = threadIdx.x; r0 < nr; r0 += kMsCodes * kMsBlock) {
+  const uint32_t *to = im.occ_off + bt.code_base + 2 * b + (n1 - ni) + 1;
+  const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
+  const uint32_t *cv = im.cval + bt.d_base + bt.tree_base;
+  const uint32_t *tch = im.tchild + bt.tree_base + b;
+  auto row_code = [&](uint32_t t) { return t < ni ? t : t - ni + n1; };
+  // this thread's first kMbRows tree rows: their occurrence and children ranges,
+  // loaded while g is staged
+  uint32_t o0[kMbRows], o1[kMbRows], k0[kMbRows], k1[kMbRows];
+#pragma unroll
+  for (int i = 0; i < kMbRows; ++i) {
+    const uint32_t t = threadIdx.x + (uint32_t)(i * kMbBlock);
+    o0[i] = o1[i] = k0[i] = k1[i] = 0u;
+    if (t < n_tree) {
+      o0[i] = to[t];
+      o1[i] = to[t + 1];
+      k0[i] = tch[t];
+      k1[i] = tch[t + 1];
+    }
+  }
+  for (int r0 = threadIdx.x; r0 < nr; r0 += kMsCodes * kMbBlock) {
     float t[kMsCodes];
 #pragma unroll
     for (int q = 0; q < kMsCodes; ++q) {
-      const int r = r0 + q * kMsBlock;
+      const int r = r0 + q * kMbBlock;
       t[q] = r < nr ? g[r] : 0.0f;
     }
 #pragma unroll
     for (int q = 0; q < kMsCodes; ++q) {
-      const int r = r0 + q * kMsBlock;
+      const int r = r0 + q * kMbBlock;
       if (r < nr) Gs[r] = t[q];
     }
   }
   __syncthreads();
-  // tree rows: the gradients of the tuples holding the code, then the children's
-  // rows added into their parents, deepest level first
-  const uint32_t *to = im.occ_off + bt.code_base + 2 * b + (n1 - ni) + 1;
-  const uint32_t *ce = im.centry + bt.d_base + bt.tree_base;
-  const uint32_t *cv = im.cval + bt.d_base + bt.tree_base;
-  for (uint32_t t = threadIdx.x; t < n_tree; t += kMsBlock) {
-    const uint32_t o1 = to[t + 1];
-    float s = 0.0f;
-#pragma unroll 4
-    for (uint32_t o = to[t]; o < o1; ++o) s += Gs[ce[o] & ~kMgFirst];
-    Ht[t] = s;
+  // tree rows: the gradients of the tuples holding the code (the first
+  // occurrences of a thread's rows loaded together)
+  {
+    uint32_t w0[kMbRows];
+#pragma unroll
+    for (int i = 0; i < kMbRows; ++i) w0[i] = o1[i] > o0[i] ? ce[o0[i]] : 0u;
+#pragma unroll
+    for (int i = 0; i < kMbRows; ++i) {
+      const uint32_t t = threadIdx.x + (uint32_t)(i * kMbBlock);
+      if (t >= n_tree) continue;
+      float s = 0.0f;
+      if (o1[i] > o0[i]) s += Gs[w0[i] & ~kMgFirst];
+      for (uint32_t o = o0[i] + 1; o < o1[i]; ++o) s += Gs[ce[o] & ~kMgFirst];
+      Ht[t] = s;
+    }
+    for (uint32_t t = threadIdx.x + (uint32_t)(kMbRows * kMbBlock); t < n_tree; t += kMbBlock) {
+      const uint32_t e1 = to[t + 1];
+      float s = 0.0f;
+      for (uint32_t o = to[t]; o < e1; ++o) s += Gs[ce[o] & ~kMgFirst];
+      Ht[t] = s;
+    }
   }
   __syncthreads();
+  // children added into parents, deepest level first (a thread's first rows from
+  // the ranges it holds, the others from memory)
   const uint32_t *lvl = im.level + bt.lvl_base;
-  const uint32_t *tch = im.tchild + bt.tree_base + b;
   for (int d = bt.n_levels - 1; d >= 1; --d) {
     const uint32_t a = d == 1 ? 0u : lvl[d - 1], e = d == 1 ? ni : lvl[d];
-    for (uint32_t c = a + threadIdx.x; c < e; c += kMsBlock) {
-      const uint32_t t = c < ni ? c : c - n1 + ni;
+#pragma unroll
+    for (int i = 0; i < kMbRows; ++i) {
+      const uint32_t t = threadIdx.x + (uint32_t)(i * kMbBlock);
+      const uint32_t c = row_code(t);
+      if (t < n_tree && c >= a && c < e) {
+        float s = Ht[t];
+        for (uint32_t ch = k0[i]; ch < k1[i]; ++ch) s += Ht[ch - n1 + ni];
+        Ht[t] = s;
+      }
+    }
+    for (uint32_t t = threadIdx.x + (uint32_t)(kMbRows * kMbBlock); t < n_tree; t += kMbBlock) {
+      const uint32_t c = row_code(t);
+      if (c < a || c >= e) continue;
       float s = Ht[t];
       const uint32_t c1 = tch[t + 1];
       for (uint32_t ch = tch[t]; ch < c1; ++ch) s += Ht[ch - n1 + ni];
@@ -383,51 +427,49 @@ __global__ __launch_bounds__(kMsBlock) void mgds_bwd_kernel(MgImg im, int64_t b,
     }
     __syncthreads();
   }
-  // this workgroup's used columns
+  // this workgroup's used columns, a 16-lane group per column
   const uint32_t *cx = im.cols + b * 4 * (int64_t)(m + 1);
   const uint32_t *Ost = cx + (m + 1), *Toff = cx + 2 * (m + 1), *Ord = cx + 3 * (m + 1);
   const uint32_t n_lo = Ost[m];      // leaf occurrences; the tree entries follow them
   const int n_used = bt.n_ucols;
   const float step = lr / (float)nr;
   const int lane = threadIdx.x % kMsLanes, grp = threadIdx.x / kMsLanes;
-  for (int pass = 0; pass < kMsColPasses; ++pass) {
-    const int u = ((int)blockIdx.x * kMsColPasses + pass) * kMsGroups + grp;
-    uint32_t j = 0, lst = 0, tst = 0, nl = 0, nt = 0;
-    if (u < n_used) {
-      j = Ord[u];
-      lst = Ost[j];
-      nl = Ost[j + 1] - lst;
-      tst = n_lo + Toff[j];
-      nt = Toff[j + 1] - Toff[j];
-    }
-    float s = 0.0f;
-    for (uint32_t q0 = lane; q0 < nl + nt; q0 += kMsLanes * kMsCodes) {
-      uint32_t w[kMsCodes];
-      float v[kMsCodes];
-#pragma unroll
-      for (int i = 0; i < kMsCodes; ++i) {
-        const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
-        const uint32_t at = q < nl ? lst + q : tst + (q - nl);
-        w[i] = q < nl + nt ? ce[at] : 0u;
-        v[i] = q < nl + nt ? __uint_as_float(cv[at]) : 0.0f;
-      }
-      float part = 0.0f;
-#pragma unroll
-      for (int i = 0; i < kMsCodes; ++i) {
-        const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
-        if (q < nl) {
-          part = fmaf(v[i], Gs[w[i] & ~kMgFirst], part);
-        } else if (q < nl + nt) {
-          const uint32_t c = w[i] & ~toc::kTreeEntry;
-          part = fmaf(v[i], Ht[c < ni ? c : c - n1 + ni], part);
-        }
-      }
-      s += part;
-    }
-#pragma unroll
-    for (int o = kMsLanes / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, kMsLanes);
-    if (u < n_used && lane == 0) h[j] = fmaf(-step, s, h[j]);
+  const int u = (int)blockIdx.x * kMbGroups + grp;
+  uint32_t j = 0, lst = 0, tst = 0, nl = 0, nt = 0;
+  if (u < n_used) {
+    j = Ord[u];
+    lst = Ost[j];
+    nl = Ost[j + 1] - lst;
+    tst = n_lo + Toff[j];
+    nt = Toff[j + 1] - Toff[j];
   }
+  float s = 0.0f;
+  for (uint32_t q0 = lane; q0 < nl + nt; q0 += kMsLanes * kMsCodes) {
+    uint32_t w[kMsCodes];
+    float v[kMsCodes];
+#pragma unroll
+    for (int i = 0; i < kMsCodes; ++i) {
+      const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
+      const uint32_t at = q < nl ? lst + q : tst + (q - nl);
+      w[i] = q < nl + nt ? ce[at] : 0u;
+      v[i] = q < nl + nt ? __uint_as_float(cv[at]) : 0.0f;
+    }
+    float part = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMsCodes; ++i) {
+      const uint32_t q = q0 + (uint32_t)(i * kMsLanes);
+      if (q < nl) {
+        part = fmaf(v[i], Gs[w[i] & ~kMgFirst], part);
+      } else if (q < nl + nt) {
+        const uint32_t c = w[i] & ~toc::kTreeEntry;
+        part = fmaf(v[i], Ht[c < ni ? c : c - n1 + ni], part);
+      }
+    }
+    s += part;
+  }
+#pragma unroll
+  for (int o = kMsLanes / 2; o > 0; o >>= 1) s += __shfl_xor(s, o, kMsLanes);
+  if (u < n_used && lane == 0) h[j] = fmaf(-step, s, h[j]);
 }
 
 }  // namespace
@@ -549,9 +591,8 @@ toc_status toc_mgd_epoch_split(const toc_dev *d, int64_t b0, int64_t n_batches, 
       hipLaunchKernelGGL(mgds_fwd_kernel<false>, dim3(gf), dim3(kMsBlock), 0, s, im, b, m, (int)loss,
                          y, (const float *)h, g);
     if (bt.n_ucols > 0) {                     // no used column: no entry of h changes
-      const int per = kMsGroups * kMsColPasses;
-      const unsigned gb = (unsigned)((bt.n_ucols + per - 1) / per);
-      hipLaunchKernelGGL(mgds_bwd_kernel, dim3(gb), dim3(kMsBlock), lds, s, im, b, m, d->max_rows, lr,
+      const unsigned gb = (unsigned)((bt.n_ucols + kMbGroups - 1) / kMbGroups);
+      hipLaunchKernelGGL(mgds_bwd_kernel, dim3(gb), dim3(kMbBlock), lds, s, im, b, m, d->max_rows, lr,
                          (const float *)g, h);
     }
   }
