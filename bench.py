@@ -522,8 +522,10 @@ def time_cprime(sample, stream, reps=3):
 
 def time_mgd(w, stream, lr=0.1):
     """One epoch of mini-batch gradient descent for logistic regression (k = 1) over
-    every batch of the resident image, in one toc_mgd_epoch launch (each step
-    depends on the previous one), with seeded labels of +-1 and h = 0 at the start."""
+    every batch of the resident image (each step depends on the previous one), with
+    seeded labels of +-1 and h = 0 at the start: with the steps split over many
+    workgroups (toc_mgd_epoch_split, two launches a step; the reported figure), and
+    in one launch of one workgroup (toc_mgd_epoch)."""
     import torch
     import paper_1702_06943_amd as T
     info = w.info
@@ -531,25 +533,37 @@ def time_mgd(w, stream, lr=0.1):
     gen.manual_seed(1702)
     y = (torch.randint(0, 2, (info["n_rows"],), generator=gen, device="cuda:0") * 2 - 1).float()
     h = torch.zeros(info["n_cols"], device="cuda:0")
-    try:
-        T.toc_mgd_epoch(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr, b0=0, n_batches=1)
-    except T.TocError as e:
-        log(f"MGD epoch skipped: {e}")
+    ws = torch.empty(T.toc_mgd_workspace_size(w.dev), dtype=torch.uint8, device="cuda:0")
+    runs = {"split": lambda **kw: T.toc_mgd_epoch_split(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr, ws, **kw),
+            "one": lambda **kw: T.toc_mgd_epoch(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr, **kw)}
+    ms = {}
+    for kind, run in runs.items():
+        try:
+            run(b0=0, n_batches=1)
+        except T.TocError as e:
+            log(f"MGD epoch ({kind}) skipped: {e}")
+            continue
+        h.zero_()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        run()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        ms[kind] = ev[0].elapsed_time(ev[1])
+        if not bool(torch.isfinite(h).all().item()):
+            ms[kind] = None
+    if not ms.get("split"):
         return None
-    h.zero_()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
-    ev[0].record(stream)
-    T.toc_mgd_epoch(w.dev, y, h, T.TOC_MGD_LOGISTIC, lr)
-    ev[1].record(stream)
-    torch.cuda.synchronize()
-    ms = ev[0].elapsed_time(ev[1])
-    ok = bool(torch.isfinite(h).all().item())
-    res = {"loss": "logistic", "batches": info["n_batches"], "ms": round(ms, 3),
-           "batches_per_s": info["n_batches"] / (ms / 1e3),
-           "nnz_per_s": info["nnz"] / (ms / 1e3), "model_finite": ok}
-    log(f"MGD epoch (logistic, {info['n_batches']} steps in one launch): {ms:.1f} ms, "
-        f"{res['batches_per_s']:.0f} steps/s")
+    t = ms["split"]
+    res = {"loss": "logistic", "batches": info["n_batches"], "ms": round(t, 3),
+           "us_per_step": t / info["n_batches"] * 1e3,
+           "batches_per_s": info["n_batches"] / (t / 1e3),
+           "nnz_per_s": info["nnz"] / (t / 1e3), "model_finite": True,
+           "single_workgroup_ms": round(ms["one"], 3) if ms.get("one") else None}
+    log(f"MGD epoch (logistic, {info['n_batches']} steps, split over workgroups): {t:.1f} ms, "
+        f"{res['us_per_step']:.1f} us/step; one workgroup: "
+        f"{ms.get('one') or float('nan'):.1f} ms")
     return res
 
 
