@@ -271,11 +271,58 @@ constexpr int kMbGroups = kMbBlock / kMsLanes; // its columns: one per 16-lane g
 constexpr int kMbRows = 4;                     // tree rows per thread whose ranges it holds
 constexpr uint32_t kMsNone = 0xFFFFFFFFu;
 
+// Reads one word of every 128-byte line of the arrays of batch b that one side of
+// a split step reads (fwd: the forward launch's, else the backward launch's), so
+// that the launch finds them in this XCD's L2; the extra workgroups of each launch
+// (one per XCD) run it beside the launch's work.
+template <int NT>
+__device__ void mgds_touch(const MgImg &im, int64_t b, int32_t m, const float *y, bool fwd) {
+  const toc_batch bt = im.batches[b];
+  const int64_t nc = bt.n_codes, n1 = bt.n_lvl1, nd = bt.n_d, nr = bt.n_rows;
+  const int64_t nt = bt.n_int1 + nc - n1;
+  struct Range { const void *p; int64_t bytes; };
+  const Range rf[] = {
+      {im.dcodes + bt.d_base, 4 * nd},
+      {im.key + bt.code_base, 8 * nc},
+      {im.link + bt.deep_base, 8 * (nc - n1)},
+      {im.span + bt.span_base, 4 * (nr + 1)},
+      {y + bt.row_base, 4 * nr},
+  };
+  const Range rb[] = {
+      {im.occ_off + bt.code_base + 2 * b + (n1 - bt.n_int1) + 1, 4 * (nt + 1)},
+      {im.centry + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+      {im.cval + bt.d_base + bt.tree_base, 4 * (nd + nt)},
+      {im.cols + b * 4 * (int64_t)(m + 1) + (m + 1), 4 * 3 * (int64_t)(m + 1)},
+      {im.tchild + bt.tree_base + b, 4 * (nt + 1)},
+      {im.level + bt.lvl_base, 4 * ((int64_t)bt.n_levels + 1)},
+  };
+  uint32_t acc = 0;
+  const Range *r = fwd ? rf : rb;
+  const int n = fwd ? 5 : 6;
+  for (int i = 0; i < n; ++i)
+    for (int64_t o0 = (int64_t)threadIdx.x * 128; o0 < r[i].bytes; o0 += (int64_t)kMsCodes * NT * 128) {
+      uint32_t t[kMsCodes];
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) {
+        const int64_t o = o0 + (int64_t)q * NT * 128;
+        t[q] = o < r[i].bytes ? *(const uint32_t *)((const char *)r[i].p + o) : 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < kMsCodes; ++q) acc += t[q];
+    }
+  asm volatile("" : : "v"(acc));    // the loads are the point: keep them
+}
+
 template <bool HLDS>
 __global__ __launch_bounds__(kMsBlock) void mgds_fwd_kernel(MgImg im, int64_t b, int32_t m, int loss,
                                                             const float *__restrict__ y,
                                                             const float *__restrict__ hg,
-                                                            float *__restrict__ g) {
+                                                            float *__restrict__ g, int n_work) {
+  // the workgroups past n_work read the backward launch's arrays of this batch
+  if ((int)blockIdx.x >= n_work) {
+    mgds_touch<kMsBlock>(im, b, m, y, false);
+    return;
+  }
   __shared__ float hs[HLDS ? kMsHlds : 1];
   const toc_batch bt = im.batches[b];
   if (HLDS) {
@@ -338,7 +385,14 @@ __global__ __launch_bounds__(kMsBlock) void mgds_fwd_kernel(MgImg im, int64_t b,
 __global__ __launch_bounds__(kMbBlock) void mgds_bwd_kernel(MgImg im, int64_t b, int32_t m,
                                                             int32_t max_rows, float lr,
                                                             const float *__restrict__ g,
-                                                            float *__restrict__ h) {
+                                                            float *__restrict__ h, int n_work,
+                                                            int64_t next,
+                                                            const float *__restrict__ y) {
+  // the workgroups past n_work read the next step's forward arrays
+  if ((int)blockIdx.x >= n_work) {
+    if (next >= 0) mgds_touch<kMbBlock>(im, next, m, y, true);
+    return;
+  }
   extern __shared__ float sm[];
   float *Gs = sm;                  // per tuple: d loss / d r
   float *Ht = sm + max_rows;       // per tree row (tree code c: row c < ni ? c : c - n1 + ni)
@@ -580,21 +634,28 @@ toc_status toc_mgd_epoch_split(const toc_dev *d, int64_t b0, int64_t n_batches, 
   const bool hl = m <= kMsHlds;
   float *g = (float *)ws;
   hipStream_t s = (hipStream_t)stream;
-  for (int64_t b = b0; b < b0 + n_batches; ++b) {
+  // each launch has kMgXcds more workgroups, one per XCD, that read ahead: the
+  // forward launch the backward launch's arrays, the backward launch the next
+  // step's forward arrays
+  int64_t b = b0;
+  while (b < b0 + n_batches && d->batches[(size_t)b].n_rows == 0) ++b;
+  while (b < b0 + n_batches) {
     const toc_batch &bt = d->batches[(size_t)b];
-    if (bt.n_rows == 0) continue;             // no tuple: the step leaves h unchanged
-    const unsigned gf = (unsigned)((bt.n_rows + kMsGroups - 1) / kMsGroups);
+    int64_t next = b + 1;                     // the next batch with tuples, or -1
+    while (next < b0 + n_batches && d->batches[(size_t)next].n_rows == 0) ++next;
+    const int gf = (bt.n_rows + kMsGroups - 1) / kMsGroups;
     if (hl)
-      hipLaunchKernelGGL(mgds_fwd_kernel<true>, dim3(gf), dim3(kMsBlock), 0, s, im, b, m, (int)loss, y,
-                         (const float *)h, g);
+      hipLaunchKernelGGL(mgds_fwd_kernel<true>, dim3(gf + kMgXcds), dim3(kMsBlock), 0, s, im, b, m,
+                         (int)loss, y, (const float *)h, g, gf);
     else
-      hipLaunchKernelGGL(mgds_fwd_kernel<false>, dim3(gf), dim3(kMsBlock), 0, s, im, b, m, (int)loss,
-                         y, (const float *)h, g);
-    if (bt.n_ucols > 0) {                     // no used column: no entry of h changes
-      const unsigned gb = (unsigned)((bt.n_ucols + kMbGroups - 1) / kMbGroups);
-      hipLaunchKernelGGL(mgds_bwd_kernel, dim3(gb), dim3(kMbBlock), lds, s, im, b, m, d->max_rows, lr,
-                         (const float *)g, h);
-    }
+      hipLaunchKernelGGL(mgds_fwd_kernel<false>, dim3(gf + kMgXcds), dim3(kMsBlock), 0, s, im, b, m,
+                         (int)loss, y, (const float *)h, g, gf);
+    // (a batch without used columns changes no entry of h: its launch only reads ahead)
+    const int gb = (bt.n_ucols + kMbGroups - 1) / kMbGroups;
+    hipLaunchKernelGGL(mgds_bwd_kernel, dim3(gb + kMgXcds), dim3(kMbBlock), lds, s, im, b, m,
+                       d->max_rows, lr, (const float *)g, h, gb,
+                       next < b0 + n_batches ? next : (int64_t)-1, y);
+    b = next;
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TOC_EDEVICE, "mgds kernels: %s", hipGetErrorString(e));
