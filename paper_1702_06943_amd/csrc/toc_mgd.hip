@@ -255,11 +255,13 @@ __global__ __launch_bounds__(kMgBlock) void mgd_kernel(MgImg im, int64_t b0, int
 //    occurrences (its tree row) and adds children into parents deepest level
 //    first in LDS (a thread holds the ranges of its first kMbRows rows), then
 //    takes 64 of the batch's used columns (a 16-lane group per column): the
-//    gradient of column j sums val * g over its
-//    leaf occurrences and val * (tree row) over its tree codes, the multipliers
-//    beside the entries, and h_j -= lr / |B| * gradient.
-// Every sum has a fixed order, so one call over many batches equals the batches
-// one call each, bit for bit.
+//    gradient of column j sums val * g over its leaf occurrences and
+//    val * (tree row) over its tree codes, the multipliers beside the entries,
+//    and h_j -= lr / |B| * gradient.
+// Each launch has kMgXcds more workgroups (one per XCD) that read ahead, so
+// neither launch starts on arrays found in HBM only.  Every sum has a fixed
+// order, so one call over many batches equals the batches one call each, bit for
+// bit.
 // ---------------------------------------------------------------------------
 constexpr int kMsBlock = 256;
 constexpr int kMsLanes = 16;                   // lanes per tuple or column
