@@ -242,26 +242,28 @@ __global__ __launch_bounds__(kNnBlock) void mlp_rows_kernel(
 
 // Weight gradients of layers 2 and 3 (sums over the batch's n tuples) and their
 // updates.  Workgroups below n_w2 each take a V x U block of W2 (U = min(h2, 256),
-// V = 256 / U), summing over the tuples 64 at a time with the block's columns of
+// V = 256 / U), summing over the tuples ch2 at a time with the block's columns of
 // H1 and dZ2 staged in LDS (the blocks of W2's first rows also sum b2's gradient);
-// the workgroups after them take 256 entries each of W3 and b3.  Runs after every
-// tuple's dZ1 was computed from the old W2.
+// the workgroups after them take 256 entries each of W3 and b3, the tuples ch3 at
+// a time.  The host makes a chunk the whole batch when its rows fit 96 KiB, so a
+// step stages its inputs with one load latency.  Runs after every tuple's dZ1 was
+// computed from the old W2.
 
 __global__ __launch_bounds__(256) void mlp_grad_kernel(
     int n, int n_w2, const float *__restrict__ act1, int h1, int h2, int C,
     const float *__restrict__ H2g, const float *__restrict__ dZ2g, const float *__restrict__ dZ3g,
     float lr, float *__restrict__ W2, float *__restrict__ b2, float *__restrict__ W3,
-    float *__restrict__ b3) {
+    float *__restrict__ b3, int ch2, int ch3) {
   extern __shared__ float gs[];
   if ((int)blockIdx.x < n_w2) {
     const int U = min(h2, 256), V = 256 / U, nub = (h2 + U - 1) / U;
     const int v0 = (blockIdx.x / nub) * V, u0 = (blockIdx.x % nub) * U;
-    float *As = gs, *Gs = gs + 64 * V;
+    float *As = gs, *Gs = gs + ch2 * V;
     const int lv = threadIdx.x / U, lu = threadIdx.x - lv * U;
     const int v = v0 + lv, u = u0 + lu;
     float g = 0.0f, gb = 0.0f;                  // gb: b2's gradient, by the first row of blocks
-    for (int i0 = 0; i0 < n; i0 += 64) {
-      const int ni = min(64, n - i0);
+    for (int i0 = 0; i0 < n; i0 += ch2) {
+      const int ni = min(ch2, n - i0);
       stage<256>(As, ni * V, [&](int x) {
         const int ii = x / V, vv = v0 + (x - ii * V);
         return vv < h1 ? act1[(int64_t)(i0 + ii) * h1 + vv] : 0.0f;
@@ -282,7 +284,7 @@ __global__ __launch_bounds__(256) void mlp_grad_kernel(
     return;
   }
   // W3 and b3 (b3 as a row of W3 whose H2 column is 1), tuples staged TI at a time
-  const int TI = max(1, min(64, 16384 / (h2 + C)));
+  const int TI = ch3;
   float *Hs = gs, *Zs = gs + TI * h2;
   const int n_out3 = (h2 + 1) * C;
   {
@@ -548,9 +550,12 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
   const int gU = std::min(h2, 256), gV = 256 / gU;
   const int n_w2 = ((h1 + gV - 1) / gV) * ((h2 + gU - 1) / gU);
   const int n_w3 = ((h2 + 1) * n_out + 255) / 256;
-  // W2 blocks stage 64 (U + V) floats; the W3 workgroup stages TI (h2 + n_out)
-  const int gTI = std::max(1, std::min(64, 16384 / (h2 + n_out)));
-  const size_t lds_g = (size_t)std::max(64 * (gU + gV), gTI * (h2 + n_out)) * 4;
+  // W2 blocks stage ch2 (U + V) floats, the W3 workgroups ch3 (h2 + n_out): as
+  // many tuples as 96 KiB holds, at most a batch
+  const int ch_max = std::max<int32_t>(d->max_rows, 1);
+  const int ch2 = std::max(1, std::min(ch_max, 24576 / (gU + gV)));
+  const int ch3 = std::max(1, std::min(ch_max, 24576 / (h2 + n_out)));
+  const size_t lds_g = (size_t)std::max(ch2 * (gU + gV), ch3 * (h2 + n_out)) * 4;
   toc_status st;
   if ((st = allow((const void *)mlp_fwd1_kernel<false>, lds_f)) ||
       (st = allow((const void *)mlp_bwd1_kernel<false>, lds_b)) ||
@@ -597,7 +602,7 @@ toc_status toc_mlp_epoch(const toc_dev *d, int64_t b0, int64_t n_batches, int32_
                          dim3(kNnBlock), lds_r, s, bt.n_rows, R, bt.row_base, act1, h1, h2, n_out,
                          W2, b2, W3, b3, labels, H2g, dZ2g, dZ3g, dz1);
     hipLaunchKernelGGL(mlp_grad_kernel, dim3((unsigned)(n_w2 + n_w3)), dim3(256), lds_g, s, bt.n_rows, n_w2,
-                       act1, h1, h2, n_out, H2g, dZ2g, dZ3g, lr, W2, b2, W3, b3);
+                       act1, h1, h2, n_out, H2g, dZ2g, dZ3g, lr, W2, b2, W3, b3, ch2, ch3);
     // the next step's batch with rows (its arrays are read ahead by the last
     // kernel of this step)
     int64_t next = b + 1;
