@@ -1983,6 +1983,12 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     };
     __syncthreads();   // the previous item no longer reads the LDS rows and tables
     if (threadIdx.x == 0) cg_next[parity ^ 1u] = kLtWaves;
+    // the first pass of the column index and of the tree rows' occurrences is
+    // loaded before the G tile and stored after it
+    const uint4 *csrc = (const uint4 *)(cols_all + b * 4 * (int64_t)(m + 1));
+    const uint32_t *tch = tchild_all + bt.tree_base + b;
+    const uint4 cx0 = threadIdx.x < m + 1 ? csrc[threadIdx.x] : make_uint4(0u, 0u, 0u, 0u);
+    const uint32_t oc0 = use_ocr && threadIdx.x < n_p3 ? orow[p3 + threadIdx.x] : 0u;
     // G tile: all loads of a pass first, then the stores
     {
       const int n4 = nrows * (TW / 4);
@@ -2017,9 +2023,8 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
     // the batch's column index, children ranges and (when they fit) occurrence
     // offsets, from the image
     {
-      const uint4 *src = (const uint4 *)(cols_all + b * 4 * (int64_t)(m + 1));
-      for (int e = threadIdx.x; e < m + 1; e += kLtBlock) ((uint4 *)Loff)[e] = src[e];
-      const uint32_t *tch = tchild_all + bt.tree_base + b;
+      if (threadIdx.x < m + 1) ((uint4 *)Loff)[threadIdx.x] = cx0;
+      for (int e = threadIdx.x + kLtBlock; e < m + 1; e += kLtBlock) ((uint4 *)Loff)[e] = csrc[e];
       // (a thread's loads of a pass, up to kLtCopy of each table, before its stores)
       for (uint32_t h0 = threadIdx.x; h0 <= n_tree; h0 += kLtCopy * kLtBlock) {
         uint32_t ct[kLtCopy], ot[kLtCopy];
@@ -2038,8 +2043,10 @@ __global__ __launch_bounds__(kLtBlock) void left_tiled_kernel(
           }
         }
       }
-      if (use_ocr)
-        for (uint32_t t = threadIdx.x; t < n_p3; t += kLtBlock) Ocr[t] = orow[p3 + t];
+      if (use_ocr) {
+        if (threadIdx.x < n_p3) Ocr[threadIdx.x] = oc0;
+        for (uint32_t t = threadIdx.x + kLtBlock; t < n_p3; t += kLtBlock) Ocr[t] = orow[p3 + t];
+      }
     }
     __syncthreads();
     // Tree codes, deepest level first: H = own occurrences' G rows + children's
