@@ -334,20 +334,18 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
   float *H = sm + max_rows;                           // max_codes
   auto hrow = [&](uint32_t c) -> uint32_t { return ox.hrow(c); };
   float *ob = out + b * (int64_t)m * ldo;
-  for (int r = threadIdx.x; r < bt.n_rows; r += kBlock) Gs[r] = G[(bt.row_base + r) * ldg];
-  __syncthreads();
   // G(c) for every code; a leaf's times its value (read beside its first
-  // occurrence), since a leaf has no children to add first
-  for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
-    uint32_t o0[kK1Codes], o1[kK1Codes], vb[kK1Codes];
+  // occurrence), since a leaf has no children to add first.  A pass loads the
+  // occurrence ranges and first entries of kK1Codes codes per thread; the first
+  // pass's loads are issued before the G rows are staged, as they need none
+  uint32_t o0[kK1Codes], o1[kK1Codes], vb[kK1Codes], w[kK1Codes][kK1Occ];
+  auto load_pass = [&](uint32_t c0) {
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       const uint32_t c = c0 + u * kBlock;
       o0[u] = c < nc ? ox.start(c) : 0u;
       o1[u] = c < nc ? ox.end(c) : 0u;
     }
-    float s[kK1Codes];
-    uint32_t w[kK1Codes][kK1Occ];
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       const uint32_t c = c0 + u * kBlock;
@@ -356,6 +354,13 @@ __global__ __launch_bounds__(kBlock) void left_k1_kernel(
 #pragma unroll
       for (int v = 0; v < kK1Occ; ++v) w[u][v] = o0[u] + v < o1[u] ? ox.ce[o0[u] + v] : 0xFFFFFFFFu;
     }
+  };
+  load_pass(threadIdx.x);
+  for (int r = threadIdx.x; r < bt.n_rows; r += kBlock) Gs[r] = G[(bt.row_base + r) * ldg];
+  __syncthreads();
+  for (uint32_t c0 = threadIdx.x; c0 < nc; c0 += kBlock * kK1Codes) {
+    if (c0 != threadIdx.x) load_pass(c0);
+    float s[kK1Codes];
 #pragma unroll
     for (int u = 0; u < kK1Codes; ++u) {
       s[u] = 0.0f;
